@@ -1,0 +1,191 @@
+/*
+ * samd.h - C ABI of the SAMD quantized-convolution library for MI355X (gfx950).
+ *
+ * Method: Anderson, Doyle, Gregg, "Scalar Arithmetic Multiple Data: Customizable
+ * Precision for Deep Neural Networks" (arXiv 1809.10572).  b-bit (1..8) signed or
+ * unsigned integers are packed into machine words; a 1-D convolution is read out of
+ * one wide integer multiply of a packed input word by a packed kernel word (Sec. 5,
+ * "Convolution as Long Multiplication"); signed and mixed-sign lanes are made exact
+ * by sign extension before the multiply and the underflow fix-up after it (Sec. 6).
+ *
+ * Conventions for every entry point:
+ *  - Pointers are DEVICE pointers unless a parameter says "host".  The caller owns
+ *    every buffer; the library allocates nothing and keeps no state between calls
+ *    apart from a thread-local error message.
+ *  - Work is enqueued asynchronously on `stream` (0 = the default stream).  A return
+ *    of SAMD_OK means the launch was accepted; results are ready once the stream is
+ *    synchronised.
+ *  - Arguments are validated on the host before any HIP call.  On a validation error
+ *    nothing is enqueued and the GPU is not touched, so validation can be exercised
+ *    without a GPU.  Nothing is thrown across the ABI.
+ *  - Device buffers of 32-bit elements must be 4-byte aligned (SAMD_EALIGN).
+ *
+ * Packed storage format (shared by activations, weights and requantised outputs):
+ *   a row of `len` b-bit values occupies ceil(len / P) uint32 words, P = floor(32/b);
+ *   value j lies in bits [(j mod P)*b, (j mod P)*b + b) of word floor(j / P) as a
+ *   b-bit two's-complement field when signed, unsigned otherwise; unused bits are 0;
+ *   every row starts on a new word.  Storage stays dense: spacer bits exist only
+ *   inside the kernels (temporary spacer bits, Sec. 2.2).  Signed 1-bit values are
+ *   {-1, 0}.
+ */
+#ifndef SAMD_H
+#define SAMD_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Bit width (1..8) and signedness of one operand. */
+typedef struct {
+    int32_t bits;
+    int32_t is_signed;
+} samd_fmt;
+
+/* 2-D convolution shape: input N x C x H x W, weights M x C x KH x KW, output
+ * N x M x Ho x Wo with Ho = (H + 2 pad_h - KH) / stride_h + 1 and likewise Wo. */
+typedef struct {
+    int32_t N, C, H, W, M, KH, KW, stride_h, stride_w, pad_h, pad_w;
+} samd_conv2d_desc;
+
+enum {
+    SAMD_OK = 0,
+    SAMD_EINVAL = -1,       /* bad argument: null pointer, bits out of 1..8, bad shape */
+    SAMD_EALIGN = -2,       /* a 32-bit buffer is not 4-byte aligned */
+    SAMD_EUNSUPPORTED = -3, /* no exact lane geometry exists for this shape / format */
+    SAMD_EOVERFLOW = -4,    /* an exact result could exceed int32 */
+    SAMD_EHIP = -5,         /* the HIP runtime reported an error (see samd_last_error) */
+    SAMD_ENOSPC = -6        /* the workspace is smaller than the query returned */
+};
+
+/* Lane geometry chosen for a convolution (host-only query, for inspection and tests).
+ *   lane_bits    L: bit width of one lane of the 64-bit accumulator
+ *   lanes        I: input values per 32-bit operand word
+ *   taps_max     Kmax: taps of the widest stride phase, ceil(KW / stride_w)
+ *   words_per_row nq: operand words per output row, ceil((Wo + Kmax - 1) / I)
+ *   flush_channels G: input channels accumulated before the lanes are decoded
+ *   out_lanes    lanes of an accumulator that can be non-zero; the highest of them
+ *                takes all the accumulator's remaining bits
+ *   tap_words    kernel words per (input channel, kernel row)
+ *   phase[i], tap0[i], ntaps[i] for i < tap_words: kernel word i holds ntaps[i]
+ *                consecutive taps of stride phase phase[i], starting at phase tap tap0[i]
+ *   macs_per_mad multiply-accumulates delivered per 32x32->64 multiply (I * taps) */
+typedef struct {
+    int32_t lane_bits, lanes, taps_max, words_per_row, flush_channels, out_lanes, tap_words;
+    int32_t phase[16], tap0[16], ntaps[16];
+    int32_t rows_per_block, mblock;
+    double macs_per_mad;
+} samd_conv2d_plan;
+
+/* Human-readable name of a status code; never NULL. */
+const char *samd_status_str(int status);
+
+/* Detail of the last error on the calling thread ("" if none); valid until the next
+ * call on this thread. */
+const char *samd_last_error(void);
+
+/* Words per packed row: ceil(len / floor(32 / f.bits)); negative status on error. */
+int64_t samd_row_words(int64_t len, samd_fmt f);
+
+/* Pack `rows` x `len` values (int8 when f.is_signed, else uint8; row-major) into the
+ * packed storage format, dst holding rows x samd_row_words(len, f) words.  Values
+ * outside the b-bit range are stored as their low b bits; when `oor_count` is not
+ * NULL the number of such values is ADDED to *oor_count (a device int32).
+ * The paper's baseline unpacks to the nearest native type (Sec. 7); this is the
+ * inverse step. */
+int samd_pack(const void *src, int64_t rows, int64_t len, samd_fmt f, uint32_t *dst,
+              int32_t *oor_count, hipStream_t stream);
+
+/* Inverse of samd_pack: dst is int8 (sign-extended) when f.is_signed, else uint8. */
+int samd_unpack(const uint32_t *src, int64_t rows, int64_t len, samd_fmt f, void *dst,
+                hipStream_t stream);
+
+/* Valid-mode 1-D true convolution of one packed row of n unsigned b-bit values
+ * with a K-tap unsigned kernel given on the HOST in natural order:
+ *     y[i] = sum_{t<K} taps[t] * x[i + K - 1 - t],   i = 0 .. n - K,
+ * i.e. the complete lanes of the long multiplication of Sec. 5.1, with partial lanes
+ * of neighbouring words added (overlap-add of the "parallelograms").  y holds n-K+1
+ * int32.  Both formats must be unsigned (the standalone 1-D operator of the paper's
+ * Sec. 5); 1 <= K <= 16 and K <= n. */
+int samd_conv1d(const uint32_t *x, int64_t n, samd_fmt xf, const int32_t *taps, int32_t K,
+                samd_fmt kf, int32_t *y, hipStream_t stream);
+
+/* Lane geometry of a 1-D convolution (host-only query):
+ *   lane_bits L, lanes I (values per 32-bit operand word), groups (kernel words; group
+ *   g holds taps [tap0[g], tap0[g] + ntaps[g]) in natural order), extra (following
+ *   operand words whose low lanes reach an output word), out_lanes (lanes that can be
+ *   non-zero; the highest takes the product's remaining bits). */
+typedef struct {
+    int32_t lane_bits, lanes, groups, extra, out_lanes;
+    int32_t tap0[16], ntaps[16];
+} samd_conv1d_plan;
+
+/* Host-only: the lane geometry samd_conv1d would use (same argument rules). */
+int samd_conv1d_plan_query(int64_t n, samd_fmt xf, const int32_t *taps, int32_t K, samd_fmt kf,
+                           samd_conv1d_plan *out);
+
+/* Host-only: the lane geometry samd_conv2d would use. */
+int samd_conv2d_plan_query(const samd_conv2d_desc *d, samd_fmt xf, samd_fmt wf,
+                           samd_conv2d_plan *out);
+
+/* Workspace bytes samd_conv2d needs (prepared kernel words). */
+int samd_conv2d_workspace(const samd_conv2d_desc *d, samd_fmt xf, samd_fmt wf, size_t *bytes);
+
+/* Quantized 2-D convolution by SAMD long multiplication, the DNN loop of Sec. 7
+ * (direct-sum2d figure) with batch, stride and zero padding:
+ *   y[n][m][ho][wo] = sum_c sum_ky sum_kx x[n][c][ho*sh+ky-ph][wo*sw+kx-pw] * w[m][c][ky][kx]
+ * (cross-correlation; out-of-image inputs are 0; y is overwritten, not accumulated).
+ *   x  packed activations, N*C*H rows of W values (format xf)
+ *   w  packed weights,     M*C*KH rows of KW values (format wf)
+ *   y  int32 output, N x M x Ho x Wo
+ *   ws workspace of at least samd_conv2d_workspace() bytes, 256-byte aligned
+ * Each kernel row is sign-extended into one or more 32-bit kernel words (Sec. 6,
+ * sign-extension figure), each x row is spread into lanes with temporary spacer bits
+ * and sign-extended the same way, products are accumulated over input channels
+ * before the lanes are resolved (Sec. 5), and the fix-up of the signed-convolution
+ * figure makes each lane exact.  Returns SAMD_EOVERFLOW when
+ * C*KH*KW*max|x|*max|w| >= 2^31. */
+int samd_conv2d(const uint32_t *x, samd_fmt xf, const uint32_t *w, samd_fmt wf,
+                const samd_conv2d_desc *d, int32_t *y, void *ws, size_t ws_bytes,
+                hipStream_t stream);
+
+/* Workspace bytes samd_conv2d_int8 needs (reordered int8 weights and per-filter sums). */
+int samd_conv2d_int8_workspace(const samd_conv2d_desc *d, samd_fmt xf, size_t *bytes);
+
+/* The native 8-bit baseline of Sec. 7: the same convolution on values unpacked to
+ * 8 bits, computed with the gfx950 int8 matrix cores.
+ *   x  unpacked activations, N x H x W x C (channels innermost), int8 when xf is
+ *      signed, else uint8 (unsigned 8-bit values use a -128 zero point internally)
+ *   w  int8 weights, M x C x KH x KW
+ *   y  int32 output, N x M x Ho x Wo
+ * Same semantics and overflow rule as samd_conv2d. */
+int samd_conv2d_int8(const void *x, samd_fmt xf, const int8_t *w, samd_fmt wf,
+                     const samd_conv2d_desc *d, int32_t *y, void *ws, size_t ws_bytes,
+                     hipStream_t stream);
+
+/* Maximum of n int32 values, written to *dev_max (device); n >= 1. */
+int samd_max_i32(const int32_t *src, int64_t n, int32_t *dev_max, hipStream_t stream);
+
+/* ReLU and requantisation to unsigned b bits between layers (the paper gives no rule;
+ * this library's): with mx = max(*dev_max, 0), s = the smallest s >= 0 such that
+ * mx >> s <= 2^b - 1, each value becomes min((max(v,0) + (s ? 2^(s-1) : 0)) >> s,
+ * 2^b - 1).  acc is rows x len int32 (rows of an NCHW tensor, len = W); the result is
+ * written in the packed storage format (format `out`, which must be unsigned).
+ * When dev_shift is not NULL, s is stored there. */
+int samd_relu_requant_pack(const int32_t *acc, int64_t rows, int64_t len, const int32_t *dev_max,
+                           samd_fmt out, uint32_t *dst, int32_t *dev_shift, hipStream_t stream);
+
+/* The same requantisation for the 8-bit baseline chain: acc is N x C x H x W int32,
+ * dst is N x H x W x C uint8 (channels innermost, the layout samd_conv2d_int8 reads). */
+int samd_relu_requant_nhwc_u8(const int32_t *acc, int32_t N, int32_t C, int32_t H, int32_t W,
+                              const int32_t *dev_max, samd_fmt out, uint8_t *dst,
+                              hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SAMD_H */

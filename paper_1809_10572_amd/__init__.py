@@ -1,0 +1,263 @@
+"""SAMD b-bit quantized convolution for MI355X (gfx950): Python binding of libsamd.so.
+
+The binding only marshals arguments: torch tensors supply device memory and the current
+HIP stream, and every step runs in the HIP library.  Importing works without a GPU; any
+call that would launch work raises if the library is missing or no GPU is visible.
+
+Packed words are held in torch.int32 tensors (bit patterns of the library's uint32
+words).  See include/samd.h for the storage format and the semantics of every call.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence, Tuple
+
+import torch
+
+__all__ = ["Fmt", "Conv2dDesc", "Conv1dPlan", "Conv2dPlan", "SamdError", "lib", "row_words", "pack", "unpack", "conv1d",
+           "conv1d_plan", "conv2d_plan", "conv2d_workspace", "conv2d", "conv2d_int8_workspace", "conv2d_int8", "max_i32",
+           "relu_requant_pack", "relu_requant_nhwc_u8", "out_hw", "LIB_PATH"]
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsamd.so")
+
+SAMD_OK, SAMD_EINVAL, SAMD_EALIGN, SAMD_EUNSUPPORTED, SAMD_EOVERFLOW, SAMD_EHIP, SAMD_ENOSPC = 0, -1, -2, -3, -4, -5, -6
+
+
+class Fmt(ctypes.Structure):
+    _fields_ = [("bits", ctypes.c_int32), ("is_signed", ctypes.c_int32)]
+
+    def __init__(self, bits: int, is_signed: bool):
+        super().__init__(int(bits), int(bool(is_signed)))
+
+    def __repr__(self):
+        return f"Fmt({self.bits}, {'s' if self.is_signed else 'u'})"
+
+
+_DESC_FIELDS = ["N", "C", "H", "W", "M", "KH", "KW", "stride_h", "stride_w", "pad_h", "pad_w"]
+
+
+class Conv2dDesc(ctypes.Structure):
+    _fields_ = [(f, ctypes.c_int32) for f in _DESC_FIELDS]
+
+    @classmethod
+    def of(cls, shape) -> "Conv2dDesc":
+        vals = shape.as_tuple() if hasattr(shape, "as_tuple") else tuple(shape)
+        return cls(*[int(v) for v in vals])
+
+
+class Conv2dPlan(ctypes.Structure):
+    _fields_ = [("lane_bits", ctypes.c_int32), ("lanes", ctypes.c_int32), ("taps_max", ctypes.c_int32),
+                ("words_per_row", ctypes.c_int32), ("flush_channels", ctypes.c_int32),
+                ("out_lanes", ctypes.c_int32), ("tap_words", ctypes.c_int32), ("phase", ctypes.c_int32 * 16), ("tap0", ctypes.c_int32 * 16),
+                ("ntaps", ctypes.c_int32 * 16), ("rows_per_block", ctypes.c_int32), ("mblock", ctypes.c_int32),
+                ("macs_per_mad", ctypes.c_double)]
+
+
+class Conv1dPlan(ctypes.Structure):
+    _fields_ = [("lane_bits", ctypes.c_int32), ("lanes", ctypes.c_int32), ("groups", ctypes.c_int32),
+                ("extra", ctypes.c_int32), ("out_lanes", ctypes.c_int32), ("tap0", ctypes.c_int32 * 16),
+                ("ntaps", ctypes.c_int32 * 16)]
+
+
+class SamdError(RuntimeError):
+    def __init__(self, status: int, name: str, detail: str):
+        super().__init__(f"{name} ({detail})" if detail else name)
+        self.status = status
+
+
+_lib = None
+_p, _i64, _i32, _sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_size_t
+
+
+def lib():
+    """The loaded libsamd.so; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_1809_10572_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        sigs = {
+            "samd_status_str": (ctypes.c_char_p, [ctypes.c_int]),
+            "samd_last_error": (ctypes.c_char_p, []),
+            "samd_row_words": (_i64, [_i64, Fmt]),
+            "samd_pack": (ctypes.c_int, [_p, _i64, _i64, Fmt, _p, _p, _p]),
+            "samd_unpack": (ctypes.c_int, [_p, _i64, _i64, Fmt, _p, _p]),
+            "samd_conv1d": (ctypes.c_int, [_p, _i64, Fmt, _p, _i32, Fmt, _p, _p]),
+            "samd_conv1d_plan_query": (ctypes.c_int, [_i64, Fmt, _p, _i32, Fmt, ctypes.POINTER(Conv1dPlan)]),
+            "samd_conv2d_plan_query": (ctypes.c_int, [ctypes.POINTER(Conv2dDesc), Fmt, Fmt,
+                                                      ctypes.POINTER(Conv2dPlan)]),
+            "samd_conv2d_workspace": (ctypes.c_int, [ctypes.POINTER(Conv2dDesc), Fmt, Fmt, ctypes.POINTER(_sz)]),
+            "samd_conv2d": (ctypes.c_int, [_p, Fmt, _p, Fmt, ctypes.POINTER(Conv2dDesc), _p, _p, _sz, _p]),
+            "samd_conv2d_int8_workspace": (ctypes.c_int, [ctypes.POINTER(Conv2dDesc), Fmt, ctypes.POINTER(_sz)]),
+            "samd_conv2d_int8": (ctypes.c_int, [_p, Fmt, _p, Fmt, ctypes.POINTER(Conv2dDesc), _p, _p, _sz, _p]),
+            "samd_max_i32": (ctypes.c_int, [_p, _i64, _p, _p]),
+            "samd_relu_requant_pack": (ctypes.c_int, [_p, _i64, _i64, _p, Fmt, _p, _p, _p]),
+            "samd_relu_requant_nhwc_u8": (ctypes.c_int, [_p, _i32, _i32, _i32, _i32, _p, Fmt, _p, _p]),
+        }
+        for name, (res, args) in sigs.items():
+            fn = getattr(L, name)
+            fn.restype, fn.argtypes = res, args
+        _lib = L
+    return _lib
+
+
+def _check(status: int) -> None:
+    if status != SAMD_OK:
+        L = lib()
+        raise SamdError(status, L.samd_status_str(status).decode(), L.samd_last_error().decode())
+
+
+def _stream(t: torch.Tensor) -> int:
+    return torch.cuda.current_stream(t.device).cuda_stream
+
+
+def _dev(t: torch.Tensor, dtype=None, name="tensor") -> torch.Tensor:
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor")
+    if dtype is not None and t.dtype not in (dtype if isinstance(dtype, tuple) else (dtype,)):
+        raise ValueError(f"{name} must have dtype {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t
+
+
+def out_hw(shape) -> Tuple[int, int]:
+    d = Conv2dDesc.of(shape)
+    return (d.H + 2 * d.pad_h - d.KH) // d.stride_h + 1, (d.W + 2 * d.pad_w - d.KW) // d.stride_w + 1
+
+
+def row_words(length: int, bits: int) -> int:
+    r = lib().samd_row_words(length, Fmt(bits, False))
+    if r < 0:
+        _check(int(r))
+    return int(r)
+
+
+def pack(values: torch.Tensor, bits: int, signed: bool, oor: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Pack the last axis of an int8 (signed) / uint8 (unsigned) GPU tensor."""
+    _dev(values, torch.int8 if signed else torch.uint8, "values")
+    length = values.shape[-1]
+    rows = values.numel() // length if length else 0
+    out = torch.empty(values.shape[:-1] + (row_words(length, bits),), dtype=torch.int32, device=values.device)
+    _check(lib().samd_pack(values.data_ptr(), rows, length, Fmt(bits, signed), out.data_ptr(),
+                           oor.data_ptr() if oor is not None else None, _stream(values)))
+    return out
+
+
+def unpack(words: torch.Tensor, length: int, bits: int, signed: bool) -> torch.Tensor:
+    _dev(words, torch.int32, "words")
+    rows = words.numel() // words.shape[-1] if words.shape[-1] else 0
+    out = torch.empty(words.shape[:-1] + (length,), dtype=torch.int8 if signed else torch.uint8, device=words.device)
+    _check(lib().samd_unpack(words.data_ptr(), rows, length, Fmt(bits, signed), out.data_ptr(), _stream(words)))
+    return out
+
+
+def conv1d(xp: torch.Tensor, n: int, bits: int, taps: Sequence[int], kbits: int,
+           out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Valid-mode true convolution of one packed unsigned row with host taps."""
+    _dev(xp, torch.int32, "xp")
+    K = len(taps)
+    arr = (ctypes.c_int32 * K)(*[int(t) for t in taps])
+    if out is None:
+        out = torch.empty(max(n - K + 1, 0), dtype=torch.int32, device=xp.device)
+    _check(lib().samd_conv1d(xp.data_ptr(), n, Fmt(bits, False), arr, K, Fmt(kbits, False), out.data_ptr(),
+                             _stream(xp)))
+    return out
+
+
+def conv1d_plan(n: int, bits: int, taps: Sequence[int], kbits: int) -> Conv1dPlan:
+    K = len(taps)
+    arr = (ctypes.c_int32 * K)(*[int(t) for t in taps])
+    plan = Conv1dPlan()
+    _check(lib().samd_conv1d_plan_query(n, Fmt(bits, False), arr, K, Fmt(kbits, False), ctypes.byref(plan)))
+    return plan
+
+
+def conv2d_plan(shape, xfmt: Fmt, wfmt: Fmt) -> Conv2dPlan:
+    plan = Conv2dPlan()
+    _check(lib().samd_conv2d_plan_query(ctypes.byref(Conv2dDesc.of(shape)), xfmt, wfmt, ctypes.byref(plan)))
+    return plan
+
+
+def conv2d_workspace(shape, xfmt: Fmt, wfmt: Fmt) -> int:
+    n = _sz(0)
+    _check(lib().samd_conv2d_workspace(ctypes.byref(Conv2dDesc.of(shape)), xfmt, wfmt, ctypes.byref(n)))
+    return int(n.value)
+
+
+def _workspace(nbytes: int, device) -> torch.Tensor:
+    # torch's caching allocator returns blocks aligned to at least 512 bytes
+    return torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
+
+
+def conv2d(xp: torch.Tensor, xfmt: Fmt, wp: torch.Tensor, wfmt: Fmt, shape, ws: Optional[torch.Tensor] = None,
+           out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """SAMD conv2d of packed activations (N*C*H rows of W) and packed weights
+    (M*C*KH rows of KW); returns int32 N x M x Ho x Wo."""
+    _dev(xp, torch.int32, "xp")
+    _dev(wp, torch.int32, "wp")
+    d = Conv2dDesc.of(shape)
+    Ho, Wo = out_hw(shape)
+    if ws is None:
+        ws = _workspace(conv2d_workspace(shape, xfmt, wfmt), xp.device)
+    if out is None:
+        out = torch.empty((d.N, d.M, Ho, Wo), dtype=torch.int32, device=xp.device)
+    _check(lib().samd_conv2d(xp.data_ptr(), xfmt, wp.data_ptr(), wfmt, ctypes.byref(d), out.data_ptr(),
+                             ws.data_ptr(), ws.numel(), _stream(xp)))
+    return out
+
+
+def conv2d_int8_workspace(shape, xfmt: Fmt) -> int:
+    n = _sz(0)
+    _check(lib().samd_conv2d_int8_workspace(ctypes.byref(Conv2dDesc.of(shape)), xfmt, ctypes.byref(n)))
+    return int(n.value)
+
+
+def conv2d_int8(x_nhwc: torch.Tensor, xfmt: Fmt, w: torch.Tensor, wfmt: Fmt, shape,
+                ws: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Native 8-bit baseline: x is N x H x W x C int8/uint8, w is M x C x KH x KW int8."""
+    _dev(x_nhwc, (torch.int8, torch.uint8), "x_nhwc")
+    _dev(w, torch.int8, "w")
+    d = Conv2dDesc.of(shape)
+    Ho, Wo = out_hw(shape)
+    if ws is None:
+        ws = _workspace(conv2d_int8_workspace(shape, xfmt), x_nhwc.device)
+    if out is None:
+        out = torch.empty((d.N, d.M, Ho, Wo), dtype=torch.int32, device=x_nhwc.device)
+    _check(lib().samd_conv2d_int8(x_nhwc.data_ptr(), xfmt, w.data_ptr(), wfmt, ctypes.byref(d), out.data_ptr(),
+                                  ws.data_ptr(), ws.numel(), _stream(x_nhwc)))
+    return out
+
+
+def max_i32(t: torch.Tensor, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    _dev(t, torch.int32, "t")
+    if out is None:
+        out = torch.empty(1, dtype=torch.int32, device=t.device)
+    _check(lib().samd_max_i32(t.data_ptr(), t.numel(), out.data_ptr(), _stream(t)))
+    return out
+
+
+def relu_requant_pack(acc: torch.Tensor, dev_max: torch.Tensor, bits: int,
+                      shift_out: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """ReLU + requantise an int32 tensor's rows (last axis) to packed unsigned b bits."""
+    _dev(acc, torch.int32, "acc")
+    length = acc.shape[-1]
+    rows = acc.numel() // length
+    if out is None:
+        out = torch.empty(acc.shape[:-1] + (row_words(length, bits),), dtype=torch.int32, device=acc.device)
+    _check(lib().samd_relu_requant_pack(acc.data_ptr(), rows, length, dev_max.data_ptr(), Fmt(bits, False),
+                                        out.data_ptr(), shift_out.data_ptr() if shift_out is not None else None,
+                                        _stream(acc)))
+    return out
+
+
+def relu_requant_nhwc_u8(acc: torch.Tensor, dev_max: torch.Tensor, bits: int,
+                         out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    _dev(acc, torch.int32, "acc")
+    N, C, H, W = acc.shape
+    if out is None:
+        out = torch.empty((N, H, W, C), dtype=torch.uint8, device=acc.device)
+    _check(lib().samd_relu_requant_nhwc_u8(acc.data_ptr(), N, C, H, W, dev_max.data_ptr(), Fmt(bits, False),
+                                           out.data_ptr(), _stream(acc)))
+    return out

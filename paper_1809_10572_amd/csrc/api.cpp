@@ -1,0 +1,319 @@
+// C ABI of the SAMD library: argument validation (host only, before any HIP call),
+// planning, and dispatch to the kernel launchers.
+#include <cstdarg>
+#include <cstdint>
+#include <cstdio>
+#include <string>
+
+#include "samd_internal.hpp"
+
+namespace samd {
+
+static thread_local std::string g_last_error;
+
+void set_error(const std::string &msg) { g_last_error = msg; }
+
+}  // namespace samd
+
+using namespace samd;
+
+namespace {
+
+int fail(int status, const char *fmt, ...) __attribute__((format(printf, 2, 3)));
+
+int fail(int status, const char *fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    set_error(buf);
+    return status;
+}
+
+int check_fmt(samd_fmt f, const char *name) {
+    if (f.bits < 1 || f.bits > 8)
+        return fail(SAMD_EINVAL, "%s.bits = %d is outside 1..8", name, f.bits);
+    if (f.is_signed != 0 && f.is_signed != 1)
+        return fail(SAMD_EINVAL, "%s.is_signed = %d must be 0 or 1", name, f.is_signed);
+    return SAMD_OK;
+}
+
+bool aligned4(const void *p) { return ((uintptr_t)p & 3) == 0; }
+
+int64_t max_abs(samd_fmt f) { return f.is_signed ? (int64_t)1 << (f.bits - 1) : ((int64_t)1 << f.bits) - 1; }
+
+int check_conv2d_desc(const samd_conv2d_desc *d) {
+    if (!d) return fail(SAMD_EINVAL, "descriptor is NULL");
+    if (d->N < 1 || d->C < 1 || d->H < 1 || d->W < 1 || d->M < 1 || d->KH < 1 || d->KW < 1)
+        return fail(SAMD_EINVAL, "shape N=%d C=%d H=%d W=%d M=%d KH=%d KW=%d must be positive", d->N, d->C,
+                    d->H, d->W, d->M, d->KH, d->KW);
+    if (d->stride_h < 1 || d->stride_w < 1 || d->pad_h < 0 || d->pad_w < 0)
+        return fail(SAMD_EINVAL, "strides must be >= 1 and pads >= 0");
+    if (d->pad_h >= d->KH || d->pad_w >= d->KW)
+        return fail(SAMD_EINVAL, "padding must be smaller than the kernel");
+    if (d->H + 2 * d->pad_h < d->KH || d->W + 2 * d->pad_w < d->KW)
+        return fail(SAMD_EINVAL, "kernel larger than the padded input");
+    return SAMD_OK;
+}
+
+// Exact int32 results: every output is a sum of C*KH*KW products of magnitude at most
+// max|x| * max|w|.
+int check_overflow(const samd_conv2d_desc *d, samd_fmt xf, samd_fmt wf) {
+    __int128 bound = (__int128)d->C * d->KH * d->KW * max_abs(xf) * max_abs(wf);
+    if (bound >= ((__int128)1 << 31))
+        return fail(SAMD_EOVERFLOW, "C*KH*KW*max|x|*max|w| = %lld does not fit int32", (long long)bound);
+    return SAMD_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *samd_status_str(int status) {
+    switch (status) {
+        case SAMD_OK: return "SAMD_OK";
+        case SAMD_EINVAL: return "SAMD_EINVAL: invalid argument";
+        case SAMD_EALIGN: return "SAMD_EALIGN: buffer not 4-byte aligned";
+        case SAMD_EUNSUPPORTED: return "SAMD_EUNSUPPORTED: no exact lane geometry";
+        case SAMD_EOVERFLOW: return "SAMD_EOVERFLOW: result may exceed int32";
+        case SAMD_EHIP: return "SAMD_EHIP: HIP runtime error";
+        case SAMD_ENOSPC: return "SAMD_ENOSPC: workspace too small";
+        default: return "unknown SAMD status";
+    }
+}
+
+const char *samd_last_error(void) { return g_last_error.c_str(); }
+
+int64_t samd_row_words(int64_t len, samd_fmt f) {
+    int st = check_fmt(f, "fmt");
+    if (st) return st;
+    if (len < 0) return fail(SAMD_EINVAL, "len = %lld is negative", (long long)len);
+    return row_words(len, f.bits);
+}
+
+int samd_pack(const void *src, int64_t rows, int64_t len, samd_fmt f, uint32_t *dst, int32_t *oor_count,
+              hipStream_t stream) {
+    set_error("");
+    int st = check_fmt(f, "fmt");
+    if (st) return st;
+    if (rows < 0 || len < 0) return fail(SAMD_EINVAL, "rows and len must be >= 0");
+    if (rows == 0 || len == 0) return SAMD_OK;
+    if (!src || !dst) return fail(SAMD_EINVAL, "src and dst must not be NULL");
+    if (!aligned4(dst) || (oor_count && !aligned4(oor_count))) return fail(SAMD_EALIGN, "dst / oor_count not aligned");
+    return launch_pack(src, rows, len, f.bits, f.is_signed, dst, oor_count, stream);
+}
+
+int samd_unpack(const uint32_t *src, int64_t rows, int64_t len, samd_fmt f, void *dst, hipStream_t stream) {
+    set_error("");
+    int st = check_fmt(f, "fmt");
+    if (st) return st;
+    if (rows < 0 || len < 0) return fail(SAMD_EINVAL, "rows and len must be >= 0");
+    if (rows == 0 || len == 0) return SAMD_OK;
+    if (!src || !dst) return fail(SAMD_EINVAL, "src and dst must not be NULL");
+    if (!aligned4(src)) return fail(SAMD_EALIGN, "src not aligned");
+    return launch_unpack(src, rows, len, f.bits, f.is_signed, dst, stream);
+}
+
+}  // extern "C"
+
+namespace {
+
+// Checks shared by samd_conv1d and its plan query; plans into g.
+int conv1d_checks(int64_t n, samd_fmt xf, const int32_t *taps, int32_t K, samd_fmt kf, Conv1dGeom &g) {
+    int st = check_fmt(xf, "xf");
+    if (!st) st = check_fmt(kf, "kf");
+    if (st) return st;
+    if (xf.is_signed || kf.is_signed) return fail(SAMD_EINVAL, "samd_conv1d takes unsigned operands");
+    if (!taps) return fail(SAMD_EINVAL, "taps must not be NULL");
+    if (K < 1 || K > 16) return fail(SAMD_EINVAL, "K = %d is outside 1..16", K);
+    if (n < K) return fail(SAMD_EINVAL, "n = %lld is shorter than the kernel", (long long)n);
+    if (n > ((int64_t)1 << 31)) return fail(SAMD_EINVAL, "n = %lld too large", (long long)n);
+    for (int t = 0; t < K; ++t)
+        if (taps[t] < 0 || taps[t] > (1 << kf.bits) - 1)
+            return fail(SAMD_EINVAL, "tap %d = %d outside the %d-bit unsigned range", t, taps[t], kf.bits);
+    __int128 bound = (__int128)K * (((int64_t)1 << xf.bits) - 1) * (((int64_t)1 << kf.bits) - 1);
+    if (bound >= ((__int128)1 << 31)) return fail(SAMD_EOVERFLOW, "K*max|x|*max|k| does not fit int32");
+    std::string err;
+    st = plan_conv1d(n, xf, taps, K, kf, g, err);
+    if (st) return fail(st, "%s", err.c_str());
+    return SAMD_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int samd_conv1d(const uint32_t *x, int64_t n, samd_fmt xf, const int32_t *taps, int32_t K, samd_fmt kf,
+                int32_t *y, hipStream_t stream) {
+    set_error("");
+    Conv1dGeom g;
+    int st = conv1d_checks(n, xf, taps, K, kf, g);
+    if (st) return st;
+    if (!x || !y) return fail(SAMD_EINVAL, "x and y must not be NULL");
+    if (!aligned4(x) || !aligned4(y)) return fail(SAMD_EALIGN, "x / y not aligned");
+    return launch_conv1d(x, g, y, stream);
+}
+
+int samd_conv1d_plan_query(int64_t n, samd_fmt xf, const int32_t *taps, int32_t K, samd_fmt kf,
+                           samd_conv1d_plan *out) {
+    set_error("");
+    Conv1dGeom g;
+    int st = conv1d_checks(n, xf, taps, K, kf, g);
+    if (st) return st;
+    if (!out) return fail(SAMD_EINVAL, "out must not be NULL");
+    *out = samd_conv1d_plan{};
+    out->lane_bits = g.L;
+    out->lanes = g.I;
+    out->groups = g.ngroups;
+    out->extra = g.extra;
+    out->out_lanes = g.nl;
+    for (int q = 0; q < g.ngroups; ++q) {
+        out->tap0[q] = g.g_tap0[q];
+        out->ntaps[q] = g.g_ntaps[q];
+    }
+    return SAMD_OK;
+}
+
+int samd_conv2d_plan_query(const samd_conv2d_desc *d, samd_fmt xf, samd_fmt wf, samd_conv2d_plan *out) {
+    set_error("");
+    int st = check_fmt(xf, "xf");
+    if (!st) st = check_fmt(wf, "wf");
+    if (!st) st = check_conv2d_desc(d);
+    if (!st) st = check_overflow(d, xf, wf);
+    if (st) return st;
+    if (!out) return fail(SAMD_EINVAL, "out must not be NULL");
+    Conv2dGeom g;
+    std::string err;
+    st = plan_conv2d(*d, xf, wf, g, err);
+    if (st) return fail(st, "%s", err.c_str());
+    *out = samd_conv2d_plan{};
+    out->lane_bits = g.L;
+    out->lanes = g.I;
+    out->taps_max = g.Kmax;
+    out->words_per_row = g.nq;
+    out->flush_channels = g.G;
+    out->out_lanes = g.nl;
+    out->tap_words = g.ntw;
+    for (int t = 0; t < g.ntw; ++t) {
+        out->phase[t] = g.tw_phase[t];
+        out->tap0[t] = g.tw_tap0[t];
+        out->ntaps[t] = g.tw_ntaps[t];
+    }
+    out->rows_per_block = g.rows_blk;
+    out->mblock = g.mblk;
+    out->macs_per_mad = g.macs_per_mad;
+    return SAMD_OK;
+}
+
+int samd_conv2d_workspace(const samd_conv2d_desc *d, samd_fmt xf, samd_fmt wf, size_t *bytes) {
+    set_error("");
+    int st = check_fmt(xf, "xf");
+    if (!st) st = check_fmt(wf, "wf");
+    if (!st) st = check_conv2d_desc(d);
+    if (!st) st = check_overflow(d, xf, wf);
+    if (st) return st;
+    if (!bytes) return fail(SAMD_EINVAL, "bytes must not be NULL");
+    Conv2dGeom g;
+    std::string err;
+    st = plan_conv2d(*d, xf, wf, g, err);
+    if (st) return fail(st, "%s", err.c_str());
+    *bytes = conv2d_workspace_bytes(g);
+    return SAMD_OK;
+}
+
+int samd_conv2d(const uint32_t *x, samd_fmt xf, const uint32_t *w, samd_fmt wf, const samd_conv2d_desc *d,
+                int32_t *y, void *ws, size_t ws_bytes, hipStream_t stream) {
+    set_error("");
+    int st = check_fmt(xf, "xf");
+    if (!st) st = check_fmt(wf, "wf");
+    if (!st) st = check_conv2d_desc(d);
+    if (!st) st = check_overflow(d, xf, wf);
+    if (st) return st;
+    if (!x || !w || !y || !ws) return fail(SAMD_EINVAL, "x, w, y and ws must not be NULL");
+    if (!aligned4(x) || !aligned4(w) || !aligned4(y)) return fail(SAMD_EALIGN, "x / w / y not aligned");
+    if (((uintptr_t)ws & 255) != 0) return fail(SAMD_EALIGN, "workspace not 256-byte aligned");
+    Conv2dGeom g;
+    std::string err;
+    st = plan_conv2d(*d, xf, wf, g, err);
+    if (st) return fail(st, "%s", err.c_str());
+    size_t need = conv2d_workspace_bytes(g);
+    if (ws_bytes < need)
+        return fail(SAMD_ENOSPC, "workspace %zu bytes < %zu needed", ws_bytes, need);
+    return launch_conv2d_samd(x, w, g, y, ws, stream);
+}
+
+namespace {
+
+// The 8-bit baseline takes signed activations, or unsigned ones of up to 8 bits, and
+// signed weights (8-bit unsigned weights do not fit int8).
+int check_int8_formats(samd_fmt xf, samd_fmt wf) {
+    int st = check_fmt(xf, "xf");
+    if (!st) st = check_fmt(wf, "wf");
+    if (st) return st;
+    if (!wf.is_signed && wf.bits == 8) return fail(SAMD_EINVAL, "8-bit unsigned weights do not fit int8");
+    return SAMD_OK;
+}
+
+}  // namespace
+
+int samd_conv2d_int8_workspace(const samd_conv2d_desc *d, samd_fmt xf, size_t *bytes) {
+    set_error("");
+    int st = check_fmt(xf, "xf");
+    if (!st) st = check_conv2d_desc(d);
+    if (st) return st;
+    if (!bytes) return fail(SAMD_EINVAL, "bytes must not be NULL");
+    *bytes = conv2d_i8_workspace_bytes(*d, xf);
+    return SAMD_OK;
+}
+
+int samd_conv2d_int8(const void *x, samd_fmt xf, const int8_t *w, samd_fmt wf, const samd_conv2d_desc *d,
+                     int32_t *y, void *ws, size_t ws_bytes, hipStream_t stream) {
+    set_error("");
+    int st = check_int8_formats(xf, wf);
+    if (!st) st = check_conv2d_desc(d);
+    if (!st) st = check_overflow(d, xf, wf);
+    if (st) return st;
+    if (!x || !w || !y || !ws) return fail(SAMD_EINVAL, "x, w, y and ws must not be NULL");
+    if (!aligned4(y)) return fail(SAMD_EALIGN, "y not aligned");
+    if (((uintptr_t)ws & 255) != 0) return fail(SAMD_EALIGN, "workspace not 256-byte aligned");
+    size_t need = conv2d_i8_workspace_bytes(*d, xf);
+    if (ws_bytes < need) return fail(SAMD_ENOSPC, "workspace %zu bytes < %zu needed", ws_bytes, need);
+    return launch_conv2d_i8(x, xf, w, *d, y, ws, stream);
+}
+
+int samd_max_i32(const int32_t *src, int64_t n, int32_t *dev_max, hipStream_t stream) {
+    set_error("");
+    if (n < 1) return fail(SAMD_EINVAL, "n must be >= 1");
+    if (!src || !dev_max) return fail(SAMD_EINVAL, "src and dev_max must not be NULL");
+    if (!aligned4(src) || !aligned4(dev_max)) return fail(SAMD_EALIGN, "src / dev_max not aligned");
+    return launch_max_i32(src, n, dev_max, stream);
+}
+
+int samd_relu_requant_pack(const int32_t *acc, int64_t rows, int64_t len, const int32_t *dev_max, samd_fmt out,
+                           uint32_t *dst, int32_t *dev_shift, hipStream_t stream) {
+    set_error("");
+    int st = check_fmt(out, "out");
+    if (st) return st;
+    if (out.is_signed) return fail(SAMD_EINVAL, "requantised activations are unsigned");
+    if (rows < 0 || len < 0) return fail(SAMD_EINVAL, "rows and len must be >= 0");
+    if (!acc || !dev_max || !dst) return fail(SAMD_EINVAL, "acc, dev_max and dst must not be NULL");
+    if (!aligned4(acc) || !aligned4(dst) || !aligned4(dev_max) || (dev_shift && !aligned4(dev_shift)))
+        return fail(SAMD_EALIGN, "buffer not aligned");
+    if (rows == 0 || len == 0) return SAMD_OK;
+    return launch_relu_requant_pack(acc, rows, len, dev_max, out.bits, dst, dev_shift, stream);
+}
+
+int samd_relu_requant_nhwc_u8(const int32_t *acc, int32_t N, int32_t C, int32_t H, int32_t W,
+                              const int32_t *dev_max, samd_fmt out, uint8_t *dst, hipStream_t stream) {
+    set_error("");
+    int st = check_fmt(out, "out");
+    if (st) return st;
+    if (out.is_signed) return fail(SAMD_EINVAL, "requantised activations are unsigned");
+    if (N < 1 || C < 1 || H < 1 || W < 1) return fail(SAMD_EINVAL, "shape must be positive");
+    if (!acc || !dev_max || !dst) return fail(SAMD_EINVAL, "acc, dev_max and dst must not be NULL");
+    if (!aligned4(acc) || !aligned4(dev_max)) return fail(SAMD_EALIGN, "buffer not aligned");
+    return launch_relu_requant_nhwc_u8(acc, N, C, H, W, dev_max, out.bits, dst, stream);
+}
+
+}  // extern "C"

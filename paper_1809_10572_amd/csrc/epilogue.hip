@@ -1,0 +1,120 @@
+// Between-layer epilogue of the AlexNet-shaped stack: the layer maximum, then ReLU and
+// requantisation to unsigned b bits, written either in the packed storage format (the
+// SAMD chain) or as NHWC uint8 (the 8-bit baseline chain).  The paper fixes no rule;
+// the library's rule: mx = max(max(acc), 0), s = the smallest s >= 0 with
+// mx >> s <= 2^b - 1, q = min((max(v, 0) + (s ? 2^(s-1) : 0)) >> s, 2^b - 1).
+#include <hip/hip_runtime.h>
+
+#include <climits>
+
+#include "hip_util.hpp"
+
+namespace samd {
+
+namespace {
+
+constexpr int kBlock = 256;
+
+__global__ void max_init_kernel(int32_t *dev_max) {
+    if (threadIdx.x == 0 && blockIdx.x == 0) *dev_max = INT_MIN;
+}
+
+__global__ __launch_bounds__(kBlock) void max_kernel(const int32_t *__restrict__ src, int64_t n, int32_t *dev_max) {
+    int32_t m = INT_MIN;
+    for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < n; i += (int64_t)gridDim.x * kBlock)
+        m = max(m, src[i]);
+    for (int off = 32; off > 0; off >>= 1) m = max(m, __shfl_xor(m, off, 64));
+    if ((threadIdx.x & 63) == 0) atomicMax(dev_max, m);
+}
+
+// Requantisation shift for a layer maximum.
+__device__ inline int requant_shift(int32_t layer_max, int bits) {
+    const uint32_t mx = layer_max > 0 ? (uint32_t)layer_max : 0u;
+    const int len = 32 - __clz(mx);   // bit length, 0 for 0
+    return len > bits ? len - bits : 0;
+}
+
+__device__ inline uint32_t requant(int32_t v, int shift, int bits) {
+    const int64_t r = v > 0 ? v : 0;
+    const int64_t half = shift ? (int64_t)1 << (shift - 1) : 0;
+    const int64_t q = (r + half) >> shift;
+    const int64_t top = ((int64_t)1 << bits) - 1;
+    return (uint32_t)(q < top ? q : top);
+}
+
+template <int B>
+__global__ __launch_bounds__(kBlock) void relu_requant_pack_kernel(const int32_t *__restrict__ acc, int64_t rows,
+                                                                   int64_t len, int64_t words_per_row,
+                                                                   const int32_t *__restrict__ dev_max,
+                                                                   uint32_t *__restrict__ dst,
+                                                                   int32_t *__restrict__ dev_shift) {
+    constexpr int P = 32 / B;
+    const int shift = requant_shift(*dev_max, B);
+    if (dev_shift && blockIdx.x == 0 && threadIdx.x == 0) *dev_shift = shift;
+    const int64_t total = rows * words_per_row;
+    for (int64_t w = (int64_t)blockIdx.x * kBlock + threadIdx.x; w < total; w += (int64_t)gridDim.x * kBlock) {
+        const int64_t r = w / words_per_row, q = w - r * words_per_row;
+        const int64_t j0 = q * P;
+        const int cnt = (int)min((int64_t)P, len - j0);
+        const int32_t *a = acc + r * len + j0;
+        uint32_t word = 0;
+#pragma unroll
+        for (int i = 0; i < P; ++i)
+            if (i < cnt) word |= requant(a[i], shift, B) << (i * B);
+        dst[w] = word;
+    }
+}
+
+// One thread per NHWC output byte; reads the NCHW accumulator.
+__global__ __launch_bounds__(kBlock) void relu_requant_nhwc_kernel(const int32_t *__restrict__ acc, int N, int C,
+                                                                   int H, int W, const int32_t *__restrict__ dev_max,
+                                                                   int bits, uint8_t *__restrict__ dst) {
+    const int shift = requant_shift(*dev_max, bits);
+    const int64_t total = (int64_t)N * C * H * W;
+    for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < total; i += (int64_t)gridDim.x * kBlock) {
+        const int c = (int)(i % C);
+        const int64_t p = i / C;   // (n, h, w)
+        const int w = (int)(p % W);
+        const int64_t t = p / W;
+        const int h = (int)(t % H);
+        const int n = (int)(t / H);
+        dst[i] = (uint8_t)requant(acc[(((int64_t)n * C + c) * H + h) * W + w], shift, bits);
+    }
+}
+
+}  // namespace
+
+int launch_max_i32(const int32_t *src, int64_t n, int32_t *dev_max, hipStream_t s) {
+    hipLaunchKernelGGL(max_init_kernel, dim3(1), dim3(64), 0, s, dev_max);
+    int st = check_launch("max init");
+    if (st) return st;
+    const int grid = std::min(grid_for(n, kBlock), 2048);
+    hipLaunchKernelGGL(max_kernel, dim3(grid), dim3(kBlock), 0, s, src, n, dev_max);
+    return check_launch("max");
+}
+
+int launch_relu_requant_pack(const int32_t *acc, int64_t rows, int64_t len, const int32_t *dev_max, int bits,
+                             uint32_t *dst, int32_t *dev_shift, hipStream_t s) {
+    const int64_t wpr = row_words(len, bits);
+    const int grid = grid_for(rows * wpr, kBlock);
+#define SAMD_REQ_CASE(B)                                                                                         \
+    if (bits == B) {                                                                                             \
+        hipLaunchKernelGGL((relu_requant_pack_kernel<B>), dim3(grid), dim3(kBlock), 0, s, acc, rows, len, wpr, \
+                           dev_max, dst, dev_shift);                                                           \
+        return check_launch("relu_requant_pack");                                                              \
+    }
+    SAMD_REQ_CASE(1) SAMD_REQ_CASE(2) SAMD_REQ_CASE(3) SAMD_REQ_CASE(4)
+    SAMD_REQ_CASE(5) SAMD_REQ_CASE(6) SAMD_REQ_CASE(7) SAMD_REQ_CASE(8)
+#undef SAMD_REQ_CASE
+    set_error("relu_requant_pack: unsupported bits");
+    return SAMD_EINVAL;
+}
+
+int launch_relu_requant_nhwc_u8(const int32_t *acc, int N, int C, int H, int W, const int32_t *dev_max, int bits,
+                                uint8_t *dst, hipStream_t s) {
+    const int grid = grid_for((int64_t)N * C * H * W, kBlock);
+    hipLaunchKernelGGL(relu_requant_nhwc_kernel, dim3(grid), dim3(kBlock), 0, s, acc, N, C, H, W, dev_max, bits, dst);
+    return check_launch("relu_requant_nhwc_u8");
+}
+
+}  // namespace samd

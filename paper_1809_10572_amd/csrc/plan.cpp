@@ -1,0 +1,276 @@
+// Host-side lane-geometry planning for the SAMD convolutions.  Pure C++: no HIP calls,
+// so it runs (and is tested) without a GPU.
+//
+// The paper sizes lanes so that no lane can overflow into its neighbour (Sec. 5.1:
+// a K-term sum of b x b-bit products needs 2b + log2 K bits) and keeps one bit of
+// margin in signed lanes for the borrow a negative lane hands to the lane above it
+// (Sec. 6).  Here the bound is computed exactly, per lane, for the products actually
+// accumulated into it before the lanes are decoded, and the planner picks among the
+// exact geometries the one with the lowest modelled cost.
+#include <algorithm>
+#include <cstdio>
+#include <limits>
+
+#include "samd_internal.hpp"
+
+namespace samd {
+
+namespace {
+
+typedef __int128 i128;
+
+i128 pow2(int e) { return (i128)1 << e; }
+
+// Range of a b-bit value.
+void value_range(int bits, bool is_signed, i128 &lo, i128 &hi) {
+    lo = is_signed ? -pow2(bits - 1) : 0;
+    hi = is_signed ? pow2(bits - 1) - 1 : pow2(bits) - 1;
+}
+
+i128 max_abs(int bits, bool is_signed) { return is_signed ? pow2(bits - 1) : pow2(bits) - 1; }
+
+// Does sum_{i<n} v_i 2^(i L) stay inside [lo_lim, hi_lim] for every b-bit v_i?
+bool word_fits(int bits, bool is_signed, int L, int n, i128 lo_lim, i128 hi_lim) {
+    if ((n - 1) * L + bits > 64) return false;
+    i128 lo, hi, place = 0;
+    value_range(bits, is_signed, lo, hi);
+    for (int i = 0; i < n; ++i) place += pow2(i * L);
+    return lo * place >= lo_lim && hi * place <= hi_lim;
+}
+
+const i128 kI32Min = -pow2(31), kI32Max = pow2(31) - 1;
+const i128 kI64Max = pow2(63) - 1;
+
+// Products of an I-value word and a k-tap word that land in lane j.
+int pairs_in_lane(int j, int I, int k) {
+    if (j < 0 || j > I + k - 2) return 0;
+    return std::min(std::min(j + 1, k), std::min(I, I + k - 1 - j));
+}
+
+// Split `count` consecutive taps into ceil(count / kmax) near-equal groups.
+void split_taps(int count, int kmax, int *t0, int *nt, int &ngroups) {
+    ngroups = (count + kmax - 1) / kmax;
+    int base = count / ngroups, extra = count % ngroups, at = 0;
+    for (int g = 0; g < ngroups; ++g) {
+        nt[g] = base + (g < extra ? 1 : 0);
+        t0[g] = at;
+        at += nt[g];
+    }
+}
+
+int pick_waves_m(int M) {
+    int best = 1;
+    long best_pad = std::numeric_limits<long>::max();
+    for (int wm : {4, 2, 1}) {
+        long blk = (long)wm * kWaveM;
+        long pad = (M + blk - 1) / blk * blk - M;
+        if (pad < best_pad) { best_pad = pad; best = wm; }
+    }
+    return best;
+}
+
+}  // namespace
+
+int plan_conv2d(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, Conv2dGeom &best, std::string &err) {
+    Conv2dGeom g = {};
+    g.N = d.N; g.C = d.C; g.H = d.H; g.W = d.W; g.M = d.M; g.KH = d.KH; g.KW = d.KW;
+    g.sh = d.stride_h; g.sw = d.stride_w; g.ph = d.pad_h; g.pw = d.pad_w;
+    g.Ho = (d.H + 2 * d.pad_h - d.KH) / d.stride_h + 1;
+    g.Wo = (d.W + 2 * d.pad_w - d.KW) / d.stride_w + 1;
+    g.xbits = xf.bits; g.xsigned = xf.is_signed; g.wbits = wf.bits; g.wsigned = wf.is_signed;
+    g.result_signed = (xf.is_signed || wf.is_signed) ? 1 : 0;
+    g.xrw = (int32_t)row_words(d.W, xf.bits);
+    g.wrw = (int32_t)row_words(d.KW, wf.bits);
+    g.wm = pick_waves_m(d.M);
+    g.mblk = g.wm * kWaveM;
+    g.nmb = (d.M + g.mblk - 1) / g.mblk;
+
+    const int S = d.stride_w;
+    g.Kmax = (d.KW + S - 1) / S;
+    const i128 prod = max_abs(xf.bits, xf.is_signed) * max_abs(wf.bits, wf.is_signed);
+    bool found = false;
+    best.cost = 1e300;
+
+    for (int L = 2; L <= 31; ++L) {
+        // widest kernel word and input word that stay int32 at this lane width
+        int kmax = 0;
+        for (int k = 1; k <= g.Kmax; ++k)
+            if (word_fits(wf.bits, wf.is_signed, L, k, kI32Min, kI32Max)) kmax = k;
+        if (kmax == 0) continue;
+        int imax = 0;
+        for (int i = 1; i <= kMaxLanes; ++i)
+            if (word_fits(xf.bits, xf.is_signed, L, i, kI32Min, kI32Max)) imax = i;
+        for (int I = 1; I <= imax; ++I) {
+            Conv2dGeom c = g;
+            c.L = L;
+            c.I = I;
+            // kernel words: every stride phase's taps in groups of at most kmax
+            c.ntw = 0;
+            c.nvar = 0;
+            bool ok = true;
+            for (int r = 0; r < S && ok; ++r) {
+                int Kr = r < d.KW ? (d.KW - r + S - 1) / S : 0;
+                if (Kr == 0) continue;
+                int t0[kMaxTapWords], nt[kMaxTapWords], ng;
+                split_taps(Kr, kmax, t0, nt, ng);
+                for (int q = 0; q < ng; ++q) {
+                    if (c.ntw >= kMaxTapWords) { ok = false; break; }
+                    int delta = t0[q] + nt[q] - c.Kmax;
+                    int v = -1;
+                    for (int u = 0; u < c.nvar; ++u)
+                        if (c.var_phase[u] == r && c.var_delta[u] == delta) v = u;
+                    if (v < 0) {
+                        if (c.nvar >= kMaxVariants) { ok = false; break; }
+                        v = c.nvar++;
+                        c.var_phase[v] = r;
+                        c.var_delta[v] = delta;
+                    }
+                    c.tw_phase[c.ntw] = r;
+                    c.tw_tap0[c.ntw] = t0[q];
+                    c.tw_ntaps[c.ntw] = nt[q];
+                    c.tw_var[c.ntw] = v;
+                    ++c.ntw;
+                }
+            }
+            if (!ok) continue;
+            // products per lane for one (channel, kernel row)
+            int nj[kMaxOutLanes + 8] = {0};
+            int top = -1;
+            for (int j = 0; j < I + c.Kmax - 1; ++j) {
+                for (int t = 0; t < c.ntw; ++t) nj[j] += pairs_in_lane(j, I, c.tw_ntaps[t]);
+                if (nj[j] > 0) top = j;
+            }
+            c.nl = top + 1;
+            if (c.nl > kMaxOutLanes) continue;
+            // largest number of channels whose sums every lane (and the whole word) holds
+            const i128 cap = c.result_signed ? pow2(L - 1) - 1 : pow2(L) - 1;
+            i128 gmax = d.C;
+            i128 place = 0;
+            for (int j = 0; j < c.nl; ++j) {
+                if (nj[j] == 0) continue;
+                i128 per = (i128)d.KH * nj[j] * prod;
+                if (j < c.nl - 1) gmax = std::min(gmax, cap / per);
+                if (j * L > 62) { gmax = 0; break; }
+                place += (i128)nj[j] * pow2(j * L);
+            }
+            if (gmax >= 1) gmax = std::min(gmax, kI64Max / ((i128)d.KH * prod * place));
+            if (gmax < 1) continue;
+            c.G = (int32_t)gmax;
+            c.msb_mask = 0;
+            for (int j = 0; j < c.nl - 1; ++j) c.msb_mask |= (uint64_t)1 << (j * L + L - 1);
+            c.nq = (c.Wo + c.Kmax - 1 + I - 1) / I;
+            if (c.nq > 64) continue;
+            c.rows_blk = std::max(1, std::min(64 / c.nq, c.Ho));
+            c.trows = (c.rows_blk - 1) * d.stride_h + d.KH;
+            c.nrt = d.KH * c.ntw;
+            // LDS: output tile, spread operand words and raw packed rows of a channel chunk
+            c.lds_tile = c.mblk * c.rows_blk * c.Wo;
+            c.cc = std::min(d.C, 8);
+            for (;;) {
+                c.lds_spread = c.cc * c.trows * c.nvar * c.nq;
+                c.lds_raw = c.cc * c.trows * c.xrw;
+                if ((long)(c.lds_tile + c.lds_spread + c.lds_raw) * 4 <= 65536 || c.cc == 1) break;
+                --c.cc;
+            }
+            if ((long)(c.lds_tile + c.lds_spread + c.lds_raw) * 4 > 65536) continue;
+            // cost per output value, in VALU issue slots
+            double mads = (double)d.C * d.KH * c.ntw;
+            double flushes = (double)((d.C + c.G - 1) / c.G);
+            double decode = (c.result_signed ? 6.0 : 0.0) + 4.0 * c.nl;
+            double staging = (double)d.C * c.trows * c.nvar * (6.0 * I + 4.0) / ((double)c.rows_blk * c.mblk);
+            double lane_util = (double)c.rows_blk * c.nq / 64.0;
+            int row_tiles = (c.Ho + c.rows_blk - 1) / c.rows_blk;
+            double row_util = (double)c.Ho / ((double)row_tiles * c.rows_blk);
+            c.cost = (mads + flushes * decode + staging) / I / (lane_util * row_util);
+            c.macs_per_mad = (double)I * d.KW / (double)c.ntw;
+            if (c.cost < best.cost) {
+                best = c;
+                found = true;
+            }
+        }
+    }
+    if (!found) {
+        char buf[160];
+        snprintf(buf, sizeof buf, "no exact SAMD lane geometry for %d-bit x %d-bit, KW=%d stride %d, Wo=%d",
+                 xf.bits, wf.bits, d.KW, d.stride_w, g.Wo);
+        err = buf;
+        return SAMD_EUNSUPPORTED;
+    }
+    return SAMD_OK;
+}
+
+size_t conv2d_workspace_bytes(const Conv2dGeom &g) {
+    return (size_t)g.nmb * g.mblk * g.C * g.nrt * sizeof(int32_t);
+}
+
+int plan_conv1d(int64_t n, samd_fmt xf, const int32_t *taps, int32_t K, samd_fmt kf, Conv1dGeom &best,
+                std::string &err) {
+    Conv1dGeom g = {};
+    g.n = n;
+    g.nout = n - K + 1;
+    g.bits = xf.bits;
+    g.K = K;
+    g.xrw = (int32_t)row_words(n, xf.bits);
+    const i128 xmax = pow2(xf.bits) - 1, kmax_v = pow2(kf.bits) - 1;
+    const i128 u32max = pow2(32) - 1, u64max = pow2(64) - 1;
+    double best_cost = 1e300;
+    bool found = false;
+    for (int L = 1; L <= 32; ++L) {
+        int kmax = 0;
+        for (int k = 1; k <= K; ++k)
+            if (word_fits(kf.bits, false, L, k, 0, u32max)) kmax = k;
+        if (kmax == 0) continue;
+        int imax = 0;
+        for (int i = 1; i <= 32; ++i)
+            if (word_fits(xf.bits, false, L, i, 0, u32max)) imax = i;
+        for (int I = 1; I <= imax; ++I) {
+            Conv1dGeom c = g;
+            c.L = L;
+            c.I = I;
+            int t0[kMaxTapWords], nt[kMaxTapWords];
+            if ((K + kmax - 1) / kmax > kMaxTapWords) continue;
+            split_taps(K, kmax, t0, nt, c.ngroups);
+            // lanes: j <-> output q*I + j - (K - 1); group g's window starts at q*I - t0[g]
+            int nl = I + K - 1, top = -1;
+            int nj[64] = {0};
+            for (int j = 0; j < nl; ++j) {
+                for (int q = 0; q < c.ngroups; ++q) nj[j] += pairs_in_lane(j, I, nt[q]);
+                if (nj[j]) top = j;
+            }
+            bool ok = true;
+            i128 total = 0;
+            for (int j = 0; j <= top && ok; ++j) {
+                i128 dmax = (i128)nj[j] * xmax * kmax_v;
+                if (j < top && dmax > pow2(L) - 1) ok = false;
+                if (j * L > 63 && dmax > 0) ok = false;
+                if (ok) total += dmax * pow2(j * L);
+            }
+            if (!ok || total > u64max) continue;
+            c.nl = top + 1;
+            for (int q = 0; q < c.ngroups; ++q) {
+                c.g_tap0[q] = t0[q];
+                c.g_ntaps[q] = nt[q];
+                c.g_delta[q] = -t0[q];
+                uint64_t word = 0;
+                for (int s = 0; s < nt[q]; ++s) word |= (uint64_t)(uint32_t)taps[t0[q] + s] << (s * L);
+                c.g_word[q] = (uint32_t)word;
+            }
+            c.extra = (K - 1 + I - 1) / I;
+            if (c.extra > kMaxConv1dExtra) continue;
+            c.nwords = (c.nout + I - 1) / I;
+            double cost = (double)c.ngroups * (1 + c.extra) * (2.0 + 3.0 * I) / I + 3.0 * (I + K) * (1 + c.extra) / I;
+            if (cost < best_cost) {
+                best_cost = cost;
+                best = c;
+                found = true;
+            }
+        }
+    }
+    if (!found) {
+        err = "no exact SAMD lane geometry for this 1-D convolution";
+        return SAMD_EUNSUPPORTED;
+    }
+    return SAMD_OK;
+}
+
+}  // namespace samd

@@ -1,0 +1,96 @@
+// Internal declarations of the SAMD library: the lane-geometry plans computed on the
+// host, the kernel launchers, and small helpers shared by host and device code.
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <string>
+
+#include "samd.h"
+
+namespace samd {
+
+constexpr int kMaxTapWords = 16;   // kernel words per (input channel, kernel row)
+constexpr int kMaxVariants = 16;   // distinct (stride phase, window offset) operand words
+constexpr int kMaxLanes = 16;      // I: values per operand word
+constexpr int kMaxOutLanes = 20;   // I + Kmax - 1: lanes of an accumulator that are decoded
+constexpr int kWaveM = 16;         // output channels per wave (64-bit accumulators per thread)
+constexpr int kMaxConv1dExtra = 15; // following words whose low lanes reach a 1-D output word
+
+// Geometry of one SAMD 2-D convolution.  Every operand word is a signed 32-bit
+// integer A = sum_i v_i 2^(i L) holding I input values of one stride phase of one
+// input row (temporary spacer bits between them, negative values sign-extended);
+// every kernel word B = sum_s w_s 2^(s L) holds up to Kmax taps of one phase of one
+// kernel row, reversed.  A*B accumulates into a 64-bit integer whose L-bit lane j
+// holds a partial sum for output column q*I + j - (Kmax - 1).
+struct Conv2dGeom {
+    int32_t N, C, H, W, M, KH, KW, sh, sw, ph, pw, Ho, Wo;
+    int32_t xbits, xsigned, wbits, wsigned;
+    int32_t L, I, Kmax, nq, G;      // lane bits, values/word, widest phase, words/row, flush channels
+    int32_t nl;                     // decoded lanes per accumulator, I + Kmax - 1
+    int32_t result_signed;          // any operand signed: lanes need the fix-up
+    uint64_t msb_mask;              // sign bit of lanes 0 .. nl-2
+    int32_t ntw;                    // kernel words per (channel, kernel row)
+    int32_t tw_phase[kMaxTapWords], tw_tap0[kMaxTapWords], tw_ntaps[kMaxTapWords];
+    int32_t tw_var[kMaxTapWords];   // operand-word variant each kernel word multiplies
+    int32_t nvar;                   // operand-word variants
+    int32_t var_phase[kMaxVariants], var_delta[kMaxVariants];
+    int32_t nrt;                    // row-taps per channel: KH * ntw
+    // launch shape
+    int32_t rows_blk;               // output rows per workgroup (lanes = rows_blk * nq <= 64)
+    int32_t wm;                     // waves per workgroup, each kWaveM output channels
+    int32_t mblk;                   // output channels per workgroup, wm * kWaveM
+    int32_t nmb;                    // output-channel blocks
+    int32_t cc;                     // input channels staged per chunk
+    int32_t trows;                  // input rows staged per chunk, (rows_blk-1)*sh + KH
+    int32_t xrw;                    // packed words per input row
+    int32_t wrw;                    // packed words per kernel row
+    int32_t lds_tile, lds_spread, lds_raw;  // LDS words of each region
+    double macs_per_mad, cost;
+};
+
+// 1-D convolution geometry (unsigned operands, 32x32 -> 64-bit products).
+struct Conv1dGeom {
+    int64_t n, nout, nwords;        // inputs, outputs, output words
+    int32_t bits, K, L, I, extra;   // extra: following words whose low lanes reach a word's outputs
+    int32_t nl;                     // lanes that can be non-zero; lane nl-1 takes all remaining bits
+    int32_t ngroups;
+    int32_t g_tap0[kMaxTapWords], g_ntaps[kMaxTapWords];
+    int32_t g_delta[kMaxTapWords];  // window offset of each kernel word
+    uint32_t g_word[kMaxTapWords];  // the kernel words themselves (taps packed, unsigned)
+    int32_t xrw;
+};
+
+// Host planning (pure C++, no HIP calls).  Return SAMD_OK or an error with `err` set.
+int plan_conv2d(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, Conv2dGeom &g, std::string &err);
+int plan_conv1d(int64_t n, samd_fmt xf, const int32_t *taps, int32_t K, samd_fmt kf, Conv1dGeom &g,
+                std::string &err);
+size_t conv2d_workspace_bytes(const Conv2dGeom &g);
+
+// Kernel launchers (enqueue only; report launch errors through the return value).
+int launch_pack(const void *src, int64_t rows, int64_t len, int bits, int is_signed, uint32_t *dst,
+                int32_t *oor, hipStream_t s);
+int launch_unpack(const uint32_t *src, int64_t rows, int64_t len, int bits, int is_signed, void *dst,
+                  hipStream_t s);
+int launch_conv1d(const uint32_t *x, const Conv1dGeom &g, int32_t *y, hipStream_t s);
+int launch_conv2d_samd(const uint32_t *x, const uint32_t *w, const Conv2dGeom &g, int32_t *y, void *ws,
+                       hipStream_t s);
+size_t conv2d_i8_workspace_bytes(const samd_conv2d_desc &d, samd_fmt xf);
+int launch_conv2d_i8(const void *x, samd_fmt xf, const int8_t *w, const samd_conv2d_desc &d, int32_t *y, void *ws,
+                     hipStream_t s);
+int launch_max_i32(const int32_t *src, int64_t n, int32_t *dev_max, hipStream_t s);
+int launch_relu_requant_pack(const int32_t *acc, int64_t rows, int64_t len, const int32_t *dev_max, int bits,
+                             uint32_t *dst, int32_t *dev_shift, hipStream_t s);
+int launch_relu_requant_nhwc_u8(const int32_t *acc, int N, int C, int H, int W, const int32_t *dev_max,
+                                int bits, uint8_t *dst, hipStream_t s);
+
+// Error detail for the calling thread.
+void set_error(const std::string &msg);
+
+inline int64_t row_words(int64_t len, int bits) {
+    const int64_t per = 32 / bits;
+    return (len + per - 1) / per;
+}
+
+}  // namespace samd

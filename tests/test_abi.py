@@ -1,0 +1,133 @@
+"""The C ABI without a GPU: the library loads, exports every function include/samd.h
+declares, and rejects bad arguments on the host before any HIP call."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_1809_10572_amd as samd
+from paper_1809_10572_amd import Conv2dDesc, Fmt
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "samd.h")
+
+OK, EINVAL, EALIGN, EUNSUP, EOVERFLOW, EHIP, ENOSPC = 0, -1, -2, -3, -4, -5, -6
+MID = Conv2dDesc(8, 128, 56, 56, 128, 3, 3, 1, 1, 1, 1)
+# fake device addresses: validation must reject before anything is dereferenced
+P4, P1 = 0x10000, 0x10001
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(samd_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_function():
+    names = declared_functions()
+    assert len(names) >= 14
+    L = ctypes.CDLL(samd.LIB_PATH)
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def test_status_strings():
+    L = samd.lib()
+    for code in (OK, EINVAL, EALIGN, EUNSUP, EOVERFLOW, EHIP, ENOSPC):
+        assert L.samd_status_str(code).startswith(b"SAMD_")
+    assert L.samd_status_str(12345) == b"unknown SAMD status"
+
+
+def test_row_words_and_format_checks():
+    L = samd.lib()
+    assert L.samd_row_words(56, Fmt(4, 0)) == 7 and L.samd_row_words(1 << 20, Fmt(3, 0)) == 104858
+    assert L.samd_row_words(10, Fmt(0, 0)) == EINVAL and L.samd_row_words(10, Fmt(9, 1)) == EINVAL
+    assert L.samd_row_words(-1, Fmt(4, 0)) == EINVAL
+    raw = Fmt(4, 0)
+    raw.is_signed = 2          # the ABI accepts only 0 or 1
+    assert L.samd_row_words(10, raw) == EINVAL
+    assert b"outside 1..8" in L.samd_last_error() or b"must be 0 or 1" in L.samd_last_error()
+
+
+def test_pack_unpack_validation():
+    L = samd.lib()
+    assert L.samd_pack(P4, 2, 8, Fmt(9, 0), P4, None, None) == EINVAL
+    assert L.samd_pack(None, 2, 8, Fmt(4, 0), P4, None, None) == EINVAL
+    assert L.samd_pack(P4, 2, 8, Fmt(4, 0), P1, None, None) == EALIGN
+    assert L.samd_pack(P4, 2, 8, Fmt(4, 0), P4, P1, None) == EALIGN
+    assert L.samd_pack(P4, -1, 8, Fmt(4, 0), P4, None, None) == EINVAL
+    assert L.samd_pack(None, 0, 8, Fmt(4, 0), None, None, None) == OK   # empty: nothing to do
+    assert L.samd_unpack(P1, 2, 8, Fmt(4, 0), P4, None) == EALIGN
+    assert L.samd_unpack(P4, 2, 8, Fmt(4, 0), None, None) == EINVAL
+
+
+def test_conv1d_validation():
+    L = samd.lib()
+    taps = (ctypes.c_int32 * 3)(1, 2, 3)
+    assert L.samd_conv1d(P4, 100, Fmt(4, 1), taps, 3, Fmt(4, 0), P4, None) == EINVAL     # signed input
+    assert L.samd_conv1d(P4, 100, Fmt(4, 0), None, 3, Fmt(4, 0), P4, None) == EINVAL
+    assert L.samd_conv1d(P4, 2, Fmt(4, 0), taps, 3, Fmt(4, 0), P4, None) == EINVAL        # n < K
+    assert L.samd_conv1d(P4, 100, Fmt(4, 0), taps, 0, Fmt(4, 0), P4, None) == EINVAL
+    bad = (ctypes.c_int32 * 3)(1, 16, 3)
+    assert L.samd_conv1d(P4, 100, Fmt(4, 0), bad, 3, Fmt(4, 0), P4, None) == EINVAL       # tap too wide
+    assert L.samd_conv1d(P1, 100, Fmt(4, 0), taps, 3, Fmt(4, 0), P4, None) == EALIGN
+
+
+def test_conv2d_validation():
+    L = samd.lib()
+    n = ctypes.c_size_t(0)
+    assert L.samd_conv2d_workspace(ctypes.byref(MID), Fmt(4, 0), Fmt(4, 1), ctypes.byref(n)) == OK
+    assert n.value > 0
+    need = n.value
+    args = lambda **kw: dict(dict(x=P4, xf=Fmt(4, 0), w=P4, wf=Fmt(4, 1), d=MID, y=P4, ws=P4 * 16, nb=need), **kw)
+
+    def call(**kw):
+        a = args(**kw)
+        return L.samd_conv2d(a["x"], a["xf"], a["w"], a["wf"], ctypes.byref(a["d"]) if a["d"] else None, a["y"],
+                             a["ws"], a["nb"], None)
+
+    assert call(xf=Fmt(0, 0)) == EINVAL
+    raw = Fmt(4, 0)
+    raw.is_signed = 3
+    assert call(wf=raw) == EINVAL
+    assert call(d=None) == EINVAL
+    assert call(d=Conv2dDesc(8, 0, 56, 56, 128, 3, 3, 1, 1, 1, 1)) == EINVAL
+    assert call(d=Conv2dDesc(8, 128, 56, 56, 128, 3, 3, 0, 1, 1, 1)) == EINVAL
+    assert call(d=Conv2dDesc(8, 128, 56, 56, 128, 3, 3, 1, 1, 3, 1)) == EINVAL      # pad >= kernel
+    assert call(d=Conv2dDesc(1, 1, 2, 2, 1, 5, 5, 1, 1, 1, 1)) == EINVAL            # kernel > padded input
+    assert call(x=None) == EINVAL
+    assert call(y=P1) == EALIGN
+    assert call(ws=P4 * 16 + 4) == EALIGN
+    assert call(nb=need - 1) == ENOSPC
+    # 8-bit x 8-bit over 256 channels of 3x3: 256*9*255*128 < 2^31, but 16x16 taps do not fit
+    big = Conv2dDesc(1, 512, 16, 16, 1, 16, 16, 1, 1, 0, 0)
+    assert call(d=big, xf=Fmt(8, 0), wf=Fmt(8, 1)) == EOVERFLOW
+    assert b"does not fit int32" in L.samd_last_error()
+
+
+def test_conv2d_int8_validation():
+    L = samd.lib()
+    n = ctypes.c_size_t(0)
+    assert L.samd_conv2d_int8_workspace(ctypes.byref(MID), Fmt(8, 0), ctypes.byref(n)) == OK and n.value > 0
+    call = lambda xf=Fmt(8, 0), wf=Fmt(8, 1), y=P4, ws=P4 * 16, nb=n.value: L.samd_conv2d_int8(
+        P4, xf, P4, wf, ctypes.byref(MID), y, ws, nb, None)
+    assert call(wf=Fmt(8, 0)) == EINVAL          # unsigned 8-bit weights do not fit int8
+    assert call(y=P1) == EALIGN
+    assert call(nb=n.value - 1) == ENOSPC
+    assert call(ws=P4 + 64) == EALIGN
+
+
+def test_epilogue_validation():
+    L = samd.lib()
+    assert L.samd_max_i32(P4, 0, P4, None) == EINVAL
+    assert L.samd_max_i32(P1, 10, P4, None) == EALIGN
+    assert L.samd_relu_requant_pack(P4, 4, 4, P4, Fmt(4, 1), P4, None, None) == EINVAL   # signed output
+    assert L.samd_relu_requant_pack(P4, 4, 4, None, Fmt(4, 0), P4, None, None) == EINVAL
+    assert L.samd_relu_requant_nhwc_u8(P4, 1, 0, 1, 1, P4, Fmt(4, 0), P4, None) == EINVAL
+
+
+def test_calls_fail_loudly_without_a_gpu_tensor():
+    import torch
+    with pytest.raises(ValueError):
+        samd.pack(torch.zeros(4, dtype=torch.uint8), 4, False)

@@ -1,0 +1,271 @@
+"""GPU parity: every result of the HIP library, called through its C ABI, compared
+element by element with the CPU oracle on the same seeded inputs.  All results are
+integers, so the bar is bit-exact equality."""
+import numpy as np
+import pytest
+import torch
+
+import paper_1809_10572_amd as samd
+import samd_workloads as wl
+from oracle import reference as ref
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+
+
+def gpu_vals(a: np.ndarray, signed: bool) -> torch.Tensor:
+    return torch.from_numpy(np.ascontiguousarray(a).astype(np.int8 if signed else np.uint8)).to(DEV)
+
+
+def gpu_words(words: np.ndarray) -> torch.Tensor:
+    return torch.from_numpy(np.ascontiguousarray(words).view(np.int32)).to(DEV)
+
+
+def host_words(t: torch.Tensor) -> np.ndarray:
+    return t.cpu().numpy().view(np.uint32)
+
+
+def run_conv2d(x, w, shape, xf, wf):
+    """Pack on the GPU, convolve with SAMD, return int32 numpy."""
+    xs = gpu_vals(x, xf.is_signed)
+    ws = gpu_vals(w, wf.is_signed)
+    xp = samd.pack(xs, xf.bits, xf.is_signed)
+    wp = samd.pack(ws, wf.bits, wf.is_signed)
+    y = samd.conv2d(xp, xf, wp, wf, shape)
+    torch.cuda.synchronize()
+    return y.cpu().numpy()
+
+
+def run_conv2d_int8(x, w, shape, xf, wf):
+    xs = gpu_vals(np.transpose(x, (0, 2, 3, 1)), xf.is_signed)   # NHWC
+    ws = gpu_vals(w, True)
+    y = samd.conv2d_int8(xs, xf, ws, wf, shape)
+    torch.cuda.synchronize()
+    return y.cpu().numpy()
+
+
+# --- packing ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("bits", range(1, 9))
+@pytest.mark.parametrize("signed", [False, True])
+def test_pack_unpack_match_oracle(bits, signed):
+    rng = np.random.default_rng(bits * 2 + signed)
+    for rows, length in ((37, 101), (1, 1), (3, 32 // bits), (5, 32 // bits + 1), (64, 56)):
+        v = wl.uniform(rng, (rows, length), bits, signed)
+        want, bad = ref.pack(v, bits, signed)
+        got = samd.pack(gpu_vals(v, signed), bits, signed)
+        np.testing.assert_array_equal(host_words(got), want)
+        back = samd.unpack(got, length, bits, signed).cpu().numpy().astype(np.int32)
+        np.testing.assert_array_equal(back, v)
+
+
+@pytest.mark.parametrize("bits", [1, 3, 7])
+def test_pack_counts_out_of_range(bits):
+    v = np.array([[0, (1 << bits), 255, 1, (1 << bits) - 1]], dtype=np.int32)
+    want, bad = ref.pack(v, bits, False)
+    oor = torch.zeros(1, dtype=torch.int32, device=DEV)
+    got = samd.pack(gpu_vals(v, False), bits, False, oor)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(host_words(got), want)
+    assert int(oor.item()) == bad == 2
+
+
+# --- 1-D convolution (workload 2) ------------------------------------------------------
+
+@pytest.mark.parametrize("bits", range(1, 9))
+@pytest.mark.parametrize("K", [3, 5])
+def test_conv1d_full_size(bits, K):
+    case = wl.conv1d_case(bits, K)
+    want = ref.conv1d(case.x, case.k)
+    words, _ = ref.pack(case.x, bits, False)
+    y = samd.conv1d(gpu_words(words), case.x.size, bits, case.k.tolist(), bits)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(y.cpu().numpy(), want)
+
+
+@pytest.mark.parametrize("bits", [1, 2, 5, 8])
+def test_conv1d_ragged_and_degenerate(bits):
+    rng = np.random.default_rng(bits)
+    for n, K in ((1, 1), (3, 3), (4, 3), (5, 5), (33, 3), (97, 5), (1000, 7), (257, 16), (65, 1)):
+        x = wl.uniform(rng, (n,), bits, False)
+        k = wl.uniform(rng, (K,), bits, False)
+        words, _ = ref.pack(x, bits, False)
+        y = samd.conv1d(gpu_words(words), n, bits, k.tolist(), bits)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(y.cpu().numpy(), ref.conv1d(x, k), err_msg=f"n={n} K={K}")
+    # every value at the top of the range
+    x = np.full(999, (1 << bits) - 1, np.int32)
+    k = np.full(5, (1 << bits) - 1, np.int32)
+    words, _ = ref.pack(x, bits, False)
+    y = samd.conv1d(gpu_words(words), 999, bits, k.tolist(), bits)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(y.cpu().numpy(), ref.conv1d(x, k))
+
+
+# --- 2-D convolution: workloads 1, 3, 4 at full size -----------------------------------
+
+def conv2d_full(cfg, bits):
+    case = wl.conv2d_case(cfg, bits)
+    xf, wf = samd.Fmt(bits, case.x_signed), samd.Fmt(bits, case.w_signed)
+    want = ref.conv2d(case.x, case.w, case.shape.as_tuple())
+    return case, xf, wf, want
+
+
+@pytest.mark.parametrize("bits", range(1, 9))
+def test_conv2d_single_layer(bits):
+    case, xf, wf, want = conv2d_full(1, bits)
+    np.testing.assert_array_equal(run_conv2d(case.x, case.w, case.shape, xf, wf), want)
+
+
+@pytest.mark.parametrize("bits", range(1, 9))
+def test_conv2d_mid_layer_full(bits):
+    case, xf, wf, want = conv2d_full(3, bits)
+    np.testing.assert_array_equal(run_conv2d(case.x, case.w, case.shape, xf, wf), want)
+
+
+@pytest.mark.parametrize("bits", range(2, 9))
+def test_conv2d_mixed_sign_stress_full(bits):
+    case, xf, wf, want = conv2d_full(4, bits)
+    np.testing.assert_array_equal(run_conv2d(case.x, case.w, case.shape, xf, wf), want)
+
+
+EDGE = [
+    wl.Conv2dShape(1, 1, 1, 1, 1, 1, 1),                      # a single MAC
+    wl.Conv2dShape(1, 1, 1, 7, 1, 1, 3, 1, 1, 0, 1),          # H = 1
+    wl.Conv2dShape(2, 3, 5, 61, 17, 3, 3, 1, 1, 1, 1),        # W not a multiple of any lane count, M = 17
+    wl.Conv2dShape(1, 9, 13, 13, 33, 3, 3, 1, 1, 0, 0),       # no padding
+    wl.Conv2dShape(1, 4, 12, 12, 16, 5, 5, 1, 1, 2, 2),       # 5x5, pad 2
+    wl.Conv2dShape(2, 3, 45, 47, 20, 11, 11, 4, 4, 2, 2),     # 11x11 stride 4
+    wl.Conv2dShape(1, 5, 17, 19, 8, 3, 3, 2, 2, 1, 1),        # stride 2
+    wl.Conv2dShape(1, 2, 9, 30, 4, 3, 5, 1, 2, 1, 2),         # asymmetric kernel and stride
+    wl.Conv2dShape(1, 300, 6, 6, 70, 3, 3, 1, 1, 1, 1),       # many channels, several decodes
+    wl.Conv2dShape(3, 16, 8, 120, 48, 1, 1, 1, 1, 0, 0),      # 1x1, the vector-scale case
+    wl.Conv2dShape(1, 8, 130, 9, 16, 3, 3, 1, 1, 1, 1),       # tall image, many row blocks
+]
+
+
+@pytest.mark.parametrize("shape", EDGE, ids=lambda s: "x".join(map(str, s.as_tuple())))
+@pytest.mark.parametrize("bx,sx,bw,sw", [(1, 0, 1, 1), (2, 1, 2, 1), (3, 0, 5, 1), (4, 0, 4, 1), (6, 1, 2, 0),
+                                         (8, 0, 8, 1), (7, 1, 7, 1), (1, 1, 8, 1), (5, 0, 3, 0)])
+def test_conv2d_edge_shapes(shape, bx, sx, bw, sw):
+    xf, wf = samd.Fmt(bx, sx), samd.Fmt(bw, sw)
+    try:
+        samd.conv2d_plan(shape, xf, wf)
+    except samd.SamdError as e:
+        assert e.status in (samd.SAMD_EOVERFLOW, samd.SAMD_EUNSUPPORTED)
+        pytest.skip(f"rejected on the host: {e}")
+    rng = np.random.default_rng(sum(shape.as_tuple()) + bx * 100 + bw)
+    for gen in (wl.uniform, wl.half_extremes):
+        x = gen(rng, (shape.N, shape.C, shape.H, shape.W), bx, bool(sx))
+        w = gen(rng, (shape.M, shape.C, shape.KH, shape.KW), bw, bool(sw))
+        np.testing.assert_array_equal(run_conv2d(x, w, shape, xf, wf), ref.conv2d(x, w, shape.as_tuple()))
+    # every product at the negative extreme: the largest borrow chains
+    lo_x, hi_x = wl.value_range(bx, bool(sx))
+    lo_w, hi_w = wl.value_range(bw, bool(sw))
+    x = np.full((shape.N, shape.C, shape.H, shape.W), hi_x if lo_x == 0 else lo_x, np.int32)
+    w = np.full((shape.M, shape.C, shape.KH, shape.KW), lo_w if lo_x == 0 else hi_w, np.int32)
+    np.testing.assert_array_equal(run_conv2d(x, w, shape, xf, wf), ref.conv2d(x, w, shape.as_tuple()))
+
+
+def test_conv2d_rejects_and_leaves_output_untouched():
+    shape = wl.Conv2dShape(1, 512, 16, 16, 1, 16, 16, 1, 1, 0, 0)
+    x = torch.zeros(512 * 16 * 2, dtype=torch.int32, device=DEV)
+    w = torch.zeros(512 * 16 * 4, dtype=torch.int32, device=DEV)
+    out = torch.full((1, 1, 1, 1), 7, dtype=torch.int32, device=DEV)
+    with pytest.raises(samd.SamdError) as e:
+        samd.conv2d(x, samd.Fmt(8, 0), w, samd.Fmt(8, 1), shape, ws=torch.zeros(1 << 20, dtype=torch.uint8,
+                                                                                   device=DEV), out=out)
+    assert e.value.status == samd.SAMD_EOVERFLOW
+    assert int(out.item()) == 7
+
+
+# --- the native 8-bit baseline -----------------------------------------------------------
+
+@pytest.mark.parametrize("cfg,bits", [(1, 4), (3, 1), (3, 4), (3, 8), (4, 2), (4, 8)])
+def test_conv2d_int8_baseline_full(cfg, bits):
+    case, xf, wf, want = conv2d_full(cfg, bits)
+    np.testing.assert_array_equal(run_conv2d_int8(case.x, case.w, case.shape, xf, wf), want)
+
+
+@pytest.mark.parametrize("shape", [EDGE[2], EDGE[4], EDGE[5], EDGE[8], wl.Conv2dShape(1, 3, 224, 224, 96, 11, 11, 4, 4, 2, 2)],
+                         ids=["W61", "5x5", "11x11s4", "C300", "alex1"])
+@pytest.mark.parametrize("bx,sx", [(8, 0), (8, 1), (4, 0)])
+def test_conv2d_int8_baseline_edges(shape, bx, sx):
+    rng = np.random.default_rng(bx + sx)
+    x = wl.half_extremes(rng, (shape.N, shape.C, shape.H, shape.W), bx, bool(sx))
+    w = wl.half_extremes(rng, (shape.M, shape.C, shape.KH, shape.KW), 8, True)
+    got = run_conv2d_int8(x, w, shape, samd.Fmt(bx, sx), samd.Fmt(8, 1))
+    np.testing.assert_array_equal(got, ref.conv2d(x, w, shape.as_tuple()))
+
+
+# --- requantisation and the AlexNet-shaped stack (workload 5) ---------------------------
+
+@pytest.mark.parametrize("bits", [1, 2, 4, 8])
+def test_max_and_relu_requant(bits):
+    rng = np.random.default_rng(bits)
+    for scale in (0, 3, 1000, 1 << 26):
+        acc = rng.integers(-scale - 1, scale + 1, (3, 5, 7, 29)).astype(np.int32)
+        a = torch.from_numpy(acc).to(DEV)
+        mx = samd.max_i32(a)
+        shift = torch.zeros(1, dtype=torch.int32, device=DEV)
+        packed = samd.relu_requant_pack(a, mx, bits, shift_out=shift)
+        nhwc = samd.relu_requant_nhwc_u8(a, mx, bits)
+        torch.cuda.synchronize()
+        assert int(mx.item()) == int(acc.max())
+        s = ref.requant_shift(acc.astype(np.int64), bits)
+        assert int(shift.item()) == s
+        q = ref.relu_requant(acc.astype(np.int64), s, bits)
+        want, _ = ref.pack(q.reshape(-1, 29), bits, False)
+        np.testing.assert_array_equal(host_words(packed).reshape(-1, want.shape[-1]), want)
+        np.testing.assert_array_equal(nhwc.cpu().numpy(), np.transpose(q, (0, 2, 3, 1)))
+
+
+def run_stack_samd(case):
+    bits = case.bits
+    x = samd.pack(gpu_vals(case.x, False), bits, False)
+    accs, acts = [], []
+    for li, (w, shp) in enumerate(zip(case.ws, case.layers)):
+        wp = samd.pack(gpu_vals(w, True), bits, True)
+        y = samd.conv2d(x, samd.Fmt(bits, False), wp, samd.Fmt(bits, True), shp)
+        accs.append(y)
+        if li + 1 < len(case.ws):
+            x = samd.relu_requant_pack(y, samd.max_i32(y), bits)
+            acts.append(x)
+    torch.cuda.synchronize()
+    return [a.cpu().numpy() for a in accs], acts
+
+
+def run_stack_int8(case):
+    bits = case.bits
+    x = gpu_vals(np.transpose(case.x, (0, 2, 3, 1)), False)
+    accs = []
+    for li, (w, shp) in enumerate(zip(case.ws, case.layers)):
+        y = samd.conv2d_int8(x, samd.Fmt(bits, False), gpu_vals(w, True), samd.Fmt(bits, True), shp)
+        accs.append(y)
+        if li + 1 < len(case.ws):
+            x = samd.relu_requant_nhwc_u8(y, samd.max_i32(y), bits)
+    torch.cuda.synchronize()
+    return [a.cpu().numpy() for a in accs]
+
+
+@pytest.mark.parametrize("bits", [2, 4, 8])
+def test_alexnet_stack_batch2(bits):
+    case = wl.stack_case(bits, batch=2)
+    want_accs, want_acts, _ = ref.stack(case.x, case.ws, [l.as_tuple() for l in case.layers], bits)
+    got_accs, got_acts = run_stack_samd(case)
+    for li, (g, w) in enumerate(zip(got_accs, want_accs)):
+        np.testing.assert_array_equal(g, w, err_msg=f"SAMD layer {li + 1}")
+    for li, (g, w) in enumerate(zip(got_acts, want_acts[1:])):
+        packed, _ = ref.pack(w, bits, False)
+        np.testing.assert_array_equal(host_words(g), packed, err_msg=f"activation after layer {li + 1}")
+    for li, (g, w) in enumerate(zip(run_stack_int8(case), want_accs)):
+        np.testing.assert_array_equal(g, w, err_msg=f"int8 layer {li + 1}")
+
+
+@pytest.mark.parametrize("bits", [2, 4, 8])
+def test_alexnet_stack_full_batch(bits):
+    case = wl.stack_case(bits)
+    want_accs, _, _ = ref.stack(case.x, case.ws, [l.as_tuple() for l in case.layers], bits)
+    got_accs, _ = run_stack_samd(case)
+    for li, (g, w) in enumerate(zip(got_accs, want_accs)):
+        np.testing.assert_array_equal(g, w, err_msg=f"SAMD layer {li + 1}")
