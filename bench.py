@@ -1,0 +1,184 @@
+#!/usr/bin/env python3
+"""Benchmark of the SAMD b-bit quantized conv2d on one MI355X.
+
+Workload: conv2d 8 x 128 x 56 x 56 -> 128 channels, 3x3, stride 1, pad 1, unsigned b-bit
+activations x signed b-bit weights (seeded synthetic values), swept over b = 1..8.
+
+One step = one pass of the whole hot path at every bit width: pack the int8/uint8
+activations into b-bit words, prepare the layer's kernel words, run the SAMD
+convolution.  `value` is the whole sweep's throughput (all MACs of the 8 layers / time
+of the step) in GMAC/s.  Per bit width the line also reports the convolution kernel's
+own rate (HIP events around it), the native-int8 matrix-core baseline on the same
+layer, their speedup, and the roofline fractions; the CPU oracle is timed on the host.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--bits 1,2,...]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+PEAK_VALU_OPS = 256 * 64 * 2.4e9      # int32 VALU lane-ops/s: 256 CUs x 64 lanes x 2.4 GHz
+PEAK_HBM = 8.0e12                     # bytes/s
+PEAK_I8_MACS = 2.5e15                 # dense int8 matrix-core MAC/s (5.0 POP/s)
+
+
+def parse():
+    p = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=100)
+    p.add_argument("--warmup", type=int, default=10)
+    p.add_argument("--bits", default="1,2,3,4,5,6,7,8")
+    p.add_argument("--cpu-seconds", type=float, default=10.0, help="CPU oracle sample budget")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-check", action="store_true", help="skip the sampled parity check")
+    return p.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print("bench.py measures one GPU: this build runs on a single MI355X and has no multi-GPU path "
+              "(--gpus must be 1)", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    import paper_1809_10572_amd as samd
+    import samd_workloads as wl
+
+    bits_list = [int(b) for b in args.bits.split(",")]
+    dev = torch.device("cuda:0")
+    shape = wl.MID
+    N, C, H, W, M, KH, KW = shape.N, shape.C, shape.H, shape.W, shape.M, shape.KH, shape.KW
+    Ho, Wo = samd.out_hw(shape)
+    macs = N * M * Ho * Wo * C * KH * KW
+
+    layers = []
+    for b in bits_list:
+        case = wl.conv2d_case(3, b)
+        xf, wf = samd.Fmt(b, case.x_signed), samd.Fmt(b, case.w_signed)
+        x = torch.from_numpy(case.x.astype(np.uint8)).to(dev)
+        x_nhwc = torch.from_numpy(np.ascontiguousarray(np.transpose(case.x, (0, 2, 3, 1))).astype(np.uint8)).to(dev)
+        w8 = torch.from_numpy(case.w.astype(np.int8)).to(dev)
+        wp = samd.pack(w8, b, True)
+        xp = torch.empty((N, C, H, samd.row_words(W, b)), dtype=torch.int32, device=dev)
+        ws = torch.empty(max(samd.conv2d_workspace(shape, xf, wf), 256), dtype=torch.uint8, device=dev)
+        ws8 = samd.conv2d_int8_prepare(w8, wf, shape, xf)
+        plan = samd.conv2d_plan(shape, xf, wf)
+        layers.append(dict(b=b, case=case, xf=xf, wf=wf, x=x, x_nhwc=x_nhwc, wp=wp, xp=xp, ws=ws, ws8=ws8, plan=plan,
+                           y=torch.empty((N, M, Ho, Wo), dtype=torch.int32, device=dev),
+                           y8=torch.empty((N, M, Ho, Wo), dtype=torch.int32, device=dev), ev=[]))
+    torch.cuda.synchronize()
+
+    def step(record: bool):
+        for L in layers:
+            samd.pack(L["x"], L["b"], False, out=L["xp"])
+            samd.conv2d_prepare(L["wp"], L["wf"], shape, L["xf"], ws=L["ws"])
+            if record:
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record()
+            samd.conv2d_prepared(L["xp"], L["xf"], L["wf"], shape, L["ws"], out=L["y"])
+            if record:
+                e1.record()
+                L["ev"].append((e0, e1))
+
+    for _ in range(args.warmup):
+        step(False)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step(True)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+
+    # native 8-bit baseline on the same layers, timed the same way
+    for L in layers:
+        for _ in range(args.warmup):
+            samd.conv2d_int8_prepared(L["x_nhwc"], L["xf"], L["wf"], shape, L["ws8"], out=L["y8"])
+        evs = []
+        for _ in range(args.steps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            samd.conv2d_int8_prepared(L["x_nhwc"], L["xf"], L["wf"], shape, L["ws8"], out=L["y8"])
+            e1.record()
+            evs.append((e0, e1))
+        L["ev8"] = evs
+    torch.cuda.synchronize()
+
+    # sampled parity against the oracle, same inputs, both paths
+    parity = {}
+    if not args.no_check:
+        from oracle import reference as ref
+        rng = np.random.default_rng(0)
+        idx = np.stack([rng.integers(0, s, 256) for s in (N, M, Ho, Wo)], axis=1)
+        for L in layers:
+            want = ref.conv2d_points(L["case"].x, L["case"].w, shape.as_tuple(), idx)
+            got = L["y"].cpu().numpy()[tuple(idx.T)]
+            got8 = L["y8"].cpu().numpy()[tuple(idx.T)]
+            parity[L["b"]] = bool(np.array_equal(got, want) and np.array_equal(got8, want))
+
+    per_bits, tot_mads, tot_conv_s = {}, 0.0, 0.0
+    for L in layers:
+        t = sum(a.elapsed_time(b) for a, b in L["ev"]) / len(L["ev"]) * 1e-3
+        t8 = sum(a.elapsed_time(b) for a, b in L["ev8"]) / len(L["ev8"]) * 1e-3
+        p = L["plan"]
+        mads = N * M * Ho * p.words_per_row * C * KH * p.tap_words
+        b = L["b"]
+        hbm_bytes = N * C * H * samd.row_words(W, b) * 4 + M * C * KH * samd.row_words(KW, b) * 4 + N * M * Ho * Wo * 4
+        tot_mads += mads
+        tot_conv_s += t
+        per_bits[str(b)] = {
+            "conv_us": round(t * 1e6, 2), "gmacs": round(macs / t / 1e9, 1),
+            "int8_us": round(t8 * 1e6, 2), "int8_gmacs": round(macs / t8 / 1e9, 1),
+            "speedup_vs_int8": round(t8 / t, 3),
+            "valu_frac": round(mads / t / PEAK_VALU_OPS, 4),
+            "hbm_frac": round(hbm_bytes / t / PEAK_HBM, 4),
+            "int8_mfma_frac": round(macs / t8 / PEAK_I8_MACS, 4),
+            "lane_bits": p.lane_bits, "lanes": p.lanes, "tap_words": p.tap_words,
+            "flush_channels": p.flush_channels, "macs_per_mad": round(p.macs_per_mad, 2),
+            "parity": parity.get(b),
+        }
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        from oracle import reference as ref
+        done, spent, sample = 0, 0.0, []
+        for L in layers:
+            if spent >= args.cpu_seconds:
+                break
+            c0 = time.perf_counter()
+            ref.conv2d(L["case"].x, L["case"].w, shape.as_tuple())
+            spent += time.perf_counter() - c0
+            done += macs
+            sample.append(L["b"])
+        cpu = {"value": round(done / spent / 1e9, 2), "unit": "GMAC/s", "cores": ref.threads(), "kind": "oracle",
+               "sample": f"int64 direct conv2d of the same layer at b={sample} ({len(sample)} layers, "
+                         f"{done / 1e9:.1f} GMAC, {spent:.1f} s)"}
+
+    achieved = tot_mads / tot_conv_s
+    line = {
+        "metric": "b-bit quantized conv2d GMAC/s (b=1..8) vs native-int8; % of VALU-int peak",
+        "value": round(macs * len(layers) / (ms_per_step * 1e-3) / 1e9, 1),
+        "unit": "GMAC/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "int64", "data": "synthetic",
+        "config": {"workload": "conv2d 8x128x56x56 -> 128, 3x3, stride 1, pad 1; unsigned b-bit activations x "
+                               "signed b-bit weights; one step = pack + prepare + SAMD conv at each b",
+                   "bits": bits_list, "global_batch": N, "macs_per_layer": macs},
+        "roofline": {"bound": "alu", "achieved": round(achieved / 1e12, 3), "peak": round(PEAK_VALU_OPS / 1e12, 2),
+                     "unit": "TOP/s", "frac": round(achieved / PEAK_VALU_OPS, 4), "traffic": None,
+                     "kernel": "conv2d_samd_kernel", "op": "32x32->64-bit multiply-accumulate (v_mad_i64_i32)"},
+        "cpu_baseline": cpu,
+        "per_bits": per_bits,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

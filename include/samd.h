@@ -152,6 +152,16 @@ int samd_conv2d(const uint32_t *x, samd_fmt xf, const uint32_t *w, samd_fmt wf,
                 const samd_conv2d_desc *d, int32_t *y, void *ws, size_t ws_bytes,
                 hipStream_t stream);
 
+/* samd_conv2d split in its two steps, for callers that reuse one layer's weights:
+ * samd_conv2d_prepare writes the layer's kernel words into ws (each kernel row reversed
+ * and sign-extended into 32-bit words, Sec. 6); samd_conv2d_prepared then convolves any
+ * number of inputs with them.  Both take the same formats, descriptor and workspace as
+ * samd_conv2d; the prepared workspace is valid for exactly that (xf, wf, *d). */
+int samd_conv2d_prepare(const uint32_t *w, samd_fmt wf, const samd_conv2d_desc *d, samd_fmt xf, void *ws,
+                        size_t ws_bytes, hipStream_t stream);
+int samd_conv2d_prepared(const uint32_t *x, samd_fmt xf, samd_fmt wf, const samd_conv2d_desc *d, int32_t *y,
+                         const void *ws, size_t ws_bytes, hipStream_t stream);
+
 /* Workspace bytes samd_conv2d_int8 needs (reordered int8 weights and per-filter sums). */
 int samd_conv2d_int8_workspace(const samd_conv2d_desc *d, samd_fmt xf, size_t *bytes);
 
@@ -165,6 +175,12 @@ int samd_conv2d_int8_workspace(const samd_conv2d_desc *d, samd_fmt xf, size_t *b
 int samd_conv2d_int8(const void *x, samd_fmt xf, const int8_t *w, samd_fmt wf,
                      const samd_conv2d_desc *d, int32_t *y, void *ws, size_t ws_bytes,
                      hipStream_t stream);
+
+/* samd_conv2d_int8 split in weight reordering and convolution, as for samd_conv2d. */
+int samd_conv2d_int8_prepare(const int8_t *w, samd_fmt wf, const samd_conv2d_desc *d, samd_fmt xf, void *ws,
+                             size_t ws_bytes, hipStream_t stream);
+int samd_conv2d_int8_prepared(const void *x, samd_fmt xf, samd_fmt wf, const samd_conv2d_desc *d, int32_t *y,
+                              const void *ws, size_t ws_bytes, hipStream_t stream);
 
 /* Maximum of n int32 values, written to *dev_max (device); n >= 1. */
 int samd_max_i32(const int32_t *src, int64_t n, int32_t *dev_max, hipStream_t stream);

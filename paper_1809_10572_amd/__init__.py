@@ -16,7 +16,8 @@ from typing import Optional, Sequence, Tuple
 import torch
 
 __all__ = ["Fmt", "Conv2dDesc", "Conv1dPlan", "Conv2dPlan", "SamdError", "lib", "row_words", "pack", "unpack", "conv1d",
-           "conv1d_plan", "conv2d_plan", "conv2d_workspace", "conv2d", "conv2d_int8_workspace", "conv2d_int8", "max_i32",
+           "conv1d_plan", "conv2d_plan", "conv2d_workspace", "conv2d", "conv2d_prepare", "conv2d_prepared",
+           "conv2d_int8_prepare", "conv2d_int8_prepared", "conv2d_int8_workspace", "conv2d_int8", "max_i32",
            "relu_requant_pack", "relu_requant_nhwc_u8", "out_hw", "LIB_PATH"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsamd.so")
@@ -89,6 +90,11 @@ def lib():
                                                       ctypes.POINTER(Conv2dPlan)]),
             "samd_conv2d_workspace": (ctypes.c_int, [ctypes.POINTER(Conv2dDesc), Fmt, Fmt, ctypes.POINTER(_sz)]),
             "samd_conv2d": (ctypes.c_int, [_p, Fmt, _p, Fmt, ctypes.POINTER(Conv2dDesc), _p, _p, _sz, _p]),
+            "samd_conv2d_prepare": (ctypes.c_int, [_p, Fmt, ctypes.POINTER(Conv2dDesc), Fmt, _p, _sz, _p]),
+            "samd_conv2d_prepared": (ctypes.c_int, [_p, Fmt, Fmt, ctypes.POINTER(Conv2dDesc), _p, _p, _sz, _p]),
+            "samd_conv2d_int8_prepare": (ctypes.c_int, [_p, Fmt, ctypes.POINTER(Conv2dDesc), Fmt, _p, _sz, _p]),
+            "samd_conv2d_int8_prepared": (ctypes.c_int, [_p, Fmt, Fmt, ctypes.POINTER(Conv2dDesc), _p, _p, _sz,
+                                                         _p]),
             "samd_conv2d_int8_workspace": (ctypes.c_int, [ctypes.POINTER(Conv2dDesc), Fmt, ctypes.POINTER(_sz)]),
             "samd_conv2d_int8": (ctypes.c_int, [_p, Fmt, _p, Fmt, ctypes.POINTER(Conv2dDesc), _p, _p, _sz, _p]),
             "samd_max_i32": (ctypes.c_int, [_p, _i64, _p, _p]),
@@ -134,12 +140,17 @@ def row_words(length: int, bits: int) -> int:
     return int(r)
 
 
-def pack(values: torch.Tensor, bits: int, signed: bool, oor: Optional[torch.Tensor] = None) -> torch.Tensor:
+def pack(values: torch.Tensor, bits: int, signed: bool, oor: Optional[torch.Tensor] = None,
+         out: Optional[torch.Tensor] = None) -> torch.Tensor:
     """Pack the last axis of an int8 (signed) / uint8 (unsigned) GPU tensor."""
     _dev(values, torch.int8 if signed else torch.uint8, "values")
     length = values.shape[-1]
     rows = values.numel() // length if length else 0
-    out = torch.empty(values.shape[:-1] + (row_words(length, bits),), dtype=torch.int32, device=values.device)
+    shape = values.shape[:-1] + (row_words(length, bits),)
+    if out is None:
+        out = torch.empty(shape, dtype=torch.int32, device=values.device)
+    elif out.dtype != torch.int32 or tuple(out.shape) != tuple(shape) or not out.is_contiguous():
+        raise ValueError(f"out must be a contiguous int32 tensor of shape {tuple(shape)}")
     _check(lib().samd_pack(values.data_ptr(), rows, length, Fmt(bits, signed), out.data_ptr(),
                            oor.data_ptr() if oor is not None else None, _stream(values)))
     return out
@@ -205,6 +216,49 @@ def conv2d(xp: torch.Tensor, xfmt: Fmt, wp: torch.Tensor, wfmt: Fmt, shape, ws: 
         out = torch.empty((d.N, d.M, Ho, Wo), dtype=torch.int32, device=xp.device)
     _check(lib().samd_conv2d(xp.data_ptr(), xfmt, wp.data_ptr(), wfmt, ctypes.byref(d), out.data_ptr(),
                              ws.data_ptr(), ws.numel(), _stream(xp)))
+    return out
+
+
+def conv2d_prepare(wp: torch.Tensor, wfmt: Fmt, shape, xfmt: Fmt, ws: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Kernel words of one layer, for any number of conv2d_prepared calls."""
+    _dev(wp, torch.int32, "wp")
+    if ws is None:
+        ws = _workspace(conv2d_workspace(shape, xfmt, wfmt), wp.device)
+    _check(lib().samd_conv2d_prepare(wp.data_ptr(), wfmt, ctypes.byref(Conv2dDesc.of(shape)), xfmt, ws.data_ptr(),
+                                     ws.numel(), _stream(wp)))
+    return ws
+
+
+def conv2d_prepared(xp: torch.Tensor, xfmt: Fmt, wfmt: Fmt, shape, ws: torch.Tensor,
+                    out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    _dev(xp, torch.int32, "xp")
+    d = Conv2dDesc.of(shape)
+    Ho, Wo = out_hw(shape)
+    if out is None:
+        out = torch.empty((d.N, d.M, Ho, Wo), dtype=torch.int32, device=xp.device)
+    _check(lib().samd_conv2d_prepared(xp.data_ptr(), xfmt, wfmt, ctypes.byref(d), out.data_ptr(), ws.data_ptr(),
+                                      ws.numel(), _stream(xp)))
+    return out
+
+
+def conv2d_int8_prepare(w: torch.Tensor, wfmt: Fmt, shape, xfmt: Fmt, ws: Optional[torch.Tensor] = None):
+    _dev(w, torch.int8, "w")
+    if ws is None:
+        ws = _workspace(conv2d_int8_workspace(shape, xfmt), w.device)
+    _check(lib().samd_conv2d_int8_prepare(w.data_ptr(), wfmt, ctypes.byref(Conv2dDesc.of(shape)), xfmt,
+                                          ws.data_ptr(), ws.numel(), _stream(w)))
+    return ws
+
+
+def conv2d_int8_prepared(x_nhwc: torch.Tensor, xfmt: Fmt, wfmt: Fmt, shape, ws: torch.Tensor,
+                         out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    _dev(x_nhwc, (torch.int8, torch.uint8), "x_nhwc")
+    d = Conv2dDesc.of(shape)
+    Ho, Wo = out_hw(shape)
+    if out is None:
+        out = torch.empty((d.N, d.M, Ho, Wo), dtype=torch.int32, device=x_nhwc.device)
+    _check(lib().samd_conv2d_int8_prepared(x_nhwc.data_ptr(), xfmt, wfmt, ctypes.byref(d), out.data_ptr(),
+                                           ws.data_ptr(), ws.numel(), _stream(x_nhwc)))
     return out
 
 

@@ -222,25 +222,65 @@ int samd_conv2d_workspace(const samd_conv2d_desc *d, samd_fmt xf, samd_fmt wf, s
     return SAMD_OK;
 }
 
-int samd_conv2d(const uint32_t *x, samd_fmt xf, const uint32_t *w, samd_fmt wf, const samd_conv2d_desc *d,
-                int32_t *y, void *ws, size_t ws_bytes, hipStream_t stream) {
-    set_error("");
+}  // extern "C"
+
+namespace {
+
+// Validation and planning shared by the SAMD conv2d entry points.
+int conv2d_setup(samd_fmt xf, samd_fmt wf, const samd_conv2d_desc *d, const void *ws, size_t ws_bytes,
+                 Conv2dGeom &g) {
     int st = check_fmt(xf, "xf");
     if (!st) st = check_fmt(wf, "wf");
     if (!st) st = check_conv2d_desc(d);
     if (!st) st = check_overflow(d, xf, wf);
     if (st) return st;
-    if (!x || !w || !y || !ws) return fail(SAMD_EINVAL, "x, w, y and ws must not be NULL");
-    if (!aligned4(x) || !aligned4(w) || !aligned4(y)) return fail(SAMD_EALIGN, "x / w / y not aligned");
+    if (!ws) return fail(SAMD_EINVAL, "ws must not be NULL");
     if (((uintptr_t)ws & 255) != 0) return fail(SAMD_EALIGN, "workspace not 256-byte aligned");
-    Conv2dGeom g;
     std::string err;
     st = plan_conv2d(*d, xf, wf, g, err);
     if (st) return fail(st, "%s", err.c_str());
     size_t need = conv2d_workspace_bytes(g);
-    if (ws_bytes < need)
-        return fail(SAMD_ENOSPC, "workspace %zu bytes < %zu needed", ws_bytes, need);
-    return launch_conv2d_samd(x, w, g, y, ws, stream);
+    if (ws_bytes < need) return fail(SAMD_ENOSPC, "workspace %zu bytes < %zu needed", ws_bytes, need);
+    return SAMD_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int samd_conv2d_prepare(const uint32_t *w, samd_fmt wf, const samd_conv2d_desc *d, samd_fmt xf, void *ws,
+                        size_t ws_bytes, hipStream_t stream) {
+    set_error("");
+    Conv2dGeom g;
+    int st = conv2d_setup(xf, wf, d, ws, ws_bytes, g);
+    if (st) return st;
+    if (!w) return fail(SAMD_EINVAL, "w must not be NULL");
+    if (!aligned4(w)) return fail(SAMD_EALIGN, "w not aligned");
+    return launch_conv2d_prepare(w, g, ws, stream);
+}
+
+int samd_conv2d_prepared(const uint32_t *x, samd_fmt xf, samd_fmt wf, const samd_conv2d_desc *d, int32_t *y,
+                         const void *ws, size_t ws_bytes, hipStream_t stream) {
+    set_error("");
+    Conv2dGeom g;
+    int st = conv2d_setup(xf, wf, d, ws, ws_bytes, g);
+    if (st) return st;
+    if (!x || !y) return fail(SAMD_EINVAL, "x and y must not be NULL");
+    if (!aligned4(x) || !aligned4(y)) return fail(SAMD_EALIGN, "x / y not aligned");
+    return launch_conv2d_samd(x, g, y, ws, stream);
+}
+
+int samd_conv2d(const uint32_t *x, samd_fmt xf, const uint32_t *w, samd_fmt wf, const samd_conv2d_desc *d,
+                int32_t *y, void *ws, size_t ws_bytes, hipStream_t stream) {
+    set_error("");
+    Conv2dGeom g;
+    int st = conv2d_setup(xf, wf, d, ws, ws_bytes, g);
+    if (st) return st;
+    if (!x || !w || !y) return fail(SAMD_EINVAL, "x, w and y must not be NULL");
+    if (!aligned4(x) || !aligned4(w) || !aligned4(y)) return fail(SAMD_EALIGN, "x / w / y not aligned");
+    st = launch_conv2d_prepare(w, g, ws, stream);
+    if (st) return st;
+    return launch_conv2d_samd(x, g, y, ws, stream);
 }
 
 namespace {
@@ -267,19 +307,55 @@ int samd_conv2d_int8_workspace(const samd_conv2d_desc *d, samd_fmt xf, size_t *b
     return SAMD_OK;
 }
 
-int samd_conv2d_int8(const void *x, samd_fmt xf, const int8_t *w, samd_fmt wf, const samd_conv2d_desc *d,
-                     int32_t *y, void *ws, size_t ws_bytes, hipStream_t stream) {
-    set_error("");
+}  // extern "C"
+
+namespace {
+
+int int8_setup(samd_fmt xf, samd_fmt wf, const samd_conv2d_desc *d, const void *ws, size_t ws_bytes) {
     int st = check_int8_formats(xf, wf);
     if (!st) st = check_conv2d_desc(d);
     if (!st) st = check_overflow(d, xf, wf);
     if (st) return st;
-    if (!x || !w || !y || !ws) return fail(SAMD_EINVAL, "x, w, y and ws must not be NULL");
-    if (!aligned4(y)) return fail(SAMD_EALIGN, "y not aligned");
+    if (!ws) return fail(SAMD_EINVAL, "ws must not be NULL");
     if (((uintptr_t)ws & 255) != 0) return fail(SAMD_EALIGN, "workspace not 256-byte aligned");
     size_t need = conv2d_i8_workspace_bytes(*d, xf);
     if (ws_bytes < need) return fail(SAMD_ENOSPC, "workspace %zu bytes < %zu needed", ws_bytes, need);
-    return launch_conv2d_i8(x, xf, w, *d, y, ws, stream);
+    return SAMD_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int samd_conv2d_int8_prepare(const int8_t *w, samd_fmt wf, const samd_conv2d_desc *d, samd_fmt xf, void *ws,
+                             size_t ws_bytes, hipStream_t stream) {
+    set_error("");
+    int st = int8_setup(xf, wf, d, ws, ws_bytes);
+    if (st) return st;
+    if (!w) return fail(SAMD_EINVAL, "w must not be NULL");
+    return launch_conv2d_i8_prepare(w, xf, *d, ws, stream);
+}
+
+int samd_conv2d_int8_prepared(const void *x, samd_fmt xf, samd_fmt wf, const samd_conv2d_desc *d, int32_t *y,
+                              const void *ws, size_t ws_bytes, hipStream_t stream) {
+    set_error("");
+    int st = int8_setup(xf, wf, d, ws, ws_bytes);
+    if (st) return st;
+    if (!x || !y) return fail(SAMD_EINVAL, "x and y must not be NULL");
+    if (!aligned4(y)) return fail(SAMD_EALIGN, "y not aligned");
+    return launch_conv2d_i8(x, xf, *d, y, ws, stream);
+}
+
+int samd_conv2d_int8(const void *x, samd_fmt xf, const int8_t *w, samd_fmt wf, const samd_conv2d_desc *d,
+                     int32_t *y, void *ws, size_t ws_bytes, hipStream_t stream) {
+    set_error("");
+    int st = int8_setup(xf, wf, d, ws, ws_bytes);
+    if (st) return st;
+    if (!x || !w || !y) return fail(SAMD_EINVAL, "x, w and y must not be NULL");
+    if (!aligned4(y)) return fail(SAMD_EALIGN, "y not aligned");
+    st = launch_conv2d_i8_prepare(w, xf, *d, ws, stream);
+    if (st) return st;
+    return launch_conv2d_i8(x, xf, *d, y, ws, stream);
 }
 
 int samd_max_i32(const int32_t *src, int64_t n, int32_t *dev_max, hipStream_t stream) {

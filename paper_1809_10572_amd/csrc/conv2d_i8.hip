@@ -192,23 +192,43 @@ size_t conv2d_i8_workspace_bytes(const samd_conv2d_desc &d, samd_fmt xf) {
     return wr + sums + tot;
 }
 
-int launch_conv2d_i8(const void *x, samd_fmt xf, const int8_t *w, const samd_conv2d_desc &d, int32_t *y, void *ws,
-                     hipStream_t s) {
-    I8Geom g = make_geom(d, xf);
-    int8_t *wr = (int8_t *)ws;
-    int32_t *wsum = (int32_t *)((char *)ws + align256((size_t)g.Mp * g.KH * g.KW * g.Cp));
-    int32_t *wtot = (int32_t *)((char *)wsum + align256((size_t)g.M * g.KH * g.KW * 4));
+namespace {
+
+struct I8Workspace {
+    int8_t *wr;
+    int32_t *wsum, *wtot;
+};
+
+I8Workspace carve(const I8Geom &g, void *ws) {
+    I8Workspace w;
+    w.wr = (int8_t *)ws;
+    w.wsum = (int32_t *)((char *)ws + align256((size_t)g.Mp * g.KH * g.KW * g.Cp));
+    w.wtot = (int32_t *)((char *)w.wsum + align256((size_t)g.M * g.KH * g.KW * 4));
+    return w;
+}
+
+}  // namespace
+
+int launch_conv2d_i8_prepare(const int8_t *w, samd_fmt xf, const samd_conv2d_desc &d, void *ws, hipStream_t s) {
+    const I8Geom g = make_geom(d, xf);
+    const I8Workspace p = carve(g, ws);
     const int pgrid = grid_for((int64_t)g.Mp * g.KH * g.KW * g.Cp, 256);
-    hipLaunchKernelGGL(i8_prep_kernel, dim3(pgrid), dim3(256), 0, s, w, g, wr, wsum, wtot);
-    int st = check_launch("conv2d_int8 weight reorder");
-    if (st) return st;
+    hipLaunchKernelGGL(i8_prep_kernel, dim3(pgrid), dim3(256), 0, s, w, g, p.wr, p.wsum, p.wtot);
+    return check_launch("conv2d_int8 weight reorder");
+}
+
+int launch_conv2d_i8(const void *x, samd_fmt xf, const samd_conv2d_desc &d, int32_t *y, const void *ws,
+                     hipStream_t s) {
+    const I8Geom g = make_geom(d, xf);
+    const I8Workspace p = carve(g, const_cast<void *>(ws));
     const dim3 grid((unsigned)((g.P + 63) / 64), g.Mp / 64);
     const bool vec = (g.C % 16) == 0 && ((uintptr_t)x % 16) == 0;
     if (vec)
-        hipLaunchKernelGGL((conv2d_i8_kernel<true>), grid, dim3(256), 0, s, (const uint8_t *)x, wr, wsum, wtot, y, g);
+        hipLaunchKernelGGL((conv2d_i8_kernel<true>), grid, dim3(256), 0, s, (const uint8_t *)x, p.wr, p.wsum,
+                           p.wtot, y, g);
     else
-        hipLaunchKernelGGL((conv2d_i8_kernel<false>), grid, dim3(256), 0, s, (const uint8_t *)x, wr, wsum, wtot, y,
-                           g);
+        hipLaunchKernelGGL((conv2d_i8_kernel<false>), grid, dim3(256), 0, s, (const uint8_t *)x, p.wr, p.wsum,
+                           p.wtot, y, g);
     return check_launch("conv2d_int8");
 }
 

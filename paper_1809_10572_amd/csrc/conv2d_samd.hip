@@ -187,8 +187,7 @@ __global__ __launch_bounds__(256) void conv2d_samd_kernel(const uint32_t *__rest
 
 }  // namespace
 
-int launch_conv2d_samd(const uint32_t *x, const uint32_t *w, const Conv2dGeom &g, int32_t *y, void *ws,
-                       hipStream_t s) {
+int launch_conv2d_prepare(const uint32_t *w, const Conv2dGeom &g, void *ws, hipStream_t s) {
     int32_t *kw = (int32_t *)ws;
     const int64_t nkw = (int64_t)g.nmb * g.C * g.nrt * g.mblk;
     const int pgrid = grid_for(nkw, 256);
@@ -200,11 +199,14 @@ int launch_conv2d_samd(const uint32_t *x, const uint32_t *w, const Conv2dGeom &g
     }
     SAMD_FOR_EACH_FMT(SAMD_PREP_CASE)
 #undef SAMD_PREP_CASE
-    int st = check_launch("conv2d weight preparation");
-    if (st) return st;
+    return check_launch("conv2d weight preparation");
+}
+
+int launch_conv2d_samd(const uint32_t *x, const Conv2dGeom &g, int32_t *y, const void *ws, hipStream_t s) {
+    const int32_t *kw = (const int32_t *)ws;
     const dim3 grid((g.Ho + g.rows_blk - 1) / g.rows_blk, g.nmb, g.N);
     const size_t shm = (size_t)(g.lds_tile + g.lds_spread + g.lds_raw) * 4;
-    launched = false;
+    bool launched = false;
 #define SAMD_CONV_CASE(B, SG)                                                                               \
     if (!launched && g.xbits == B && (bool)g.xsigned == SG) {                                               \
         hipLaunchKernelGGL((conv2d_samd_kernel<B, SG>), grid, dim3(g.wm * 64), shm, s, x, kw, y, g);        \

@@ -74,10 +74,11 @@ int launch_pack(const void *src, int64_t rows, int64_t len, int bits, int is_sig
 int launch_unpack(const uint32_t *src, int64_t rows, int64_t len, int bits, int is_signed, void *dst,
                   hipStream_t s);
 int launch_conv1d(const uint32_t *x, const Conv1dGeom &g, int32_t *y, hipStream_t s);
-int launch_conv2d_samd(const uint32_t *x, const uint32_t *w, const Conv2dGeom &g, int32_t *y, void *ws,
-                       hipStream_t s);
+int launch_conv2d_prepare(const uint32_t *w, const Conv2dGeom &g, void *ws, hipStream_t s);
+int launch_conv2d_samd(const uint32_t *x, const Conv2dGeom &g, int32_t *y, const void *ws, hipStream_t s);
 size_t conv2d_i8_workspace_bytes(const samd_conv2d_desc &d, samd_fmt xf);
-int launch_conv2d_i8(const void *x, samd_fmt xf, const int8_t *w, const samd_conv2d_desc &d, int32_t *y, void *ws,
+int launch_conv2d_i8_prepare(const int8_t *w, samd_fmt xf, const samd_conv2d_desc &d, void *ws, hipStream_t s);
+int launch_conv2d_i8(const void *x, samd_fmt xf, const samd_conv2d_desc &d, int32_t *y, const void *ws,
                      hipStream_t s);
 int launch_max_i32(const int32_t *src, int64_t n, int32_t *dev_max, hipStream_t s);
 int launch_relu_requant_pack(const int32_t *acc, int64_t rows, int64_t len, const int32_t *dev_max, int bits,

@@ -269,3 +269,22 @@ def test_alexnet_stack_full_batch(bits):
     got_accs, _ = run_stack_samd(case)
     for li, (g, w) in enumerate(zip(got_accs, want_accs)):
         np.testing.assert_array_equal(g, w, err_msg=f"SAMD layer {li + 1}")
+
+
+@pytest.mark.parametrize("bits", [1, 4, 8])
+def test_prepared_weights_are_reusable(bits):
+    shape = EDGE[2]
+    xf, wf = samd.Fmt(bits, False), samd.Fmt(bits, True)
+    rng = np.random.default_rng(40 + bits)
+    w = wl.uniform(rng, (shape.M, shape.C, shape.KH, shape.KW), bits, True)
+    wp = samd.pack(gpu_vals(w, True), bits, True)
+    ws = samd.conv2d_prepare(wp, wf, shape, xf)
+    ws8 = samd.conv2d_int8_prepare(gpu_vals(w, True), wf, shape, xf)
+    for _ in range(2):
+        x = wl.uniform(rng, (shape.N, shape.C, shape.H, shape.W), bits, False)
+        want = ref.conv2d(x, w, shape.as_tuple())
+        y = samd.conv2d_prepared(samd.pack(gpu_vals(x, False), bits, False), xf, wf, shape, ws)
+        y8 = samd.conv2d_int8_prepared(gpu_vals(np.transpose(x, (0, 2, 3, 1)), False), xf, wf, shape, ws8)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(y.cpu().numpy(), want)
+        np.testing.assert_array_equal(y8.cpu().numpy(), want)
