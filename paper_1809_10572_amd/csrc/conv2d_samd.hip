@@ -1,21 +1,20 @@
 // SAMD 2-D convolution for gfx950: convolution by long multiplication (Sec. 5) with
 // signed sign-extension and the underflow fix-up (Sec. 6).
 //
-// Workgroup = one image n, rows_blk output rows, mblk output channels; each of its wm
-// waves owns kWaveM output channels, each lane one operand-word column q of one output
-// row.  Per channel chunk the workgroup
-//   1. copies the packed input rows it needs into LDS (coalesced),
-//   2. spreads them into operand words: I values of one stride phase, L bits apart
-//      (temporary spacer bits), negative values sign-extended - every operand word is
-//      then the int32 sum_i v_i 2^(i L),
-//   3. multiplies every operand word by the kernel words of its kernel rows and adds the
-//      exact signed 32x32 -> 64-bit products into one accumulator per output channel
-//      (v_mad_i64_i32; the kernel words are wave-uniform and come in through SGPRs).
-// After every G channels each accumulator is decoded: the fix-up (add every lane's sign
-// bit to itself, then xor it back) makes every lane its own two's-complement value, the
-// lanes are extracted and added into an LDS tile of int32 outputs - which also performs
-// the overlap-add of neighbouring words' partial lanes.  The tile is finally written to
-// HBM row by row.
+// Three kernels:
+//  * prep_weights_kernel: every kernel row -> its kernel words (taps reversed, sign-
+//    extended, L bits apart), laid out as one contiguous stream per group of kWaveM
+//    output channels, so a wave walks its kernel words with scalar loads;
+//  * spread_kernel: every packed input row -> operand words, I values of one stride
+//    phase L bits apart (temporary spacer bits), negative values sign-extended, so that
+//    each word is the int32 sum_i v_i 2^(i L); rows of the zero padding are written too;
+//  * conv2d_samd_kernel: a workgroup owns a tile of output rows of one image and wm*8
+//    output channels.  Per chunk of input channels it copies the tile's operand words
+//    into LDS (double-buffered, one barrier per chunk); every wave multiplies them by its
+//    8 SGPR-resident kernel words and adds the exact signed 32x32 -> 64-bit products
+//    into 64-bit accumulators (v_mad_i64_i32).  Every G channels the accumulators are
+//    decoded - fix-up, lane extraction - and added into an LDS tile of int32 outputs,
+//    which also performs the overlap-add of neighbouring words' partial lanes.
 #include <hip/hip_runtime.h>
 
 #include "hip_util.hpp"
@@ -25,6 +24,7 @@ namespace samd {
 namespace {
 
 constexpr int RM = kWaveM;
+constexpr int kPrefetch = kStagePerThread;   // operand words each thread carries into the next chunk
 
 template <int B, bool S>
 __device__ inline int32_t packed_field(const uint32_t *row, int col) {
@@ -34,147 +34,287 @@ __device__ inline int32_t packed_field(const uint32_t *row, int col) {
     return (int32_t)f;
 }
 
-// Kernel words, laid out [channel block][channel][kernel row x tap word][mblk] so that
-// each wave reads its kWaveM words of one (channel, row-tap) as one contiguous run.
+// Kernel-word stream of output-channel group wb: step s = c*nrt + ky*ntw + t holds the
+// kWaveM words of kernel word t of row ky of channel c; kStreamPad zero steps pad the end.
 template <int B, bool S>
 __global__ __launch_bounds__(256) void prep_weights_kernel(const uint32_t *__restrict__ w, const Conv2dGeom g,
                                                            int32_t *__restrict__ kw) {
-    const int64_t total = (int64_t)g.nmb * g.C * g.nrt * g.mblk;
-    for (int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x; idx < total; idx += (int64_t)gridDim.x * 256) {
-        const int mm = (int)(idx % g.mblk);
-        int64_t t = idx / g.mblk;
-        const int rt = (int)(t % g.nrt);
-        t /= g.nrt;
-        const int c = (int)(t % g.C);
-        const int mb = (int)(t / g.C);
-        const int m = mb * g.mblk + mm;
+    const int64_t steps = (int64_t)g.C * g.nrt + kStreamPad;
+    for (int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x; idx < g.kw_words; idx += (int64_t)gridDim.x * 256) {
+        const int mm = (int)(idx % RM);
+        const int64_t s = (idx / RM) % steps;
+        const int64_t wb = idx / (RM * steps);
+        const int m = (int)(wb * RM + mm);
         uint32_t word = 0;
-        if (m < g.M) {
-            const int ky = rt / g.ntw, tw = rt % g.ntw;
+        if (m < g.M && s < (int64_t)g.C * g.nrt) {
+            const int c = (int)(s / g.nrt), rt = (int)(s % g.nrt);
+            const int ky = rt / g.ntw, t = rt % g.ntw;
             const uint32_t *row = w + ((int64_t)(m * g.C + c) * g.KH + ky) * g.wrw;
-            const int k = g.tw_ntaps[tw], a0 = g.tw_tap0[tw], r = g.tw_phase[tw];
-            for (int s = 0; s < k; ++s) {
-                const int tap = g.sw * (a0 + k - 1 - s) + r;   // reversed: lane s holds tap a0+k-1-s
-                word += (uint32_t)packed_field<B, S>(row, tap) << (s * g.L);
+            const int k = g.tw_ntaps[t], a0 = g.tw_tap0[t], r = g.tw_phase[t];
+            for (int si = 0; si < k; ++si) {
+                const int tap = g.sw * (a0 + k - 1 - si) + r;   // reversed: lane si holds tap a0+k-1-si
+                word += (uint32_t)packed_field<B, S>(row, tap) << (si * g.L);
             }
         }
         kw[idx] = (int32_t)word;
     }
 }
 
+// Operand words xs[n][c][hp][t][q] for padded rows hp in [0, H + 2 ph).
 template <int B, bool S>
-__global__ __launch_bounds__(256) void conv2d_samd_kernel(const uint32_t *__restrict__ x,
+__global__ __launch_bounds__(256) void spread_kernel(const uint32_t *__restrict__ x, const Conv2dGeom g,
+                                                     int32_t *__restrict__ xs) {
+    for (int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x; idx < g.spread_words;
+         idx += (int64_t)gridDim.x * 256) {
+        const int q = (int)(idx % g.nq);
+        int64_t t1 = idx / g.nq;
+        const int t = (int)(t1 % g.ntw);
+        t1 /= g.ntw;
+        const int hp = (int)(t1 % g.Hp);
+        const int64_t nc = t1 / g.Hp;
+        const int h = hp - g.ph;
+        uint32_t word = 0;
+        if (h >= 0 && h < g.H) {
+            const uint32_t *row = x + (nc * g.H + h) * g.xrw;
+            const int delta = g.tw_tap0[t] + g.tw_ntaps[t] - g.Kmax;
+            const int col0 = g.sw * (q * g.I + delta) + g.tw_phase[t] - g.pw;
+            for (int ii = 0; ii < g.I; ++ii) {
+                const int col = col0 + g.sw * ii;
+                if (col >= 0 && col < g.W) word += (uint32_t)packed_field<B, S>(row, col) << (ii * g.L);
+            }
+        }
+        xs[idx] = (int32_t)word;
+    }
+}
+
+// Empty register barrier: the accumulator is treated as rewritten here, so the products
+// of successive steps cannot be summed first and added afterwards (integer addition is
+// associative, and that rewrite costs one extra 64-bit add per batch); every product
+// stays one v_mad_i64_i32 into its accumulator.
+__device__ __forceinline__ void keep(int64_t &acc) { asm volatile("" : "+v"(acc)); }
+
+// NRT: steps (kernel row x kernel word) per input channel when it is 3 or 6 (every 3x3
+// layer), so batches never straddle channels and all LDS offsets are immediates; 0 for
+// any other count.
+template <int RH, int NRT>
+__global__ __launch_bounds__(256) void conv2d_samd_kernel(const int32_t *__restrict__ xs,
                                                           const int32_t *__restrict__ kw, int32_t *__restrict__ y,
                                                           const Conv2dGeom g) {
     extern __shared__ int32_t lds[];
     int32_t *tile = lds;
-    int32_t *spread = lds + g.lds_tile;
-    uint32_t *raw = (uint32_t *)(lds + g.lds_tile + g.lds_spread);
+    int32_t *abuf0 = lds + g.lds_tile;
+    int32_t *abuf1 = abuf0 + g.lds_abuf;
+
+    // Consecutive workgroups on one XCD (hardware assigns workgroup p to XCD p % 8) take
+    // all channel blocks of one spatial tile, so its operand words are reused from L2.
+    const int p = blockIdx.x;
+    const int slot = p >> 3;
+    const int mb = slot % g.nmb;
+    const int tile_id = (slot / g.nmb) * 8 + (p & 7);
+    if (tile_id >= g.N * g.row_tiles) return;   // padding workgroup: exits as a whole
+    const int n = tile_id / g.row_tiles;
+    const int ho0 = (tile_id % g.row_tiles) * g.rows_blk;
 
     const int tid = threadIdx.x;
     const int nthr = g.wm * 64;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int lane = tid & 63;
-    const int ho0 = blockIdx.x * g.rows_blk;
-    const int mb = blockIdx.y;
-    const int n = blockIdx.z;
-    const int rloc_raw = lane / g.nq;
-    const bool active = rloc_raw < g.rows_blk && ho0 + rloc_raw < g.Ho;
-    const int rloc = active ? rloc_raw : 0;
-    const int q = active ? lane - rloc_raw * g.nq : 0;
-    const int hin0 = ho0 * g.sh - g.ph;
+    const int grp_raw = lane / g.nq;
+    const bool lane_ok = grp_raw < g.groups;
+    const int grp = lane_ok ? grp_raw : 0;
+    const int q = lane_ok ? lane - grp_raw * g.nq : 0;
+    const int wb = mb * g.wm + wave;
 
     for (int i = tid; i < g.lds_tile; i += nthr) tile[i] = 0;
 
-    int64_t acc[RM];
+    // LDS chunk layout [cc][q][tr * ntw + t] with an odd stride per q (conflict-free):
+    // a thread's steps (ky, t) of one channel and row are consecutive words.
+    const int T = g.trows * g.ntw;                 // words per (channel, q)
+    const int qs = g.lds_qstride;                  // T rounded up to odd
+    const int cs = g.nq * qs;                      // words per channel
+    const int gblk = T * g.nq;                     // global words per channel of the tile
+    const int64_t ch_stride = (int64_t)g.Hp * g.ntw * g.nq;
+    const int in_words = min(g.trows, g.Hp - ho0 * g.sh) * g.ntw * g.nq;   // rows that exist
+    const int32_t *xs_tile = xs + ((int64_t)n * g.C * g.Hp + ho0 * g.sh) * g.ntw * g.nq;
+    // Thread element j of a chunk: global word i of channel cc (global order [tr][t][q]);
+    // the same (cc, i) in every chunk, so offsets are computed once.
+    int e_cc[kPrefetch], e_lds[kPrefetch];
+    int64_t e_off[kPrefetch];
+    bool e_row[kPrefetch];
+    const int chunk_words = g.chk * gblk;
 #pragma unroll
-    for (int m = 0; m < RM; ++m) acc[m] = 0;
-    int pending = 0;
+    for (int j = 0; j < kPrefetch; ++j) {
+        const int e = tid + j * nthr;
+        const int cc = e / gblk, i = e - cc * gblk;
+        const int qq = i % g.nq, rt = i / g.nq;
+        e_cc[j] = e < chunk_words ? cc : 1 << 30;
+        e_off[j] = cc * ch_stride + i;
+        e_lds[j] = cc * cs + qq * qs + rt;
+        e_row[j] = i < in_words;
+    }
+    // words past the kPrefetch carried per thread (large staged tiles only): loaded and
+    // stored directly
+    auto stage_rest = [&](int32_t *dst, const int32_t *src, int ncc) {
+        for (int e = tid + kPrefetch * nthr; e < ncc * gblk; e += nthr) {
+            const int cc = e / gblk, i = e - cc * gblk;
+            const int qq = i % g.nq, rt = i / g.nq;
+            dst[cc * cs + qq * qs + rt] = i < in_words ? src[cc * ch_stride + i] : 0;
+        }
+    };
+    const int nchunks = (g.C + g.chk - 1) / g.chk;
+    {
+        const int ncc = min(g.chk, g.C);
+#pragma unroll
+        for (int j = 0; j < kPrefetch; ++j)
+            if (e_cc[j] < ncc) abuf0[e_lds[j]] = e_row[j] ? xs_tile[e_off[j]] : 0;
+        stage_rest(abuf0, xs_tile, ncc);
+    }
+    __syncthreads();
 
-    const int32_t *kwave = kw + (int64_t)mb * g.C * g.nrt * g.mblk + wave * RM;
-    int32_t *tile_row = tile + ((wave * RM) * g.rows_blk + rloc) * g.Wo;
-    const int tile_mstride = g.rows_blk * g.Wo;
-    const int obase = q * g.I - g.Kmax + 1;
+    int64_t acc[RH][RM];
+#pragma unroll
+    for (int r = 0; r < RH; ++r)
+#pragma unroll
+        for (int m = 0; m < RM; ++m) acc[r][m] = 0;
+
+    const int64_t stream_len = ((int64_t)g.C * g.nrt + kStreamPad) * RM;
+    const int32_t *kstream = kw + wb * stream_len;
+    // LDS word offset of each of the thread's rows within a channel (rows past the tile
+    // reuse the last one; their results are never decoded)
+    int rowoff[RH];
+#pragma unroll
+    for (int r = 0; r < RH; ++r) rowoff[r] = q * qs + min(grp * RH + r, g.rows_blk - 1) * g.sh * g.ntw;
 
     auto decode = [&]() {
+        const int obase = q * g.I - g.Kmax + 1;
 #pragma unroll
-        for (int m = 0; m < RM; ++m) {
-            uint64_t v = (uint64_t)acc[m];
-            acc[m] = 0;
-            if (g.result_signed) {
-                const uint64_t s = v & g.msb_mask;
-                v = (v + s) ^ s;
-            }
-            int32_t *trow = tile_row + m * tile_mstride;
-            for (int j = 0; j < g.nl; ++j) {
-                int32_t d;
-                if (j < g.nl - 1) {
-                    const uint32_t w32 = (uint32_t)(v >> (j * g.L));
-                    d = g.result_signed ? ((int32_t)(w32 << (32 - g.L)) >> (32 - g.L))
-                                        : (int32_t)(w32 & ((1u << g.L) - 1));
-                } else {
-                    d = g.result_signed ? (int32_t)((int64_t)v >> (j * g.L)) : (int32_t)(v >> (j * g.L));
+        for (int r = 0; r < RH; ++r) {
+            const int rloc = grp * RH + r;
+            const bool ok = lane_ok && rloc < g.rows_blk && ho0 + rloc < g.Ho;
+#pragma unroll
+            for (int m = 0; m < RM; ++m) {
+                uint64_t v = (uint64_t)acc[r][m];
+                acc[r][m] = 0;
+                if (g.result_signed) {
+                    const uint64_t s = v & g.msb_mask;
+                    v = (v + s) ^ s;
                 }
-                const int o = obase + j;
-                if (active && o >= 0 && o < g.Wo) atomicAdd(&trow[o], d);
+                int32_t *trow = tile + ((wave * RM + m) * g.rows_blk + (ok ? rloc : 0)) * g.Wo;
+                for (int j = 0; j < g.nl; ++j) {
+                    int32_t d;
+                    if (j < g.nl - 1) {
+                        const uint32_t w32 = (uint32_t)(v >> (j * g.L));
+                        d = g.result_signed ? ((int32_t)(w32 << (32 - g.L)) >> (32 - g.L))
+                                            : (int32_t)(w32 & ((1u << g.L) - 1));
+                    } else {
+                        d = g.result_signed ? (int32_t)((int64_t)v >> (j * g.L)) : (int32_t)(v >> (j * g.L));
+                    }
+                    const int o = obase + j;
+                    if (ok && o >= 0 && o < g.Wo) atomicAdd(&trow[o], d);
+                }
             }
         }
     };
 
-    for (int c0 = 0; c0 < g.C; c0 += g.cc) {
-        const int ncc = min(g.cc, g.C - c0);
-        __syncthreads();
-        // 1. packed input rows of this channel chunk (zero rows above / below the image)
-        const int nraw = ncc * g.trows * g.xrw;
-        for (int i = tid; i < nraw; i += nthr) {
-            const int wd = i % g.xrw;
-            const int t = i / g.xrw;
-            const int tr = t % g.trows, cc = t / g.trows;
-            const int h = hin0 + tr;
-            uint32_t v = 0;
-            if (h >= 0 && h < g.H) v = x[(((int64_t)n * g.C + c0 + cc) * g.H + h) * g.xrw + wd];
-            raw[i] = v;
-        }
-        __syncthreads();
-        // 2. operand words: I values of stride phase r starting at phase index q*I + delta
-        const int nsp = ncc * g.trows * g.nvar * g.nq;
-        for (int i = tid; i < nsp; i += nthr) {
-            const int qq = i % g.nq;
-            int t = i / g.nq;
-            const int v = t % g.nvar;
-            t /= g.nvar;
-            const uint32_t *row = raw + t * g.xrw;
-            const int col0 = g.sw * (qq * g.I + g.var_delta[v]) + g.var_phase[v] - g.pw;
-            uint32_t word = 0;
-            for (int ii = 0; ii < g.I; ++ii) {
-                const int col = col0 + g.sw * ii;
-                if (col >= 0 && col < g.W) word += (uint32_t)packed_field<B, S>(row, col) << (ii * g.L);
-            }
-            spread[i] = (int32_t)word;
-        }
-        __syncthreads();
-        // 3. multiply-accumulate: one v_mad_i64_i32 per (row-tap, output channel)
-        for (int cc = 0; cc < ncc; ++cc) {
-            const int32_t *kc = kwave + (int64_t)(c0 + cc) * g.nrt * g.mblk;
-            const int32_t *sp = spread + (cc * g.trows + rloc * g.sh) * g.nvar * g.nq + q;
-            int rt = 0;
-            for (int ky = 0; ky < g.KH; ++ky) {
-                for (int tw = 0; tw < g.ntw; ++tw, ++rt) {
-                    const int32_t a = active ? sp[(ky * g.nvar + g.tw_var[tw]) * g.nq] : 0;
-                    const int32_t *kr = kc + rt * g.mblk;
+    for (int k = 0; k < nchunks; ++k) {
+        const int32_t *cur = (k & 1) ? abuf1 : abuf0;
+        int32_t *nxt = (k & 1) ? abuf0 : abuf1;
+        const int c0 = k * g.chk;
+        const int ncc = min(g.chk, g.C - c0);
+        const int c1 = c0 + g.chk;
+        const int ncc1 = k + 1 < nchunks ? min(g.chk, g.C - c1) : 0;
+
+        // operand words of the next chunk: global loads now, LDS stores after the compute
+        int32_t pre[kPrefetch];
+        const int32_t *src1 = xs_tile + c1 * ch_stride;
 #pragma unroll
-                    for (int m = 0; m < RM; ++m) acc[m] += (int64_t)a * (int64_t)kr[m];
+        for (int j = 0; j < kPrefetch; ++j) pre[j] = (e_cc[j] < ncc1 && e_row[j]) ? src1[e_off[j]] : 0;
+
+        // Batches of kStepBatch steps: kernel words in SGPRs, operand words from LDS.  With
+        // 3 or 6 steps per channel a chunk is a whole number of batches, and a partial last
+        // batch can only end the last chunk, where it runs on the stream's zero padding.
+        const int nsteps = ncc * g.nrt;
+        const int nbat = (nsteps + kStepBatch - 1) / kStepBatch;
+        const int32_t *ks = kstream + (int64_t)c0 * g.nrt * RM;
+        int32_t kA[kStepBatch * RM], aA[kStepBatch][RH], kB[kStepBatch * RM], aB[kStepBatch][RH];
+        int gs = 0;   // generic layout: step index of the next batch to load
+        auto load_batch = [&](int b, int32_t (&kb)[kStepBatch * RM], int32_t (&ab)[kStepBatch][RH]) {
+#pragma unroll
+            for (int j = 0; j < kStepBatch * RM; ++j) kb[j] = ks[b * kStepBatch * RM + j];
+            if (NRT != 0) {
+                // batch b: channel b / (NRT/3), steps (b % (NRT/3))*3 .. +2 of it
+                constexpr int BPC = NRT / kStepBatch;
+                const int base = (b / BPC) * cs + (b % BPC) * kStepBatch;
+#pragma unroll
+                for (int r = 0; r < RH; ++r) {
+                    const int32_t *src = cur + base + rowoff[r];
+#pragma unroll
+                    for (int j = 0; j < kStepBatch; ++j) ab[j][r] = src[j];
                 }
+            } else {
+#pragma unroll
+                for (int j = 0; j < kStepBatch; ++j) {
+                    // steps past the chunk (its step count need not be a multiple of the
+                    // batch) multiply the next chunk's kernel words: their operand is 0
+                    const bool live = gs + j < nsteps;
+                    const int st = min(gs + j, nsteps - 1);
+                    const int cc = st / g.nrt, rt = st - cc * g.nrt;
+#pragma unroll
+                    for (int r = 0; r < RH; ++r) {
+                        const int32_t v = cur[cc * cs + rt + rowoff[r]];
+                        ab[j][r] = live ? v : 0;
+                    }
+                }
+                gs += kStepBatch;
             }
-            if (++pending == g.G) {
-                decode();
-                pending = 0;
+        };
+        auto mac_batch = [&](const int32_t (&kb)[kStepBatch * RM], const int32_t (&ab)[kStepBatch][RH]) {
+#pragma unroll
+            for (int j = 0; j < kStepBatch; ++j) {
+#pragma unroll
+                for (int r = 0; r < RH; ++r)
+#pragma unroll
+                    for (int m = 0; m < RM; ++m) acc[r][m] += (int64_t)ab[j][r] * (int64_t)kb[j * RM + m];
+#pragma unroll
+                for (int r = 0; r < RH; ++r)
+#pragma unroll
+                    for (int m = 0; m < RM; ++m) keep(acc[r][m]);
             }
+        };
+        // Ping-pong over two register sets.  Before a batch's kernel words are used, all
+        // outstanding scalar and LDS loads are waited for, and only then is the next batch
+        // requested: scalar loads return out of order, so a wait placed after requesting
+        // the next batch would wait for it too.
+        // The batch after the last one is fetched too (its results are never used): the
+        // kernel-word stream ends in kStreamPad padding steps and the LDS buffers are
+        // followed by one spare channel block, so it reads padding.
+        load_batch(0, kA, aA);
+        for (int b = 0; b < nbat; b += 2) {
+            __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0)
+            load_batch(b + 1, kB, aB);
+            __builtin_amdgcn_sched_barrier(0);
+            mac_batch(kA, aA);
+            __builtin_amdgcn_sched_barrier(0);
+            if (b + 1 >= nbat) break;
+            __builtin_amdgcn_s_waitcnt(0xc07f);
+            load_batch(b + 2, kA, aA);
+            __builtin_amdgcn_sched_barrier(0);
+            mac_batch(kB, aB);
+            __builtin_amdgcn_sched_barrier(0);
         }
+
+        // the next chunk's operand words into the other buffer (last read a chunk ago,
+        // before the previous barrier)
+#pragma unroll
+        for (int j = 0; j < kPrefetch; ++j)
+            if (e_cc[j] < ncc1) nxt[e_lds[j]] = pre[j];
+        stage_rest(nxt, src1, ncc1);
+
+        if ((k + 1) % g.flush_chunks == 0 || k + 1 == nchunks) decode();
+        __syncthreads();
     }
-    if (pending) decode();
-    __syncthreads();
-    // 4. write the output tile, whole rows at a time
+
+    // output tile -> y, whole rows
     const int tile_n = g.mblk * g.rows_blk * g.Wo;
     for (int i = tid; i < tile_n; i += nthr) {
         const int o = i % g.Wo;
@@ -189,8 +329,7 @@ __global__ __launch_bounds__(256) void conv2d_samd_kernel(const uint32_t *__rest
 
 int launch_conv2d_prepare(const uint32_t *w, const Conv2dGeom &g, void *ws, hipStream_t s) {
     int32_t *kw = (int32_t *)ws;
-    const int64_t nkw = (int64_t)g.nmb * g.C * g.nrt * g.mblk;
-    const int pgrid = grid_for(nkw, 256);
+    const int pgrid = grid_for(g.kw_words, 256);
     bool launched = false;
 #define SAMD_PREP_CASE(B, SG)                                                                            \
     if (!launched && g.wbits == B && (bool)g.wsigned == SG) {                                            \
@@ -204,17 +343,30 @@ int launch_conv2d_prepare(const uint32_t *w, const Conv2dGeom &g, void *ws, hipS
 
 int launch_conv2d_samd(const uint32_t *x, const Conv2dGeom &g, int32_t *y, const void *ws, hipStream_t s) {
     const int32_t *kw = (const int32_t *)ws;
-    const dim3 grid((g.Ho + g.rows_blk - 1) / g.rows_blk, g.nmb, g.N);
-    const size_t shm = (size_t)(g.lds_tile + g.lds_spread + g.lds_raw) * 4;
+    int32_t *xs = (int32_t *)((char *)const_cast<void *>(ws) + conv2d_kw_bytes(g));
+    const int sgrid = grid_for(g.spread_words, 256);
     bool launched = false;
-#define SAMD_CONV_CASE(B, SG)                                                                               \
-    if (!launched && g.xbits == B && (bool)g.xsigned == SG) {                                               \
-        hipLaunchKernelGGL((conv2d_samd_kernel<B, SG>), grid, dim3(g.wm * 64), shm, s, x, kw, y, g);        \
-        launched = true;                                                                                    \
+#define SAMD_SPREAD_CASE(B, SG)                                                                            \
+    if (!launched && g.xbits == B && (bool)g.xsigned == SG) {                                              \
+        hipLaunchKernelGGL((spread_kernel<B, SG>), dim3(sgrid), dim3(256), 0, s, x, g, xs);                \
+        launched = true;                                                                                   \
     }
-    SAMD_FOR_EACH_FMT(SAMD_CONV_CASE)
+    SAMD_FOR_EACH_FMT(SAMD_SPREAD_CASE)
+#undef SAMD_SPREAD_CASE
+    int st = check_launch("conv2d operand spread");
+    if (st) return st;
+    const dim3 grid((unsigned)g.tiles * g.nmb), block(g.wm * 64);
+    const size_t shm = (size_t)g.lds_words * 4;
+#define SAMD_CONV_CASE(RH_, NRT_)                                                                     \
+    if (g.rh == RH_ && (NRT_ == 0 ? (g.nrt != 3 && g.nrt != 6) : g.nrt == NRT_)) {                     \
+        hipLaunchKernelGGL((conv2d_samd_kernel<RH_, NRT_>), grid, block, shm, s, xs, kw, y, g);          \
+        return check_launch("conv2d");                                                                \
+    }
+    SAMD_CONV_CASE(1, 3) SAMD_CONV_CASE(1, 6) SAMD_CONV_CASE(1, 0)
+    SAMD_CONV_CASE(2, 3) SAMD_CONV_CASE(2, 6) SAMD_CONV_CASE(2, 0)
 #undef SAMD_CONV_CASE
-    return check_launch("conv2d");
+    set_error("conv2d: no kernel for this geometry");
+    return SAMD_EUNSUPPORTED;
 }
 
 }  // namespace samd

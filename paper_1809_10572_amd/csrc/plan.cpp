@@ -8,6 +8,7 @@
 // accumulated into it before the lanes are decoded, and the planner picks among the
 // exact geometries the one with the lowest modelled cost.
 #include <algorithm>
+#include <cmath>
 #include <cstdio>
 #include <limits>
 
@@ -47,15 +48,18 @@ int pairs_in_lane(int j, int I, int k) {
     return std::min(std::min(j + 1, k), std::min(I, I + k - 1 - j));
 }
 
-// Split `count` consecutive taps into ceil(count / kmax) near-equal groups.
-void split_taps(int count, int kmax, int *t0, int *nt, int &ngroups) {
+// Split `count` consecutive taps into ceil(count / kmax) near-equal groups; false (and
+// nothing written) when that is more than kMaxTapWords groups.
+bool split_taps(int count, int kmax, int *t0, int *nt, int &ngroups) {
     ngroups = (count + kmax - 1) / kmax;
+    if (ngroups > kMaxTapWords) return false;
     int base = count / ngroups, extra = count % ngroups, at = 0;
     for (int g = 0; g < ngroups; ++g) {
         nt[g] = base + (g < extra ? 1 : 0);
         t0[g] = at;
         at += nt[g];
     }
+    return true;
 }
 
 int pick_waves_m(int M) {
@@ -106,35 +110,27 @@ int plan_conv2d(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, Conv2dGeom 
             c.I = I;
             // kernel words: every stride phase's taps in groups of at most kmax
             c.ntw = 0;
-            c.nvar = 0;
             bool ok = true;
             for (int r = 0; r < S && ok; ++r) {
                 int Kr = r < d.KW ? (d.KW - r + S - 1) / S : 0;
                 if (Kr == 0) continue;
                 int t0[kMaxTapWords], nt[kMaxTapWords], ng;
-                split_taps(Kr, kmax, t0, nt, ng);
+                if (!split_taps(Kr, kmax, t0, nt, ng)) {
+                    ok = false;
+                    break;
+                }
                 for (int q = 0; q < ng; ++q) {
                     if (c.ntw >= kMaxTapWords) { ok = false; break; }
-                    int delta = t0[q] + nt[q] - c.Kmax;
-                    int v = -1;
-                    for (int u = 0; u < c.nvar; ++u)
-                        if (c.var_phase[u] == r && c.var_delta[u] == delta) v = u;
-                    if (v < 0) {
-                        if (c.nvar >= kMaxVariants) { ok = false; break; }
-                        v = c.nvar++;
-                        c.var_phase[v] = r;
-                        c.var_delta[v] = delta;
-                    }
                     c.tw_phase[c.ntw] = r;
                     c.tw_tap0[c.ntw] = t0[q];
                     c.tw_ntaps[c.ntw] = nt[q];
-                    c.tw_var[c.ntw] = v;
                     ++c.ntw;
                 }
             }
             if (!ok) continue;
             // products per lane for one (channel, kernel row)
-            int nj[kMaxOutLanes + 8] = {0};
+            if (I + c.Kmax - 1 > kMaxOutLanes) continue;
+            int nj[kMaxOutLanes] = {0};
             int top = -1;
             for (int j = 0; j < I + c.Kmax - 1; ++j) {
                 for (int t = 0; t < c.ntw; ++t) nj[j] += pairs_in_lane(j, I, c.tw_ntaps[t]);
@@ -160,28 +156,57 @@ int plan_conv2d(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, Conv2dGeom 
             for (int j = 0; j < c.nl - 1; ++j) c.msb_mask |= (uint64_t)1 << (j * L + L - 1);
             c.nq = (c.Wo + c.Kmax - 1 + I - 1) / I;
             if (c.nq > 64) continue;
-            c.rows_blk = std::max(1, std::min(64 / c.nq, c.Ho));
-            c.trows = (c.rows_blk - 1) * d.stride_h + d.KH;
             c.nrt = d.KH * c.ntw;
-            // LDS: output tile, spread operand words and raw packed rows of a channel chunk
-            c.lds_tile = c.mblk * c.rows_blk * c.Wo;
-            c.cc = std::min(d.C, 8);
-            for (;;) {
-                c.lds_spread = c.cc * c.trows * c.nvar * c.nq;
-                c.lds_raw = c.cc * c.trows * c.xrw;
-                if ((long)(c.lds_tile + c.lds_spread + c.lds_raw) * 4 <= 65536 || c.cc == 1) break;
-                --c.cc;
+            c.Hp = d.H + 2 * d.pad_h;
+            // Two output rows per thread halve the waves: keep them while the grid still
+            // gives every SIMD (1024 of them) more than one wave.  Then the largest tile
+            // (row groups per wave) whose LDS fits.
+            bool placed = false;
+            const int grp_max = 64 / c.nq;
+            int rh_pref[2] = {1, 1};
+            {
+                int rows2 = std::min(2 * grp_max, c.Ho);
+                long tiles2 = (long)d.N * ((c.Ho + rows2 - 1) / rows2);
+                if (tiles2 * c.nmb * c.wm >= 1536 && c.Ho >= 2) rh_pref[0] = 2;
             }
-            if ((long)(c.lds_tile + c.lds_spread + c.lds_raw) * 4 > 65536) continue;
+            for (int pi = 0; pi < 2 && !placed; ++pi) {
+                c.rh = rh_pref[pi];
+                for (int gr = grp_max; gr >= 1 && !placed; --gr) {
+                    c.groups = gr;
+                    c.rows_blk = std::min(c.rh * c.groups, c.Ho);
+                    c.trows = (c.rows_blk - 1) * d.stride_h + d.KH;
+                    c.lds_tile = c.mblk * c.rows_blk * c.Wo;
+                    c.lds_qstride = (c.trows * c.ntw) | 1;
+                    // prefer chunks every thread stages from registers (kStagePerThread words)
+                    for (c.chk = std::min(std::min(d.C, kMaxChunk), c.G); c.chk >= 1; --c.chk) {
+                        long staged = (long)c.chk * c.trows * c.ntw * c.nq;
+                        c.lds_abuf = c.chk * c.nq * c.lds_qstride;
+                        // a spare channel block after the buffers: the batch after the last one
+                        // of a chunk is fetched as well and reads there
+                        c.lds_words = c.lds_tile + 2 * c.lds_abuf + c.nq * c.lds_qstride + kStepBatch;
+                        if ((long)c.lds_words * 4 > 65536) continue;
+                        if (staged <= kStagePerThread * c.wm * 64 || c.chk == 1) {
+                            placed = true;
+                            break;
+                        }
+                    }
+                }
+            }
+            if (!placed) continue;
+            c.row_tiles = (c.Ho + c.rows_blk - 1) / c.rows_blk;
+            c.tiles = (d.N * c.row_tiles + 7) / 8 * 8;
+            c.flush_chunks = c.G / c.chk;
+            c.kw_words = (int64_t)c.nmb * c.wm * ((int64_t)d.C * c.nrt + kStreamPad) * kWaveM;
+            c.spread_words = (int64_t)d.N * d.C * c.Hp * c.ntw * c.nq;
             // cost per output value, in VALU issue slots
-            double mads = (double)d.C * d.KH * c.ntw;
-            double flushes = (double)((d.C + c.G - 1) / c.G);
+            double mads = (double)d.C * c.nrt;
+            double flushes = std::ceil((double)d.C / ((double)c.flush_chunks * c.chk));
             double decode = (c.result_signed ? 6.0 : 0.0) + 4.0 * c.nl;
-            double staging = (double)d.C * c.trows * c.nvar * (6.0 * I + 4.0) / ((double)c.rows_blk * c.mblk);
-            double lane_util = (double)c.rows_blk * c.nq / 64.0;
-            int row_tiles = (c.Ho + c.rows_blk - 1) / c.rows_blk;
-            double row_util = (double)c.Ho / ((double)row_tiles * c.rows_blk);
-            c.cost = (mads + flushes * decode + staging) / I / (lane_util * row_util);
+            double staging = (double)d.C * c.trows * c.ntw * 2.0 / ((double)c.rows_blk * c.mblk);
+            double spread = (double)d.C * c.Hp * c.ntw * c.nq * (6.0 * I + 4.0) / ((double)d.M * c.Ho * c.Wo);
+            double lane_util = (double)c.groups * c.nq / 64.0;
+            double row_util = (double)c.Ho / ((double)c.row_tiles * c.rows_blk);
+            c.cost = ((mads + flushes * decode + staging) / I + spread) / (lane_util * row_util);
             c.macs_per_mad = (double)I * d.KW / (double)c.ntw;
             if (c.cost < best.cost) {
                 best = c;
@@ -199,8 +224,11 @@ int plan_conv2d(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, Conv2dGeom 
     return SAMD_OK;
 }
 
+// Workspace: kernel-word streams, then the operand words of one call (256-byte aligned).
+size_t conv2d_kw_bytes(const Conv2dGeom &g) { return ((size_t)g.kw_words * 4 + 255) / 256 * 256; }
+
 size_t conv2d_workspace_bytes(const Conv2dGeom &g) {
-    return (size_t)g.nmb * g.mblk * g.C * g.nrt * sizeof(int32_t);
+    return conv2d_kw_bytes(g) + ((size_t)g.spread_words * 4 + 255) / 256 * 256;
 }
 
 int plan_conv1d(int64_t n, samd_fmt xf, const int32_t *taps, int32_t K, samd_fmt kf, Conv1dGeom &best,
@@ -228,10 +256,10 @@ int plan_conv1d(int64_t n, samd_fmt xf, const int32_t *taps, int32_t K, samd_fmt
             c.L = L;
             c.I = I;
             int t0[kMaxTapWords], nt[kMaxTapWords];
-            if ((K + kmax - 1) / kmax > kMaxTapWords) continue;
-            split_taps(K, kmax, t0, nt, c.ngroups);
+            if (!split_taps(K, kmax, t0, nt, c.ngroups)) continue;
             // lanes: j <-> output q*I + j - (K - 1); group g's window starts at q*I - t0[g]
             int nl = I + K - 1, top = -1;
+            if (nl > 64) continue;
             int nj[64] = {0};
             for (int j = 0; j < nl; ++j) {
                 for (int q = 0; q < c.ngroups; ++q) nj[j] += pairs_in_lane(j, I, nt[q]);

@@ -12,11 +12,14 @@
 namespace samd {
 
 constexpr int kMaxTapWords = 16;   // kernel words per (input channel, kernel row)
-constexpr int kMaxVariants = 16;   // distinct (stride phase, window offset) operand words
 constexpr int kMaxLanes = 16;      // I: values per operand word
 constexpr int kMaxOutLanes = 20;   // I + Kmax - 1: lanes of an accumulator that are decoded
-constexpr int kWaveM = 16;         // output channels per wave (64-bit accumulators per thread)
+constexpr int kWaveM = 8;          // output channels per wave (kernel words per step, in SGPRs)
 constexpr int kMaxConv1dExtra = 15; // following words whose low lanes reach a 1-D output word
+constexpr int kStepBatch = 3;      // kernel-word steps fetched per scalar-load batch
+constexpr int kStreamPad = 2 * kStepBatch;  // zero steps after each kernel-word stream
+constexpr int kMaxChunk = 8;       // input channels staged in LDS per chunk
+constexpr int kStagePerThread = 8; // operand words each conv2d thread stages per chunk
 
 // Geometry of one SAMD 2-D convolution.  Every operand word is a signed 32-bit
 // integer A = sum_i v_i 2^(i L) holding I input values of one stride phase of one
@@ -24,29 +27,38 @@ constexpr int kMaxConv1dExtra = 15; // following words whose low lanes reach a 1
 // every kernel word B = sum_s w_s 2^(s L) holds up to Kmax taps of one phase of one
 // kernel row, reversed.  A*B accumulates into a 64-bit integer whose L-bit lane j
 // holds a partial sum for output column q*I + j - (Kmax - 1).
+//
+// Kernel word t of a kernel row multiplies operand words whose window starts at phase
+// index q*I + delta_t, delta_t = tap0_t + ntaps_t - Kmax; each kernel word has its own
+// operand-word variant, stored at index t.
 struct Conv2dGeom {
-    int32_t N, C, H, W, M, KH, KW, sh, sw, ph, pw, Ho, Wo;
+    int32_t N, C, H, W, M, KH, KW, sh, sw, ph, pw, Ho, Wo, Hp;
     int32_t xbits, xsigned, wbits, wsigned;
     int32_t L, I, Kmax, nq, G;      // lane bits, values/word, widest phase, words/row, flush channels
-    int32_t nl;                     // decoded lanes per accumulator, I + Kmax - 1
+    int32_t nl;                     // decoded lanes per accumulator; lane nl-1 takes the remaining bits
     int32_t result_signed;          // any operand signed: lanes need the fix-up
     uint64_t msb_mask;              // sign bit of lanes 0 .. nl-2
-    int32_t ntw;                    // kernel words per (channel, kernel row)
+    int32_t ntw;                    // kernel words (and operand-word variants) per (channel, kernel row)
     int32_t tw_phase[kMaxTapWords], tw_tap0[kMaxTapWords], tw_ntaps[kMaxTapWords];
-    int32_t tw_var[kMaxTapWords];   // operand-word variant each kernel word multiplies
-    int32_t nvar;                   // operand-word variants
-    int32_t var_phase[kMaxVariants], var_delta[kMaxVariants];
-    int32_t nrt;                    // row-taps per channel: KH * ntw
+    int32_t nrt;                    // steps per channel: KH * ntw
     // launch shape
-    int32_t rows_blk;               // output rows per workgroup (lanes = rows_blk * nq <= 64)
+    int32_t rh;                     // output rows per thread
+    int32_t groups;                 // row groups per wave: 64 / nq
+    int32_t rows_blk;               // output rows per workgroup: rh * groups
     int32_t wm;                     // waves per workgroup, each kWaveM output channels
     int32_t mblk;                   // output channels per workgroup, wm * kWaveM
     int32_t nmb;                    // output-channel blocks
-    int32_t cc;                     // input channels staged per chunk
-    int32_t trows;                  // input rows staged per chunk, (rows_blk-1)*sh + KH
+    int32_t row_tiles;              // ceil(Ho / rows_blk)
+    int32_t tiles;                  // N * row_tiles, rounded up to a multiple of 8 (one per XCD)
+    int32_t chk;                    // input channels staged per chunk
+    int32_t flush_chunks;           // chunks between decodes
+    int32_t trows;                  // staged input rows per chunk, (rows_blk-1)*sh + KH
     int32_t xrw;                    // packed words per input row
     int32_t wrw;                    // packed words per kernel row
-    int32_t lds_tile, lds_spread, lds_raw;  // LDS words of each region
+    int32_t lds_tile, lds_abuf;     // LDS words: output tile, one operand-word buffer
+    int32_t lds_words;              // LDS words in all: tile, two buffers, one spare channel block
+    int32_t lds_qstride;            // LDS words per (channel, q) in a buffer: trows*ntw made odd
+    int64_t kw_words, spread_words; // workspace: kernel-word streams, operand words
     double macs_per_mad, cost;
 };
 
@@ -67,6 +79,7 @@ int plan_conv2d(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, Conv2dGeom 
 int plan_conv1d(int64_t n, samd_fmt xf, const int32_t *taps, int32_t K, samd_fmt kf, Conv1dGeom &g,
                 std::string &err);
 size_t conv2d_workspace_bytes(const Conv2dGeom &g);
+size_t conv2d_kw_bytes(const Conv2dGeom &g);
 
 // Kernel launchers (enqueue only; report launch errors through the return value).
 int launch_pack(const void *src, int64_t rows, int64_t len, int bits, int is_signed, uint32_t *dst,
