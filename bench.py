@@ -4,12 +4,14 @@
 Workload: conv2d 8 x 128 x 56 x 56 -> 128 channels, 3x3, stride 1, pad 1, unsigned b-bit
 activations x signed b-bit weights (seeded synthetic values), swept over b = 1..8.
 
-One step = one pass of the whole hot path at every bit width: pack the int8/uint8
-activations into b-bit words, prepare the layer's kernel words, run the SAMD
-convolution.  `value` is the whole sweep's throughput (all MACs of the 8 layers / time
-of the step) in GMAC/s.  Per bit width the line also reports the convolution kernel's
-own rate (HIP events around it), the native-int8 matrix-core baseline on the same
-layer, their speedup, and the roofline fractions; the CPU oracle is timed on the host.
+One step = one pass of the whole hot path at every bit width: pack the uint8
+activations into b-bit words, spread them into operand words (stage), multiply,
+accumulate, decode and store (accumulate).  Each layer's kernel words are prepared once,
+before timing, as weights are constant.  `value` is the whole sweep's throughput (all
+MACs of the 8 layers / wall time of the step) in GMAC/s.  Per bit width the line also
+reports each kernel's own duration (HIP events around back-to-back launches), the
+native-int8 matrix-core baseline on the same layer, their speedup, and the roofline
+fractions; the CPU oracle is timed on the host.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--bits 1,2,...]
 """
@@ -32,6 +34,7 @@ def parse():
     p.add_argument("--steps", type=int, default=100)
     p.add_argument("--warmup", type=int, default=10)
     p.add_argument("--bits", default="1,2,3,4,5,6,7,8")
+    p.add_argument("--reps", type=int, default=20, help="back-to-back launches per kernel timing")
     p.add_argument("--cpu-seconds", type=float, default=10.0, help="CPU oracle sample budget")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-check", action="store_true", help="skip the sampled parity check")
@@ -56,6 +59,7 @@ def main():
     N, C, H, W, M, KH, KW = shape.N, shape.C, shape.H, shape.W, shape.M, shape.KH, shape.KW
     Ho, Wo = samd.out_hw(shape)
     macs = N * M * Ho * Wo * C * KH * KW
+    samd_hp = H + 2 * shape.pad_h
 
     layers = []
     for b in bits_list:
@@ -71,43 +75,50 @@ def main():
         plan = samd.conv2d_plan(shape, xf, wf)
         layers.append(dict(b=b, case=case, xf=xf, wf=wf, x=x, x_nhwc=x_nhwc, wp=wp, xp=xp, ws=ws, ws8=ws8, plan=plan,
                            y=torch.empty((N, M, Ho, Wo), dtype=torch.int32, device=dev),
-                           y8=torch.empty((N, M, Ho, Wo), dtype=torch.int32, device=dev), ev=[]))
+                           y8=torch.empty((N, M, Ho, Wo), dtype=torch.int32, device=dev)))
     torch.cuda.synchronize()
 
-    def step(record: bool):
+    # the layer's kernel words are prepared once per layer (weights are constant)
+    for L in layers:
+        samd.conv2d_prepare(L["wp"], L["wf"], shape, L["xf"], ws=L["ws"])
+
+    def step():
         for L in layers:
             samd.pack(L["x"], L["b"], False, out=L["xp"])
-            samd.conv2d_prepare(L["wp"], L["wf"], shape, L["xf"], ws=L["ws"])
-            if record:
-                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-                e0.record()
             samd.conv2d_prepared(L["xp"], L["xf"], L["wf"], shape, L["ws"], out=L["y"])
-            if record:
-                e1.record()
-                L["ev"].append((e0, e1))
 
     for _ in range(args.warmup):
-        step(False)
+        step()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
-        step(True)
+        step()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     ms_per_step = (t1 - t0) * 1e3 / args.steps
 
-    # native 8-bit baseline on the same layers, timed the same way
+    # Per-kernel durations: HIP events on the launching stream around REPS back-to-back
+    # launches of one kernel (so the GPU never waits for the host between them).
+    stream = torch.cuda.current_stream()
+
+    def timed(fn, reps):
+        for _ in range(3):
+            fn()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            fn()
+        e1.record(stream)
+        e1.synchronize()
+        return e0.elapsed_time(e1) * 1e-3 / reps
+
     for L in layers:
-        for _ in range(args.warmup):
-            samd.conv2d_int8_prepared(L["x_nhwc"], L["xf"], L["wf"], shape, L["ws8"], out=L["y8"])
-        evs = []
-        for _ in range(args.steps):
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record()
-            samd.conv2d_int8_prepared(L["x_nhwc"], L["xf"], L["wf"], shape, L["ws8"], out=L["y8"])
-            e1.record()
-            evs.append((e0, e1))
-        L["ev8"] = evs
+        samd.conv2d_stage(L["xp"], L["xf"], L["wf"], shape, L["ws"])
+        L["t_conv"] = timed(lambda: samd.conv2d_accumulate(L["xf"], L["wf"], shape, L["ws"], out=L["y"]), args.reps)
+        L["t_stage"] = timed(lambda: samd.conv2d_stage(L["xp"], L["xf"], L["wf"], shape, L["ws"]), args.reps)
+        L["t_pack"] = timed(lambda: samd.pack(L["x"], L["b"], False, out=L["xp"]), args.reps)
+        L["t_int8"] = timed(lambda: samd.conv2d_int8_prepared(L["x_nhwc"], L["xf"], L["wf"], shape, L["ws8"],
+                                                              out=L["y8"]), args.reps)
     torch.cuda.synchronize()
 
     # sampled parity against the oracle, same inputs, both paths
@@ -124,23 +135,29 @@ def main():
 
     per_bits, tot_mads, tot_conv_s = {}, 0.0, 0.0
     for L in layers:
-        t = sum(a.elapsed_time(b) for a, b in L["ev"]) / len(L["ev"]) * 1e-3
-        t8 = sum(a.elapsed_time(b) for a, b in L["ev8"]) / len(L["ev8"]) * 1e-3
+        t, t8 = L["t_conv"], L["t_int8"]
         p = L["plan"]
         mads = N * M * Ho * p.words_per_row * C * KH * p.tap_words
         b = L["b"]
-        hbm_bytes = N * C * H * samd.row_words(W, b) * 4 + M * C * KH * samd.row_words(KW, b) * 4 + N * M * Ho * Wo * 4
+        # operand words and kernel words read once, int32 outputs written once
+        hbm_bytes = (N * C * samd_hp * p.tap_words * p.words_per_row * 4 + M * C * KH * p.tap_words * 4
+                     + N * M * Ho * Wo * 4)
         tot_mads += mads
         tot_conv_s += t
         per_bits[str(b)] = {
-            "conv_us": round(t * 1e6, 2), "gmacs": round(macs / t / 1e9, 1),
+            "conv_us": round(t * 1e6, 2), "stage_us": round(L["t_stage"] * 1e6, 2),
+            "pack_us": round(L["t_pack"] * 1e6, 2),
+            "gmacs": round(macs / t / 1e9, 1),
+            "gmacs_with_stage": round(macs / (t + L["t_stage"]) / 1e9, 1),
             "int8_us": round(t8 * 1e6, 2), "int8_gmacs": round(macs / t8 / 1e9, 1),
-            "speedup_vs_int8": round(t8 / t, 3),
+            "speedup_vs_int8": round(t8 / (t + L["t_stage"]), 3),
             "valu_frac": round(mads / t / PEAK_VALU_OPS, 4),
             "hbm_frac": round(hbm_bytes / t / PEAK_HBM, 4),
             "int8_mfma_frac": round(macs / t8 / PEAK_I8_MACS, 4),
             "lane_bits": p.lane_bits, "lanes": p.lanes, "tap_words": p.tap_words,
             "flush_channels": p.flush_channels, "macs_per_mad": round(p.macs_per_mad, 2),
+            "tile": f"{p.rows_per_block}x{p.mblock}", "split_waves": p.split_waves,
+            "chunk_channels": p.chunk_channels,
             "parity": parity.get(b),
         }
 
@@ -169,7 +186,7 @@ def main():
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "int64", "data": "synthetic",
         "config": {"workload": "conv2d 8x128x56x56 -> 128, 3x3, stride 1, pad 1; unsigned b-bit activations x "
-                               "signed b-bit weights; one step = pack + prepare + SAMD conv at each b",
+                               "signed b-bit weights; one step = pack + stage + accumulate at each b (kernel words prepared once per layer)",
                    "bits": bits_list, "global_batch": N, "macs_per_layer": macs},
         "roofline": {"bound": "alu", "achieved": round(achieved / 1e12, 3), "peak": round(PEAK_VALU_OPS / 1e12, 2),
                      "unit": "TOP/s", "frac": round(achieved / PEAK_VALU_OPS, 4), "traffic": None,

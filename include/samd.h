@@ -72,11 +72,15 @@ enum {
  *   tap_words    kernel words per (input channel, kernel row)
  *   phase[i], tap0[i], ntaps[i] for i < tap_words: kernel word i holds ntaps[i]
  *                consecutive taps of stride phase phase[i], starting at phase tap tap0[i]
+ *   rows_per_block, mblock: output rows and output channels of one workgroup's tile
+ *   split_waves  waves that share one tile's output channels, each multiplying its own
+ *                slice of every chunk of input channels (their sums meet in the tile)
+ *   chunk_channels input channels staged in LDS per chunk
  *   macs_per_mad multiply-accumulates delivered per 32x32->64 multiply (I * taps) */
 typedef struct {
     int32_t lane_bits, lanes, taps_max, words_per_row, flush_channels, out_lanes, tap_words;
     int32_t phase[16], tap0[16], ntaps[16];
-    int32_t rows_per_block, mblock;
+    int32_t rows_per_block, mblock, split_waves, chunk_channels;
     double macs_per_mad;
 } samd_conv2d_plan;
 
@@ -161,6 +165,20 @@ int samd_conv2d_prepare(const uint32_t *w, samd_fmt wf, const samd_conv2d_desc *
                         size_t ws_bytes, hipStream_t stream);
 int samd_conv2d_prepared(const uint32_t *x, samd_fmt xf, samd_fmt wf, const samd_conv2d_desc *d, int32_t *y,
                          const void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* samd_conv2d_prepared split once more, into its operand staging and its arithmetic:
+ * samd_conv2d_stage spreads x (packed rows) into operand words in ws - I values of one
+ * stride phase per 32-bit word, L bits apart (temporary spacers, Sec. 2.2), signed values
+ * sign-extended (Sec. 6) - for every padded input row; samd_conv2d_accumulate multiplies
+ * them with the prepared kernel words, accumulates the 64-bit products over input
+ * channels (Sec. 5), decodes the lanes with the fix-up of Sec. 6, overlap-adds partial
+ * lanes of neighbouring words and stores y (NCHW int32).  stage + accumulate is
+ * samd_conv2d_prepared; the staged operand words stay valid until the next stage call
+ * on the same workspace, so one staged input can be accumulated several times. */
+int samd_conv2d_stage(const uint32_t *x, samd_fmt xf, samd_fmt wf, const samd_conv2d_desc *d, void *ws,
+                      size_t ws_bytes, hipStream_t stream);
+int samd_conv2d_accumulate(samd_fmt xf, samd_fmt wf, const samd_conv2d_desc *d, int32_t *y, const void *ws,
+                           size_t ws_bytes, hipStream_t stream);
 
 /* Workspace bytes samd_conv2d_int8 needs (reordered int8 weights and per-filter sums). */
 int samd_conv2d_int8_workspace(const samd_conv2d_desc *d, samd_fmt xf, size_t *bytes);

@@ -17,6 +17,7 @@ import torch
 
 __all__ = ["Fmt", "Conv2dDesc", "Conv1dPlan", "Conv2dPlan", "SamdError", "lib", "row_words", "pack", "unpack", "conv1d",
            "conv1d_plan", "conv2d_plan", "conv2d_workspace", "conv2d", "conv2d_prepare", "conv2d_prepared",
+           "conv2d_stage", "conv2d_accumulate",
            "conv2d_int8_prepare", "conv2d_int8_prepared", "conv2d_int8_workspace", "conv2d_int8", "max_i32",
            "relu_requant_pack", "relu_requant_nhwc_u8", "out_hw", "LIB_PATH"]
 
@@ -52,7 +53,7 @@ class Conv2dPlan(ctypes.Structure):
                 ("words_per_row", ctypes.c_int32), ("flush_channels", ctypes.c_int32),
                 ("out_lanes", ctypes.c_int32), ("tap_words", ctypes.c_int32), ("phase", ctypes.c_int32 * 16), ("tap0", ctypes.c_int32 * 16),
                 ("ntaps", ctypes.c_int32 * 16), ("rows_per_block", ctypes.c_int32), ("mblock", ctypes.c_int32),
-                ("macs_per_mad", ctypes.c_double)]
+                ("split_waves", ctypes.c_int32), ("chunk_channels", ctypes.c_int32), ("macs_per_mad", ctypes.c_double)]
 
 
 class Conv1dPlan(ctypes.Structure):
@@ -92,6 +93,8 @@ def lib():
             "samd_conv2d": (ctypes.c_int, [_p, Fmt, _p, Fmt, ctypes.POINTER(Conv2dDesc), _p, _p, _sz, _p]),
             "samd_conv2d_prepare": (ctypes.c_int, [_p, Fmt, ctypes.POINTER(Conv2dDesc), Fmt, _p, _sz, _p]),
             "samd_conv2d_prepared": (ctypes.c_int, [_p, Fmt, Fmt, ctypes.POINTER(Conv2dDesc), _p, _p, _sz, _p]),
+            "samd_conv2d_stage": (ctypes.c_int, [_p, Fmt, Fmt, ctypes.POINTER(Conv2dDesc), _p, _sz, _p]),
+            "samd_conv2d_accumulate": (ctypes.c_int, [Fmt, Fmt, ctypes.POINTER(Conv2dDesc), _p, _p, _sz, _p]),
             "samd_conv2d_int8_prepare": (ctypes.c_int, [_p, Fmt, ctypes.POINTER(Conv2dDesc), Fmt, _p, _sz, _p]),
             "samd_conv2d_int8_prepared": (ctypes.c_int, [_p, Fmt, Fmt, ctypes.POINTER(Conv2dDesc), _p, _p, _sz,
                                                          _p]),
@@ -125,6 +128,13 @@ def _dev(t: torch.Tensor, dtype=None, name="tensor") -> torch.Tensor:
         raise ValueError(f"{name} must have dtype {dtype}, got {t.dtype}")
     if not t.is_contiguous():
         raise ValueError(f"{name} must be contiguous")
+    return t
+
+
+def _out(t: torch.Tensor, numel: int) -> torch.Tensor:
+    _dev(t, torch.int32, "out")
+    if t.numel() != numel:
+        raise ValueError(f"out must hold {numel} int32 values, got {t.numel()}")
     return t
 
 
@@ -172,6 +182,7 @@ def conv1d(xp: torch.Tensor, n: int, bits: int, taps: Sequence[int], kbits: int,
     arr = (ctypes.c_int32 * K)(*[int(t) for t in taps])
     if out is None:
         out = torch.empty(max(n - K + 1, 0), dtype=torch.int32, device=xp.device)
+    _out(out, max(n - K + 1, 0))
     _check(lib().samd_conv1d(xp.data_ptr(), n, Fmt(bits, False), arr, K, Fmt(kbits, False), out.data_ptr(),
                              _stream(xp)))
     return out
@@ -214,6 +225,7 @@ def conv2d(xp: torch.Tensor, xfmt: Fmt, wp: torch.Tensor, wfmt: Fmt, shape, ws: 
         ws = _workspace(conv2d_workspace(shape, xfmt, wfmt), xp.device)
     if out is None:
         out = torch.empty((d.N, d.M, Ho, Wo), dtype=torch.int32, device=xp.device)
+    _out(out, d.N * d.M * Ho * Wo)
     _check(lib().samd_conv2d(xp.data_ptr(), xfmt, wp.data_ptr(), wfmt, ctypes.byref(d), out.data_ptr(),
                              ws.data_ptr(), ws.numel(), _stream(xp)))
     return out
@@ -236,8 +248,32 @@ def conv2d_prepared(xp: torch.Tensor, xfmt: Fmt, wfmt: Fmt, shape, ws: torch.Ten
     Ho, Wo = out_hw(shape)
     if out is None:
         out = torch.empty((d.N, d.M, Ho, Wo), dtype=torch.int32, device=xp.device)
+    _out(out, d.N * d.M * Ho * Wo)
     _check(lib().samd_conv2d_prepared(xp.data_ptr(), xfmt, wfmt, ctypes.byref(d), out.data_ptr(), ws.data_ptr(),
                                       ws.numel(), _stream(xp)))
+    return out
+
+
+def conv2d_stage(xp: torch.Tensor, xfmt: Fmt, wfmt: Fmt, shape, ws: torch.Tensor) -> torch.Tensor:
+    """Spread the packed input into the workspace's operand words (first half of conv2d_prepared)."""
+    _dev(xp, torch.int32, "xp")
+    _dev(ws, torch.uint8, "ws")
+    _check(lib().samd_conv2d_stage(xp.data_ptr(), xfmt, wfmt, ctypes.byref(Conv2dDesc.of(shape)), ws.data_ptr(),
+                                   ws.numel(), _stream(xp)))
+    return ws
+
+
+def conv2d_accumulate(xfmt: Fmt, wfmt: Fmt, shape, ws: torch.Tensor,
+                      out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Multiply, accumulate, decode and store from a prepared and staged workspace."""
+    _dev(ws, torch.uint8, "ws")
+    d = Conv2dDesc.of(shape)
+    Ho, Wo = out_hw(shape)
+    if out is None:
+        out = torch.empty((d.N, d.M, Ho, Wo), dtype=torch.int32, device=ws.device)
+    _out(out, d.N * d.M * Ho * Wo)
+    _check(lib().samd_conv2d_accumulate(xfmt, wfmt, ctypes.byref(d), out.data_ptr(), ws.data_ptr(), ws.numel(),
+                                        _stream(ws)))
     return out
 
 
@@ -257,6 +293,7 @@ def conv2d_int8_prepared(x_nhwc: torch.Tensor, xfmt: Fmt, wfmt: Fmt, shape, ws: 
     Ho, Wo = out_hw(shape)
     if out is None:
         out = torch.empty((d.N, d.M, Ho, Wo), dtype=torch.int32, device=x_nhwc.device)
+    _out(out, d.N * d.M * Ho * Wo)
     _check(lib().samd_conv2d_int8_prepared(x_nhwc.data_ptr(), xfmt, wfmt, ctypes.byref(d), out.data_ptr(),
                                            ws.data_ptr(), ws.numel(), _stream(x_nhwc)))
     return out
@@ -279,6 +316,7 @@ def conv2d_int8(x_nhwc: torch.Tensor, xfmt: Fmt, w: torch.Tensor, wfmt: Fmt, sha
         ws = _workspace(conv2d_int8_workspace(shape, xfmt), x_nhwc.device)
     if out is None:
         out = torch.empty((d.N, d.M, Ho, Wo), dtype=torch.int32, device=x_nhwc.device)
+    _out(out, d.N * d.M * Ho * Wo)
     _check(lib().samd_conv2d_int8(x_nhwc.data_ptr(), xfmt, w.data_ptr(), wfmt, ctypes.byref(d), out.data_ptr(),
                                   ws.data_ptr(), ws.numel(), _stream(x_nhwc)))
     return out

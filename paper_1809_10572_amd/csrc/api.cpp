@@ -202,6 +202,8 @@ int samd_conv2d_plan_query(const samd_conv2d_desc *d, samd_fmt xf, samd_fmt wf, 
     }
     out->rows_per_block = g.rows_blk;
     out->mblock = g.mblk;
+    out->split_waves = g.ks;
+    out->chunk_channels = g.chk;
     out->macs_per_mad = g.macs_per_mad;
     return SAMD_OK;
 }
@@ -268,6 +270,28 @@ int samd_conv2d_prepared(const uint32_t *x, samd_fmt xf, samd_fmt wf, const samd
     if (!x || !y) return fail(SAMD_EINVAL, "x and y must not be NULL");
     if (!aligned4(x) || !aligned4(y)) return fail(SAMD_EALIGN, "x / y not aligned");
     return launch_conv2d_samd(x, g, y, ws, stream);
+}
+
+int samd_conv2d_stage(const uint32_t *x, samd_fmt xf, samd_fmt wf, const samd_conv2d_desc *d, void *ws,
+                      size_t ws_bytes, hipStream_t stream) {
+    set_error("");
+    Conv2dGeom g;
+    int st = conv2d_setup(xf, wf, d, ws, ws_bytes, g);
+    if (st) return st;
+    if (!x) return fail(SAMD_EINVAL, "x must not be NULL");
+    if (!aligned4(x)) return fail(SAMD_EALIGN, "x not aligned");
+    return launch_conv2d_spread(x, g, ws, stream);
+}
+
+int samd_conv2d_accumulate(samd_fmt xf, samd_fmt wf, const samd_conv2d_desc *d, int32_t *y, const void *ws,
+                           size_t ws_bytes, hipStream_t stream) {
+    set_error("");
+    Conv2dGeom g;
+    int st = conv2d_setup(xf, wf, d, ws, ws_bytes, g);
+    if (st) return st;
+    if (!y) return fail(SAMD_EINVAL, "y must not be NULL");
+    if (!aligned4(y)) return fail(SAMD_EALIGN, "y not aligned");
+    return launch_conv2d_multiply(g, y, ws, stream);
 }
 
 int samd_conv2d(const uint32_t *x, samd_fmt xf, const uint32_t *w, samd_fmt wf, const samd_conv2d_desc *d,

@@ -93,13 +93,18 @@ __global__ __launch_bounds__(256) void spread_kernel(const uint32_t *__restrict_
 // stays one v_mad_i64_i32 into its accumulator.
 __device__ __forceinline__ void keep(int64_t &acc) { asm volatile("" : "+v"(acc)); }
 
+// A workgroup has wm x ks waves.  Wave (kq, mw) owns output channels mw*8 .. +7 of the
+// block and multiplies slice kq (cpw channels) of every chunk; the ks waves of one
+// output-channel group add their decoded partial sums into the same LDS tile, whose
+// atomic adds are also the overlap-add of neighbouring words' partial lanes.
+//
 // NRT: steps (kernel row x kernel word) per input channel when it is 3 or 6 (every 3x3
 // layer), so batches never straddle channels and all LDS offsets are immediates; 0 for
 // any other count.
 template <int RH, int NRT>
-__global__ __launch_bounds__(256) void conv2d_samd_kernel(const int32_t *__restrict__ xs,
-                                                          const int32_t *__restrict__ kw, int32_t *__restrict__ y,
-                                                          const Conv2dGeom g) {
+__global__ __launch_bounds__(1024) void conv2d_samd_kernel(const int32_t *__restrict__ xs,
+                                                           const int32_t *__restrict__ kw, int32_t *__restrict__ y,
+                                                           const Conv2dGeom g) {
     extern __shared__ int32_t lds[];
     int32_t *tile = lds;
     int32_t *abuf0 = lds + g.lds_tile;
@@ -116,14 +121,16 @@ __global__ __launch_bounds__(256) void conv2d_samd_kernel(const int32_t *__restr
     const int ho0 = (tile_id % g.row_tiles) * g.rows_blk;
 
     const int tid = threadIdx.x;
-    const int nthr = g.wm * 64;
+    const int nthr = g.wm * g.ks * 64;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int kq = wave / g.wm;
+    const int mw = wave - kq * g.wm;
     const int lane = tid & 63;
     const int grp_raw = lane / g.nq;
     const bool lane_ok = grp_raw < g.groups;
     const int grp = lane_ok ? grp_raw : 0;
     const int q = lane_ok ? lane - grp_raw * g.nq : 0;
-    const int wb = mb * g.wm + wave;
+    const int wb = mb * g.wm + mw;
 
     for (int i = tid; i < g.lds_tile; i += nthr) tile[i] = 0;
 
@@ -138,8 +145,7 @@ __global__ __launch_bounds__(256) void conv2d_samd_kernel(const int32_t *__restr
     const int32_t *xs_tile = xs + ((int64_t)n * g.C * g.Hp + ho0 * g.sh) * g.ntw * g.nq;
     // Thread element j of a chunk: global word i of channel cc (global order [tr][t][q]);
     // the same (cc, i) in every chunk, so offsets are computed once.
-    int e_cc[kPrefetch], e_lds[kPrefetch];
-    int64_t e_off[kPrefetch];
+    int e_cc[kPrefetch], e_lds[kPrefetch], e_off[kPrefetch];
     bool e_row[kPrefetch];
     const int chunk_words = g.chk * gblk;
 #pragma unroll
@@ -148,7 +154,7 @@ __global__ __launch_bounds__(256) void conv2d_samd_kernel(const int32_t *__restr
         const int cc = e / gblk, i = e - cc * gblk;
         const int qq = i % g.nq, rt = i / g.nq;
         e_cc[j] = e < chunk_words ? cc : 1 << 30;
-        e_off[j] = cc * ch_stride + i;
+        e_off[j] = (int)(cc * ch_stride) + i;
         e_lds[j] = cc * cs + qq * qs + rt;
         e_row[j] = i < in_words;
     }
@@ -180,40 +186,48 @@ __global__ __launch_bounds__(256) void conv2d_samd_kernel(const int32_t *__restr
     const int64_t stream_len = ((int64_t)g.C * g.nrt + kStreamPad) * RM;
     const int32_t *kstream = kw + wb * stream_len;
     // LDS word offset of each of the thread's rows within a channel (rows past the tile
-    // reuse the last one; their results are never decoded)
+    // reuse the last one; their results are never stored)
     int rowoff[RH];
 #pragma unroll
     for (int r = 0; r < RH; ++r) rowoff[r] = q * qs + min(grp * RH + r, g.rows_blk - 1) * g.sh * g.ntw;
+    const int cw0 = kq * g.cpw;   // first channel of this wave's slice of a chunk
 
+    // Decode: fix-up (signed results), then lane j of word q goes to output column
+    // q*I + j - (Kmax-1), stored at tile column q*I + j; the top lane takes the bits left.
+    // Tile rows cover every row a wave computes, so no lane needs a bounds check.
+    int32_t *const tbase = tile + ((mw * RM) * g.tile_rows + grp * RH) * g.tile_row + q * g.I;
+    const int mstride = g.tile_rows * g.tile_row;
     auto decode = [&]() {
-        const int obase = q * g.I - g.Kmax + 1;
+        if (lane_ok) {
 #pragma unroll
-        for (int r = 0; r < RH; ++r) {
-            const int rloc = grp * RH + r;
-            const bool ok = lane_ok && rloc < g.rows_blk && ho0 + rloc < g.Ho;
+            for (int r = 0; r < RH; ++r) {
 #pragma unroll
-            for (int m = 0; m < RM; ++m) {
-                uint64_t v = (uint64_t)acc[r][m];
-                acc[r][m] = 0;
-                if (g.result_signed) {
-                    const uint64_t s = v & g.msb_mask;
-                    v = (v + s) ^ s;
-                }
-                int32_t *trow = tile + ((wave * RM + m) * g.rows_blk + (ok ? rloc : 0)) * g.Wo;
-                for (int j = 0; j < g.nl; ++j) {
-                    int32_t d;
-                    if (j < g.nl - 1) {
-                        const uint32_t w32 = (uint32_t)(v >> (j * g.L));
-                        d = g.result_signed ? ((int32_t)(w32 << (32 - g.L)) >> (32 - g.L))
-                                            : (int32_t)(w32 & ((1u << g.L) - 1));
-                    } else {
-                        d = g.result_signed ? (int32_t)((int64_t)v >> (j * g.L)) : (int32_t)(v >> (j * g.L));
+                for (int m = 0; m < RM; ++m) {
+                    uint64_t v = (uint64_t)acc[r][m];
+                    if (g.result_signed) {
+                        const uint64_t s = v & g.msb_mask;
+                        v = (v + s) ^ s;
                     }
-                    const int o = obase + j;
-                    if (ok && o >= 0 && o < g.Wo) atomicAdd(&trow[o], d);
+                    int32_t *pm = tbase + r * g.tile_row + m * mstride;
+                    // lanes from the bottom: extract the low L bits, then shift them out
+#pragma unroll
+                    for (int j = 0; j < kMaxOutLanes - 1; ++j) {
+                        if (j >= g.nl - 1) break;
+                        const uint32_t w32 = (uint32_t)v;
+                        const int32_t d = g.result_signed ? ((int32_t)(w32 << (32 - g.L)) >> (32 - g.L))
+                                                          : (int32_t)(w32 & ((1u << g.L) - 1));
+                        atomicAdd(pm + j, d);
+                        v = g.result_signed ? (uint64_t)((int64_t)v >> g.L) : v >> g.L;
+                    }
+                    const int32_t top = (int32_t)v;
+                    atomicAdd(pm + (g.nl - 1), top);
                 }
             }
         }
+#pragma unroll
+        for (int r = 0; r < RH; ++r)
+#pragma unroll
+            for (int m = 0; m < RM; ++m) acc[r][m] = 0;
     };
 
     for (int k = 0; k < nchunks; ++k) {
@@ -230,12 +244,14 @@ __global__ __launch_bounds__(256) void conv2d_samd_kernel(const int32_t *__restr
 #pragma unroll
         for (int j = 0; j < kPrefetch; ++j) pre[j] = (e_cc[j] < ncc1 && e_row[j]) ? src1[e_off[j]] : 0;
 
-        // Batches of kStepBatch steps: kernel words in SGPRs, operand words from LDS.  With
-        // 3 or 6 steps per channel a chunk is a whole number of batches, and a partial last
-        // batch can only end the last chunk, where it runs on the stream's zero padding.
-        const int nsteps = ncc * g.nrt;
+        // This wave's slice: channels cw0 .. cw0 + nch - 1 of the chunk, in batches of
+        // kStepBatch steps: kernel words in SGPRs, operand words from LDS.  With 3 or 6
+        // steps per channel a slice is a whole number of batches.
+        const int nch = min(max(ncc - cw0, 0), g.cpw);
+        const int nsteps = nch * g.nrt;
         const int nbat = (nsteps + kStepBatch - 1) / kStepBatch;
-        const int32_t *ks = kstream + (int64_t)c0 * g.nrt * RM;
+        const int32_t *ks = kstream + (int64_t)(c0 + cw0) * g.nrt * RM;
+        const int32_t *wcur = cur + cw0 * cs;
         int32_t kA[kStepBatch * RM], aA[kStepBatch][RH], kB[kStepBatch * RM], aB[kStepBatch][RH];
         int gs = 0;   // generic layout: step index of the next batch to load
         auto load_batch = [&](int b, int32_t (&kb)[kStepBatch * RM], int32_t (&ab)[kStepBatch][RH]) {
@@ -247,21 +263,21 @@ __global__ __launch_bounds__(256) void conv2d_samd_kernel(const int32_t *__restr
                 const int base = (b / BPC) * cs + (b % BPC) * kStepBatch;
 #pragma unroll
                 for (int r = 0; r < RH; ++r) {
-                    const int32_t *src = cur + base + rowoff[r];
+                    const int32_t *src = wcur + base + rowoff[r];
 #pragma unroll
                     for (int j = 0; j < kStepBatch; ++j) ab[j][r] = src[j];
                 }
             } else {
 #pragma unroll
                 for (int j = 0; j < kStepBatch; ++j) {
-                    // steps past the chunk (its step count need not be a multiple of the
-                    // batch) multiply the next chunk's kernel words: their operand is 0
+                    // steps past the slice (its step count need not be a multiple of the
+                    // batch) multiply the following channel's kernel words: their operand is 0
                     const bool live = gs + j < nsteps;
                     const int st = min(gs + j, nsteps - 1);
                     const int cc = st / g.nrt, rt = st - cc * g.nrt;
 #pragma unroll
                     for (int r = 0; r < RH; ++r) {
-                        const int32_t v = cur[cc * cs + rt + rowoff[r]];
+                        const int32_t v = wcur[cc * cs + rt + rowoff[r]];
                         ab[j][r] = live ? v : 0;
                     }
                 }
@@ -285,22 +301,29 @@ __global__ __launch_bounds__(256) void conv2d_samd_kernel(const int32_t *__restr
         // outstanding scalar and LDS loads are waited for, and only then is the next batch
         // requested: scalar loads return out of order, so a wait placed after requesting
         // the next batch would wait for it too.
-        // The batch after the last one is fetched too (its results are never used): the
-        // kernel-word stream ends in kStreamPad padding steps and the LDS buffers are
-        // followed by one spare channel block, so it reads padding.
-        load_batch(0, kA, aA);
-        for (int b = 0; b < nbat; b += 2) {
-            __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0)
-            load_batch(b + 1, kB, aB);
-            __builtin_amdgcn_sched_barrier(0);
-            mac_batch(kA, aA);
-            __builtin_amdgcn_sched_barrier(0);
-            if (b + 1 >= nbat) break;
-            __builtin_amdgcn_s_waitcnt(0xc07f);
-            load_batch(b + 2, kA, aA);
-            __builtin_amdgcn_sched_barrier(0);
-            mac_batch(kB, aB);
-            __builtin_amdgcn_sched_barrier(0);
+        // The batch after the slice's last one is fetched too (its results are never
+        // used): it reads the next slice's channel, or for the last slice the spare
+        // channel block after the LDS buffers and the kStreamPad padding steps of the
+        // kernel-word stream.
+        if (nbat > 0) {
+            load_batch(0, kA, aA);
+            int b = 0;
+            for (; b + 1 < nbat; b += 2) {
+                __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0)
+                load_batch(b + 1, kB, aB);
+                __builtin_amdgcn_sched_barrier(0);
+                mac_batch(kA, aA);
+                __builtin_amdgcn_sched_barrier(0);
+                __builtin_amdgcn_s_waitcnt(0xc07f);
+                load_batch(b + 2, kA, aA);
+                __builtin_amdgcn_sched_barrier(0);
+                mac_batch(kB, aB);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+            if (b < nbat) {   // odd batch count: the last batch
+                __builtin_amdgcn_s_waitcnt(0xc07f);
+                mac_batch(kA, aA);
+            }
         }
 
         // the next chunk's operand words into the other buffer (last read a chunk ago,
@@ -314,14 +337,15 @@ __global__ __launch_bounds__(256) void conv2d_samd_kernel(const int32_t *__restr
         __syncthreads();
     }
 
-    // output tile -> y, whole rows
-    const int tile_n = g.mblk * g.rows_blk * g.Wo;
-    for (int i = tid; i < tile_n; i += nthr) {
-        const int o = i % g.Wo;
-        const int t = i / g.Wo;
-        const int r = t % g.rows_blk, mm = t / g.rows_blk;
+    // output tile -> y, one row per wave at a time
+    const int nwaves = g.wm * g.ks;
+    for (int rr = wave; rr < g.mblk * g.rows_blk; rr += nwaves) {
+        const int mm = rr / g.rows_blk, r = rr - mm * g.rows_blk;
         const int m = mb * g.mblk + mm, ho = ho0 + r;
-        if (m < g.M && ho < g.Ho) y[(((int64_t)n * g.M + m) * g.Ho + ho) * g.Wo + o] = tile[i];
+        if (m >= g.M || ho >= g.Ho) continue;
+        const int32_t *src = tile + (mm * g.tile_rows + r) * g.tile_row + (g.Kmax - 1);
+        int32_t *dst = y + (((int64_t)n * g.M + m) * g.Ho + ho) * g.Wo;
+        for (int o = lane; o < g.Wo; o += 64) dst[o] = src[o];
     }
 }
 
@@ -341,9 +365,8 @@ int launch_conv2d_prepare(const uint32_t *w, const Conv2dGeom &g, void *ws, hipS
     return check_launch("conv2d weight preparation");
 }
 
-int launch_conv2d_samd(const uint32_t *x, const Conv2dGeom &g, int32_t *y, const void *ws, hipStream_t s) {
-    const int32_t *kw = (const int32_t *)ws;
-    int32_t *xs = (int32_t *)((char *)const_cast<void *>(ws) + conv2d_kw_bytes(g));
+int launch_conv2d_spread(const uint32_t *x, const Conv2dGeom &g, void *ws, hipStream_t s) {
+    int32_t *xs = (int32_t *)((char *)ws + conv2d_kw_bytes(g));
     const int sgrid = grid_for(g.spread_words, 256);
     bool launched = false;
 #define SAMD_SPREAD_CASE(B, SG)                                                                            \
@@ -353,9 +376,13 @@ int launch_conv2d_samd(const uint32_t *x, const Conv2dGeom &g, int32_t *y, const
     }
     SAMD_FOR_EACH_FMT(SAMD_SPREAD_CASE)
 #undef SAMD_SPREAD_CASE
-    int st = check_launch("conv2d operand spread");
-    if (st) return st;
-    const dim3 grid((unsigned)g.tiles * g.nmb), block(g.wm * 64);
+    return check_launch("conv2d operand spread");
+}
+
+int launch_conv2d_multiply(const Conv2dGeom &g, int32_t *y, const void *ws, hipStream_t s) {
+    const int32_t *kw = (const int32_t *)ws;
+    const int32_t *xs = (const int32_t *)((const char *)ws + conv2d_kw_bytes(g));
+    const dim3 grid((unsigned)g.tiles * g.nmb), block(g.wm * g.ks * 64);
     const size_t shm = (size_t)g.lds_words * 4;
 #define SAMD_CONV_CASE(RH_, NRT_)                                                                     \
     if (g.rh == RH_ && (NRT_ == 0 ? (g.nrt != 3 && g.nrt != 6) : g.nrt == NRT_)) {                     \
@@ -367,6 +394,12 @@ int launch_conv2d_samd(const uint32_t *x, const Conv2dGeom &g, int32_t *y, const
 #undef SAMD_CONV_CASE
     set_error("conv2d: no kernel for this geometry");
     return SAMD_EUNSUPPORTED;
+}
+
+int launch_conv2d_samd(const uint32_t *x, const Conv2dGeom &g, int32_t *y, const void *ws, hipStream_t s) {
+    const int st = launch_conv2d_spread(x, g, const_cast<void *>(ws), s);
+    if (st) return st;
+    return launch_conv2d_multiply(g, y, ws, s);
 }
 
 }  // namespace samd

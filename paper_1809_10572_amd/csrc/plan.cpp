@@ -10,7 +10,10 @@
 #include <algorithm>
 #include <cmath>
 #include <cstdio>
+#include <array>
 #include <limits>
+#include <map>
+#include <mutex>
 
 #include "samd_internal.hpp"
 
@@ -62,20 +65,99 @@ bool split_taps(int count, int kmax, int *t0, int *nt, int &ngroups) {
     return true;
 }
 
-int pick_waves_m(int M) {
-    int best = 1;
-    long best_pad = std::numeric_limits<long>::max();
-    for (int wm : {4, 2, 1}) {
-        long blk = (long)wm * kWaveM;
-        long pad = (M + blk - 1) / blk * blk - M;
-        if (pad < best_pad) { best_pad = pad; best = wm; }
+// Launch shape of one lane geometry: output rows per thread (rh), row groups per wave,
+// output-channel waves (wm) and channel-split waves (ks) per workgroup, channels per
+// chunk.  Every candidate is priced in VALU issue cycles of the busiest SIMD: the
+// multiply-adds, decodes and staging of the workgroups one compute unit runs, divided by
+// an issue efficiency that grows with the waves resident per SIMD (latency hiding), plus
+// the operand-spread pass.  Returns false when nothing fits the LDS.
+bool place_launch(const samd_conv2d_desc &d, Conv2dGeom &c) {
+    const int grp_max = 64 / c.nq;
+    bool found = false;
+    Conv2dGeom best = c;
+    best.cost = 1e300;
+    for (int rh = 1; rh <= 2; ++rh) {
+        if (rh == 2 && c.Ho < 2) continue;
+        for (int gr = grp_max; gr >= 1; --gr) {
+            for (int wm : {1, 2, 4}) {
+                for (int ks : {1, 2, 4, 8, 16}) {
+                    if (wm * ks > kMaxBlockWaves) continue;
+                    Conv2dGeom t = c;
+                    t.rh = rh;
+                    t.groups = gr;
+                    t.rows_blk = std::min(rh * gr, c.Ho);
+                    t.trows = (t.rows_blk - 1) * d.stride_h + d.KH;
+                    t.wm = wm;
+                    t.ks = ks;
+                    t.mblk = wm * kWaveM;
+                    t.nmb = (d.M + t.mblk - 1) / t.mblk;
+                    t.tile_rows = gr * rh;
+                    t.tile_row = c.nq * c.I + c.Kmax - 1;
+                    t.lds_tile = t.mblk * t.tile_rows * t.tile_row;
+                    t.lds_qstride = (t.trows * c.ntw) | 1;
+                    const int threads = wm * ks * 64;
+                    // largest chunk whose LDS fits; a slice per wave of at most G channels
+                    const int cpw_hi = std::min(std::min(kMaxChunkPerWave, c.G), (d.C + ks - 1) / ks);
+                    bool placed = false;
+                    for (t.cpw = cpw_hi; t.cpw >= 1; --t.cpw) {
+                        t.chk = t.cpw * ks;
+                        if (t.chk > kMaxChunk && t.cpw > 1) continue;
+                        t.lds_abuf = t.chk * c.nq * t.lds_qstride;
+                        // a spare channel block after the buffers: the batch after a wave's last
+                        // one is fetched as well and may read there
+                        t.lds_words = t.lds_tile + 2 * t.lds_abuf + c.nq * t.lds_qstride + kStepBatch;
+                        if ((long)t.lds_words * 4 <= kMaxLdsBytes) {
+                            placed = true;
+                            break;
+                        }
+                    }
+                    if (!placed) continue;
+                    t.row_tiles = (c.Ho + t.rows_blk - 1) / t.rows_blk;
+                    t.tiles = (d.N * t.row_tiles + 7) / 8 * 8;
+                    t.flush_chunks = c.G / t.cpw;
+                    t.kw_words = (int64_t)t.nmb * wm * ((int64_t)d.C * c.nrt + kStreamPad) * kWaveM;
+                    t.spread_words = (int64_t)d.N * d.C * c.Hp * c.ntw * c.nq;
+
+                    const double nchunks = std::ceil((double)d.C / t.chk);
+                    const double nflush = std::ceil(nchunks / t.flush_chunks);
+                    const double staged = (double)t.chk * t.trows * c.ntw * c.nq;
+                    // wave-instructions of one workgroup
+                    double mads = (double)wm * kWaveM * rh * d.C * c.nrt * 1.08;
+                    double decode = (double)wm * ks * nflush * kWaveM * rh *
+                                    ((c.result_signed ? 5.0 : 0.0) + 1.0 + 2.0 * c.nl);
+                    double staging = nchunks * std::ceil(staged / threads) * wm * ks * 4.0;
+                    double tile = (double)t.lds_tile / 64.0 * 3.0;
+                    double wg = mads + decode + staging + tile;
+                    // residency: LDS, and at most 8 waves per SIMD
+                    const double wgs = (double)t.tiles * t.nmb;
+                    const double per_cu = std::ceil(wgs / 256.0);
+                    const double res = std::max(1.0, std::min(std::floor(163840.0 / (t.lds_words * 4.0)),
+                                                              std::floor(32.0 / (wm * ks))));
+                    const double occ = std::min(per_cu, res) * wm * ks / 4.0;
+                    const double eff = occ / (occ + 0.7);
+                    const double spread = (double)t.spread_words * (6.0 * c.I + 4.0) / 64.0 / 1024.0;
+                    t.cost = per_cu * wg / 4.0 / eff + spread;
+                    if (t.cost < best.cost) {
+                        best = t;
+                        found = true;
+                    }
+                }
+            }
+        }
     }
-    return best;
+    if (found) {
+        const double keep = c.macs_per_mad;
+        c = best;
+        c.macs_per_mad = keep;
+    }
+    return found;
 }
 
 }  // namespace
 
-int plan_conv2d(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, Conv2dGeom &best, std::string &err) {
+namespace {
+
+int search_conv2d(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, Conv2dGeom &best, std::string &err) {
     Conv2dGeom g = {};
     g.N = d.N; g.C = d.C; g.H = d.H; g.W = d.W; g.M = d.M; g.KH = d.KH; g.KW = d.KW;
     g.sh = d.stride_h; g.sw = d.stride_w; g.ph = d.pad_h; g.pw = d.pad_w;
@@ -85,9 +167,6 @@ int plan_conv2d(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, Conv2dGeom 
     g.result_signed = (xf.is_signed || wf.is_signed) ? 1 : 0;
     g.xrw = (int32_t)row_words(d.W, xf.bits);
     g.wrw = (int32_t)row_words(d.KW, wf.bits);
-    g.wm = pick_waves_m(d.M);
-    g.mblk = g.wm * kWaveM;
-    g.nmb = (d.M + g.mblk - 1) / g.mblk;
 
     const int S = d.stride_w;
     g.Kmax = (d.KW + S - 1) / S;
@@ -158,56 +237,11 @@ int plan_conv2d(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, Conv2dGeom 
             if (c.nq > 64) continue;
             c.nrt = d.KH * c.ntw;
             c.Hp = d.H + 2 * d.pad_h;
-            // Two output rows per thread halve the waves: keep them while the grid still
-            // gives every SIMD (1024 of them) more than one wave.  Then the largest tile
-            // (row groups per wave) whose LDS fits.
-            bool placed = false;
-            const int grp_max = 64 / c.nq;
-            int rh_pref[2] = {1, 1};
-            {
-                int rows2 = std::min(2 * grp_max, c.Ho);
-                long tiles2 = (long)d.N * ((c.Ho + rows2 - 1) / rows2);
-                if (tiles2 * c.nmb * c.wm >= 1536 && c.Ho >= 2) rh_pref[0] = 2;
-            }
-            for (int pi = 0; pi < 2 && !placed; ++pi) {
-                c.rh = rh_pref[pi];
-                for (int gr = grp_max; gr >= 1 && !placed; --gr) {
-                    c.groups = gr;
-                    c.rows_blk = std::min(c.rh * c.groups, c.Ho);
-                    c.trows = (c.rows_blk - 1) * d.stride_h + d.KH;
-                    c.lds_tile = c.mblk * c.rows_blk * c.Wo;
-                    c.lds_qstride = (c.trows * c.ntw) | 1;
-                    // prefer chunks every thread stages from registers (kStagePerThread words)
-                    for (c.chk = std::min(std::min(d.C, kMaxChunk), c.G); c.chk >= 1; --c.chk) {
-                        long staged = (long)c.chk * c.trows * c.ntw * c.nq;
-                        c.lds_abuf = c.chk * c.nq * c.lds_qstride;
-                        // a spare channel block after the buffers: the batch after the last one
-                        // of a chunk is fetched as well and reads there
-                        c.lds_words = c.lds_tile + 2 * c.lds_abuf + c.nq * c.lds_qstride + kStepBatch;
-                        if ((long)c.lds_words * 4 > 65536) continue;
-                        if (staged <= kStagePerThread * c.wm * 64 || c.chk == 1) {
-                            placed = true;
-                            break;
-                        }
-                    }
-                }
-            }
-            if (!placed) continue;
-            c.row_tiles = (c.Ho + c.rows_blk - 1) / c.rows_blk;
-            c.tiles = (d.N * c.row_tiles + 7) / 8 * 8;
-            c.flush_chunks = c.G / c.chk;
-            c.kw_words = (int64_t)c.nmb * c.wm * ((int64_t)d.C * c.nrt + kStreamPad) * kWaveM;
-            c.spread_words = (int64_t)d.N * d.C * c.Hp * c.ntw * c.nq;
-            // cost per output value, in VALU issue slots
-            double mads = (double)d.C * c.nrt;
-            double flushes = std::ceil((double)d.C / ((double)c.flush_chunks * c.chk));
-            double decode = (c.result_signed ? 6.0 : 0.0) + 4.0 * c.nl;
-            double staging = (double)d.C * c.trows * c.ntw * 2.0 / ((double)c.rows_blk * c.mblk);
-            double spread = (double)d.C * c.Hp * c.ntw * c.nq * (6.0 * I + 4.0) / ((double)d.M * c.Ho * c.Wo);
-            double lane_util = (double)c.groups * c.nq / 64.0;
-            double row_util = (double)c.Ho / ((double)c.row_tiles * c.rows_blk);
-            c.cost = ((mads + flushes * decode + staging) / I + spread) / (lane_util * row_util);
             c.macs_per_mad = (double)I * d.KW / (double)c.ntw;
+            // the multiply-adds alone, spread perfectly over every SIMD, bound the cost below
+            const double floor_cost = (double)d.N * c.Ho * c.nq * d.M * d.C * c.nrt / 64.0 / 1024.0;
+            if (found && floor_cost >= best.cost) continue;
+            if (!place_launch(d, c)) continue;
             if (c.cost < best.cost) {
                 best = c;
                 found = true;
@@ -222,6 +256,35 @@ int plan_conv2d(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, Conv2dGeom 
         return SAMD_EUNSUPPORTED;
     }
     return SAMD_OK;
+}
+
+// Plans are a pure function of (shape, formats); the search prices thousands of launch
+// shapes, so found plans are kept (under a lock) and later calls look them up.
+using PlanKey = std::array<int32_t, 15>;
+std::mutex plan_mu;
+std::map<PlanKey, Conv2dGeom> plan_cache;
+constexpr size_t kPlanCacheMax = 4096;
+
+}  // namespace
+
+int plan_conv2d(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, Conv2dGeom &g, std::string &err) {
+    const PlanKey key = {d.N, d.C, d.H, d.W, d.M, d.KH, d.KW, d.stride_h, d.stride_w, d.pad_h, d.pad_w,
+                         xf.bits, xf.is_signed, wf.bits, wf.is_signed};
+    {
+        std::lock_guard<std::mutex> lock(plan_mu);
+        auto it = plan_cache.find(key);
+        if (it != plan_cache.end()) {
+            g = it->second;
+            return SAMD_OK;
+        }
+    }
+    const int st = search_conv2d(d, xf, wf, g, err);
+    if (st == SAMD_OK) {
+        std::lock_guard<std::mutex> lock(plan_mu);
+        if (plan_cache.size() >= kPlanCacheMax) plan_cache.clear();
+        plan_cache.emplace(key, g);
+    }
+    return st;
 }
 
 // Workspace: kernel-word streams, then the operand words of one call (256-byte aligned).

@@ -18,8 +18,11 @@ constexpr int kWaveM = 8;          // output channels per wave (kernel words per
 constexpr int kMaxConv1dExtra = 15; // following words whose low lanes reach a 1-D output word
 constexpr int kStepBatch = 3;      // kernel-word steps fetched per scalar-load batch
 constexpr int kStreamPad = 2 * kStepBatch;  // zero steps after each kernel-word stream
-constexpr int kMaxChunk = 8;       // input channels staged in LDS per chunk
-constexpr int kStagePerThread = 8; // operand words each conv2d thread stages per chunk
+constexpr int kMaxChunk = 64;      // input channels staged in LDS per chunk
+constexpr int kMaxChunkPerWave = 16; // channels one wave multiplies per chunk
+constexpr int kStagePerThread = 4; // operand words each conv2d thread stages per chunk from registers
+constexpr int kMaxBlockWaves = 16; // waves per conv2d workgroup
+constexpr int kMaxLdsBytes = 65536; // LDS per conv2d workgroup
 
 // Geometry of one SAMD 2-D convolution.  Every operand word is a signed 32-bit
 // integer A = sum_i v_i 2^(i L) holding I input values of one stride phase of one
@@ -45,16 +48,20 @@ struct Conv2dGeom {
     int32_t rh;                     // output rows per thread
     int32_t groups;                 // row groups per wave: 64 / nq
     int32_t rows_blk;               // output rows per workgroup: rh * groups
-    int32_t wm;                     // waves per workgroup, each kWaveM output channels
+    int32_t wm;                     // output-channel waves per workgroup, each kWaveM channels
+    int32_t ks;                     // channel-split waves: wave (kq, mw) multiplies channel slice kq
     int32_t mblk;                   // output channels per workgroup, wm * kWaveM
     int32_t nmb;                    // output-channel blocks
     int32_t row_tiles;              // ceil(Ho / rows_blk)
     int32_t tiles;                  // N * row_tiles, rounded up to a multiple of 8 (one per XCD)
-    int32_t chk;                    // input channels staged per chunk
-    int32_t flush_chunks;           // chunks between decodes
+    int32_t chk;                    // input channels staged per chunk, ks * cpw
+    int32_t cpw;                    // channels of a chunk multiplied by one wave
+    int32_t flush_chunks;           // chunks between decodes: G / cpw
     int32_t trows;                  // staged input rows per chunk, (rows_blk-1)*sh + KH
     int32_t xrw;                    // packed words per input row
     int32_t wrw;                    // packed words per kernel row
+    int32_t tile_rows;              // output-tile rows per channel: groups * rh
+    int32_t tile_row;               // output-tile words per row: nq * I + Kmax - 1 (column o at o + Kmax - 1)
     int32_t lds_tile, lds_abuf;     // LDS words: output tile, one operand-word buffer
     int32_t lds_words;              // LDS words in all: tile, two buffers, one spare channel block
     int32_t lds_qstride;            // LDS words per (channel, q) in a buffer: trows*ntw made odd
@@ -89,6 +96,8 @@ int launch_unpack(const uint32_t *src, int64_t rows, int64_t len, int bits, int 
 int launch_conv1d(const uint32_t *x, const Conv1dGeom &g, int32_t *y, hipStream_t s);
 int launch_conv2d_prepare(const uint32_t *w, const Conv2dGeom &g, void *ws, hipStream_t s);
 int launch_conv2d_samd(const uint32_t *x, const Conv2dGeom &g, int32_t *y, const void *ws, hipStream_t s);
+int launch_conv2d_spread(const uint32_t *x, const Conv2dGeom &g, void *ws, hipStream_t s);
+int launch_conv2d_multiply(const Conv2dGeom &g, int32_t *y, const void *ws, hipStream_t s);
 size_t conv2d_i8_workspace_bytes(const samd_conv2d_desc &d, samd_fmt xf);
 int launch_conv2d_i8_prepare(const int8_t *w, samd_fmt xf, const samd_conv2d_desc &d, void *ws, hipStream_t s);
 int launch_conv2d_i8(const void *x, samd_fmt xf, const samd_conv2d_desc &d, int32_t *y, const void *ws,

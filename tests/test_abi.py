@@ -106,6 +106,21 @@ def test_conv2d_validation():
     assert b"does not fit int32" in L.samd_last_error()
 
 
+def test_conv2d_stage_and_accumulate_validation():
+    L = samd.lib()
+    n = ctypes.c_size_t(0)
+    assert L.samd_conv2d_workspace(ctypes.byref(MID), Fmt(2, 0), Fmt(2, 1), ctypes.byref(n)) == OK
+    need = n.value
+    assert L.samd_conv2d_stage(None, Fmt(2, 0), Fmt(2, 1), ctypes.byref(MID), P4 * 16, need, None) == EINVAL
+    assert L.samd_conv2d_stage(P1, Fmt(2, 0), Fmt(2, 1), ctypes.byref(MID), P4 * 16, need, None) == EALIGN
+    assert L.samd_conv2d_stage(P4, Fmt(2, 0), Fmt(2, 1), ctypes.byref(MID), P4 * 16, need - 1, None) == ENOSPC
+    assert L.samd_conv2d_stage(P4, Fmt(9, 0), Fmt(2, 1), ctypes.byref(MID), P4 * 16, need, None) == EINVAL
+    assert L.samd_conv2d_accumulate(Fmt(2, 0), Fmt(2, 1), ctypes.byref(MID), None, P4 * 16, need, None) == EINVAL
+    assert L.samd_conv2d_accumulate(Fmt(2, 0), Fmt(2, 1), ctypes.byref(MID), P1, P4 * 16, need, None) == EALIGN
+    assert L.samd_conv2d_accumulate(Fmt(2, 0), Fmt(2, 1), ctypes.byref(MID), P4, None, need, None) == EINVAL
+    assert L.samd_conv2d_accumulate(Fmt(2, 0), Fmt(2, 1), None, P4, P4 * 16, need, None) == EINVAL
+
+
 def test_conv2d_int8_validation():
     L = samd.lib()
     n = ctypes.c_size_t(0)

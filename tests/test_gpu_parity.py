@@ -288,3 +288,20 @@ def test_prepared_weights_are_reusable(bits):
         torch.cuda.synchronize()
         np.testing.assert_array_equal(y.cpu().numpy(), want)
         np.testing.assert_array_equal(y8.cpu().numpy(), want)
+
+
+@pytest.mark.parametrize("bits", [2, 5])
+def test_staged_input_accumulates_against_several_weight_sets(bits):
+    """stage once, then prepare + accumulate two weight sets on the same staged words."""
+    shape = EDGE[2]
+    xf, wf = samd.Fmt(bits, False), samd.Fmt(bits, True)
+    rng = np.random.default_rng(70 + bits)
+    x = wl.uniform(rng, (shape.N, shape.C, shape.H, shape.W), bits, False)
+    ws = torch.empty(samd.conv2d_workspace(shape, xf, wf), dtype=torch.uint8, device=DEV)
+    samd.conv2d_stage(samd.pack(gpu_vals(x, False), bits, False), xf, wf, shape, ws)
+    for _ in range(2):
+        w = wl.uniform(rng, (shape.M, shape.C, shape.KH, shape.KW), bits, True)
+        samd.conv2d_prepare(samd.pack(gpu_vals(w, True), bits, True), wf, shape, xf, ws=ws)
+        y = samd.conv2d_accumulate(xf, wf, shape, ws)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(y.cpu().numpy(), ref.conv2d(x, w, shape.as_tuple()))
