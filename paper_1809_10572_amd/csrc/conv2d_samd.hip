@@ -17,6 +17,8 @@
 //    which also performs the overlap-add of neighbouring words' partial lanes.
 #include <hip/hip_runtime.h>
 
+#include <climits>
+
 #include "hip_util.hpp"
 
 namespace samd {
@@ -93,6 +95,49 @@ __global__ __launch_bounds__(256) void spread_kernel(const uint32_t *__restrict_
 // stays one v_mad_i64_i32 into its accumulator.
 __device__ __forceinline__ void keep(int64_t &acc) { asm volatile("" : "+v"(acc)); }
 
+// Sign- or zero-extended field of the low L bits (v_bfe with a uniform width).
+template <bool SG>
+__device__ __forceinline__ int32_t low_field(uint32_t w, int L) {
+    int32_t d;
+    if (SG)
+        asm("v_bfe_i32 %0, %1, 0, %2" : "=v"(d) : "v"(w), "s"(L));
+    else
+        asm("v_bfe_u32 %0, %1, 0, %2" : "=v"(d) : "v"(w), "s"(L));
+    return d;
+}
+
+// Decode of one accumulator (Sec. 6): the fix-up of the signed-convolution figure for
+// signed results, then lanes from the bottom - take the low L bits, shift them out -
+// each added into its output column (p + j); lane NL-1 takes all remaining bits.
+template <bool SG, int NL>
+__device__ __forceinline__ void decode_word(uint64_t v, uint64_t msb_mask, int L, int32_t *p) {
+    if (SG) {
+        const uint64_t s = v & msb_mask;
+        v = (v + s) ^ s;
+    }
+#pragma unroll
+    for (int j = 0; j < NL - 1; ++j) {
+        atomicAdd(p + j, low_field<SG>((uint32_t)v, L));
+        v = SG ? (uint64_t)((int64_t)v >> L) : v >> L;
+    }
+    atomicAdd(p + NL - 1, (int32_t)v);
+}
+
+// The same for a lane count known only at run time.
+template <bool SG>
+__device__ __forceinline__ void decode_word_n(uint64_t v, uint64_t msb_mask, int L, int nl, int32_t *p) {
+    if (SG) {
+        const uint64_t s = v & msb_mask;
+        v = (v + s) ^ s;
+    }
+#pragma unroll 1
+    for (int j = 0; j < nl - 1; ++j) {
+        atomicAdd(p + j, low_field<SG>((uint32_t)v, L));
+        v = SG ? (uint64_t)((int64_t)v >> L) : v >> L;
+    }
+    atomicAdd(p + nl - 1, (int32_t)v);
+}
+
 // A workgroup has wm x ks waves.  Wave (kq, mw) owns output channels mw*8 .. +7 of the
 // block and multiplies slice kq (cpw channels) of every chunk; the ks waves of one
 // output-channel group add their decoded partial sums into the same LDS tile, whose
@@ -100,8 +145,9 @@ __device__ __forceinline__ void keep(int64_t &acc) { asm volatile("" : "+v"(acc)
 //
 // NRT: steps (kernel row x kernel word) per input channel when it is 3 or 6 (every 3x3
 // layer), so batches never straddle channels and all LDS offsets are immediates; 0 for
-// any other count.
-template <int RH, int NRT>
+// any other count.  SG: the result is signed (either operand signed), so lanes need
+// the fix-up and are sign-extended.
+template <int RH, int NRT, bool SG>
 __global__ __launch_bounds__(1024) void conv2d_samd_kernel(const int32_t *__restrict__ xs,
                                                            const int32_t *__restrict__ kw, int32_t *__restrict__ y,
                                                            const Conv2dGeom g) {
@@ -145,18 +191,17 @@ __global__ __launch_bounds__(1024) void conv2d_samd_kernel(const int32_t *__rest
     const int32_t *xs_tile = xs + ((int64_t)n * g.C * g.Hp + ho0 * g.sh) * g.ntw * g.nq;
     // Thread element j of a chunk: global word i of channel cc (global order [tr][t][q]);
     // the same (cc, i) in every chunk, so offsets are computed once.
-    int e_cc[kPrefetch], e_lds[kPrefetch], e_off[kPrefetch];
-    bool e_row[kPrefetch];
+    // e_off < 0: the row lies past the padded image and stages as 0; e_lds = INT_MAX: no
+    // element (past the chunk).  Channel cc < n of a chunk  <=>  e_lds < n * cs.
+    int e_lds[kPrefetch], e_off[kPrefetch];
     const int chunk_words = g.chk * gblk;
 #pragma unroll
     for (int j = 0; j < kPrefetch; ++j) {
         const int e = tid + j * nthr;
         const int cc = e / gblk, i = e - cc * gblk;
         const int qq = i % g.nq, rt = i / g.nq;
-        e_cc[j] = e < chunk_words ? cc : 1 << 30;
-        e_off[j] = (int)(cc * ch_stride) + i;
-        e_lds[j] = cc * cs + qq * qs + rt;
-        e_row[j] = i < in_words;
+        e_lds[j] = e < chunk_words ? cc * cs + qq * qs + rt : INT_MAX;
+        e_off[j] = i < in_words ? (int)(cc * ch_stride) + i : -1;
     }
     // words past the kPrefetch carried per thread (large staged tiles only): loaded and
     // stored directly
@@ -170,9 +215,10 @@ __global__ __launch_bounds__(1024) void conv2d_samd_kernel(const int32_t *__rest
     const int nchunks = (g.C + g.chk - 1) / g.chk;
     {
         const int ncc = min(g.chk, g.C);
+        const int lim = ncc * cs;
 #pragma unroll
         for (int j = 0; j < kPrefetch; ++j)
-            if (e_cc[j] < ncc) abuf0[e_lds[j]] = e_row[j] ? xs_tile[e_off[j]] : 0;
+            if (e_lds[j] < lim) abuf0[e_lds[j]] = e_off[j] >= 0 ? xs_tile[e_off[j]] : 0;
         stage_rest(abuf0, xs_tile, ncc);
     }
     __syncthreads();
@@ -199,30 +245,25 @@ __global__ __launch_bounds__(1024) void conv2d_samd_kernel(const int32_t *__rest
     const int mstride = g.tile_rows * g.tile_row;
     auto decode = [&]() {
         if (lane_ok) {
+            const uint64_t msb = g.msb_mask;
+            const int L = g.L;
+#define SAMD_DECODE_NL(NL_)                                                                           \
+    case NL_:                                                                                         \
+        _Pragma("unroll") for (int r = 0; r < RH; ++r)                                               \
+            _Pragma("unroll") for (int m = 0; m < RM; ++m)                                           \
+                decode_word<SG, NL_>((uint64_t)acc[r][m], msb, L, tbase + r * g.tile_row + m * mstride); \
+        break;
+            switch (g.nl) {
+                SAMD_DECODE_NL(2) SAMD_DECODE_NL(3) SAMD_DECODE_NL(4) SAMD_DECODE_NL(5)
+                SAMD_DECODE_NL(6) SAMD_DECODE_NL(7) SAMD_DECODE_NL(8)
+            default:
 #pragma unroll
-            for (int r = 0; r < RH; ++r) {
+                for (int r = 0; r < RH; ++r)
 #pragma unroll
-                for (int m = 0; m < RM; ++m) {
-                    uint64_t v = (uint64_t)acc[r][m];
-                    if (g.result_signed) {
-                        const uint64_t s = v & g.msb_mask;
-                        v = (v + s) ^ s;
-                    }
-                    int32_t *pm = tbase + r * g.tile_row + m * mstride;
-                    // lanes from the bottom: extract the low L bits, then shift them out
-#pragma unroll
-                    for (int j = 0; j < kMaxOutLanes - 1; ++j) {
-                        if (j >= g.nl - 1) break;
-                        const uint32_t w32 = (uint32_t)v;
-                        const int32_t d = g.result_signed ? ((int32_t)(w32 << (32 - g.L)) >> (32 - g.L))
-                                                          : (int32_t)(w32 & ((1u << g.L) - 1));
-                        atomicAdd(pm + j, d);
-                        v = g.result_signed ? (uint64_t)((int64_t)v >> g.L) : v >> g.L;
-                    }
-                    const int32_t top = (int32_t)v;
-                    atomicAdd(pm + (g.nl - 1), top);
-                }
+                    for (int m = 0; m < RM; ++m)
+                        decode_word_n<SG>((uint64_t)acc[r][m], msb, L, g.nl, tbase + r * g.tile_row + m * mstride);
             }
+#undef SAMD_DECODE_NL
         }
 #pragma unroll
         for (int r = 0; r < RH; ++r)
@@ -241,8 +282,9 @@ __global__ __launch_bounds__(1024) void conv2d_samd_kernel(const int32_t *__rest
         // operand words of the next chunk: global loads now, LDS stores after the compute
         int32_t pre[kPrefetch];
         const int32_t *src1 = xs_tile + c1 * ch_stride;
+        const int lim1 = ncc1 * cs;
 #pragma unroll
-        for (int j = 0; j < kPrefetch; ++j) pre[j] = (e_cc[j] < ncc1 && e_row[j]) ? src1[e_off[j]] : 0;
+        for (int j = 0; j < kPrefetch; ++j) pre[j] = (e_lds[j] < lim1 && e_off[j] >= 0) ? src1[e_off[j]] : 0;
 
         // This wave's slice: channels cw0 .. cw0 + nch - 1 of the chunk, in batches of
         // kStepBatch steps: kernel words in SGPRs, operand words from LDS.  With 3 or 6
@@ -257,7 +299,7 @@ __global__ __launch_bounds__(1024) void conv2d_samd_kernel(const int32_t *__rest
         auto load_batch = [&](int b, int32_t (&kb)[kStepBatch * RM], int32_t (&ab)[kStepBatch][RH]) {
 #pragma unroll
             for (int j = 0; j < kStepBatch * RM; ++j) kb[j] = ks[b * kStepBatch * RM + j];
-            if (NRT != 0) {
+            if constexpr (NRT != 0) {
                 // batch b: channel b / (NRT/3), steps (b % (NRT/3))*3 .. +2 of it
                 constexpr int BPC = NRT / kStepBatch;
                 const int base = (b / BPC) * cs + (b % BPC) * kStepBatch;
@@ -330,7 +372,7 @@ __global__ __launch_bounds__(1024) void conv2d_samd_kernel(const int32_t *__rest
         // before the previous barrier)
 #pragma unroll
         for (int j = 0; j < kPrefetch; ++j)
-            if (e_cc[j] < ncc1) nxt[e_lds[j]] = pre[j];
+            if (e_lds[j] < lim1) nxt[e_lds[j]] = pre[j];
         stage_rest(nxt, src1, ncc1);
 
         if ((k + 1) % g.flush_chunks == 0 || k + 1 == nchunks) decode();
@@ -384,13 +426,16 @@ int launch_conv2d_multiply(const Conv2dGeom &g, int32_t *y, const void *ws, hipS
     const int32_t *xs = (const int32_t *)((const char *)ws + conv2d_kw_bytes(g));
     const dim3 grid((unsigned)g.tiles * g.nmb), block(g.wm * g.ks * 64);
     const size_t shm = (size_t)g.lds_words * 4;
-#define SAMD_CONV_CASE(RH_, NRT_)                                                                     \
-    if (g.rh == RH_ && (NRT_ == 0 ? (g.nrt != 3 && g.nrt != 6) : g.nrt == NRT_)) {                     \
-        hipLaunchKernelGGL((conv2d_samd_kernel<RH_, NRT_>), grid, block, shm, s, xs, kw, y, g);          \
+#define SAMD_CONV_CASE(RH_, NRT_, SG_)                                                                \
+    if (g.rh == RH_ && (NRT_ == 0 ? (g.nrt != 3 && g.nrt != 6) : g.nrt == NRT_) &&                     \
+        (bool)g.result_signed == SG_) {                                                               \
+        hipLaunchKernelGGL((conv2d_samd_kernel<RH_, NRT_, SG_>), grid, block, shm, s, xs, kw, y, g);   \
         return check_launch("conv2d");                                                                \
     }
-    SAMD_CONV_CASE(1, 3) SAMD_CONV_CASE(1, 6) SAMD_CONV_CASE(1, 0)
-    SAMD_CONV_CASE(2, 3) SAMD_CONV_CASE(2, 6) SAMD_CONV_CASE(2, 0)
+    SAMD_CONV_CASE(1, 3, false) SAMD_CONV_CASE(1, 6, false) SAMD_CONV_CASE(1, 0, false)
+    SAMD_CONV_CASE(2, 3, false) SAMD_CONV_CASE(2, 6, false) SAMD_CONV_CASE(2, 0, false)
+    SAMD_CONV_CASE(1, 3, true) SAMD_CONV_CASE(1, 6, true) SAMD_CONV_CASE(1, 0, true)
+    SAMD_CONV_CASE(2, 3, true) SAMD_CONV_CASE(2, 6, true) SAMD_CONV_CASE(2, 0, true)
 #undef SAMD_CONV_CASE
     set_error("conv2d: no kernel for this geometry");
     return SAMD_EUNSUPPORTED;

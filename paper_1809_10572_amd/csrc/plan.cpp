@@ -125,7 +125,12 @@ bool place_launch(const samd_conv2d_desc &d, Conv2dGeom &c) {
                     double mads = (double)wm * kWaveM * rh * d.C * c.nrt * 1.08;
                     double decode = (double)wm * ks * nflush * kWaveM * rh *
                                     ((c.result_signed ? 5.0 : 0.0) + 1.0 + 2.0 * c.nl);
-                    double staging = nchunks * std::ceil(staged / threads) * wm * ks * 4.0;
+                    // words beyond kStagePerThread per thread take the slow path (index
+                    // arithmetic per word)
+                    const double per_thr = std::ceil(staged / threads);
+                    double staging = nchunks * wm * ks *
+                                     (std::min(per_thr, (double)kStagePerThread) * 4.0 +
+                                      std::max(per_thr - kStagePerThread, 0.0) * 70.0);
                     double tile = (double)t.lds_tile / 64.0 * 3.0;
                     double wg = mads + decode + staging + tile;
                     // residency: LDS, and at most 8 waves per SIMD

@@ -20,7 +20,7 @@ constexpr int kStepBatch = 3;      // kernel-word steps fetched per scalar-load 
 constexpr int kStreamPad = 2 * kStepBatch;  // zero steps after each kernel-word stream
 constexpr int kMaxChunk = 64;      // input channels staged in LDS per chunk
 constexpr int kMaxChunkPerWave = 16; // channels one wave multiplies per chunk
-constexpr int kStagePerThread = 4; // operand words each conv2d thread stages per chunk from registers
+constexpr int kStagePerThread = 8; // operand words each conv2d thread stages per chunk from registers
 constexpr int kMaxBlockWaves = 16; // waves per conv2d workgroup
 constexpr int kMaxLdsBytes = 65536; // LDS per conv2d workgroup
 
