@@ -26,7 +26,6 @@ namespace samd {
 namespace {
 
 constexpr int RM = kWaveM;
-constexpr int kPrefetch = kStagePerThread;   // operand words each thread carries into the next chunk
 
 template <int B, bool S>
 __device__ inline int32_t packed_field(const uint32_t *row, int col) {
@@ -89,6 +88,15 @@ __global__ __launch_bounds__(256) void spread_kernel(const uint32_t *__restrict_
     }
 }
 
+// Operand words are read through a buffer resource over one image's operand words: the
+// per-lane byte offset is a VGPR, the per-step offset an SGPR (no address arithmetic in
+// the vector unit).  Word 3 is the gfx9 raw-buffer format (32-bit data, no swizzle).
+constexpr int kBufferWord3 = 0x00020000;
+
+__device__ __forceinline__ int32_t buffer_word(__amdgpu_buffer_rsrc_t r, int lane_bytes, int step_bytes) {
+    return __builtin_amdgcn_raw_buffer_load_b32(r, lane_bytes, step_bytes, 0);
+}
+
 // Empty register barrier: the accumulator is treated as rewritten here, so the products
 // of successive steps cannot be summed first and added afterwards (integer addition is
 // associative, and that rewrite costs one extra 64-bit add per batch); every product
@@ -138,23 +146,24 @@ __device__ __forceinline__ void decode_word_n(uint64_t v, uint64_t msb_mask, int
     atomicAdd(p + nl - 1, (int32_t)v);
 }
 
-// A workgroup has wm x ks waves.  Wave (kq, mw) owns output channels mw*8 .. +7 of the
-// block and multiplies slice kq (cpw channels) of every chunk; the ks waves of one
-// output-channel group add their decoded partial sums into the same LDS tile, whose
-// atomic adds are also the overlap-add of neighbouring words' partial lanes.
+// A workgroup has wm x ks waves and owns rows_blk output rows x all Wo columns x mblk
+// output channels of one image.  Wave (kq, mw) computes output channels mw*8 .. +7 of the
+// block over its slice kq of the input channels; lane (grp, q) holds output word q of rows
+// grp*RH .. +RH-1.  Operand words come straight from the spread buffer (global memory,
+// L1/L2-resident: every word is reused by the block's wm waves and its KH kernel rows),
+// kernel words from the wave's stream through scalar loads.  After at most G channels the
+// accumulators are decoded into an LDS tile of int32 outputs whose atomic adds also sum
+// the ks channel slices and overlap-add neighbouring words' partial lanes.
 //
 // NRT: steps (kernel row x kernel word) per input channel when it is 3 or 6 (every 3x3
-// layer), so batches never straddle channels and all LDS offsets are immediates; 0 for
-// any other count.  SG: the result is signed (either operand signed), so lanes need
-// the fix-up and are sign-extended.
+// layer), so batches never straddle channels; 0 for any other count.  SG: the result is
+// signed (either operand signed), so lanes need the fix-up and are sign-extended.
 template <int RH, int NRT, bool SG>
 __global__ __launch_bounds__(1024) void conv2d_samd_kernel(const int32_t *__restrict__ xs,
                                                            const int32_t *__restrict__ kw, int32_t *__restrict__ y,
                                                            const Conv2dGeom g) {
     extern __shared__ int32_t lds[];
     int32_t *tile = lds;
-    int32_t *abuf0 = lds + g.lds_tile;
-    int32_t *abuf1 = abuf0 + g.lds_abuf;
 
     // Consecutive workgroups on one XCD (hardware assigns workgroup p to XCD p % 8) take
     // all channel blocks of one spatial tile, so its operand words are reused from L2.
@@ -178,50 +187,26 @@ __global__ __launch_bounds__(1024) void conv2d_samd_kernel(const int32_t *__rest
     const int q = lane_ok ? lane - grp_raw * g.nq : 0;
     const int wb = mb * g.wm + mw;
 
-    for (int i = tid; i < g.lds_tile; i += nthr) tile[i] = 0;
-
-    // LDS chunk layout [cc][q][tr * ntw + t] with an odd stride per q (conflict-free):
-    // a thread's steps (ky, t) of one channel and row are consecutive words.
-    const int T = g.trows * g.ntw;                 // words per (channel, q)
-    const int qs = g.lds_qstride;                  // T rounded up to odd
-    const int cs = g.nq * qs;                      // words per channel
-    const int gblk = T * g.nq;                     // global words per channel of the tile
-    const int64_t ch_stride = (int64_t)g.Hp * g.ntw * g.nq;
-    const int in_words = min(g.trows, g.Hp - ho0 * g.sh) * g.ntw * g.nq;   // rows that exist
-    const int32_t *xs_tile = xs + ((int64_t)n * g.C * g.Hp + ho0 * g.sh) * g.ntw * g.nq;
-    // Thread element j of a chunk: global word i of channel cc (global order [tr][t][q]);
-    // the same (cc, i) in every chunk, so offsets are computed once.
-    // e_off < 0: the row lies past the padded image and stages as 0; e_lds = INT_MAX: no
-    // element (past the chunk).  Channel cc < n of a chunk  <=>  e_lds < n * cs.
-    int e_lds[kPrefetch], e_off[kPrefetch];
-    const int chunk_words = g.chk * gblk;
-#pragma unroll
-    for (int j = 0; j < kPrefetch; ++j) {
-        const int e = tid + j * nthr;
-        const int cc = e / gblk, i = e - cc * gblk;
-        const int qq = i % g.nq, rt = i / g.nq;
-        e_lds[j] = e < chunk_words ? cc * cs + qq * qs + rt : INT_MAX;
-        e_off[j] = i < in_words ? (int)(cc * ch_stride) + i : -1;
-    }
-    // words past the kPrefetch carried per thread (large staged tiles only): loaded and
-    // stored directly
-    auto stage_rest = [&](int32_t *dst, const int32_t *src, int ncc) {
-        for (int e = tid + kPrefetch * nthr; e < ncc * gblk; e += nthr) {
-            const int cc = e / gblk, i = e - cc * gblk;
-            const int qq = i % g.nq, rt = i / g.nq;
-            dst[cc * cs + qq * qs + rt] = i < in_words ? src[cc * ch_stride + i] : 0;
-        }
-    };
-    const int nchunks = (g.C + g.chk - 1) / g.chk;
     {
-        const int ncc = min(g.chk, g.C);
-        const int lim = ncc * cs;
-#pragma unroll
-        for (int j = 0; j < kPrefetch; ++j)
-            if (e_lds[j] < lim) abuf0[e_lds[j]] = e_off[j] >= 0 ? xs_tile[e_off[j]] : 0;
-        stage_rest(abuf0, xs_tile, ncc);
+        int4 *t4 = (int4 *)tile;   // lds_tile is a multiple of 4 words
+        for (int i = tid; i < g.lds_tile / 4; i += nthr) t4[i] = int4{0, 0, 0, 0};
     }
     __syncthreads();
+
+    // Operand word of step s (s = ky*ntw + t) of channel c for this lane's row r:
+    // xs[n][c][hp][t][q] with hp = (ho0 + row)*sh + ky, i.e. word
+    // (c*Hp*ntw + (ho0 + row)*sh*ntw + s)*nq + q of image n.  Rows past the image (the last
+    // row tile, idle lanes) read the last output row's inputs; their sums are not stored.
+    const int ch_stride = g.Hp * g.ntw * g.nq;
+    int lb[RH];   // byte offset of the lane's word in channel 0, step 0
+#pragma unroll
+    for (int r = 0; r < RH; ++r) {
+        const int row = min(ho0 + min(grp * RH + r, g.rows_blk - 1), g.Ho - 1);
+        lb[r] = (row * g.sh * g.ntw * g.nq + q) * 4;
+    }
+    // the image's channels and one spare channel after them
+    const __amdgpu_buffer_rsrc_t xrs = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)(xs + (int64_t)n * g.C * ch_stride), (short)0, (g.C + 1) * ch_stride * 4, kBufferWord3);
 
     int64_t acc[RH][RM];
 #pragma unroll
@@ -231,16 +216,10 @@ __global__ __launch_bounds__(1024) void conv2d_samd_kernel(const int32_t *__rest
 
     const int64_t stream_len = ((int64_t)g.C * g.nrt + kStreamPad) * RM;
     const int32_t *kstream = kw + wb * stream_len;
-    // LDS word offset of each of the thread's rows within a channel (rows past the tile
-    // reuse the last one; their results are never stored)
-    int rowoff[RH];
-#pragma unroll
-    for (int r = 0; r < RH; ++r) rowoff[r] = q * qs + min(grp * RH + r, g.rows_blk - 1) * g.sh * g.ntw;
-    const int cw0 = kq * g.cpw;   // first channel of this wave's slice of a chunk
 
-    // Decode: fix-up (signed results), then lane j of word q goes to output column
-    // q*I + j - (Kmax-1), stored at tile column q*I + j; the top lane takes the bits left.
-    // Tile rows cover every row a wave computes, so no lane needs a bounds check.
+    // Decode: lane j of word q goes to output column q*I + j - (Kmax-1), stored at tile
+    // column q*I + j.  Tile rows cover every row a wave computes, so no lane needs a
+    // bounds check.
     int32_t *const tbase = tile + ((mw * RM) * g.tile_rows + grp * RH) * g.tile_row + q * g.I;
     const int mstride = g.tile_rows * g.tile_row;
     auto decode = [&]() {
@@ -271,59 +250,46 @@ __global__ __launch_bounds__(1024) void conv2d_samd_kernel(const int32_t *__rest
             for (int m = 0; m < RM; ++m) acc[r][m] = 0;
     };
 
-    for (int k = 0; k < nchunks; ++k) {
-        const int32_t *cur = (k & 1) ? abuf1 : abuf0;
-        int32_t *nxt = (k & 1) ? abuf0 : abuf1;
-        const int c0 = k * g.chk;
-        const int ncc = min(g.chk, g.C - c0);
-        const int c1 = c0 + g.chk;
-        const int ncc1 = k + 1 < nchunks ? min(g.chk, g.C - c1) : 0;
-
-        // operand words of the next chunk: global loads now, LDS stores after the compute
-        int32_t pre[kPrefetch];
-        const int32_t *src1 = xs_tile + c1 * ch_stride;
-        const int lim1 = ncc1 * cs;
-#pragma unroll
-        for (int j = 0; j < kPrefetch; ++j) pre[j] = (e_lds[j] < lim1 && e_off[j] >= 0) ? src1[e_off[j]] : 0;
-
-        // This wave's slice: channels cw0 .. cw0 + nch - 1 of the chunk, in batches of
-        // kStepBatch steps: kernel words in SGPRs, operand words from LDS.  With 3 or 6
-        // steps per channel a slice is a whole number of batches.
-        const int nch = min(max(ncc - cw0, 0), g.cpw);
+    // This wave's channel slice, in segments of at most G channels between decodes.
+    const int cbeg = min(kq * g.cpw, g.C), cend = min(cbeg + g.cpw, g.C);
+    for (int c0 = cbeg; c0 < cend; c0 += g.G) {
+        const int nch = min(g.G, cend - c0);
         const int nsteps = nch * g.nrt;
         const int nbat = (nsteps + kStepBatch - 1) / kStepBatch;
-        const int32_t *ks = kstream + (int64_t)(c0 + cw0) * g.nrt * RM;
-        const int32_t *wcur = cur + cw0 * cs;
+        const int32_t *ks = kstream + (int64_t)c0 * g.nrt * RM;
         int32_t kA[kStepBatch * RM], aA[kStepBatch][RH], kB[kStepBatch * RM], aB[kStepBatch][RH];
-        int gs = 0;   // generic layout: step index of the next batch to load
+        // Batch b: kernel words in SGPRs, the lane's operand words from global memory.
+        // With 3 or 6 steps per channel, batch b is steps (b % (NRT/3))*3 .. +2 of channel
+        // b / (NRT/3).  The batch after the segment's last one is fetched as well (its
+        // results are never used): it reads the next channel, which exists (the spread
+        // buffer has one spare channel after the last image) or the kStreamPad padding
+        // steps of the kernel-word stream.
         auto load_batch = [&](int b, int32_t (&kb)[kStepBatch * RM], int32_t (&ab)[kStepBatch][RH]) {
 #pragma unroll
             for (int j = 0; j < kStepBatch * RM; ++j) kb[j] = ks[b * kStepBatch * RM + j];
             if constexpr (NRT != 0) {
-                // batch b: channel b / (NRT/3), steps (b % (NRT/3))*3 .. +2 of it
                 constexpr int BPC = NRT / kStepBatch;
-                const int base = (b / BPC) * cs + (b % BPC) * kStepBatch;
+                const int sb = ((c0 + b / BPC) * ch_stride + (b % BPC) * kStepBatch * g.nq) * 4;
 #pragma unroll
-                for (int r = 0; r < RH; ++r) {
-                    const int32_t *src = wcur + base + rowoff[r];
+                for (int j = 0; j < kStepBatch; ++j)
 #pragma unroll
-                    for (int j = 0; j < kStepBatch; ++j) ab[j][r] = src[j];
-                }
+                    for (int r = 0; r < RH; ++r) ab[j][r] = buffer_word(xrs, lb[r], sb + j * g.nq * 4);
             } else {
 #pragma unroll
                 for (int j = 0; j < kStepBatch; ++j) {
-                    // steps past the slice (its step count need not be a multiple of the
+                    // steps past the segment (its step count need not be a multiple of the
                     // batch) multiply the following channel's kernel words: their operand is 0
-                    const bool live = gs + j < nsteps;
-                    const int st = min(gs + j, nsteps - 1);
+                    const int st0 = b * kStepBatch + j;
+                    const bool live = st0 < nsteps;
+                    const int st = min(st0, nsteps - 1);
                     const int cc = st / g.nrt, rt = st - cc * g.nrt;
+                    const int sb = ((c0 + cc) * ch_stride + rt * g.nq) * 4;
 #pragma unroll
                     for (int r = 0; r < RH; ++r) {
-                        const int32_t v = wcur[cc * cs + rt + rowoff[r]];
+                        const int32_t v = buffer_word(xrs, lb[r], sb);
                         ab[j][r] = live ? v : 0;
                     }
                 }
-                gs += kStepBatch;
             }
         };
         auto mac_batch = [&](const int32_t (&kb)[kStepBatch * RM], const int32_t (&ab)[kStepBatch][RH]) {
@@ -340,54 +306,50 @@ __global__ __launch_bounds__(1024) void conv2d_samd_kernel(const int32_t *__rest
             }
         };
         // Ping-pong over two register sets.  Before a batch's kernel words are used, all
-        // outstanding scalar and LDS loads are waited for, and only then is the next batch
+        // outstanding scalar loads are waited for, and only then is the next batch
         // requested: scalar loads return out of order, so a wait placed after requesting
-        // the next batch would wait for it too.
-        // The batch after the slice's last one is fetched too (its results are never
-        // used): it reads the next slice's channel, or for the last slice the spare
-        // channel block after the LDS buffers and the kStreamPad padding steps of the
-        // kernel-word stream.
-        if (nbat > 0) {
-            load_batch(0, kA, aA);
-            int b = 0;
-            for (; b + 1 < nbat; b += 2) {
-                __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0)
-                load_batch(b + 1, kB, aB);
-                __builtin_amdgcn_sched_barrier(0);
-                mac_batch(kA, aA);
-                __builtin_amdgcn_sched_barrier(0);
-                __builtin_amdgcn_s_waitcnt(0xc07f);
-                load_batch(b + 2, kA, aA);
-                __builtin_amdgcn_sched_barrier(0);
-                mac_batch(kB, aB);
-                __builtin_amdgcn_sched_barrier(0);
-            }
-            if (b < nbat) {   // odd batch count: the last batch
-                __builtin_amdgcn_s_waitcnt(0xc07f);
-                mac_batch(kA, aA);
-            }
+        // the next batch would wait for it too.  Operand loads are vector loads, which
+        // complete in order, so the compiler waits for exactly the batch in use.
+        load_batch(0, kA, aA);
+        int b = 0;
+        for (; b + 1 < nbat; b += 2) {
+            __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0)
+            load_batch(b + 1, kB, aB);
+            __builtin_amdgcn_sched_barrier(0);
+            mac_batch(kA, aA);
+            __builtin_amdgcn_sched_barrier(0);
+            __builtin_amdgcn_s_waitcnt(0xc07f);
+            load_batch(b + 2, kA, aA);
+            __builtin_amdgcn_sched_barrier(0);
+            mac_batch(kB, aB);
+            __builtin_amdgcn_sched_barrier(0);
         }
-
-        // the next chunk's operand words into the other buffer (last read a chunk ago,
-        // before the previous barrier)
-#pragma unroll
-        for (int j = 0; j < kPrefetch; ++j)
-            if (e_lds[j] < lim1) nxt[e_lds[j]] = pre[j];
-        stage_rest(nxt, src1, ncc1);
-
-        if ((k + 1) % g.flush_chunks == 0 || k + 1 == nchunks) decode();
-        __syncthreads();
+        if (b < nbat) {   // odd batch count: the last batch
+            __builtin_amdgcn_s_waitcnt(0xc07f);
+            mac_batch(kA, aA);
+        }
+        decode();
     }
+    __syncthreads();
 
-    // output tile -> y, one row per wave at a time
+    // output tile -> y: wave w copies rows rr = w, w + nwaves, ... (rr = mm * rows_blk + r)
+    // of the tile, lanes along the row
     const int nwaves = g.wm * g.ks;
-    for (int rr = wave; rr < g.mblk * g.rows_blk; rr += nwaves) {
-        const int mm = rr / g.rows_blk, r = rr - mm * g.rows_blk;
+    const int dmm = nwaves / g.rows_blk, dr = nwaves - dmm * g.rows_blk;
+    int mm = wave / g.rows_blk, r = wave - mm * g.rows_blk;
+    while (mm < g.mblk) {
         const int m = mb * g.mblk + mm, ho = ho0 + r;
-        if (m >= g.M || ho >= g.Ho) continue;
-        const int32_t *src = tile + (mm * g.tile_rows + r) * g.tile_row + (g.Kmax - 1);
-        int32_t *dst = y + (((int64_t)n * g.M + m) * g.Ho + ho) * g.Wo;
-        for (int o = lane; o < g.Wo; o += 64) dst[o] = src[o];
+        if (m < g.M && ho < g.Ho) {
+            const int32_t *src = tile + (mm * g.tile_rows + r) * g.tile_row + (g.Kmax - 1);
+            int32_t *dst = y + (((int64_t)n * g.M + m) * g.Ho + ho) * g.Wo;
+            for (int o = lane; o < g.Wo; o += 64) dst[o] = src[o];
+        }
+        mm += dmm;
+        r += dr;
+        if (r >= g.rows_blk) {
+            r -= g.rows_blk;
+            ++mm;
+        }
     }
 }
 

@@ -66,11 +66,11 @@ bool split_taps(int count, int kmax, int *t0, int *nt, int &ngroups) {
 }
 
 // Launch shape of one lane geometry: output rows per thread (rh), row groups per wave,
-// output-channel waves (wm) and channel-split waves (ks) per workgroup, channels per
-// chunk.  Every candidate is priced in VALU issue cycles of the busiest SIMD: the
-// multiply-adds, decodes and staging of the workgroups one compute unit runs, divided by
-// an issue efficiency that grows with the waves resident per SIMD (latency hiding), plus
-// the operand-spread pass.  Returns false when nothing fits the LDS.
+// output-channel waves (wm) and channel-slice waves (ks) per workgroup.  Every candidate
+// is priced in VALU issue cycles of the busiest SIMD: the multiply-adds and decodes of
+// the workgroups one compute unit runs, divided by an issue efficiency that grows with
+// the waves resident per SIMD (latency hiding), plus the operand-spread pass.  Returns
+// false when no tile fits the LDS.
 bool place_launch(const samd_conv2d_desc &d, Conv2dGeom &c) {
     const int grp_max = 64 / c.nq;
     bool found = false;
@@ -82,6 +82,7 @@ bool place_launch(const samd_conv2d_desc &d, Conv2dGeom &c) {
             for (int wm : {1, 2, 4}) {
                 for (int ks : {1, 2, 4, 8, 16}) {
                     if (wm * ks > kMaxBlockWaves) continue;
+                    if (ks > 1 && (d.C + ks - 1) / ks < 1) continue;
                     Conv2dGeom t = c;
                     t.rh = rh;
                     t.groups = gr;
@@ -93,46 +94,24 @@ bool place_launch(const samd_conv2d_desc &d, Conv2dGeom &c) {
                     t.nmb = (d.M + t.mblk - 1) / t.mblk;
                     t.tile_rows = gr * rh;
                     t.tile_row = c.nq * c.I + c.Kmax - 1;
-                    t.lds_tile = t.mblk * t.tile_rows * t.tile_row;
-                    t.lds_qstride = (t.trows * c.ntw) | 1;
-                    const int threads = wm * ks * 64;
-                    // largest chunk whose LDS fits; a slice per wave of at most G channels
-                    const int cpw_hi = std::min(std::min(kMaxChunkPerWave, c.G), (d.C + ks - 1) / ks);
-                    bool placed = false;
-                    for (t.cpw = cpw_hi; t.cpw >= 1; --t.cpw) {
-                        t.chk = t.cpw * ks;
-                        if (t.chk > kMaxChunk && t.cpw > 1) continue;
-                        t.lds_abuf = t.chk * c.nq * t.lds_qstride;
-                        // a spare channel block after the buffers: the batch after a wave's last
-                        // one is fetched as well and may read there
-                        t.lds_words = t.lds_tile + 2 * t.lds_abuf + c.nq * t.lds_qstride + kStepBatch;
-                        if ((long)t.lds_words * 4 <= kMaxLdsBytes) {
-                            placed = true;
-                            break;
-                        }
-                    }
-                    if (!placed) continue;
+                    t.lds_tile = (t.mblk * t.tile_rows * t.tile_row + 3) / 4 * 4;
+                    t.lds_words = t.lds_tile;
+                    if ((long)t.lds_words * 4 > kMaxLdsBytes) continue;
+                    t.cpw = (d.C + ks - 1) / ks;           // channels per slice
+                    if (ks > 1 && (long)(ks - 1) * t.cpw >= d.C) continue;   // an empty slice
+                    t.chk = t.cpw * ks;
                     t.row_tiles = (c.Ho + t.rows_blk - 1) / t.rows_blk;
                     t.tiles = (d.N * t.row_tiles + 7) / 8 * 8;
-                    t.flush_chunks = c.G / t.cpw;
                     t.kw_words = (int64_t)t.nmb * wm * ((int64_t)d.C * c.nrt + kStreamPad) * kWaveM;
                     t.spread_words = (int64_t)d.N * d.C * c.Hp * c.ntw * c.nq;
 
-                    const double nchunks = std::ceil((double)d.C / t.chk);
-                    const double nflush = std::ceil(nchunks / t.flush_chunks);
-                    const double staged = (double)t.chk * t.trows * c.ntw * c.nq;
                     // wave-instructions of one workgroup
-                    double mads = (double)wm * kWaveM * rh * d.C * c.nrt * 1.08;
-                    double decode = (double)wm * ks * nflush * kWaveM * rh *
-                                    ((c.result_signed ? 5.0 : 0.0) + 1.0 + 2.0 * c.nl);
-                    // words beyond kStagePerThread per thread take the slow path (index
-                    // arithmetic per word)
-                    const double per_thr = std::ceil(staged / threads);
-                    double staging = nchunks * wm * ks *
-                                     (std::min(per_thr, (double)kStagePerThread) * 4.0 +
-                                      std::max(per_thr - kStagePerThread, 0.0) * 70.0);
-                    double tile = (double)t.lds_tile / 64.0 * 3.0;
-                    double wg = mads + decode + staging + tile;
+                    const double nflush = std::ceil((double)t.cpw / c.G);
+                    const double mads = (double)wm * ks * kWaveM * rh * t.cpw * c.nrt * 1.08;
+                    const double decode = (double)wm * ks * nflush * kWaveM * rh *
+                                          ((c.result_signed ? 5.0 : 0.0) + 1.0 + 2.0 * c.nl);
+                    const double fixed = (double)wm * ks * 150.0 + (double)t.lds_tile / 64.0 * 3.0;
+                    const double wg = mads + decode + fixed;
                     // residency: LDS, and at most 8 waves per SIMD
                     const double wgs = (double)t.tiles * t.nmb;
                     const double per_cu = std::ceil(wgs / 256.0);
@@ -296,7 +275,10 @@ int plan_conv2d(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, Conv2dGeom 
 size_t conv2d_kw_bytes(const Conv2dGeom &g) { return ((size_t)g.kw_words * 4 + 255) / 256 * 256; }
 
 size_t conv2d_workspace_bytes(const Conv2dGeom &g) {
-    return conv2d_kw_bytes(g) + ((size_t)g.spread_words * 4 + 255) / 256 * 256;
+    // one spare channel after the last image: the batch fetched after a slice's last one
+    // may read it (its products are never used)
+    const size_t spare = (size_t)g.Hp * g.ntw * g.nq;
+    return conv2d_kw_bytes(g) + ((size_t)(g.spread_words + spare) * 4 + 255) / 256 * 256;
 }
 
 int plan_conv1d(int64_t n, samd_fmt xf, const int32_t *taps, int32_t K, samd_fmt kf, Conv1dGeom &best,

@@ -18,9 +18,6 @@ constexpr int kWaveM = 8;          // output channels per wave (kernel words per
 constexpr int kMaxConv1dExtra = 15; // following words whose low lanes reach a 1-D output word
 constexpr int kStepBatch = 3;      // kernel-word steps fetched per scalar-load batch
 constexpr int kStreamPad = 2 * kStepBatch;  // zero steps after each kernel-word stream
-constexpr int kMaxChunk = 64;      // input channels staged in LDS per chunk
-constexpr int kMaxChunkPerWave = 16; // channels one wave multiplies per chunk
-constexpr int kStagePerThread = 8; // operand words each conv2d thread stages per chunk from registers
 constexpr int kMaxBlockWaves = 16; // waves per conv2d workgroup
 constexpr int kMaxLdsBytes = 65536; // LDS per conv2d workgroup
 
@@ -54,17 +51,15 @@ struct Conv2dGeom {
     int32_t nmb;                    // output-channel blocks
     int32_t row_tiles;              // ceil(Ho / rows_blk)
     int32_t tiles;                  // N * row_tiles, rounded up to a multiple of 8 (one per XCD)
-    int32_t chk;                    // input channels staged per chunk, ks * cpw
-    int32_t cpw;                    // channels of a chunk multiplied by one wave
-    int32_t flush_chunks;           // chunks between decodes: G / cpw
-    int32_t trows;                  // staged input rows per chunk, (rows_blk-1)*sh + KH
+    int32_t chk;                    // ks * cpw (reported)
+    int32_t cpw;                    // input channels of one wave's slice: ceil(C / ks)
+    int32_t trows;                  // input rows a tile reads, (rows_blk-1)*sh + KH
     int32_t xrw;                    // packed words per input row
     int32_t wrw;                    // packed words per kernel row
     int32_t tile_rows;              // output-tile rows per channel: groups * rh
     int32_t tile_row;               // output-tile words per row: nq * I + Kmax - 1 (column o at o + Kmax - 1)
-    int32_t lds_tile, lds_abuf;     // LDS words: output tile, one operand-word buffer
-    int32_t lds_words;              // LDS words in all: tile, two buffers, one spare channel block
-    int32_t lds_qstride;            // LDS words per (channel, q) in a buffer: trows*ntw made odd
+    int32_t lds_tile;               // LDS words of the output tile (a multiple of 4)
+    int32_t lds_words;              // LDS words in all
     int64_t kw_words, spread_words; // workspace: kernel-word streams, operand words
     double macs_per_mad, cost;
 };
