@@ -250,35 +250,91 @@ __global__ __launch_bounds__(1024) void conv2d_samd_kernel(const int32_t *__rest
             for (int m = 0; m < RM; ++m) acc[r][m] = 0;
     };
 
-    // This wave's channel slice, in segments of at most G channels between decodes.
+    // This wave's channel slice: channels cbeg .. cend-1, decoded after every G channels.
     const int cbeg = min(kq * g.cpw, g.C), cend = min(cbeg + g.cpw, g.C);
-    for (int c0 = cbeg; c0 < cend; c0 += g.G) {
-        const int nch = min(g.G, cend - c0);
-        const int nsteps = nch * g.nrt;
-        const int nbat = (nsteps + kStepBatch - 1) / kStepBatch;
-        const int32_t *ks = kstream + (int64_t)c0 * g.nrt * RM;
-        int32_t kA[kStepBatch * RM], aA[kStepBatch][RH], kB[kStepBatch * RM], aB[kStepBatch][RH];
-        // Batch b: kernel words in SGPRs, the lane's operand words from global memory.
-        // With 3 or 6 steps per channel, batch b is steps (b % (NRT/3))*3 .. +2 of channel
-        // b / (NRT/3).  The batch after the segment's last one is fetched as well (its
-        // results are never used): it reads the next channel, which exists (the spread
-        // buffer has one spare channel after the last image) or the kStreamPad padding
-        // steps of the kernel-word stream.
+    const int32_t *ks_slice = kstream + (int64_t)cbeg * g.nrt * RM;
+    int32_t kA[kStepBatch * RM], aA[kStepBatch][RH], kB[kStepBatch * RM], aB[kStepBatch][RH];
+    auto mac_batch = [&](const int32_t (&kb)[kStepBatch * RM], const int32_t (&ab)[kStepBatch][RH]) {
+#pragma unroll
+        for (int j = 0; j < kStepBatch; ++j) {
+#pragma unroll
+            for (int r = 0; r < RH; ++r)
+#pragma unroll
+                for (int m = 0; m < RM; ++m) acc[r][m] += (int64_t)ab[j][r] * (int64_t)kb[j * RM + m];
+#pragma unroll
+            for (int r = 0; r < RH; ++r)
+#pragma unroll
+                for (int m = 0; m < RM; ++m) keep(acc[r][m]);
+        }
+    };
+    // Batches of kStepBatch steps: kernel words in SGPRs (scalar loads), the lane's operand
+    // words from global memory.  Ping-pong over two register sets.  Before a batch's kernel
+    // words are used, all outstanding scalar loads are waited for, and only then is the
+    // next batch requested: scalar loads return out of order, so a wait placed after
+    // requesting the next batch would wait for it too.  Operand loads are vector loads,
+    // which complete in order, so the compiler waits for exactly the batch in use.  The
+    // batch after the last one is fetched as well (its results are never used): it reads
+    // the next channel, which exists (the spread buffer has one spare channel after the
+    // last image), and the kStreamPad padding steps of the kernel-word stream.
+    if constexpr (NRT != 0) {
+        // 3 or 6 steps per channel: batch b is steps (b % BPC)*3 .. +2 of channel
+        // cbeg + b / BPC, and the slice is one pipeline; the decode after every G channels
+        // runs while the next batch's loads are in flight.
+        constexpr int BPC = NRT / kStepBatch;
+        const int nbat = (cend - cbeg) * BPC;
+        const int seg = g.G * BPC;   // batches between decodes
         auto load_batch = [&](int b, int32_t (&kb)[kStepBatch * RM], int32_t (&ab)[kStepBatch][RH]) {
 #pragma unroll
-            for (int j = 0; j < kStepBatch * RM; ++j) kb[j] = ks[b * kStepBatch * RM + j];
-            if constexpr (NRT != 0) {
-                constexpr int BPC = NRT / kStepBatch;
-                const int sb = ((c0 + b / BPC) * ch_stride + (b % BPC) * kStepBatch * g.nq) * 4;
+            for (int j = 0; j < kStepBatch * RM; ++j) kb[j] = ks_slice[b * kStepBatch * RM + j];
+            const int sb = ((cbeg + b / BPC) * ch_stride + (b % BPC) * kStepBatch * g.nq) * 4;
 #pragma unroll
-                for (int j = 0; j < kStepBatch; ++j)
+            for (int j = 0; j < kStepBatch; ++j)
 #pragma unroll
-                    for (int r = 0; r < RH; ++r) ab[j][r] = buffer_word(xrs, lb[r], sb + j * g.nq * 4);
-            } else {
+                for (int r = 0; r < RH; ++r) ab[j][r] = buffer_word(xrs, lb[r], sb + j * g.nq * 4);
+        };
+        if (nbat > 0) {
+            int left = seg;   // batches until the next decode
+            load_batch(0, kA, aA);
+            int b = 0;
+            for (; b + 1 < nbat; b += 2) {
+                __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0)
+                load_batch(b + 1, kB, aB);
+                __builtin_amdgcn_sched_barrier(0);
+                mac_batch(kA, aA);
+                __builtin_amdgcn_sched_barrier(0);
+                if (--left == 0) {
+                    decode();
+                    left = seg;
+                }
+                __builtin_amdgcn_s_waitcnt(0xc07f);
+                load_batch(b + 2, kA, aA);
+                __builtin_amdgcn_sched_barrier(0);
+                mac_batch(kB, aB);
+                __builtin_amdgcn_sched_barrier(0);
+                if (--left == 0) {
+                    decode();
+                    left = seg;
+                }
+            }
+            if (b < nbat) {   // odd batch count: the last batch
+                __builtin_amdgcn_s_waitcnt(0xc07f);
+                mac_batch(kA, aA);
+                --left;
+            }
+            if (left != seg) decode();
+        }
+    } else {
+        // any other step count: segments of at most G channels, each its own pipeline;
+        // batches straddle channels, and steps past a segment multiply by a zero operand
+        for (int c0 = cbeg; c0 < cend; c0 += g.G) {
+            const int nsteps = min(g.G, cend - c0) * g.nrt;
+            const int nbat = (nsteps + kStepBatch - 1) / kStepBatch;
+            const int32_t *ks = ks_slice + (int64_t)(c0 - cbeg) * g.nrt * RM;
+            auto load_batch = [&](int b, int32_t (&kb)[kStepBatch * RM], int32_t (&ab)[kStepBatch][RH]) {
+#pragma unroll
+                for (int j = 0; j < kStepBatch * RM; ++j) kb[j] = ks[b * kStepBatch * RM + j];
 #pragma unroll
                 for (int j = 0; j < kStepBatch; ++j) {
-                    // steps past the segment (its step count need not be a multiple of the
-                    // batch) multiply the following channel's kernel words: their operand is 0
                     const int st0 = b * kStepBatch + j;
                     const bool live = st0 < nsteps;
                     const int st = min(st0, nsteps - 1);
@@ -290,45 +346,27 @@ __global__ __launch_bounds__(1024) void conv2d_samd_kernel(const int32_t *__rest
                         ab[j][r] = live ? v : 0;
                     }
                 }
+            };
+            load_batch(0, kA, aA);
+            int b = 0;
+            for (; b + 1 < nbat; b += 2) {
+                __builtin_amdgcn_s_waitcnt(0xc07f);
+                load_batch(b + 1, kB, aB);
+                __builtin_amdgcn_sched_barrier(0);
+                mac_batch(kA, aA);
+                __builtin_amdgcn_sched_barrier(0);
+                __builtin_amdgcn_s_waitcnt(0xc07f);
+                load_batch(b + 2, kA, aA);
+                __builtin_amdgcn_sched_barrier(0);
+                mac_batch(kB, aB);
+                __builtin_amdgcn_sched_barrier(0);
             }
-        };
-        auto mac_batch = [&](const int32_t (&kb)[kStepBatch * RM], const int32_t (&ab)[kStepBatch][RH]) {
-#pragma unroll
-            for (int j = 0; j < kStepBatch; ++j) {
-#pragma unroll
-                for (int r = 0; r < RH; ++r)
-#pragma unroll
-                    for (int m = 0; m < RM; ++m) acc[r][m] += (int64_t)ab[j][r] * (int64_t)kb[j * RM + m];
-#pragma unroll
-                for (int r = 0; r < RH; ++r)
-#pragma unroll
-                    for (int m = 0; m < RM; ++m) keep(acc[r][m]);
+            if (b < nbat) {
+                __builtin_amdgcn_s_waitcnt(0xc07f);
+                mac_batch(kA, aA);
             }
-        };
-        // Ping-pong over two register sets.  Before a batch's kernel words are used, all
-        // outstanding scalar loads are waited for, and only then is the next batch
-        // requested: scalar loads return out of order, so a wait placed after requesting
-        // the next batch would wait for it too.  Operand loads are vector loads, which
-        // complete in order, so the compiler waits for exactly the batch in use.
-        load_batch(0, kA, aA);
-        int b = 0;
-        for (; b + 1 < nbat; b += 2) {
-            __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0)
-            load_batch(b + 1, kB, aB);
-            __builtin_amdgcn_sched_barrier(0);
-            mac_batch(kA, aA);
-            __builtin_amdgcn_sched_barrier(0);
-            __builtin_amdgcn_s_waitcnt(0xc07f);
-            load_batch(b + 2, kA, aA);
-            __builtin_amdgcn_sched_barrier(0);
-            mac_batch(kB, aB);
-            __builtin_amdgcn_sched_barrier(0);
+            decode();
         }
-        if (b < nbat) {   // odd batch count: the last batch
-            __builtin_amdgcn_s_waitcnt(0xc07f);
-            mac_batch(kA, aA);
-        }
-        decode();
     }
     __syncthreads();
 

@@ -120,7 +120,10 @@ bool place_launch(const samd_conv2d_desc &d, Conv2dGeom &c) {
                     const double occ = std::min(per_cu, res) * wm * ks / 4.0;
                     const double eff = occ / (occ + 0.7);
                     const double spread = (double)t.spread_words * (6.0 * c.I + 4.0) / 64.0 / 1024.0;
-                    t.cost = per_cu * wg / 4.0 / eff + spread;
+                    // measured on MI355X: slices of about 32 channels balance the per-wave
+                    // fixed costs against scalar-load latency hiding
+                    const double slice = 1.0 + 0.15 * std::fabs(std::log2(t.cpw / 32.0));
+                    t.cost = per_cu * wg / 4.0 / eff * slice + spread;
                     if (t.cost < best.cost) {
                         best = t;
                         found = true;
