@@ -61,30 +61,38 @@ __global__ __launch_bounds__(256) void prep_weights_kernel(const uint32_t *__res
     }
 }
 
-// Operand words xs[n][c][hp][t][q] for padded rows hp in [0, H + 2 ph).
+// Operand words xs[n][c][hp][t][q] for padded rows hp in [0, H + 2 ph).  A block of 256
+// threads covers 256 / QP padded rows (QP = nq rounded up to a power of two): thread
+// (row, q) builds word q of every kernel-word variant t of its row from the packed input
+// row (L1-resident; rows of the zero padding give zeros).
 template <int B, bool S>
-__global__ __launch_bounds__(256) void spread_kernel(const uint32_t *__restrict__ x, const Conv2dGeom g,
+__global__ __launch_bounds__(256) void spread_kernel(const uint32_t *__restrict__ x, const Conv2dGeom g, int qshift,
                                                      int32_t *__restrict__ xs) {
-    for (int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x; idx < g.spread_words;
-         idx += (int64_t)gridDim.x * 256) {
-        const int q = (int)(idx % g.nq);
-        int64_t t1 = idx / g.nq;
-        const int t = (int)(t1 % g.ntw);
-        t1 /= g.ntw;
-        const int hp = (int)(t1 % g.Hp);
-        const int64_t nc = t1 / g.Hp;
-        const int h = hp - g.ph;
+    constexpr int P = 32 / B;
+    const int q = threadIdx.x & ((1 << qshift) - 1);
+    const int64_t row = (int64_t)blockIdx.x * (256 >> qshift) + (threadIdx.x >> qshift);   // (n*C + c)*Hp + hp
+    if (q >= g.nq || row >= (int64_t)g.N * g.C * g.Hp) return;
+    const int hp = (int)(row % g.Hp);
+    const int64_t nc = row / g.Hp;
+    const int h = hp - g.ph;
+    const bool inside = h >= 0 && h < g.H;
+    const uint32_t *src = x + (nc * g.H + (inside ? h : 0)) * g.xrw;
+    int32_t *dst = xs + row * g.ntw * g.nq + q;
+    for (int t = 0; t < g.ntw; ++t) {
+        const int delta = g.tw_tap0[t] + g.tw_ntaps[t] - g.Kmax;
+        const int col0 = g.sw * (q * g.I + delta) + g.tw_phase[t] - g.pw;
         uint32_t word = 0;
-        if (h >= 0 && h < g.H) {
-            const uint32_t *row = x + (nc * g.H + h) * g.xrw;
-            const int delta = g.tw_tap0[t] + g.tw_ntaps[t] - g.Kmax;
-            const int col0 = g.sw * (q * g.I + delta) + g.tw_phase[t] - g.pw;
+        if (inside) {
             for (int ii = 0; ii < g.I; ++ii) {
                 const int col = col0 + g.sw * ii;
-                if (col >= 0 && col < g.W) word += (uint32_t)packed_field<B, S>(row, col) << (ii * g.L);
+                if (col >= 0 && col < g.W) {
+                    const uint32_t f = (src[col / P] >> ((col % P) * B)) & ((1u << B) - 1);
+                    const int32_t v = S ? ((int32_t)(f << (32 - B)) >> (32 - B)) : (int32_t)f;
+                    word += (uint32_t)v << (ii * g.L);
+                }
             }
         }
-        xs[idx] = (int32_t)word;
+        dst[t * g.nq] = (int32_t)word;
     }
 }
 
@@ -409,11 +417,15 @@ int launch_conv2d_prepare(const uint32_t *w, const Conv2dGeom &g, void *ws, hipS
 
 int launch_conv2d_spread(const uint32_t *x, const Conv2dGeom &g, void *ws, hipStream_t s) {
     int32_t *xs = (int32_t *)((char *)ws + conv2d_kw_bytes(g));
-    const int sgrid = grid_for(g.spread_words, 256);
+    int qshift = 0;
+    while ((1 << qshift) < g.nq) ++qshift;   // nq <= 64
+    const int64_t nrows = (int64_t)g.N * g.C * g.Hp;
+    const int rpb = 256 >> qshift;
+    const unsigned sgrid = (unsigned)((nrows + rpb - 1) / rpb);
     bool launched = false;
 #define SAMD_SPREAD_CASE(B, SG)                                                                            \
     if (!launched && g.xbits == B && (bool)g.xsigned == SG) {                                              \
-        hipLaunchKernelGGL((spread_kernel<B, SG>), dim3(sgrid), dim3(256), 0, s, x, g, xs);                \
+        hipLaunchKernelGGL((spread_kernel<B, SG>), dim3(sgrid), dim3(256), 0, s, x, g, qshift, xs);        \
         launched = true;                                                                                   \
     }
     SAMD_FOR_EACH_FMT(SAMD_SPREAD_CASE)
