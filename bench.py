@@ -8,8 +8,10 @@ One step = one pass of the whole hot path at every bit width: pack the uint8
 activations into b-bit words, spread them into operand words (stage), multiply,
 accumulate, decode and store (accumulate).  Each layer's kernel words are prepared once,
 before timing, as weights are constant.  `value` is the whole sweep's throughput (all
-MACs of the 8 layers / wall time of the step) in GMAC/s.  Per bit width the line also
-reports each kernel's own duration (HIP events around back-to-back launches), the
+MACs of the 8 layers / wall time of the step) in GMAC/s, with the step replayed from a
+captured HIP graph; `eager_ms_per_step` is the same step launched kernel by kernel from
+Python.  Per bit width the line also reports each kernel's own duration (HIP events
+around a graph of back-to-back launches of that kernel alone), the
 native-int8 matrix-core baseline on the same layer, their speedup, and the roofline
 fractions; the CPU oracle is timed on the host.
 
@@ -87,6 +89,20 @@ def main():
             samd.pack(L["x"], L["b"], False, out=L["xp"])
             samd.conv2d_prepared(L["xp"], L["xf"], L["wf"], shape, L["ws"], out=L["y"])
 
+    def capture(fn, reps):
+        """fn() called reps times, captured once into a HIP graph (replays skip the host)."""
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            fn()
+        torch.cuda.current_stream().wait_stream(side)
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            for _ in range(reps):
+                fn()
+        return graph
+
+    # eager steps: every kernel launched from the host
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -94,20 +110,29 @@ def main():
     for _ in range(args.steps):
         step()
     torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    eager_ms = (time.perf_counter() - t0) * 1e3 / args.steps
 
-    # Per-kernel durations: HIP events on the launching stream around REPS back-to-back
-    # launches of one kernel (so the GPU never waits for the host between them).
+    # the same steps replayed from one captured graph: the rate a fixed pipeline runs at
+    step_graph = capture(step, 1)
+    for _ in range(args.warmup):
+        step_graph.replay()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step_graph.replay()
+    torch.cuda.synchronize()
+    ms_per_step = (time.perf_counter() - t0) * 1e3 / args.steps
+
+    # Per-kernel durations: HIP events on the launching stream around one replay of a
+    # graph of REPS launches of that kernel alone (the GPU never waits for the host).
     stream = torch.cuda.current_stream()
 
     def timed(fn, reps):
-        for _ in range(3):
-            fn()
+        graph = capture(fn, reps)
+        graph.replay()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record(stream)
-        for _ in range(reps):
-            fn()
+        graph.replay()
         e1.record(stream)
         e1.synchronize()
         return e0.elapsed_time(e1) * 1e-3 / reps
@@ -183,6 +208,7 @@ def main():
         "value": round(macs * len(layers) / (ms_per_step * 1e-3) / 1e9, 1),
         "unit": "GMAC/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
+        "eager_ms_per_step": round(eager_ms, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "int64", "data": "synthetic",
         "config": {"workload": "conv2d 8x128x56x56 -> 128, 3x3, stride 1, pad 1; unsigned b-bit activations x "

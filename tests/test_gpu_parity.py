@@ -305,3 +305,45 @@ def test_staged_input_accumulates_against_several_weight_sets(bits):
         y = samd.conv2d_accumulate(xf, wf, shape, ws)
         torch.cuda.synchronize()
         np.testing.assert_array_equal(y.cpu().numpy(), ref.conv2d(x, w, shape.as_tuple()))
+
+
+@pytest.mark.parametrize("bits", [1, 4, 8])
+def test_graph_replays_match_eager(bits):
+    """pack + stage + accumulate captured in a HIP graph: every replay (with eager work
+    and synchronisations in between) equals the eager result and the oracle."""
+    shape = EDGE[2]
+    xf, wf = samd.Fmt(bits, False), samd.Fmt(bits, True)
+    rng = np.random.default_rng(90 + bits)
+    x = wl.uniform(rng, (shape.N, shape.C, shape.H, shape.W), bits, False)
+    w = wl.uniform(rng, (shape.M, shape.C, shape.KH, shape.KW), bits, True)
+    want = ref.conv2d(x, w, shape.as_tuple())
+    xg = gpu_vals(x, False)
+    ws = samd.conv2d_prepare(samd.pack(gpu_vals(w, True), bits, True), wf, shape, xf)
+    xp = torch.empty((shape.N, shape.C, shape.H, samd.row_words(shape.W, bits)), dtype=torch.int32, device=DEV)
+    Ho, Wo = samd.out_hw(shape)
+    y = torch.empty((shape.N, shape.M, Ho, Wo), dtype=torch.int32, device=DEV)
+
+    def step():
+        samd.pack(xg, bits, False, out=xp)
+        samd.conv2d_prepared(xp, xf, wf, shape, ws, out=y)
+
+    step()
+    torch.cuda.synchronize()
+    eager = y.cpu().numpy()
+    np.testing.assert_array_equal(eager, want)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step()
+    torch.cuda.current_stream().wait_stream(side)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step()
+    for i in range(4):
+        y.fill_(-1)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(y.cpu().numpy(), eager, err_msg=f"replay {i}")
+        step()   # eager work between replays
+        torch.cuda.synchronize()
