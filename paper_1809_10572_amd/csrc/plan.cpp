@@ -93,7 +93,16 @@ bool place_launch(const samd_conv2d_desc &d, Conv2dGeom &c) {
                     t.mblk = wm * kWaveM;
                     t.nmb = (d.M + t.mblk - 1) / t.mblk;
                     t.tile_rows = gr * rh;
+                    // tile row stride: the columns a row needs, padded so that the rows of
+                    // neighbouring lane groups start on different LDS banks (row groups are
+                    // rh rows apart; their offset mod 32 banks should not be a multiple of
+                    // the lane stride I)
                     t.tile_row = c.nq * c.I + c.Kmax - 1;
+                    for (int pad = 0; pad < c.I && c.I > 1; ++pad)
+                        if ((rh * (t.tile_row + pad)) % 32 % c.I != 0) {
+                            t.tile_row += pad;
+                            break;
+                        }
                     t.lds_tile = (t.mblk * t.tile_rows * t.tile_row + 3) / 4 * 4;
                     t.lds_words = t.lds_tile;
                     if ((long)t.lds_words * 4 > kMaxLdsBytes) continue;
