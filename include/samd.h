@@ -75,12 +75,17 @@ enum {
  *   rows_per_block, mblock: output rows and output channels of one workgroup's tile
  *   split_waves  waves that share one tile's output channels, each multiplying its own
  *                slice of every chunk of input channels (their sums meet in the tile)
- *   chunk_channels input channels staged in LDS per chunk
+ *   chunk_channels input channels per wave slice times split_waves
+ *   x_offset     0, or 2^(b-1) when unsigned activations are recentred: x - x_offset
+ *                (a signed b-bit value) enters the lanes, halving the largest product,
+ *                and x_offset times the sum of each output's in-image weights is added
+ *                back when the output is stored
  *   macs_per_mad multiply-accumulates delivered per 32x32->64 multiply (I * taps) */
 typedef struct {
     int32_t lane_bits, lanes, taps_max, words_per_row, flush_channels, out_lanes, tap_words;
     int32_t phase[16], tap0[16], ntaps[16];
     int32_t rows_per_block, mblock, split_waves, chunk_channels;
+    int32_t x_offset;
     double macs_per_mad;
 } samd_conv2d_plan;
 

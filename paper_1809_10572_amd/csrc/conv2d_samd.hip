@@ -61,7 +61,29 @@ __global__ __launch_bounds__(256) void prep_weights_kernel(const uint32_t *__res
     }
 }
 
-// Operand words xs[n][c][hp][t][q] for padded rows hp in [0, H + 2 ph).  A block of 256
+// Correction table of recentred activations: pre[m][i][j] = sum of w[m][c][ky][kx] over
+// all c, ky < i, kx < j (i <= KH, j <= KW), so an output's in-image taps [ky0, ky1) x
+// [kx0, kx1) sum to a rectangle of four entries.
+template <int B, bool S>
+__global__ __launch_bounds__(256) void prefix_kernel(const uint32_t *__restrict__ w, const Conv2dGeom g,
+                                                     int32_t *__restrict__ pre) {
+    const int pwid = (g.KH + 1) * (g.KW + 1);
+    const int total = g.M * pwid;
+    for (int e = blockIdx.x * 256 + threadIdx.x; e < total; e += gridDim.x * 256) {
+        const int m = e / pwid, ij = e - m * pwid;
+        const int i = ij / (g.KW + 1), j = ij - i * (g.KW + 1);
+        int32_t sum = 0;
+        for (int c = 0; c < g.C; ++c)
+            for (int ky = 0; ky < i; ++ky) {
+                const uint32_t *row = w + ((int64_t)(m * g.C + c) * g.KH + ky) * g.wrw;
+                for (int kx = 0; kx < j; ++kx) sum += packed_field<B, S>(row, kx);
+            }
+        pre[e] = sum;
+    }
+}
+
+// Operand words xs[n][c][hp][t][q] for padded rows hp in [0, H + 2 ph), of the
+// activations minus xoff (recentred unsigned activations).  A block of 256
 // threads covers 256 / QP padded rows (QP = nq rounded up to a power of two): thread
 // (row, q) builds word q of every kernel-word variant t of its row from the packed input
 // row (L1-resident; rows of the zero padding give zeros).
@@ -87,7 +109,7 @@ __global__ __launch_bounds__(256) void spread_kernel(const uint32_t *__restrict_
                 const int col = col0 + g.sw * ii;
                 if (col >= 0 && col < g.W) {
                     const uint32_t f = (src[col / P] >> ((col % P) * B)) & ((1u << B) - 1);
-                    const int32_t v = S ? ((int32_t)(f << (32 - B)) >> (32 - B)) : (int32_t)f;
+                    const int32_t v = (S ? ((int32_t)(f << (32 - B)) >> (32 - B)) : (int32_t)f) - g.xoff;
                     word += (uint32_t)v << (ii * g.L);
                 }
             }
@@ -168,7 +190,8 @@ __device__ __forceinline__ void decode_word_n(uint64_t v, uint64_t msb_mask, int
 // signed (either operand signed), so lanes need the fix-up and are sign-extended.
 template <int RH, int NRT, bool SG>
 __global__ __launch_bounds__(1024) void conv2d_samd_kernel(const int32_t *__restrict__ xs,
-                                                           const int32_t *__restrict__ kw, int32_t *__restrict__ y,
+                                                           const int32_t *__restrict__ kw,
+                                                           const int32_t *__restrict__ pre, int32_t *__restrict__ y,
                                                            const Conv2dGeom g) {
     extern __shared__ int32_t lds[];
     int32_t *tile = lds;
@@ -388,7 +411,20 @@ __global__ __launch_bounds__(1024) void conv2d_samd_kernel(const int32_t *__rest
         if (m < g.M && ho < g.Ho) {
             const int32_t *src = tile + (mm * g.tile_rows + r) * g.tile_row + (g.Kmax - 1);
             int32_t *dst = y + (((int64_t)n * g.M + m) * g.Ho + ho) * g.Wo;
-            for (int o = lane; o < g.Wo; o += 64) dst[o] = src[o];
+            if (g.xoff == 0) {
+                for (int o = lane; o < g.Wo; o += 64) dst[o] = src[o];
+            } else {
+                // recentred activations: + xoff * (weights over the output's in-image taps)
+                const int hb = ho * g.sh - g.ph, kwid = g.KW + 1;
+                const int ky0 = max(0, -hb) * kwid, ky1 = min(g.KH, g.H - hb) * kwid;
+                const int32_t *pm = pre + m * (g.KH + 1) * kwid;
+                for (int o = lane; o < g.Wo; o += 64) {
+                    const int wb = o * g.sw - g.pw;
+                    const int kx0 = max(0, -wb), kx1 = min(g.KW, g.W - wb);
+                    const int32_t rect = pm[ky1 + kx1] - pm[ky0 + kx1] - pm[ky1 + kx0] + pm[ky0 + kx0];
+                    dst[o] = src[o] + g.xoff * rect;
+                }
+            }
         }
         mm += dmm;
         r += dr;
@@ -412,11 +448,23 @@ int launch_conv2d_prepare(const uint32_t *w, const Conv2dGeom &g, void *ws, hipS
     }
     SAMD_FOR_EACH_FMT(SAMD_PREP_CASE)
 #undef SAMD_PREP_CASE
-    return check_launch("conv2d weight preparation");
+    int st = check_launch("conv2d weight preparation");
+    if (st || !g.xoff) return st;
+    int32_t *pre = (int32_t *)((char *)ws + conv2d_kw_bytes(g));
+    const int fgrid = grid_for((int64_t)g.M * (g.KH + 1) * (g.KW + 1), 256);
+    launched = false;
+#define SAMD_PREFIX_CASE(B, SG)                                                                          \
+    if (!launched && g.wbits == B && (bool)g.wsigned == SG) {                                            \
+        hipLaunchKernelGGL((prefix_kernel<B, SG>), dim3(fgrid), dim3(256), 0, s, w, g, pre);             \
+        launched = true;                                                                                 \
+    }
+    SAMD_FOR_EACH_FMT(SAMD_PREFIX_CASE)
+#undef SAMD_PREFIX_CASE
+    return check_launch("conv2d correction table");
 }
 
 int launch_conv2d_spread(const uint32_t *x, const Conv2dGeom &g, void *ws, hipStream_t s) {
-    int32_t *xs = (int32_t *)((char *)ws + conv2d_kw_bytes(g));
+    int32_t *xs = (int32_t *)((char *)ws + conv2d_kw_bytes(g) + conv2d_pre_bytes(g));
     int qshift = 0;
     while ((1 << qshift) < g.nq) ++qshift;   // nq <= 64
     const int64_t nrows = (int64_t)g.N * g.C * g.Hp;
@@ -435,13 +483,14 @@ int launch_conv2d_spread(const uint32_t *x, const Conv2dGeom &g, void *ws, hipSt
 
 int launch_conv2d_multiply(const Conv2dGeom &g, int32_t *y, const void *ws, hipStream_t s) {
     const int32_t *kw = (const int32_t *)ws;
-    const int32_t *xs = (const int32_t *)((const char *)ws + conv2d_kw_bytes(g));
+    const int32_t *pre = (const int32_t *)((const char *)ws + conv2d_kw_bytes(g));
+    const int32_t *xs = (const int32_t *)((const char *)ws + conv2d_kw_bytes(g) + conv2d_pre_bytes(g));
     const dim3 grid((unsigned)g.tiles * g.nmb), block(g.wm * g.ks * 64);
     const size_t shm = (size_t)g.lds_words * 4;
 #define SAMD_CONV_CASE(RH_, NRT_, SG_)                                                                \
     if (g.rh == RH_ && (NRT_ == 0 ? (g.nrt != 3 && g.nrt != 6) : g.nrt == NRT_) &&                     \
         (bool)g.result_signed == SG_) {                                                               \
-        hipLaunchKernelGGL((conv2d_samd_kernel<RH_, NRT_, SG_>), grid, block, shm, s, xs, kw, y, g);   \
+        hipLaunchKernelGGL((conv2d_samd_kernel<RH_, NRT_, SG_>), grid, block, shm, s, xs, kw, pre, y, g);   \
         return check_launch("conv2d");                                                                \
     }
     SAMD_CONV_CASE(1, 3, false) SAMD_CONV_CASE(1, 6, false) SAMD_CONV_CASE(1, 0, false)

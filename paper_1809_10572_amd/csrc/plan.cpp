@@ -153,13 +153,18 @@ bool place_launch(const samd_conv2d_desc &d, Conv2dGeom &c) {
 
 namespace {
 
-int search_conv2d(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, Conv2dGeom &best, std::string &err) {
+// xf: the activations as the lanes see them; xoff: the value subtracted from every
+// stored activation before it enters a lane (0, or 2^(b-1) for recentred unsigned
+// activations, which then behave as signed b-bit values).
+int search_lanes(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, int xoff, Conv2dGeom &best,
+                 std::string &err) {
     Conv2dGeom g = {};
     g.N = d.N; g.C = d.C; g.H = d.H; g.W = d.W; g.M = d.M; g.KH = d.KH; g.KW = d.KW;
     g.sh = d.stride_h; g.sw = d.stride_w; g.ph = d.pad_h; g.pw = d.pad_w;
     g.Ho = (d.H + 2 * d.pad_h - d.KH) / d.stride_h + 1;
     g.Wo = (d.W + 2 * d.pad_w - d.KW) / d.stride_w + 1;
-    g.xbits = xf.bits; g.xsigned = xf.is_signed; g.wbits = wf.bits; g.wsigned = wf.is_signed;
+    g.xbits = xf.bits; g.xsigned = xoff ? 0 : xf.is_signed; g.wbits = wf.bits; g.wsigned = wf.is_signed;
+    g.xoff = xoff;
     g.result_signed = (xf.is_signed || wf.is_signed) ? 1 : 0;
     g.xrw = (int32_t)row_words(d.W, xf.bits);
     g.wrw = (int32_t)row_words(d.KW, wf.bits);
@@ -254,6 +259,28 @@ int search_conv2d(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, Conv2dGeo
     return SAMD_OK;
 }
 
+// Unsigned activations with signed weights may also be recentred: x - 2^(b-1) is a
+// signed b-bit value, so products are half as large and a lane holds twice as many;
+// the offset comes back exactly as 2^(b-1) times the sum of the weights over each
+// output's in-image taps.  Both are planned and the cheaper kept.
+int search_conv2d(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, Conv2dGeom &best, std::string &err) {
+    int st = search_lanes(d, xf, wf, 0, best, err);
+    if (!xf.is_signed && wf.is_signed && xf.bits >= 2) {
+        Conv2dGeom alt;
+        std::string err2;
+        const samd_fmt xs = {xf.bits, 1};
+        if (search_lanes(d, xs, wf, 1 << (xf.bits - 1), alt, err2) == SAMD_OK) {
+            // the correction: four table lookups and a multiply-add per output
+            alt.cost += (double)d.N * d.M * alt.Ho * alt.Wo * 8.0 / 64.0 / 1024.0;
+            if (st != SAMD_OK || alt.cost < best.cost) {
+                best = alt;
+                st = SAMD_OK;
+            }
+        }
+    }
+    return st;
+}
+
 // Plans are a pure function of (shape, formats); the search prices thousands of launch
 // shapes, so found plans are kept (under a lock) and later calls look them up.
 using PlanKey = std::array<int32_t, 15>;
@@ -286,11 +313,15 @@ int plan_conv2d(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, Conv2dGeom 
 // Workspace: kernel-word streams, then the operand words of one call (256-byte aligned).
 size_t conv2d_kw_bytes(const Conv2dGeom &g) { return ((size_t)g.kw_words * 4 + 255) / 256 * 256; }
 
+size_t conv2d_pre_bytes(const Conv2dGeom &g) {
+    return g.xoff ? ((size_t)g.M * (g.KH + 1) * (g.KW + 1) * 4 + 255) / 256 * 256 : 0;
+}
+
 size_t conv2d_workspace_bytes(const Conv2dGeom &g) {
     // one spare channel after the last image: the batch fetched after a slice's last one
     // may read it (its products are never used)
     const size_t spare = (size_t)g.Hp * g.ntw * g.nq;
-    return conv2d_kw_bytes(g) + ((size_t)(g.spread_words + spare) * 4 + 255) / 256 * 256;
+    return conv2d_kw_bytes(g) + conv2d_pre_bytes(g) + ((size_t)(g.spread_words + spare) * 4 + 255) / 256 * 256;
 }
 
 int plan_conv1d(int64_t n, samd_fmt xf, const int32_t *taps, int32_t K, samd_fmt kf, Conv1dGeom &best,

@@ -33,7 +33,9 @@ constexpr int kMaxLdsBytes = 65536; // LDS per conv2d workgroup
 // operand-word variant, stored at index t.
 struct Conv2dGeom {
     int32_t N, C, H, W, M, KH, KW, sh, sw, ph, pw, Ho, Wo, Hp;
-    int32_t xbits, xsigned, wbits, wsigned;
+    int32_t xbits, xsigned, wbits, wsigned;   // xsigned: how stored activations are read
+    int32_t xoff;                   // subtracted from every activation (recentred unsigned
+                                    // activations: 2^(xbits-1)); 0 otherwise
     int32_t L, I, Kmax, nq, G;      // lane bits, values/word, widest phase, words/row, flush channels
     int32_t nl;                     // decoded lanes per accumulator; lane nl-1 takes the remaining bits
     int32_t result_signed;          // any operand signed: lanes need the fix-up
@@ -60,7 +62,8 @@ struct Conv2dGeom {
     int32_t tile_row;               // output-tile words per row: nq * I + Kmax - 1 (column o at o + Kmax - 1)
     int32_t lds_tile;               // LDS words of the output tile (a multiple of 4)
     int32_t lds_words;              // LDS words in all
-    int64_t kw_words, spread_words; // workspace: kernel-word streams, operand words
+    int64_t kw_words, spread_words; // workspace: kernel-word streams, operand words (after the
+                                    // correction table when xoff != 0)
     double macs_per_mad, cost;
 };
 
@@ -82,6 +85,7 @@ int plan_conv1d(int64_t n, samd_fmt xf, const int32_t *taps, int32_t K, samd_fmt
                 std::string &err);
 size_t conv2d_workspace_bytes(const Conv2dGeom &g);
 size_t conv2d_kw_bytes(const Conv2dGeom &g);
+size_t conv2d_pre_bytes(const Conv2dGeom &g);   // the recentring correction table
 
 // Kernel launchers (enqueue only; report launch errors through the return value).
 int launch_pack(const void *src, int64_t rows, int64_t len, int bits, int is_signed, uint32_t *dst,

@@ -47,11 +47,13 @@ def planned_conv2d(x, w, shape, xf, wf, plan):
     L, I, Kmax, G = plan.lane_bits, plan.lanes, plan.taps_max, plan.flush_channels
     nq = plan.words_per_row
     tws = tap_words(plan)
-    signed = bool(xf.is_signed or wf.is_signed)
+    off = plan.x_offset
+    signed = bool(xf.is_signed or wf.is_signed or off)
     y = np.zeros((N, M, Ho, Wo), dtype=np.int64)
 
     def xval(n, c, h, col):
-        return int(x[n, c, h, col]) if 0 <= h < H and 0 <= col < W else 0
+        # recentred activations enter the lanes as x - off; the zero padding stays 0
+        return int(x[n, c, h, col]) - off if 0 <= h < H and 0 <= col < W else 0
 
     nl_max = plan.out_lanes
     for n, m, ho in itertools.product(range(N), range(M), range(Ho)):
@@ -73,6 +75,10 @@ def planned_conv2d(x, w, shape, xf, wf, plan):
                         if 0 <= o < Wo:
                             y[n, m, ho, o] += d
                     acc = 0
+    if off:
+        # add back off * (the weights of every output's in-image taps)
+        ones = np.ones((N, C, H, W), dtype=np.int64)
+        y += off * ref.conv2d(ones, w, shape)
     return y
 
 
@@ -120,12 +126,13 @@ def test_planned_geometry_is_exact_at_the_bound(name, shape, xf, wf):
     assert 1 <= G <= shape.C and plan.macs_per_mad > 0
     tws = tap_words(plan)
     assert sum(k for (_, _, k) in tws) == shape.KW
-    xlo, xhi = wl.value_range(xf.bits, bool(xf.is_signed))
+    # recentred unsigned activations reach the lanes as signed b-bit values
+    xlo, xhi = wl.value_range(xf.bits, bool(xf.is_signed) or plan.x_offset != 0)
     wlo, whi = wl.value_range(wf.bits, bool(wf.is_signed))
     for lo, hi, n in [(xlo, xhi, I)] + [(wlo, whi, k) for (_, _, k) in tws]:
         place = sum(1 << (i * L) for i in range(n))
         assert lo * place >= I32[0] and hi * place <= I32[1]
-    signed = bool(xf.is_signed or wf.is_signed)
+    signed = bool(xf.is_signed or wf.is_signed or plan.x_offset)
     rnd = random.Random(hash(name) & 0xFFFF)
     rows = G * shape.KH
     # adversarial operands: every product at its most positive / most negative value,
