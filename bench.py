@@ -33,20 +33,105 @@ PEAK_I8_MACS = 2.5e15                 # dense int8 matrix-core MAC/s (5.0 POP/s)
 def parse():
     p = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=100)
-    p.add_argument("--warmup", type=int, default=10)
+    p.add_argument("--steps", type=int, default=1000)
+    p.add_argument("--warmup", type=int, default=1000)
     p.add_argument("--bits", default="1,2,3,4,5,6,7,8")
     p.add_argument("--reps", type=int, default=20, help="back-to-back launches per kernel timing")
+    p.add_argument("--kernel-warm-s", type=float, default=0.2,
+                   help="seconds of back-to-back replays before each kernel's timed replay (clocks settle)")
     p.add_argument("--cpu-seconds", type=float, default=10.0, help="CPU oracle sample budget")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-check", action="store_true", help="skip the sampled parity check")
+    p.add_argument("--counters", action="store_true",
+                   help="launch each kernel once per bit width, eagerly, then a 1 GiB streaming copy, and exit "
+                        "(the program rocprofv3 --pmc passes run)")
+    p.add_argument("--traffic-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                   help="print the HBM-traffic summary of two rocprofv3 --pmc output folders of --counters runs "
+                        "(FETCH_SIZE, then WRITE_SIZE) and exit")
     return p.parse_args()
+
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+TRAFFIC_FILE = os.path.join(HERE, "profiles", "conv2d_samd_mid_sweep_hbm_traffic.md")
+COPY_BYTES = 1 << 30                  # the calibration copy reads and writes this many bytes
+
+
+def kernel_source_sha():
+    """Hash of the sources that decide what the SAMD conv kernel reads and writes."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in ("conv2d_samd.hip", "plan.cpp", "samd_internal.hpp"):
+        with open(os.path.join(HERE, "paper_1809_10572_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def read_counter_csv(folder, counter):
+    """{dispatch id: (kernel name, value)} of one counter from a rocprofv3 csv output folder."""
+    import csv
+    import glob
+    files = glob.glob(os.path.join(folder, "**", "*counter_collection.csv"), recursive=True)
+    if len(files) != 1:
+        raise SystemExit(f"expected one counter_collection.csv under {folder}, found {len(files)}")
+    out = {}
+    with open(files[0]) as fh:
+        for row in csv.DictReader(fh):
+            if row["Counter_Name"] == counter:
+                d = int(row["Dispatch_Id"])
+                name, v = out.get(d, (row["Kernel_Name"], 0.0))
+                out[d] = (name, v + float(row["Counter_Value"]))
+    return out
+
+
+def traffic_summary(fetch_dir, write_dir, bits_list):
+    """HBM bytes per launch of the SAMD conv kernel at each bit width, from FETCH_SIZE and
+    WRITE_SIZE (KiB per dispatch) scaled by what the counters read for a copy of known size."""
+    per = {}
+    for key, folder, counter in (("fetch", fetch_dir, "FETCH_SIZE"), ("write", write_dir, "WRITE_SIZE")):
+        rows = read_counter_csv(folder, counter)
+        order = sorted(rows)
+        conv = [rows[d][1] for d in order if "conv2d_samd_kernel" in rows[d][0]]
+        copy = [rows[d][1] for d in order if "bitwise_not" in rows[d][0]]
+        if len(conv) != len(bits_list) or len(copy) < 1:
+            raise SystemExit(f"{folder}: {len(conv)} conv dispatches for bits {bits_list}, {len(copy)} copies")
+        factor = COPY_BYTES / (copy[-1] * 1024.0)
+        per[key] = (conv, copy[-1], factor)
+    res = {"kernel": "conv2d_samd_kernel", "source_sha256": kernel_source_sha(),
+           "copy": {"bytes_each_way": COPY_BYTES, "fetch_kib": per["fetch"][1], "write_kib": per["write"][1],
+                    "fetch_factor": round(per["fetch"][2], 4), "write_factor": round(per["write"][2], 4)},
+           "per_bits": {}}
+    tot = 0.0
+    for i, b in enumerate(bits_list):
+        fk, wk = per["fetch"][0][i], per["write"][0][i]
+        fb, wb = fk * 1024 * per["fetch"][2], wk * 1024 * per["write"][2]
+        res["per_bits"][str(b)] = {"fetch_kib": fk, "write_kib": wk, "fetch_bytes": round(fb), "write_bytes": round(wb)}
+        tot += fb + wb
+    res["bytes_per_launch"] = round(tot / len(bits_list))
+    return res
+
+
+def stored_traffic():
+    """The traffic summary committed under profiles/, or None when the kernel's sources have
+    changed since the counters were taken."""
+    try:
+        text = open(TRAFFIC_FILE).read()
+    except OSError:
+        return None
+    start = text.find("```json")
+    if start < 0:
+        return None
+    end = text.find("```", start + 7)
+    data = json.loads(text[start + 7:end])
+    return data if data.get("source_sha256") == kernel_source_sha() else None
 
 
 def main():
     args = parse()
+    if args.traffic_summary:
+        print(json.dumps(traffic_summary(*args.traffic_summary, [int(b) for b in args.bits.split(",")]), indent=1))
+        return
     if args.gpus != 1:
-        print("bench.py measures one GPU: this build runs on a single MI355X and has no multi-GPU path "
+        print("bench.py measures one GPU: the SAMD library runs on a single MI355X and has no multi-GPU path "
               "(--gpus must be 1)", file=sys.stderr)
         sys.exit(2)
     import numpy as np
@@ -83,6 +168,24 @@ def main():
     # the layer's kernel words are prepared once per layer (weights are constant)
     for L in layers:
         samd.conv2d_prepare(L["wp"], L["wf"], shape, L["xf"], ws=L["ws"])
+
+    if args.counters:
+        # one eager launch of each kernel per bit width, in step order, then the calibration
+        # copy (twice; the second is the one read)
+        for L in layers:
+            samd.pack(L["x"], L["b"], False, out=L["xp"])
+            samd.conv2d_stage(L["xp"], L["xf"], L["wf"], shape, L["ws"])
+            samd.conv2d_accumulate(L["xf"], L["wf"], shape, L["ws"], out=L["y"])
+            samd.conv2d_int8_prepared(L["x_nhwc"], L["xf"], L["wf"], shape, L["ws8"], out=L["y8"])
+            torch.cuda.synchronize()
+            print(f"counters: b={L['b']} launched", flush=True)
+        src = torch.empty(COPY_BYTES // 4, dtype=torch.int32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(2):
+            torch.bitwise_not(src, out=dst)
+        torch.cuda.synchronize()
+        print(f"counters: copy of {COPY_BYTES} bytes done; kernel sources {kernel_source_sha()}", flush=True)
+        return
 
     def step():
         for L in layers:
@@ -130,6 +233,11 @@ def main():
     def timed(fn, reps):
         graph = capture(fn, reps)
         graph.replay()
+        torch.cuda.synchronize()
+        t_end = time.perf_counter() + args.kernel_warm_s
+        while time.perf_counter() < t_end:
+            graph.replay()
+            torch.cuda.synchronize()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record(stream)
         graph.replay()
@@ -158,7 +266,8 @@ def main():
             got8 = L["y8"].cpu().numpy()[tuple(idx.T)]
             parity[L["b"]] = bool(np.array_equal(got, want) and np.array_equal(got8, want))
 
-    per_bits, tot_mads, tot_conv_s = {}, 0.0, 0.0
+    traffic = stored_traffic()
+    per_bits, tot_mads, tot_conv_s, tot_alg_bytes = {}, 0.0, 0.0, 0.0
     for L in layers:
         t, t8 = L["t_conv"], L["t_int8"]
         p = L["plan"]
@@ -169,6 +278,7 @@ def main():
                      + N * M * Ho * Wo * 4)
         tot_mads += mads
         tot_conv_s += t
+        tot_alg_bytes += hbm_bytes
         per_bits[str(b)] = {
             "conv_us": round(t * 1e6, 2), "stage_us": round(L["t_stage"] * 1e6, 2),
             "pack_us": round(L["t_pack"] * 1e6, 2),
@@ -178,6 +288,9 @@ def main():
             "speedup_vs_int8": round(t8 / (t + L["t_stage"]), 3),
             "valu_frac": round(mads / t / PEAK_VALU_OPS, 4),
             "hbm_frac": round(hbm_bytes / t / PEAK_HBM, 4),
+            "hbm_bytes_alg": hbm_bytes,
+            "hbm_bytes_counted": (traffic["per_bits"][str(b)]["fetch_bytes"] + traffic["per_bits"][str(b)]["write_bytes"]
+                                  if traffic and str(b) in traffic["per_bits"] else None),
             "int8_mfma_frac": round(macs / t8 / PEAK_I8_MACS, 4),
             "lane_bits": p.lane_bits, "lanes": p.lanes, "tap_words": p.tap_words,
             "flush_channels": p.flush_channels, "macs_per_mad": round(p.macs_per_mad, 2),
@@ -215,7 +328,12 @@ def main():
                                "signed b-bit weights; one step = pack + stage + accumulate at each b (kernel words prepared once per layer)",
                    "bits": bits_list, "global_batch": N, "macs_per_layer": macs},
         "roofline": {"bound": "alu", "achieved": round(achieved / 1e12, 3), "peak": round(PEAK_VALU_OPS / 1e12, 2),
-                     "unit": "TOP/s", "frac": round(achieved / PEAK_VALU_OPS, 4), "traffic": None,
+                     "unit": "TOP/s", "frac": round(achieved / PEAK_VALU_OPS, 4),
+                     # HBM bytes per launch counted by FETCH_SIZE + WRITE_SIZE (mean over the bit
+                     # widths), next to the algorithmic bytes the kernel must move
+                     "traffic": (round(sum(v["hbm_bytes_counted"] for v in per_bits.values()) / len(layers))
+                                 if all(v["hbm_bytes_counted"] is not None for v in per_bits.values()) else None),
+                     "alg_bytes_per_launch": round(tot_alg_bytes / len(layers)),
                      "kernel": "conv2d_samd_kernel", "op": "32x32->64-bit multiply-accumulate (v_mad_i64_i32)"},
         "cpu_baseline": cpu,
         "per_bits": per_bits,
