@@ -18,6 +18,9 @@
 #include <hip/hip_runtime.h>
 
 #include <climits>
+#include <map>
+#include <mutex>
+#include <tuple>
 
 #include "hip_util.hpp"
 
@@ -35,11 +38,15 @@ __device__ inline int32_t packed_field(const uint32_t *row, int col) {
     return (int32_t)f;
 }
 
-// Kernel-word stream of output-channel group wb: step s = c*nrt + ky*ntw + t holds the
-// kWaveM words of kernel word t of row ky of channel c; kStreamPad zero steps pad the end.
+// Kernel-word stream of output-channel group wb: step s = c*nrt + ky*ntw + t (or
+// c*nrt + t*KH + ky on the shared-row path) holds the kWaveM words of kernel word t of
+// row ky of channel c; kStreamPad zero steps pad the end.
+// Also zeroes the multiply kernel's ticket counters.
 template <int B, bool S>
 __global__ __launch_bounds__(256) void prep_weights_kernel(const uint32_t *__restrict__ w, const Conv2dGeom g,
-                                                           int32_t *__restrict__ kw) {
+                                                           int32_t *__restrict__ kw, int32_t *__restrict__ queue) {
+    if (blockIdx.x == 0)
+        for (int i = threadIdx.x; i < kQueueBytes / 4; i += 256) queue[i] = 0;
     const int64_t steps = (int64_t)g.C * g.nrt + kStreamPad;
     for (int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x; idx < g.kw_words; idx += (int64_t)gridDim.x * 256) {
         const int mm = (int)(idx % RM);
@@ -49,7 +56,9 @@ __global__ __launch_bounds__(256) void prep_weights_kernel(const uint32_t *__res
         uint32_t word = 0;
         if (m < g.M && s < (int64_t)g.C * g.nrt) {
             const int c = (int)(s / g.nrt), rt = (int)(s % g.nrt);
-            const int ky = rt / g.ntw, t = rt % g.ntw;
+            // steps of a channel: kernel-row-major, or kernel-word-major for the
+            // shared-row path
+            const int ky = g.rows_path ? rt % g.KH : rt / g.ntw, t = g.rows_path ? rt / g.KH : rt % g.ntw;
             const uint32_t *row = w + ((int64_t)(m * g.C + c) * g.KH + ky) * g.wrw;
             const int k = g.tw_ntaps[t], a0 = g.tw_tap0[t], r = g.tw_phase[t];
             for (int si = 0; si < k; ++si) {
@@ -176,35 +185,53 @@ __device__ __forceinline__ void decode_word_n(uint64_t v, uint64_t msb_mask, int
     atomicAdd(p + nl - 1, (int32_t)v);
 }
 
-// A workgroup has wm x ks waves and owns rows_blk output rows x all Wo columns x mblk
-// output channels of one image.  Wave (kq, mw) computes output channels mw*8 .. +7 of the
-// block over its slice kq of the input channels; lane (grp, q) holds output word q of rows
-// grp*RH .. +RH-1.  Operand words come straight from the spread buffer (global memory,
-// L1/L2-resident: every word is reused by the block's wm waves and its KH kernel rows),
-// kernel words from the wave's stream through scalar loads.  After at most G channels the
-// accumulators are decoded into an LDS tile of int32 outputs whose atomic adds also sum
-// the ks channel slices and overlap-add neighbouring words' partial lanes.
+// Work item: rows_blk output rows x all Wo columns x mblk output channels of one image,
+// computed by one workgroup of wm x ks waves.  Wave (kq, mw) computes output channels
+// mw*8 .. +7 of the block over its slice kq of the input channels; lane (grp, q) holds
+// output word q of rows grp*RH .. +RH-1.  Operand words come straight from the spread
+// buffer (global memory, L1/L2-resident: every word is reused by the block's wm waves and
+// its KH kernel rows), kernel words from the wave's stream through scalar loads.  After at
+// most G channels the accumulators are decoded into an LDS tile of int32 outputs whose
+// atomic adds also sum the ks channel slices and overlap-add neighbouring words' partial
+// lanes.
+//
+// The grid holds at most as many workgroups as the chip keeps resident.  XCD x (hardware
+// assigns workgroup p to XCD p % 8) owns the spatial tiles t = x (mod 8), each with all its
+// channel blocks in consecutive items, so a tile's operand words are fetched into that
+// XCD's L2 and reused there.  Workgroup p first computes item p / 8 of its XCD; the items
+// beyond the XCD's workgroups go to whichever workgroup frees up first, through a ticket
+// counter per XCD: waves of equal work finish far apart (the SIMD issues the oldest wave
+// first), and a fixed assignment would leave the chip draining for much of the launch.
+// A launch takes exactly T = extra items + workgroups tickets from each counter (every
+// workgroup ends on one ticket past the items), so ticket t stands for local index
+// t mod T: the counters never need resetting between launches.  Each workgroup asks for
+// its next ticket when it starts an item, so the atomic's latency hides behind the item.
 //
 // NRT: steps (kernel row x kernel word) per input channel when it is 3 or 6 (every 3x3
 // layer), so batches never straddle channels; 0 for any other count.  SG: the result is
-// signed (either operand signed), so lanes need the fix-up and are sign-extended.
-template <int RH, int NRT, bool SG>
+// signed (either operand signed), so lanes need the fix-up and are sign-extended.  RNTW:
+// 0, or the kernel words per kernel row (1 or 2) of a 3-row, stride-1 kernel whose rows
+// share operand loads: output row r with kernel row ky reads input row r + ky, so the
+// lane's RH rows need RH + 2 operand words per (channel, kernel word) instead of 3 RH.
+// Every operand load costs the compute unit's texture path far more cycles than a
+// multiply-add costs a SIMD, and the four SIMDs share that path, so loads, not
+// multiply-adds, bound the loop unless each load feeds enough of them.
+template <int RH, int NRT, bool SG, int RNTW>
 __global__ __launch_bounds__(1024) void conv2d_samd_kernel(const int32_t *__restrict__ xs,
                                                            const int32_t *__restrict__ kw,
                                                            const int32_t *__restrict__ pre, int32_t *__restrict__ y,
+                                                           unsigned long long *__restrict__ tickets,
                                                            const Conv2dGeom g) {
     extern __shared__ int32_t lds[];
     int32_t *tile = lds;
+    __shared__ int32_t next_item;
 
-    // Consecutive workgroups on one XCD (hardware assigns workgroup p to XCD p % 8) take
-    // all channel blocks of one spatial tile, so its operand words are reused from L2.
-    const int p = blockIdx.x;
-    const int slot = p >> 3;
-    const int mb = slot % g.nmb;
-    const int tile_id = (slot / g.nmb) * 8 + (p & 7);
-    if (tile_id >= g.N * g.row_tiles) return;   // padding workgroup: exits as a whole
-    const int n = tile_id / g.row_tiles;
-    const int ho0 = (tile_id % g.row_tiles) * g.rows_blk;
+    const int xcd = blockIdx.x % kNumXcd;
+    const int ntiles = g.N * g.row_tiles;
+    const int nitems = (ntiles - xcd + kNumXcd - 1) / kNumXcd * g.nmb;   // items of this XCD
+    const int nwg = gridDim.x / kNumXcd;                                 // workgroups of this XCD
+    const int nextra = max(0, nitems - nwg);                             // items handed out by ticket
+    unsigned long long *const counter = tickets + xcd * (kTicketStride / 8);
 
     const int tid = threadIdx.x;
     const int nthr = g.wm * g.ks * 64;
@@ -216,28 +243,11 @@ __global__ __launch_bounds__(1024) void conv2d_samd_kernel(const int32_t *__rest
     const bool lane_ok = grp_raw < g.groups;
     const int grp = lane_ok ? grp_raw : 0;
     const int q = lane_ok ? lane - grp_raw * g.nq : 0;
-    const int wb = mb * g.wm + mw;
 
     {
         int4 *t4 = (int4 *)tile;   // lds_tile is a multiple of 4 words
         for (int i = tid; i < g.lds_tile / 4; i += nthr) t4[i] = int4{0, 0, 0, 0};
     }
-    __syncthreads();
-
-    // Operand word of step s (s = ky*ntw + t) of channel c for this lane's row r:
-    // xs[n][c][hp][t][q] with hp = (ho0 + row)*sh + ky, i.e. word
-    // (c*Hp*ntw + (ho0 + row)*sh*ntw + s)*nq + q of image n.  Rows past the image (the last
-    // row tile, idle lanes) read the last output row's inputs; their sums are not stored.
-    const int ch_stride = g.Hp * g.ntw * g.nq;
-    int lb[RH];   // byte offset of the lane's word in channel 0, step 0
-#pragma unroll
-    for (int r = 0; r < RH; ++r) {
-        const int row = min(ho0 + min(grp * RH + r, g.rows_blk - 1), g.Ho - 1);
-        lb[r] = (row * g.sh * g.ntw * g.nq + q) * 4;
-    }
-    // the image's channels and one spare channel after them
-    const __amdgpu_buffer_rsrc_t xrs = __builtin_amdgcn_make_buffer_rsrc(
-        (void *)(xs + (int64_t)n * g.C * ch_stride), (short)0, (g.C + 1) * ch_stride * 4, kBufferWord3);
 
     int64_t acc[RH][RM];
 #pragma unroll
@@ -245,35 +255,41 @@ __global__ __launch_bounds__(1024) void conv2d_samd_kernel(const int32_t *__rest
 #pragma unroll
         for (int m = 0; m < RM; ++m) acc[r][m] = 0;
 
-    const int64_t stream_len = ((int64_t)g.C * g.nrt + kStreamPad) * RM;
-    const int32_t *kstream = kw + wb * stream_len;
-
     // Decode: lane j of word q goes to output column q*I + j - (Kmax-1), stored at tile
     // column q*I + j.  Tile rows cover every row a wave computes, so no lane needs a
-    // bounds check.
-    int32_t *const tbase = tile + ((mw * RM) * g.tile_rows + grp * RH) * g.tile_row + q * g.I;
+    // bounds check.  The tile index of each (row, channel) accumulator is one add away from
+    // the previous one; the running index is opaque to the compiler, which would otherwise
+    // keep all RH*8 indices (times every lane-count case) live across the main loop and
+    // cut the waves a SIMD can hold.
+    const int tidx0 = ((mw * RM) * g.tile_rows + grp * RH) * g.tile_row + q * g.I;
     const int mstride = g.tile_rows * g.tile_row;
     auto decode = [&]() {
         if (lane_ok) {
             const uint64_t msb = g.msb_mask;
             const int L = g.L;
+            int ti = tidx0;
+#define SAMD_DECODE_LOOP(CALL)                                                                        \
+    _Pragma("unroll") for (int m = 0; m < RM; ++m) {                                                 \
+        asm volatile("" : "+v"(ti));                                                                  \
+        int tr = ti;                                                                                  \
+        _Pragma("unroll") for (int r = 0; r < RH; ++r) {                                             \
+            CALL;                                                                                     \
+            tr += g.tile_row;                                                                         \
+        }                                                                                             \
+        ti += mstride;                                                                                \
+    }
 #define SAMD_DECODE_NL(NL_)                                                                           \
     case NL_:                                                                                         \
-        _Pragma("unroll") for (int r = 0; r < RH; ++r)                                               \
-            _Pragma("unroll") for (int m = 0; m < RM; ++m)                                           \
-                decode_word<SG, NL_>((uint64_t)acc[r][m], msb, L, tbase + r * g.tile_row + m * mstride); \
+        SAMD_DECODE_LOOP((decode_word<SG, NL_>((uint64_t)acc[r][m], msb, L, tile + tr)))              \
         break;
             switch (g.nl) {
                 SAMD_DECODE_NL(2) SAMD_DECODE_NL(3) SAMD_DECODE_NL(4) SAMD_DECODE_NL(5)
                 SAMD_DECODE_NL(6) SAMD_DECODE_NL(7) SAMD_DECODE_NL(8)
             default:
-#pragma unroll
-                for (int r = 0; r < RH; ++r)
-#pragma unroll
-                    for (int m = 0; m < RM; ++m)
-                        decode_word_n<SG>((uint64_t)acc[r][m], msb, L, g.nl, tbase + r * g.tile_row + m * mstride);
+                SAMD_DECODE_LOOP((decode_word_n<SG>((uint64_t)acc[r][m], msb, L, g.nl, tile + tr)))
             }
 #undef SAMD_DECODE_NL
+#undef SAMD_DECODE_LOOP
         }
 #pragma unroll
         for (int r = 0; r < RH; ++r)
@@ -281,157 +297,267 @@ __global__ __launch_bounds__(1024) void conv2d_samd_kernel(const int32_t *__rest
             for (int m = 0; m < RM; ++m) acc[r][m] = 0;
     };
 
-    // This wave's channel slice: channels cbeg .. cend-1, decoded after every G channels.
-    const int cbeg = min(kq * g.cpw, g.C), cend = min(cbeg + g.cpw, g.C);
-    const int32_t *ks_slice = kstream + (int64_t)cbeg * g.nrt * RM;
-    int32_t kA[kStepBatch * RM], aA[kStepBatch][RH], kB[kStepBatch * RM], aB[kStepBatch][RH];
-    auto mac_batch = [&](const int32_t (&kb)[kStepBatch * RM], const int32_t (&ab)[kStepBatch][RH]) {
+    // orders the tile's zeroing before the first item's decodes
+    __syncthreads();
+    for (int item = blockIdx.x / kNumXcd; item < nitems;) {
+        unsigned long long ticket = 0;
+        if (nextra > 0 && tid == 0) ticket = atomicAdd(counter, 1ull);
+        const int mb = item % g.nmb;
+        const int tile_id = (item / g.nmb) * kNumXcd + xcd;
+        const int n = tile_id / g.row_tiles;
+        const int ho0 = (tile_id % g.row_tiles) * g.rows_blk;
+        const int wb = mb * g.wm + mw;
+
+        // Operand word of step s (s = ky*ntw + t) of channel c for this lane's row r:
+        // xs[n][c][hp][t][q] with hp = (ho0 + row)*sh + ky, i.e. word
+        // (c*Hp*ntw + (ho0 + row)*sh*ntw + s)*nq + q of image n.  Rows past the image (the last
+        // row tile, idle lanes) read the last output row's inputs; their sums are not stored.
+        const int ch_stride = g.Hp * g.ntw * g.nq;
+        int lb[RH];   // byte offset of the lane's word in channel 0, step 0
 #pragma unroll
-        for (int j = 0; j < kStepBatch; ++j) {
-#pragma unroll
-            for (int r = 0; r < RH; ++r)
-#pragma unroll
-                for (int m = 0; m < RM; ++m) acc[r][m] += (int64_t)ab[j][r] * (int64_t)kb[j * RM + m];
-#pragma unroll
-            for (int r = 0; r < RH; ++r)
-#pragma unroll
-                for (int m = 0; m < RM; ++m) keep(acc[r][m]);
+        for (int r = 0; r < RH; ++r) {
+            const int row = min(ho0 + min(grp * RH + r, g.rows_blk - 1), g.Ho - 1);
+            lb[r] = (row * g.sh * g.ntw * g.nq + q) * 4;
         }
-    };
-    // Batches of kStepBatch steps: kernel words in SGPRs (scalar loads), the lane's operand
-    // words from global memory.  Ping-pong over two register sets.  Before a batch's kernel
-    // words are used, all outstanding scalar loads are waited for, and only then is the
-    // next batch requested: scalar loads return out of order, so a wait placed after
-    // requesting the next batch would wait for it too.  Operand loads are vector loads,
-    // which complete in order, so the compiler waits for exactly the batch in use.  The
-    // batch after the last one is fetched as well (its results are never used): it reads
-    // the next channel, which exists (the spread buffer has one spare channel after the
-    // last image), and the kStreamPad padding steps of the kernel-word stream.
-    if constexpr (NRT != 0) {
-        // 3 or 6 steps per channel: batch b is steps (b % BPC)*3 .. +2 of channel
-        // cbeg + b / BPC, and the slice is one pipeline; the decode after every G channels
-        // runs while the next batch's loads are in flight.
-        constexpr int BPC = NRT / kStepBatch;
-        const int nbat = (cend - cbeg) * BPC;
-        const int seg = g.G * BPC;   // batches between decodes
-        auto load_batch = [&](int b, int32_t (&kb)[kStepBatch * RM], int32_t (&ab)[kStepBatch][RH]) {
+        // the image's channels and one spare channel after them
+        const __amdgpu_buffer_rsrc_t xrs = __builtin_amdgcn_make_buffer_rsrc(
+            (void *)(xs + (int64_t)n * g.C * ch_stride), (short)0, (g.C + 1) * ch_stride * 4, kBufferWord3);
+
+        const int64_t stream_len = ((int64_t)g.C * g.nrt + kStreamPad) * RM;
+        const int32_t *kstream = kw + wb * stream_len;
+
+        // This wave's channel slice: channels cbeg .. cend-1, decoded after every G channels.
+        const int cbeg = min(kq * g.cpw, g.C), cend = min(cbeg + g.cpw, g.C);
+        const int32_t *ks_slice = kstream + (int64_t)cbeg * g.nrt * RM;
+        int32_t kA[kStepBatch * RM], aA[kStepBatch][RH], kB[kStepBatch * RM], aB[kStepBatch][RH];
+        auto mac_batch = [&](const int32_t (&kb)[kStepBatch * RM], const int32_t (&ab)[kStepBatch][RH]) {
 #pragma unroll
-            for (int j = 0; j < kStepBatch * RM; ++j) kb[j] = ks_slice[b * kStepBatch * RM + j];
-            const int sb = ((cbeg + b / BPC) * ch_stride + (b % BPC) * kStepBatch * g.nq) * 4;
+            for (int j = 0; j < kStepBatch; ++j) {
 #pragma unroll
-            for (int j = 0; j < kStepBatch; ++j)
+                for (int r = 0; r < RH; ++r)
 #pragma unroll
-                for (int r = 0; r < RH; ++r) ab[j][r] = buffer_word(xrs, lb[r], sb + j * g.nq * 4);
+                    for (int m = 0; m < RM; ++m) acc[r][m] += (int64_t)ab[j][r] * (int64_t)kb[j * RM + m];
+#pragma unroll
+                for (int r = 0; r < RH; ++r)
+#pragma unroll
+                    for (int m = 0; m < RM; ++m) keep(acc[r][m]);
+            }
         };
-        if (nbat > 0) {
-            int left = seg;   // batches until the next decode
-            load_batch(0, kA, aA);
-            int b = 0;
-            for (; b + 1 < nbat; b += 2) {
-                __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0)
-                load_batch(b + 1, kB, aB);
-                __builtin_amdgcn_sched_barrier(0);
-                mac_batch(kA, aA);
-                __builtin_amdgcn_sched_barrier(0);
-                if (--left == 0) {
-                    decode();
-                    left = seg;
-                }
-                __builtin_amdgcn_s_waitcnt(0xc07f);
-                load_batch(b + 2, kA, aA);
-                __builtin_amdgcn_sched_barrier(0);
-                mac_batch(kB, aB);
-                __builtin_amdgcn_sched_barrier(0);
-                if (--left == 0) {
-                    decode();
-                    left = seg;
-                }
-            }
-            if (b < nbat) {   // odd batch count: the last batch
-                __builtin_amdgcn_s_waitcnt(0xc07f);
-                mac_batch(kA, aA);
-                --left;
-            }
-            if (left != seg) decode();
-        }
-    } else {
-        // any other step count: segments of at most G channels, each its own pipeline;
-        // batches straddle channels, and steps past a segment multiply by a zero operand
-        for (int c0 = cbeg; c0 < cend; c0 += g.G) {
-            const int nsteps = min(g.G, cend - c0) * g.nrt;
-            const int nbat = (nsteps + kStepBatch - 1) / kStepBatch;
-            const int32_t *ks = ks_slice + (int64_t)(c0 - cbeg) * g.nrt * RM;
-            auto load_batch = [&](int b, int32_t (&kb)[kStepBatch * RM], int32_t (&ab)[kStepBatch][RH]) {
+        // Batches of kStepBatch steps: kernel words in SGPRs (scalar loads), the lane's operand
+        // words from global memory.  Ping-pong over two register sets.  Before a batch's kernel
+        // words are used, all outstanding scalar loads are waited for, and only then is the
+        // next batch requested: scalar loads return out of order, so a wait placed after
+        // requesting the next batch would wait for it too.  Operand loads are vector loads,
+        // which complete in order, so the compiler waits for exactly the batch in use.  The
+        // batch after the last one is fetched as well (its results are never used): it reads
+        // the next channel, which exists (the spread buffer has one spare channel after the
+        // last image), and the kStreamPad padding steps of the kernel-word stream.
+        if constexpr (RNTW != 0) {
+            // batch b: kernel word t = b % RNTW of channel cbeg + b / RNTW, its three kernel
+            // rows (the stream is kernel-word-major within a channel, so they are steps
+            // 3b .. 3b+2 of the slice); operand words of input rows hp0 + i, i < RH + 2
+            // (rows past the padded image are clamped to its last row: they only reach
+            // output rows that are never stored)
+            constexpr int NA = RH + 2;
+            int lbi[NA];
 #pragma unroll
-                for (int j = 0; j < kStepBatch * RM; ++j) kb[j] = ks[b * kStepBatch * RM + j];
+            for (int i = 0; i < NA; ++i)
+                lbi[i] = (min(ho0 + grp * RH + i, g.Hp - 1) * RNTW * g.nq + q) * 4;
+            const int nbat = (cend - cbeg) * RNTW;
+            const int seg = g.G * RNTW;
+            int32_t kRA[kStepBatch * RM], aRA[NA], kRB[kStepBatch * RM], aRB[NA];
+            auto load_rows = [&](int b, int32_t (&kb)[kStepBatch * RM], int32_t (&ab)[NA]) {
 #pragma unroll
-                for (int j = 0; j < kStepBatch; ++j) {
-                    const int st0 = b * kStepBatch + j;
-                    const bool live = st0 < nsteps;
-                    const int st = min(st0, nsteps - 1);
-                    const int cc = st / g.nrt, rt = st - cc * g.nrt;
-                    const int sb = ((c0 + cc) * ch_stride + rt * g.nq) * 4;
+                for (int j = 0; j < kStepBatch * RM; ++j) kb[j] = ks_slice[b * kStepBatch * RM + j];
+                const int sb = ((cbeg + b / RNTW) * ch_stride + (b % RNTW) * g.nq) * 4;
 #pragma unroll
-                    for (int r = 0; r < RH; ++r) {
-                        const int32_t v = buffer_word(xrs, lb[r], sb);
-                        ab[j][r] = live ? v : 0;
-                    }
+                for (int i = 0; i < NA; ++i) ab[i] = buffer_word(xrs, lbi[i], sb);
+            };
+            auto mac_rows = [&](const int32_t (&kb)[kStepBatch * RM], const int32_t (&ab)[NA]) {
+#pragma unroll
+                for (int ky = 0; ky < kStepBatch; ++ky) {
+#pragma unroll
+                    for (int r = 0; r < RH; ++r)
+#pragma unroll
+                        for (int m = 0; m < RM; ++m)
+                            acc[r][m] += (int64_t)ab[r + ky] * (int64_t)kb[ky * RM + m];
+#pragma unroll
+                    for (int r = 0; r < RH; ++r)
+#pragma unroll
+                        for (int m = 0; m < RM; ++m) keep(acc[r][m]);
                 }
             };
-            load_batch(0, kA, aA);
-            int b = 0;
-            for (; b + 1 < nbat; b += 2) {
-                __builtin_amdgcn_s_waitcnt(0xc07f);
-                load_batch(b + 1, kB, aB);
-                __builtin_amdgcn_sched_barrier(0);
-                mac_batch(kA, aA);
-                __builtin_amdgcn_sched_barrier(0);
-                __builtin_amdgcn_s_waitcnt(0xc07f);
-                load_batch(b + 2, kA, aA);
-                __builtin_amdgcn_sched_barrier(0);
-                mac_batch(kB, aB);
-                __builtin_amdgcn_sched_barrier(0);
-            }
-            if (b < nbat) {
-                __builtin_amdgcn_s_waitcnt(0xc07f);
-                mac_batch(kA, aA);
-            }
-            decode();
-        }
-    }
-    __syncthreads();
-
-    // output tile -> y: wave w copies rows rr = w, w + nwaves, ... (rr = mm * rows_blk + r)
-    // of the tile, lanes along the row
-    const int nwaves = g.wm * g.ks;
-    const int dmm = nwaves / g.rows_blk, dr = nwaves - dmm * g.rows_blk;
-    int mm = wave / g.rows_blk, r = wave - mm * g.rows_blk;
-    while (mm < g.mblk) {
-        const int m = mb * g.mblk + mm, ho = ho0 + r;
-        if (m < g.M && ho < g.Ho) {
-            const int32_t *src = tile + (mm * g.tile_rows + r) * g.tile_row + (g.Kmax - 1);
-            int32_t *dst = y + (((int64_t)n * g.M + m) * g.Ho + ho) * g.Wo;
-            if (g.xoff == 0) {
-                for (int o = lane; o < g.Wo; o += 64) dst[o] = src[o];
-            } else {
-                // recentred activations: + xoff * (weights over the output's in-image taps)
-                const int hb = ho * g.sh - g.ph, kwid = g.KW + 1;
-                const int ky0 = max(0, -hb) * kwid, ky1 = min(g.KH, g.H - hb) * kwid;
-                const int32_t *pm = pre + m * (g.KH + 1) * kwid;
-                for (int o = lane; o < g.Wo; o += 64) {
-                    const int wb = o * g.sw - g.pw;
-                    const int kx0 = max(0, -wb), kx1 = min(g.KW, g.W - wb);
-                    const int32_t rect = pm[ky1 + kx1] - pm[ky0 + kx1] - pm[ky1 + kx0] + pm[ky0 + kx0];
-                    dst[o] = src[o] + g.xoff * rect;
+            if (nbat > 0) {
+                int left = seg;   // batches until the next decode
+                load_rows(0, kRA, aRA);
+                int b = 0;
+                for (; b + 1 < nbat; b += 2) {
+                    __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0)
+                    load_rows(b + 1, kRB, aRB);
+                    __builtin_amdgcn_sched_barrier(0);
+                    mac_rows(kRA, aRA);
+                    __builtin_amdgcn_sched_barrier(0);
+                    if (--left == 0) {
+                        decode();
+                        left = seg;
+                    }
+                    __builtin_amdgcn_s_waitcnt(0xc07f);
+                    load_rows(b + 2, kRA, aRA);
+                    __builtin_amdgcn_sched_barrier(0);
+                    mac_rows(kRB, aRB);
+                    __builtin_amdgcn_sched_barrier(0);
+                    if (--left == 0) {
+                        decode();
+                        left = seg;
+                    }
                 }
+                if (b < nbat) {   // odd batch count: the last batch
+                    __builtin_amdgcn_s_waitcnt(0xc07f);
+                    mac_rows(kRA, aRA);
+                    --left;
+                }
+                if (left != seg) decode();
+            }
+        } else if constexpr (NRT != 0) {
+            // 3 or 6 steps per channel: batch b is steps (b % BPC)*3 .. +2 of channel
+            // cbeg + b / BPC, and the slice is one pipeline; the decode after every G channels
+            // runs while the next batch's loads are in flight.
+            constexpr int BPC = NRT / kStepBatch;
+            const int nbat = (cend - cbeg) * BPC;
+            const int seg = g.G * BPC;   // batches between decodes
+            auto load_batch = [&](int b, int32_t (&kb)[kStepBatch * RM], int32_t (&ab)[kStepBatch][RH]) {
+#pragma unroll
+                for (int j = 0; j < kStepBatch * RM; ++j) kb[j] = ks_slice[b * kStepBatch * RM + j];
+                const int sb = ((cbeg + b / BPC) * ch_stride + (b % BPC) * kStepBatch * g.nq) * 4;
+#pragma unroll
+                for (int j = 0; j < kStepBatch; ++j)
+#pragma unroll
+                    for (int r = 0; r < RH; ++r) ab[j][r] = buffer_word(xrs, lb[r], sb + j * g.nq * 4);
+            };
+            if (nbat > 0) {
+                int left = seg;   // batches until the next decode
+                load_batch(0, kA, aA);
+                int b = 0;
+                for (; b + 1 < nbat; b += 2) {
+                    __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0)
+                    load_batch(b + 1, kB, aB);
+                    __builtin_amdgcn_sched_barrier(0);
+                    mac_batch(kA, aA);
+                    __builtin_amdgcn_sched_barrier(0);
+                    if (--left == 0) {
+                        decode();
+                        left = seg;
+                    }
+                    __builtin_amdgcn_s_waitcnt(0xc07f);
+                    load_batch(b + 2, kA, aA);
+                    __builtin_amdgcn_sched_barrier(0);
+                    mac_batch(kB, aB);
+                    __builtin_amdgcn_sched_barrier(0);
+                    if (--left == 0) {
+                        decode();
+                        left = seg;
+                    }
+                }
+                if (b < nbat) {   // odd batch count: the last batch
+                    __builtin_amdgcn_s_waitcnt(0xc07f);
+                    mac_batch(kA, aA);
+                    --left;
+                }
+                if (left != seg) decode();
+            }
+        } else {
+            // any other step count: segments of at most G channels, each its own pipeline;
+            // batches straddle channels, and steps past a segment multiply by a zero operand
+            for (int c0 = cbeg; c0 < cend; c0 += g.G) {
+                const int nsteps = min(g.G, cend - c0) * g.nrt;
+                const int nbat = (nsteps + kStepBatch - 1) / kStepBatch;
+                const int32_t *ks = ks_slice + (int64_t)(c0 - cbeg) * g.nrt * RM;
+                auto load_batch = [&](int b, int32_t (&kb)[kStepBatch * RM], int32_t (&ab)[kStepBatch][RH]) {
+#pragma unroll
+                    for (int j = 0; j < kStepBatch * RM; ++j) kb[j] = ks[b * kStepBatch * RM + j];
+#pragma unroll
+                    for (int j = 0; j < kStepBatch; ++j) {
+                        const int st0 = b * kStepBatch + j;
+                        const bool live = st0 < nsteps;
+                        const int st = min(st0, nsteps - 1);
+                        const int cc = st / g.nrt, rt = st - cc * g.nrt;
+                        const int sb = ((c0 + cc) * ch_stride + rt * g.nq) * 4;
+#pragma unroll
+                        for (int r = 0; r < RH; ++r) {
+                            const int32_t v = buffer_word(xrs, lb[r], sb);
+                            ab[j][r] = live ? v : 0;
+                        }
+                    }
+                };
+                load_batch(0, kA, aA);
+                int b = 0;
+                for (; b + 1 < nbat; b += 2) {
+                    __builtin_amdgcn_s_waitcnt(0xc07f);
+                    load_batch(b + 1, kB, aB);
+                    __builtin_amdgcn_sched_barrier(0);
+                    mac_batch(kA, aA);
+                    __builtin_amdgcn_sched_barrier(0);
+                    __builtin_amdgcn_s_waitcnt(0xc07f);
+                    load_batch(b + 2, kA, aA);
+                    __builtin_amdgcn_sched_barrier(0);
+                    mac_batch(kB, aB);
+                    __builtin_amdgcn_sched_barrier(0);
+                }
+                if (b < nbat) {
+                    __builtin_amdgcn_s_waitcnt(0xc07f);
+                    mac_batch(kA, aA);
+                }
+                decode();
             }
         }
-        mm += dmm;
-        r += dr;
-        if (r >= g.rows_blk) {
-            r -= g.rows_blk;
-            ++mm;
+        if (tid == 0)
+            next_item = nextra > 0 ? nwg + (int)(ticket % (unsigned long long)(nextra + nwg)) : nitems;
+        __syncthreads();
+        const int following = __builtin_amdgcn_readfirstlane(next_item);
+
+        // output tile -> y: wave w copies rows rr = w, w + nwaves, ... (rr = mm * rows_blk + r)
+        // of the tile, lanes along the row
+        const int nwaves = g.wm * g.ks;
+        const int dmm = nwaves / g.rows_blk, dr = nwaves - dmm * g.rows_blk;
+        int mm = wave / g.rows_blk, r = wave - mm * g.rows_blk;
+        while (mm < g.mblk) {
+            const int m = mb * g.mblk + mm, ho = ho0 + r;
+            // each tile word of an output column is zeroed for the next item once read,
+            // also in rows past the image and channels past M, which another item stores
+            int32_t *src = tile + (mm * g.tile_rows + r) * g.tile_row + (g.Kmax - 1);
+            if (m < g.M && ho < g.Ho) {
+                int32_t *dst = y + (((int64_t)n * g.M + m) * g.Ho + ho) * g.Wo;
+                if (g.xoff == 0) {
+                    for (int o = lane; o < g.Wo; o += 64) {
+                        dst[o] = src[o];
+                        src[o] = 0;
+                    }
+                } else {
+                    // recentred activations: + xoff * (weights over the output's in-image taps)
+                    const int hb = ho * g.sh - g.ph, kwid = g.KW + 1;
+                    const int ky0 = max(0, -hb) * kwid, ky1 = min(g.KH, g.H - hb) * kwid;
+                    const int32_t *pm = pre + m * (g.KH + 1) * kwid;
+                    for (int o = lane; o < g.Wo; o += 64) {
+                        const int wbeg = o * g.sw - g.pw;
+                        const int kx0 = max(0, -wbeg), kx1 = min(g.KW, g.W - wbeg);
+                        const int32_t rect = pm[ky1 + kx1] - pm[ky0 + kx1] - pm[ky1 + kx0] + pm[ky0 + kx0];
+                        dst[o] = src[o] + g.xoff * rect;
+                        src[o] = 0;
+                    }
+                }
+            } else {
+                for (int o = lane; o < g.Wo; o += 64) src[o] = 0;
+            }
+            mm += dmm;
+            r += dr;
+            if (r >= g.rows_blk) {
+                r -= g.rows_blk;
+                ++mm;
+            }
         }
+        item = following;
+        // the write-out (and the tile's re-zeroing) ends before the next item's decodes
+        if (item < nitems) __syncthreads();
     }
 }
 
@@ -439,11 +565,12 @@ __global__ __launch_bounds__(1024) void conv2d_samd_kernel(const int32_t *__rest
 
 int launch_conv2d_prepare(const uint32_t *w, const Conv2dGeom &g, void *ws, hipStream_t s) {
     int32_t *kw = (int32_t *)ws;
+    int32_t *queue = (int32_t *)((char *)ws + conv2d_queue_offset(g));
     const int pgrid = grid_for(g.kw_words, 256);
     bool launched = false;
 #define SAMD_PREP_CASE(B, SG)                                                                            \
     if (!launched && g.wbits == B && (bool)g.wsigned == SG) {                                            \
-        hipLaunchKernelGGL((prep_weights_kernel<B, SG>), dim3(pgrid), dim3(256), 0, s, w, g, kw);        \
+        hipLaunchKernelGGL((prep_weights_kernel<B, SG>), dim3(pgrid), dim3(256), 0, s, w, g, kw, queue);        \
         launched = true;                                                                                 \
     }
     SAMD_FOR_EACH_FMT(SAMD_PREP_CASE)
@@ -464,7 +591,7 @@ int launch_conv2d_prepare(const uint32_t *w, const Conv2dGeom &g, void *ws, hipS
 }
 
 int launch_conv2d_spread(const uint32_t *x, const Conv2dGeom &g, void *ws, hipStream_t s) {
-    int32_t *xs = (int32_t *)((char *)ws + conv2d_kw_bytes(g) + conv2d_pre_bytes(g));
+    int32_t *xs = (int32_t *)((char *)ws + conv2d_xs_offset(g));
     int qshift = 0;
     while ((1 << qshift) < g.nq) ++qshift;   // nq <= 64
     const int64_t nrows = (int64_t)g.N * g.C * g.Hp;
@@ -481,23 +608,84 @@ int launch_conv2d_spread(const uint32_t *x, const Conv2dGeom &g, void *ws, hipSt
     return check_launch("conv2d operand spread");
 }
 
-int launch_conv2d_multiply(const Conv2dGeom &g, int32_t *y, const void *ws, hipStream_t s) {
+namespace {
+
+// Workgroups of `kernel` the current device keeps resident at once (all compute units),
+// looked up once per (device, kernel, block, LDS bytes).
+int resident_workgroups(const void *kernel, int block, size_t shm, int &out) {
+    static std::mutex mu;
+    static std::map<std::tuple<int, const void *, int, size_t>, int> cache;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) {
+        set_error("conv2d: hipGetDevice failed");
+        return SAMD_EHIP;
+    }
+    const auto key = std::make_tuple(dev, kernel, block, shm);
+    {
+        std::lock_guard<std::mutex> lock(mu);
+        auto it = cache.find(key);
+        if (it != cache.end()) {
+            out = it->second;
+            return SAMD_OK;
+        }
+    }
+    int per_cu = 0, cus = 0;
+    hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, block, shm);
+    if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) {
+        set_error(std::string("conv2d: occupancy query: ") + hipGetErrorString(e));
+        return SAMD_EHIP;
+    }
+    out = std::max(1, per_cu) * std::max(1, cus);
+    std::lock_guard<std::mutex> lock(mu);
+    cache[key] = out;
+    return SAMD_OK;
+}
+
+template <int RH, int NRT, bool SG, int RNTW>
+int launch_multiply(const Conv2dGeom &g, int32_t *y, const void *ws, hipStream_t s) {
     const int32_t *kw = (const int32_t *)ws;
     const int32_t *pre = (const int32_t *)((const char *)ws + conv2d_kw_bytes(g));
-    const int32_t *xs = (const int32_t *)((const char *)ws + conv2d_kw_bytes(g) + conv2d_pre_bytes(g));
-    const dim3 grid((unsigned)g.tiles * g.nmb), block(g.wm * g.ks * 64);
+    unsigned long long *tickets =
+        (unsigned long long *)((char *)const_cast<void *>(ws) + conv2d_queue_offset(g));
+    const int32_t *xs = (const int32_t *)((const char *)ws + conv2d_xs_offset(g));
+    const int block = g.wm * g.ks * 64;
     const size_t shm = (size_t)g.lds_words * 4;
+    const void *fn = (const void *)conv2d_samd_kernel<RH, NRT, SG, RNTW>;
+    int resident = 0;
+    const int st = resident_workgroups(fn, block, shm, resident);
+    if (st) return st;
+    // every XCD gets the same number of workgroups; none gets more than its items
+    const int64_t xitems = (int64_t)(g.N * g.row_tiles + kNumXcd - 1) / kNumXcd * g.nmb;
+    const int64_t per_xcd = std::max<int64_t>(1, std::min<int64_t>(xitems, resident / kNumXcd));
+    hipLaunchKernelGGL((conv2d_samd_kernel<RH, NRT, SG, RNTW>), dim3((unsigned)(per_xcd * kNumXcd)), dim3(block), shm, s,
+                       xs, kw, pre, y, tickets, g);
+    return check_launch("conv2d");
+}
+
+}  // namespace
+
+int launch_conv2d_multiply(const Conv2dGeom &g, int32_t *y, const void *ws, hipStream_t s) {
+    if (g.rows_path) {
+#define SAMD_ROWS_CASE(RH_, NTW_, SG_)                                                                \
+    if (g.rh == RH_ && g.ntw == NTW_ && (bool)g.result_signed == SG_)                                 \
+        return launch_multiply<RH_, 0, SG_, NTW_>(g, y, ws, s);
+        SAMD_ROWS_CASE(1, 1, false) SAMD_ROWS_CASE(2, 1, false) SAMD_ROWS_CASE(3, 1, false) SAMD_ROWS_CASE(4, 1, false)
+        SAMD_ROWS_CASE(1, 2, false) SAMD_ROWS_CASE(2, 2, false) SAMD_ROWS_CASE(3, 2, false) SAMD_ROWS_CASE(4, 2, false)
+        SAMD_ROWS_CASE(1, 1, true) SAMD_ROWS_CASE(2, 1, true) SAMD_ROWS_CASE(3, 1, true) SAMD_ROWS_CASE(4, 1, true)
+        SAMD_ROWS_CASE(1, 2, true) SAMD_ROWS_CASE(2, 2, true) SAMD_ROWS_CASE(3, 2, true) SAMD_ROWS_CASE(4, 2, true)
+#undef SAMD_ROWS_CASE
+    } else {
 #define SAMD_CONV_CASE(RH_, NRT_, SG_)                                                                \
     if (g.rh == RH_ && (NRT_ == 0 ? (g.nrt != 3 && g.nrt != 6) : g.nrt == NRT_) &&                     \
-        (bool)g.result_signed == SG_) {                                                               \
-        hipLaunchKernelGGL((conv2d_samd_kernel<RH_, NRT_, SG_>), grid, block, shm, s, xs, kw, pre, y, g);   \
-        return check_launch("conv2d");                                                                \
-    }
-    SAMD_CONV_CASE(1, 3, false) SAMD_CONV_CASE(1, 6, false) SAMD_CONV_CASE(1, 0, false)
-    SAMD_CONV_CASE(2, 3, false) SAMD_CONV_CASE(2, 6, false) SAMD_CONV_CASE(2, 0, false)
-    SAMD_CONV_CASE(1, 3, true) SAMD_CONV_CASE(1, 6, true) SAMD_CONV_CASE(1, 0, true)
-    SAMD_CONV_CASE(2, 3, true) SAMD_CONV_CASE(2, 6, true) SAMD_CONV_CASE(2, 0, true)
+        (bool)g.result_signed == SG_)                                                                 \
+        return launch_multiply<RH_, NRT_, SG_, 0>(g, y, ws, s);
+        SAMD_CONV_CASE(1, 3, false) SAMD_CONV_CASE(1, 6, false) SAMD_CONV_CASE(1, 0, false)
+        SAMD_CONV_CASE(2, 3, false) SAMD_CONV_CASE(2, 6, false) SAMD_CONV_CASE(2, 0, false)
+        SAMD_CONV_CASE(1, 3, true) SAMD_CONV_CASE(1, 6, true) SAMD_CONV_CASE(1, 0, true)
+        SAMD_CONV_CASE(2, 3, true) SAMD_CONV_CASE(2, 6, true) SAMD_CONV_CASE(2, 0, true)
 #undef SAMD_CONV_CASE
+    }
     set_error("conv2d: no kernel for this geometry");
     return SAMD_EUNSUPPORTED;
 }

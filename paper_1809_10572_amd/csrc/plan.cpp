@@ -66,24 +66,32 @@ bool split_taps(int count, int kmax, int *t0, int *nt, int &ngroups) {
 }
 
 // Launch shape of one lane geometry: output rows per thread (rh), row groups per wave,
-// output-channel waves (wm) and channel-slice waves (ks) per workgroup.  Every candidate
-// is priced in VALU issue cycles of the busiest SIMD: the multiply-adds and decodes of
-// the workgroups one compute unit runs, divided by an issue efficiency that grows with
-// the waves resident per SIMD (latency hiding), plus the operand-spread pass.  Returns
-// false when no tile fits the LDS.
+// output-channel waves (wm) and channel-slice waves (ks) per workgroup, and whether the
+// lane's rows share operand loads (3-row, stride-1 kernels).  Every candidate is priced
+// in issue cycles of one compute unit (units of 4 clocks): its SIMDs' multiply-adds and
+// decodes, and its texture path's operand loads (about 12 clocks per wave-wide load on
+// MI355X, shared by the 4 SIMDs), whichever binds, divided by an issue efficiency that
+// grows with the waves resident per SIMD (latency hiding), plus the last item's drain and
+// the operand-spread pass.  Returns false when no tile fits the LDS.
 bool place_launch(const samd_conv2d_desc &d, Conv2dGeom &c) {
     const int grp_max = 64 / c.nq;
+    const bool rows_ok = d.KH == 3 && d.stride_h == 1 && (c.ntw == 1 || c.ntw == 2);
     bool found = false;
     Conv2dGeom best = c;
     best.cost = 1e300;
-    for (int rh = 1; rh <= 2; ++rh) {
-        if (rh == 2 && c.Ho < 2) continue;
+    for (int rows = 0; rows <= (rows_ok ? 1 : 0); ++rows) {
+    for (int rh = 1; rh <= (rows ? 4 : 2); ++rh) {
+        if (rh > 1 && c.Ho < rh) continue;
+        // waves per SIMD the kernel's registers allow (as compiled for gfx950), and at
+        // most kResidentWavesPerSimd
+        const int reg_waves = std::min(kResidentWavesPerSimd, rh <= 2 ? 7 : (rh == 3 ? 5 : 4));
         for (int gr = grp_max; gr >= 1; --gr) {
             for (int wm : {1, 2, 4}) {
                 for (int ks : {1, 2, 4, 8, 16}) {
                     if (wm * ks > kMaxBlockWaves) continue;
                     if (ks > 1 && (d.C + ks - 1) / ks < 1) continue;
                     Conv2dGeom t = c;
+                    t.rows_path = rows;
                     t.rh = rh;
                     t.groups = gr;
                     t.rows_blk = std::min(rh * gr, c.Ho);
@@ -110,29 +118,35 @@ bool place_launch(const samd_conv2d_desc &d, Conv2dGeom &c) {
                     if (ks > 1 && (long)(ks - 1) * t.cpw >= d.C) continue;   // an empty slice
                     t.chk = t.cpw * ks;
                     t.row_tiles = (c.Ho + t.rows_blk - 1) / t.rows_blk;
-                    t.tiles = (d.N * t.row_tiles + 7) / 8 * 8;
+                    t.tiles = d.N * t.row_tiles;
                     t.kw_words = (int64_t)t.nmb * wm * ((int64_t)d.C * c.nrt + kStreamPad) * kWaveM;
                     t.spread_words = (int64_t)d.N * d.C * c.Hp * c.ntw * c.nq;
 
-                    // wave-instructions of one workgroup
+                    // wave-instructions and operand loads of one workgroup's item
+                    const double waves = (double)wm * ks;
                     const double nflush = std::ceil((double)t.cpw / c.G);
-                    const double mads = (double)wm * ks * kWaveM * rh * t.cpw * c.nrt * 1.08;
-                    const double decode = (double)wm * ks * nflush * kWaveM * rh *
+                    const double mads = waves * kWaveM * rh * t.cpw * c.nrt * 1.08;
+                    const double decode = waves * nflush * kWaveM * rh *
                                           ((c.result_signed ? 5.0 : 0.0) + 1.0 + 2.0 * c.nl);
-                    const double fixed = (double)wm * ks * 150.0 + (double)t.lds_tile / 64.0 * 3.0;
+                    const double fixed = waves * 150.0 + (double)t.lds_tile / 64.0 * 3.0;
                     const double wg = mads + decode + fixed;
-                    // residency: LDS, and at most 8 waves per SIMD
-                    const double wgs = (double)t.tiles * t.nmb;
-                    const double per_cu = std::ceil(wgs / 256.0);
+                    const double loads = waves * t.cpw * (rows ? c.ntw * (rh + 2.0) : (double)c.nrt * rh);
+                    // one compute unit's share of the items (taken as workgroups free up)
+                    const double items = std::max(1.0, (double)t.tiles * t.nmb / 256.0);
+                    const double valu = items * wg / 4.0;
+                    const double tex = items * loads * 3.0;
+                    const double busy = std::max(valu, tex) + 0.25 * std::min(valu, tex);
+                    // residency: LDS and registers
                     const double res = std::max(1.0, std::min(std::floor(163840.0 / (t.lds_words * 4.0)),
-                                                              std::floor(32.0 / (wm * ks))));
-                    const double occ = std::min(per_cu, res) * wm * ks / 4.0;
+                                                              std::floor(4.0 * reg_waves / waves)));
+                    const double occ = std::min(items, res) * waves / 4.0;
                     const double eff = occ / (occ + 0.7);
+                    const double drain = 0.5 * wg / waves;
                     const double spread = (double)t.spread_words * (6.0 * c.I + 4.0) / 64.0 / 1024.0;
                     // measured on MI355X: slices of about 32 channels balance the per-wave
                     // fixed costs against scalar-load latency hiding
                     const double slice = 1.0 + 0.15 * std::fabs(std::log2(t.cpw / 32.0));
-                    t.cost = per_cu * wg / 4.0 / eff * slice + spread;
+                    t.cost = (busy / eff + drain) * slice + spread;
                     if (t.cost < best.cost) {
                         best = t;
                         found = true;
@@ -140,6 +154,7 @@ bool place_launch(const samd_conv2d_desc &d, Conv2dGeom &c) {
                 }
             }
         }
+    }
     }
     if (found) {
         const double keep = c.macs_per_mad;
@@ -312,18 +327,23 @@ int plan_conv2d(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, Conv2dGeom 
     return st;
 }
 
-// Workspace: kernel-word streams, then the operand words of one call (256-byte aligned).
+// Workspace: kernel-word streams, the recentring correction table, the work queues of
+// the multiply kernel, then the operand words of one call (each 256-byte aligned).
 size_t conv2d_kw_bytes(const Conv2dGeom &g) { return ((size_t)g.kw_words * 4 + 255) / 256 * 256; }
 
 size_t conv2d_pre_bytes(const Conv2dGeom &g) {
     return g.xoff ? ((size_t)g.M * (g.KH + 1) * (g.KW + 1) * 4 + 255) / 256 * 256 : 0;
 }
 
+size_t conv2d_queue_offset(const Conv2dGeom &g) { return conv2d_kw_bytes(g) + conv2d_pre_bytes(g); }
+
+size_t conv2d_xs_offset(const Conv2dGeom &g) { return conv2d_queue_offset(g) + kQueueBytes; }
+
 size_t conv2d_workspace_bytes(const Conv2dGeom &g) {
     // one spare channel after the last image: the batch fetched after a slice's last one
     // may read it (its products are never used)
     const size_t spare = (size_t)g.Hp * g.ntw * g.nq;
-    return conv2d_kw_bytes(g) + conv2d_pre_bytes(g) + ((size_t)(g.spread_words + spare) * 4 + 255) / 256 * 256;
+    return conv2d_xs_offset(g) + ((size_t)(g.spread_words + spare) * 4 + 255) / 256 * 256;
 }
 
 int plan_conv1d(int64_t n, samd_fmt xf, const int32_t *taps, int32_t K, samd_fmt kf, Conv1dGeom &best,

@@ -20,6 +20,10 @@ constexpr int kStepBatch = 3;      // kernel-word steps fetched per scalar-load 
 constexpr int kStreamPad = 2 * kStepBatch;  // zero steps after each kernel-word stream
 constexpr int kMaxBlockWaves = 16; // waves per conv2d workgroup
 constexpr int kMaxLdsBytes = 65536; // LDS per conv2d workgroup
+constexpr int kNumXcd = 8;          // accelerator complexes (each with its own L2); workgroup p runs on p % 8
+constexpr int kTicketStride = 256;  // bytes between the conv2d ticket counters (one per XCD)
+constexpr int kQueueBytes = kNumXcd * kTicketStride;
+constexpr int kResidentWavesPerSimd = 6;  // conv2d multiply kernel, as measured (register-limited)
 
 // Geometry of one SAMD 2-D convolution.  Every operand word is a signed 32-bit
 // integer A = sum_i v_i 2^(i L) holding I input values of one stride phase of one
@@ -44,6 +48,8 @@ struct Conv2dGeom {
     int32_t tw_phase[kMaxTapWords], tw_tap0[kMaxTapWords], tw_ntaps[kMaxTapWords];
     int32_t nrt;                    // steps per channel: KH * ntw
     // launch shape
+    int32_t rows_path;              // 1: 3-row stride-1 kernel whose output rows share operand loads
+                                    // (kernel-word streams kernel-word-major within a channel)
     int32_t rh;                     // output rows per thread
     int32_t groups;                 // row groups per wave: 64 / nq
     int32_t rows_blk;               // output rows per workgroup: rh * groups
@@ -52,7 +58,7 @@ struct Conv2dGeom {
     int32_t mblk;                   // output channels per workgroup, wm * kWaveM
     int32_t nmb;                    // output-channel blocks
     int32_t row_tiles;              // ceil(Ho / rows_blk)
-    int32_t tiles;                  // N * row_tiles, rounded up to a multiple of 8 (one per XCD)
+    int32_t tiles;                  // N * row_tiles
     int32_t chk;                    // ks * cpw (reported)
     int32_t cpw;                    // input channels of one wave's slice: ceil(C / ks)
     int32_t trows;                  // input rows a tile reads, (rows_blk-1)*sh + KH
@@ -86,6 +92,8 @@ int plan_conv1d(int64_t n, samd_fmt xf, const int32_t *taps, int32_t K, samd_fmt
 size_t conv2d_workspace_bytes(const Conv2dGeom &g);
 size_t conv2d_kw_bytes(const Conv2dGeom &g);
 size_t conv2d_pre_bytes(const Conv2dGeom &g);   // the recentring correction table
+size_t conv2d_queue_offset(const Conv2dGeom &g); // work queues of the multiply kernel
+size_t conv2d_xs_offset(const Conv2dGeom &g);    // operand words
 
 // Kernel launchers (enqueue only; report launch errors through the return value).
 int launch_pack(const void *src, int64_t rows, int64_t len, int bits, int is_signed, uint32_t *dst,

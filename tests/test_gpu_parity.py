@@ -290,6 +290,24 @@ def test_prepared_weights_are_reusable(bits):
         np.testing.assert_array_equal(y8.cpu().numpy(), want)
 
 
+@pytest.mark.parametrize("bx,sx,bw,sw", [(1, 0, 1, 1), (4, 0, 4, 1), (5, 1, 6, 1), (8, 0, 8, 1)])
+def test_conv2d_many_items_per_workgroup(bx, sx, bw, sw):
+    """More work items than resident workgroups, a partial last row tile and M not a
+    multiple of the channel block: workgroups take several items each, so every tile
+    word must be re-zeroed between items.  Three inputs in a row on one workspace also
+    check that the work queues are re-armed after every launch."""
+    shape = wl.Conv2dShape(32, 16, 61, 23, 44, 3, 3, 1, 1, 1, 1)
+    xf, wf = samd.Fmt(bx, sx), samd.Fmt(bw, sw)
+    rng = np.random.default_rng(7 * bx + bw)
+    w = wl.uniform(rng, (shape.M, shape.C, shape.KH, shape.KW), bw, bool(sw))
+    ws = samd.conv2d_prepare(samd.pack(gpu_vals(w, bool(sw)), bw, bool(sw)), wf, shape, xf)
+    for gen in (wl.uniform, wl.half_extremes, wl.uniform):
+        x = gen(rng, (shape.N, shape.C, shape.H, shape.W), bx, bool(sx))
+        y = samd.conv2d_prepared(samd.pack(gpu_vals(x, bool(sx)), bx, bool(sx)), xf, wf, shape, ws)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(y.cpu().numpy(), ref.conv2d(x, w, shape.as_tuple()))
+
+
 @pytest.mark.parametrize("bits", [2, 5])
 def test_staged_input_accumulates_against_several_weight_sets(bits):
     """stage once, then prepare + accumulate two weight sets on the same staged words."""
