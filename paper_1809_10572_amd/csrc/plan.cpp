@@ -318,7 +318,14 @@ int plan_conv2d(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, Conv2dGeom 
             return SAMD_OK;
         }
     }
-    const int st = search_conv2d(d, xf, wf, g, err);
+    int st = search_conv2d(d, xf, wf, g, err);
+    // the kernels address one image's operand words (and one spare channel) with 32-bit
+    // byte offsets, and padded rows with 32-bit indices
+    if (st == SAMD_OK && ((int64_t)(d.C + 1) * g.Hp * g.ntw * g.nq * 4 >= ((int64_t)1 << 31) ||
+                          (int64_t)d.N * d.C * g.Hp >= ((int64_t)1 << 31))) {
+        err = "operand words of one image exceed 2 GiB";
+        st = SAMD_EUNSUPPORTED;
+    }
     if (st == SAMD_OK) {
         std::lock_guard<std::mutex> lock(plan_mu);
         if (plan_cache.size() >= kPlanCacheMax) plan_cache.clear();
