@@ -45,6 +45,8 @@ def parse():
     p.add_argument("--counters", action="store_true",
                    help="launch each kernel once per bit width, eagerly, then a 1 GiB streaming copy, and exit "
                         "(the program rocprofv3 --pmc passes run)")
+    p.add_argument("--trace-summary", metavar="TRACE_DIR",
+                   help="print markdown tables of a rocprofv3 --kernel-trace --stats output folder (csv) and exit")
     p.add_argument("--traffic-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                    help="print the HBM-traffic summary of two rocprofv3 --pmc output folders of --counters runs "
                         "(FETCH_SIZE, then WRITE_SIZE) and exit")
@@ -110,6 +112,49 @@ def traffic_summary(fetch_dir, write_dir, bits_list):
     return res
 
 
+def trace_summary(folder):
+    """Markdown tables of a rocprofv3 --kernel-trace --stats csv folder: the stats of every
+    kernel called at least 5 times, then per kernel and launch shape the dispatch count,
+    resources and durations (End - Start), including the mean of its last 20 dispatches."""
+    import csv
+    import glob
+
+    def one(pattern):
+        files = glob.glob(os.path.join(folder, "**", pattern), recursive=True)
+        if len(files) != 1:
+            raise SystemExit(f"expected one {pattern} under {folder}, found {len(files)}")
+        return list(csv.DictReader(open(files[0])))
+
+    def short(name):
+        name = name.replace("samd::(anonymous namespace)::", "")
+        return name[5:] if name.startswith("void ") else name
+
+    out = ["| kernel | calls | avg us | min us | max us | % of GPU time |", "|---|---|---|---|---|---|"]
+    for r in one("*kernel_stats.csv"):
+        if int(r["Calls"]) < 5:
+            continue
+        out.append(f"| {short(r['Name']).split('(')[0]} | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
+                   f"{float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} | {float(r['Percentage']):.2f} |")
+    def size(r, what):   # Workgroup_Size / Grid_Size, or the product of their _X, _Y, _Z columns
+        if what in r:
+            return r[what]
+        return str(int(r[what + "_X"]) * int(r[what + "_Y"]) * int(r[what + "_Z"]))
+
+    shapes = {}
+    for r in one("*kernel_trace.csv"):
+        key = (short(r["Kernel_Name"]).split("(")[0], size(r, "Workgroup_Size"), size(r, "Grid_Size"),
+               r.get("VGPR_Count", ""), r.get("SGPR_Count", ""))
+        shapes.setdefault(key, []).append(int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
+    out += ["", "| kernel | workgroup | grid (threads) | VGPR | SGPR | dispatches | avg us | min us | avg of the last 20 us |",
+            "|---|---|---|---|---|---|---|---|---|"]
+    for (name, wg, grid, vg, sg), d in shapes.items():
+        if len(d) < 5:
+            continue
+        out.append(f"| {name} | {wg} | {grid} | {vg} | {sg} | {len(d)} | {sum(d) / len(d) / 1e3:.2f} | "
+                   f"{min(d) / 1e3:.2f} | {sum(d[-20:]) / len(d[-20:]) / 1e3:.2f} |")
+    return "\n".join(out)
+
+
 def stored_traffic():
     """The traffic summary committed under profiles/, or None when the kernel's sources have
     changed since the counters were taken."""
@@ -127,6 +172,9 @@ def stored_traffic():
 
 def main():
     args = parse()
+    if args.trace_summary:
+        print(trace_summary(args.trace_summary))
+        return
     if args.traffic_summary:
         print(json.dumps(traffic_summary(*args.traffic_summary, [int(b) for b in args.bits.split(",")]), indent=1))
         return
@@ -302,18 +350,18 @@ def main():
     cpu = None
     if not args.no_cpu_baseline:
         from oracle import reference as ref
-        done, spent, sample = 0, 0.0, []
-        for L in layers:
-            if spent >= args.cpu_seconds:
-                break
+        # the layers in step order, repeated until the time budget is spent
+        done, spent, nlayers = 0, 0.0, 0
+        while spent < args.cpu_seconds:
+            L = layers[nlayers % len(layers)]
             c0 = time.perf_counter()
             ref.conv2d(L["case"].x, L["case"].w, shape.as_tuple())
             spent += time.perf_counter() - c0
             done += macs
-            sample.append(L["b"])
+            nlayers += 1
         cpu = {"value": round(done / spent / 1e9, 2), "unit": "GMAC/s", "cores": ref.threads(), "kind": "oracle",
-               "sample": f"int64 direct conv2d of the same layer at b={sample} ({len(sample)} layers, "
-                         f"{done / 1e9:.1f} GMAC, {spent:.1f} s)"}
+               "sample": f"int64 direct conv2d of the same layer, the step's bit widths {bits_list} in turn "
+                         f"({nlayers} layers, {done / 1e9:.1f} GMAC, {spent:.1f} s)"}
 
     achieved = tot_mads / tot_conv_s
     line = {
