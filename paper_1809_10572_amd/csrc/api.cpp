@@ -341,6 +341,12 @@ int int8_setup(samd_fmt xf, samd_fmt wf, const samd_conv2d_desc *d, const void *
     if (!st) st = check_conv2d_desc(d);
     if (!st) st = check_overflow(d, xf, wf);
     if (st) return st;
+    // the kernel addresses the activations and 128 filters' reordered weights with
+    // 32-bit byte offsets
+    const int64_t cp = (d->C + 127) / 128 * 128;
+    if ((int64_t)d->N * d->H * d->W * d->C >= ((int64_t)1 << 31) ||
+        (int64_t)128 * d->KH * d->KW * cp >= ((int64_t)1 << 31))
+        return fail(SAMD_EUNSUPPORTED, "the activations or 128 filters exceed 2 GiB");
     if (!ws) return fail(SAMD_EINVAL, "ws must not be NULL");
     if (((uintptr_t)ws & 255) != 0) return fail(SAMD_EALIGN, "workspace not 256-byte aligned");
     size_t need = conv2d_i8_workspace_bytes(*d, xf);
