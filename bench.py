@@ -45,6 +45,9 @@ def parse():
     p.add_argument("--counters", action="store_true",
                    help="launch each kernel once per bit width, eagerly, then a 1 GiB streaming copy, and exit "
                         "(the program rocprofv3 --pmc passes run)")
+    p.add_argument("--vggb", action="store_true",
+                   help="instead of the default workload, sweep the ten VGG-B convolution layers (batch 1) over "
+                        "N-bit signed activations and weights, N = 8..2 (or --bits), SAMD and int8 baseline")
     p.add_argument("--trace-summary", metavar="TRACE_DIR",
                    help="print markdown tables of a rocprofv3 --kernel-trace --stats output folder (csv) and exit")
     p.add_argument("--traffic-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
@@ -170,8 +173,110 @@ def stored_traffic():
     return data if data.get("source_sha256") == kernel_source_sha() else None
 
 
+def capture_graph(fn, reps):
+    """fn() called reps times, captured once into a HIP graph (replays skip the host)."""
+    import torch
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        fn()
+    torch.cuda.current_stream().wait_stream(side)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        for _ in range(reps):
+            fn()
+    return graph
+
+
+def timed_graph(fn, reps, warm_s):
+    """Seconds per call of fn: HIP events on the launching stream around one replay of a
+    graph of reps calls (the GPU never waits for the host), after warm_s seconds of
+    back-to-back replays (the clocks rise under sustained load)."""
+    import torch
+    graph = capture_graph(fn, reps)
+    graph.replay()
+    torch.cuda.synchronize()
+    t_end = time.perf_counter() + warm_s
+    while time.perf_counter() < t_end:
+        graph.replay()
+        torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    graph.replay()
+    e1.record(stream)
+    e1.synchronize()
+    return e0.elapsed_time(e1) * 1e-3 / reps
+
+
+def run_vggb(args):
+    """The paper's own experiment (Sec. 7): every VGG-B convolution layer at batch 1 with
+    N-bit signed activations and weights, N = 8 down to 2, next to the native-int8
+    baseline on the same layer.  Prints one JSON line."""
+    import numpy as np
+    import torch
+
+    import paper_1809_10572_amd as samd
+    import samd_workloads as wl
+    from oracle import reference as ref
+
+    dev = torch.device("cuda:0")
+    bits_list = [int(b) for b in args.bits.split(",")] if args.bits_given else wl.BITS_SWEEP[6]
+    rows, tot_macs, tot_s, tot_int8_s = [], 0, 0.0, 0.0
+    for li, shape in enumerate(wl.VGGB_LAYERS):
+        Ho, Wo = samd.out_hw(shape)
+        macs = shape.N * shape.M * Ho * Wo * shape.C * shape.KH * shape.KW
+        for b in bits_list:
+            case = wl.vggb_case(li, b)
+            f = samd.Fmt(b, True)
+            x = torch.from_numpy(case.x.astype(np.int8)).to(dev)
+            x_nhwc = torch.from_numpy(np.ascontiguousarray(np.transpose(case.x, (0, 2, 3, 1))).astype(np.int8)).to(dev)
+            w8 = torch.from_numpy(case.w.astype(np.int8)).to(dev)
+            ws = samd.conv2d_prepare(samd.pack(w8, b, True), f, shape, f)
+            ws8 = samd.conv2d_int8_prepare(w8, f, shape, f)
+            xp = samd.pack(x, b, True)
+            y = torch.empty((shape.N, shape.M, Ho, Wo), dtype=torch.int32, device=dev)
+            y8 = torch.empty_like(y)
+            t_pack = timed_graph(lambda: samd.pack(x, b, True, out=xp), args.reps, args.kernel_warm_s)
+            t_samd = timed_graph(lambda: samd.conv2d_prepared(xp, f, f, shape, ws, out=y), args.reps,
+                                 args.kernel_warm_s)
+            t_int8 = timed_graph(lambda: samd.conv2d_int8_prepared(x_nhwc, f, f, shape, ws8, out=y8), args.reps,
+                                 args.kernel_warm_s)
+            torch.cuda.synchronize()
+            rng = np.random.default_rng(li * 10 + b)
+            idx = np.stack([rng.integers(0, n, 256) for n in (shape.N, shape.M, Ho, Wo)], axis=1)
+            want = ref.conv2d_points(case.x, case.w, shape.as_tuple(), idx)
+            ok = bool(np.array_equal(y.cpu().numpy()[tuple(idx.T)], want) and
+                      np.array_equal(y8.cpu().numpy()[tuple(idx.T)], want))
+            p = samd.conv2d_plan(shape, f, f)
+            rows.append({"layer": li + 1, "C": shape.C, "M": shape.M, "HW": shape.H, "bits": b,
+                         "samd_us": round(t_samd * 1e6, 2), "pack_us": round(t_pack * 1e6, 2),
+                         "int8_us": round(t_int8 * 1e6, 2), "samd_gmacs": round(macs / t_samd / 1e9, 1),
+                         "int8_gmacs": round(macs / t_int8 / 1e9, 1), "speedup_vs_int8": round(t_int8 / t_samd, 3),
+                         "lane_bits": p.lane_bits, "lanes": p.lanes, "tap_words": p.tap_words,
+                         "flush_channels": p.flush_channels, "parity": ok})
+            tot_macs += macs
+            tot_s += t_samd
+            tot_int8_s += t_int8
+            print(f"vggb: layer {li + 1} b={b} samd {t_samd * 1e6:.1f} us int8 {t_int8 * 1e6:.1f} us "
+                  f"parity {ok}", file=sys.stderr, flush=True)
+    line = {"metric": "VGG-B conv layers, N-bit signed activations and weights (N = 8..2), GMAC/s",
+            "value": round(tot_macs / tot_s / 1e9, 1), "unit": "GMAC/s", "n_gpus": 1,
+            "higher_is_better": True, "dtype": "int64", "data": "synthetic",
+            "config": {"workload": "VGG-B's ten 3x3 convolution layers, batch 1, each layer on its own; "
+                                   "one call = stage + accumulate with prepared kernel words",
+                       "bits": bits_list},
+            "int8_gmacs": round(tot_macs / tot_int8_s / 1e9, 1),
+            "per_layer": rows}
+    print(json.dumps(line), flush=True)
+
+
 def main():
     args = parse()
+    args.bits_given = "--bits" in sys.argv
+    if args.vggb:
+        run_vggb(args)
+        return
     if args.trace_summary:
         print(trace_summary(args.trace_summary))
         return
@@ -240,18 +345,7 @@ def main():
             samd.pack(L["x"], L["b"], False, out=L["xp"])
             samd.conv2d_prepared(L["xp"], L["xf"], L["wf"], shape, L["ws"], out=L["y"])
 
-    def capture(fn, reps):
-        """fn() called reps times, captured once into a HIP graph (replays skip the host)."""
-        side = torch.cuda.Stream()
-        side.wait_stream(torch.cuda.current_stream())
-        with torch.cuda.stream(side):
-            fn()
-        torch.cuda.current_stream().wait_stream(side)
-        graph = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(graph):
-            for _ in range(reps):
-                fn()
-        return graph
+    capture = capture_graph
 
     # eager steps: every kernel launched from the host
     for _ in range(args.warmup):
@@ -274,24 +368,8 @@ def main():
     torch.cuda.synchronize()
     ms_per_step = (time.perf_counter() - t0) * 1e3 / args.steps
 
-    # Per-kernel durations: HIP events on the launching stream around one replay of a
-    # graph of REPS launches of that kernel alone (the GPU never waits for the host).
-    stream = torch.cuda.current_stream()
-
     def timed(fn, reps):
-        graph = capture(fn, reps)
-        graph.replay()
-        torch.cuda.synchronize()
-        t_end = time.perf_counter() + args.kernel_warm_s
-        while time.perf_counter() < t_end:
-            graph.replay()
-            torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        graph.replay()
-        e1.record(stream)
-        e1.synchronize()
-        return e0.elapsed_time(e1) * 1e-3 / reps
+        return timed_graph(fn, reps, args.kernel_warm_s)
 
     for L in layers:
         samd.conv2d_stage(L["xp"], L["xf"], L["wf"], shape, L["ws"])

@@ -80,12 +80,17 @@ enum {
  *                (a signed b-bit value) enters the lanes, halving the largest product,
  *                and x_offset times the sum of each output's in-image weights is added
  *                back when the output is stored
+ *   col_segments, segment_columns: output rows of more than 64 operand words are split
+ *                into col_segments ranges of segment_columns output columns (a multiple
+ *                of I), each computed from the at most 64 words it needs (words reaching
+ *                two ranges are computed for both); 1 and Wo otherwise
  *   macs_per_mad multiply-accumulates delivered per 32x32->64 multiply (I * taps) */
 typedef struct {
     int32_t lane_bits, lanes, taps_max, words_per_row, flush_channels, out_lanes, tap_words;
     int32_t phase[16], tap0[16], ntaps[16];
     int32_t rows_per_block, mblock, split_waves, chunk_channels;
     int32_t x_offset;
+    int32_t col_segments, segment_columns;
     double macs_per_mad;
 } samd_conv2d_plan;
 

@@ -54,6 +54,7 @@ class Conv2dPlan(ctypes.Structure):
                 ("out_lanes", ctypes.c_int32), ("tap_words", ctypes.c_int32), ("phase", ctypes.c_int32 * 16), ("tap0", ctypes.c_int32 * 16),
                 ("ntaps", ctypes.c_int32 * 16), ("rows_per_block", ctypes.c_int32), ("mblock", ctypes.c_int32),
                 ("split_waves", ctypes.c_int32), ("chunk_channels", ctypes.c_int32), ("x_offset", ctypes.c_int32),
+                ("col_segments", ctypes.c_int32), ("segment_columns", ctypes.c_int32),
                 ("macs_per_mad", ctypes.c_double)]
 
 

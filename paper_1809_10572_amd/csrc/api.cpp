@@ -205,6 +205,8 @@ int samd_conv2d_plan_query(const samd_conv2d_desc *d, samd_fmt xf, samd_fmt wf, 
     out->split_waves = g.ks;
     out->chunk_channels = g.chk;
     out->x_offset = g.xoff;
+    out->col_segments = g.ncs;
+    out->segment_columns = g.cw;
     out->macs_per_mad = g.macs_per_mad;
     return SAMD_OK;
 }

@@ -93,37 +93,40 @@ __global__ __launch_bounds__(256) void prefix_kernel(const uint32_t *__restrict_
 
 // Operand words xs[n][c][hp][t][q] for padded rows hp in [0, H + 2 ph), of the
 // activations minus xoff (recentred unsigned activations).  A block of 256
-// threads covers 256 / QP padded rows (QP = nq rounded up to a power of two): thread
-// (row, q) builds word q of every kernel-word variant t of its row from the packed input
-// row (L1-resident; rows of the zero padding give zeros).
+// threads covers 256 / QP padded rows (QP = nq rounded up to a power of two, at most
+// 256): thread (row, q) builds word q (and q + QP, ... for rows of more than 256 words)
+// of every kernel-word variant t of its row from the packed input row (L1-resident; rows
+// of the zero padding give zeros).
 template <int B, bool S>
 __global__ __launch_bounds__(256) void spread_kernel(const uint32_t *__restrict__ x, const Conv2dGeom g, int qshift,
                                                      int32_t *__restrict__ xs) {
     constexpr int P = 32 / B;
-    const int q = threadIdx.x & ((1 << qshift) - 1);
     const int64_t row = (int64_t)blockIdx.x * (256 >> qshift) + (threadIdx.x >> qshift);   // (n*C + c)*Hp + hp
-    if (q >= g.nq || row >= (int64_t)g.N * g.C * g.Hp) return;
+    if (row >= (int64_t)g.N * g.C * g.Hp) return;
     const int hp = (int)(row % g.Hp);
     const int64_t nc = row / g.Hp;
     const int h = hp - g.ph;
     const bool inside = h >= 0 && h < g.H;
     const uint32_t *src = x + (nc * g.H + (inside ? h : 0)) * g.xrw;
-    int32_t *dst = xs + row * g.ntw * g.nq + q;
-    for (int t = 0; t < g.ntw; ++t) {
-        const int delta = g.tw_tap0[t] + g.tw_ntaps[t] - g.Kmax;
-        const int col0 = g.sw * (q * g.I + delta) + g.tw_phase[t] - g.pw;
-        uint32_t word = 0;
-        if (inside) {
-            for (int ii = 0; ii < g.I; ++ii) {
-                const int col = col0 + g.sw * ii;
-                if (col >= 0 && col < g.W) {
-                    const uint32_t f = (src[col / P] >> ((col % P) * B)) & ((1u << B) - 1);
-                    const int32_t v = (S ? ((int32_t)(f << (32 - B)) >> (32 - B)) : (int32_t)f) - g.xoff;
-                    word += (uint32_t)v << (ii * g.L);
+    // words q, q + 2^qshift, ... of the row (one pass unless the row has more than 256)
+    for (int q = threadIdx.x & ((1 << qshift) - 1); q < g.nq; q += 1 << qshift) {
+        int32_t *dst = xs + row * g.ntw * g.nq + q;
+        for (int t = 0; t < g.ntw; ++t) {
+            const int delta = g.tw_tap0[t] + g.tw_ntaps[t] - g.Kmax;
+            const int col0 = g.sw * (q * g.I + delta) + g.tw_phase[t] - g.pw;
+            uint32_t word = 0;
+            if (inside) {
+                for (int ii = 0; ii < g.I; ++ii) {
+                    const int col = col0 + g.sw * ii;
+                    if (col >= 0 && col < g.W) {
+                        const uint32_t f = (src[col / P] >> ((col % P) * B)) & ((1u << B) - 1);
+                        const int32_t v = (S ? ((int32_t)(f << (32 - B)) >> (32 - B)) : (int32_t)f) - g.xoff;
+                        word += (uint32_t)v << (ii * g.L);
+                    }
                 }
             }
+            dst[t * g.nq] = (int32_t)word;
         }
-        dst[t * g.nq] = (int32_t)word;
     }
 }
 
@@ -227,7 +230,7 @@ __global__ __launch_bounds__(1024) void conv2d_samd_kernel(const int32_t *__rest
     __shared__ int32_t next_item;
 
     const int xcd = blockIdx.x % kNumXcd;
-    const int ntiles = g.N * g.row_tiles;
+    const int ntiles = g.tiles;                                          // N x row tiles x column segments
     const int nitems = (ntiles - xcd + kNumXcd - 1) / kNumXcd * g.nmb;   // items of this XCD
     const int nwg = gridDim.x / kNumXcd;                                 // workgroups of this XCD
     const int nextra = max(0, nitems - nwg);                             // items handed out by ticket
@@ -239,10 +242,10 @@ __global__ __launch_bounds__(1024) void conv2d_samd_kernel(const int32_t *__rest
     const int kq = wave / g.wm;
     const int mw = wave - kq * g.wm;
     const int lane = tid & 63;
-    const int grp_raw = lane / g.nq;
+    const int grp_raw = lane / g.nqs;
     const bool lane_ok = grp_raw < g.groups;
     const int grp = lane_ok ? grp_raw : 0;
-    const int q = lane_ok ? lane - grp_raw * g.nq : 0;
+    const int q = lane_ok ? lane - grp_raw * g.nqs : 0;   // word within the column segment
 
     {
         int4 *t4 = (int4 *)tile;   // lds_tile is a multiple of 4 words
@@ -303,10 +306,14 @@ __global__ __launch_bounds__(1024) void conv2d_samd_kernel(const int32_t *__rest
         unsigned long long ticket = 0;
         if (nextra > 0 && tid == 0) ticket = atomicAdd(counter, 1ull);
         const int mb = item % g.nmb;
-        const int tile_id = (item / g.nmb) * kNumXcd + xcd;
-        const int n = tile_id / g.row_tiles;
-        const int ho0 = (tile_id % g.row_tiles) * g.rows_blk;
+        const int tile_id = (item / g.nmb) * kNumXcd + xcd;   // (n, row tile, column segment)
+        const int cs = tile_id % g.ncs;
+        const int n = tile_id / g.ncs / g.row_tiles;
+        const int ho0 = (tile_id / g.ncs % g.row_tiles) * g.rows_blk;
         const int wb = mb * g.wm + mw;
+        // the lane's word in the row; words past the row (last segment) read its last
+        // word and only reach columns that are never stored
+        const int qg = min(cs * (g.cw / g.I) + q, g.nq - 1);
 
         // Operand word of step s (s = ky*ntw + t) of channel c for this lane's row r:
         // xs[n][c][hp][t][q] with hp = (ho0 + row)*sh + ky, i.e. word
@@ -317,7 +324,7 @@ __global__ __launch_bounds__(1024) void conv2d_samd_kernel(const int32_t *__rest
 #pragma unroll
         for (int r = 0; r < RH; ++r) {
             const int row = min(ho0 + min(grp * RH + r, g.rows_blk - 1), g.Ho - 1);
-            lb[r] = (row * g.sh * g.ntw * g.nq + q) * 4;
+            lb[r] = (row * g.sh * g.ntw * g.nq + qg) * 4;
         }
         // the image's channels and one spare channel after them
         const __amdgpu_buffer_rsrc_t xrs = __builtin_amdgcn_make_buffer_rsrc(
@@ -362,7 +369,7 @@ __global__ __launch_bounds__(1024) void conv2d_samd_kernel(const int32_t *__rest
             int lbi[NA];
 #pragma unroll
             for (int i = 0; i < NA; ++i)
-                lbi[i] = (min(ho0 + grp * RH + i, g.Hp - 1) * RNTW * g.nq + q) * 4;
+                lbi[i] = (min(ho0 + grp * RH + i, g.Hp - 1) * RNTW * g.nq + qg) * 4;
             const int nbat = (cend - cbeg) * RNTW;
             const int seg = g.G * RNTW;
             int32_t kRA[kStepBatch * RM], aRA[NA], kRB[kStepBatch * RM], aRB[NA];
@@ -520,16 +527,18 @@ __global__ __launch_bounds__(1024) void conv2d_samd_kernel(const int32_t *__rest
         const int nwaves = g.wm * g.ks;
         const int dmm = nwaves / g.rows_blk, dr = nwaves - dmm * g.rows_blk;
         int mm = wave / g.rows_blk, r = wave - mm * g.rows_blk;
+        const int c0 = cs * g.cw, ncols = min(g.cw, g.Wo - c0);   // the segment's output columns
         while (mm < g.mblk) {
             const int m = mb * g.mblk + mm, ho = ho0 + r;
-            // each tile word of an output column is zeroed for the next item once read,
-            // also in rows past the image and channels past M, which another item stores
+            // every tile word of a segment column (cw of them) is zeroed for the next item
+            // once read, also in rows past the image, channels past M and columns past Wo,
+            // which another item stores
             int32_t *src = tile + (mm * g.tile_rows + r) * g.tile_row + (g.Kmax - 1);
             if (m < g.M && ho < g.Ho) {
-                int32_t *dst = y + (((int64_t)n * g.M + m) * g.Ho + ho) * g.Wo;
+                int32_t *dst = y + (((int64_t)n * g.M + m) * g.Ho + ho) * g.Wo + c0;
                 if (g.xoff == 0) {
-                    for (int o = lane; o < g.Wo; o += 64) {
-                        dst[o] = src[o];
+                    for (int o = lane; o < g.cw; o += 64) {
+                        if (o < ncols) dst[o] = src[o];
                         src[o] = 0;
                     }
                 } else {
@@ -537,16 +546,18 @@ __global__ __launch_bounds__(1024) void conv2d_samd_kernel(const int32_t *__rest
                     const int hb = ho * g.sh - g.ph, kwid = g.KW + 1;
                     const int ky0 = max(0, -hb) * kwid, ky1 = min(g.KH, g.H - hb) * kwid;
                     const int32_t *pm = pre + m * (g.KH + 1) * kwid;
-                    for (int o = lane; o < g.Wo; o += 64) {
-                        const int wbeg = o * g.sw - g.pw;
-                        const int kx0 = max(0, -wbeg), kx1 = min(g.KW, g.W - wbeg);
-                        const int32_t rect = pm[ky1 + kx1] - pm[ky0 + kx1] - pm[ky1 + kx0] + pm[ky0 + kx0];
-                        dst[o] = src[o] + g.xoff * rect;
+                    for (int o = lane; o < g.cw; o += 64) {
+                        if (o < ncols) {
+                            const int wbeg = (c0 + o) * g.sw - g.pw;
+                            const int kx0 = max(0, -wbeg), kx1 = min(g.KW, g.W - wbeg);
+                            const int32_t rect = pm[ky1 + kx1] - pm[ky0 + kx1] - pm[ky1 + kx0] + pm[ky0 + kx0];
+                            dst[o] = src[o] + g.xoff * rect;
+                        }
                         src[o] = 0;
                     }
                 }
             } else {
-                for (int o = lane; o < g.Wo; o += 64) src[o] = 0;
+                for (int o = lane; o < g.cw; o += 64) src[o] = 0;
             }
             mm += dmm;
             r += dr;
@@ -593,7 +604,7 @@ int launch_conv2d_prepare(const uint32_t *w, const Conv2dGeom &g, void *ws, hipS
 int launch_conv2d_spread(const uint32_t *x, const Conv2dGeom &g, void *ws, hipStream_t s) {
     int32_t *xs = (int32_t *)((char *)ws + conv2d_xs_offset(g));
     int qshift = 0;
-    while ((1 << qshift) < g.nq) ++qshift;   // nq <= 64
+    while ((1 << qshift) < g.nq && qshift < 8) ++qshift;   // up to 256 threads per row
     const int64_t nrows = (int64_t)g.N * g.C * g.Hp;
     const int rpb = 256 >> qshift;
     const unsigned sgrid = (unsigned)((nrows + rpb - 1) / rpb);
@@ -656,7 +667,7 @@ int launch_multiply(const Conv2dGeom &g, int32_t *y, const void *ws, hipStream_t
     const int st = resident_workgroups(fn, block, shm, resident);
     if (st) return st;
     // every XCD gets the same number of workgroups; none gets more than its items
-    const int64_t xitems = (int64_t)(g.N * g.row_tiles + kNumXcd - 1) / kNumXcd * g.nmb;
+    const int64_t xitems = (int64_t)(g.tiles + kNumXcd - 1) / kNumXcd * g.nmb;
     const int64_t per_xcd = std::max<int64_t>(1, std::min<int64_t>(xitems, resident / kNumXcd));
     hipLaunchKernelGGL((conv2d_samd_kernel<RH, NRT, SG, RNTW>), dim3((unsigned)(per_xcd * kNumXcd)), dim3(block), shm, s,
                        xs, kw, pre, y, tickets, g);

@@ -74,7 +74,7 @@ bool split_taps(int count, int kmax, int *t0, int *nt, int &ngroups) {
 // grows with the waves resident per SIMD (latency hiding), plus the last item's drain and
 // the operand-spread pass.  Returns false when no tile fits the LDS.
 bool place_launch(const samd_conv2d_desc &d, Conv2dGeom &c) {
-    const int grp_max = 64 / c.nq;
+    const int grp_max = 64 / c.nqs;
     const bool rows_ok = d.KH == 3 && d.stride_h == 1 && (c.ntw == 1 || c.ntw == 2);
     bool found = false;
     Conv2dGeom best = c;
@@ -105,7 +105,7 @@ bool place_launch(const samd_conv2d_desc &d, Conv2dGeom &c) {
                     // neighbouring lane groups start on different LDS banks (row groups are
                     // rh rows apart; their offset mod 32 banks should not be a multiple of
                     // the lane stride I)
-                    t.tile_row = c.nq * c.I + c.Kmax - 1;
+                    t.tile_row = c.nqs * c.I + c.Kmax - 1;
                     for (int pad = 0; pad < c.I && c.I > 1; ++pad)
                         if ((rh * (t.tile_row + pad)) % 32 % c.I != 0) {
                             t.tile_row += pad;
@@ -118,7 +118,7 @@ bool place_launch(const samd_conv2d_desc &d, Conv2dGeom &c) {
                     if (ks > 1 && (long)(ks - 1) * t.cpw >= d.C) continue;   // an empty slice
                     t.chk = t.cpw * ks;
                     t.row_tiles = (c.Ho + t.rows_blk - 1) / t.rows_blk;
-                    t.tiles = d.N * t.row_tiles;
+                    t.tiles = d.N * t.row_tiles * c.ncs;
                     t.kw_words = (int64_t)t.nmb * wm * ((int64_t)d.C * c.nrt + kStreamPad) * kWaveM;
                     t.spread_words = (int64_t)d.N * d.C * c.Hp * c.ntw * c.nq;
 
@@ -250,12 +250,25 @@ int search_lanes(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, int xoff, 
             c.msb_mask = 0;
             for (int j = 0; j < c.nl - 1; ++j) c.msb_mask |= (uint64_t)1 << (j * L + L - 1);
             c.nq = (c.Wo + c.Kmax - 1 + I - 1) / I;
-            if (c.nq > 64) continue;
+            if (c.nq <= 64) {
+                c.nqs = c.nq;
+                c.cw = c.Wo;
+                c.ncs = 1;
+            } else {
+                // a row too wide for one wave's lanes: column segments of cw output
+                // columns (a multiple of I), each needing at most 64 words, words
+                // [c0/I, (c0 + cw + Kmax - 2)/I]; the words reaching two segments are
+                // computed by both
+                c.nqs = 64;
+                c.cw = ((c.nqs - 1) * I - (c.Kmax - 2)) / I * I;
+                if (c.cw < I) continue;
+                c.ncs = (c.Wo + c.cw - 1) / c.cw;
+            }
             c.nrt = d.KH * c.ntw;
             c.Hp = d.H + 2 * d.pad_h;
             c.macs_per_mad = (double)I * d.KW / (double)c.ntw;
             // the multiply-adds alone, spread perfectly over every SIMD, bound the cost below
-            const double floor_cost = (double)d.N * c.Ho * c.nq * d.M * d.C * c.nrt / 64.0 / 1024.0;
+            const double floor_cost = (double)d.N * c.Ho * c.ncs * c.nqs * d.M * d.C * c.nrt / 64.0 / 1024.0;
             if (found && floor_cost >= best.cost) continue;
             if (!place_launch(d, c)) continue;
             if (c.cost < best.cost) {

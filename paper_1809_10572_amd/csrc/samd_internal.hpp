@@ -41,6 +41,9 @@ struct Conv2dGeom {
     int32_t xoff;                   // subtracted from every activation (recentred unsigned
                                     // activations: 2^(xbits-1)); 0 otherwise
     int32_t L, I, Kmax, nq, G;      // lane bits, values/word, widest phase, words/row, flush channels
+    int32_t nqs;                    // words of one column segment (<= 64: a lane group's words)
+    int32_t cw;                     // output columns per column segment (Wo when ncs == 1)
+    int32_t ncs;                    // column segments per output row
     int32_t nl;                     // decoded lanes per accumulator; lane nl-1 takes the remaining bits
     int32_t result_signed;          // any operand signed: lanes need the fix-up
     uint64_t msb_mask;              // sign bit of lanes 0 .. nl-2
@@ -51,21 +54,21 @@ struct Conv2dGeom {
     int32_t rows_path;              // 1: 3-row stride-1 kernel whose output rows share operand loads
                                     // (kernel-word streams kernel-word-major within a channel)
     int32_t rh;                     // output rows per thread
-    int32_t groups;                 // row groups per wave: 64 / nq
+    int32_t groups;                 // row groups per wave: 64 / nqs
     int32_t rows_blk;               // output rows per workgroup: rh * groups
     int32_t wm;                     // output-channel waves per workgroup, each kWaveM channels
     int32_t ks;                     // channel-split waves: wave (kq, mw) multiplies channel slice kq
     int32_t mblk;                   // output channels per workgroup, wm * kWaveM
     int32_t nmb;                    // output-channel blocks
     int32_t row_tiles;              // ceil(Ho / rows_blk)
-    int32_t tiles;                  // N * row_tiles
+    int32_t tiles;                  // spatial tiles: N * row_tiles * ncs
     int32_t chk;                    // ks * cpw (reported)
     int32_t cpw;                    // input channels of one wave's slice: ceil(C / ks)
     int32_t trows;                  // input rows a tile reads, (rows_blk-1)*sh + KH
     int32_t xrw;                    // packed words per input row
     int32_t wrw;                    // packed words per kernel row
     int32_t tile_rows;              // output-tile rows per channel: groups * rh
-    int32_t tile_row;               // output-tile words per row: nq * I + Kmax - 1 (column o at o + Kmax - 1)
+    int32_t tile_row;               // output-tile words per row: nqs * I + Kmax - 1 (segment column o at o + Kmax - 1)
     int32_t lds_tile;               // LDS words of the output tile (a multiple of 4)
     int32_t lds_words;              // LDS words in all
     int64_t kw_words, spread_words; // workspace: kernel-word streams, operand words (after the

@@ -4,9 +4,11 @@ This module is shared by the CPU oracle (``oracle/``) and the GPU path's tests a
 benchmark.  It draws integers and describes shapes; it holds none of the method's
 arithmetic (no packing, no convolution, no requantisation).
 
-Every input is synthetic.  The paper measures the VGG-B convolution layers
-(Experimental Setup, Sec. 7), whose shapes live in the cited VGG paper and are not
-reproduced here; the five workloads below stand in for them:
+Every input is synthetic: no trained weights or images are used.  The paper measures
+the convolution layers of VGG-B (Experimental Setup, Sec. 7) with N-bit signed weights
+and activations, N = 8 down to 2; workload 6 has those layer shapes (the published
+architecture: 3x3 kernels, stride 1, pad 1, batch 1) with uniform synthetic values.
+Workloads 1-5 are the other cases:
 
 1. ``single``  - one conv2d layer, 1x16x16x16 -> 16 channels, 3x3, stride 1, pad 1,
    unsigned b-bit activations, signed b-bit weights (b = 4 by default).
@@ -17,6 +19,9 @@ reproduced here; the five workloads below stand in for them:
    the values at the two range extremes (sign fix-up and carry stress).
 5. ``alexnet`` - five-layer AlexNet-shaped stack on 16x3x224x224 (11x11/4 96ch,
    5x5 256ch, 3x3 384ch, 3x3 384ch, 3x3 256ch), unsigned activations, signed weights.
+6. ``vggb``    - the ten VGG-B convolution layers, each on its own (batch 1, input
+   sizes as after VGG-B's max-pools: 224, 224, 112, 112, 56, 56, 28, 28, 14, 14),
+   signed b-bit activations and weights, uniform; seed offset = layer index.
 
 Value recipe: numpy ``Generator(PCG64(seed))`` with
 ``seed = 1809105720 + 1000*cfg + 10*bits + K`` (K = taps for conv1d, else 0).
@@ -122,7 +127,24 @@ ALEXNET_LAYERS = [
     Conv2dShape(16, 384, 55, 55, 256, 3, 3, 1, 1, 1, 1),
 ]
 
-BITS_SWEEP = {1: [4], 2: list(range(1, 9)), 3: list(range(1, 9)), 4: list(range(2, 9)), 5: [2, 4, 8]}
+# VGG-B (configuration B of Simonyan and Zisserman): ten 3x3 convolutions, stride 1,
+# pad 1; a 2x2 max-pool halves the size after layers 2, 4, 6 and 8 (the pools are not
+# part of these single-layer workloads).
+VGGB_LAYERS = [
+    Conv2dShape(1, 3, 224, 224, 64, 3, 3, 1, 1, 1, 1),
+    Conv2dShape(1, 64, 224, 224, 64, 3, 3, 1, 1, 1, 1),
+    Conv2dShape(1, 64, 112, 112, 128, 3, 3, 1, 1, 1, 1),
+    Conv2dShape(1, 128, 112, 112, 128, 3, 3, 1, 1, 1, 1),
+    Conv2dShape(1, 128, 56, 56, 256, 3, 3, 1, 1, 1, 1),
+    Conv2dShape(1, 256, 56, 56, 256, 3, 3, 1, 1, 1, 1),
+    Conv2dShape(1, 256, 28, 28, 512, 3, 3, 1, 1, 1, 1),
+    Conv2dShape(1, 512, 28, 28, 512, 3, 3, 1, 1, 1, 1),
+    Conv2dShape(1, 512, 14, 14, 512, 3, 3, 1, 1, 1, 1),
+    Conv2dShape(1, 512, 14, 14, 512, 3, 3, 1, 1, 1, 1),
+]
+
+BITS_SWEEP = {1: [4], 2: list(range(1, 9)), 3: list(range(1, 9)), 4: list(range(2, 9)), 5: [2, 4, 8],
+              6: list(range(8, 1, -1))}
 
 
 def conv2d_case(cfg: int, bits: int, shape: Conv2dShape = None) -> Conv2dCase:
@@ -164,3 +186,16 @@ def stack_case(bits: int, batch: int = None, layers: List[Conv2dShape] = None) -
     x = uniform(rng, (first.N, first.C, first.H, first.W), bits, False)
     ws = [uniform(rng, (l.M, l.C, l.KH, l.KW), bits, True) for l in lys]
     return StackCase(bits, lys, x, ws, seed)
+
+
+def vggb_case(layer: int, bits: int, batch: int = 1) -> Conv2dCase:
+    """Workload 6: VGG-B convolution layer ``layer`` (0-9), signed b-bit activations and
+    weights, uniform over the range."""
+    seed = seed_for(6, bits, layer)
+    rng = np.random.Generator(np.random.PCG64(seed))
+    shp = VGGB_LAYERS[layer]
+    if batch != shp.N:
+        shp = Conv2dShape(batch, *shp.as_tuple()[1:])
+    x = uniform(rng, (shp.N, shp.C, shp.H, shp.W), bits, True)
+    w = uniform(rng, (shp.M, shp.C, shp.KH, shp.KW), bits, True)
+    return Conv2dCase(6, bits, shp, True, True, x, w, seed)

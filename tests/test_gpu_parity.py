@@ -141,6 +141,9 @@ EDGE = [
     wl.Conv2dShape(1, 300, 6, 6, 70, 3, 3, 1, 1, 1, 1),       # many channels, several decodes
     wl.Conv2dShape(3, 16, 8, 120, 48, 1, 1, 1, 1, 0, 0),      # 1x1, the vector-scale case
     wl.Conv2dShape(1, 8, 130, 9, 16, 3, 3, 1, 1, 1, 1),       # tall image, many row blocks
+    wl.Conv2dShape(2, 5, 6, 300, 12, 3, 3, 1, 1, 1, 1),       # wide rows: several column segments
+    wl.Conv2dShape(1, 3, 7, 700, 9, 3, 5, 2, 2, 1, 2),        # wide, strided, 5 taps
+    wl.Conv2dShape(1, 2, 3, 1100, 8, 3, 3, 1, 1, 1, 1),       # rows of more than 256 operand words
 ]
 
 
@@ -288,6 +291,21 @@ def test_prepared_weights_are_reusable(bits):
         torch.cuda.synchronize()
         np.testing.assert_array_equal(y.cpu().numpy(), want)
         np.testing.assert_array_equal(y8.cpu().numpy(), want)
+
+
+@pytest.mark.parametrize("bits", [2, 3, 5, 8])
+def test_vggb_layers(bits):
+    """The paper's experiment shapes (Sec. 7): all ten VGG-B convolution layers at batch
+    1 with signed b-bit activations and weights, SAMD and the int8 baseline, every output
+    against the oracle."""
+    f = samd.Fmt(bits, True)
+    for li in range(len(wl.VGGB_LAYERS)):
+        case = wl.vggb_case(li, bits)
+        want = ref.conv2d(case.x, case.w, case.shape.as_tuple())
+        np.testing.assert_array_equal(run_conv2d(case.x, case.w, case.shape, f, f), want,
+                                      err_msg=f"SAMD layer {li + 1}")
+        np.testing.assert_array_equal(run_conv2d_int8(case.x, case.w, case.shape, f, f), want,
+                                      err_msg=f"int8 layer {li + 1}")
 
 
 @pytest.mark.parametrize("bx,sx,bw,sw", [(1, 0, 1, 1), (4, 0, 4, 1), (5, 1, 6, 1), (8, 0, 8, 1)])
