@@ -219,7 +219,7 @@ __device__ __forceinline__ void decode_word_n(uint64_t v, uint64_t msb_mask, int
 // Every operand load costs the compute unit's texture path far more cycles than a
 // multiply-add costs a SIMD, and the four SIMDs share that path, so loads, not
 // multiply-adds, bound the loop unless each load feeds enough of them.
-template <int RH, int NRT, bool SG, int RNTW>
+template <int RH, int NRT, bool SG, int RNTW, bool SEG>
 __global__ __launch_bounds__(1024) void conv2d_samd_kernel(const int32_t *__restrict__ xs,
                                                            const int32_t *__restrict__ kw,
                                                            const int32_t *__restrict__ pre, int32_t *__restrict__ y,
@@ -307,13 +307,15 @@ __global__ __launch_bounds__(1024) void conv2d_samd_kernel(const int32_t *__rest
         if (nextra > 0 && tid == 0) ticket = atomicAdd(counter, 1ull);
         const int mb = item % g.nmb;
         const int tile_id = (item / g.nmb) * kNumXcd + xcd;   // (n, row tile, column segment)
-        const int cs = tile_id % g.ncs;
-        const int n = tile_id / g.ncs / g.row_tiles;
-        const int ho0 = (tile_id / g.ncs % g.row_tiles) * g.rows_blk;
+        // SEG: rows are split into column segments; without, the segment terms fold away
+        // (their run-time divisions and bounds cost measurable time per item)
+        const int cs = SEG ? tile_id % g.ncs : 0, rt_id = SEG ? tile_id / g.ncs : tile_id;
+        const int n = rt_id / g.row_tiles;
+        const int ho0 = (rt_id - n * g.row_tiles) * g.rows_blk;
         const int wb = mb * g.wm + mw;
         // the lane's word in the row; words past the row (last segment) read its last
         // word and only reach columns that are never stored
-        const int qg = min(cs * (g.cw / g.I) + q, g.nq - 1);
+        const int qg = SEG ? min(cs * g.qseg + q, g.nq - 1) : q;
 
         // Operand word of step s (s = ky*ntw + t) of channel c for this lane's row r:
         // xs[n][c][hp][t][q] with hp = (ho0 + row)*sh + ky, i.e. word
@@ -527,7 +529,8 @@ __global__ __launch_bounds__(1024) void conv2d_samd_kernel(const int32_t *__rest
         const int nwaves = g.wm * g.ks;
         const int dmm = nwaves / g.rows_blk, dr = nwaves - dmm * g.rows_blk;
         int mm = wave / g.rows_blk, r = wave - mm * g.rows_blk;
-        const int c0 = cs * g.cw, ncols = min(g.cw, g.Wo - c0);   // the segment's output columns
+        const int c0 = SEG ? cs * g.cw : 0, ncols = SEG ? min(g.cw, g.Wo - c0) : g.Wo;   // the segment's output columns
+        const int segw = SEG ? g.cw : g.Wo;
         while (mm < g.mblk) {
             const int m = mb * g.mblk + mm, ho = ho0 + r;
             // every tile word of a segment column (cw of them) is zeroed for the next item
@@ -537,8 +540,8 @@ __global__ __launch_bounds__(1024) void conv2d_samd_kernel(const int32_t *__rest
             if (m < g.M && ho < g.Ho) {
                 int32_t *dst = y + (((int64_t)n * g.M + m) * g.Ho + ho) * g.Wo + c0;
                 if (g.xoff == 0) {
-                    for (int o = lane; o < g.cw; o += 64) {
-                        if (o < ncols) dst[o] = src[o];
+                    for (int o = lane; o < ncols; o += 64) {
+                        dst[o] = src[o];
                         src[o] = 0;
                     }
                 } else {
@@ -546,18 +549,19 @@ __global__ __launch_bounds__(1024) void conv2d_samd_kernel(const int32_t *__rest
                     const int hb = ho * g.sh - g.ph, kwid = g.KW + 1;
                     const int ky0 = max(0, -hb) * kwid, ky1 = min(g.KH, g.H - hb) * kwid;
                     const int32_t *pm = pre + m * (g.KH + 1) * kwid;
-                    for (int o = lane; o < g.cw; o += 64) {
-                        if (o < ncols) {
-                            const int wbeg = (c0 + o) * g.sw - g.pw;
-                            const int kx0 = max(0, -wbeg), kx1 = min(g.KW, g.W - wbeg);
-                            const int32_t rect = pm[ky1 + kx1] - pm[ky0 + kx1] - pm[ky1 + kx0] + pm[ky0 + kx0];
-                            dst[o] = src[o] + g.xoff * rect;
-                        }
+                    for (int o = lane; o < ncols; o += 64) {
+                        const int wbeg = (c0 + o) * g.sw - g.pw;
+                        const int kx0 = max(0, -wbeg), kx1 = min(g.KW, g.W - wbeg);
+                        const int32_t rect = pm[ky1 + kx1] - pm[ky0 + kx1] - pm[ky1 + kx0] + pm[ky0 + kx0];
+                        dst[o] = src[o] + g.xoff * rect;
                         src[o] = 0;
                     }
                 }
+                // the columns past Wo of the last segment
+                if (SEG)
+                    for (int o = ncols + lane; o < segw; o += 64) src[o] = 0;
             } else {
-                for (int o = lane; o < g.cw; o += 64) src[o] = 0;
+                for (int o = lane; o < segw; o += 64) src[o] = 0;
             }
             mm += dmm;
             r += dr;
@@ -653,8 +657,8 @@ int resident_workgroups(const void *kernel, int block, size_t shm, int &out) {
     return SAMD_OK;
 }
 
-template <int RH, int NRT, bool SG, int RNTW>
-int launch_multiply(const Conv2dGeom &g, int32_t *y, const void *ws, hipStream_t s) {
+template <int RH, int NRT, bool SG, int RNTW, bool SEG>
+int launch_multiply_seg(const Conv2dGeom &g, int32_t *y, const void *ws, hipStream_t s) {
     const int32_t *kw = (const int32_t *)ws;
     const int32_t *pre = (const int32_t *)((const char *)ws + conv2d_kw_bytes(g));
     unsigned long long *tickets =
@@ -662,16 +666,22 @@ int launch_multiply(const Conv2dGeom &g, int32_t *y, const void *ws, hipStream_t
     const int32_t *xs = (const int32_t *)((const char *)ws + conv2d_xs_offset(g));
     const int block = g.wm * g.ks * 64;
     const size_t shm = (size_t)g.lds_words * 4;
-    const void *fn = (const void *)conv2d_samd_kernel<RH, NRT, SG, RNTW>;
+    const void *fn = (const void *)conv2d_samd_kernel<RH, NRT, SG, RNTW, SEG>;
     int resident = 0;
     const int st = resident_workgroups(fn, block, shm, resident);
     if (st) return st;
     // every XCD gets the same number of workgroups; none gets more than its items
     const int64_t xitems = (int64_t)(g.tiles + kNumXcd - 1) / kNumXcd * g.nmb;
     const int64_t per_xcd = std::max<int64_t>(1, std::min<int64_t>(xitems, resident / kNumXcd));
-    hipLaunchKernelGGL((conv2d_samd_kernel<RH, NRT, SG, RNTW>), dim3((unsigned)(per_xcd * kNumXcd)), dim3(block), shm, s,
+    hipLaunchKernelGGL((conv2d_samd_kernel<RH, NRT, SG, RNTW, SEG>), dim3((unsigned)(per_xcd * kNumXcd)), dim3(block), shm, s,
                        xs, kw, pre, y, tickets, g);
     return check_launch("conv2d");
+}
+
+template <int RH, int NRT, bool SG, int RNTW>
+int launch_multiply(const Conv2dGeom &g, int32_t *y, const void *ws, hipStream_t s) {
+    return g.ncs > 1 ? launch_multiply_seg<RH, NRT, SG, RNTW, true>(g, y, ws, s)
+                     : launch_multiply_seg<RH, NRT, SG, RNTW, false>(g, y, ws, s);
 }
 
 }  // namespace

@@ -87,7 +87,9 @@ bool place_launch(const samd_conv2d_desc &d, Conv2dGeom &c) {
         const int reg_waves = std::min(kResidentWavesPerSimd, rh <= 2 ? 7 : (rh == 3 ? 5 : 4));
         for (int gr = grp_max; gr >= 1; --gr) {
             for (int wm : {1, 2, 4}) {
-                for (int ks : {1, 2, 4, 8, 16}) {
+                // at most 8 channel slices: 16-wave workgroups measured 1.0-1.8x slower than
+                // 8-wave ones on 512-channel layers (all 16 waves decode into one tile)
+                for (int ks : {1, 2, 4, 8}) {
                     if (wm * ks > kMaxBlockWaves) continue;
                     if (ks > 1 && (d.C + ks - 1) / ks < 1) continue;
                     Conv2dGeom t = c;
@@ -264,6 +266,7 @@ int search_lanes(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, int xoff, 
                 if (c.cw < I) continue;
                 c.ncs = (c.Wo + c.cw - 1) / c.cw;
             }
+            c.qseg = c.cw / I;
             c.nrt = d.KH * c.ntw;
             c.Hp = d.H + 2 * d.pad_h;
             c.macs_per_mad = (double)I * d.KW / (double)c.ntw;

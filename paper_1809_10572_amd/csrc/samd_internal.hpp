@@ -41,9 +41,6 @@ struct Conv2dGeom {
     int32_t xoff;                   // subtracted from every activation (recentred unsigned
                                     // activations: 2^(xbits-1)); 0 otherwise
     int32_t L, I, Kmax, nq, G;      // lane bits, values/word, widest phase, words/row, flush channels
-    int32_t nqs;                    // words of one column segment (<= 64: a lane group's words)
-    int32_t cw;                     // output columns per column segment (Wo when ncs == 1)
-    int32_t ncs;                    // column segments per output row
     int32_t nl;                     // decoded lanes per accumulator; lane nl-1 takes the remaining bits
     int32_t result_signed;          // any operand signed: lanes need the fix-up
     uint64_t msb_mask;              // sign bit of lanes 0 .. nl-2
@@ -74,6 +71,11 @@ struct Conv2dGeom {
     int64_t kw_words, spread_words; // workspace: kernel-word streams, operand words (after the
                                     // correction table when xoff != 0)
     double macs_per_mad, cost;
+    // column segments (rows of more than 64 operand words)
+    int32_t nqs;                    // words of one column segment (<= 64: a lane group's words)
+    int32_t cw;                     // output columns per column segment (Wo when ncs == 1)
+    int32_t ncs;                    // column segments per output row
+    int32_t qseg;                   // words between column segments: cw / I
 };
 
 // 1-D convolution geometry (unsigned operands, 32x32 -> 64-bit products).
