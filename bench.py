@@ -48,6 +48,8 @@ def parse():
     p.add_argument("--vggb", action="store_true",
                    help="instead of the default workload, sweep the ten VGG-B convolution layers (batch 1) over "
                         "N-bit signed activations and weights, N = 8..2 (or --bits), SAMD and int8 baseline")
+    p.add_argument("--lanewise", action="store_true",
+                   help="instead of the default workload, time lane-wise add/sub/mul/scale on packed words (GB/s)")
     p.add_argument("--trace-summary", metavar="TRACE_DIR",
                    help="print markdown tables of a rocprofv3 --kernel-trace --stats output folder (csv) and exit")
     p.add_argument("--traffic-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
@@ -271,11 +273,52 @@ def run_vggb(args):
     print(json.dumps(line), flush=True)
 
 
+def run_lanewise(args):
+    """Lane-wise SAMD arithmetic on packed words (add, subtract, multiply, vector scale):
+    HBM-bound elementwise kernels over 64 Mi words per operand.  Prints one JSON line of
+    achieved GB/s per (operation, bit width) against the 8 TB/s HBM peak."""
+    import torch
+
+    import paper_1809_10572_amd as samd
+
+    nwords = 64 << 20
+    dev = torch.device("cuda:0")
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(1809105720)
+    a = torch.randint(-(1 << 31), (1 << 31) - 1, (nwords,), dtype=torch.int32, device=dev, generator=gen)
+    b = torch.randint(-(1 << 31), (1 << 31) - 1, (nwords,), dtype=torch.int32, device=dev, generator=gen)
+    out = torch.empty_like(a)
+    rows = []
+    bits_list = [int(v) for v in args.bits.split(",")]
+    for bits in bits_list:
+        # clear the bits above each word's last lane (the packed format keeps them zero)
+        P = 32 // bits
+        valid = (1 << (P * bits)) - 1 if P * bits < 32 else -1
+        av, bv = a & valid if valid != -1 else a, b & valid if valid != -1 else b
+        for name, fn, nbytes in (("add", lambda: samd.lanewise(samd.LANE_ADD, av, bv, bits, False, out=out), 12),
+                                 ("sub", lambda: samd.lanewise(samd.LANE_SUB, av, bv, bits, False, out=out), 12),
+                                 ("mul", lambda: samd.lanewise(samd.LANE_MUL, av, bv, bits, False, out=out), 12),
+                                 ("scale", lambda: samd.scale(av, 5, bits, False, out=out), 8)):
+            t = timed_graph(fn, 5, args.kernel_warm_s)
+            gbs = nwords * nbytes / t / 1e9
+            rows.append({"op": name, "bits": bits, "us": round(t * 1e6, 1), "GB_s": round(gbs, 1),
+                         "hbm_frac": round(gbs * 1e9 / PEAK_HBM, 3),
+                         "G_lanes_s": round(nwords * P / t / 1e9, 1)})
+    print(json.dumps({"metric": "lane-wise SAMD arithmetic on packed words, GB/s", "unit": "GB/s",
+                      "value": round(sum(r["GB_s"] for r in rows) / len(rows), 1), "n_gpus": 1,
+                      "config": {"workload": f"{nwords} packed uint32 words per operand (inputs 2x256 MiB)",
+                                 "bits": bits_list},
+                      "per_op": rows}), flush=True)
+
+
 def main():
     args = parse()
     args.bits_given = "--bits" in sys.argv
     if args.vggb:
         run_vggb(args)
+        return
+    if args.lanewise:
+        run_lanewise(args)
         return
     if args.trace_summary:
         print(trace_summary(args.trace_summary))

@@ -228,6 +228,28 @@ int samd_relu_requant_nhwc_u8(const int32_t *acc, int32_t N, int32_t C, int32_t 
                               const int32_t *dev_max, samd_fmt out, uint8_t *dst,
                               hipStream_t stream);
 
+/* Lane-wise SAMD arithmetic on packed words (Sec. 3, conventional SAMD arithmetic: the
+ * add figure, the subtract passage and the lane-wise multiply figure).
+ *   op   SAMD_LANE_ADD, SAMD_LANE_SUB or SAMD_LANE_MUL
+ *   a, b nwords packed words each (device), in the format of samd_pack: any number of
+ *        rows, each starting on a word, the bits above a word's last lane zero
+ *   dst  nwords words (device; may alias a or b), same format
+ * Lane i of every result word is (a_i op b_i) mod 2^bits: for signed formats the
+ * two's-complement wrap-around of the exact result, for unsigned the value mod 2^bits.
+ * The whole word is computed at once with temporary spacer bits (each lane's top bit);
+ * the multiply takes bits shift-and-add steps.  Bits above the last lane stay zero when
+ * they are zero in a and b. */
+enum { SAMD_LANE_ADD = 0, SAMD_LANE_SUB = 1, SAMD_LANE_MUL = 2, SAMD_LANE_SCALE = 3 };
+int samd_lanewise(int op, const uint32_t *a, const uint32_t *b, int64_t nwords, samd_fmt f, uint32_t *dst,
+                  hipStream_t stream);
+
+/* Vector scale (Sec. 4, scale-wrap figure): every lane of a times one scalar, modulo
+ * 2^bits.  The scalar is taken as its low bits bits (a negative scalar of a signed
+ * format is its two's-complement pattern); the low bits of a product do not depend on
+ * signedness, so the result lanes are (a_i * scalar) mod 2^bits for either format.
+ * Arguments as samd_lanewise. */
+int samd_scale(const uint32_t *a, int64_t nwords, samd_fmt f, int32_t scalar, uint32_t *dst, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

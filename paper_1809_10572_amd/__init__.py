@@ -105,6 +105,8 @@ def lib():
             "samd_max_i32": (ctypes.c_int, [_p, _i64, _p, _p]),
             "samd_relu_requant_pack": (ctypes.c_int, [_p, _i64, _i64, _p, Fmt, _p, _p, _p]),
             "samd_relu_requant_nhwc_u8": (ctypes.c_int, [_p, _i32, _i32, _i32, _i32, _p, Fmt, _p, _p]),
+            "samd_lanewise": (ctypes.c_int, [ctypes.c_int, _p, _p, _i64, Fmt, _p, _p]),
+            "samd_scale": (ctypes.c_int, [_p, _i64, Fmt, _i32, _p, _p]),
         }
         for name, (res, args) in sigs.items():
             fn = getattr(L, name)
@@ -354,4 +356,29 @@ def relu_requant_nhwc_u8(acc: torch.Tensor, dev_max: torch.Tensor, bits: int,
         out = torch.empty((N, H, W, C), dtype=torch.uint8, device=acc.device)
     _check(lib().samd_relu_requant_nhwc_u8(acc.data_ptr(), N, C, H, W, dev_max.data_ptr(), Fmt(bits, False),
                                            out.data_ptr(), _stream(acc)))
+    return out
+
+
+LANE_ADD, LANE_SUB, LANE_MUL = 0, 1, 2
+
+
+def lanewise(op: int, a: torch.Tensor, b: torch.Tensor, bits: int, signed: bool,
+             out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Lane-wise add, subtract or multiply (LANE_ADD / LANE_SUB / LANE_MUL) of two packed
+    int32 word tensors of the same shape; lanes wrap modulo 2**bits."""
+    a = _dev(a, torch.int32, "a")
+    b = _dev(b, torch.int32, "b")
+    if a.shape != b.shape:
+        raise ValueError("a and b must have the same shape")
+    out = _out(out, a.numel()) if out is not None else torch.empty_like(a)
+    _check(lib().samd_lanewise(op, a.data_ptr(), b.data_ptr(), a.numel(), Fmt(bits, signed), out.data_ptr(),
+                               _stream(a)))
+    return out
+
+
+def scale(a: torch.Tensor, scalar: int, bits: int, signed: bool, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Every lane of the packed words a times one scalar, modulo 2**bits."""
+    a = _dev(a, torch.int32, "a")
+    out = _out(out, a.numel()) if out is not None else torch.empty_like(a)
+    _check(lib().samd_scale(a.data_ptr(), a.numel(), Fmt(bits, signed), int(scalar), out.data_ptr(), _stream(a)))
     return out

@@ -399,6 +399,33 @@ int samd_max_i32(const int32_t *src, int64_t n, int32_t *dev_max, hipStream_t st
     return launch_max_i32(src, n, dev_max, stream);
 }
 
+int samd_lanewise(int op, const uint32_t *a, const uint32_t *b, int64_t nwords, samd_fmt f, uint32_t *dst,
+                  hipStream_t stream) {
+    set_error("");
+    int st = check_fmt(f, "f");
+    if (st) return st;
+    if (op != SAMD_LANE_ADD && op != SAMD_LANE_SUB && op != SAMD_LANE_MUL)
+        return fail(SAMD_EINVAL, "op %d is not SAMD_LANE_ADD, SAMD_LANE_SUB or SAMD_LANE_MUL", op);
+    if (nwords < 0) return fail(SAMD_EINVAL, "nwords must be >= 0");
+    if (nwords == 0) return SAMD_OK;
+    if (!a || !b || !dst) return fail(SAMD_EINVAL, "a, b and dst must not be NULL");
+    if (((uintptr_t)a & 15) || ((uintptr_t)b & 15) || ((uintptr_t)dst & 15))
+        return fail(SAMD_EALIGN, "a, b and dst must be 16-byte aligned");
+    return launch_lanewise(op, a, b, nwords, f.bits, 0, dst, stream);
+}
+
+int samd_scale(const uint32_t *a, int64_t nwords, samd_fmt f, int32_t scalar, uint32_t *dst, hipStream_t stream) {
+    set_error("");
+    int st = check_fmt(f, "f");
+    if (st) return st;
+    if (nwords < 0) return fail(SAMD_EINVAL, "nwords must be >= 0");
+    if (nwords == 0) return SAMD_OK;
+    if (!a || !dst) return fail(SAMD_EINVAL, "a and dst must not be NULL");
+    if (((uintptr_t)a & 15) || ((uintptr_t)dst & 15)) return fail(SAMD_EALIGN, "a and dst must be 16-byte aligned");
+    const uint32_t s = (uint32_t)scalar & ((1u << f.bits) - 1);   // the scalar's b-bit pattern
+    return launch_lanewise(SAMD_LANE_SCALE, a, a, nwords, f.bits, s, dst, stream);
+}
+
 int samd_relu_requant_pack(const int32_t *acc, int64_t rows, int64_t len, const int32_t *dev_max, samd_fmt out,
                            uint32_t *dst, int32_t *dev_shift, hipStream_t stream) {
     set_error("");

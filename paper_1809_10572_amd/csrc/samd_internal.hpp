@@ -115,6 +115,8 @@ int launch_conv2d_i8_prepare(const int8_t *w, samd_fmt xf, const samd_conv2d_des
 int launch_conv2d_i8(const void *x, samd_fmt xf, const samd_conv2d_desc &d, int32_t *y, const void *ws,
                      hipStream_t s);
 int launch_max_i32(const int32_t *src, int64_t n, int32_t *dev_max, hipStream_t s);
+int launch_lanewise(int op, const uint32_t *a, const uint32_t *b, int64_t nwords, int bits, uint32_t scalar,
+                    uint32_t *dst, hipStream_t s);
 int launch_relu_requant_pack(const int32_t *acc, int64_t rows, int64_t len, const int32_t *dev_max, int bits,
                              uint32_t *dst, int32_t *dev_shift, hipStream_t s);
 int launch_relu_requant_nhwc_u8(const int32_t *acc, int N, int C, int H, int W, const int32_t *dev_max,

@@ -146,3 +146,19 @@ def test_calls_fail_loudly_without_a_gpu_tensor():
     import torch
     with pytest.raises(ValueError):
         samd.pack(torch.zeros(4, dtype=torch.uint8), 4, False)
+
+
+def test_lanewise_and_scale_validation():
+    L = samd.lib()
+    A16, A4 = 0x10000, 0x10004
+    assert L.samd_lanewise(0, A16, A16, 8, Fmt(9, 0), A16, None) == EINVAL      # format
+    assert L.samd_lanewise(3, A16, A16, 8, Fmt(4, 0), A16, None) == EINVAL      # scale is samd_scale
+    assert L.samd_lanewise(-1, A16, A16, 8, Fmt(4, 0), A16, None) == EINVAL
+    assert L.samd_lanewise(0, A16, A16, -1, Fmt(4, 0), A16, None) == EINVAL
+    assert L.samd_lanewise(0, None, A16, 8, Fmt(4, 0), A16, None) == EINVAL
+    assert L.samd_lanewise(0, A16, A4, 8, Fmt(4, 0), A16, None) == EALIGN
+    assert L.samd_lanewise(1, None, None, 0, Fmt(4, 1), None, None) == OK       # empty: nothing to do
+    assert L.samd_scale(A16, 8, Fmt(0, 0), 3, A16, None) == EINVAL
+    assert L.samd_scale(A16, -2, Fmt(4, 0), 3, A16, None) == EINVAL
+    assert L.samd_scale(A16, 8, Fmt(4, 0), 3, A4, None) == EALIGN
+    assert L.samd_scale(None, 0, Fmt(4, 0), 3, None, None) == OK

@@ -102,6 +102,58 @@ def test_conv1d_ragged_and_degenerate(bits):
     np.testing.assert_array_equal(y.cpu().numpy(), ref.conv1d(x, k))
 
 
+# --- lane-wise SAMD arithmetic on packed words ---------------------------------------
+
+def wrap(v: np.ndarray, bits: int, signed: bool) -> np.ndarray:
+    """v modulo 2**bits, read as a b-bit two's-complement (signed) or unsigned value."""
+    m = np.asarray(v, np.int64) & ((1 << bits) - 1)
+    return np.where(m >= (1 << (bits - 1)), m - (1 << bits), m) if signed else m
+
+
+LANE_CASES = [(3, 61), (5, 256), (2, 7)]   # (rows, values per row): ragged rows, odd word counts
+
+
+@pytest.mark.parametrize("bits", range(1, 9))
+@pytest.mark.parametrize("signed", [False, True])
+def test_lanewise_ops_match_elementwise(bits, signed):
+    rng = np.random.default_rng(300 + 2 * bits + signed)
+    for rows, n in LANE_CASES:
+        for gen in (wl.uniform, wl.half_extremes):
+            x = gen(rng, (rows, n), bits, signed)
+            y = gen(rng, (rows, n), bits, signed)
+            xw, _ = ref.pack(x, bits, signed)
+            yw, _ = ref.pack(y, bits, signed)
+            xg, yg = gpu_words(xw), gpu_words(yw)
+            for op, fn in ((samd.LANE_ADD, np.add), (samd.LANE_SUB, np.subtract), (samd.LANE_MUL, np.multiply)):
+                got = samd.lanewise(op, xg, yg, bits, signed)
+                torch.cuda.synchronize()
+                want, _ = ref.pack(wrap(fn(x.astype(np.int64), y), bits, signed), bits, signed)
+                np.testing.assert_array_equal(host_words(got), want, err_msg=f"op {op} rows {rows} len {n}")
+                np.testing.assert_array_equal(ref.unpack(host_words(got), n, bits, signed),
+                                              wrap(fn(x.astype(np.int64), y), bits, signed))
+            # in place: dst is a
+            samd.lanewise(samd.LANE_ADD, xg, yg, bits, signed, out=xg)
+            torch.cuda.synchronize()
+            np.testing.assert_array_equal(ref.unpack(host_words(xg), n, bits, signed), wrap(x + y, bits, signed))
+
+
+@pytest.mark.parametrize("bits", range(1, 9))
+@pytest.mark.parametrize("signed", [False, True])
+def test_vector_scale_matches_elementwise(bits, signed):
+    rng = np.random.default_rng(400 + 2 * bits + signed)
+    lo, hi = wl.value_range(bits, signed)
+    for rows, n in LANE_CASES:
+        x = wl.half_extremes(rng, (rows, n), bits, signed)
+        xw, _ = ref.pack(x, bits, signed)
+        xg = gpu_words(xw)
+        for s in sorted({lo, hi, 0, 1, -1, lo + 1, int(rng.integers(lo, hi + 1))}):
+            got = samd.scale(xg, s, bits, signed)
+            torch.cuda.synchronize()
+            want = wrap(x.astype(np.int64) * s, bits, signed)
+            np.testing.assert_array_equal(ref.unpack(host_words(got), n, bits, signed), want, err_msg=f"scalar {s}")
+            np.testing.assert_array_equal(host_words(got), ref.pack(want, bits, signed)[0])
+
+
 # --- 2-D convolution: workloads 1, 3, 4 at full size -----------------------------------
 
 def conv2d_full(cfg, bits):
