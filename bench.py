@@ -48,6 +48,9 @@ def parse():
     p.add_argument("--vggb", action="store_true",
                    help="instead of the default workload, sweep the ten VGG-B convolution layers (batch 1) over "
                         "N-bit signed activations and weights, N = 8..2 (or --bits), SAMD and int8 baseline")
+    p.add_argument("--stack", action="store_true",
+                   help="instead of the default workload, time the AlexNet-shaped five-layer stack (b = 2, 4, 8 or "
+                        "--bits): SAMD with packed or operand-word activations between layers, and int8")
     p.add_argument("--lanewise", action="store_true",
                    help="instead of the default workload, time lane-wise add/sub/mul/scale on packed words (GB/s)")
     p.add_argument("--trace-summary", metavar="TRACE_DIR",
@@ -273,6 +276,81 @@ def run_vggb(args):
     print(json.dumps(line), flush=True)
 
 
+def run_stack(args):
+    """The AlexNet-shaped stack (five conv layers, ReLU + requantisation between them,
+    batch 16): one forward pass per step, kernel words prepared once.  Three chains:
+    SAMD with packed activations between layers (max, relu_requant_pack, pack-format
+    stage), SAMD with the epilogue writing the next layer's operand words directly
+    (max, relu_requant_stage), and the int8 baseline (max, NHWC uint8 requantisation).
+    Prints one JSON line."""
+    import numpy as np
+    import torch
+
+    import paper_1809_10572_amd as samd
+    import samd_workloads as wl
+
+    dev = torch.device("cuda:0")
+    bits_list = [int(b) for b in args.bits.split(",")] if args.bits_given else wl.BITS_SWEEP[5]
+    rows = []
+    for bits in bits_list:
+        case = wl.stack_case(bits)
+        xf, wf = samd.Fmt(bits, False), samd.Fmt(bits, True)
+        lys = case.layers
+        macs = 0
+        for l in lys:
+            Ho, Wo = samd.out_hw(l)
+            macs += l.N * l.M * Ho * Wo * l.C * l.KH * l.KW
+        wss = [samd.conv2d_prepare(samd.pack(torch.from_numpy(w.astype(np.int8)).to(dev), bits, True), wf, l, xf)
+               for w, l in zip(case.ws, lys)]
+        ws8 = [samd.conv2d_int8_prepare(torch.from_numpy(w.astype(np.int8)).to(dev), wf, l, xf)
+               for w, l in zip(case.ws, lys)]
+        x8 = torch.from_numpy(case.x.astype(np.uint8)).to(dev)
+        xn = torch.from_numpy(np.ascontiguousarray(np.transpose(case.x, (0, 2, 3, 1))).astype(np.uint8)).to(dev)
+        ys = [torch.empty((l.N, l.M) + samd.out_hw(l), dtype=torch.int32, device=dev) for l in lys]
+        mx = torch.empty(1, dtype=torch.int32, device=dev)
+        xps = [torch.empty((l.N, l.C, l.H, samd.row_words(l.W, bits)), dtype=torch.int32, device=dev) for l in lys]
+        x8s = [xn] + [torch.empty((l.N, l.H, l.W, l.C), dtype=torch.uint8, device=dev) for l in lys[1:]]
+
+        def chain_packed():
+            samd.pack(x8, bits, False, out=xps[0])
+            for li, l in enumerate(lys):
+                samd.conv2d_prepared(xps[li], xf, wf, l, wss[li], out=ys[li])
+                if li + 1 < len(lys):
+                    samd.max_i32(ys[li], out=mx)
+                    samd.relu_requant_pack(ys[li], mx, bits, out=xps[li + 1])
+
+        def chain_fused():
+            samd.pack(x8, bits, False, out=xps[0])
+            samd.conv2d_stage(xps[0], xf, wf, lys[0], wss[0])
+            for li, l in enumerate(lys):
+                samd.conv2d_accumulate(xf, wf, l, wss[li], out=ys[li])
+                if li + 1 < len(lys):
+                    samd.max_i32(ys[li], out=mx)
+                    samd.relu_requant_stage(ys[li], mx, bits, wf, lys[li + 1], wss[li + 1])
+
+        def chain_int8():
+            for li, l in enumerate(lys):
+                samd.conv2d_int8_prepared(x8s[li], xf, wf, l, ws8[li], out=ys[li])
+                if li + 1 < len(lys):
+                    samd.max_i32(ys[li], out=mx)
+                    samd.relu_requant_nhwc_u8(ys[li], mx, bits, out=x8s[li + 1])
+
+        t = {name: timed_graph(fn, 3, args.kernel_warm_s) for name, fn in
+             (("samd_packed", chain_packed), ("samd_fused", chain_fused), ("int8", chain_int8))}
+        rows.append({"bits": bits, **{f"{k}_ms": round(v * 1e3, 3) for k, v in t.items()},
+                     **{f"{k}_gmacs": round(macs / v / 1e9, 1) for k, v in t.items()},
+                     "fused_saving": round(1 - t["samd_fused"] / t["samd_packed"], 3)})
+        print(f"stack: b={bits} " + " ".join(f"{k} {v * 1e3:.3f} ms" for k, v in t.items()), file=sys.stderr,
+              flush=True)
+    print(json.dumps({"metric": "AlexNet-shaped conv stack forward, GMAC/s", "unit": "GMAC/s",
+                      "value": round(sum(r["samd_fused_gmacs"] for r in rows) / len(rows), 1), "n_gpus": 1,
+                      "data": "synthetic",
+                      "config": {"workload": "five conv layers (11x11/4 96, 5x5 256, 3x3 384, 3x3 384, 3x3 256) on "
+                                             "16x3x224x224, no pooling, ReLU + requantisation between layers",
+                                 "bits": bits_list, "macs": macs},
+                      "per_bits": rows}), flush=True)
+
+
 def run_lanewise(args):
     """Lane-wise SAMD arithmetic on packed words (add, subtract, multiply, vector scale):
     HBM-bound elementwise kernels over 64 Mi words per operand.  Prints one JSON line of
@@ -319,6 +397,9 @@ def main():
         return
     if args.lanewise:
         run_lanewise(args)
+        return
+    if args.stack:
+        run_stack(args)
         return
     if args.trace_summary:
         print(trace_summary(args.trace_summary))

@@ -228,6 +228,23 @@ int samd_relu_requant_nhwc_u8(const int32_t *acc, int32_t N, int32_t C, int32_t 
                               const int32_t *dev_max, samd_fmt out, uint8_t *dst,
                               hipStream_t stream);
 
+/* ReLU and requantisation, as samd_relu_requant_pack, written straight into the next
+ * layer's operand words instead of packed rows: the result equals samd_relu_requant_pack
+ * followed by samd_conv2d_stage of the next layer, without the dense packed activations
+ * in between.  Between layers the activations stay in the lanes-with-spacers layout the
+ * multiply reads (the permanent-spacer storage of Sec. 2.2 and Sec. 7: more bytes, no
+ * repacking).  Afterwards samd_conv2d_accumulate computes the next layer.
+ *   acc       int32 accumulators, NCHW with the next layer's d->N, C, H, W (device)
+ *   dev_max   device int32 maximum of acc (samd_max_i32)
+ *   xf        the next layer's activation format: unsigned, bits = requantisation bits
+ *   wf, d     the next layer's weight format and descriptor
+ *   ws        the next layer's workspace (samd_conv2d_workspace bytes, 256-byte aligned;
+ *             its kernel words prepared before samd_conv2d_accumulate)
+ *   dev_shift nullable device int32: receives the shift used */
+int samd_relu_requant_stage(const int32_t *acc, const int32_t *dev_max, samd_fmt xf, samd_fmt wf,
+                            const samd_conv2d_desc *d, void *ws, size_t ws_bytes, int32_t *dev_shift,
+                            hipStream_t stream);
+
 /* Lane-wise SAMD arithmetic on packed words (Sec. 3, conventional SAMD arithmetic: the
  * add figure, the subtract passage and the lane-wise multiply figure).
  *   op   SAMD_LANE_ADD, SAMD_LANE_SUB or SAMD_LANE_MUL

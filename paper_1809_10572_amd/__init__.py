@@ -105,6 +105,8 @@ def lib():
             "samd_max_i32": (ctypes.c_int, [_p, _i64, _p, _p]),
             "samd_relu_requant_pack": (ctypes.c_int, [_p, _i64, _i64, _p, Fmt, _p, _p, _p]),
             "samd_relu_requant_nhwc_u8": (ctypes.c_int, [_p, _i32, _i32, _i32, _i32, _p, Fmt, _p, _p]),
+            "samd_relu_requant_stage": (ctypes.c_int, [_p, _p, Fmt, Fmt, ctypes.POINTER(Conv2dDesc), _p, _sz, _p,
+                                                       _p]),
             "samd_lanewise": (ctypes.c_int, [ctypes.c_int, _p, _p, _i64, Fmt, _p, _p]),
             "samd_scale": (ctypes.c_int, [_p, _i64, Fmt, _i32, _p, _p]),
         }
@@ -382,3 +384,16 @@ def scale(a: torch.Tensor, scalar: int, bits: int, signed: bool, out: Optional[t
     out = _out(out, a.numel()) if out is not None else torch.empty_like(a)
     _check(lib().samd_scale(a.data_ptr(), a.numel(), Fmt(bits, signed), int(scalar), out.data_ptr(), _stream(a)))
     return out
+
+
+def relu_requant_stage(acc: torch.Tensor, dev_max: torch.Tensor, bits: int, wfmt: Fmt, shape, ws: torch.Tensor,
+                       dev_shift: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """ReLU + requantisation of acc to unsigned `bits`, written as the operand words of the
+    next layer (descriptor `shape`, weight format `wfmt`) into its workspace `ws`; follow
+    with conv2d_accumulate.  Returns ws."""
+    acc = _dev(acc, torch.int32, "acc")
+    d = Conv2dDesc.of(shape)
+    _check(lib().samd_relu_requant_stage(acc.data_ptr(), dev_max.data_ptr(), Fmt(bits, False), wfmt,
+                                         ctypes.byref(d), ws.data_ptr(), ws.numel(),
+                                         dev_shift.data_ptr() if dev_shift is not None else None, _stream(acc)))
+    return ws

@@ -286,6 +286,20 @@ int samd_conv2d_stage(const uint32_t *x, samd_fmt xf, samd_fmt wf, const samd_co
     return launch_conv2d_spread(x, g, ws, stream);
 }
 
+int samd_relu_requant_stage(const int32_t *acc, const int32_t *dev_max, samd_fmt xf, samd_fmt wf,
+                            const samd_conv2d_desc *d, void *ws, size_t ws_bytes, int32_t *dev_shift,
+                            hipStream_t stream) {
+    set_error("");
+    if (xf.is_signed) return fail(SAMD_EINVAL, "requantised activations are unsigned");
+    Conv2dGeom g;
+    int st = conv2d_setup(xf, wf, d, ws, ws_bytes, g);
+    if (st) return st;
+    if (!acc || !dev_max) return fail(SAMD_EINVAL, "acc and dev_max must not be NULL");
+    if (!aligned4(acc) || !aligned4(dev_max) || (dev_shift && !aligned4(dev_shift)))
+        return fail(SAMD_EALIGN, "acc / dev_max / dev_shift not aligned");
+    return launch_relu_requant_stage(acc, dev_max, g, ws, dev_shift, stream);
+}
+
 int samd_conv2d_accumulate(samd_fmt xf, samd_fmt wf, const samd_conv2d_desc *d, int32_t *y, const void *ws,
                            size_t ws_bytes, hipStream_t stream) {
     set_error("");

@@ -1,6 +1,7 @@
 // Between-layer epilogue of the AlexNet-shaped stack: the layer maximum, then ReLU and
-// requantisation to unsigned b bits, written either in the packed storage format (the
-// SAMD chain) or as NHWC uint8 (the 8-bit baseline chain).  The paper fixes no rule;
+// requantisation to unsigned b bits, written in the packed storage format, straight into
+// the next layer's operand words (the SAMD chain), or as NHWC uint8 (the 8-bit baseline
+// chain).  The paper fixes no rule;
 // the library's rule: mx = max(max(acc), 0), s = the smallest s >= 0 with
 // mx >> s <= 2^b - 1, q = min((max(v, 0) + (s ? 2^(s-1) : 0)) >> s, 2^b - 1).
 #include <hip/hip_runtime.h>
@@ -65,6 +66,45 @@ __global__ __launch_bounds__(kBlock) void relu_requant_pack_kernel(const int32_t
     }
 }
 
+// ReLU + requantisation written straight into the next layer's operand words: the
+// activations never take the dense packed form between layers, they go from the int32
+// accumulators into lanes with spacer bits (the layout the next layer multiplies).
+// Word q of kernel-word variant t of padded row hp of channel c of image n holds, lane
+// ii, the requantised activation of column sw (q I + delta_t + ii) + phase_t - pw of row
+// hp - ph, minus the next layer's recentring offset; columns and rows outside the image
+// are 0.  The same words the next layer's operand spread builds from packed rows.
+// A block of 256 threads covers 256 / QP padded rows, as that spread does.
+__global__ __launch_bounds__(kBlock) void relu_requant_stage_kernel(const int32_t *__restrict__ acc,
+                                                                    const int32_t *__restrict__ dev_max,
+                                                                    const Conv2dGeom g, int qshift,
+                                                                    int32_t *__restrict__ xs,
+                                                                    int32_t *__restrict__ dev_shift) {
+    const int shift = requant_shift(*dev_max, g.xbits);
+    if (dev_shift && blockIdx.x == 0 && threadIdx.x == 0) *dev_shift = shift;
+    const int64_t row = (int64_t)blockIdx.x * (kBlock >> qshift) + (threadIdx.x >> qshift);   // (n*C + c)*Hp + hp
+    if (row >= (int64_t)g.N * g.C * g.Hp) return;
+    const int hp = (int)(row % g.Hp);
+    const int64_t nc = row / g.Hp;
+    const int h = hp - g.ph;
+    const bool inside = h >= 0 && h < g.H;
+    const int32_t *src = acc + (nc * g.H + (inside ? h : 0)) * g.W;
+    for (int q = threadIdx.x & ((1 << qshift) - 1); q < g.nq; q += 1 << qshift) {
+        int32_t *dst = xs + row * g.ntw * g.nq + q;
+        for (int t = 0; t < g.ntw; ++t) {
+            const int delta = g.tw_tap0[t] + g.tw_ntaps[t] - g.Kmax;
+            const int col0 = g.sw * (q * g.I + delta) + g.tw_phase[t] - g.pw;
+            uint32_t word = 0;
+            if (inside)
+                for (int ii = 0; ii < g.I; ++ii) {
+                    const int col = col0 + g.sw * ii;
+                    if (col >= 0 && col < g.W)
+                        word += (uint32_t)((int32_t)requant(src[col], shift, g.xbits) - g.xoff) << (ii * g.L);
+                }
+            dst[t * g.nq] = (int32_t)word;
+        }
+    }
+}
+
 // One thread per NHWC output byte; reads the NCHW accumulator.
 __global__ __launch_bounds__(kBlock) void relu_requant_nhwc_kernel(const int32_t *__restrict__ acc, int N, int C,
                                                                    int H, int W, const int32_t *__restrict__ dev_max,
@@ -108,6 +148,18 @@ int launch_relu_requant_pack(const int32_t *acc, int64_t rows, int64_t len, cons
 #undef SAMD_REQ_CASE
     set_error("relu_requant_pack: unsupported bits");
     return SAMD_EINVAL;
+}
+
+int launch_relu_requant_stage(const int32_t *acc, const int32_t *dev_max, const Conv2dGeom &g, void *ws,
+                              int32_t *dev_shift, hipStream_t s) {
+    int32_t *xs = (int32_t *)((char *)ws + conv2d_xs_offset(g));
+    int qshift = 0;
+    while ((1 << qshift) < g.nq && qshift < 8) ++qshift;   // up to 256 threads per row
+    const int64_t nrows = (int64_t)g.N * g.C * g.Hp;
+    const int rpb = kBlock >> qshift;
+    hipLaunchKernelGGL(relu_requant_stage_kernel, dim3((unsigned)((nrows + rpb - 1) / rpb)), dim3(kBlock), 0, s, acc,
+                       dev_max, g, qshift, xs, dev_shift);
+    return check_launch("relu_requant_stage");
 }
 
 int launch_relu_requant_nhwc_u8(const int32_t *acc, int N, int C, int H, int W, const int32_t *dev_max, int bits,

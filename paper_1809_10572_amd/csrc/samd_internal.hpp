@@ -119,6 +119,8 @@ int launch_lanewise(int op, const uint32_t *a, const uint32_t *b, int64_t nwords
                     uint32_t *dst, hipStream_t s);
 int launch_relu_requant_pack(const int32_t *acc, int64_t rows, int64_t len, const int32_t *dev_max, int bits,
                              uint32_t *dst, int32_t *dev_shift, hipStream_t s);
+int launch_relu_requant_stage(const int32_t *acc, const int32_t *dev_max, const Conv2dGeom &g, void *ws,
+                              int32_t *dev_shift, hipStream_t s);
 int launch_relu_requant_nhwc_u8(const int32_t *acc, int N, int C, int H, int W, const int32_t *dev_max,
                                 int bits, uint8_t *dst, hipStream_t s);
 

@@ -317,6 +317,38 @@ def test_alexnet_stack_batch2(bits):
         np.testing.assert_array_equal(g, w, err_msg=f"int8 layer {li + 1}")
 
 
+def run_stack_samd_fused(case):
+    """The SAMD chain with the epilogue writing the next layer's operand words directly
+    (relu_requant_stage), no packed activations between layers."""
+    bits = case.bits
+    xf, wf = samd.Fmt(bits, False), samd.Fmt(bits, True)
+    wss = [samd.conv2d_prepare(samd.pack(gpu_vals(w, True), bits, True), wf, shp, xf)
+           for w, shp in zip(case.ws, case.layers)]
+    samd.conv2d_stage(samd.pack(gpu_vals(case.x, False), bits, False), xf, wf, case.layers[0], wss[0])
+    accs, shifts = [], []
+    for li, shp in enumerate(case.layers):
+        y = samd.conv2d_accumulate(xf, wf, shp, wss[li])
+        accs.append(y)
+        if li + 1 < len(case.layers):
+            sh = torch.zeros(1, dtype=torch.int32, device=DEV)
+            samd.relu_requant_stage(y, samd.max_i32(y), bits, wf, case.layers[li + 1], wss[li + 1], dev_shift=sh)
+            shifts.append(sh)
+    torch.cuda.synchronize()
+    return [a.cpu().numpy() for a in accs], [int(s.item()) for s in shifts]
+
+
+@pytest.mark.parametrize("bits", [1, 2, 3, 4, 5, 8])
+def test_alexnet_stack_fused_epilogue(bits):
+    """ReLU + requantisation straight into the next layer's operand words gives every
+    layer's accumulators and shifts of the oracle (batch 2)."""
+    case = wl.stack_case(bits, batch=2)
+    want_accs, _, want_shifts = ref.stack(case.x, case.ws, [l.as_tuple() for l in case.layers], bits)
+    got_accs, got_shifts = run_stack_samd_fused(case)
+    assert got_shifts == list(want_shifts)
+    for li, (g, w) in enumerate(zip(got_accs, want_accs)):
+        np.testing.assert_array_equal(g, w, err_msg=f"SAMD layer {li + 1}")
+
+
 @pytest.mark.parametrize("bits", [2, 4, 8])
 def test_alexnet_stack_full_batch(bits):
     case = wl.stack_case(bits)
