@@ -101,16 +101,17 @@ template <int B, bool S>
 __global__ __launch_bounds__(256) void spread_kernel(const uint32_t *__restrict__ x, const Conv2dGeom g, int qshift,
                                                      int32_t *__restrict__ xs) {
     constexpr int P = 32 / B;
-    const int64_t row = (int64_t)blockIdx.x * (256 >> qshift) + (threadIdx.x >> qshift);   // (n*C + c)*Hp + hp
-    if (row >= (int64_t)g.N * g.C * g.Hp) return;
-    const int hp = (int)(row % g.Hp);
-    const int64_t nc = row / g.Hp;
+    // 32-bit row indices: the planner keeps N * C * Hp below 2^31
+    const uint32_t row = blockIdx.x * (256u >> qshift) + (threadIdx.x >> qshift);   // (n*C + c)*Hp + hp
+    if (row >= (uint32_t)(g.N * g.C * g.Hp)) return;
+    const uint32_t nc = row / (uint32_t)g.Hp;
+    const int hp = (int)(row - nc * (uint32_t)g.Hp);
     const int h = hp - g.ph;
     const bool inside = h >= 0 && h < g.H;
-    const uint32_t *src = x + (nc * g.H + (inside ? h : 0)) * g.xrw;
+    const uint32_t *src = x + ((int64_t)nc * g.H + (inside ? h : 0)) * g.xrw;
     // words q, q + 2^qshift, ... of the row (one pass unless the row has more than 256)
     for (int q = threadIdx.x & ((1 << qshift) - 1); q < g.nq; q += 1 << qshift) {
-        int32_t *dst = xs + row * g.ntw * g.nq + q;
+        int32_t *dst = xs + (int64_t)row * g.ntw * g.nq + q;
         for (int t = 0; t < g.ntw; ++t) {
             const int delta = g.tw_tap0[t] + g.tw_ntaps[t] - g.Kmax;
             const int col0 = g.sw * (q * g.I + delta) + g.tw_phase[t] - g.pw;
