@@ -42,6 +42,9 @@ def parse():
     p.add_argument("--cpu-seconds", type=float, default=10.0, help="CPU oracle sample budget")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-check", action="store_true", help="skip the sampled parity check")
+    p.add_argument("--no-tune", action="store_true",
+                   help="use the planner's model plans (default: time the top candidates at set-up)")
+    p.add_argument("--tune-candidates", type=int, default=16, help="candidate plans timed per bit width")
     p.add_argument("--counters", action="store_true",
                    help="launch each kernel once per bit width, eagerly, then a 1 GiB streaming copy, and exit "
                         "(the program rocprofv3 --pmc passes run)")
@@ -442,6 +445,17 @@ def main():
                            y8=torch.empty((N, M, Ho, Wo), dtype=torch.int32, device=dev)))
     torch.cuda.synchronize()
 
+    # set-up: each bit width's plan chosen by timing the planner's top candidates on the
+    # layer's own inputs (outside every timed region); the workspace is then sized again
+    if not args.no_tune:
+        for L in layers:
+            samd.pack(L["x"], L["b"], False, out=L["xp"])
+            samd.conv2d_tune(L["xp"], L["xf"], L["wp"], L["wf"], shape, candidates=args.tune_candidates, reps=10)
+            L["ws"] = torch.empty(max(samd.conv2d_workspace(shape, L["xf"], L["wf"]), 256), dtype=torch.uint8,
+                                  device=dev)
+            L["plan"] = samd.conv2d_plan(shape, L["xf"], L["wf"])
+        torch.cuda.synchronize()
+
     # the layer's kernel words are prepared once per layer (weights are constant)
     for L in layers:
         samd.conv2d_prepare(L["wp"], L["wf"], shape, L["xf"], ws=L["ws"])
@@ -545,6 +559,7 @@ def main():
             "lane_bits": p.lane_bits, "lanes": p.lanes, "tap_words": p.tap_words,
             "flush_channels": p.flush_channels, "macs_per_mad": round(p.macs_per_mad, 2),
             "tile": f"{p.rows_per_block}x{p.mblock}", "split_waves": p.split_waves,
+            "rows_per_thread": p.rows_per_thread, "shared_rows": bool(p.shared_rows),
             "chunk_channels": p.chunk_channels,
             "parity": parity.get(b),
         }
@@ -576,6 +591,7 @@ def main():
         "dtype": "int64", "data": "synthetic",
         "config": {"workload": "conv2d 8x128x56x56 -> 128, 3x3, stride 1, pad 1; unsigned b-bit activations x "
                                "signed b-bit weights; one step = pack + stage + accumulate at each b (kernel words prepared once per layer)",
+                   "plans": "model" if args.no_tune else f"tuned at set-up ({args.tune_candidates} candidates timed)",
                    "bits": bits_list, "global_batch": N, "macs_per_layer": macs},
         "roofline": {"bound": "alu", "achieved": round(achieved / 1e12, 3), "peak": round(PEAK_VALU_OPS / 1e12, 2),
                      "unit": "TOP/s", "frac": round(achieved / PEAK_VALU_OPS, 4),

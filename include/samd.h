@@ -11,7 +11,8 @@
  * Conventions for every entry point:
  *  - Pointers are DEVICE pointers unless a parameter says "host".  The caller owns
  *    every buffer; the library allocates nothing and keeps no state between calls
- *    apart from a thread-local error message.
+ *    apart from a thread-local error message and the plans chosen by
+ *    samd_conv2d_tune (process-wide, until samd_conv2d_untune).
  *  - Work is enqueued asynchronously on `stream` (0 = the default stream).  A return
  *    of SAMD_OK means the launch was accepted; results are ready once the stream is
  *    synchronised.
@@ -84,7 +85,11 @@ enum {
  *                into col_segments ranges of segment_columns output columns (a multiple
  *                of I), each computed from the at most 64 words it needs (words reaching
  *                two ranges are computed for both); 1 and Wo otherwise
- *   macs_per_mad multiply-accumulates delivered per 32x32->64 multiply (I * taps) */
+ *   macs_per_mad multiply-accumulates delivered per 32x32->64 multiply (I * taps)
+ *   rows_per_thread, shared_rows: output rows each lane computes, and whether they share
+ *                operand loads (3-row, stride-1 kernels: RH + 2 loads per channel and
+ *                kernel word instead of 3 RH)
+ *   model_cost   the planner's cost estimate (issue cycles of one compute unit) */
 typedef struct {
     int32_t lane_bits, lanes, taps_max, words_per_row, flush_channels, out_lanes, tap_words;
     int32_t phase[16], tap0[16], ntaps[16];
@@ -92,6 +97,8 @@ typedef struct {
     int32_t x_offset;
     int32_t col_segments, segment_columns;
     double macs_per_mad;
+    int32_t rows_per_thread, shared_rows;
+    double model_cost;
 } samd_conv2d_plan;
 
 /* Human-readable name of a status code; never NULL. */
@@ -189,6 +196,51 @@ int samd_conv2d_stage(const uint32_t *x, samd_fmt xf, samd_fmt wf, const samd_co
                       size_t ws_bytes, hipStream_t stream);
 int samd_conv2d_accumulate(samd_fmt xf, samd_fmt wf, const samd_conv2d_desc *d, int32_t *y, const void *ws,
                            size_t ws_bytes, hipStream_t stream);
+
+/* ---- Autotuning ----
+ * The paper specialises the SAMD instruction sequence for each precision with a code
+ * generator (Sec. 1, Sec. 7).  Here the specialisations are compiled kernel templates
+ * (lane geometry x launch shape), the planner picks one with a cost model, and these
+ * calls let a caller pick by measurement instead.
+ *
+ * At most SAMD_MAX_CANDIDATES plans are listed or timed per call. */
+#define SAMD_MAX_CANDIDATES 64
+
+/* Host-only: up to max_count candidate plans for (xf, wf, *d), ranked by the planner's
+ * cost model, the planner's own choice first; out holds max_count entries, *count
+ * receives the number written.  Tuned plans (below) do not affect this list. */
+int samd_conv2d_candidates(const samd_conv2d_desc *d, samd_fmt xf, samd_fmt wf, int32_t max_count,
+                           samd_conv2d_plan *out, int32_t *count);
+
+/* Workspace bytes samd_conv2d_tune needs to time the first `candidates` candidates: the
+ * largest of their workspaces, plus a second output tensor and a counter. */
+int samd_conv2d_tune_workspace(const samd_conv2d_desc *d, samd_fmt xf, samd_fmt wf, int32_t candidates,
+                               size_t *bytes);
+
+/* Times the first `candidates` candidate plans on the caller's x and w (stage +
+ * accumulate, `reps` times each, HIP events on `stream`) and makes the fastest the plan
+ * of (xf, wf, *d) for every later call in this process, until samd_conv2d_untune.
+ *   x, w, y as for samd_conv2d (y receives the convolution)
+ *   ws      256-byte aligned; candidates whose workspace does not fit next to the
+ *           second output are skipped (SAMD_ENOSPC if the planner's own plan does not);
+ *           samd_conv2d_tune_workspace gives the size that fits them all
+ *   candidates 1..SAMD_MAX_CANDIDATES; reps 1..1000
+ *   chosen  (host, nullable) receives the chosen plan
+ * Every candidate's output is compared on the device with the planner's plan's output;
+ * any difference is an error (SAMD_EHIP, detail in samd_last_error) and nothing is
+ * tuned.  Unlike the other calls this one BLOCKS: it synchronises `stream` to read the
+ * timings.  On return ws is prepared for the chosen plan (as by samd_conv2d_prepare).
+ * Workspaces prepared for the shape before tuning must be prepared again, and their
+ * size queried again (samd_conv2d_workspace reports the tuned plan's).  The tuned plans
+ * are process-wide state shared by all threads: tune during set-up, not while other
+ * threads run the same shape. */
+int samd_conv2d_tune(const uint32_t *x, samd_fmt xf, const uint32_t *w, samd_fmt wf,
+                     const samd_conv2d_desc *d, int32_t *y, void *ws, size_t ws_bytes,
+                     int32_t candidates, int32_t reps, samd_conv2d_plan *chosen, hipStream_t stream);
+
+/* Host-only: forget the tuned plan of (xf, wf, *d), or of every shape when d is NULL
+ * (xf and wf are then ignored); the planner's model decides again. */
+int samd_conv2d_untune(const samd_conv2d_desc *d, samd_fmt xf, samd_fmt wf);
 
 /* Workspace bytes samd_conv2d_int8 needs (reordered int8 weights and per-filter sums). */
 int samd_conv2d_int8_workspace(const samd_conv2d_desc *d, samd_fmt xf, size_t *bytes);

@@ -11,12 +11,13 @@ from __future__ import annotations
 
 import ctypes
 import os
-from typing import Optional, Sequence, Tuple
+from typing import List, Optional, Sequence, Tuple
 
 import torch
 
 __all__ = ["Fmt", "Conv2dDesc", "Conv1dPlan", "Conv2dPlan", "SamdError", "lib", "row_words", "pack", "unpack", "conv1d",
-           "conv1d_plan", "conv2d_plan", "conv2d_workspace", "conv2d", "conv2d_prepare", "conv2d_prepared",
+           "conv1d_plan", "conv2d_plan", "conv2d_candidates", "conv2d_tune_workspace", "conv2d_tune", "conv2d_untune",
+           "conv2d_workspace", "conv2d", "conv2d_prepare", "conv2d_prepared",
            "conv2d_stage", "conv2d_accumulate",
            "conv2d_int8_prepare", "conv2d_int8_prepared", "conv2d_int8_workspace", "conv2d_int8", "max_i32",
            "relu_requant_pack", "relu_requant_nhwc_u8", "out_hw", "LIB_PATH"]
@@ -55,7 +56,8 @@ class Conv2dPlan(ctypes.Structure):
                 ("ntaps", ctypes.c_int32 * 16), ("rows_per_block", ctypes.c_int32), ("mblock", ctypes.c_int32),
                 ("split_waves", ctypes.c_int32), ("chunk_channels", ctypes.c_int32), ("x_offset", ctypes.c_int32),
                 ("col_segments", ctypes.c_int32), ("segment_columns", ctypes.c_int32),
-                ("macs_per_mad", ctypes.c_double)]
+                ("macs_per_mad", ctypes.c_double), ("rows_per_thread", ctypes.c_int32),
+                ("shared_rows", ctypes.c_int32), ("model_cost", ctypes.c_double)]
 
 
 class Conv1dPlan(ctypes.Structure):
@@ -109,6 +111,13 @@ def lib():
                                                        _p]),
             "samd_lanewise": (ctypes.c_int, [ctypes.c_int, _p, _p, _i64, Fmt, _p, _p]),
             "samd_scale": (ctypes.c_int, [_p, _i64, Fmt, _i32, _p, _p]),
+            "samd_conv2d_candidates": (ctypes.c_int, [ctypes.POINTER(Conv2dDesc), Fmt, Fmt, _i32,
+                                                      ctypes.POINTER(Conv2dPlan), ctypes.POINTER(_i32)]),
+            "samd_conv2d_tune_workspace": (ctypes.c_int, [ctypes.POINTER(Conv2dDesc), Fmt, Fmt, _i32,
+                                                          ctypes.POINTER(_sz)]),
+            "samd_conv2d_tune": (ctypes.c_int, [_p, Fmt, _p, Fmt, ctypes.POINTER(Conv2dDesc), _p, _p, _sz, _i32, _i32,
+                                                ctypes.POINTER(Conv2dPlan), _p]),
+            "samd_conv2d_untune": (ctypes.c_int, [ctypes.POINTER(Conv2dDesc), Fmt, Fmt]),
         }
         for name, (res, args) in sigs.items():
             fn = getattr(L, name)
@@ -212,6 +221,53 @@ def conv2d_workspace(shape, xfmt: Fmt, wfmt: Fmt) -> int:
     n = _sz(0)
     _check(lib().samd_conv2d_workspace(ctypes.byref(Conv2dDesc.of(shape)), xfmt, wfmt, ctypes.byref(n)))
     return int(n.value)
+
+
+MAX_CANDIDATES = 64
+
+
+def conv2d_candidates(shape, xfmt: Fmt, wfmt: Fmt, max_count: int = 16) -> List[Conv2dPlan]:
+    """Candidate plans ranked by the planner's cost model, its own choice first."""
+    arr = (Conv2dPlan * max(1, min(max_count, MAX_CANDIDATES)))()
+    n = _i32(0)
+    _check(lib().samd_conv2d_candidates(ctypes.byref(Conv2dDesc.of(shape)), xfmt, wfmt, max_count, arr,
+                                        ctypes.byref(n)))
+    return [arr[i] for i in range(n.value)]
+
+
+def conv2d_tune_workspace(shape, xfmt: Fmt, wfmt: Fmt, candidates: int = 16) -> int:
+    n = _sz(0)
+    _check(lib().samd_conv2d_tune_workspace(ctypes.byref(Conv2dDesc.of(shape)), xfmt, wfmt, candidates,
+                                            ctypes.byref(n)))
+    return int(n.value)
+
+
+def conv2d_tune(xp: torch.Tensor, xfmt: Fmt, wp: torch.Tensor, wfmt: Fmt, shape, candidates: int = 16,
+                reps: int = 5, ws: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None) -> Conv2dPlan:
+    """Time the first `candidates` plans on these inputs and keep the fastest for the shape
+    (blocks until the timings are read).  Workspaces prepared for the shape earlier must
+    be sized and prepared again afterwards."""
+    _dev(xp, torch.int32, "xp")
+    _dev(wp, torch.int32, "wp")
+    d = Conv2dDesc.of(shape)
+    Ho, Wo = out_hw(shape)
+    if ws is None:
+        ws = _workspace(conv2d_tune_workspace(shape, xfmt, wfmt, candidates), xp.device)
+    if out is None:
+        out = torch.empty((d.N, d.M, Ho, Wo), dtype=torch.int32, device=xp.device)
+    _out(out, d.N * d.M * Ho * Wo)
+    plan = Conv2dPlan()
+    _check(lib().samd_conv2d_tune(xp.data_ptr(), xfmt, wp.data_ptr(), wfmt, ctypes.byref(d), out.data_ptr(),
+                                  ws.data_ptr(), ws.numel(), candidates, reps, ctypes.byref(plan), _stream(xp)))
+    return plan
+
+
+def conv2d_untune(shape=None, xfmt: Optional[Fmt] = None, wfmt: Optional[Fmt] = None) -> None:
+    """Forget the tuned plan of one shape, or of every shape (shape None)."""
+    if shape is None:
+        _check(lib().samd_conv2d_untune(None, Fmt(1, False), Fmt(1, False)))
+    else:
+        _check(lib().samd_conv2d_untune(ctypes.byref(Conv2dDesc.of(shape)), xfmt, wfmt))
 
 
 def _workspace(nbytes: int, device) -> torch.Tensor:

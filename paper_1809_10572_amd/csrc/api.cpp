@@ -3,7 +3,9 @@
 #include <cstdarg>
 #include <cstdint>
 #include <cstdio>
+#include <algorithm>
 #include <string>
+#include <vector>
 
 #include "samd_internal.hpp"
 
@@ -175,18 +177,11 @@ int samd_conv1d_plan_query(int64_t n, samd_fmt xf, const int32_t *taps, int32_t 
     return SAMD_OK;
 }
 
-int samd_conv2d_plan_query(const samd_conv2d_desc *d, samd_fmt xf, samd_fmt wf, samd_conv2d_plan *out) {
-    set_error("");
-    int st = check_fmt(xf, "xf");
-    if (!st) st = check_fmt(wf, "wf");
-    if (!st) st = check_conv2d_desc(d);
-    if (!st) st = check_overflow(d, xf, wf);
-    if (st) return st;
-    if (!out) return fail(SAMD_EINVAL, "out must not be NULL");
-    Conv2dGeom g;
-    std::string err;
-    st = plan_conv2d(*d, xf, wf, g, err);
-    if (st) return fail(st, "%s", err.c_str());
+}  // extern "C"
+
+namespace {
+
+void fill_plan(const Conv2dGeom &g, samd_conv2d_plan *out) {
     *out = samd_conv2d_plan{};
     out->lane_bits = g.L;
     out->lanes = g.I;
@@ -208,6 +203,28 @@ int samd_conv2d_plan_query(const samd_conv2d_desc *d, samd_fmt xf, samd_fmt wf, 
     out->col_segments = g.ncs;
     out->segment_columns = g.cw;
     out->macs_per_mad = g.macs_per_mad;
+    out->rows_per_thread = g.rh;
+    out->shared_rows = g.rows_path;
+    out->model_cost = g.cost;
+}
+
+}  // namespace
+
+extern "C" {
+
+int samd_conv2d_plan_query(const samd_conv2d_desc *d, samd_fmt xf, samd_fmt wf, samd_conv2d_plan *out) {
+    set_error("");
+    int st = check_fmt(xf, "xf");
+    if (!st) st = check_fmt(wf, "wf");
+    if (!st) st = check_conv2d_desc(d);
+    if (!st) st = check_overflow(d, xf, wf);
+    if (st) return st;
+    if (!out) return fail(SAMD_EINVAL, "out must not be NULL");
+    Conv2dGeom g;
+    std::string err;
+    st = plan_conv2d(*d, xf, wf, g, err);
+    if (st) return fail(st, "%s", err.c_str());
+    fill_plan(g, out);
     return SAMD_OK;
 }
 
@@ -464,6 +481,178 @@ int samd_relu_requant_nhwc_u8(const int32_t *acc, int32_t N, int32_t C, int32_t 
     if (!acc || !dev_max || !dst) return fail(SAMD_EINVAL, "acc, dev_max and dst must not be NULL");
     if (!aligned4(acc) || !aligned4(dev_max)) return fail(SAMD_EALIGN, "buffer not aligned");
     return launch_relu_requant_nhwc_u8(acc, N, C, H, W, dev_max, out.bits, dst, stream);
+}
+
+// ---------------------------------------------------------------------------------------
+// Autotuning: candidate plans ranked by the model, timed on the device.
+
+}  // extern "C"
+
+namespace {
+
+// Shared validation of the candidate queries and the tuner.
+int check_tune_args(const samd_conv2d_desc *d, samd_fmt xf, samd_fmt wf, int32_t count) {
+    int st = check_fmt(xf, "xf");
+    if (!st) st = check_fmt(wf, "wf");
+    if (!st) st = check_conv2d_desc(d);
+    if (!st) st = check_overflow(d, xf, wf);
+    if (st) return st;
+    if (count < 1 || count > SAMD_MAX_CANDIDATES)
+        return fail(SAMD_EINVAL, "candidate count %d is outside 1..%d", count, SAMD_MAX_CANDIDATES);
+    return SAMD_OK;
+}
+
+size_t round256(size_t n) { return (n + 255) / 256 * 256; }
+
+// Bytes of one output tensor (the tuner's second output) and of its mismatch counter.
+size_t tune_extra_bytes(const samd_conv2d_desc &d, const Conv2dGeom &g) {
+    return round256((size_t)d.N * d.M * g.Ho * g.Wo * 4) + 256;
+}
+
+}  // namespace
+
+extern "C" {
+
+int samd_conv2d_candidates(const samd_conv2d_desc *d, samd_fmt xf, samd_fmt wf, int32_t max_count,
+                           samd_conv2d_plan *out, int32_t *count) {
+    set_error("");
+    int st = check_tune_args(d, xf, wf, max_count);
+    if (st) return st;
+    if (!out || !count) return fail(SAMD_EINVAL, "out and count must not be NULL");
+    std::vector<Conv2dGeom> cands;
+    std::string err;
+    st = conv2d_candidates(*d, xf, wf, max_count, cands, err);
+    if (st) return fail(st, "%s", err.c_str());
+    for (size_t i = 0; i < cands.size(); ++i) fill_plan(cands[i], out + i);
+    *count = (int32_t)cands.size();
+    return SAMD_OK;
+}
+
+int samd_conv2d_tune_workspace(const samd_conv2d_desc *d, samd_fmt xf, samd_fmt wf, int32_t candidates,
+                               size_t *bytes) {
+    set_error("");
+    int st = check_tune_args(d, xf, wf, candidates);
+    if (st) return st;
+    if (!bytes) return fail(SAMD_EINVAL, "bytes must not be NULL");
+    std::vector<Conv2dGeom> cands;
+    std::string err;
+    st = conv2d_candidates(*d, xf, wf, candidates, cands, err);
+    if (st) return fail(st, "%s", err.c_str());
+    size_t most = 0;
+    for (const Conv2dGeom &c : cands) most = std::max(most, conv2d_workspace_bytes(c));
+    *bytes = most + tune_extra_bytes(*d, cands[0]);
+    return SAMD_OK;
+}
+
+int samd_conv2d_tune(const uint32_t *x, samd_fmt xf, const uint32_t *w, samd_fmt wf, const samd_conv2d_desc *d,
+                     int32_t *y, void *ws, size_t ws_bytes, int32_t candidates, int32_t reps,
+                     samd_conv2d_plan *chosen, hipStream_t stream) {
+    set_error("");
+    int st = check_tune_args(d, xf, wf, candidates);
+    if (st) return st;
+    if (reps < 1 || reps > 1000) return fail(SAMD_EINVAL, "reps = %d is outside 1..1000", reps);
+    if (!x || !w || !y || !ws) return fail(SAMD_EINVAL, "x, w, y and ws must not be NULL");
+    if (!aligned4(x) || !aligned4(w) || !aligned4(y)) return fail(SAMD_EALIGN, "x / w / y not aligned");
+    if (((uintptr_t)ws & 255) != 0) return fail(SAMD_EALIGN, "workspace not 256-byte aligned");
+    std::vector<Conv2dGeom> cands;
+    std::string err;
+    st = conv2d_candidates(*d, xf, wf, candidates, cands, err);
+    if (st) return fail(st, "%s", err.c_str());
+    // the candidates whose workspace fits next to the second output and its counter
+    const size_t extra = tune_extra_bytes(*d, cands[0]);
+    if (ws_bytes < extra + conv2d_workspace_bytes(cands[0]))
+        return fail(SAMD_ENOSPC, "workspace %zu bytes < %zu needed for the model's plan", ws_bytes,
+                    extra + conv2d_workspace_bytes(cands[0]));
+    const size_t room = ws_bytes - extra;
+    std::vector<Conv2dGeom> fit;
+    for (const Conv2dGeom &c : cands)
+        if (conv2d_workspace_bytes(c) <= room) fit.push_back(c);
+    int32_t *y_alt = (int32_t *)((char *)ws + room);
+    int32_t *mismatches = (int32_t *)((char *)ws + room + extra - 256);
+    const int64_t ny = (int64_t)d->N * d->M * cands[0].Ho * cands[0].Wo;
+
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    auto cleanup = [&](int status) {
+        if (e0) (void)hipEventDestroy(e0);
+        if (e1) (void)hipEventDestroy(e1);
+        return status;
+    };
+    auto hip_fail = [&](hipError_t e, const char *what) {
+        return fail(SAMD_EHIP, "%s: %s", what, hipGetErrorString(e));
+    };
+    hipError_t he = hipEventCreate(&e0);
+    if (he == hipSuccess) he = hipEventCreate(&e1);
+    if (he != hipSuccess) return cleanup(hip_fail(he, "hipEventCreate"));
+
+    // Round 0 prepares each candidate, checks its result and times it; round 1 times every
+    // candidate again (each keeps its faster time), so that clock ramps and other
+    // transients do not decide.  Before round 0 the model's plan runs untimed for a while
+    // to bring the clocks up.
+    auto run = [&](const Conv2dGeom &c, int32_t *out, int n) {
+        int rs = SAMD_OK;
+        for (int r = 0; r < n && !rs; ++r)
+            if (!(rs = launch_conv2d_spread(x, c, ws, stream))) rs = launch_conv2d_multiply(c, out, ws, stream);
+        return rs;
+    };
+    auto timed = [&](const Conv2dGeom &c, int32_t *out, float &ms) {
+        hipError_t e = hipEventRecord(e0, stream);
+        if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
+        int rs = run(c, out, reps);
+        if (rs) return rs;
+        e = hipEventRecord(e1, stream);
+        if (e == hipSuccess) e = hipEventSynchronize(e1);
+        if (e == hipSuccess) e = hipEventElapsedTime(&ms, e0, e1);
+        return e == hipSuccess ? SAMD_OK : hip_fail(e, "timing");
+    };
+    std::vector<float> best_of(fit.size(), 0.0f);
+    for (int round = 0; round < 2; ++round) {
+        for (size_t i = 0; i < fit.size(); ++i) {
+            const Conv2dGeom &c = fit[i];
+            int32_t *out = i == 0 ? y : y_alt;   // the model's plan writes the reference into y
+            if ((st = launch_conv2d_prepare(w, c, ws, stream)) || (st = run(c, out, 1))) return cleanup(st);
+            if (round == 0 && i == 0 && (st = run(c, out, 4 * reps))) return cleanup(st);
+            if (round == 0 && i > 0) {
+                // every candidate must reproduce the model plan's result exactly
+                if ((st = launch_count_mismatch(y, y_alt, ny, mismatches, stream))) return cleanup(st);
+                int32_t host = -1;
+                he = hipMemcpyAsync(&host, mismatches, sizeof host, hipMemcpyDeviceToHost, stream);
+                if (he == hipSuccess) he = hipStreamSynchronize(stream);
+                if (he != hipSuccess) return cleanup(hip_fail(he, "mismatch count"));
+                if (host != 0)
+                    return cleanup(fail(SAMD_EHIP, "candidate plan %zu (L=%d I=%d rows=%d x %d) differs from the "
+                                                   "model's plan in %d outputs", i, c.L, c.I, c.rows_blk, c.mblk,
+                                        host));
+            }
+            float ms = 0.0f;
+            if ((st = timed(c, out, ms))) return cleanup(st);
+            best_of[i] = round == 0 ? ms : std::min(best_of[i], ms);
+        }
+    }
+    // a candidate must beat the best so far by 2 %: near-ties keep the higher-ranked plan,
+    // so repeated tuning of one shape settles on the same plan
+    size_t best = 0;
+    for (size_t i = 1; i < fit.size(); ++i)
+        if (best_of[i] < best_of[best] * 0.98f) best = i;
+    const Conv2dGeom &g = fit[best];
+    set_tuned_conv2d(*d, xf, wf, g);
+    // leave the workspace prepared for the chosen plan (and y holding its result)
+    if ((st = launch_conv2d_prepare(w, g, ws, stream)) || (st = launch_conv2d_spread(x, g, ws, stream)) ||
+        (st = launch_conv2d_multiply(g, y, ws, stream)))
+        return cleanup(st);
+    if (chosen) fill_plan(g, chosen);
+    return cleanup(SAMD_OK);
+}
+
+int samd_conv2d_untune(const samd_conv2d_desc *d, samd_fmt xf, samd_fmt wf) {
+    set_error("");
+    if (d) {
+        int st = check_fmt(xf, "xf");
+        if (!st) st = check_fmt(wf, "wf");
+        if (!st) st = check_conv2d_desc(d);
+        if (st) return st;
+    }
+    clear_tuned_conv2d(d, xf, wf);
+    return SAMD_OK;
 }
 
 }  // extern "C"

@@ -28,6 +28,21 @@ __global__ __launch_bounds__(kBlock) void max_kernel(const int32_t *__restrict__
     if ((threadIdx.x & 63) == 0) atomicMax(dev_max, m);
 }
 
+__global__ void zero_count_kernel(int32_t *count) {
+    if (threadIdx.x == 0 && blockIdx.x == 0) *count = 0;
+}
+
+// Number of positions where two int32 arrays differ, added to *count.
+__global__ __launch_bounds__(kBlock) void mismatch_kernel(const int32_t *__restrict__ a,
+                                                          const int32_t *__restrict__ b, int64_t n,
+                                                          int32_t *count) {
+    int32_t c = 0;
+    for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < n; i += (int64_t)gridDim.x * kBlock)
+        c += a[i] != b[i] ? 1 : 0;
+    for (int off = 32; off > 0; off >>= 1) c += __shfl_xor(c, off, 64);
+    if ((threadIdx.x & 63) == 0 && c != 0) atomicAdd(count, c);
+}
+
 // Requantisation shift for a layer maximum.
 __device__ inline int requant_shift(int32_t layer_max, int bits) {
     const uint32_t mx = layer_max > 0 ? (uint32_t)layer_max : 0u;
@@ -131,6 +146,15 @@ int launch_max_i32(const int32_t *src, int64_t n, int32_t *dev_max, hipStream_t 
     const int grid = std::min(grid_for(n, kBlock), 2048);
     hipLaunchKernelGGL(max_kernel, dim3(grid), dim3(kBlock), 0, s, src, n, dev_max);
     return check_launch("max");
+}
+
+int launch_count_mismatch(const int32_t *a, const int32_t *b, int64_t n, int32_t *count, hipStream_t s) {
+    hipLaunchKernelGGL(zero_count_kernel, dim3(1), dim3(64), 0, s, count);
+    int st = check_launch("mismatch count init");
+    if (st) return st;
+    const int grid = std::max(1, std::min(grid_for(n, kBlock), 2048));
+    hipLaunchKernelGGL(mismatch_kernel, dim3(grid), dim3(kBlock), 0, s, a, b, n, count);
+    return check_launch("mismatch count");
 }
 
 int launch_relu_requant_pack(const int32_t *acc, int64_t rows, int64_t len, const int32_t *dev_max, int bits,

@@ -14,6 +14,7 @@
 #include <limits>
 #include <map>
 #include <mutex>
+#include <vector>
 
 #include "samd_internal.hpp"
 
@@ -72,8 +73,9 @@ bool split_taps(int count, int kmax, int *t0, int *nt, int &ngroups) {
 // decodes, and its texture path's operand loads (about 12 clocks per wave-wide load on
 // MI355X, shared by the 4 SIMDs), whichever binds, divided by an issue efficiency that
 // grows with the waves resident per SIMD (latency hiding), plus the last item's drain and
-// the operand-spread pass.  Returns false when no tile fits the LDS.
-bool place_launch(const samd_conv2d_desc &d, Conv2dGeom &c) {
+// the operand-spread pass.  Returns false when no tile fits the LDS.  With `all`, every
+// launch shape that fits is also appended to it, priced.
+bool place_launch(const samd_conv2d_desc &d, Conv2dGeom &c, std::vector<Conv2dGeom> *all = nullptr) {
     const int grp_max = 64 / c.nqs;
     const bool rows_ok = d.KH == 3 && d.stride_h == 1 && (c.ntw == 1 || c.ntw == 2);
     bool found = false;
@@ -149,6 +151,7 @@ bool place_launch(const samd_conv2d_desc &d, Conv2dGeom &c) {
                     // fixed costs against scalar-load latency hiding
                     const double slice = 1.0 + 0.15 * std::fabs(std::log2(t.cpw / 32.0));
                     t.cost = (busy / eff + drain) * slice + spread;
+                    if (all) all->push_back(t);
                     if (t.cost < best.cost) {
                         best = t;
                         found = true;
@@ -174,7 +177,7 @@ namespace {
 // stored activation before it enters a lane (0, or 2^(b-1) for recentred unsigned
 // activations, which then behave as signed b-bit values).
 int search_lanes(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, int xoff, Conv2dGeom &best,
-                 std::string &err) {
+                 std::string &err, std::vector<Conv2dGeom> *all = nullptr) {
     Conv2dGeom g = {};
     g.N = d.N; g.C = d.C; g.H = d.H; g.W = d.W; g.M = d.M; g.KH = d.KH; g.KW = d.KW;
     g.sh = d.stride_h; g.sw = d.stride_w; g.ph = d.pad_h; g.pw = d.pad_w;
@@ -272,8 +275,8 @@ int search_lanes(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, int xoff, 
             c.macs_per_mad = (double)I * d.KW / (double)c.ntw;
             // the multiply-adds alone, spread perfectly over every SIMD, bound the cost below
             const double floor_cost = (double)d.N * c.Ho * c.ncs * c.nqs * d.M * d.C * c.nrt / 64.0 / 1024.0;
-            if (found && floor_cost >= best.cost) continue;
-            if (!place_launch(d, c)) continue;
+            if (!all && found && floor_cost >= best.cost) continue;
+            if (!place_launch(d, c, all)) continue;
             if (c.cost < best.cost) {
                 best = c;
                 found = true;
@@ -294,17 +297,22 @@ int search_lanes(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, int xoff, 
 // signed b-bit value, so products are half as large and a lane holds twice as many;
 // the offset comes back exactly as 2^(b-1) times the sum of the weights over each
 // output's in-image taps.  Both are planned and the cheaper kept.
-int search_conv2d(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, Conv2dGeom &best, std::string &err) {
-    int st = search_lanes(d, xf, wf, 0, best, err);
+int search_conv2d(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, Conv2dGeom &best, std::string &err,
+                  std::vector<Conv2dGeom> *all = nullptr) {
+    int st = search_lanes(d, xf, wf, 0, best, err, all);
     if (!xf.is_signed && wf.is_signed && xf.bits >= 2) {
         Conv2dGeom alt;
         std::string err2;
         const samd_fmt xs = {xf.bits, 1};
-        if (search_lanes(d, xs, wf, 1 << (xf.bits - 1), alt, err2) == SAMD_OK) {
+        const size_t first = all ? all->size() : 0;
+        if (search_lanes(d, xs, wf, 1 << (xf.bits - 1), alt, err2, all) == SAMD_OK) {
             // the correction: four table lookups and a multiply-add per output, issued after
             // the last barrier where nothing hides their latency (about 40 issue cycles per
             // output in measurements on MI355X)
-            alt.cost += (double)d.N * d.M * alt.Ho * alt.Wo * 40.0 / 64.0 / 1024.0;
+            const double correction = (double)d.N * d.M * alt.Ho * alt.Wo * 40.0 / 64.0 / 1024.0;
+            alt.cost += correction;
+            if (all)
+                for (size_t i = first; i < all->size(); ++i) (*all)[i].cost += correction;
             if (st != SAMD_OK || alt.cost < best.cost) {
                 best = alt;
                 st = SAMD_OK;
@@ -320,14 +328,33 @@ using PlanKey = std::array<int32_t, 15>;
 std::mutex plan_mu;
 std::map<PlanKey, Conv2dGeom> plan_cache;
 constexpr size_t kPlanCacheMax = 4096;
+// Plans chosen by measurement (samd_conv2d_tune): they take precedence over the model's
+// and are kept until cleared, since workspaces prepared under them depend on them.
+std::map<PlanKey, Conv2dGeom> tuned_plans;
+
+PlanKey plan_key(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf) {
+    return {d.N, d.C, d.H, d.W, d.M, d.KH, d.KW, d.stride_h, d.stride_w, d.pad_h, d.pad_w,
+            xf.bits, xf.is_signed, wf.bits, wf.is_signed};
+}
+
+// The kernels address one image's operand words (and one spare channel) with 32-bit
+// byte offsets, and padded rows with 32-bit indices.
+bool addressable(const samd_conv2d_desc &d, const Conv2dGeom &g) {
+    return (int64_t)(d.C + 1) * g.Hp * g.ntw * g.nq * 4 < ((int64_t)1 << 31) &&
+           (int64_t)d.N * d.C * g.Hp < ((int64_t)1 << 31);
+}
 
 }  // namespace
 
 int plan_conv2d(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, Conv2dGeom &g, std::string &err) {
-    const PlanKey key = {d.N, d.C, d.H, d.W, d.M, d.KH, d.KW, d.stride_h, d.stride_w, d.pad_h, d.pad_w,
-                         xf.bits, xf.is_signed, wf.bits, wf.is_signed};
+    const PlanKey key = plan_key(d, xf, wf);
     {
         std::lock_guard<std::mutex> lock(plan_mu);
+        auto tu = tuned_plans.find(key);
+        if (tu != tuned_plans.end()) {
+            g = tu->second;
+            return SAMD_OK;
+        }
         auto it = plan_cache.find(key);
         if (it != plan_cache.end()) {
             g = it->second;
@@ -335,10 +362,7 @@ int plan_conv2d(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, Conv2dGeom 
         }
     }
     int st = search_conv2d(d, xf, wf, g, err);
-    // the kernels address one image's operand words (and one spare channel) with 32-bit
-    // byte offsets, and padded rows with 32-bit indices
-    if (st == SAMD_OK && ((int64_t)(d.C + 1) * g.Hp * g.ntw * g.nq * 4 >= ((int64_t)1 << 31) ||
-                          (int64_t)d.N * d.C * g.Hp >= ((int64_t)1 << 31))) {
+    if (st == SAMD_OK && !addressable(d, g)) {
         err = "operand words of one image exceed 2 GiB";
         st = SAMD_EUNSUPPORTED;
     }
@@ -348,6 +372,50 @@ int plan_conv2d(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, Conv2dGeom 
         plan_cache.emplace(key, g);
     }
     return st;
+}
+
+int conv2d_candidates(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, int max_count,
+                      std::vector<Conv2dGeom> &out, std::string &err) {
+    out.clear();
+    // the model alone (no cache, no tuned plan): its choice, then every priced candidate
+    Conv2dGeom model;
+    std::vector<Conv2dGeom> all;
+    int st = search_conv2d(d, xf, wf, model, err, &all);
+    if (st) return st;
+    if (!addressable(d, model)) {
+        err = "operand words of one image exceed 2 GiB";
+        return SAMD_EUNSUPPORTED;
+    }
+    std::vector<Conv2dGeom> keep;
+    for (const Conv2dGeom &c : all)
+        if (addressable(d, c)) keep.push_back(c);
+    std::stable_sort(keep.begin(), keep.end(),
+                     [](const Conv2dGeom &a, const Conv2dGeom &b) { return a.cost < b.cost; });
+    auto same = [](const Conv2dGeom &a, const Conv2dGeom &b) {
+        return a.L == b.L && a.I == b.I && a.xoff == b.xoff && a.rows_path == b.rows_path && a.rh == b.rh &&
+               a.groups == b.groups && a.wm == b.wm && a.ks == b.ks;
+    };
+    out.push_back(model);
+    for (const Conv2dGeom &c : keep) {
+        if ((int)out.size() >= max_count) break;
+        bool dup = false;
+        for (const Conv2dGeom &o : out) dup = dup || same(o, c);
+        if (!dup) out.push_back(c);
+    }
+    return SAMD_OK;
+}
+
+void set_tuned_conv2d(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, const Conv2dGeom &g) {
+    std::lock_guard<std::mutex> lock(plan_mu);
+    tuned_plans[plan_key(d, xf, wf)] = g;
+}
+
+void clear_tuned_conv2d(const samd_conv2d_desc *d, samd_fmt xf, samd_fmt wf) {
+    std::lock_guard<std::mutex> lock(plan_mu);
+    if (!d)
+        tuned_plans.clear();
+    else
+        tuned_plans.erase(plan_key(*d, xf, wf));
 }
 
 // Workspace: kernel-word streams, the recentring correction table, the work queues of

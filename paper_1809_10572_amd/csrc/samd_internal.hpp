@@ -6,6 +6,7 @@
 #include <stdint.h>
 
 #include <string>
+#include <vector>
 
 #include "samd.h"
 
@@ -94,6 +95,14 @@ struct Conv1dGeom {
 int plan_conv2d(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, Conv2dGeom &g, std::string &err);
 int plan_conv1d(int64_t n, samd_fmt xf, const int32_t *taps, int32_t K, samd_fmt kf, Conv1dGeom &g,
                 std::string &err);
+// Candidate plans of a shape, ranked by the model's cost, the model's choice first, at
+// most max_count of them (distinct lane geometries and launch shapes).
+int conv2d_candidates(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, int max_count,
+                      std::vector<Conv2dGeom> &out, std::string &err);
+// Plans chosen by measurement take precedence in plan_conv2d until cleared (d == NULL:
+// every shape).
+void set_tuned_conv2d(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, const Conv2dGeom &g);
+void clear_tuned_conv2d(const samd_conv2d_desc *d, samd_fmt xf, samd_fmt wf);
 size_t conv2d_workspace_bytes(const Conv2dGeom &g);
 size_t conv2d_kw_bytes(const Conv2dGeom &g);
 size_t conv2d_pre_bytes(const Conv2dGeom &g);   // the recentring correction table
@@ -115,6 +124,7 @@ int launch_conv2d_i8_prepare(const int8_t *w, samd_fmt xf, const samd_conv2d_des
 int launch_conv2d_i8(const void *x, samd_fmt xf, const samd_conv2d_desc &d, int32_t *y, const void *ws,
                      hipStream_t s);
 int launch_max_i32(const int32_t *src, int64_t n, int32_t *dev_max, hipStream_t s);
+int launch_count_mismatch(const int32_t *a, const int32_t *b, int64_t n, int32_t *count, hipStream_t s);
 int launch_lanewise(int op, const uint32_t *a, const uint32_t *b, int64_t nwords, int bits, uint32_t scalar,
                     uint32_t *dst, hipStream_t s);
 int launch_relu_requant_pack(const int32_t *acc, int64_t rows, int64_t len, const int32_t *dev_max, int bits,

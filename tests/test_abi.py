@@ -162,3 +162,56 @@ def test_lanewise_and_scale_validation():
     assert L.samd_scale(A16, -2, Fmt(4, 0), 3, A16, None) == EINVAL
     assert L.samd_scale(A16, 8, Fmt(4, 0), 3, A4, None) == EALIGN
     assert L.samd_scale(None, 0, Fmt(4, 0), 3, None, None) == OK
+
+
+def test_candidates_and_tune_validation():
+    L = samd.lib()
+    xf, wf = Fmt(4, 0), Fmt(4, 1)
+    arr = (samd.Conv2dPlan * 8)()
+    cnt = ctypes.c_int32(0)
+    assert L.samd_conv2d_candidates(ctypes.byref(MID), xf, wf, 0, arr, ctypes.byref(cnt)) == EINVAL
+    assert L.samd_conv2d_candidates(ctypes.byref(MID), xf, wf, samd.MAX_CANDIDATES + 1, arr,
+                                    ctypes.byref(cnt)) == EINVAL
+    assert L.samd_conv2d_candidates(ctypes.byref(MID), xf, wf, 8, None, ctypes.byref(cnt)) == EINVAL
+    assert L.samd_conv2d_candidates(ctypes.byref(MID), Fmt(9, 0), wf, 8, arr, ctypes.byref(cnt)) == EINVAL
+    assert L.samd_conv2d_candidates(ctypes.byref(MID), xf, wf, 8, arr, ctypes.byref(cnt)) == OK
+    assert 1 <= cnt.value <= 8
+    need = ctypes.c_size_t(0)
+    assert L.samd_conv2d_tune_workspace(ctypes.byref(MID), xf, wf, 8, ctypes.byref(need)) == OK
+    one = ctypes.c_size_t(0)
+    assert L.samd_conv2d_workspace(ctypes.byref(MID), xf, wf, ctypes.byref(one)) == OK
+    assert need.value >= one.value + 8 * 128 * 56 * 56 * 4      # the second output fits beside it
+
+    def tune(**kw):
+        a = dict(dict(x=P4, w=P4, y=P4, ws=P4 * 16, nb=need.value, cands=8, reps=3, d=MID, xf=xf, wf=wf), **kw)
+        return L.samd_conv2d_tune(a["x"], a["xf"], a["w"], a["wf"], ctypes.byref(a["d"]), a["y"], a["ws"], a["nb"],
+                                  a["cands"], a["reps"], None, None)
+
+    # every rejection happens on the host, before anything is dereferenced or launched
+    assert tune(x=None) == EINVAL
+    assert tune(ws=None) == EINVAL
+    assert tune(cands=0) == EINVAL
+    assert tune(reps=0) == EINVAL
+    assert tune(reps=1001) == EINVAL
+    assert tune(y=P1) == EALIGN
+    assert tune(ws=P4 * 16 + 64) == EALIGN
+    assert tune(nb=one.value) == ENOSPC
+    assert tune(d=Conv2dDesc(1, 512, 16, 16, 1, 16, 16, 1, 1, 0, 0), xf=Fmt(8, 0), wf=Fmt(8, 1)) == EOVERFLOW
+    assert L.samd_conv2d_untune(None, Fmt(0, 0), Fmt(0, 0)) == OK       # all shapes: formats ignored
+    assert L.samd_conv2d_untune(ctypes.byref(MID), Fmt(0, 0), wf) == EINVAL
+    assert L.samd_conv2d_untune(ctypes.byref(MID), xf, wf) == OK
+
+
+@pytest.mark.parametrize("bits", [1, 4, 8])
+def test_candidates_rank_the_planner_choice_first(bits):
+    # the planner's own plan leads the list; the rest are distinct shapes priced no lower
+    shape = (8, 128, 56, 56, 128, 3, 3, 1, 1, 1, 1)
+    xf, wf = Fmt(bits, 0), Fmt(bits, 1)
+    plan = samd.conv2d_plan(shape, xf, wf)
+    cands = samd.conv2d_candidates(shape, xf, wf, 16)
+    key = lambda p: (p.lane_bits, p.lanes, p.x_offset, p.shared_rows, p.rows_per_thread, p.rows_per_block,
+                     p.mblock, p.split_waves)
+    assert key(cands[0]) == key(plan)
+    assert len(set(map(key, cands))) == len(cands)
+    assert all(c.model_cost >= cands[0].model_cost for c in cands[1:])
+    assert [c.model_cost for c in cands[1:]] == sorted(c.model_cost for c in cands[1:])

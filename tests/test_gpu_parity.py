@@ -467,3 +467,76 @@ def test_graph_replays_match_eager(bits):
         np.testing.assert_array_equal(y.cpu().numpy(), eager, err_msg=f"replay {i}")
         step()   # eager work between replays
         torch.cuda.synchronize()
+
+
+# --- autotuning ------------------------------------------------------------------------
+
+def plan_key(p):
+    return (p.lane_bits, p.lanes, p.x_offset, p.shared_rows, p.rows_per_thread, p.rows_per_block, p.mblock,
+            p.split_waves)
+
+
+TUNE_CASES = [
+    # (shape, x bits, x signed, w bits): shared-row candidates, strided and 5-wide kernels,
+    # recentred unsigned activations, and a row of more than 64 operand words
+    ((2, 24, 17, 45, 20, 3, 3, 1, 1, 1, 1), 2, False, 2),
+    ((2, 24, 17, 45, 20, 3, 3, 1, 1, 1, 1), 8, False, 8),
+    ((1, 9, 23, 61, 10, 3, 5, 2, 2, 1, 2), 5, True, 4),
+    ((1, 6, 5, 300, 9, 3, 3, 1, 1, 1, 1), 6, True, 6),
+]
+
+
+@pytest.mark.parametrize("case", range(len(TUNE_CASES)))
+def test_conv2d_tune_keeps_results_exact(case):
+    shape, xb, xs, wb = TUNE_CASES[case]
+    N, C, H, W, M, KH, KW = shape[:7]
+    rng = np.random.default_rng(1000 + case)
+    x = wl.uniform(rng, (N, C, H, W), xb, xs)
+    w = wl.uniform(rng, (M, C, KH, KW), wb, True)
+    xf, wf = samd.Fmt(xb, xs), samd.Fmt(wb, True)
+    want = ref.conv2d(x, w, shape)
+    xp = samd.pack(gpu_vals(x, xs), xb, xs)
+    wp = samd.pack(gpu_vals(w, True), wb, True)
+    cands = samd.conv2d_candidates(shape, xf, wf, 12)
+    model = samd.conv2d_plan(shape, xf, wf)
+    assert plan_key(cands[0]) == plan_key(model)
+    try:
+        # every candidate's output is checked against the model plan's inside the call
+        chosen = samd.conv2d_tune(xp, xf, wp, wf, shape, candidates=12, reps=2)
+        assert plan_key(chosen) in [plan_key(c) for c in cands]
+        assert plan_key(samd.conv2d_plan(shape, xf, wf)) == plan_key(chosen)
+        # later calls use the tuned plan (workspace sized and prepared under it)
+        y = samd.conv2d(xp, xf, wp, wf, shape)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(y.cpu().numpy(), want)
+    finally:
+        samd.conv2d_untune(shape, xf, wf)
+    assert plan_key(samd.conv2d_plan(shape, xf, wf)) == plan_key(model)
+
+
+def test_conv2d_tune_output_and_prepared_workspace():
+    # the tuner leaves y holding the result and ws prepared for the chosen plan; with room
+    # for the model plan only, the candidates that need more workspace are skipped
+    shape = (2, 16, 12, 30, 12, 3, 3, 1, 1, 1, 1)
+    rng = np.random.default_rng(77)
+    x = wl.uniform(rng, (2, 16, 12, 30), 3, False)
+    w = wl.uniform(rng, (12, 16, 3, 3), 3, True)
+    xf, wf = samd.Fmt(3, False), samd.Fmt(3, True)
+    want = ref.conv2d(x, w, shape)
+    xp = samd.pack(gpu_vals(x, False), 3, False)
+    wp = samd.pack(gpu_vals(w, True), 3, True)
+    full = samd.conv2d_tune_workspace(shape, xf, wf, 8)
+    extra = (2 * 12 * 12 * 30 * 4 + 255) // 256 * 256 + 256     # the second output and its counter
+    tight = samd.conv2d_workspace(shape, xf, wf) + extra
+    for nbytes in (full, tight):
+        ws = torch.empty(nbytes, dtype=torch.uint8, device=DEV)
+        y = torch.full((2, 12, 12, 30), -7, dtype=torch.int32, device=DEV)
+        try:
+            samd.conv2d_tune(xp, xf, wp, wf, shape, candidates=8, reps=1, ws=ws, out=y)
+            torch.cuda.synchronize()
+            np.testing.assert_array_equal(y.cpu().numpy(), want)
+            y2 = samd.conv2d_prepared(xp, xf, wf, shape, ws)
+            torch.cuda.synchronize()
+            np.testing.assert_array_equal(y2.cpu().numpy(), want)
+        finally:
+            samd.conv2d_untune(None)
