@@ -45,6 +45,10 @@ def parse():
     p.add_argument("--no-tune", action="store_true",
                    help="use the planner's model plans (default: time the top candidates at set-up)")
     p.add_argument("--tune-candidates", type=int, default=16, help="candidate plans timed per bit width")
+    p.add_argument("--plans-out", metavar="FILE", help="write the plans used per bit width (JSON)")
+    p.add_argument("--plans-in", metavar="FILE",
+                   help="use the plans of a --plans-out file instead of tuning (profiled runs replay the plans "
+                        "of an untraced one)")
     p.add_argument("--counters", action="store_true",
                    help="launch each kernel once per bit width, eagerly, then a 1 GiB streaming copy, and exit "
                         "(the program rocprofv3 --pmc passes run)")
@@ -447,14 +451,21 @@ def main():
 
     # set-up: each bit width's plan chosen by timing the planner's top candidates on the
     # layer's own inputs (outside every timed region); the workspace is then sized again
-    if not args.no_tune:
+    plans_in = json.load(open(args.plans_in)) if args.plans_in else None
+    if plans_in or not args.no_tune:
         for L in layers:
-            samd.pack(L["x"], L["b"], False, out=L["xp"])
-            samd.conv2d_tune(L["xp"], L["xf"], L["wp"], L["wf"], shape, candidates=args.tune_candidates, reps=10)
+            if plans_in:
+                samd.conv2d_use_plan(shape, L["xf"], L["wf"], plans_in[str(L["b"])])
+            else:
+                samd.pack(L["x"], L["b"], False, out=L["xp"])
+                samd.conv2d_tune(L["xp"], L["xf"], L["wp"], L["wf"], shape, candidates=args.tune_candidates, reps=10)
             L["ws"] = torch.empty(max(samd.conv2d_workspace(shape, L["xf"], L["wf"]), 256), dtype=torch.uint8,
                                   device=dev)
             L["plan"] = samd.conv2d_plan(shape, L["xf"], L["wf"])
         torch.cuda.synchronize()
+    if args.plans_out:
+        with open(args.plans_out, "w") as fh:
+            json.dump({str(L["b"]): samd.plan_key(L["plan"]) for L in layers}, fh, indent=1)
 
     # the layer's kernel words are prepared once per layer (weights are constant)
     for L in layers:
@@ -591,7 +602,8 @@ def main():
         "dtype": "int64", "data": "synthetic",
         "config": {"workload": "conv2d 8x128x56x56 -> 128, 3x3, stride 1, pad 1; unsigned b-bit activations x "
                                "signed b-bit weights; one step = pack + stage + accumulate at each b (kernel words prepared once per layer)",
-                   "plans": "model" if args.no_tune else f"tuned at set-up ({args.tune_candidates} candidates timed)",
+                   "plans": (f"from {os.path.basename(args.plans_in)}" if args.plans_in else "model" if args.no_tune
+                             else f"tuned at set-up ({args.tune_candidates} candidates timed)"),
                    "bits": bits_list, "global_batch": N, "macs_per_layer": macs},
         "roofline": {"bound": "alu", "achieved": round(achieved / 1e12, 3), "peak": round(PEAK_VALU_OPS / 1e12, 2),
                      "unit": "TOP/s", "frac": round(achieved / PEAK_VALU_OPS, 4),

@@ -238,6 +238,13 @@ int samd_conv2d_tune(const uint32_t *x, samd_fmt xf, const uint32_t *w, samd_fmt
                      const samd_conv2d_desc *d, int32_t *y, void *ws, size_t ws_bytes,
                      int32_t candidates, int32_t reps, samd_conv2d_plan *chosen, hipStream_t stream);
 
+/* Host-only: make `plan` - one reported for this shape by samd_conv2d_candidates,
+ * samd_conv2d_tune or samd_conv2d_plan_query, matched by its lane geometry (lane_bits,
+ * lanes, x_offset) and launch shape (shared_rows, rows_per_thread, rows_per_block,
+ * mblock, split_waves) - the plan of (xf, wf, *d), as if tuned: a tuning result kept
+ * from an earlier process.  SAMD_EINVAL when no candidate of the shape matches. */
+int samd_conv2d_use_plan(const samd_conv2d_desc *d, samd_fmt xf, samd_fmt wf, const samd_conv2d_plan *plan);
+
 /* Host-only: forget the tuned plan of (xf, wf, *d), or of every shape when d is NULL
  * (xf and wf are then ignored); the planner's model decides again. */
 int samd_conv2d_untune(const samd_conv2d_desc *d, samd_fmt xf, samd_fmt wf);

@@ -17,6 +17,7 @@ import torch
 
 __all__ = ["Fmt", "Conv2dDesc", "Conv1dPlan", "Conv2dPlan", "SamdError", "lib", "row_words", "pack", "unpack", "conv1d",
            "conv1d_plan", "conv2d_plan", "conv2d_candidates", "conv2d_tune_workspace", "conv2d_tune", "conv2d_untune",
+           "conv2d_use_plan", "plan_key",
            "conv2d_workspace", "conv2d", "conv2d_prepare", "conv2d_prepared",
            "conv2d_stage", "conv2d_accumulate",
            "conv2d_int8_prepare", "conv2d_int8_prepared", "conv2d_int8_workspace", "conv2d_int8", "max_i32",
@@ -118,6 +119,8 @@ def lib():
             "samd_conv2d_tune": (ctypes.c_int, [_p, Fmt, _p, Fmt, ctypes.POINTER(Conv2dDesc), _p, _p, _sz, _i32, _i32,
                                                 ctypes.POINTER(Conv2dPlan), _p]),
             "samd_conv2d_untune": (ctypes.c_int, [ctypes.POINTER(Conv2dDesc), Fmt, Fmt]),
+            "samd_conv2d_use_plan": (ctypes.c_int, [ctypes.POINTER(Conv2dDesc), Fmt, Fmt,
+                                                    ctypes.POINTER(Conv2dPlan)]),
         }
         for name, (res, args) in sigs.items():
             fn = getattr(L, name)
@@ -260,6 +263,25 @@ def conv2d_tune(xp: torch.Tensor, xfmt: Fmt, wp: torch.Tensor, wfmt: Fmt, shape,
     _check(lib().samd_conv2d_tune(xp.data_ptr(), xfmt, wp.data_ptr(), wfmt, ctypes.byref(d), out.data_ptr(),
                                   ws.data_ptr(), ws.numel(), candidates, reps, ctypes.byref(plan), _stream(xp)))
     return plan
+
+
+PLAN_KEY_FIELDS = ("lane_bits", "lanes", "x_offset", "shared_rows", "rows_per_thread", "rows_per_block", "mblock",
+                   "split_waves")
+
+
+def plan_key(plan: Conv2dPlan) -> dict:
+    """The fields that identify a plan among a shape's candidates (for conv2d_use_plan)."""
+    return {f: int(getattr(plan, f)) for f in PLAN_KEY_FIELDS}
+
+
+def conv2d_use_plan(shape, xfmt: Fmt, wfmt: Fmt, plan) -> None:
+    """Make a plan (a Conv2dPlan, or a plan_key dict) the shape's plan, as if tuned."""
+    if isinstance(plan, dict):
+        p = Conv2dPlan()
+        for f in PLAN_KEY_FIELDS:
+            setattr(p, f, int(plan[f]))
+        plan = p
+    _check(lib().samd_conv2d_use_plan(ctypes.byref(Conv2dDesc.of(shape)), xfmt, wfmt, ctypes.byref(plan)))
 
 
 def conv2d_untune(shape=None, xfmt: Optional[Fmt] = None, wfmt: Optional[Fmt] = None) -> None:

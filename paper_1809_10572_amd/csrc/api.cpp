@@ -643,6 +643,27 @@ int samd_conv2d_tune(const uint32_t *x, samd_fmt xf, const uint32_t *w, samd_fmt
     return cleanup(SAMD_OK);
 }
 
+int samd_conv2d_use_plan(const samd_conv2d_desc *d, samd_fmt xf, samd_fmt wf, const samd_conv2d_plan *plan) {
+    set_error("");
+    int st = check_tune_args(d, xf, wf, 1);
+    if (st) return st;
+    if (!plan) return fail(SAMD_EINVAL, "plan must not be NULL");
+    const samd_conv2d_plan want = *plan;
+    Conv2dGeom g;
+    std::string err;
+    st = find_conv2d_candidate(
+        *d, xf, wf,
+        [&](const Conv2dGeom &c) {
+            return c.L == want.lane_bits && c.I == want.lanes && c.xoff == want.x_offset &&
+                   c.rows_path == want.shared_rows && c.rh == want.rows_per_thread &&
+                   c.rows_blk == want.rows_per_block && c.mblk == want.mblock && c.ks == want.split_waves;
+        },
+        g, err);
+    if (st) return fail(st, "%s", err.c_str());
+    set_tuned_conv2d(*d, xf, wf, g);
+    return SAMD_OK;
+}
+
 int samd_conv2d_untune(const samd_conv2d_desc *d, samd_fmt xf, samd_fmt wf) {
     set_error("");
     if (d) {

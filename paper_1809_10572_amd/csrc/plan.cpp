@@ -12,6 +12,7 @@
 #include <cstdio>
 #include <array>
 #include <limits>
+#include <functional>
 #include <map>
 #include <mutex>
 #include <vector>
@@ -403,6 +404,21 @@ int conv2d_candidates(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, int m
         if (!dup) out.push_back(c);
     }
     return SAMD_OK;
+}
+
+int find_conv2d_candidate(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf,
+                          const std::function<bool(const Conv2dGeom &)> &match, Conv2dGeom &out,
+                          std::string &err) {
+    std::vector<Conv2dGeom> all;
+    int st = conv2d_candidates(d, xf, wf, std::numeric_limits<int>::max(), all, err);
+    if (st) return st;
+    for (const Conv2dGeom &c : all)
+        if (match(c)) {
+            out = c;
+            return SAMD_OK;
+        }
+    err = "no candidate plan of this shape matches";
+    return SAMD_EINVAL;
 }
 
 void set_tuned_conv2d(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, const Conv2dGeom &g) {

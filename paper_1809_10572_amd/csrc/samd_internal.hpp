@@ -5,6 +5,7 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <functional>
 #include <string>
 #include <vector>
 
@@ -99,6 +100,10 @@ int plan_conv1d(int64_t n, samd_fmt xf, const int32_t *taps, int32_t K, samd_fmt
 // most max_count of them (distinct lane geometries and launch shapes).
 int conv2d_candidates(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, int max_count,
                       std::vector<Conv2dGeom> &out, std::string &err);
+// The first of all candidate plans (no count limit) that `match` accepts.
+int find_conv2d_candidate(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf,
+                          const std::function<bool(const Conv2dGeom &)> &match, Conv2dGeom &out,
+                          std::string &err);
 // Plans chosen by measurement take precedence in plan_conv2d until cleared (d == NULL:
 // every shape).
 void set_tuned_conv2d(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, const Conv2dGeom &g);

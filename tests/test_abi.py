@@ -215,3 +215,23 @@ def test_candidates_rank_the_planner_choice_first(bits):
     assert len(set(map(key, cands))) == len(cands)
     assert all(c.model_cost >= cands[0].model_cost for c in cands[1:])
     assert [c.model_cost for c in cands[1:]] == sorted(c.model_cost for c in cands[1:])
+
+
+def test_use_plan_installs_a_candidate():
+    shape = (2, 24, 17, 45, 20, 3, 3, 1, 1, 1, 1)
+    xf, wf = Fmt(5, 0), Fmt(5, 1)
+    model = samd.conv2d_plan(shape, xf, wf)
+    cands = samd.conv2d_candidates(shape, xf, wf, 8)
+    try:
+        for c in cands[1:4]:
+            samd.conv2d_use_plan(shape, xf, wf, samd.plan_key(c))
+            assert samd.plan_key(samd.conv2d_plan(shape, xf, wf)) == samd.plan_key(c)
+            assert samd.conv2d_workspace(shape, xf, wf) > 0
+        bogus = dict(samd.plan_key(model), split_waves=3)
+        with pytest.raises(samd.SamdError):
+            samd.conv2d_use_plan(shape, xf, wf, bogus)
+    finally:
+        samd.conv2d_untune(shape, xf, wf)
+    assert samd.plan_key(samd.conv2d_plan(shape, xf, wf)) == samd.plan_key(model)
+    L = samd.lib()
+    assert L.samd_conv2d_use_plan(ctypes.byref(MID), xf, wf, None) == EINVAL
