@@ -200,9 +200,10 @@ __device__ __forceinline__ void decode_word_n(uint64_t v, uint64_t msb_mask, int
 // lanes.
 //
 // The grid holds at most as many workgroups as the chip keeps resident.  XCD x (hardware
-// assigns workgroup p to XCD p % 8) owns the spatial tiles t = x (mod 8), each with all its
-// channel blocks in consecutive items, so a tile's operand words are fetched into that
-// XCD's L2 and reused there.  Workgroup p first computes item p / 8 of its XCD; the items
+// assigns workgroup p to XCD p % 8) owns one contiguous eighth of the spatial tiles, each
+// with all its channel blocks in consecutive items, so a tile's operand words - and the
+// halo rows it shares with the next row tile - are fetched into that XCD's L2 once and
+// reused there.  Workgroup p first computes item p / 8 of its XCD; the items
 // beyond the XCD's workgroups go to whichever workgroup frees up first, through a ticket
 // counter per XCD: waves of equal work finish far apart (the SIMD issues the oldest wave
 // first), and a fixed assignment would leave the chip draining for much of the launch.
@@ -232,7 +233,10 @@ __global__ __launch_bounds__(1024) void conv2d_samd_kernel(const int32_t *__rest
 
     const int xcd = blockIdx.x % kNumXcd;
     const int ntiles = g.tiles;                                          // N x row tiles x column segments
-    const int nitems = (ntiles - xcd + kNumXcd - 1) / kNumXcd * g.nmb;   // items of this XCD
+    // XCD x owns the tiles [t0, t1): a contiguous range, so neighbouring row tiles (which
+    // share their halo input rows) meet in one L2
+    const int t0 = (int)((int64_t)xcd * ntiles / kNumXcd), t1 = (int)((int64_t)(xcd + 1) * ntiles / kNumXcd);
+    const int nitems = (t1 - t0) * g.nmb;                                // items of this XCD
     const int nwg = gridDim.x / kNumXcd;                                 // workgroups of this XCD
     const int nextra = max(0, nitems - nwg);                             // items handed out by ticket
     unsigned long long *const counter = tickets + xcd * (kTicketStride / 8);
@@ -307,7 +311,7 @@ __global__ __launch_bounds__(1024) void conv2d_samd_kernel(const int32_t *__rest
         unsigned long long ticket = 0;
         if (nextra > 0 && tid == 0) ticket = atomicAdd(counter, 1ull);
         const int mb = item % g.nmb;
-        const int tile_id = (item / g.nmb) * kNumXcd + xcd;   // (n, row tile, column segment)
+        const int tile_id = t0 + item / g.nmb;   // (n, row tile, column segment)
         // SEG: rows are split into column segments; without, the segment terms fold away
         // (their run-time divisions and bounds cost measurable time per item)
         const int cs = SEG ? tile_id % g.ncs : 0, rt_id = SEG ? tile_id / g.ncs : tile_id;
