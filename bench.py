@@ -244,9 +244,13 @@ def run_vggb(args):
             x = torch.from_numpy(case.x.astype(np.int8)).to(dev)
             x_nhwc = torch.from_numpy(np.ascontiguousarray(np.transpose(case.x, (0, 2, 3, 1))).astype(np.int8)).to(dev)
             w8 = torch.from_numpy(case.w.astype(np.int8)).to(dev)
-            ws = samd.conv2d_prepare(samd.pack(w8, b, True), f, shape, f)
-            ws8 = samd.conv2d_int8_prepare(w8, f, shape, f)
+            wp = samd.pack(w8, b, True)
             xp = samd.pack(x, b, True)
+            if not args.no_tune:
+                # set-up: the layer's plan chosen by timing the model's top candidates
+                samd.conv2d_tune(xp, f, wp, f, shape, candidates=args.tune_candidates, reps=10)
+            ws = samd.conv2d_prepare(wp, f, shape, f)
+            ws8 = samd.conv2d_int8_prepare(w8, f, shape, f)
             y = torch.empty((shape.N, shape.M, Ho, Wo), dtype=torch.int32, device=dev)
             y8 = torch.empty_like(y)
             t_pack = timed_graph(lambda: samd.pack(x, b, True, out=xp), args.reps, args.kernel_warm_s)
@@ -266,7 +270,9 @@ def run_vggb(args):
                          "int8_us": round(t_int8 * 1e6, 2), "samd_gmacs": round(macs / t_samd / 1e9, 1),
                          "int8_gmacs": round(macs / t_int8 / 1e9, 1), "speedup_vs_int8": round(t_int8 / t_samd, 3),
                          "lane_bits": p.lane_bits, "lanes": p.lanes, "tap_words": p.tap_words,
-                         "flush_channels": p.flush_channels, "parity": ok})
+                         "flush_channels": p.flush_channels, "tile": f"{p.rows_per_block}x{p.mblock}",
+                         "rows_per_thread": p.rows_per_thread, "shared_rows": bool(p.shared_rows),
+                         "split_waves": p.split_waves, "parity": ok})
             tot_macs += macs
             tot_s += t_samd
             tot_int8_s += t_int8
@@ -277,7 +283,8 @@ def run_vggb(args):
             "higher_is_better": True, "dtype": "int64", "data": "synthetic",
             "config": {"workload": "VGG-B's ten 3x3 convolution layers, batch 1, each layer on its own; "
                                    "one call = stage + accumulate with prepared kernel words",
-                       "bits": bits_list},
+                       "bits": bits_list,
+                       "plans": "model" if args.no_tune else f"tuned at set-up ({args.tune_candidates} candidates timed)"},
             "int8_gmacs": round(tot_macs / tot_int8_s / 1e9, 1),
             "per_layer": rows}
     print(json.dumps(line), flush=True)
@@ -307,8 +314,8 @@ def run_stack(args):
         for l in lys:
             Ho, Wo = samd.out_hw(l)
             macs += l.N * l.M * Ho * Wo * l.C * l.KH * l.KW
-        wss = [samd.conv2d_prepare(samd.pack(torch.from_numpy(w.astype(np.int8)).to(dev), bits, True), wf, l, xf)
-               for w, l in zip(case.ws, lys)]
+        wps = [samd.pack(torch.from_numpy(w.astype(np.int8)).to(dev), bits, True) for w in case.ws]
+        wss = [samd.conv2d_prepare(wp, wf, l, xf) for wp, l in zip(wps, lys)]
         ws8 = [samd.conv2d_int8_prepare(torch.from_numpy(w.astype(np.int8)).to(dev), wf, l, xf)
                for w, l in zip(case.ws, lys)]
         x8 = torch.from_numpy(case.x.astype(np.uint8)).to(dev)
@@ -335,6 +342,15 @@ def run_stack(args):
                     samd.max_i32(ys[li], out=mx)
                     samd.relu_requant_stage(ys[li], mx, bits, wf, lys[li + 1], wss[li + 1])
 
+        if not args.no_tune:
+            # set-up: each layer's plan tuned on its own input (one pass of the packed chain
+            # gives every layer's activations), then the kernel words prepared again
+            chain_packed()
+            for li, l in enumerate(lys):
+                samd.conv2d_tune(xps[li], xf, wps[li], wf, l, candidates=args.tune_candidates, reps=3)
+                wss[li] = samd.conv2d_prepare(wps[li], wf, l, xf)
+            torch.cuda.synchronize()
+
         def chain_int8():
             for li, l in enumerate(lys):
                 samd.conv2d_int8_prepared(x8s[li], xf, wf, l, ws8[li], out=ys[li])
@@ -354,7 +370,9 @@ def run_stack(args):
                       "data": "synthetic",
                       "config": {"workload": "five conv layers (11x11/4 96, 5x5 256, 3x3 384, 3x3 384, 3x3 256) on "
                                              "16x3x224x224, no pooling, ReLU + requantisation between layers",
-                                 "bits": bits_list, "macs": macs},
+                                 "bits": bits_list, "macs": macs,
+                                 "plans": "model" if args.no_tune else
+                                 f"tuned per layer at set-up ({args.tune_candidates} candidates timed)"},
                       "per_bits": rows}), flush=True)
 
 
