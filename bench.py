@@ -58,6 +58,9 @@ def parse():
     p.add_argument("--stack", action="store_true",
                    help="instead of the default workload, time the AlexNet-shaped five-layer stack (b = 2, 4, 8 or "
                         "--bits): SAMD with packed or operand-word activations between layers, and int8")
+    p.add_argument("--configs", action="store_true",
+                   help="instead of the default workload, time the other workloads: the single small layer, "
+                        "the 2^20-value conv1d (b = 1..8, 3 and 5 taps) and the extremes-heavy signed layer")
     p.add_argument("--lanewise", action="store_true",
                    help="instead of the default workload, time lane-wise add/sub/mul/scale on packed words (GB/s)")
     p.add_argument("--trace-summary", metavar="TRACE_DIR",
@@ -219,6 +222,83 @@ def timed_graph(fn, reps, warm_s):
     e1.record(stream)
     e1.synchronize()
     return e0.elapsed_time(e1) * 1e-3 / reps
+
+
+def run_configs(args):
+    """Workloads 1, 2 and 4 next to the default one: per (workload, b[, K]) GMAC/s, the
+    roofline fraction of the bound that applies (VALU multiply-adds for conv2d, HBM bytes
+    for conv1d), the int8 baseline where it applies, and a parity check against the
+    oracle on the same inputs.  Prints one JSON line."""
+    import numpy as np
+    import torch
+
+    import paper_1809_10572_amd as samd
+    import samd_workloads as wl
+    from oracle import reference as ref
+
+    dev = torch.device("cuda:0")
+    out = {"single": [], "conv1d": [], "stress": []}
+
+    def conv2d_row(cfg, b, shape, case):
+        xf, wf = samd.Fmt(b, case.x_signed), samd.Fmt(b, case.w_signed)
+        x = torch.from_numpy(case.x.astype(np.int8 if case.x_signed else np.uint8)).to(dev)
+        x_nhwc = torch.from_numpy(np.ascontiguousarray(np.transpose(case.x, (0, 2, 3, 1))).astype(
+            np.int8 if case.x_signed else np.uint8)).to(dev)
+        w8 = torch.from_numpy(case.w.astype(np.int8)).to(dev)
+        wp = samd.pack(w8, b, True)
+        xp = samd.pack(x, b, case.x_signed)
+        if not args.no_tune:
+            samd.conv2d_tune(xp, xf, wp, wf, shape, candidates=args.tune_candidates, reps=10)
+        ws = samd.conv2d_prepare(wp, wf, shape, xf)
+        ws8 = samd.conv2d_int8_prepare(w8, wf, shape, xf)
+        Ho, Wo = samd.out_hw(shape)
+        y = torch.empty((shape.N, shape.M, Ho, Wo), dtype=torch.int32, device=dev)
+        y8 = torch.empty_like(y)
+        t = timed_graph(lambda: samd.conv2d_prepared(xp, xf, wf, shape, ws, out=y), args.reps, args.kernel_warm_s)
+        ta = timed_graph(lambda: samd.conv2d_accumulate(xf, wf, shape, ws, out=y), args.reps, args.kernel_warm_s)
+        t8 = timed_graph(lambda: samd.conv2d_int8_prepared(x_nhwc, xf, wf, shape, ws8, out=y8), args.reps,
+                         args.kernel_warm_s)
+        samd.conv2d_prepared(xp, xf, wf, shape, ws, out=y)
+        torch.cuda.synchronize()
+        rng = np.random.default_rng(cfg * 100 + b)
+        idx = np.stack([rng.integers(0, n, 512) for n in (shape.N, shape.M, Ho, Wo)], axis=1)
+        want = ref.conv2d_points(case.x, case.w, shape.as_tuple(), idx)
+        ok = bool(np.array_equal(y.cpu().numpy()[tuple(idx.T)], want) and
+                  np.array_equal(y8.cpu().numpy()[tuple(idx.T)], want))
+        p = samd.conv2d_plan(shape, xf, wf)
+        macs = shape.N * shape.M * Ho * Wo * shape.C * shape.KH * shape.KW
+        mads = shape.N * shape.M * Ho * p.words_per_row * shape.C * shape.KH * p.tap_words
+        return {"bits": b, "us": round(t * 1e6, 2), "accumulate_us": round(ta * 1e6, 2),
+                "gmacs": round(macs / t / 1e9, 1), "valu_frac": round(mads / ta / PEAK_VALU_OPS, 4),
+                "int8_us": round(t8 * 1e6, 2), "speedup_vs_int8": round(t8 / t, 3),
+                "lane_bits": p.lane_bits, "lanes": p.lanes, "flush_channels": p.flush_channels, "parity": ok}
+
+    for b in (4,):
+        out["single"].append(conv2d_row(1, b, wl.SINGLE, wl.conv2d_case(1, b)))
+    for b in range(1, 9):
+        for K in (3, 5):
+            case = wl.conv1d_case(b, K)
+            n = case.x.size
+            xp = samd.pack(torch.from_numpy(case.x.astype(np.uint8)).to(dev).view(1, n), b, False).view(-1)
+            y = samd.conv1d(xp, n, b, case.k.tolist(), b)
+            t = timed_graph(lambda: samd.conv1d(xp, n, b, case.k.tolist(), b, out=y), args.reps, args.kernel_warm_s)
+            torch.cuda.synchronize()
+            ok = bool(np.array_equal(y.cpu().numpy(), ref.conv1d(case.x, case.k)))
+            nbytes = samd.row_words(n, b) * 4 + (n - K + 1) * 4
+            out["conv1d"].append({"bits": b, "taps": K, "us": round(t * 1e6, 2),
+                                  "gmacs": round((n - K + 1) * K / t / 1e9, 1),
+                                  "gbps": round(nbytes / t / 1e9, 1), "hbm_frac": round(nbytes / t / PEAK_HBM, 4),
+                                  "parity": ok})
+    for b in wl.BITS_SWEEP[4]:
+        out["stress"].append(conv2d_row(4, b, wl.STRESS, wl.conv2d_case(4, b)))
+    print(json.dumps({"metric": "SAMD workloads 1, 2 and 4: GMAC/s and roofline fractions", "n_gpus": 1,
+                      "data": "synthetic", "dtype": "int64",
+                      "config": {"single": "1x16x16x16 -> 16, 3x3, u4 x s4",
+                                 "conv1d": "2^20 unsigned b-bit values, 3 and 5 unsigned taps, valid mode",
+                                 "stress": "4x256x28x28 -> 256, 3x3, signed x signed, half the values at the range ends",
+                                 "timing": "stage + accumulate (kernel words prepared once); conv1d whole call",
+                                 "plans": "model" if args.no_tune else "tuned at set-up"},
+                      **out}), flush=True)
 
 
 def run_vggb(args):
@@ -419,6 +499,9 @@ def main():
     args.bits_given = "--bits" in sys.argv
     if args.vggb:
         run_vggb(args)
+        return
+    if args.configs:
+        run_configs(args)
         return
     if args.lanewise:
         run_lanewise(args)

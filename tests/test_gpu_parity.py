@@ -83,10 +83,13 @@ def test_conv1d_full_size(bits, K):
     np.testing.assert_array_equal(y.cpu().numpy(), want)
 
 
-@pytest.mark.parametrize("bits", [1, 2, 5, 8])
+@pytest.mark.parametrize("bits", range(1, 9))
 def test_conv1d_ragged_and_degenerate(bits):
     rng = np.random.default_rng(bits)
-    for n, K in ((1, 1), (3, 3), (4, 3), (5, 5), (33, 3), (97, 5), (1000, 7), (257, 16), (65, 1)):
+    # tiny and degenerate rows, then rows of several blocks of output words with ragged ends
+    # and wide kernels (several following words per output word)
+    for n, K in ((1, 1), (3, 3), (4, 3), (5, 5), (33, 3), (97, 5), (1000, 7), (257, 16), (65, 1),
+                 (100003, 3), (70001, 9), (8197, 16), (4096 * 3 + 1, 2)):
         x = wl.uniform(rng, (n,), bits, False)
         k = wl.uniform(rng, (K,), bits, False)
         words, _ = ref.pack(x, bits, False)
