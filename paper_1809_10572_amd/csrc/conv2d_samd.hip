@@ -93,10 +93,10 @@ __global__ __launch_bounds__(256) void prefix_kernel(const uint32_t *__restrict_
 
 // Operand words xs[n][c][hp][t][q] for padded rows hp in [0, H + 2 ph), of the
 // activations minus xoff (recentred unsigned activations).  A block of 256
-// threads covers 256 / QP padded rows (QP = nq rounded up to a power of two, at most
-// 256): thread (row, q) builds word q (and q + QP, ... for rows of more than 256 words)
-// of every kernel-word variant t of its row from the packed input row (L1-resident; rows
-// of the zero padding give zeros).
+// threads covers 256 / QP padded rows (QP, a power of two of at most 256, about nq / 2.5
+// threads per row): thread (row, q) builds words q, q + QP, ... of every kernel-word
+// variant t of its row from the packed input row (L1-resident; rows of the zero padding
+// give zeros).
 template <int B, bool S>
 __global__ __launch_bounds__(256) void spread_kernel(const uint32_t *__restrict__ x, const Conv2dGeom g, int qshift,
                                                      int32_t *__restrict__ xs) {
@@ -612,8 +612,11 @@ int launch_conv2d_prepare(const uint32_t *w, const Conv2dGeom &g, void *ws, hipS
 
 int launch_conv2d_spread(const uint32_t *x, const Conv2dGeom &g, void *ws, hipStream_t s) {
     int32_t *xs = (int32_t *)((char *)ws + conv2d_xs_offset(g));
+    // 2^qshift threads per row, each building about 2.5 of its words (words q, q + 2^qshift,
+    // ...): measured on MI355X, 2-3 words per thread amortise the per-thread row and
+    // address set-up best (one word per thread was 5-23 % slower at the mid-size layer)
     int qshift = 0;
-    while ((1 << qshift) < g.nq && qshift < 8) ++qshift;   // up to 256 threads per row
+    while ((1 << qshift) * 5 < 2 * g.nq && qshift < 8) ++qshift;   // up to 256 threads per row
     const int64_t nrows = (int64_t)g.N * g.C * g.Hp;
     const int rpb = 256 >> qshift;
     const unsigned sgrid = (unsigned)((nrows + rpb - 1) / rpb);

@@ -178,7 +178,7 @@ int launch_relu_requant_stage(const int32_t *acc, const int32_t *dev_max, const 
                               int32_t *dev_shift, hipStream_t s) {
     int32_t *xs = (int32_t *)((char *)ws + conv2d_xs_offset(g));
     int qshift = 0;
-    while ((1 << qshift) < g.nq && qshift < 8) ++qshift;   // up to 256 threads per row
+    while ((1 << qshift) * 5 < 2 * g.nq && qshift < 8) ++qshift;   // ~2.5 words per thread, as the spread
     const int64_t nrows = (int64_t)g.N * g.C * g.Hp;
     const int rpb = kBlock >> qshift;
     hipLaunchKernelGGL(relu_requant_stage_kernel, dim3((unsigned)((nrows + rpb - 1) / rpb)), dim3(kBlock), 0, s, acc,
