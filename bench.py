@@ -7,10 +7,12 @@ activations x signed b-bit weights (seeded synthetic values), swept over b = 1..
 One step = one pass of the whole hot path at every bit width: pack the uint8
 activations into b-bit words, spread them into operand words (stage), multiply,
 accumulate, decode and store (accumulate).  Each layer's kernel words are prepared once,
-before timing, as weights are constant.  `value` is the whole sweep's throughput (all
-MACs of the 8 layers / wall time of the step) in GMAC/s, with the step replayed from a
-captured HIP graph; `eager_ms_per_step` is the same step launched kernel by kernel from
-Python.  Per bit width the line also reports each kernel's own duration (HIP events
+before timing, as weights are constant, and each layer's plan is tuned at set-up.  The
+8 layers are independent, so the step runs them round-robin on 4 side streams (default
+priority) that fork from and join the launching stream.  `value` is the whole sweep's
+throughput (all MACs of the 8 layers / wall time of the step) in GMAC/s, with the step
+replayed from a captured HIP graph; `eager_ms_per_step` is the same step launched
+kernel by kernel from Python.  Per bit width the line also reports each kernel's own duration (HIP events
 around a graph of back-to-back launches of that kernel alone), the
 native-int8 matrix-core baseline on the same layer, their speedup, and the roofline
 fractions; the CPU oracle is timed on the host.
@@ -45,6 +47,9 @@ def parse():
     p.add_argument("--no-tune", action="store_true",
                    help="use the planner's model plans (default: time the top candidates at set-up)")
     p.add_argument("--tune-candidates", type=int, default=16, help="candidate plans timed per bit width")
+    p.add_argument("--streams", type=int, default=4,
+                   help="streams the step's independent bit widths are spread over (round-robin; every stream "
+                        "at the default priority)")
     p.add_argument("--plans-out", metavar="FILE", help="write the plans used per bit width (JSON)")
     p.add_argument("--plans-in", metavar="FILE",
                    help="use the plans of a --plans-out file instead of tuning (profiled runs replay the plans "
@@ -590,10 +595,27 @@ def main():
         print(f"counters: copy of {COPY_BYTES} bytes done; kernel sources {kernel_source_sha()}", flush=True)
         return
 
+    # The bit widths are independent layers (own inputs, workspaces and outputs): with
+    # --streams S > 1 they run round-robin on S side streams that fork from and join the
+    # launching stream, so one width's pack and stage and the ramp and drain of its
+    # accumulate overlap another's.  Every kernel still runs once per step.
+    side = [torch.cuda.Stream() for _ in range(args.streams)] if args.streams > 1 else []
+
     def step():
-        for L in layers:
-            samd.pack(L["x"], L["b"], False, out=L["xp"])
-            samd.conv2d_prepared(L["xp"], L["xf"], L["wf"], shape, L["ws"], out=L["y"])
+        if not side:
+            for L in layers:
+                samd.pack(L["x"], L["b"], False, out=L["xp"])
+                samd.conv2d_prepared(L["xp"], L["xf"], L["wf"], shape, L["ws"], out=L["y"])
+            return
+        main = torch.cuda.current_stream()
+        for st in side:
+            st.wait_stream(main)
+        for i, L in enumerate(layers):
+            with torch.cuda.stream(side[i % len(side)]):
+                samd.pack(L["x"], L["b"], False, out=L["xp"])
+                samd.conv2d_prepared(L["xp"], L["xf"], L["wf"], shape, L["ws"], out=L["y"])
+        for st in side:
+            main.wait_stream(st)
 
     capture = capture_graph
 
@@ -617,6 +639,9 @@ def main():
         step_graph.replay()
     torch.cuda.synchronize()
     ms_per_step = (time.perf_counter() - t0) * 1e3 / args.steps
+    # the outputs of the timed steps themselves, for the parity check below
+    for L in layers:
+        L["y_step"] = L["y"].clone()
 
     def timed(fn, reps):
         return timed_graph(fn, reps, args.kernel_warm_s)
@@ -639,8 +664,10 @@ def main():
         for L in layers:
             want = ref.conv2d_points(L["case"].x, L["case"].w, shape.as_tuple(), idx)
             got = L["y"].cpu().numpy()[tuple(idx.T)]
+            got_step = L["y_step"].cpu().numpy()[tuple(idx.T)]
             got8 = L["y8"].cpu().numpy()[tuple(idx.T)]
-            parity[L["b"]] = bool(np.array_equal(got, want) and np.array_equal(got8, want))
+            parity[L["b"]] = bool(np.array_equal(got, want) and np.array_equal(got_step, want) and
+                                  np.array_equal(got8, want))
 
     traffic = stored_traffic()
     per_bits, tot_mads, tot_conv_s, tot_alg_bytes = {}, 0.0, 0.0, 0.0
@@ -702,9 +729,10 @@ def main():
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "int64", "data": "synthetic",
         "config": {"workload": "conv2d 8x128x56x56 -> 128, 3x3, stride 1, pad 1; unsigned b-bit activations x "
-                               "signed b-bit weights; one step = pack + stage + accumulate at each b (kernel words prepared once per layer)",
+                               "signed b-bit weights; one step = pack + stage + accumulate at each b (kernel words prepared once per layer; the 8 independent layers spread over side streams)",
                    "plans": (f"from {os.path.basename(args.plans_in)}" if args.plans_in else "model" if args.no_tune
                              else f"tuned at set-up ({args.tune_candidates} candidates timed)"),
+                   "streams": args.streams,
                    "bits": bits_list, "global_batch": N, "macs_per_layer": macs},
         "roofline": {"bound": "alu", "achieved": round(achieved / 1e12, 3), "peak": round(PEAK_VALU_OPS / 1e12, 2),
                      "unit": "TOP/s", "frac": round(achieved / PEAK_VALU_OPS, 4),
