@@ -68,6 +68,9 @@ def parse():
                         "the 2^20-value conv1d (b = 1..8, 3 and 5 taps) and the extremes-heavy signed layer")
     p.add_argument("--lanewise", action="store_true",
                    help="instead of the default workload, time lane-wise add/sub/mul/scale on packed words (GB/s)")
+    p.add_argument("--valu-summary", metavar="PMC_DIR",
+                   help="print the VALU / texture-path counter table of a --counters run profiled with "
+                        "rocprofv3 --pmc " + VALU_COUNTERS)
     p.add_argument("--trace-summary", metavar="TRACE_DIR",
                    help="print markdown tables of a rocprofv3 --kernel-trace --stats output folder (csv) and exit")
     p.add_argument("--traffic-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
@@ -106,6 +109,55 @@ def read_counter_csv(folder, counter):
                 name, v = out.get(d, (row["Kernel_Name"], 0.0))
                 out[d] = (name, v + float(row["Counter_Value"]))
     return out
+
+
+VALU_COUNTERS = ("SQ_INSTS_VALU SQ_ACTIVE_INST_VALU SQ_INSTS_VMEM_RD SQ_INSTS_LDS SQ_INSTS_SALU SQ_WAIT_INST_ANY "
+                 "SQ_WAVE_CYCLES SQ_BUSY_CYCLES TA_TA_BUSY_sum TD_TD_BUSY_sum GRBM_GUI_ACTIVE")
+
+
+def valu_summary(folder, bits_list, plans_file=None):
+    """Markdown table of one `rocprofv3 --pmc <VALU_COUNTERS>` pass over `bench.py --counters`:
+    per bit width, the SAMD conv kernel's dispatch duration, VALU instructions, VALU issue
+    utilisation (4 clocks per wave-wide VALU instruction on a SIMD16, over 1024 SIMDs and
+    the dispatch's duration at 2.4 GHz), the share of multiply-adds among them, and the
+    texture-path (TA/TD) busy fractions over the 256 compute units."""
+    import csv
+    import glob
+
+    import paper_1809_10572_amd as samd
+    import samd_workloads as wl
+
+    files = glob.glob(os.path.join(folder, "**", "*counter_collection.csv"), recursive=True)
+    if len(files) != 1:
+        raise SystemExit(f"expected one counter_collection.csv under {folder}, found {len(files)}")
+    disp = {}
+    for row in csv.DictReader(open(files[0])):
+        d = disp.setdefault(int(row["Dispatch_Id"]), {"name": row["Kernel_Name"], "c": {}})
+        d["c"][row["Counter_Name"]] = d["c"].get(row["Counter_Name"], 0.0) + float(row["Counter_Value"])
+        d["dur"] = (int(row["End_Timestamp"]) - int(row["Start_Timestamp"])) * 1e-9
+    conv = [disp[k] for k in sorted(disp) if "conv2d_samd_kernel" in disp[k]["name"]]
+    if len(conv) != len(bits_list):
+        raise SystemExit(f"{len(conv)} conv dispatches for bits {bits_list}")
+    plans = json.load(open(plans_file)) if plans_file else None
+    shape = wl.MID
+    out = ["| b | dispatch µs | VALU wave-instructions | VALU issue % | multiply-adds % of VALU | "
+           "multiply-adds % of VALU peak | VMEM reads | LDS instructions | TA busy % | TD busy % |",
+           "|---|---|---|---|---|---|---|---|---|---|"]
+    for b, d in zip(bits_list, conv):
+        xf, wf = samd.Fmt(b, False), samd.Fmt(b, True)
+        if plans:
+            samd.conv2d_use_plan(shape, xf, wf, plans[str(b)])
+        p = samd.conv2d_plan(shape, xf, wf)
+        Ho, _ = samd.out_hw(shape)
+        mads = shape.N * shape.M * Ho * p.words_per_row * shape.C * shape.KH * p.tap_words
+        c, dur = d["c"], d["dur"]
+        cycles = dur * 2.4e9
+        valu = c["SQ_INSTS_VALU"]
+        out.append(f"| {b} | {dur * 1e6:.1f} | {valu:.4g} | {100 * valu * 4 / (1024 * cycles):.0f} | "
+                   f"{100 * mads / 64 / valu:.0f} | {100 * mads / dur / PEAK_VALU_OPS:.0f} | "
+                   f"{c['SQ_INSTS_VMEM_RD']:.4g} | {c['SQ_INSTS_LDS']:.4g} | "
+                   f"{100 * c['TA_TA_BUSY_sum'] / (256 * cycles):.0f} | {100 * c['TD_TD_BUSY_sum'] / (256 * cycles):.0f} |")
+    return "\n".join(out)
 
 
 def traffic_summary(fetch_dir, write_dir, bits_list):
@@ -516,6 +568,9 @@ def main():
         return
     if args.trace_summary:
         print(trace_summary(args.trace_summary))
+        return
+    if args.valu_summary:
+        print(valu_summary(args.valu_summary, [int(b) for b in args.bits.split(",")], args.plans_in))
         return
     if args.traffic_summary:
         print(json.dumps(traffic_summary(*args.traffic_summary, [int(b) for b in args.bits.split(",")]), indent=1))
