@@ -731,6 +731,7 @@ def main():
         p = L["plan"]
         mads = N * M * Ho * p.words_per_row * C * KH * p.tap_words
         b = L["b"]
+        packed_bytes = N * C * H * samd.row_words(W, b) * 4
         # operand words and kernel words read once, int32 outputs written once
         hbm_bytes = (N * C * samd_hp * p.tap_words * p.words_per_row * 4 + M * C * KH * p.tap_words * 4
                      + N * M * Ho * Wo * 4)
@@ -740,6 +741,11 @@ def main():
         per_bits[str(b)] = {
             "conv_us": round(t * 1e6, 2), "stage_us": round(L["t_stage"] * 1e6, 2),
             "pack_us": round(L["t_pack"] * 1e6, 2),
+            # packed data: pack reads 1 B per value and writes the packed words; the stage
+            # reads the packed words and writes the operand words
+            "pack_gbps": round((N * C * H * W + packed_bytes) / L["t_pack"] / 1e9, 1),
+            "stage_gbps": round((packed_bytes + N * C * samd_hp * p.tap_words * p.words_per_row * 4) / L["t_stage"]
+                                / 1e9, 1),
             "gmacs": round(macs / t / 1e9, 1),
             "gmacs_with_stage": round(macs / (t + L["t_stage"]) / 1e9, 1),
             "int8_us": round(t8 * 1e6, 2), "int8_gmacs": round(macs / t8 / 1e9, 1),
