@@ -560,10 +560,12 @@ int samd_conv2d_tune(const uint32_t *x, samd_fmt xf, const uint32_t *w, samd_fmt
     if (st) return fail(st, "%s", err.c_str());
     // the candidates whose workspace fits next to the second output and its counter
     const size_t extra = tune_extra_bytes(*d, cands[0]);
-    if (ws_bytes < extra + conv2d_workspace_bytes(cands[0]))
+    if (ws_bytes < extra + conv2d_workspace_bytes(cands[0]))   // workspace sizes are multiples of 256
         return fail(SAMD_ENOSPC, "workspace %zu bytes < %zu needed for the model's plan", ws_bytes,
                     extra + conv2d_workspace_bytes(cands[0]));
-    const size_t room = ws_bytes - extra;
+    // candidates' workspaces below, the second output and its counter above a 256-byte
+    // aligned boundary (the caller's size need not be a multiple of anything)
+    const size_t room = (ws_bytes - extra) / 256 * 256;
     std::vector<Conv2dGeom> fit;
     for (const Conv2dGeom &c : cands)
         if (conv2d_workspace_bytes(c) <= room) fit.push_back(c);
