@@ -409,11 +409,13 @@ int conv2d_candidates(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, int m
 int find_conv2d_candidate(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf,
                           const std::function<bool(const Conv2dGeom &)> &match, Conv2dGeom &out,
                           std::string &err) {
+    // every priced candidate, unsorted (matching needs no ranking)
+    Conv2dGeom model;
     std::vector<Conv2dGeom> all;
-    int st = conv2d_candidates(d, xf, wf, std::numeric_limits<int>::max(), all, err);
+    int st = search_conv2d(d, xf, wf, model, err, &all);
     if (st) return st;
     for (const Conv2dGeom &c : all)
-        if (match(c)) {
+        if (addressable(d, c) && match(c)) {
             out = c;
             return SAMD_OK;
         }
