@@ -544,3 +544,74 @@ def test_conv2d_tune_output_and_prepared_workspace():
             np.testing.assert_array_equal(y2.cpu().numpy(), want)
         finally:
             samd.conv2d_untune(None)
+
+
+# --- seeded random shapes --------------------------------------------------------------
+
+def random_cases(n, seed, wmax=300, cmax=70, hmax=40):
+    """Seeded conv2d shapes and format pairs within the library's limits: kernels 1..7
+    (stride 1..3, padding up to the kernel), rows up to wmax values, channels up to cmax."""
+    rng = np.random.default_rng(seed)
+    out = []
+    while len(out) < n:
+        KH, KW = int(rng.integers(1, 8)), int(rng.integers(1, 8))
+        sh, sw = int(rng.integers(1, 4)), int(rng.integers(1, 4))
+        ph, pw = int(rng.integers(0, KH)), int(rng.integers(0, KW))
+        H, W = int(rng.integers(max(1, KH - 2 * ph), hmax)), int(rng.integers(max(1, KW - 2 * pw), wmax + 1))
+        N, C, M = int(rng.integers(1, 4)), int(rng.integers(1, cmax + 1)), int(rng.integers(1, 41))
+        xb, wb = int(rng.integers(1, 9)), int(rng.integers(1, 9))
+        xs, ws = bool(rng.integers(0, 2)), bool(rng.integers(0, 2))
+        if C * KH * KW * (1 << xb) * (1 << wb) >= (1 << 31):
+            continue
+        out.append(((N, C, H, W, M, KH, KW, sh, sw, ph, pw), xb, xs, wb, ws))
+    return out
+
+
+# the second set: wide rows (many column segments), fewer channels and rows
+RANDOM_CASES = random_cases(40, 1809) + random_cases(24, 2024, wmax=1200, cmax=24, hmax=12)
+
+
+@pytest.mark.parametrize("case", range(24))
+def test_conv1d_random(case):
+    rng = np.random.default_rng(4000 + case)
+    bits = int(rng.integers(1, 9))
+    K = int(rng.integers(1, 17))
+    n = int(rng.integers(K, 300001))
+    x = wl.uniform(rng, (n,), bits, False)
+    k = wl.uniform(rng, (K,), bits, False)
+    words, _ = ref.pack(x, bits, False)
+    try:
+        y = samd.conv1d(gpu_words(words), n, bits, k.tolist(), bits)
+    except samd.SamdError as e:
+        assert e.status == -3, str(e)      # refused, never computed wrongly
+        return
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(y.cpu().numpy(), ref.conv1d(x, k), err_msg=f"n={n} K={K} b={bits}")
+
+
+@pytest.mark.parametrize("case", range(len(RANDOM_CASES)))
+def test_conv2d_random_shapes(case):
+    shape, xb, xs, wb, ws = RANDOM_CASES[case]
+    N, C, H, W, M, KH, KW = shape[:7]
+    rng = np.random.default_rng(3000 + case)
+    x = wl.uniform(rng, (N, C, H, W), xb, xs)
+    w = wl.uniform(rng, (M, C, KH, KW), wb, ws)
+    xf, wf = samd.Fmt(xb, xs), samd.Fmt(wb, ws)
+    want = ref.conv2d(x, w, shape)
+    try:
+        got = run_conv2d(x, w, shape, xf, wf)
+    except samd.SamdError as e:
+        # shapes without an exact lane geometry are refused, never computed wrongly
+        assert e.status == -3, str(e)
+        return
+    np.testing.assert_array_equal(got, want, err_msg=f"{shape} x{xb}{'s' if xs else 'u'} w{wb}{'s' if ws else 'u'}")
+    if case % 4 == 0:
+        xp = samd.pack(gpu_vals(x, xs), xb, xs)
+        wp = samd.pack(gpu_vals(w, ws), wb, ws)
+        try:
+            samd.conv2d_tune(xp, xf, wp, wf, shape, candidates=6, reps=1)
+            y = samd.conv2d(xp, xf, wp, wf, shape)
+            torch.cuda.synchronize()
+            np.testing.assert_array_equal(y.cpu().numpy(), want)
+        finally:
+            samd.conv2d_untune(shape, xf, wf)
