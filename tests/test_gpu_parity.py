@@ -615,3 +615,54 @@ def test_conv2d_random_shapes(case):
             np.testing.assert_array_equal(y.cpu().numpy(), want)
         finally:
             samd.conv2d_untune(shape, xf, wf)
+
+
+def random_epilogue_cases(n, seed):
+    """Seeded (accumulator shape, next layer) pairs: the next layer's input is the
+    accumulator (C = its channels, H x W = its size), any kernel 1..5, stride 1..2."""
+    rng = np.random.default_rng(seed)
+    out = []
+    while len(out) < n:
+        N, C = int(rng.integers(1, 3)), int(rng.integers(1, 40))
+        H, W = int(rng.integers(3, 20)), int(rng.integers(3, 400))
+        KH, KW = int(rng.integers(1, 6)), int(rng.integers(1, 6))
+        sh, sw = int(rng.integers(1, 3)), int(rng.integers(1, 3))
+        ph, pw = int(rng.integers(0, KH)), int(rng.integers(0, KW))
+        if H + 2 * ph < KH or W + 2 * pw < KW:
+            continue
+        bits = int(rng.integers(1, 9))
+        out.append(((N, C, H, W, int(rng.integers(1, 24)), KH, KW, sh, sw, ph, pw), bits))
+    return out
+
+
+EPILOGUE_CASES = random_epilogue_cases(16, 77)
+
+
+@pytest.mark.parametrize("case", range(len(EPILOGUE_CASES)))
+def test_fused_epilogue_random(case):
+    """ReLU + requantisation written into the next layer's operand words, under the
+    model's plan and under a tuned one, gives that layer's oracle result."""
+    shape, bits = EPILOGUE_CASES[case]
+    N, C, H, W, M, KH, KW = shape[:7]
+    rng = np.random.default_rng(5000 + case)
+    acc = rng.integers(-(1 << 20), 1 << 20, size=(N, C, H, W), dtype=np.int64).astype(np.int32)
+    w = wl.uniform(rng, (M, C, KH, KW), bits, True)
+    xf, wf = samd.Fmt(bits, False), samd.Fmt(bits, True)
+    shift = ref.requant_shift(acc, bits)
+    want = ref.conv2d(ref.relu_requant(acc, shift, bits), w, shape)
+    acc_d = torch.from_numpy(acc).to(DEV)
+    wp = samd.pack(gpu_vals(w, True), bits, True)
+    try:
+        for plan in (["model", "tuned"] if case % 2 == 0 else ["model"]):
+            if plan == "tuned":
+                xp = samd.pack(gpu_vals(ref.relu_requant(acc, shift, bits), False), bits, False)
+                samd.conv2d_tune(xp, xf, wp, wf, shape, candidates=6, reps=1)
+            ws = samd.conv2d_prepare(wp, wf, shape, xf)
+            sh = torch.zeros(1, dtype=torch.int32, device=DEV)
+            samd.relu_requant_stage(acc_d, samd.max_i32(acc_d), bits, wf, shape, ws, dev_shift=sh)
+            y = samd.conv2d_accumulate(xf, wf, shape, ws)
+            torch.cuda.synchronize()
+            assert int(sh.item()) == shift
+            np.testing.assert_array_equal(y.cpu().numpy(), want, err_msg=f"{shape} b={bits} {plan} plan")
+    finally:
+        samd.conv2d_untune(shape, xf, wf)
