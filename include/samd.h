@@ -219,8 +219,8 @@ int samd_conv2d_tune_workspace(const samd_conv2d_desc *d, samd_fmt xf, samd_fmt 
 
 /* Times the first `candidates` candidate plans on the caller's x and w (stage +
  * accumulate, `reps` times each, HIP events on `stream`; after 4 x reps untimed runs of
- * the planner's plan to bring the clocks up, two rounds over all candidates, each keeping
- * its faster round) and makes the fastest the plan of (xf, wf, *d) for every later call
+ * the planner's plan to bring the clocks up, two passes over all candidates, each keeping
+ * its faster pass) and makes the fastest the plan of (xf, wf, *d) for every later call
  * in this process, until samd_conv2d_untune.  A candidate must beat the best so far by
  * 2 % (near-ties keep the higher-ranked plan, so repeated tuning settles on one plan).
  *   x, w, y as for samd_conv2d (y receives the convolution)

@@ -586,10 +586,10 @@ int samd_conv2d_tune(const uint32_t *x, samd_fmt xf, const uint32_t *w, samd_fmt
     if (he == hipSuccess) he = hipEventCreate(&e1);
     if (he != hipSuccess) return cleanup(hip_fail(he, "hipEventCreate"));
 
-    // Round 0 prepares each candidate, checks its result and times it; round 1 times every
-    // candidate again (each keeps its faster time), so that clock ramps and other
-    // transients do not decide.  Before round 0 the model's plan runs untimed for a while
-    // to bring the clocks up.
+    // The first pass prepares each candidate, checks its result and times it; the second
+    // times every candidate again (each keeps its faster time), so that clock ramps and
+    // other transients do not decide.  Before the first pass the model's plan runs untimed
+    // for a while to bring the clocks up.
     auto run = [&](const Conv2dGeom &c, int32_t *out, int n) {
         int rs = SAMD_OK;
         for (int r = 0; r < n && !rs; ++r)
@@ -607,13 +607,13 @@ int samd_conv2d_tune(const uint32_t *x, samd_fmt xf, const uint32_t *w, samd_fmt
         return e == hipSuccess ? SAMD_OK : hip_fail(e, "timing");
     };
     std::vector<float> best_of(fit.size(), 0.0f);
-    for (int round = 0; round < 2; ++round) {
+    for (int pass = 0; pass < 2; ++pass) {
         for (size_t i = 0; i < fit.size(); ++i) {
             const Conv2dGeom &c = fit[i];
             int32_t *out = i == 0 ? y : y_alt;   // the model's plan writes the reference into y
             if ((st = launch_conv2d_prepare(w, c, ws, stream)) || (st = run(c, out, 1))) return cleanup(st);
-            if (round == 0 && i == 0 && (st = run(c, out, 4 * reps))) return cleanup(st);
-            if (round == 0 && i > 0) {
+            if (pass == 0 && i == 0 && (st = run(c, out, 4 * reps))) return cleanup(st);
+            if (pass == 0 && i > 0) {
                 // every candidate must reproduce the model plan's result exactly
                 if ((st = launch_count_mismatch(y, y_alt, ny, mismatches, stream))) return cleanup(st);
                 int32_t host = -1;
@@ -627,7 +627,7 @@ int samd_conv2d_tune(const uint32_t *x, samd_fmt xf, const uint32_t *w, samd_fmt
             }
             float ms = 0.0f;
             if ((st = timed(c, out, ms))) return cleanup(st);
-            best_of[i] = round == 0 ? ms : std::min(best_of[i], ms);
+            best_of[i] = pass == 0 ? ms : std::min(best_of[i], ms);
         }
     }
     // a candidate must beat the best so far by 2 %: near-ties keep the higher-ranked plan,

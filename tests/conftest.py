@@ -14,8 +14,8 @@ def pytest_configure(config):
 
 
 def pytest_collection_modifyitems(config, items):
-    # GPU tests are skipped, not failed, where no GPU is visible; the driver selects
-    # them explicitly with -m gpu on the GPU machine.
+    # GPU tests are skipped, not failed, where no GPU is visible; select them with -m gpu
+    # on a machine with a GPU.
     try:
         import torch
         have_gpu = torch.cuda.is_available()
