@@ -48,8 +48,11 @@ def parse():
                    help="use the planner's model plans (default: time the top candidates at set-up)")
     p.add_argument("--tune-candidates", type=int, default=16, help="candidate plans timed per bit width")
     p.add_argument("--streams", type=int, default=4,
-                   help="streams the step's independent bit widths are spread over (round-robin; every stream "
-                        "at the default priority)")
+                   help="streams the step's independent bit widths are spread over (every stream at the "
+                        "default priority)")
+    p.add_argument("--stream-order", choices=("snake", "round-robin"), default="snake",
+                   help="how bit widths map to streams: snake pairs the smallest width with the largest "
+                        "(1+8, 2+7, ...: balanced work per stream), round-robin takes them in order")
     p.add_argument("--plans-out", metavar="FILE", help="write the plans used per bit width (JSON)")
     p.add_argument("--plans-in", metavar="FILE",
                    help="use the plans of a --plans-out file instead of tuning (profiled runs replay the plans "
@@ -655,6 +658,14 @@ def main():
     # launching stream, so one width's pack and stage and the ramp and drain of its
     # accumulate overlap another's.  Every kernel still runs once per step.
     side = [torch.cuda.Stream() for _ in range(args.streams)] if args.streams > 1 else []
+    # layer i's stream: in order of bit width, 0, 1, .., S-1, then S-1, .., 0 (snake) or
+    # 0, 1, .., S-1 again (round-robin)
+    S = max(1, args.streams)
+    by_bits = sorted(range(len(layers)), key=lambda i: layers[i]["b"])
+    stream_of = [0] * len(layers)
+    for r, i in enumerate(by_bits):
+        k, lap = r % S, r // S
+        stream_of[i] = (S - 1 - k) if (args.stream_order == "snake" and lap % 2 == 1) else k
 
     def step():
         if not side:
@@ -666,7 +677,7 @@ def main():
         for st in side:
             st.wait_stream(main)
         for i, L in enumerate(layers):
-            with torch.cuda.stream(side[i % len(side)]):
+            with torch.cuda.stream(side[stream_of[i]]):
                 samd.pack(L["x"], L["b"], False, out=L["xp"])
                 samd.conv2d_prepared(L["xp"], L["xf"], L["wf"], shape, L["ws"], out=L["y"])
         for st in side:
@@ -793,7 +804,7 @@ def main():
                                "signed b-bit weights; one step = pack + stage + accumulate at each b (kernel words prepared once per layer; the 8 independent layers spread over side streams)",
                    "plans": (f"from {os.path.basename(args.plans_in)}" if args.plans_in else "model" if args.no_tune
                              else f"tuned at set-up ({args.tune_candidates} candidates timed)"),
-                   "streams": args.streams,
+                   "streams": args.streams, "stream_order": args.stream_order,
                    "bits": bits_list, "global_batch": N, "macs_per_layer": macs},
         "roofline": {"bound": "alu", "achieved": round(achieved / 1e12, 3), "peak": round(PEAK_VALU_OPS / 1e12, 2),
                      "unit": "TOP/s", "frac": round(achieved / PEAK_VALU_OPS, 4),
