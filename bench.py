@@ -122,8 +122,9 @@ def valu_summary(folder, bits_list, plans_file=None):
     """Markdown table of one `rocprofv3 --pmc <VALU_COUNTERS>` pass over `bench.py --counters`:
     per bit width, the SAMD conv kernel's dispatch duration, VALU instructions, VALU issue
     utilisation (4 clocks per wave-wide VALU instruction on a SIMD16, over 1024 SIMDs and
-    the dispatch's duration at 2.4 GHz), the share of multiply-adds among them, and the
-    texture-path (TA/TD) busy fractions over the 256 compute units."""
+    the dispatch's duration at 2.4 GHz), the share of multiply-adds among them, the
+    method's efficiency (direct MACs per VALU lane-operation, every VALU instruction
+    counted), and the texture-path (TA/TD) busy fractions over the 256 compute units."""
     import csv
     import glob
 
@@ -144,8 +145,9 @@ def valu_summary(folder, bits_list, plans_file=None):
     plans = json.load(open(plans_file)) if plans_file else None
     shape = wl.MID
     out = ["| b | dispatch µs | VALU wave-instructions | VALU issue % | multiply-adds % of VALU | "
-           "multiply-adds % of VALU peak | VMEM reads | LDS instructions | TA busy % | TD busy % |",
-           "|---|---|---|---|---|---|---|---|---|---|"]
+           "multiply-adds % of VALU peak | MACs per VALU lane-op | VMEM reads | LDS instructions | TA busy % | "
+           "TD busy % |",
+           "|---|---|---|---|---|---|---|---|---|---|---|"]
     for b, d in zip(bits_list, conv):
         xf, wf = samd.Fmt(b, False), samd.Fmt(b, True)
         if plans:
@@ -153,11 +155,12 @@ def valu_summary(folder, bits_list, plans_file=None):
         p = samd.conv2d_plan(shape, xf, wf)
         Ho, _ = samd.out_hw(shape)
         mads = shape.N * shape.M * Ho * p.words_per_row * shape.C * shape.KH * p.tap_words
+        macs = shape.N * shape.M * Ho * samd.out_hw(shape)[1] * shape.C * shape.KH * shape.KW
         c, dur = d["c"], d["dur"]
         cycles = dur * 2.4e9
         valu = c["SQ_INSTS_VALU"]
         out.append(f"| {b} | {dur * 1e6:.1f} | {valu:.4g} | {100 * valu * 4 / (1024 * cycles):.0f} | "
-                   f"{100 * mads / 64 / valu:.0f} | {100 * mads / dur / PEAK_VALU_OPS:.0f} | "
+                   f"{100 * mads / 64 / valu:.0f} | {100 * mads / dur / PEAK_VALU_OPS:.0f} | {macs / (64 * valu):.2f} | "
                    f"{c['SQ_INSTS_VMEM_RD']:.4g} | {c['SQ_INSTS_LDS']:.4g} | "
                    f"{100 * c['TA_TA_BUSY_sum'] / (256 * cycles):.0f} | {100 * c['TD_TD_BUSY_sum'] / (256 * cycles):.0f} |")
     return "\n".join(out)
