@@ -5,11 +5,11 @@
 // group's taps in natural order, one per lane.  One 32x32 -> 64-bit multiply per group
 // gives lanes j = 0 .. I+K-2, lane j holding the partial full-convolution sum for output
 // q*I + j - (K - 1) (the "parallelogram" of Sec. 5.1).  An output's complete value is its
-// lane in word q plus the low lanes of the following words (overlap-add); each thread
-// recomputes those few following products instead of exchanging them.
+// lane in word q plus the low lanes of the following words (overlap-add).
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cstdint>
 
 #include "hip_util.hpp"
 
@@ -18,55 +18,8 @@ namespace samd {
 namespace {
 
 constexpr int kBlock = 256;
-constexpr int kMaxExtra = kMaxConv1dExtra;
 
-template <int B>
-__device__ inline uint32_t field(const uint32_t *__restrict__ x, int64_t n, int64_t u) {
-    constexpr int P = 32 / B;
-    if (u < 0 || u >= n) return 0u;
-    return (x[u / P] >> ((u % P) * B)) & ((1u << B) - 1);
-}
-
-template <int B>
-__global__ __launch_bounds__(kBlock) void conv1d_kernel(const uint32_t *__restrict__ x, int32_t *__restrict__ y,
-                                                        Conv1dGeom g) {
-    const int64_t q = (int64_t)blockIdx.x * kBlock + threadIdx.x;
-    if (q >= g.nwords) return;
-    const int I = g.I, L = g.L, K = g.K;
-    const int nl = g.nl;
-    uint64_t acc[kMaxExtra + 1];
-#pragma unroll
-    for (int e = 0; e <= kMaxExtra; ++e) {
-        acc[e] = 0;
-        if (e <= g.extra) {
-            const int64_t base = (q + e) * I;
-            for (int gi = 0; gi < g.ngroups; ++gi) {
-                uint32_t A = 0;
-                for (int i = 0; i < I; ++i) A |= field<B>(x, g.n, base + g.g_delta[gi] + i) << (i * L);
-                acc[e] += (uint64_t)A * g.g_word[gi];
-            }
-        }
-    }
-    const uint64_t lmask = (L >= 64) ? ~0ull : ((1ull << L) - 1);
-    const int64_t o0 = q * I;
-    for (int r = 0; r < I; ++r) {
-        const int64_t o = o0 + r;
-        if (o >= g.nout) break;
-        uint64_t sum = 0;
-#pragma unroll
-        for (int e = 0; e <= kMaxExtra; ++e) {
-            const int j = r + K - 1 - e * I;
-            if (e <= g.extra && j >= 0 && j < nl) {
-                const uint64_t v = acc[e] >> (j * L);
-                sum += (j == nl - 1) ? v : (v & lmask);
-            }
-        }
-        y[o] = (int32_t)sum;
-    }
-}
-
-// The same computation for inputs of at most 2^30 values, staged through LDS, with the
-// overlap-add done there.  A block of W = 256 threads owns output words q0 .. q0 + W - 1,
+// The computation is staged through LDS, with the overlap-add done there.  A block of W = 256 threads owns output words q0 .. q0 + W - 1,
 // i.e. outputs
 // q0 I .. q0 I + W I - 1; word q's lanes reach outputs q I - (K - 1) .. q I + I - 1, so
 // those outputs take lanes of words q0 .. q0 + W - 1 + extra.  The block
@@ -88,15 +41,14 @@ __global__ __launch_bounds__(kBlock) void conv1d_lds_kernel(const uint32_t *__re
     uint32_t *vals = sh;                              // nvals values
     uint32_t *outs = sh + sk(nvals);                  // nouts outputs; outs[sk(K - 1)] is output q0 I
     constexpr int P = 32 / B;
-    const int n = (int)g.n;
     const int I = g.I, L = g.L, K = g.K, nl = g.nl;
     const int W = blockDim.x;
-    const int q0 = blockIdx.x * W;
-    const int u0 = q0 * I + dmin;
+    const int64_t q0 = (int64_t)blockIdx.x * W;
+    const int64_t u0 = q0 * I + dmin;   // 64-bit: rows may hold more than 2^31 values
     for (int t = threadIdx.x; t < nvals; t += W) {
-        const int u = u0 + t;
+        const int64_t u = u0 + t;
         uint32_t f = 0;
-        if (u >= 0 && u < n) f = (x[(unsigned)u / P] >> (((unsigned)u % P) * B)) & ((1u << B) - 1);
+        if (u >= 0 && u < g.n) f = (x[(uint64_t)u / P] >> (((uint64_t)u % P) * B)) & ((1u << B) - 1);
         vals[sk(t)] = f;
     }
     for (int t = threadIdx.x; t < sk(nouts); t += W) outs[t] = 0;
@@ -120,7 +72,7 @@ __global__ __launch_bounds__(kBlock) void conv1d_lds_kernel(const uint32_t *__re
         atomicAdd(outs + sk(o + nl - 1), (uint32_t)p);
     }
     __syncthreads();
-    const int64_t o0 = (int64_t)q0 * I;
+    const int64_t o0 = q0 * I;
     for (int t = threadIdx.x; t < W * I; t += W) {
         const int64_t o = o0 + t;
         if (o < g.nout) y[o] = (int32_t)outs[sk(t + K - 1)];
@@ -130,35 +82,27 @@ __global__ __launch_bounds__(kBlock) void conv1d_lds_kernel(const uint32_t *__re
 }  // namespace
 
 int launch_conv1d(const uint32_t *x, const Conv1dGeom &g, int32_t *y, hipStream_t s) {
-    const int grid = (int)((g.nwords + kBlock - 1) / kBlock);
-    if (g.n <= ((int64_t)1 << 30)) {
-        // the values a block reads: words q0 .. q0 + kBlock - 1 + extra, each from offset
-        // delta_g of its window, I values per operand word
-        int dmin = 0, dmax = 0;
-        for (int gi = 0; gi < g.ngroups; ++gi) {
-            dmin = std::min(dmin, g.g_delta[gi]);
-            dmax = std::max(dmax, g.g_delta[gi]);
-        }
-        const int wpb = kBlock;
-        const int lgrid = grid;
-        const int nvals = (wpb + g.extra) * g.I + dmax - dmin;
-        // lanes of words 0 .. wpb + extra - 1 land at outs[w I + j], j < nl
-        const int nouts = std::max((wpb + g.extra - 1) * g.I + g.nl, wpb * g.I + g.K - 1);
-        const size_t shm = ((size_t)(nvals + (nvals >> 4) + 1) + (size_t)(nouts + (nouts >> 4) + 1)) * 4;
-#define SAMD_C1L_CASE(B)                                                                                   \
-    if (g.bits == B) {                                                                                     \
-        hipLaunchKernelGGL((conv1d_lds_kernel<B>), dim3(lgrid), dim3(wpb), shm, s, x, y, g, dmin, nvals,    \
-                           nouts);                                                                         \
-        return check_launch("conv1d");                                                                     \
+    const int64_t grid = (g.nwords + kBlock - 1) / kBlock;
+    if (grid > INT32_MAX) {
+        set_error("conv1d: row too long");
+        return SAMD_EUNSUPPORTED;
     }
-        SAMD_C1L_CASE(1) SAMD_C1L_CASE(2) SAMD_C1L_CASE(3) SAMD_C1L_CASE(4)
-        SAMD_C1L_CASE(5) SAMD_C1L_CASE(6) SAMD_C1L_CASE(7) SAMD_C1L_CASE(8)
-#undef SAMD_C1L_CASE
+    // the values a block reads: words q0 .. q0 + kBlock - 1 + extra, each from offset
+    // delta_g of its window, I values per operand word
+    int dmin = 0, dmax = 0;
+    for (int gi = 0; gi < g.ngroups; ++gi) {
+        dmin = std::min(dmin, g.g_delta[gi]);
+        dmax = std::max(dmax, g.g_delta[gi]);
     }
-#define SAMD_C1_CASE(B)                                                                                  \
-    if (g.bits == B) {                                                                                   \
-        hipLaunchKernelGGL((conv1d_kernel<B>), dim3(grid), dim3(kBlock), 0, s, x, y, g);                \
-        return check_launch("conv1d");                                                                   \
+    const int nvals = (kBlock + g.extra) * g.I + dmax - dmin;
+    // lanes of words 0 .. kBlock + extra - 1 land at outs[w I + j], j < nl
+    const int nouts = std::max((kBlock + g.extra - 1) * g.I + g.nl, kBlock * g.I + g.K - 1);
+    const size_t shm = ((size_t)(nvals + (nvals >> 4) + 1) + (size_t)(nouts + (nouts >> 4) + 1)) * 4;
+#define SAMD_C1_CASE(B)                                                                                   \
+    if (g.bits == B) {                                                                                    \
+        hipLaunchKernelGGL((conv1d_lds_kernel<B>), dim3((unsigned)grid), dim3(kBlock), shm, s, x, y, g, dmin, \
+                           nvals, nouts);                                                                 \
+        return check_launch("conv1d");                                                                    \
     }
     SAMD_C1_CASE(1) SAMD_C1_CASE(2) SAMD_C1_CASE(3) SAMD_C1_CASE(4)
     SAMD_C1_CASE(5) SAMD_C1_CASE(6) SAMD_C1_CASE(7) SAMD_C1_CASE(8)
