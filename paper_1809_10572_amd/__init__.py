@@ -139,8 +139,12 @@ def _stream(t: torch.Tensor) -> int:
     return torch.cuda.current_stream(t.device).cuda_stream
 
 
+def _on_gpu(t: torch.Tensor) -> bool:
+    return t.is_cuda
+
+
 def _dev(t: torch.Tensor, dtype=None, name="tensor") -> torch.Tensor:
-    if not t.is_cuda:
+    if not isinstance(t, torch.Tensor) or not _on_gpu(t):
         raise ValueError(f"{name} must be a GPU tensor")
     if dtype is not None and t.dtype not in (dtype if isinstance(dtype, tuple) else (dtype,)):
         raise ValueError(f"{name} must have dtype {dtype}, got {t.dtype}")
@@ -154,6 +158,36 @@ def _out(t: torch.Tensor, numel: int) -> torch.Tensor:
     if t.numel() != numel:
         raise ValueError(f"out must hold {numel} int32 values, got {t.numel()}")
     return t
+
+
+# The library cannot see how large a device buffer is: every tensor handed to it is
+# checked here, so that a short or host-side tensor raises instead of being read or
+# written past its end by a kernel.
+def _min(t: torch.Tensor, dtype, numel: int, name: str) -> torch.Tensor:
+    _dev(t, dtype, name)
+    if t.numel() < numel:
+        raise ValueError(f"{name} must hold at least {numel} {t.dtype} values, got {t.numel()}")
+    return t
+
+
+def _opt(t: Optional[torch.Tensor], name: str) -> Optional[int]:
+    """Pointer of an optional one-value int32 device tensor (None stays NULL)."""
+    return None if t is None else _min(t, torch.int32, 1, name).data_ptr()
+
+
+def _ws_bytes(ws: torch.Tensor) -> int:
+    _dev(ws, None, "ws")
+    return ws.numel() * ws.element_size()
+
+
+def _x_words(xp: torch.Tensor, shape, xfmt: Fmt, name: str = "xp") -> torch.Tensor:
+    d = Conv2dDesc.of(shape)
+    return _min(xp, torch.int32, d.N * d.C * d.H * row_words(d.W, xfmt.bits), name)
+
+
+def _w_words(wp: torch.Tensor, shape, wfmt: Fmt, name: str = "wp") -> torch.Tensor:
+    d = Conv2dDesc.of(shape)
+    return _min(wp, torch.int32, d.M * d.C * d.KH * row_words(d.KW, wfmt.bits), name)
 
 
 def out_hw(shape) -> Tuple[int, int]:
@@ -177,15 +211,17 @@ def pack(values: torch.Tensor, bits: int, signed: bool, oor: Optional[torch.Tens
     shape = values.shape[:-1] + (row_words(length, bits),)
     if out is None:
         out = torch.empty(shape, dtype=torch.int32, device=values.device)
-    elif out.dtype != torch.int32 or tuple(out.shape) != tuple(shape) or not out.is_contiguous():
+    elif _dev(out, torch.int32, "out").shape != shape:
         raise ValueError(f"out must be a contiguous int32 tensor of shape {tuple(shape)}")
-    _check(lib().samd_pack(values.data_ptr(), rows, length, Fmt(bits, signed), out.data_ptr(),
-                           oor.data_ptr() if oor is not None else None, _stream(values)))
+    _check(lib().samd_pack(values.data_ptr(), rows, length, Fmt(bits, signed), out.data_ptr(), _opt(oor, "oor"),
+                           _stream(values)))
     return out
 
 
 def unpack(words: torch.Tensor, length: int, bits: int, signed: bool) -> torch.Tensor:
     _dev(words, torch.int32, "words")
+    if words.dim() == 0 or words.shape[-1] != row_words(length, bits):
+        raise ValueError(f"words must have rows of {row_words(length, bits)} words for length {length}")
     rows = words.numel() // words.shape[-1] if words.shape[-1] else 0
     out = torch.empty(words.shape[:-1] + (length,), dtype=torch.int8 if signed else torch.uint8, device=words.device)
     _check(lib().samd_unpack(words.data_ptr(), rows, length, Fmt(bits, signed), out.data_ptr(), _stream(words)))
@@ -195,7 +231,7 @@ def unpack(words: torch.Tensor, length: int, bits: int, signed: bool) -> torch.T
 def conv1d(xp: torch.Tensor, n: int, bits: int, taps: Sequence[int], kbits: int,
            out: Optional[torch.Tensor] = None) -> torch.Tensor:
     """Valid-mode true convolution of one packed unsigned row with host taps."""
-    _dev(xp, torch.int32, "xp")
+    _min(xp, torch.int32, row_words(n, bits) if n > 0 else 0, "xp")
     K = len(taps)
     arr = (ctypes.c_int32 * K)(*[int(t) for t in taps])
     if out is None:
@@ -250,8 +286,8 @@ def conv2d_tune(xp: torch.Tensor, xfmt: Fmt, wp: torch.Tensor, wfmt: Fmt, shape,
     """Time the first `candidates` plans on these inputs and keep the fastest for the shape
     (blocks until the timings are read).  Workspaces prepared for the shape earlier must
     be sized and prepared again afterwards."""
-    _dev(xp, torch.int32, "xp")
-    _dev(wp, torch.int32, "wp")
+    _x_words(xp, shape, xfmt)
+    _w_words(wp, shape, wfmt)
     d = Conv2dDesc.of(shape)
     Ho, Wo = out_hw(shape)
     if ws is None:
@@ -261,7 +297,7 @@ def conv2d_tune(xp: torch.Tensor, xfmt: Fmt, wp: torch.Tensor, wfmt: Fmt, shape,
     _out(out, d.N * d.M * Ho * Wo)
     plan = Conv2dPlan()
     _check(lib().samd_conv2d_tune(xp.data_ptr(), xfmt, wp.data_ptr(), wfmt, ctypes.byref(d), out.data_ptr(),
-                                  ws.data_ptr(), ws.numel(), candidates, reps, ctypes.byref(plan), _stream(xp)))
+                                  ws.data_ptr(), _ws_bytes(ws), candidates, reps, ctypes.byref(plan), _stream(xp)))
     return plan
 
 
@@ -301,8 +337,8 @@ def conv2d(xp: torch.Tensor, xfmt: Fmt, wp: torch.Tensor, wfmt: Fmt, shape, ws: 
            out: Optional[torch.Tensor] = None) -> torch.Tensor:
     """SAMD conv2d of packed activations (N*C*H rows of W) and packed weights
     (M*C*KH rows of KW); returns int32 N x M x Ho x Wo."""
-    _dev(xp, torch.int32, "xp")
-    _dev(wp, torch.int32, "wp")
+    _x_words(xp, shape, xfmt)
+    _w_words(wp, shape, wfmt)
     d = Conv2dDesc.of(shape)
     Ho, Wo = out_hw(shape)
     if ws is None:
@@ -311,75 +347,75 @@ def conv2d(xp: torch.Tensor, xfmt: Fmt, wp: torch.Tensor, wfmt: Fmt, shape, ws: 
         out = torch.empty((d.N, d.M, Ho, Wo), dtype=torch.int32, device=xp.device)
     _out(out, d.N * d.M * Ho * Wo)
     _check(lib().samd_conv2d(xp.data_ptr(), xfmt, wp.data_ptr(), wfmt, ctypes.byref(d), out.data_ptr(),
-                             ws.data_ptr(), ws.numel(), _stream(xp)))
+                             ws.data_ptr(), _ws_bytes(ws), _stream(xp)))
     return out
 
 
 def conv2d_prepare(wp: torch.Tensor, wfmt: Fmt, shape, xfmt: Fmt, ws: Optional[torch.Tensor] = None) -> torch.Tensor:
     """Kernel words of one layer, for any number of conv2d_prepared calls."""
-    _dev(wp, torch.int32, "wp")
+    _w_words(wp, shape, wfmt)
     if ws is None:
         ws = _workspace(conv2d_workspace(shape, xfmt, wfmt), wp.device)
     _check(lib().samd_conv2d_prepare(wp.data_ptr(), wfmt, ctypes.byref(Conv2dDesc.of(shape)), xfmt, ws.data_ptr(),
-                                     ws.numel(), _stream(wp)))
+                                     _ws_bytes(ws), _stream(wp)))
     return ws
 
 
 def conv2d_prepared(xp: torch.Tensor, xfmt: Fmt, wfmt: Fmt, shape, ws: torch.Tensor,
                     out: Optional[torch.Tensor] = None) -> torch.Tensor:
-    _dev(xp, torch.int32, "xp")
+    _x_words(xp, shape, xfmt)
     d = Conv2dDesc.of(shape)
     Ho, Wo = out_hw(shape)
     if out is None:
         out = torch.empty((d.N, d.M, Ho, Wo), dtype=torch.int32, device=xp.device)
     _out(out, d.N * d.M * Ho * Wo)
     _check(lib().samd_conv2d_prepared(xp.data_ptr(), xfmt, wfmt, ctypes.byref(d), out.data_ptr(), ws.data_ptr(),
-                                      ws.numel(), _stream(xp)))
+                                      _ws_bytes(ws), _stream(xp)))
     return out
 
 
 def conv2d_stage(xp: torch.Tensor, xfmt: Fmt, wfmt: Fmt, shape, ws: torch.Tensor) -> torch.Tensor:
     """Spread the packed input into the workspace's operand words (first half of conv2d_prepared)."""
-    _dev(xp, torch.int32, "xp")
-    _dev(ws, torch.uint8, "ws")
+    _x_words(xp, shape, xfmt)
     _check(lib().samd_conv2d_stage(xp.data_ptr(), xfmt, wfmt, ctypes.byref(Conv2dDesc.of(shape)), ws.data_ptr(),
-                                   ws.numel(), _stream(xp)))
+                                   _ws_bytes(ws), _stream(xp)))
     return ws
 
 
 def conv2d_accumulate(xfmt: Fmt, wfmt: Fmt, shape, ws: torch.Tensor,
                       out: Optional[torch.Tensor] = None) -> torch.Tensor:
     """Multiply, accumulate, decode and store from a prepared and staged workspace."""
-    _dev(ws, torch.uint8, "ws")
+    ws_bytes = _ws_bytes(ws)
     d = Conv2dDesc.of(shape)
     Ho, Wo = out_hw(shape)
     if out is None:
         out = torch.empty((d.N, d.M, Ho, Wo), dtype=torch.int32, device=ws.device)
     _out(out, d.N * d.M * Ho * Wo)
-    _check(lib().samd_conv2d_accumulate(xfmt, wfmt, ctypes.byref(d), out.data_ptr(), ws.data_ptr(), ws.numel(),
+    _check(lib().samd_conv2d_accumulate(xfmt, wfmt, ctypes.byref(d), out.data_ptr(), ws.data_ptr(), ws_bytes,
                                         _stream(ws)))
     return out
 
 
 def conv2d_int8_prepare(w: torch.Tensor, wfmt: Fmt, shape, xfmt: Fmt, ws: Optional[torch.Tensor] = None):
-    _dev(w, torch.int8, "w")
+    d = Conv2dDesc.of(shape)
+    _min(w, torch.int8, d.M * d.C * d.KH * d.KW, "w")
     if ws is None:
         ws = _workspace(conv2d_int8_workspace(shape, xfmt), w.device)
-    _check(lib().samd_conv2d_int8_prepare(w.data_ptr(), wfmt, ctypes.byref(Conv2dDesc.of(shape)), xfmt,
-                                          ws.data_ptr(), ws.numel(), _stream(w)))
+    _check(lib().samd_conv2d_int8_prepare(w.data_ptr(), wfmt, ctypes.byref(d), xfmt, ws.data_ptr(), _ws_bytes(ws),
+                                          _stream(w)))
     return ws
 
 
 def conv2d_int8_prepared(x_nhwc: torch.Tensor, xfmt: Fmt, wfmt: Fmt, shape, ws: torch.Tensor,
                          out: Optional[torch.Tensor] = None) -> torch.Tensor:
-    _dev(x_nhwc, (torch.int8, torch.uint8), "x_nhwc")
     d = Conv2dDesc.of(shape)
+    _min(x_nhwc, (torch.int8, torch.uint8), d.N * d.H * d.W * d.C, "x_nhwc")
     Ho, Wo = out_hw(shape)
     if out is None:
         out = torch.empty((d.N, d.M, Ho, Wo), dtype=torch.int32, device=x_nhwc.device)
     _out(out, d.N * d.M * Ho * Wo)
     _check(lib().samd_conv2d_int8_prepared(x_nhwc.data_ptr(), xfmt, wfmt, ctypes.byref(d), out.data_ptr(),
-                                           ws.data_ptr(), ws.numel(), _stream(x_nhwc)))
+                                           ws.data_ptr(), _ws_bytes(ws), _stream(x_nhwc)))
     return out
 
 
@@ -392,9 +428,9 @@ def conv2d_int8_workspace(shape, xfmt: Fmt) -> int:
 def conv2d_int8(x_nhwc: torch.Tensor, xfmt: Fmt, w: torch.Tensor, wfmt: Fmt, shape,
                 ws: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None) -> torch.Tensor:
     """Native 8-bit baseline: x is N x H x W x C int8/uint8, w is M x C x KH x KW int8."""
-    _dev(x_nhwc, (torch.int8, torch.uint8), "x_nhwc")
-    _dev(w, torch.int8, "w")
     d = Conv2dDesc.of(shape)
+    _min(x_nhwc, (torch.int8, torch.uint8), d.N * d.H * d.W * d.C, "x_nhwc")
+    _min(w, torch.int8, d.M * d.C * d.KH * d.KW, "w")
     Ho, Wo = out_hw(shape)
     if ws is None:
         ws = _workspace(conv2d_int8_workspace(shape, xfmt), x_nhwc.device)
@@ -402,7 +438,7 @@ def conv2d_int8(x_nhwc: torch.Tensor, xfmt: Fmt, w: torch.Tensor, wfmt: Fmt, sha
         out = torch.empty((d.N, d.M, Ho, Wo), dtype=torch.int32, device=x_nhwc.device)
     _out(out, d.N * d.M * Ho * Wo)
     _check(lib().samd_conv2d_int8(x_nhwc.data_ptr(), xfmt, w.data_ptr(), wfmt, ctypes.byref(d), out.data_ptr(),
-                                  ws.data_ptr(), ws.numel(), _stream(x_nhwc)))
+                                  ws.data_ptr(), _ws_bytes(ws), _stream(x_nhwc)))
     return out
 
 
@@ -410,7 +446,7 @@ def max_i32(t: torch.Tensor, out: Optional[torch.Tensor] = None) -> torch.Tensor
     _dev(t, torch.int32, "t")
     if out is None:
         out = torch.empty(1, dtype=torch.int32, device=t.device)
-    _check(lib().samd_max_i32(t.data_ptr(), t.numel(), out.data_ptr(), _stream(t)))
+    _check(lib().samd_max_i32(t.data_ptr(), t.numel(), _opt(out, "out"), _stream(t)))
     return out
 
 
@@ -422,9 +458,9 @@ def relu_requant_pack(acc: torch.Tensor, dev_max: torch.Tensor, bits: int,
     rows = acc.numel() // length
     if out is None:
         out = torch.empty(acc.shape[:-1] + (row_words(length, bits),), dtype=torch.int32, device=acc.device)
-    _check(lib().samd_relu_requant_pack(acc.data_ptr(), rows, length, dev_max.data_ptr(), Fmt(bits, False),
-                                        out.data_ptr(), shift_out.data_ptr() if shift_out is not None else None,
-                                        _stream(acc)))
+    _min(out, torch.int32, rows * row_words(length, bits), "out")
+    _check(lib().samd_relu_requant_pack(acc.data_ptr(), rows, length, _opt(dev_max, "dev_max"), Fmt(bits, False),
+                                        out.data_ptr(), _opt(shift_out, "shift_out"), _stream(acc)))
     return out
 
 
@@ -434,7 +470,8 @@ def relu_requant_nhwc_u8(acc: torch.Tensor, dev_max: torch.Tensor, bits: int,
     N, C, H, W = acc.shape
     if out is None:
         out = torch.empty((N, H, W, C), dtype=torch.uint8, device=acc.device)
-    _check(lib().samd_relu_requant_nhwc_u8(acc.data_ptr(), N, C, H, W, dev_max.data_ptr(), Fmt(bits, False),
+    _min(out, torch.uint8, N * H * W * C, "out")
+    _check(lib().samd_relu_requant_nhwc_u8(acc.data_ptr(), N, C, H, W, _opt(dev_max, "dev_max"), Fmt(bits, False),
                                            out.data_ptr(), _stream(acc)))
     return out
 
@@ -469,9 +506,9 @@ def relu_requant_stage(acc: torch.Tensor, dev_max: torch.Tensor, bits: int, wfmt
     """ReLU + requantisation of acc to unsigned `bits`, written as the operand words of the
     next layer (descriptor `shape`, weight format `wfmt`) into its workspace `ws`; follow
     with conv2d_accumulate.  Returns ws."""
-    acc = _dev(acc, torch.int32, "acc")
     d = Conv2dDesc.of(shape)
-    _check(lib().samd_relu_requant_stage(acc.data_ptr(), dev_max.data_ptr(), Fmt(bits, False), wfmt,
-                                         ctypes.byref(d), ws.data_ptr(), ws.numel(),
-                                         dev_shift.data_ptr() if dev_shift is not None else None, _stream(acc)))
+    _min(acc, torch.int32, d.N * d.C * d.H * d.W, "acc")
+    _check(lib().samd_relu_requant_stage(acc.data_ptr(), _opt(dev_max, "dev_max"), Fmt(bits, False), wfmt,
+                                         ctypes.byref(d), ws.data_ptr(), _ws_bytes(ws), _opt(dev_shift, "dev_shift"),
+                                         _stream(acc)))
     return ws

@@ -227,7 +227,7 @@ def test_conv2d_edge_shapes(shape, bx, sx, bw, sw):
 
 def test_conv2d_rejects_and_leaves_output_untouched():
     shape = wl.Conv2dShape(1, 512, 16, 16, 1, 16, 16, 1, 1, 0, 0)
-    x = torch.zeros(512 * 16 * 2, dtype=torch.int32, device=DEV)
+    x = torch.zeros(512 * 16 * 4, dtype=torch.int32, device=DEV)
     w = torch.zeros(512 * 16 * 4, dtype=torch.int32, device=DEV)
     out = torch.full((1, 1, 1, 1), 7, dtype=torch.int32, device=DEV)
     with pytest.raises(samd.SamdError) as e:
