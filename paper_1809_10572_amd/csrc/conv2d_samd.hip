@@ -59,7 +59,7 @@ __global__ __launch_bounds__(256) void prep_weights_kernel(const uint32_t *__res
             // steps of a channel: kernel-row-major, or kernel-word-major for the
             // shared-row path
             const int ky = g.rows_path ? rt % g.KH : rt / g.ntw, t = g.rows_path ? rt / g.KH : rt % g.ntw;
-            const uint32_t *row = w + ((int64_t)(m * g.C + c) * g.KH + ky) * g.wrw;
+            const uint32_t *row = w + (((int64_t)m * g.C + c) * g.KH + ky) * g.wrw;
             const int k = g.tw_ntaps[t], a0 = g.tw_tap0[t], r = g.tw_phase[t];
             for (int si = 0; si < k; ++si) {
                 const int tap = g.sw * (a0 + k - 1 - si) + r;   // reversed: lane si holds tap a0+k-1-si
@@ -77,14 +77,14 @@ template <int B, bool S>
 __global__ __launch_bounds__(256) void prefix_kernel(const uint32_t *__restrict__ w, const Conv2dGeom g,
                                                      int32_t *__restrict__ pre) {
     const int pwid = (g.KH + 1) * (g.KW + 1);
-    const int total = g.M * pwid;
-    for (int e = blockIdx.x * 256 + threadIdx.x; e < total; e += gridDim.x * 256) {
-        const int m = e / pwid, ij = e - m * pwid;
+    const int64_t total = (int64_t)g.M * pwid;
+    for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < total; e += (int64_t)gridDim.x * 256) {
+        const int m = (int)(e / pwid), ij = (int)(e - (int64_t)m * pwid);
         const int i = ij / (g.KW + 1), j = ij - i * (g.KW + 1);
         int32_t sum = 0;
         for (int c = 0; c < g.C; ++c)
             for (int ky = 0; ky < i; ++ky) {
-                const uint32_t *row = w + ((int64_t)(m * g.C + c) * g.KH + ky) * g.wrw;
+                const uint32_t *row = w + (((int64_t)m * g.C + c) * g.KH + ky) * g.wrw;
                 for (int kx = 0; kx < j; ++kx) sum += packed_field<B, S>(row, kx);
             }
         pre[e] = sum;
@@ -553,7 +553,7 @@ __global__ __launch_bounds__(1024) void conv2d_samd_kernel(const int32_t *__rest
                     // recentred activations: + xoff * (weights over the output's in-image taps)
                     const int hb = ho * g.sh - g.ph, kwid = g.KW + 1;
                     const int ky0 = max(0, -hb) * kwid, ky1 = min(g.KH, g.H - hb) * kwid;
-                    const int32_t *pm = pre + m * (g.KH + 1) * kwid;
+                    const int32_t *pm = pre + (int64_t)m * (g.KH + 1) * kwid;
                     for (int o = lane; o < ncols; o += 64) {
                         const int wbeg = (c0 + o) * g.sw - g.pw;
                         const int kx0 = max(0, -wbeg), kx1 = min(g.KW, g.W - wbeg);
@@ -619,7 +619,12 @@ int launch_conv2d_spread(const uint32_t *x, const Conv2dGeom &g, void *ws, hipSt
     while ((1 << qshift) * 5 < 2 * g.nq && qshift < 8) ++qshift;   // up to 256 threads per row
     const int64_t nrows = (int64_t)g.N * g.C * g.Hp;
     const int rpb = 256 >> qshift;
-    const unsigned sgrid = (unsigned)((nrows + rpb - 1) / rpb);
+    const int64_t blocks = (nrows + rpb - 1) / rpb;   // one thread group per row, no grid-stride loop
+    if (blocks * 256 > (int64_t)0xffffffff) {
+        set_error("conv2d operand spread: more than 2^32 threads in one launch");
+        return SAMD_EUNSUPPORTED;
+    }
+    const unsigned sgrid = (unsigned)blocks;
     bool launched = false;
 #define SAMD_SPREAD_CASE(B, SG)                                                                            \
     if (!launched && g.xbits == B && (bool)g.xsigned == SG) {                                              \

@@ -181,8 +181,13 @@ int launch_relu_requant_stage(const int32_t *acc, const int32_t *dev_max, const 
     while ((1 << qshift) * 5 < 2 * g.nq && qshift < 8) ++qshift;   // ~2.5 words per thread, as the spread
     const int64_t nrows = (int64_t)g.N * g.C * g.Hp;
     const int rpb = kBlock >> qshift;
-    hipLaunchKernelGGL(relu_requant_stage_kernel, dim3((unsigned)((nrows + rpb - 1) / rpb)), dim3(kBlock), 0, s, acc,
-                       dev_max, g, qshift, xs, dev_shift);
+    const int64_t blocks = (nrows + rpb - 1) / rpb;   // one thread group per row, no grid-stride loop
+    if (blocks * kBlock > (int64_t)0xffffffff) {
+        set_error("relu_requant_stage: more than 2^32 threads in one launch");
+        return SAMD_EUNSUPPORTED;
+    }
+    hipLaunchKernelGGL(relu_requant_stage_kernel, dim3((unsigned)blocks), dim3(kBlock), 0, s, acc, dev_max, g, qshift,
+                       xs, dev_shift);
     return check_launch("relu_requant_stage");
 }
 

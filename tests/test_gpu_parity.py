@@ -237,6 +237,30 @@ def test_conv2d_rejects_and_leaves_output_untouched():
     assert int(out.item()) == 7
 
 
+def test_conv2d_weights_past_2g_rows():
+    """A 1x1 layer whose M*C weight rows pass 2^31 (C = 32768, M = 66000, u8 x s8: 8.6 GB
+    of packed weights and as much kernel words): rows past the 2^31st are found with
+    64-bit indices, and every output matches the oracle."""
+    C, M = 32768, 66000
+    shape = (1, C, 1, 1, M, 1, 1, 1, 1, 0, 0)
+    assert M * C > 1 << 31
+    rng = np.random.default_rng(2 ** 31)
+    x = rng.integers(0, 256, size=(1, C, 1, 1), dtype=np.uint8)
+    w = rng.integers(-128, 128, size=(M, C, 1, 1), dtype=np.int8)
+    xf, wf = samd.Fmt(8, False), samd.Fmt(8, True)
+    xp = samd.pack(gpu_vals(x, False), 8, False)
+    wv = gpu_vals(w, True)
+    wp = samd.pack(wv, 8, True)
+    del wv
+    y = samd.conv2d(xp, xf, wp, wf, shape)
+    torch.cuda.synchronize()
+    got = y.cpu().numpy()
+    del wp, y
+    torch.cuda.empty_cache()
+    want = ref.conv2d(x, w, shape)
+    np.testing.assert_array_equal(got, want)
+
+
 # --- the native 8-bit baseline -----------------------------------------------------------
 
 @pytest.mark.parametrize("cfg,bits", [(1, 4), (3, 1), (3, 4), (3, 8), (4, 2), (4, 8)])
