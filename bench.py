@@ -35,8 +35,17 @@ PEAK_I8_MACS = 2.5e15                 # dense int8 matrix-core MAC/s (5.0 POP/s)
 def parse():
     p = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=1000)
-    p.add_argument("--warmup", type=int, default=1000)
+    p.add_argument("--steps", type=int, default=200)
+    p.add_argument("--warmup", type=int, default=20)
+    p.add_argument("--step-warm-s", type=float, default=0.5,
+                   help="seconds of back-to-back step replays before the timed steps (at least --warmup replays)")
+    p.add_argument("--samples", type=int, default=5,
+                   help="timed graph replays per kernel timing (median and min reported)")
+    p.add_argument("--no-peak-check", action="store_true",
+                   help="skip the short v_mad_i64_i32 issue-rate measurement reported next to the roofline")
+    p.add_argument("--peaks", action="store_true",
+                   help="instead of the default workload, measure the ceilings: v_mad_i64_i32 and int32 add issue "
+                        "rates, int8 MFMA rate, streaming copy and read bandwidth")
     p.add_argument("--bits", default="1,2,3,4,5,6,7,8")
     p.add_argument("--reps", type=int, default=20, help="back-to-back launches per kernel timing")
     p.add_argument("--kernel-warm-s", type=float, default=0.2,
@@ -266,10 +275,10 @@ def capture_graph(fn, reps):
     return graph
 
 
-def timed_graph(fn, reps, warm_s):
-    """Seconds per call of fn: HIP events on the launching stream around one replay of a
-    graph of reps calls (the GPU never waits for the host), after warm_s seconds of
-    back-to-back replays (the clocks rise under sustained load)."""
+def timed_graph_stats(fn, reps, warm_s, samples=5):
+    """(median, min) seconds per call of fn: HIP events on the launching stream around each
+    of `samples` replays of a graph of reps calls (the GPU never waits for the host), after
+    warm_s seconds of back-to-back replays (the clocks rise under sustained load)."""
     import torch
     graph = capture_graph(fn, reps)
     graph.replay()
@@ -279,12 +288,98 @@ def timed_graph(fn, reps, warm_s):
         graph.replay()
         torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record(stream)
-    graph.replay()
-    e1.record(stream)
-    e1.synchronize()
-    return e0.elapsed_time(e1) * 1e-3 / reps
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(samples + 1)]
+    ev[0].record(stream)
+    for i in range(samples):
+        graph.replay()
+        ev[i + 1].record(stream)
+    ev[-1].synchronize()
+    per = sorted(ev[i].elapsed_time(ev[i + 1]) * 1e-3 / reps for i in range(samples))
+    return per[len(per) // 2], per[0]
+
+
+def timed_graph(fn, reps, warm_s, samples=5):
+    """Median seconds per call of fn (see timed_graph_stats)."""
+    return timed_graph_stats(fn, reps, warm_s, samples)[0]
+
+
+SPEC = {"mad": (PEAK_VALU_OPS, "T lane-ops/s", "alu"), "valu": (PEAK_VALU_OPS, "T lane-ops/s", "alu"),
+        "mfma_i8": (PEAK_I8_MACS, "T MAC/s", "mfma"), "copy": (PEAK_HBM, "TB/s", "hbm"),
+        "read": (PEAK_HBM, "TB/s", "hbm")}
+
+
+def measure_peak(samd, kind, seconds=0.3):
+    """Rate of one ceiling microbenchmark (include/samd_peaks.h) in work units per second:
+    the median of 5 HIP-event-timed launches after `seconds` of back-to-back launches."""
+    import torch
+    code = {"mad": samd.PEAK_MAD_I64_I32, "valu": samd.PEAK_VALU_I32, "mfma_i8": samd.PEAK_MFMA_I8,
+            "copy": samd.PEAK_COPY, "read": samd.PEAK_READ}[kind]
+    dev = torch.device("cuda:0")
+    nbytes = 1 << 30
+    if kind in ("copy", "read"):
+        blocks, iters = 256 * 8 * 4, 1
+        src = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+        src.fill_(1)
+        dst = torch.empty(nbytes if kind == "copy" else 4 * blocks, dtype=torch.uint8, device=dev)
+    else:
+        # 8 workgroups of 4 waves per compute unit: 8 waves per SIMD
+        blocks, iters, src = 256 * 8, (1 << 14) if kind != "mfma_i8" else (1 << 12), None
+        dst = torch.empty(4 * 256 * blocks, dtype=torch.uint8, device=dev)
+    fn = lambda: samd.peak_launch(code, iters, blocks, dst, src, nbytes if src is not None else 0)
+    fn()
+    torch.cuda.synchronize()
+    t_end = time.perf_counter() + seconds
+    while time.perf_counter() < t_end:
+        fn()
+        torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(6)]
+    ev[0].record(stream)
+    for i in range(5):
+        fn()
+        ev[i + 1].record(stream)
+    ev[-1].synchronize()
+    t = sorted(ev[i].elapsed_time(ev[i + 1]) * 1e-3 for i in range(5))[2]
+    work = samd.peak_work(code, iters, blocks, nbytes if src is not None else 0)
+    return work / t
+
+
+def device_info(torch):
+    """GPU name, compute units, ROCm / HIP and torch versions of the run."""
+    prop = torch.cuda.get_device_properties(0)
+    info = {"name": prop.name, "gcn_arch": getattr(prop, "gcnArchName", None),
+            "compute_units": prop.multi_processor_count, "hip": torch.version.hip, "torch": torch.__version__}
+    try:
+        info["rocm"] = open("/opt/rocm/.info/version").read().strip()
+    except OSError:
+        info["rocm"] = None
+    return info
+
+
+def run_peaks(args):
+    """The ceilings the roofline fractions divide by, measured on this GPU next to the
+    published / unit-count figures.  Prints one JSON line."""
+    import torch
+
+    import paper_1809_10572_amd as samd
+
+    rows = {}
+    for kind in ("mad", "valu", "mfma_i8", "copy", "read"):
+        rate = measure_peak(samd, kind, seconds=0.5)
+        spec, unit, bound = SPEC[kind]
+        rows[kind] = {"measured": round(rate / 1e12, 3), "spec": round(spec / 1e12, 3), "unit": unit,
+                      "frac_of_spec": round(rate / spec, 4)}
+        print(f"peaks: {kind} {rate / 1e12:.3f} {unit} ({rate / spec:.3f} of {spec / 1e12:.2f})", file=sys.stderr,
+              flush=True)
+    print(json.dumps({"metric": "MI355X ceilings, measured", "n_gpus": 1, "device": device_info(torch),
+                      "notes": {"mad": "v_mad_i64_i32 (exact signed 32x32->64 multiply-add), 8 independent chains "
+                                       "per lane, uniform multiplier; spec = 256 CUs x 64 lanes x 2.4 GHz",
+                                "valu": "v_add_u32, 8 independent chains per lane; same spec",
+                                "mfma_i8": "v_mfma_i32_16x16x64_i8, 4 independent accumulators per wave; "
+                                           "spec = 5.0 POP/s dense = 2.5 P MAC/s",
+                                "copy": "16-byte loads and stores, 1 GiB each way, bytes read + written",
+                                "read": "16-byte loads of 1 GiB"},
+                      "peaks": rows}), flush=True)
 
 
 def run_configs(args):
@@ -503,9 +598,54 @@ def run_stack(args):
 
         t = {name: timed_graph(fn, 3, args.kernel_warm_s) for name, fn in
              (("samd_packed", chain_packed), ("samd_fused", chain_fused), ("int8", chain_int8))}
+
+        # per layer: each chain's convolution and the epilogue that follows it
+        layer_rows = []
+        for li, l in enumerate(lys):
+            Ho, Wo = samd.out_hw(l)
+            lmacs = l.N * l.M * Ho * Wo * l.C * l.KH * l.KW
+            r = {"layer": li + 1, "gmac": round(lmacs / 1e9, 2),
+                 "samd_conv_ms": timed_graph(lambda: samd.conv2d_prepared(xps[li], xf, wf, l, wss[li], out=ys[li]),
+                                             3, args.kernel_warm_s) * 1e3,
+                 "samd_accumulate_ms": timed_graph(lambda: samd.conv2d_accumulate(xf, wf, l, wss[li], out=ys[li]),
+                                                   3, args.kernel_warm_s) * 1e3,
+                 "int8_conv_ms": timed_graph(lambda: samd.conv2d_int8_prepared(x8s[li], xf, wf, l, ws8[li],
+                                                                               out=ys[li]), 3, args.kernel_warm_s) * 1e3}
+            if li + 1 < len(lys):
+                nxt = lys[li + 1]
+                r["epilogue_packed_ms"] = timed_graph(lambda: (samd.max_i32(ys[li], out=mx),
+                                                               samd.relu_requant_pack(ys[li], mx, bits,
+                                                                                      out=xps[li + 1])),
+                                                      3, args.kernel_warm_s) * 1e3
+                r["epilogue_fused_ms"] = timed_graph(lambda: (samd.max_i32(ys[li], out=mx),
+                                                              samd.relu_requant_stage(ys[li], mx, bits, wf, nxt,
+                                                                                      wss[li + 1])),
+                                                     3, args.kernel_warm_s) * 1e3
+                r["epilogue_int8_ms"] = timed_graph(lambda: (samd.max_i32(ys[li], out=mx),
+                                                             samd.relu_requant_nhwc_u8(ys[li], mx, bits,
+                                                                                       out=x8s[li + 1])),
+                                                    3, args.kernel_warm_s) * 1e3
+            r["samd_conv_gmacs"] = round(lmacs / r["samd_conv_ms"] / 1e6, 1)
+            r["int8_conv_gmacs"] = round(lmacs / r["int8_conv_ms"] / 1e6, 1)
+            layer_rows.append({k: (round(v, 4) if isinstance(v, float) and k.endswith("_ms") else v)
+                               for k, v in r.items()})
+
+        # parity: every layer's int32 output of each chain, at full batch, against the oracle
+        parity = None
+        if not args.no_check:
+            from oracle import reference as ref
+            accs, _, _ = ref.stack(case.x, case.ws, [l.as_tuple() for l in lys], bits)
+            parity = {}
+            for name, fn in (("samd_packed", chain_packed), ("samd_fused", chain_fused), ("int8", chain_int8)):
+                fn()
+                torch.cuda.synchronize()
+                parity[name] = all(np.array_equal(ys[li].cpu().numpy(), accs[li]) for li in range(len(lys)))
+            print(f"stack: b={bits} parity {parity}", file=sys.stderr, flush=True)
+
         rows.append({"bits": bits, **{f"{k}_ms": round(v * 1e3, 3) for k, v in t.items()},
                      **{f"{k}_gmacs": round(macs / v / 1e9, 1) for k, v in t.items()},
-                     "fused_saving": round(1 - t["samd_fused"] / t["samd_packed"], 3)})
+                     "fused_saving": round(1 - t["samd_fused"] / t["samd_packed"], 3),
+                     "parity": parity, "per_layer": layer_rows})
         print(f"stack: b={bits} " + " ".join(f"{k} {v * 1e3:.3f} ms" for k, v in t.items()), file=sys.stderr,
               flush=True)
     print(json.dumps({"metric": "AlexNet-shaped conv stack forward, GMAC/s", "unit": "GMAC/s",
@@ -560,6 +700,9 @@ def run_lanewise(args):
 def main():
     args = parse()
     args.bits_given = "--bits" in sys.argv
+    if args.peaks:
+        run_peaks(args)
+        return
     if args.vggb:
         run_vggb(args)
         return
@@ -686,10 +829,8 @@ def main():
         for st in side:
             main.wait_stream(st)
 
-    capture = capture_graph
-
-    # eager steps: every kernel launched from the host
-    for _ in range(args.warmup):
+    # eager steps: every kernel launched from the host (context only)
+    for _ in range(min(args.warmup, 20)):
         step()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -698,31 +839,48 @@ def main():
     torch.cuda.synchronize()
     eager_ms = (time.perf_counter() - t0) * 1e3 / args.steps
 
-    # the same steps replayed from one captured graph: the rate a fixed pipeline runs at
-    step_graph = capture(step, 1)
+    # The timed steps: the step captured once into a HIP graph and replayed.  Warm-up is
+    # `warmup` replays and at least `step_warm_s` seconds of them (the GPU's clocks rise
+    # under sustained load; a short warm-up would time the ramp), then exactly `steps`
+    # replays between two synchronisations, timed with HIP events on the launching stream
+    # (the side streams fork from and join it inside the graph).
+    step_graph = capture_graph(step, 1)
+    stream = torch.cuda.current_stream()
     for _ in range(args.warmup):
         step_graph.replay()
     torch.cuda.synchronize()
+    t_end = time.perf_counter() + args.step_warm_s
+    while time.perf_counter() < t_end:
+        for _ in range(10):
+            step_graph.replay()
+        torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
     t0 = time.perf_counter()
+    e0.record(stream)
     for _ in range(args.steps):
         step_graph.replay()
+    e1.record(stream)
     torch.cuda.synchronize()
-    ms_per_step = (time.perf_counter() - t0) * 1e3 / args.steps
+    wall_ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    ms_per_step = e0.elapsed_time(e1) / args.steps
     # the outputs of the timed steps themselves, for the parity check below
     for L in layers:
         L["y_step"] = L["y"].clone()
 
     def timed(fn, reps):
-        return timed_graph(fn, reps, args.kernel_warm_s)
+        return timed_graph_stats(fn, reps, args.kernel_warm_s, args.samples)
 
     for L in layers:
         samd.conv2d_stage(L["xp"], L["xf"], L["wf"], shape, L["ws"])
-        L["t_conv"] = timed(lambda: samd.conv2d_accumulate(L["xf"], L["wf"], shape, L["ws"], out=L["y"]), args.reps)
-        L["t_stage"] = timed(lambda: samd.conv2d_stage(L["xp"], L["xf"], L["wf"], shape, L["ws"]), args.reps)
-        L["t_pack"] = timed(lambda: samd.pack(L["x"], L["b"], False, out=L["xp"]), args.reps)
-        L["t_int8"] = timed(lambda: samd.conv2d_int8_prepared(L["x_nhwc"], L["xf"], L["wf"], shape, L["ws8"],
-                                                              out=L["y8"]), args.reps)
+        L["t_conv"], L["t_conv_min"] = timed(lambda: samd.conv2d_accumulate(L["xf"], L["wf"], shape, L["ws"],
+                                                                             out=L["y"]), args.reps)
+        L["t_stage"], _ = timed(lambda: samd.conv2d_stage(L["xp"], L["xf"], L["wf"], shape, L["ws"]), args.reps)
+        L["t_pack"], _ = timed(lambda: samd.pack(L["x"], L["b"], False, out=L["xp"]), args.reps)
+        L["t_int8"], L["t_int8_min"] = timed(lambda: samd.conv2d_int8_prepared(L["x_nhwc"], L["xf"], L["wf"], shape,
+                                                                                L["ws8"], out=L["y8"]), args.reps)
     torch.cuda.synchronize()
+    peak_mad = round(measure_peak(samd, "mad") / 1e12, 3) if not args.no_peak_check else None
 
     # sampled parity against the oracle, same inputs, both paths
     parity = {}
@@ -739,21 +897,27 @@ def main():
                                   np.array_equal(got8, want))
 
     traffic = stored_traffic()
-    per_bits, tot_mads, tot_conv_s, tot_alg_bytes = {}, 0.0, 0.0, 0.0
+    per_bits, tot_mads, tot_conv_s, tot_alg_bytes, tot_word_bytes = {}, 0.0, 0.0, 0.0, 0.0
     for L in layers:
         t, t8 = L["t_conv"], L["t_int8"]
         p = L["plan"]
         mads = N * M * Ho * p.words_per_row * C * KH * p.tap_words
         b = L["b"]
         packed_bytes = N * C * H * samd.row_words(W, b) * 4
-        # operand words and kernel words read once, int32 outputs written once
-        hbm_bytes = (N * C * samd_hp * p.tap_words * p.words_per_row * 4 + M * C * KH * p.tap_words * 4
-                     + N * M * Ho * Wo * 4)
+        # what the method must move: packed activations at b bits, packed weights at b bits,
+        # int32 outputs
+        alg_bytes = packed_bytes + M * C * KH * samd.row_words(KW, b) * 4 + N * M * Ho * Wo * 4
+        # what this kernel reads and writes at best: the spread operand words and the kernel
+        # words once each, the int32 outputs
+        word_bytes = (N * C * samd_hp * p.tap_words * p.words_per_row * 4 + M * C * KH * p.tap_words * 4
+                      + N * M * Ho * Wo * 4)
         tot_mads += mads
         tot_conv_s += t
-        tot_alg_bytes += hbm_bytes
+        tot_alg_bytes += alg_bytes
+        tot_word_bytes += word_bytes
         per_bits[str(b)] = {
-            "conv_us": round(t * 1e6, 2), "stage_us": round(L["t_stage"] * 1e6, 2),
+            "conv_us": round(t * 1e6, 2), "conv_us_min": round(L["t_conv_min"] * 1e6, 2),
+            "stage_us": round(L["t_stage"] * 1e6, 2),
             "pack_us": round(L["t_pack"] * 1e6, 2),
             # packed data: pack reads 1 B per value and writes the packed words; the stage
             # reads the packed words and writes the operand words
@@ -762,11 +926,13 @@ def main():
                                 / 1e9, 1),
             "gmacs": round(macs / t / 1e9, 1),
             "gmacs_with_stage": round(macs / (t + L["t_stage"]) / 1e9, 1),
-            "int8_us": round(t8 * 1e6, 2), "int8_gmacs": round(macs / t8 / 1e9, 1),
+            "int8_us": round(t8 * 1e6, 2), "int8_us_min": round(L["t_int8_min"] * 1e6, 2),
+            "int8_gmacs": round(macs / t8 / 1e9, 1),
             "speedup_vs_int8": round(t8 / (t + L["t_stage"]), 3),
             "valu_frac": round(mads / t / PEAK_VALU_OPS, 4),
-            "hbm_frac": round(hbm_bytes / t / PEAK_HBM, 4),
-            "hbm_bytes_alg": hbm_bytes,
+            "hbm_frac": round(alg_bytes / t / PEAK_HBM, 4),
+            "hbm_bytes_alg": alg_bytes,
+            "operand_word_bytes": word_bytes,
             "hbm_bytes_counted": (traffic["per_bits"][str(b)]["fetch_bytes"] + traffic["per_bits"][str(b)]["write_bytes"]
                                   if traffic and str(b) in traffic["per_bits"] else None),
             "int8_mfma_frac": round(macs / t8 / PEAK_I8_MACS, 4),
@@ -800,6 +966,7 @@ def main():
         "value": round(macs * len(layers) / (ms_per_step * 1e-3) / 1e9, 1),
         "unit": "GMAC/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
+        "wall_ms_per_step": round(wall_ms, 4), "step_warm_s": args.step_warm_s,
         "eager_ms_per_step": round(eager_ms, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "int64", "data": "synthetic",
@@ -809,14 +976,19 @@ def main():
                              else f"tuned at set-up ({args.tune_candidates} candidates timed)"),
                    "streams": args.streams, "stream_order": args.stream_order,
                    "bits": bits_list, "global_batch": N, "macs_per_layer": macs},
+        "device": device_info(torch),
         "roofline": {"bound": "alu", "achieved": round(achieved / 1e12, 3), "peak": round(PEAK_VALU_OPS / 1e12, 2),
                      "unit": "TOP/s", "frac": round(achieved / PEAK_VALU_OPS, 4),
                      # HBM bytes per launch counted by FETCH_SIZE + WRITE_SIZE (mean over the bit
-                     # widths), next to the algorithmic bytes the kernel must move
+                     # widths), next to the algorithmic bytes the method must move (packed x and w
+                     # at b bits, int32 y) and the operand-word bytes this kernel moves at best
                      "traffic": (round(sum(v["hbm_bytes_counted"] for v in per_bits.values()) / len(layers))
                                  if all(v["hbm_bytes_counted"] is not None for v in per_bits.values()) else None),
                      "alg_bytes_per_launch": round(tot_alg_bytes / len(layers)),
-                     "kernel": "conv2d_samd_kernel", "op": "32x32->64-bit multiply-accumulate (v_mad_i64_i32)"},
+                     "operand_word_bytes_per_launch": round(tot_word_bytes / len(layers)),
+                     "measured_mad_peak": peak_mad,
+                     "kernel": "conv2d_samd_kernel", "op": "32x32->64-bit multiply-accumulate (v_mad_i64_i32)",
+                     "timing": f"median of {args.samples} HIP-event-timed replays of a graph of {args.reps} launches"},
         "cpu_baseline": cpu,
         "per_bits": per_bits,
     }

@@ -11,8 +11,9 @@
  * Conventions for every entry point:
  *  - Pointers are DEVICE pointers unless a parameter says "host".  The caller owns
  *    every buffer; the library allocates nothing and keeps no state between calls
- *    apart from a thread-local error message and the plans chosen by
- *    samd_conv2d_tune (process-wide, until samd_conv2d_untune).
+ *    apart from a thread-local error message, a cache of computed plans (a pure
+ *    function of shape and formats) and the plans chosen by samd_conv2d_tune or
+ *    samd_conv2d_use_plan (process-wide mutable state, until samd_conv2d_untune).
  *  - Work is enqueued asynchronously on `stream` (0 = the default stream).  A return
  *    of SAMD_OK means the launch was accepted; results are ready once the stream is
  *    synchronised.
@@ -108,7 +109,8 @@ const char *samd_status_str(int status);
  * call on this thread. */
 const char *samd_last_error(void);
 
-/* Words per packed row: ceil(len / floor(32 / f.bits)); negative status on error. */
+/* Library utility (sizes the packed storage format above; no passage of the paper):
+ * words per packed row, ceil(len / floor(32 / f.bits)); negative status on error. */
 int64_t samd_row_words(int64_t len, samd_fmt f);
 
 /* Pack `rows` x `len` values (int8 when f.is_signed, else uint8; row-major) into the
@@ -120,7 +122,9 @@ int64_t samd_row_words(int64_t len, samd_fmt f);
 int samd_pack(const void *src, int64_t rows, int64_t len, samd_fmt f, uint32_t *dst,
               int32_t *oor_count, hipStream_t stream);
 
-/* Inverse of samd_pack: dst is int8 (sign-extended) when f.is_signed, else uint8. */
+/* Library utility, the inverse of samd_pack (for inspection and tests; the paper's
+ * baseline unpacks to 8 bits, Sec. 7): dst is int8 (sign-extended) when f.is_signed,
+ * else uint8. */
 int samd_unpack(const uint32_t *src, int64_t rows, int64_t len, samd_fmt f, void *dst,
                 hipStream_t stream);
 
@@ -152,7 +156,14 @@ int samd_conv1d_plan_query(int64_t n, samd_fmt xf, const int32_t *taps, int32_t 
 int samd_conv2d_plan_query(const samd_conv2d_desc *d, samd_fmt xf, samd_fmt wf,
                            samd_conv2d_plan *out);
 
-/* Workspace bytes samd_conv2d needs (prepared kernel words). */
+/* Library utility: the workspace bytes samd_conv2d and its split entry points need for
+ * (xf, wf, *d) under the shape's current plan (kernel-word streams, the recentring
+ * correction table, the multiply kernel's ticket counters and the staged operand words).
+ *
+ * A workspace serves one launch at a time: the multiply kernel's per-XCD ticket counters
+ * live in it and are advanced by every launch, so two launches in flight on one
+ * workspace (different streams, or graph branches that may overlap) race.  Give each
+ * stream its own workspace. */
 int samd_conv2d_workspace(const samd_conv2d_desc *d, samd_fmt xf, samd_fmt wf, size_t *bytes);
 
 /* Quantized 2-D convolution by SAMD long multiplication, the DNN loop of Sec. 7
@@ -252,7 +263,8 @@ int samd_conv2d_use_plan(const samd_conv2d_desc *d, samd_fmt xf, samd_fmt wf, co
  * (xf and wf are then ignored); the planner's model decides again. */
 int samd_conv2d_untune(const samd_conv2d_desc *d, samd_fmt xf, samd_fmt wf);
 
-/* Workspace bytes samd_conv2d_int8 needs (reordered int8 weights and per-filter sums). */
+/* Library utility: the workspace bytes samd_conv2d_int8 needs (reordered int8 weights
+ * and the per-filter weight sums of the zero-point correction). */
 int samd_conv2d_int8_workspace(const samd_conv2d_desc *d, samd_fmt xf, size_t *bytes);
 
 /* The native 8-bit baseline of Sec. 7: the same convolution on values unpacked to
@@ -272,7 +284,9 @@ int samd_conv2d_int8_prepare(const int8_t *w, samd_fmt wf, const samd_conv2d_des
 int samd_conv2d_int8_prepared(const void *x, samd_fmt xf, samd_fmt wf, const samd_conv2d_desc *d, int32_t *y,
                               const void *ws, size_t ws_bytes, hipStream_t stream);
 
-/* Maximum of n int32 values, written to *dev_max (device); n >= 1. */
+/* Library utility for the requantisation between layers (the layer maximum that fixes
+ * the shift of samd_relu_requant_pack): maximum of n int32 values, written to *dev_max
+ * (device); n >= 1. */
 int samd_max_i32(const int32_t *src, int64_t n, int32_t *dev_max, hipStream_t stream);
 
 /* ReLU and requantisation to unsigned b bits between layers (the paper gives no rule;

@@ -21,7 +21,7 @@ __all__ = ["Fmt", "Conv2dDesc", "Conv1dPlan", "Conv2dPlan", "SamdError", "lib", 
            "conv2d_workspace", "conv2d", "conv2d_prepare", "conv2d_prepared",
            "conv2d_stage", "conv2d_accumulate",
            "conv2d_int8_prepare", "conv2d_int8_prepared", "conv2d_int8_workspace", "conv2d_int8", "max_i32",
-           "relu_requant_pack", "relu_requant_nhwc_u8", "out_hw", "LIB_PATH"]
+           "relu_requant_pack", "relu_requant_nhwc_u8", "out_hw", "peak_launch", "peak_work", "LIB_PATH"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsamd.so")
 
@@ -46,6 +46,8 @@ class Conv2dDesc(ctypes.Structure):
 
     @classmethod
     def of(cls, shape) -> "Conv2dDesc":
+        if isinstance(shape, cls):
+            return shape
         vals = shape.as_tuple() if hasattr(shape, "as_tuple") else tuple(shape)
         return cls(*[int(v) for v in vals])
 
@@ -121,6 +123,8 @@ def lib():
             "samd_conv2d_untune": (ctypes.c_int, [ctypes.POINTER(Conv2dDesc), Fmt, Fmt]),
             "samd_conv2d_use_plan": (ctypes.c_int, [ctypes.POINTER(Conv2dDesc), Fmt, Fmt,
                                                     ctypes.POINTER(Conv2dPlan)]),
+            "samd_peak_launch": (ctypes.c_int, [ctypes.c_int, _i64, _i32, _p, _p, _i64, _p]),
+            "samd_peak_work": (ctypes.c_double, [ctypes.c_int, _i64, _i32, _i64]),
         }
         for name, (res, args) in sigs.items():
             fn = getattr(L, name)
@@ -512,3 +516,33 @@ def relu_requant_stage(acc: torch.Tensor, dev_max: torch.Tensor, bits: int, wfmt
                                          ctypes.byref(d), ws.data_ptr(), _ws_bytes(ws), _opt(dev_shift, "dev_shift"),
                                          _stream(acc)))
     return ws
+
+
+PEAK_MAD_I64_I32, PEAK_VALU_I32, PEAK_MFMA_I8, PEAK_COPY, PEAK_READ = 0, 1, 2, 3, 4
+
+
+def peak_work(kind: int, iters: int, blocks: int, nbytes: int = 0) -> float:
+    """Work (lane ops, multiply-adds or bytes) of one peak_launch with these arguments."""
+    w = lib().samd_peak_work(kind, iters, blocks, nbytes)
+    if w < 0:
+        raise ValueError("bad peak microbenchmark arguments")
+    return w
+
+
+def peak_launch(kind: int, iters: int, blocks: int, dst: torch.Tensor, src: Optional[torch.Tensor] = None,
+                nbytes: int = 0) -> None:
+    """Enqueue one ceiling microbenchmark (include/samd_peaks.h) on the current stream."""
+    if kind in (PEAK_COPY, PEAK_READ):
+        if src is None:
+            raise ValueError("copy and read need src")
+        _min(src, None, 0, "src")
+        if src.numel() * src.element_size() < nbytes:
+            raise ValueError("src is shorter than nbytes")
+        need = nbytes if kind == PEAK_COPY else 4 * blocks
+    else:
+        need = 4 * 256 * blocks
+    _dev(dst, None, "dst")
+    if dst.numel() * dst.element_size() < need:
+        raise ValueError(f"dst must hold {need} bytes")
+    _check(lib().samd_peak_launch(kind, iters, blocks, None if src is None else src.data_ptr(), dst.data_ptr(),
+                                  nbytes, _stream(dst)))

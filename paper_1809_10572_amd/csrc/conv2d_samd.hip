@@ -9,12 +9,15 @@
 //    phase L bits apart (temporary spacer bits), negative values sign-extended, so that
 //    each word is the int32 sum_i v_i 2^(i L); rows of the zero padding are written too;
 //  * conv2d_samd_kernel: a workgroup owns a tile of output rows of one image and wm*8
-//    output channels.  Per chunk of input channels it copies the tile's operand words
-//    into LDS (double-buffered, one barrier per chunk); every wave multiplies them by its
-//    8 SGPR-resident kernel words and adds the exact signed 32x32 -> 64-bit products
-//    into 64-bit accumulators (v_mad_i64_i32).  Every G channels the accumulators are
-//    decoded - fix-up, lane extraction - and added into an LDS tile of int32 outputs,
-//    which also performs the overlap-add of neighbouring words' partial lanes.
+//    output channels.  Every lane reads its operand words straight from the spread buffer
+//    with raw buffer loads (L1/L2-resident: each word is reused by the workgroup's channel
+//    waves and kernel rows), every wave holds its 8 kernel words of a step in SGPRs
+//    (scalar loads from its kernel-word stream) and adds the exact signed 32x32 -> 64-bit
+//    products into 64-bit accumulators (v_mad_i64_i32).  Every G channels the
+//    accumulators are decoded - fix-up, lane extraction - and added into an LDS tile of
+//    int32 outputs (the tile is the only LDS use), which also performs the overlap-add of
+//    neighbouring words' partial lanes and sums the channel-split waves; finished rows
+//    are stored from the tile.
 #include <hip/hip_runtime.h>
 
 #include <climits>
@@ -613,13 +616,12 @@ int launch_conv2d_prepare(const uint32_t *w, const Conv2dGeom &g, void *ws, hipS
 int launch_conv2d_spread(const uint32_t *x, const Conv2dGeom &g, void *ws, hipStream_t s) {
     int32_t *xs = (int32_t *)((char *)ws + conv2d_xs_offset(g));
     // 2^qshift threads per row, each building about 2.5 of its words (words q, q + 2^qshift,
-    // ...): measured on MI355X, 2-3 words per thread amortise the per-thread row and
-    // address set-up best (one word per thread was 5-23 % slower at the mid-size layer)
-    int qshift = 0;
-    while ((1 << qshift) * 5 < 2 * g.nq && qshift < 8) ++qshift;   // up to 256 threads per row
+    // ...): one word per thread was 5-23 % slower at the mid-size layer
+    const int qshift = spread_qshift(g.nq);
     const int64_t nrows = (int64_t)g.N * g.C * g.Hp;
     const int rpb = 256 >> qshift;
     const int64_t blocks = (nrows + rpb - 1) / rpb;   // one thread group per row, no grid-stride loop
+    // the planner refuses layers that would need 2^32 threads or more (addressable())
     if (blocks * 256 > (int64_t)0xffffffff) {
         set_error("conv2d operand spread: more than 2^32 threads in one launch");
         return SAMD_EUNSUPPORTED;

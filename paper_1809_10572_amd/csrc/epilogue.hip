@@ -177,11 +177,11 @@ int launch_relu_requant_pack(const int32_t *acc, int64_t rows, int64_t len, cons
 int launch_relu_requant_stage(const int32_t *acc, const int32_t *dev_max, const Conv2dGeom &g, void *ws,
                               int32_t *dev_shift, hipStream_t s) {
     int32_t *xs = (int32_t *)((char *)ws + conv2d_xs_offset(g));
-    int qshift = 0;
-    while ((1 << qshift) * 5 < 2 * g.nq && qshift < 8) ++qshift;   // ~2.5 words per thread, as the spread
+    const int qshift = spread_qshift(g.nq);   // ~2.5 words per thread, as the spread
     const int64_t nrows = (int64_t)g.N * g.C * g.Hp;
     const int rpb = kBlock >> qshift;
     const int64_t blocks = (nrows + rpb - 1) / rpb;   // one thread group per row, no grid-stride loop
+    // the planner refuses layers that would need 2^32 threads or more (addressable())
     if (blocks * kBlock > (int64_t)0xffffffff) {
         set_error("relu_requant_stage: more than 2^32 threads in one launch");
         return SAMD_EUNSUPPORTED;

@@ -67,6 +67,22 @@ bool split_taps(int count, int kmax, int *t0, int *nt, int &ngroups) {
     return true;
 }
 
+// Index ranges the kernels assume, checked for every plan before it is used or listed:
+//  - one image's operand words (and one spare channel) are addressed with 32-bit byte
+//    offsets, and padded rows with 32-bit indices;
+//  - a wave's slice of the kernel-word stream (cpw channels, plus the padding steps) is
+//    indexed with 32-bit word offsets;
+//  - the operand spread and the fused epilogue give every padded row 2^q threads in one
+//    launch of fewer than 2^32 threads.
+bool addressable(const samd_conv2d_desc &d, const Conv2dGeom &g) {
+    const int64_t two31 = (int64_t)1 << 31;
+    const int64_t rows = (int64_t)d.N * d.C * g.Hp;
+    const int rpb = 256 >> spread_qshift(g.nq);
+    return (int64_t)(d.C + 1) * g.Hp * g.ntw * g.nq * 4 < two31 && rows < two31 &&
+           ((int64_t)g.cpw * g.nrt + kStreamPad) * kWaveM < two31 &&
+           (rows + rpb - 1) / rpb * 256 <= (int64_t)0xffffffff;
+}
+
 // Launch shape of one lane geometry: output rows per thread (rh), row groups per wave,
 // output-channel waves (wm) and channel-slice waves (ks) per workgroup, and whether the
 // lane's rows share operand loads (3-row, stride-1 kernels).  Every candidate is priced
@@ -76,7 +92,7 @@ bool split_taps(int count, int kmax, int *t0, int *nt, int &ngroups) {
 // grows with the waves resident per SIMD (latency hiding), plus the last item's drain and
 // the operand-spread pass.  Returns false when no tile fits the LDS.  With `all`, every
 // launch shape that fits is also appended to it, priced.
-bool place_launch(const samd_conv2d_desc &d, Conv2dGeom &c, std::vector<Conv2dGeom> *all = nullptr) {
+bool place_launch(const samd_conv2d_desc &d, Conv2dGeom &c, std::vector<Conv2dGeom> *all, bool &range_limited) {
     const int grp_max = 64 / c.nqs;
     const bool rows_ok = d.KH == 3 && d.stride_h == 1 && (c.ntw == 1 || c.ntw == 2);
     bool found = false;
@@ -126,6 +142,10 @@ bool place_launch(const samd_conv2d_desc &d, Conv2dGeom &c, std::vector<Conv2dGe
                     t.tiles = d.N * t.row_tiles * c.ncs;
                     t.kw_words = (int64_t)t.nmb * wm * ((int64_t)d.C * c.nrt + kStreamPad) * kWaveM;
                     t.spread_words = (int64_t)d.N * d.C * c.Hp * c.ntw * c.nq;
+                    if (!addressable(d, t)) {
+                        range_limited = true;
+                        continue;
+                    }
 
                     // wave-instructions and operand loads of one workgroup's item
                     const double waves = (double)wm * ks;
@@ -193,7 +213,7 @@ int search_lanes(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, int xoff, 
     const int S = d.stride_w;
     g.Kmax = (d.KW + S - 1) / S;
     const i128 prod = max_abs(xf.bits, xf.is_signed) * max_abs(wf.bits, wf.is_signed);
-    bool found = false;
+    bool found = false, range_limited = false;
     best.cost = 1e300;
 
     for (int L = 2; L <= 31; ++L) {
@@ -277,7 +297,7 @@ int search_lanes(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, int xoff, 
             // the multiply-adds alone, spread perfectly over every SIMD, bound the cost below
             const double floor_cost = (double)d.N * c.Ho * c.ncs * c.nqs * d.M * d.C * c.nrt / 64.0 / 1024.0;
             if (!all && found && floor_cost >= best.cost) continue;
-            if (!place_launch(d, c, all)) continue;
+            if (!place_launch(d, c, all, range_limited)) continue;
             if (c.cost < best.cost) {
                 best = c;
                 found = true;
@@ -285,9 +305,13 @@ int search_lanes(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, int xoff, 
         }
     }
     if (!found) {
-        char buf[160];
-        snprintf(buf, sizeof buf, "no exact SAMD lane geometry for %d-bit x %d-bit, KW=%d stride %d, Wo=%d",
-                 xf.bits, wf.bits, d.KW, d.stride_w, g.Wo);
+        char buf[256];
+        if (range_limited)
+            snprintf(buf, sizeof buf, "the layer exceeds the kernels' index ranges (operand words of one image "
+                     "above 2 GiB, a kernel-word slice above 2^31 words, or an operand spread of 2^32 threads or more)");
+        else
+            snprintf(buf, sizeof buf, "no exact SAMD lane geometry for %d-bit x %d-bit, KW=%d stride %d, Wo=%d",
+                     xf.bits, wf.bits, d.KW, d.stride_w, g.Wo);
         err = buf;
         return SAMD_EUNSUPPORTED;
     }
@@ -338,13 +362,6 @@ PlanKey plan_key(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf) {
             xf.bits, xf.is_signed, wf.bits, wf.is_signed};
 }
 
-// The kernels address one image's operand words (and one spare channel) with 32-bit
-// byte offsets, and padded rows with 32-bit indices.
-bool addressable(const samd_conv2d_desc &d, const Conv2dGeom &g) {
-    return (int64_t)(d.C + 1) * g.Hp * g.ntw * g.nq * 4 < ((int64_t)1 << 31) &&
-           (int64_t)d.N * d.C * g.Hp < ((int64_t)1 << 31);
-}
-
 }  // namespace
 
 int plan_conv2d(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, Conv2dGeom &g, std::string &err) {
@@ -364,7 +381,8 @@ int plan_conv2d(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, Conv2dGeom 
     }
     int st = search_conv2d(d, xf, wf, g, err);
     if (st == SAMD_OK && !addressable(d, g)) {
-        err = "operand words of one image exceed 2 GiB";
+        err = "the layer exceeds the kernels' index ranges (operand words of one image above 2 GiB, a kernel-word "
+              "slice above 2^31 words, or an operand spread of 2^32 threads or more)";
         st = SAMD_EUNSUPPORTED;
     }
     if (st == SAMD_OK) {
@@ -384,7 +402,8 @@ int conv2d_candidates(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, int m
     int st = search_conv2d(d, xf, wf, model, err, &all);
     if (st) return st;
     if (!addressable(d, model)) {
-        err = "operand words of one image exceed 2 GiB";
+        err = "the layer exceeds the kernels' index ranges (operand words of one image above 2 GiB, a kernel-word "
+              "slice above 2^31 words, or an operand spread of 2^32 threads or more)";
         return SAMD_EUNSUPPORTED;
     }
     std::vector<Conv2dGeom> keep;

@@ -142,6 +142,15 @@ int launch_relu_requant_nhwc_u8(const int32_t *acc, int N, int C, int H, int W, 
 // Error detail for the calling thread.
 void set_error(const std::string &msg);
 
+// Threads per padded row of the operand spread and the fused epilogue, as a power of two
+// 2^q: about 2.5 operand words per thread (measured on MI355X, 2-3 words per thread
+// amortise the per-thread row and address set-up best), at most 256.
+inline int spread_qshift(int nq) {
+    int q = 0;
+    while ((1 << q) * 5 < 2 * nq && q < 8) ++q;
+    return q;
+}
+
 inline int64_t row_words(int64_t len, int bits) {
     const int64_t per = 32 / bits;
     return (len + per - 1) / per;

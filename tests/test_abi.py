@@ -1,6 +1,7 @@
-"""The C ABI without a GPU: the library loads, exports every function include/samd.h
+"""The C ABI without a GPU: the library loads, exports every function include/*.h
 declares, and rejects bad arguments on the host before any HIP call."""
 import ctypes
+import glob
 import os
 import re
 
@@ -10,7 +11,7 @@ import paper_1809_10572_amd as samd
 from paper_1809_10572_amd import Conv2dDesc, Fmt
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-HEADER = os.path.join(ROOT, "include", "samd.h")
+HEADERS = sorted(glob.glob(os.path.join(ROOT, "include", "*.h")))
 
 OK, EINVAL, EALIGN, EUNSUP, EOVERFLOW, EHIP, ENOSPC = 0, -1, -2, -3, -4, -5, -6
 MID = Conv2dDesc(8, 128, 56, 56, 128, 3, 3, 1, 1, 1, 1)
@@ -19,14 +20,17 @@ P4, P1 = 0x10000, 0x10001
 
 
 def declared_functions():
-    text = open(HEADER).read()
-    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(samd_[a-z0-9_]+)\s*\(", text)))
+    names = set()
+    for h in HEADERS:
+        text = re.sub(r"/\*.*?\*/", "", open(h).read(), flags=re.S)
+        names |= set(re.findall(r"\b(samd_[a-z0-9_]+)\s*\(", text))
+    return sorted(names)
 
 
 def test_library_exports_every_declared_function():
+    assert any(h.endswith("samd.h") for h in HEADERS) and any(h.endswith("samd_peaks.h") for h in HEADERS)
     names = declared_functions()
-    assert len(names) >= 14
+    assert len(names) >= 16 and "samd_peak_launch" in names
     L = ctypes.CDLL(samd.LIB_PATH)
     for n in names:
         assert hasattr(L, n), n
@@ -235,3 +239,42 @@ def test_use_plan_installs_a_candidate():
     assert samd.plan_key(samd.conv2d_plan(shape, xf, wf)) == samd.plan_key(model)
     L = samd.lib()
     assert L.samd_conv2d_use_plan(ctypes.byref(MID), xf, wf, None) == EINVAL
+
+
+def test_peak_validation():
+    L = samd.lib()
+    f = L.samd_peak_launch
+    f.restype, f.argtypes = ctypes.c_int, [ctypes.c_int, ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p,
+                                           ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p]
+    assert f(9, 1, 1, None, P4, 0, None) == EINVAL            # unknown kind
+    assert f(0, 0, 1, None, P4, 0, None) == EINVAL            # no trips
+    assert f(0, 1, 0, None, P4, 0, None) == EINVAL            # no workgroups
+    assert f(0, 1, 1, None, None, 0, None) == EINVAL          # no output
+    assert f(3, 1, 1, None, P4, 1024, None) == EINVAL         # copy without a source
+    assert f(3, 1, 1, P4, P4, 1000, None) == EINVAL           # not a multiple of 16 bytes
+    assert f(3, 1, 1, P4 + 4, P4, 1024, None) == EALIGN       # misaligned source
+    assert samd.peak_work(0, 10, 2) == 2 * 256 * 10 * 8
+    assert samd.peak_work(2, 10, 2) == 2 * 4 * 10 * 4 * 16 * 16 * 64
+    assert samd.peak_work(3, 1, 1, 1 << 20) == 2 * (1 << 20)
+
+
+def test_planner_keeps_kernel_word_slices_within_32_bit_offsets():
+    # 3x3 layer with 10^8 one-bit channels: a single wave slice of every channel would
+    # index 2.4e9 kernel words; every listed candidate must split the channels enough
+    d = Conv2dDesc(1, 100_000_000, 1, 1, 8, 3, 3, 1, 1, 1, 1)
+    for p in samd.conv2d_candidates(d, Fmt(1, False), Fmt(1, False), 64):
+        cpw = -(-d.C // p.split_waves)
+        assert (cpw * d.KH * p.tap_words + 6) * 8 < 2 ** 31, (p.split_waves, p.tap_words)
+
+
+def test_planner_refuses_a_spread_of_2_to_the_32_threads():
+    # 2^24 padded rows of 651 operand words (8-bit lanes, two values per word) would need
+    # 2^32 spread threads: refused by the planner, before any HIP call
+    d = Conv2dDesc(65536, 8, 30, 1300, 8, 3, 3, 1, 1, 1, 1)
+    L = samd.lib()
+    plan = samd.Conv2dPlan()
+    st = L.samd_conv2d_plan_query(ctypes.byref(d), Fmt(8, False), Fmt(8, True), ctypes.byref(plan))
+    assert st == EUNSUP, st
+    assert b"index ranges" in L.samd_last_error()
+    n = ctypes.c_size_t(0)
+    assert L.samd_conv2d_workspace(ctypes.byref(d), Fmt(8, False), Fmt(8, True), ctypes.byref(n)) == EUNSUP
