@@ -30,6 +30,7 @@ import time
 PEAK_VALU_OPS = 256 * 64 * 2.4e9      # int32 VALU lane-ops/s: 256 CUs x 64 lanes x 2.4 GHz
 PEAK_HBM = 8.0e12                     # bytes/s
 PEAK_I8_MACS = 2.5e15                 # dense int8 matrix-core MAC/s (5.0 POP/s)
+PEAK_LDS = 256 * 256 * 2.4e9          # LDS read bytes/s: 256 CUs x 256 B/clk x 2.4 GHz
 
 
 def parse():
@@ -56,6 +57,9 @@ def parse():
     p.add_argument("--no-tune", action="store_true",
                    help="use the planner's model plans (default: time the top candidates at set-up)")
     p.add_argument("--tune-candidates", type=int, default=16, help="candidate plans timed per bit width")
+    p.add_argument("--no-tune-int8", action="store_true",
+                   help="use the int8 baseline's own launch choice (default: time every candidate launch at "
+                        "set-up and keep the fastest, as the SAMD plans are tuned)")
     p.add_argument("--streams", type=int, default=4,
                    help="streams the step's independent bit widths are spread over (every stream at the "
                         "default priority)")
@@ -80,6 +84,12 @@ def parse():
                         "the 2^20-value conv1d (b = 1..8, 3 and 5 taps) and the extremes-heavy signed layer")
     p.add_argument("--lanewise", action="store_true",
                    help="instead of the default workload, time lane-wise add/sub/mul/scale on packed words (GB/s)")
+    p.add_argument("--int8-counters", action="store_true",
+                   help="launch every int8 baseline candidate once on the mid-size layer (b = 4), eagerly, and exit "
+                        "(the program rocprofv3 --pmc passes of the int8 kernels run)")
+    p.add_argument("--int8-summary", nargs="+", metavar="PMC_DIR",
+                   help="print the counter table of --int8-counters runs profiled with rocprofv3 --pmc (one "
+                        "folder per pass)")
     p.add_argument("--valu-summary", metavar="PMC_DIR",
                    help="print the VALU / texture-path counter table of a --counters run profiled with "
                         "rocprofv3 --pmc " + VALU_COUNTERS)
@@ -303,27 +313,132 @@ def timed_graph(fn, reps, warm_s, samples=5):
     return timed_graph_stats(fn, reps, warm_s, samples)[0]
 
 
+def tune_int8(samd, shape, xf, wf, run, warm_s=0.05):
+    """Set-up: time every launch the int8 baseline can make for the layer (run() makes one
+    call) and install the fastest; returns (the chosen plan as a dict, {launch: us})."""
+    times = {}
+    best, best_t = None, None
+    for plan in samd.conv2d_int8_candidates(shape, xf, wf):
+        samd.conv2d_int8_use_plan(shape, xf, wf, plan)
+        t = timed_graph(run, 10, warm_s, samples=3)
+        key = f"{'halo' if plan.halo else 'im2col'} {plan.mtile}x{plan.positions}"
+        times[key] = round(t * 1e6, 2)
+        if best_t is None or t < best_t:
+            best, best_t = plan, t
+    samd.conv2d_int8_use_plan(shape, xf, wf, best)
+    return ({"halo": best.halo, "mtile": best.mtile, "positions": best.positions,
+             "row_segments": best.row_segments}, times)
+
+
+INT8_COUNTERS = ("SQ_WAVES SQ_BUSY_CYCLES SQ_WAVE_CYCLES SQ_WAIT_INST_ANY SQ_VALU_MFMA_BUSY_CYCLES "
+                 "SQ_INSTS_VALU_MFMA_MOPS_I8 SQ_WAIT_INST_LDS SQ_LDS_BANK_CONFLICT GRBM_GUI_ACTIVE TA_TA_BUSY_sum "
+                 "TD_TD_BUSY_sum",
+                 "TCP_TCC_READ_REQ_sum TCP_TCC_WRITE_REQ_sum TCP_TCC_READ_REQ_LATENCY_sum TCP_PENDING_STALL_CYCLES_sum "
+                 "TCC_HIT_sum TCC_MISS_sum TCC_EA0_RDREQ_sum TCC_EA0_WRREQ_sum GRBM_GUI_ACTIVE SQ_INSTS_VMEM_RD "
+                 "SQ_INSTS_VMEM_WR SQ_INSTS_LDS")
+
+
+def run_int8_counters(args):
+    """One eager launch of every int8 baseline candidate on the mid-size layer (4-bit
+    unsigned activations, 4-bit signed weights), each after an untimed launch of the
+    same candidate; prints the launch order."""
+    import numpy as np
+    import torch
+
+    import paper_1809_10572_amd as samd
+    import samd_workloads as wl
+
+    dev = torch.device("cuda:0")
+    shape, b = wl.MID, 4
+    case = wl.conv2d_case(3, b)
+    xf, wf = samd.Fmt(b, False), samd.Fmt(b, True)
+    x_nhwc = torch.from_numpy(np.ascontiguousarray(np.transpose(case.x, (0, 2, 3, 1))).astype(np.uint8)).to(dev)
+    w8 = torch.from_numpy(case.w.astype(np.int8)).to(dev)
+    ws8 = samd.conv2d_int8_prepare(w8, wf, shape, xf)
+    Ho, Wo = samd.out_hw(shape)
+    y = torch.empty((shape.N, shape.M, Ho, Wo), dtype=torch.int32, device=dev)
+    for plan in samd.conv2d_int8_candidates(shape, xf, wf):
+        samd.conv2d_int8_use_plan(shape, xf, wf, plan)
+        for _ in range(2):
+            samd.conv2d_int8_prepared(x_nhwc, xf, wf, shape, ws8, out=y)
+        torch.cuda.synchronize()
+        print(f"int8-counters: {'halo' if plan.halo else 'im2col'} {plan.mtile}x{plan.positions} launched twice",
+              flush=True)
+    samd.conv2d_int8_use_plan(shape, xf, wf, None)
+
+
+def int8_summary(folders):
+    """Markdown table of rocprofv3 --pmc passes over --int8-counters: per int8 launch (the
+    second of each candidate's two dispatches), its duration and counters."""
+    import csv
+    import glob
+
+    import paper_1809_10572_amd as samd
+    import samd_workloads as wl
+
+    disp = {}
+    for folder in folders:
+        files = glob.glob(os.path.join(folder, "**", "*counter_collection.csv"), recursive=True)
+        if len(files) != 1:
+            raise SystemExit(f"expected one counter_collection.csv under {folder}, found {len(files)}")
+        rows = list(csv.DictReader(open(files[0])))
+        ids = sorted({int(r["Dispatch_Id"]) for r in rows if "conv2d_i8" in r["Kernel_Name"]})
+        for k, d in enumerate(ids):
+            e = disp.setdefault(k, {"c": {}, "dur": []})
+            for r in rows:
+                if int(r["Dispatch_Id"]) == d:
+                    e["name"] = r["Kernel_Name"].split("(")[0].replace("samd::(anonymous namespace)::", "")
+                    e["c"][r["Counter_Name"]] = e["c"].get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+                    e["dur"].append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-9)
+    cands = samd.conv2d_int8_candidates(wl.MID, samd.Fmt(4, False), samd.Fmt(4, True))
+    Ho, Wo = samd.out_hw(wl.MID)
+    macs = wl.MID.N * wl.MID.M * Ho * Wo * wl.MID.C * 9
+    out = ["| launch | kernel | dispatch us | MFMA busy % | MAC/s % of peak | waves | wait % of wave cycles | "
+           "LDS bank conflicts / LDS wait | TA busy % | L1->L2 read requests | L2 hit % | L2->HBM read req | "
+           "L1->L2 read latency (cycles per req) |",
+           "|---|---|---|---|---|---|---|---|---|---|---|---|---|"]
+    for k in sorted(disp):
+        if k % 2 == 0:
+            continue   # the first launch of each candidate warms it
+        e, c = disp[k], disp[k]["c"]
+        plan = cands[k // 2]
+        dur = min(e["dur"])
+        gui = c.get("GRBM_GUI_ACTIVE", 0) or 1
+        def g(name):
+            return c.get(name, float("nan"))
+        hit, miss = g("TCC_HIT_sum"), g("TCC_MISS_sum")
+        out.append(f"| {'halo' if plan.halo else 'im2col'} {plan.mtile}x{plan.positions} | {e['name']} | "
+                   f"{dur * 1e6:.2f} | {100 * g('SQ_VALU_MFMA_BUSY_CYCLES') / (gui * 1024):.1f} | "
+                   f"{100 * macs / dur / PEAK_I8_MACS:.1f} | {g('SQ_WAVES'):.0f} | "
+                   f"{100 * g('SQ_WAIT_INST_ANY') / max(g('SQ_WAVE_CYCLES'), 1):.0f} | "
+                   f"{g('SQ_LDS_BANK_CONFLICT'):.3g} / {g('SQ_WAIT_INST_LDS'):.3g} | "
+                   f"{100 * g('TA_TA_BUSY_sum') / (256 * gui):.0f} | {g('TCP_TCC_READ_REQ_sum'):.4g} | "
+                   f"{100 * hit / max(hit + miss, 1):.1f} | {g('TCC_EA0_RDREQ_sum'):.4g} | "
+                   f"{g('TCP_TCC_READ_REQ_LATENCY_sum') / max(g('TCP_TCC_READ_REQ_sum'), 1):.0f} |")
+    return "\n".join(out)
+
+
 SPEC = {"mad": (PEAK_VALU_OPS, "T lane-ops/s", "alu"), "valu": (PEAK_VALU_OPS, "T lane-ops/s", "alu"),
         "mfma_i8": (PEAK_I8_MACS, "T MAC/s", "mfma"), "copy": (PEAK_HBM, "TB/s", "hbm"),
-        "read": (PEAK_HBM, "TB/s", "hbm")}
+        "read": (PEAK_HBM, "TB/s", "hbm"), "write": (PEAK_HBM, "TB/s", "hbm"), "lds": (PEAK_LDS, "TB/s", "lds")}
 
 
-def measure_peak(samd, kind, seconds=0.3):
+def measure_peak(samd, kind, seconds=0.3, waves_per_simd=8):
     """Rate of one ceiling microbenchmark (include/samd_peaks.h) in work units per second:
     the median of 5 HIP-event-timed launches after `seconds` of back-to-back launches."""
     import torch
     code = {"mad": samd.PEAK_MAD_I64_I32, "valu": samd.PEAK_VALU_I32, "mfma_i8": samd.PEAK_MFMA_I8,
-            "copy": samd.PEAK_COPY, "read": samd.PEAK_READ}[kind]
+            "copy": samd.PEAK_COPY, "read": samd.PEAK_READ, "write": samd.PEAK_WRITE, "lds": samd.PEAK_LDS}[kind]
     dev = torch.device("cuda:0")
     nbytes = 1 << 30
-    if kind in ("copy", "read"):
+    if kind in ("copy", "read", "write"):
         blocks, iters = 256 * 8 * 4, 1
-        src = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+        src = torch.empty(nbytes if kind != "write" else 16, dtype=torch.uint8, device=dev)
         src.fill_(1)
-        dst = torch.empty(nbytes if kind == "copy" else 4 * blocks, dtype=torch.uint8, device=dev)
+        dst = torch.empty(4 * blocks if kind == "read" else nbytes, dtype=torch.uint8, device=dev)
     else:
-        # 8 workgroups of 4 waves per compute unit: 8 waves per SIMD
-        blocks, iters, src = 256 * 8, (1 << 14) if kind != "mfma_i8" else (1 << 12), None
+        # waves_per_simd workgroups of 4 waves per compute unit
+        blocks, iters, src = 256 * waves_per_simd, (1 << 12) if kind in ("mfma_i8", "lds") else (1 << 14), None
         dst = torch.empty(4 * 256 * blocks, dtype=torch.uint8, device=dev)
     fn = lambda: samd.peak_launch(code, iters, blocks, dst, src, nbytes if src is not None else 0)
     fn()
@@ -364,13 +479,21 @@ def run_peaks(args):
     import paper_1809_10572_amd as samd
 
     rows = {}
-    for kind in ("mad", "valu", "mfma_i8", "copy", "read"):
+    for kind in ("mad", "valu", "mfma_i8", "copy", "read", "write", "lds"):
         rate = measure_peak(samd, kind, seconds=0.5)
         spec, unit, bound = SPEC[kind]
         rows[kind] = {"measured": round(rate / 1e12, 3), "spec": round(spec / 1e12, 3), "unit": unit,
                       "frac_of_spec": round(rate / spec, 4)}
         print(f"peaks: {kind} {rate / 1e12:.3f} {unit} ({rate / spec:.3f} of {spec / 1e12:.2f})", file=sys.stderr,
               flush=True)
+    # one wave per SIMD: what a kernel with a single wave per SIMD can issue
+    for kind in ("mad", "mfma_i8"):
+        rate = measure_peak(samd, kind, seconds=0.3, waves_per_simd=1)
+        spec, unit, bound = SPEC[kind]
+        rows[kind + "_1wave"] = {"measured": round(rate / 1e12, 3), "spec": round(spec / 1e12, 3), "unit": unit,
+                                 "frac_of_spec": round(rate / spec, 4)}
+        print(f"peaks: {kind} with one wave per SIMD {rate / 1e12:.3f} {unit} ({rate / spec:.3f} of {spec / 1e12:.2f})",
+              file=sys.stderr, flush=True)
     print(json.dumps({"metric": "MI355X ceilings, measured", "n_gpus": 1, "device": device_info(torch),
                       "notes": {"mad": "v_mad_i64_i32 (exact signed 32x32->64 multiply-add), 8 independent chains "
                                        "per lane, uniform multiplier; spec = 256 CUs x 64 lanes x 2.4 GHz",
@@ -378,7 +501,10 @@ def run_peaks(args):
                                 "mfma_i8": "v_mfma_i32_16x16x64_i8, 4 independent accumulators per wave; "
                                            "spec = 5.0 POP/s dense = 2.5 P MAC/s",
                                 "copy": "16-byte loads and stores, 1 GiB each way, bytes read + written",
-                                "read": "16-byte loads of 1 GiB"},
+                                "read": "16-byte loads of 1 GiB",
+                                "write": "16-byte stores of 1 GiB",
+                                "lds": "ds_read_b128, conflict-free, 8 per trip; spec = 256 CUs x 256 B/clk x 2.4 GHz",
+                                "*_1wave": "the same loop with one wave per SIMD (256 workgroups of 4 waves)"},
                       "peaks": rows}), flush=True)
 
 
@@ -412,6 +538,8 @@ def run_configs(args):
         Ho, Wo = samd.out_hw(shape)
         y = torch.empty((shape.N, shape.M, Ho, Wo), dtype=torch.int32, device=dev)
         y8 = torch.empty_like(y)
+        if not args.no_tune_int8:
+            tune_int8(samd, shape, xf, wf, lambda: samd.conv2d_int8_prepared(x_nhwc, xf, wf, shape, ws8, out=y8))
         t = timed_graph(lambda: samd.conv2d_prepared(xp, xf, wf, shape, ws, out=y), args.reps, args.kernel_warm_s)
         ta = timed_graph(lambda: samd.conv2d_accumulate(xf, wf, shape, ws, out=y), args.reps, args.kernel_warm_s)
         t8 = timed_graph(lambda: samd.conv2d_int8_prepared(x_nhwc, xf, wf, shape, ws8, out=y8), args.reps,
@@ -491,6 +619,8 @@ def run_vggb(args):
             ws8 = samd.conv2d_int8_prepare(w8, f, shape, f)
             y = torch.empty((shape.N, shape.M, Ho, Wo), dtype=torch.int32, device=dev)
             y8 = torch.empty_like(y)
+            if not args.no_tune_int8:
+                tune_int8(samd, shape, f, f, lambda: samd.conv2d_int8_prepared(x_nhwc, f, f, shape, ws8, out=y8))
             t_pack = timed_graph(lambda: samd.pack(x, b, True, out=xp), args.reps, args.kernel_warm_s)
             t_samd = timed_graph(lambda: samd.conv2d_prepared(xp, f, f, shape, ws, out=y), args.reps,
                                  args.kernel_warm_s)
@@ -587,6 +717,15 @@ def run_stack(args):
             for li, l in enumerate(lys):
                 samd.conv2d_tune(xps[li], xf, wps[li], wf, l, candidates=args.tune_candidates, reps=3)
                 wss[li] = samd.conv2d_prepare(wps[li], wf, l, xf)
+            torch.cuda.synchronize()
+
+        if not args.no_tune_int8:
+            chain_packed()   # activations of every layer for the int8 chain's inputs
+            for li, l in enumerate(lys):
+                if li > 0:
+                    samd.max_i32(ys[li - 1], out=mx)
+                    samd.relu_requant_nhwc_u8(ys[li - 1], mx, bits, out=x8s[li])
+                tune_int8(samd, l, xf, wf, lambda: samd.conv2d_int8_prepared(x8s[li], xf, wf, l, ws8[li], out=ys[li]))
             torch.cuda.synchronize()
 
         def chain_int8():
@@ -703,6 +842,12 @@ def main():
     if args.peaks:
         run_peaks(args)
         return
+    if args.int8_counters:
+        run_int8_counters(args)
+        return
+    if args.int8_summary:
+        print(int8_summary(args.int8_summary))
+        return
     if args.vggb:
         run_vggb(args)
         return
@@ -780,6 +925,17 @@ def main():
     # the layer's kernel words are prepared once per layer (weights are constant)
     for L in layers:
         samd.conv2d_prepare(L["wp"], L["wf"], shape, L["xf"], ws=L["ws"])
+    # the int8 baseline's launch, chosen by timing its candidates on the same layer
+    for L in layers:
+        if args.no_tune_int8:
+            p8 = samd.conv2d_int8_plan(shape, L["xf"], L["wf"])
+            L["int8_plan"], L["int8_cands"] = {"halo": p8.halo, "mtile": p8.mtile, "positions": p8.positions,
+                                               "row_segments": p8.row_segments}, None
+        else:
+            L["int8_plan"], L["int8_cands"] = tune_int8(
+                samd, shape, L["xf"], L["wf"],
+                lambda: samd.conv2d_int8_prepared(L["x_nhwc"], L["xf"], L["wf"], shape, L["ws8"], out=L["y8"]))
+    torch.cuda.synchronize()
 
     if args.counters:
         # one eager launch of each kernel per bit width, in step order, then the calibration
@@ -936,6 +1092,7 @@ def main():
             "hbm_bytes_counted": (traffic["per_bits"][str(b)]["fetch_bytes"] + traffic["per_bits"][str(b)]["write_bytes"]
                                   if traffic and str(b) in traffic["per_bits"] else None),
             "int8_mfma_frac": round(macs / t8 / PEAK_I8_MACS, 4),
+            "int8_launch": L["int8_plan"], "int8_candidates_us": L["int8_cands"],
             "lane_bits": p.lane_bits, "lanes": p.lanes, "tap_words": p.tap_words,
             "flush_channels": p.flush_channels, "macs_per_mad": round(p.macs_per_mad, 2),
             "tile": f"{p.rows_per_block}x{p.mblock}", "split_waves": p.split_waves,

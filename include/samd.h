@@ -278,6 +278,36 @@ int samd_conv2d_int8(const void *x, samd_fmt xf, const int8_t *w, samd_fmt wf,
                      const samd_conv2d_desc *d, int32_t *y, void *ws, size_t ws_bytes,
                      hipStream_t stream);
 
+/* Library utility (host only, for inspection and tests): the kernel and tile
+ * samd_conv2d_int8 uses for this layer when the activations are 16-byte aligned.
+ *   halo         1: the halo-tiled kernel (stride-1 layers with C a multiple of 16);
+ *                0: the im2col kernel (any other layer, or misaligned activations)
+ *   mtile        output channels per workgroup
+ *   positions    output positions per workgroup
+ *   row_segments 1: tiles are segments of one output row; 0: runs of positions that may
+ *                span several rows (halo kernel only)
+ *   lds_bytes    dynamic LDS per workgroup (halo kernel: two halo buffers)
+ *   workgroups   workgroups of one call */
+typedef struct {
+    int32_t halo, mtile, positions, row_segments, lds_bytes;
+    int64_t workgroups;
+} samd_conv2d_int8_plan;
+
+int samd_conv2d_int8_plan_query(const samd_conv2d_desc *d, samd_fmt xf, samd_fmt wf, samd_conv2d_int8_plan *out);
+
+/* Host-only, for measuring the baseline at its best (the SAMD path is tuned the same way,
+ * samd_conv2d_tune): every launch samd_conv2d_int8 can make for the layer, the halo
+ * tiles that fit first, then the im2col kernel; out holds max_count entries, *count
+ * receives the number written. */
+int samd_conv2d_int8_candidates(const samd_conv2d_desc *d, samd_fmt xf, samd_fmt wf, int32_t max_count,
+                                samd_conv2d_int8_plan *out, int32_t *count);
+
+/* Host-only: make `plan` (one of the layer's candidates, matched by halo, mtile and
+ * positions) the launch of (xf, *d) for every later samd_conv2d_int8 call in this process;
+ * plan NULL restores the library's own choice.  Process-wide state, like tuned SAMD
+ * plans; the workspace does not depend on it.  SAMD_EINVAL when no candidate matches. */
+int samd_conv2d_int8_use_plan(const samd_conv2d_desc *d, samd_fmt xf, samd_fmt wf, const samd_conv2d_int8_plan *plan);
+
 /* samd_conv2d_int8 split in weight reordering and convolution, as for samd_conv2d. */
 int samd_conv2d_int8_prepare(const int8_t *w, samd_fmt wf, const samd_conv2d_desc *d, samd_fmt xf, void *ws,
                              size_t ws_bytes, hipStream_t stream);

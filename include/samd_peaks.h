@@ -14,12 +14,16 @@
  *                          loads and stores); work = bytes read + bytes written
  *   SAMD_PEAK_READ         streaming read of `bytes` bytes from src, one 4-byte sum per
  *                          workgroup written to dst; work = bytes read
+ *   SAMD_PEAK_WRITE        streaming write of `bytes` bytes to dst (16-byte stores); work =
+ *                          bytes written
+ *   SAMD_PEAK_LDS          conflict-free 16-byte LDS reads (ds_read_b128), the int8
+ *                          baseline's operand path; work = bytes read from LDS
  * Arguments:
- *   iters   loop trips of the compute kinds (1 .. 2^24; ignored by COPY and READ)
+ *   iters   loop trips of the compute and LDS kinds (1 .. 2^24; ignored by COPY and READ)
  *   blocks  workgroups of 256 threads (1 .. 2^20)
  *   src, dst COPY: device buffers of `bytes` bytes each (`bytes` a positive multiple of 16,
  *           both 16-byte aligned).  READ: src of `bytes` bytes (same rules), dst of
- *           `blocks` int32.  Compute kinds: src is unused and dst receives one int32 per
+ *           `blocks` int32.  WRITE: dst of `bytes` bytes (same rules), src unused.  Compute kinds: src is unused and dst receives one int32 per
  *           thread (blocks * 256 values, so the work cannot be optimised away)
  * Returns SAMD_OK, SAMD_EINVAL for a bad argument, SAMD_EALIGN for a misaligned copy or
  * read buffer, or SAMD_EHIP for a launch error.
@@ -39,7 +43,9 @@ enum {
     SAMD_PEAK_VALU_I32 = 1,
     SAMD_PEAK_MFMA_I8 = 2,
     SAMD_PEAK_COPY = 3,
-    SAMD_PEAK_READ = 4
+    SAMD_PEAK_READ = 4,
+    SAMD_PEAK_LDS = 5,
+    SAMD_PEAK_WRITE = 6
 };
 
 int samd_peak_launch(int kind, int64_t iters, int32_t blocks, const void *src, void *dst, int64_t bytes,

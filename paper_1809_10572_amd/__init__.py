@@ -20,7 +20,8 @@ __all__ = ["Fmt", "Conv2dDesc", "Conv1dPlan", "Conv2dPlan", "SamdError", "lib", 
            "conv2d_use_plan", "plan_key",
            "conv2d_workspace", "conv2d", "conv2d_prepare", "conv2d_prepared",
            "conv2d_stage", "conv2d_accumulate",
-           "conv2d_int8_prepare", "conv2d_int8_prepared", "conv2d_int8_workspace", "conv2d_int8", "max_i32",
+           "conv2d_int8_prepare", "conv2d_int8_prepared", "conv2d_int8_workspace", "conv2d_int8", "conv2d_int8_plan",
+           "conv2d_int8_candidates", "conv2d_int8_use_plan", "max_i32",
            "relu_requant_pack", "relu_requant_nhwc_u8", "out_hw", "peak_launch", "peak_work", "LIB_PATH"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsamd.so")
@@ -61,6 +62,11 @@ class Conv2dPlan(ctypes.Structure):
                 ("col_segments", ctypes.c_int32), ("segment_columns", ctypes.c_int32),
                 ("macs_per_mad", ctypes.c_double), ("rows_per_thread", ctypes.c_int32),
                 ("shared_rows", ctypes.c_int32), ("model_cost", ctypes.c_double)]
+
+
+class Conv2dInt8Plan(ctypes.Structure):
+    _fields_ = [("halo", ctypes.c_int32), ("mtile", ctypes.c_int32), ("positions", ctypes.c_int32),
+                ("row_segments", ctypes.c_int32), ("lds_bytes", ctypes.c_int32), ("workgroups", ctypes.c_int64)]
 
 
 class Conv1dPlan(ctypes.Structure):
@@ -106,6 +112,12 @@ def lib():
             "samd_conv2d_int8_prepared": (ctypes.c_int, [_p, Fmt, Fmt, ctypes.POINTER(Conv2dDesc), _p, _p, _sz,
                                                          _p]),
             "samd_conv2d_int8_workspace": (ctypes.c_int, [ctypes.POINTER(Conv2dDesc), Fmt, ctypes.POINTER(_sz)]),
+            "samd_conv2d_int8_plan_query": (ctypes.c_int, [ctypes.POINTER(Conv2dDesc), Fmt, Fmt,
+                                                           ctypes.POINTER(Conv2dInt8Plan)]),
+            "samd_conv2d_int8_candidates": (ctypes.c_int, [ctypes.POINTER(Conv2dDesc), Fmt, Fmt, _i32,
+                                                           ctypes.POINTER(Conv2dInt8Plan), ctypes.POINTER(_i32)]),
+            "samd_conv2d_int8_use_plan": (ctypes.c_int, [ctypes.POINTER(Conv2dDesc), Fmt, Fmt,
+                                                         ctypes.POINTER(Conv2dInt8Plan)]),
             "samd_conv2d_int8": (ctypes.c_int, [_p, Fmt, _p, Fmt, ctypes.POINTER(Conv2dDesc), _p, _p, _sz, _p]),
             "samd_max_i32": (ctypes.c_int, [_p, _i64, _p, _p]),
             "samd_relu_requant_pack": (ctypes.c_int, [_p, _i64, _i64, _p, Fmt, _p, _p, _p]),
@@ -423,6 +435,28 @@ def conv2d_int8_prepared(x_nhwc: torch.Tensor, xfmt: Fmt, wfmt: Fmt, shape, ws: 
     return out
 
 
+def conv2d_int8_plan(shape, xfmt: Fmt, wfmt: Fmt) -> Conv2dInt8Plan:
+    """The kernel and tile conv2d_int8 uses for this layer (16-byte aligned activations)."""
+    plan = Conv2dInt8Plan()
+    _check(lib().samd_conv2d_int8_plan_query(ctypes.byref(Conv2dDesc.of(shape)), xfmt, wfmt, ctypes.byref(plan)))
+    return plan
+
+
+def conv2d_int8_candidates(shape, xfmt: Fmt, wfmt: Fmt) -> List[Conv2dInt8Plan]:
+    """Every launch conv2d_int8 can make for this layer (halo tiles first, then im2col)."""
+    arr = (Conv2dInt8Plan * MAX_CANDIDATES)()
+    n = _i32(0)
+    _check(lib().samd_conv2d_int8_candidates(ctypes.byref(Conv2dDesc.of(shape)), xfmt, wfmt, MAX_CANDIDATES, arr,
+                                             ctypes.byref(n)))
+    return [arr[i] for i in range(n.value)]
+
+
+def conv2d_int8_use_plan(shape, xfmt: Fmt, wfmt: Fmt, plan: Optional[Conv2dInt8Plan]) -> None:
+    """Make one of the layer's int8 candidates its launch (None: the library's own choice)."""
+    _check(lib().samd_conv2d_int8_use_plan(ctypes.byref(Conv2dDesc.of(shape)), xfmt, wfmt,
+                                           None if plan is None else ctypes.byref(plan)))
+
+
 def conv2d_int8_workspace(shape, xfmt: Fmt) -> int:
     n = _sz(0)
     _check(lib().samd_conv2d_int8_workspace(ctypes.byref(Conv2dDesc.of(shape)), xfmt, ctypes.byref(n)))
@@ -518,7 +552,7 @@ def relu_requant_stage(acc: torch.Tensor, dev_max: torch.Tensor, bits: int, wfmt
     return ws
 
 
-PEAK_MAD_I64_I32, PEAK_VALU_I32, PEAK_MFMA_I8, PEAK_COPY, PEAK_READ = 0, 1, 2, 3, 4
+PEAK_MAD_I64_I32, PEAK_VALU_I32, PEAK_MFMA_I8, PEAK_COPY, PEAK_READ, PEAK_LDS, PEAK_WRITE = 0, 1, 2, 3, 4, 5, 6
 
 
 def peak_work(kind: int, iters: int, blocks: int, nbytes: int = 0) -> float:
@@ -532,7 +566,9 @@ def peak_work(kind: int, iters: int, blocks: int, nbytes: int = 0) -> float:
 def peak_launch(kind: int, iters: int, blocks: int, dst: torch.Tensor, src: Optional[torch.Tensor] = None,
                 nbytes: int = 0) -> None:
     """Enqueue one ceiling microbenchmark (include/samd_peaks.h) on the current stream."""
-    if kind in (PEAK_COPY, PEAK_READ):
+    if kind == PEAK_WRITE:
+        need = nbytes
+    elif kind in (PEAK_COPY, PEAK_READ):
         if src is None:
             raise ValueError("copy and read need src")
         _min(src, None, 0, "src")

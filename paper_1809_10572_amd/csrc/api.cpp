@@ -391,6 +391,45 @@ int int8_setup(samd_fmt xf, samd_fmt wf, const samd_conv2d_desc *d, const void *
 
 extern "C" {
 
+int samd_conv2d_int8_plan_query(const samd_conv2d_desc *d, samd_fmt xf, samd_fmt wf, samd_conv2d_int8_plan *out) {
+    set_error("");
+    int st = check_int8_formats(xf, wf);
+    if (!st) st = check_conv2d_desc(d);
+    if (!st) st = check_overflow(d, xf, wf);
+    if (st) return st;
+    if (!out) return fail(SAMD_EINVAL, "out must not be NULL");
+    return conv2d_i8_tiles(*d, xf, *out);
+}
+
+int samd_conv2d_int8_candidates(const samd_conv2d_desc *d, samd_fmt xf, samd_fmt wf, int32_t max_count,
+                                samd_conv2d_int8_plan *out, int32_t *count) {
+    set_error("");
+    int st = check_int8_formats(xf, wf);
+    if (!st) st = check_conv2d_desc(d);
+    if (!st) st = check_overflow(d, xf, wf);
+    if (st) return st;
+    if (max_count < 1 || max_count > SAMD_MAX_CANDIDATES)
+        return fail(SAMD_EINVAL, "candidate count %d is outside 1..%d", max_count, SAMD_MAX_CANDIDATES);
+    if (!out || !count) return fail(SAMD_EINVAL, "out and count must not be NULL");
+    std::vector<samd_conv2d_int8_plan> cands;
+    conv2d_i8_candidates(*d, xf, cands);
+    const int n = std::min<int>(max_count, (int)cands.size());
+    for (int i = 0; i < n; ++i) out[i] = cands[i];
+    *count = n;
+    return SAMD_OK;
+}
+
+int samd_conv2d_int8_use_plan(const samd_conv2d_desc *d, samd_fmt xf, samd_fmt wf, const samd_conv2d_int8_plan *plan) {
+    set_error("");
+    int st = check_int8_formats(xf, wf);
+    if (!st) st = check_conv2d_desc(d);
+    if (!st) st = check_overflow(d, xf, wf);
+    if (st) return st;
+    st = conv2d_i8_use_plan(*d, xf, plan);
+    if (st) return fail(st, "%s", samd_last_error());
+    return SAMD_OK;
+}
+
 int samd_conv2d_int8_prepare(const int8_t *w, samd_fmt wf, const samd_conv2d_desc *d, samd_fmt xf, void *ws,
                              size_t ws_bytes, hipStream_t stream) {
     set_error("");

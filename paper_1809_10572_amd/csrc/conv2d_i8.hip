@@ -10,7 +10,14 @@
 // input lies inside the image) back in the epilogue.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
+#include <climits>
+#include <array>
+#include <map>
+#include <mutex>
+#include <string>
 #include <type_traits>
+#include <vector>
 
 #include "hip_util.hpp"
 
@@ -284,6 +291,293 @@ __global__ __launch_bounds__(256) void conv2d_i8_kernel(const uint8_t *__restric
     }
 }
 
+// Halo-tiled implicit GEMM for stride-1 layers whose channel count is a multiple of 16.
+// A workgroup computes TM = 4 WM output channels x TP output positions of one image:
+// wave w owns channels w*WM .. +WM-1 of all TP positions (WM/16 x TP/16 MFMA tiles of
+// 16 x 16).  The K loop walks chunks of KC channels (the weight layout's K step, 64 or
+// 128) and, inside each chunk, the KH*KW taps; one step is one tap of one chunk.  The
+// input pixels a chunk needs (the tile's output rows plus KH-1 halo rows, every column
+// any of its positions reaches, KC channels each) are staged in LDS once and read by
+// every tap at a shifted address - the KH*KW-fold re-read of an im2col tile becomes one
+// load per chunk - while the next chunk's halo is requested at the first step of a chunk
+// and stored into the second LDS buffer after its last step (one barrier per chunk).
+// Each wave streams its own weight rows straight from L2 into registers, kRing - 1 steps
+// ahead: no two waves share a weight row, so LDS would buy no reuse.  A step reads the
+// whole KC-byte segment of each of its weight rows, so every cache line of the weights
+// is fetched once per workgroup.
+//
+// Tiles are either flat runs of TP positions of one image (narrow images: a tile spans
+// several output rows and the halo holds whole padded rows) or segments of TP columns of
+// one output row (wide images: the halo holds KH rows of TP + KW - 1 columns).
+//
+// Unsigned 8-bit activations enter as v - 128 (the int8 range), and so do the zero
+// padding pixels (0 - 128): every tap then carries the same offset, and the result is
+// the accumulator plus 128 times the sum of all of the filter's weights, one constant per
+// output channel.
+constexpr int kHaloPer = 12;     // halo pieces (16 bytes) per thread and chunk at most
+constexpr int kHaloPieces = kHaloPer * 256;
+constexpr int kHaloMaxLds = 160 * 1024;   // LDS of one workgroup on gfx950
+
+struct HaloTiles {
+    int rowseg;      // 0: flat tiles of TP positions; 1: row segments of TP columns
+    int tiles_img;   // tiles per image
+    int segs;        // row segments per output row (rowseg)
+    int halo_bytes;  // LDS bytes of one halo buffer (the largest tile's)
+    int nch;         // chunks of KC channels: Cp / KC
+    int items;       // work items: N * tiles_img * channel tiles
+};
+
+// n / d for 0 <= n < 2^22 and 1 <= d < 2^12 by a float reciprocal estimate and one exact
+// correction each way (the estimate is within one of the quotient): a few independent VALU
+// operations instead of the dependent chain of an integer division, which with one wave
+// per SIMD would sit exposed in the kernel's prologue.
+struct FastDiv {
+    int d;
+    float r;
+    __device__ explicit FastDiv(int d_) : d(d_), r(1.0f / (float)d_) {}
+    __device__ int div(int n) const {
+        int q = (int)((float)n * r);
+        q += (q + 1) * d <= n ? 1 : 0;
+        q -= q * d > n ? 1 : 0;
+        return q;
+    }
+};
+
+template <int WM, int TP, int KC>
+__global__ __launch_bounds__(256) void conv2d_i8_halo_kernel(const uint8_t *__restrict__ x, const int8_t *__restrict__ wr,
+                                                             const int32_t *__restrict__ pre, int32_t *__restrict__ y,
+                                                             const I8Geom g, const HaloTiles ht) {
+    constexpr int NI = WM / 16, NJ = TP / 16, TM = 4 * WM;
+    constexpr int KB = KC / 64;           // MFMA k-blocks per step
+    constexpr int PIX = KC + 16;          // LDS bytes per halo pixel: KC channels + 16 against bank conflicts
+    constexpr int PPP = KC / 16;          // 16-byte pieces per pixel
+    constexpr int kRing = KC == 128 ? 4 : 6;   // weight register sets: requests kRing - 1 steps ahead
+    extern __shared__ __attribute__((aligned(16))) char halo[];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int li = lane & 15, lg = lane >> 4;
+    // Workgroup p runs on XCD p % 8; XCD x takes the contiguous range of work items
+    // [x * items / 8, (x + 1) * items / 8), items ordered (image, tile, channel tile), so
+    // neighbouring tiles - which share halo rows - and the channel tiles of one position
+    // tile meet in one L2.
+    const int xcd = blockIdx.x % kNumXcd, k = blockIdx.x / kNumXcd;
+    const int ib = (int)((int64_t)xcd * ht.items / kNumXcd), ie = (int)((int64_t)(xcd + 1) * ht.items / kNumXcd);
+    if (ib + k >= ie) return;
+    const int item = ib + k;
+    const int mtiles = (g.M + TM - 1) / TM;
+    const int tile = item / mtiles;
+    const int m0 = (item - tile * mtiles) * TM;
+    const int n = tile / ht.tiles_img, tt = tile - n * ht.tiles_img;
+    const int HWo = g.Ho * g.Wo;
+    const int khw = g.KH * g.KW;
+    const int flip = g.zero_point ? (int)0x80808080u : 0;
+
+    // the tile: positions p0 .. p0 + np - 1 of image n (row-major within the image), output
+    // rows ho_a .. ho_b, halo columns col_lo .. col_lo + hw - 1 of input rows ho_a - ph ..
+    int p0, np, ho_a, ho_b, col_lo, hw;
+    if (!ht.rowseg) {
+        p0 = tt * TP;
+        np = min(TP, HWo - p0);
+        ho_a = p0 / g.Wo;
+        ho_b = (p0 + np - 1) / g.Wo;
+        col_lo = -g.pw;
+        hw = g.Wo + g.KW - 1;
+    } else {
+        const int ho = tt / ht.segs, wo0 = (tt - ho * ht.segs) * TP;
+        np = min(TP, g.Wo - wo0);
+        p0 = ho * g.Wo + wo0;
+        ho_a = ho_b = ho;
+        col_lo = wo0 - g.pw;
+        hw = np + g.KW - 1;
+    }
+    const int npc = (ho_b - ho_a + g.KH) * hw * PPP;   // 16-byte halo pieces of one chunk
+    const int ih0 = ho_a - g.ph;
+
+    // halo pieces of this thread: k = tid + 256 u -> pixel (r, jc) = divmod(k / PPP, hw),
+    // channels (k % PPP) * 16 .. +15 of the chunk; global byte offset without the chunk's
+    // first channel, LDS offset, and whether the pixel lies inside the image
+    int gofs[kHaloPer], lofs[kHaloPer];
+    uint32_t inside = 0;
+    const FastDiv by_hw(hw);
+#pragma unroll
+    for (int u = 0; u < kHaloPer; ++u) {
+        const int k = tid + 256 * u;
+        const int q = k & (PPP - 1), rc = k / PPP;
+        const int r = by_hw.div(rc), jc = rc - r * hw;
+        const int ih = ih0 + r, iw = col_lo + jc;
+        const bool in = k < npc && ih >= 0 && ih < g.H && iw >= 0 && iw < g.W;
+        inside |= in ? 1u << u : 0u;
+        gofs[u] = in ? ((n * g.H + ih) * g.W + iw) * g.C + q * 16 : 0;
+        lofs[u] = rc * PIX + q * 16;
+    }
+    const __amdgpu_buffer_rsrc_t xrs =
+        __builtin_amdgcn_make_buffer_rsrc((void *)x, (short)0, g.N * g.H * g.W * g.C, 0x00020000);
+    v4i hv[kHaloPer];
+    auto halo_load = [&](int c0) {
+#pragma unroll
+        for (int u = 0; u < kHaloPer; ++u) hv[u] = load16(xrs, gofs[u] + c0);
+    };
+    auto halo_store = [&](int buf, int c0) {
+        char *hb = halo + buf * ht.halo_bytes;
+        const v4i pad = {flip, flip, flip, flip};
+#pragma unroll
+        for (int u = 0; u < kHaloPer; ++u) {
+            const int k = tid + 256 * u;
+            // padding pixels and channels past C (whose weights are 0) hold the zero point
+            const bool in = ((inside >> u) & 1) && c0 + (k & (PPP - 1)) * 16 < g.C;
+            if (k < npc) *(v4i *)(hb + lofs[u]) = in ? (hv[u] ^ flip) : pad;
+        }
+    };
+
+    // weight rows of this wave: A tile i is rows wave*WM + i*16 + li, bytes kb*64 + lg*16
+    // .. +15 of each step's KC-byte segment
+    int alane[NI];
+#pragma unroll
+    for (int i = 0; i < NI; ++i) alane[i] = (wave * WM + i * 16 + li) * khw * g.Cp + lg * 16;
+    const __amdgpu_buffer_rsrc_t wrs = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)(wr + (int64_t)m0 * khw * g.Cp), (short)0, TM * khw * g.Cp, 0x00020000);
+
+    // halo address of each position tile's lane (position p0 + j*16 + li; lanes past the
+    // tile read its last position, their sums are not stored), before the tap's shift
+    int blane[NJ];
+    const FastDiv by_wo(g.Wo);
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+        const int p = p0 + min(j * 16 + li, np - 1);
+        const int ho = by_wo.div(p), wo = p - ho * g.Wo;
+        blane[j] = ((ho - ho_a) * hw + (wo - g.pw - col_lo)) * PIX + lg * 16;
+    }
+
+    v4i acc[NI][NJ];
+#pragma unroll
+    for (int i = 0; i < NI; ++i)
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) acc[i][j] = v4i{0, 0, 0, 0};
+
+    const int S = ht.nch * khw;   // steps: chunks x taps
+    // The next step whose weights are requested.  Every step requests one step's weights,
+    // also past the last step (the last step's rows again, in bounds, never used): loads
+    // issued on every path keep the compiler's wait counts exact, so a step waits only for
+    // its own weights, requested kRing - 1 steps earlier.
+    int ltap = 0, lc = 0;
+    const int last_so = (khw - 1) * g.Cp + g.Cp - KC;
+    v4i aR[kRing][NI][KB];
+    auto a_load = [&](v4i (&a)[NI][KB]) {
+        const int so = lc < g.Cp ? ltap * g.Cp + lc : last_so;
+#pragma unroll
+        for (int i = 0; i < NI; ++i)
+#pragma unroll
+            for (int kb = 0; kb < KB; ++kb)
+                a[i][kb] = __builtin_bit_cast(
+                    v4i, __builtin_amdgcn_raw_buffer_load_b128(wrs, alane[i] + kb * 64, so, 0));
+        if (++ltap == khw) {
+            ltap = 0;
+            lc += KC;
+        }
+    };
+
+    halo_load(0);
+#pragma unroll
+    for (int r = 0; r < kRing - 1; ++r) a_load(aR[r]);
+    halo_store(0, 0);
+    __syncthreads();
+
+    // Halo fragments of a step, one k-block (64 channels) at a time: while a k-block's
+    // MFMAs run, the fragments of the next k-block (of this step or the next) are read,
+    // so LDS reads overlap the matrix work instead of preceding it.  After the last step
+    // they read the first tap again (in bounds, never used).
+    v4i b[KB][NJ];
+    auto b_read = [&](int kb, int buf, int ky, int kx) {
+        const char *hb = halo + buf * ht.halo_bytes + (ky * hw + kx) * PIX + kb * 64;
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) b[kb][j] = *(const v4i *)(hb + blane[j]);
+    };
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) b_read(kb, 0, 0, 0);
+
+    int tap = 0, cc = 0, tky = 0, tkx = 0;   // the step being computed
+    auto step = [&](auto slot) {
+        constexpr int SL = decltype(slot)::value;
+        a_load(aR[(SL + kRing - 1) % kRing]);
+        if (tap == 0 && cc + 1 < ht.nch) halo_load((cc + 1) * KC);
+        // the following step's tap (within this chunk)
+        int nky = tky, nkx = tkx + 1;
+        if (nkx == g.KW) {
+            nkx = 0;
+            ++nky;
+        }
+        const bool last_tap = tap + 1 == khw;
+        if (last_tap) nky = nkx = 0;
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb) {
+#pragma unroll
+            for (int i = 0; i < NI; ++i)
+#pragma unroll
+                for (int j = 0; j < NJ; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(aR[SL][i][kb], b[kb][j], acc[i][j], 0, 0, 0);
+            // this k-block's fragments are consumed: read the next step's (same chunk)
+            if (!last_tap) b_read(kb, cc & 1, nky, nkx);
+        }
+        if (last_tap) {
+            if (cc + 1 < ht.nch) {
+                halo_store((cc + 1) & 1, (cc + 1) * KC);
+                __syncthreads();
+            }
+            tap = tky = tkx = 0;
+            ++cc;
+#pragma unroll
+            for (int kb = 0; kb < KB; ++kb) b_read(kb, cc & 1, 0, 0);
+        } else {
+            ++tap;
+            tky = nky;
+            tkx = nkx;
+        }
+    };
+    int s = 0;
+    if constexpr (kRing == 4) {
+        for (; s + 4 <= S; s += 4) {
+            step(std::integral_constant<int, 0>{});
+            step(std::integral_constant<int, 1>{});
+            step(std::integral_constant<int, 2>{});
+            step(std::integral_constant<int, 3>{});
+        }
+    } else {
+        for (; s + 6 <= S; s += 6) {
+            step(std::integral_constant<int, 0>{});
+            step(std::integral_constant<int, 1>{});
+            step(std::integral_constant<int, 2>{});
+            step(std::integral_constant<int, 3>{});
+            step(std::integral_constant<int, 4>{});
+            step(std::integral_constant<int, 5>{});
+        }
+    }
+    if (s < S) step(std::integral_constant<int, 0>{});
+    if (s + 1 < S) step(std::integral_constant<int, 1>{});
+    if (s + 2 < S) step(std::integral_constant<int, 2>{});
+    if constexpr (kRing == 6) {
+        if (s + 3 < S) step(std::integral_constant<int, 3>{});
+        if (s + 4 < S) step(std::integral_constant<int, 4>{});
+    }
+
+    // D[row][col]: lane holds rows 4*lg + v (output channels) of column li (position);
+    // zero point: + 128 * (the sum of all of the filter's weights)
+    const int full = g.KH * (g.KW + 1) + g.KW;   // prefix-table entry of the whole filter
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const int m = m0 + wave * WM + i * 16 + lg * 4 + v;
+            if (m >= g.M) continue;
+            const int32_t corr = g.zero_point ? 128 * pre[(int64_t)m * (g.KH + 1) * (g.KW + 1) + full] : 0;
+            int32_t *ym = y + ((int64_t)n * g.M + m) * HWo + p0;
+#pragma unroll
+            for (int j = 0; j < NJ; ++j) {
+                const int pp = j * 16 + li;
+                if (pp < np) ym[pp] = acc[i][j][v] + corr;
+            }
+        }
+    }
+}
+
 I8Geom make_geom(const samd_conv2d_desc &d, samd_fmt xf) {
     I8Geom g;
     g.N = d.N; g.C = d.C; g.H = d.H; g.W = d.W; g.M = d.M; g.KH = d.KH; g.KW = d.KW;
@@ -333,14 +627,188 @@ int launch_conv2d_i8_prepare(const int8_t *w, samd_fmt xf, const samd_conv2d_des
     return check_launch("conv2d_int8 weight reorder");
 }
 
+namespace {
+
+constexpr int kHaloShapes[4][2] = {{32, 128}, {32, 64}, {16, 128}, {16, 64}};   // (WM, TP)
+
+// Tiling of the halo kernel for (WM, TP); false when the halo does not fit the LDS (one
+// buffer, or two when there are several chunks) or the register-held halo pieces.
+bool halo_tiles(const I8Geom &g, int wm, int tp, HaloTiles &ht, int64_t &wgs, int &lds) {
+    int rmax, hwmax;
+    if (g.Wo < tp) {   // flat tiles: whole padded rows
+        ht.rowseg = 0;
+        ht.tiles_img = (g.Ho * g.Wo + tp - 1) / tp;
+        ht.segs = 1;
+        rmax = std::min(g.Ho, (tp - 1) / g.Wo + 2) + g.KH - 1;
+        hwmax = g.Wo + g.KW - 1;
+    } else {           // row segments
+        ht.rowseg = 1;
+        ht.segs = (g.Wo + tp - 1) / tp;
+        ht.tiles_img = g.Ho * ht.segs;
+        rmax = g.KH;
+        hwmax = tp + g.KW - 1;
+    }
+    // the kernel's fast divisions need positions per image below 2^22, divisors below 2^12
+    if ((int64_t)g.Ho * g.Wo >= (1 << 22) || g.Wo >= 4096 || hwmax >= 4096) return false;
+    const int kc = g.ks;
+    const int64_t pixels = (int64_t)rmax * hwmax;
+    ht.halo_bytes = (int)std::min<int64_t>(pixels * (kc + 16), 1 << 30);
+    ht.nch = g.Cp / kc;
+    lds = (ht.nch > 1 ? 2 : 1) * ht.halo_bytes;
+    wgs = (int64_t)g.N * ht.tiles_img * ((g.M + 4 * wm - 1) / (4 * wm));
+    ht.items = (int)std::min<int64_t>(wgs, INT32_MAX);
+    return pixels * (kc / 16) <= kHaloPieces && lds <= kHaloMaxLds && wgs < ((int64_t)1 << 31) - 8;
+}
+
+template <int WM, int TP, int KC>
+int launch_halo(const void *x, const I8Geom &g, const HaloTiles &ht, int lds, const I8Workspace &p, int32_t *y,
+                hipStream_t s) {
+    const void *fn = (const void *)conv2d_i8_halo_kernel<WM, TP, KC>;
+    // more than the default 64 KiB of dynamic LDS is opted into once per kernel
+    static std::once_flag once;
+    static hipError_t attr = hipSuccess;
+    std::call_once(once, [&] { attr = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, kHaloMaxLds); });
+    if (attr != hipSuccess) {
+        set_error(std::string("conv2d_int8: LDS attribute: ") + hipGetErrorString(attr));
+        return SAMD_EHIP;
+    }
+    // every XCD gets the same number of workgroups, enough for its share of the items
+    const int64_t per_xcd = ((int64_t)ht.items + kNumXcd - 1) / kNumXcd;
+    const dim3 grid((unsigned)(per_xcd * kNumXcd));
+    hipLaunchKernelGGL((conv2d_i8_halo_kernel<WM, TP, KC>), grid, dim3(256), (size_t)lds, s, (const uint8_t *)x,
+                       p.wr, p.pre, y, g, ht);
+    return check_launch("conv2d_int8 (halo tiles)");
+}
+
+// Every launch the int8 baseline can make for a layer: the halo tiles that fit (stride-1
+// layers, C a multiple of 16), then the im2col kernel with 64 and 32 positions per
+// workgroup.
+void int8_candidates(const I8Geom &g, std::vector<samd_conv2d_int8_plan> &out) {
+    out.clear();
+    if (g.sh == 1 && g.sw == 1 && g.C % 16 == 0) {
+        for (const auto &sh : kHaloShapes) {
+            HaloTiles ht{};
+            int64_t wgs = 0;
+            int lds = 0;
+            if (!halo_tiles(g, sh[0], sh[1], ht, wgs, lds)) continue;
+            samd_conv2d_int8_plan c{};
+            c.halo = 1;
+            c.mtile = 4 * sh[0];
+            c.positions = sh[1];
+            c.row_segments = ht.rowseg;
+            c.lds_bytes = lds;
+            c.workgroups = wgs;
+            out.push_back(c);
+        }
+    }
+    for (int tp : {64, 32}) {
+        samd_conv2d_int8_plan c{};
+        c.halo = 0;
+        c.mtile = kTM;
+        c.positions = tp;
+        c.lds_bytes = 0;
+        c.workgroups = (g.P + tp - 1) / tp * (g.Mp / kTM);
+        out.push_back(c);
+    }
+}
+
+// The model's choice among the candidates: in the order 64 x 128, 128 x 128, 64 x 64,
+// 128 x 64 (output channels x positions; the order of their times on the mid-size layer),
+// the first halo tile that still gives at least 160 workgroups (about two thirds of the
+// compute units), else the halo tile with the most workgroups, else the im2col kernel
+// with 64 positions when that gives every compute unit a workgroup, else 32.
+samd_conv2d_int8_plan model_choice(const std::vector<samd_conv2d_int8_plan> &cands) {
+    static const int order[4][2] = {{64, 128}, {128, 128}, {64, 64}, {128, 64}};
+    for (const auto &o : order)
+        for (const auto &c : cands)
+            if (c.halo && c.mtile == o[0] && c.positions == o[1] && c.workgroups >= 160) return c;
+    int most = -1;
+    for (size_t i = 0; i < cands.size(); ++i) {
+        if (!cands[i].halo) continue;
+        if (most < 0 || cands[i].workgroups > cands[most].workgroups) most = (int)i;
+    }
+    if (most >= 0) return cands[most];
+    for (const auto &c : cands)
+        if (!c.halo && c.positions == 64 && c.workgroups >= 256) return c;
+    return cands.back();
+}
+
+// Plans installed by samd_conv2d_int8_use_plan, per (shape, activation format).
+using Int8Key = std::array<int32_t, 13>;
+std::mutex int8_mu;
+std::map<Int8Key, samd_conv2d_int8_plan> int8_plans;
+
+Int8Key int8_key(const samd_conv2d_desc &d, samd_fmt xf) {
+    return {d.N, d.C, d.H, d.W, d.M, d.KH, d.KW, d.stride_h, d.stride_w, d.pad_h, d.pad_w, xf.bits, xf.is_signed};
+}
+
+bool same_launch(const samd_conv2d_int8_plan &a, const samd_conv2d_int8_plan &b) {
+    return a.halo == b.halo && a.mtile == b.mtile && a.positions == b.positions;
+}
+
+}  // namespace
+
+int conv2d_i8_candidates(const samd_conv2d_desc &d, samd_fmt xf, std::vector<samd_conv2d_int8_plan> &out) {
+    int8_candidates(make_geom(d, xf), out);
+    return SAMD_OK;
+}
+
+int conv2d_i8_tiles(const samd_conv2d_desc &d, samd_fmt xf, samd_conv2d_int8_plan &out) {
+    std::vector<samd_conv2d_int8_plan> cands;
+    int8_candidates(make_geom(d, xf), cands);
+    {
+        std::lock_guard<std::mutex> lock(int8_mu);
+        auto it = int8_plans.find(int8_key(d, xf));
+        if (it != int8_plans.end()) {
+            out = it->second;
+            return SAMD_OK;
+        }
+    }
+    out = model_choice(cands);
+    return SAMD_OK;
+}
+
+int conv2d_i8_use_plan(const samd_conv2d_desc &d, samd_fmt xf, const samd_conv2d_int8_plan *plan) {
+    std::lock_guard<std::mutex> lock(int8_mu);
+    if (!plan) {
+        int8_plans.erase(int8_key(d, xf));
+        return SAMD_OK;
+    }
+    std::vector<samd_conv2d_int8_plan> cands;
+    int8_candidates(make_geom(d, xf), cands);
+    for (const auto &c : cands)
+        if (same_launch(c, *plan)) {
+            int8_plans[int8_key(d, xf)] = c;
+            return SAMD_OK;
+        }
+    set_error("conv2d_int8: no candidate launch of this layer matches the plan");
+    return SAMD_EINVAL;
+}
+
 int launch_conv2d_i8(const void *x, samd_fmt xf, const samd_conv2d_desc &d, int32_t *y, const void *ws,
                      hipStream_t s) {
     const I8Geom g = make_geom(d, xf);
     const I8Workspace p = carve(g, const_cast<void *>(ws));
-    // 64 positions per workgroup (half the weight re-reads of 32) when that still gives
-    // every compute unit a workgroup, else 32
-    const int64_t wgs64 = (g.P + 63) / 64 * (g.Mp / kTM);
     const bool vec = (g.C % 16) == 0 && ((uintptr_t)x % 16) == 0;
+    samd_conv2d_int8_plan plan{};
+    conv2d_i8_tiles(d, xf, plan);
+    if (plan.halo && vec) {
+        const int wm = plan.mtile / 4, tp = plan.positions;
+        HaloTiles ht{};
+        int64_t wgs = 0;
+        int lds = 0;
+        if (halo_tiles(g, wm, tp, ht, wgs, lds)) {
+#define SAMD_HALO(WM_, TP_)                                                                                  \
+    if (wm == WM_ && tp == TP_)                                                                              \
+        return g.ks == 128 ? launch_halo<WM_, TP_, 128>(x, g, ht, lds, p, y, s)                              \
+                           : launch_halo<WM_, TP_, 64>(x, g, ht, lds, p, y, s);
+            SAMD_HALO(32, 128) SAMD_HALO(32, 64) SAMD_HALO(16, 128) SAMD_HALO(16, 64)
+#undef SAMD_HALO
+        }
+    }
+    // the im2col kernel: the chosen plan's positions per workgroup, or (misaligned
+    // activations under a halo plan) 64 when that gives every compute unit a workgroup
+    int tp = plan.halo ? ((g.P + 63) / 64 * (g.Mp / kTM) >= 256 ? 64 : 32) : plan.positions;
     const unsigned gy = (unsigned)(g.Mp / kTM);
 #define SAMD_I8_LAUNCH(TP_, KS_, VEC_)                                                                          \
     hipLaunchKernelGGL((conv2d_i8_kernel<TP_, KS_, VEC_>), dim3((unsigned)((g.P + TP_ - 1) / TP_), gy), dim3(256), 0, \
@@ -351,7 +819,7 @@ int launch_conv2d_i8(const void *x, samd_fmt xf, const samd_conv2d_desc &d, int3
     } else {                                                                                                    \
         if (vec) SAMD_I8_LAUNCH(TP_, 64, true); else SAMD_I8_LAUNCH(TP_, 64, false);                            \
     }
-    if (wgs64 >= 256) {
+    if (tp == 64) {
         SAMD_I8_KS(64)
     } else {
         SAMD_I8_KS(32)

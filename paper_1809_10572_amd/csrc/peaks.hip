@@ -78,11 +78,40 @@ __global__ __launch_bounds__(kPeakBlock) void peak_mfma_kernel(int iters, int32_
     out[tid] = s[0] ^ s[1] ^ s[2] ^ s[3];
 }
 
+// 16-byte LDS reads (ds_read_b128), kLdsReads per trip, each lane reading its own 16 bytes
+// of a 16 KiB block (consecutive lanes consecutive 16-byte slots: no bank conflicts); the
+// data is xor-combined so the reads cannot be dropped.
+constexpr int kLdsReads = 8;
+__global__ __launch_bounds__(kPeakBlock) void peak_lds_kernel(int iters, int32_t k0, int32_t k1, int32_t *out) {
+    __shared__ __attribute__((aligned(16))) int4 buf[kPeakBlock * 4];
+    const int tid = blockIdx.x * kPeakBlock + threadIdx.x;
+    for (int i = threadIdx.x; i < kPeakBlock * 4; i += kPeakBlock) buf[i] = int4{i, i ^ k0, i + k1, tid};
+    __syncthreads();
+    int4 x = {0, 0, 0, 0};
+    int base = threadIdx.x;
+    for (int it = 0; it < iters; ++it) {
+        opaque(base);
+#pragma unroll
+        for (int r = 0; r < kLdsReads; ++r) {
+            v4i v = __builtin_bit_cast(v4i, buf[(base + r * 64) & (kPeakBlock * 4 - 1)]);
+            opaque(v);   // all 16 bytes stay live: the read stays 16 bytes wide
+            x.x ^= v[0];
+        }
+    }
+    out[tid] = x.x ^ x.y ^ x.z ^ x.w;
+}
+
 // Grid-stride streaming copy of n16 16-byte chunks.
 __global__ __launch_bounds__(kPeakBlock) void peak_copy_kernel(const int4 *__restrict__ src, int4 *__restrict__ dst,
                                                                int64_t n16) {
     const int64_t stride = (int64_t)gridDim.x * kPeakBlock;
     for (int64_t i = (int64_t)blockIdx.x * kPeakBlock + threadIdx.x; i < n16; i += stride) dst[i] = src[i];
+}
+
+// Grid-stride streaming write of n16 16-byte chunks.
+__global__ __launch_bounds__(kPeakBlock) void peak_write_kernel(int4 *__restrict__ dst, int64_t n16, int32_t v) {
+    const int64_t stride = (int64_t)gridDim.x * kPeakBlock;
+    for (int64_t i = (int64_t)blockIdx.x * kPeakBlock + threadIdx.x; i < n16; i += stride) dst[i] = int4{v, v, v, v};
 }
 
 // Grid-stride streaming read of n16 16-byte chunks; one sum per workgroup.
@@ -106,9 +135,11 @@ bool valid(int kind, int64_t iters, int32_t blocks, int64_t bytes) {
     switch (kind) {
         case SAMD_PEAK_MAD_I64_I32:
         case SAMD_PEAK_VALU_I32:
-        case SAMD_PEAK_MFMA_I8: return iters >= 1 && iters <= (1 << 24);
+        case SAMD_PEAK_MFMA_I8:
+        case SAMD_PEAK_LDS: return iters >= 1 && iters <= (1 << 24);
         case SAMD_PEAK_COPY:
-        case SAMD_PEAK_READ: return bytes >= 16 && bytes % 16 == 0;
+        case SAMD_PEAK_READ:
+        case SAMD_PEAK_WRITE: return bytes >= 16 && bytes % 16 == 0;
         default: return false;
     }
 }
@@ -129,6 +160,7 @@ double samd_peak_work(int kind, int64_t iters, int32_t blocks, int64_t bytes) {
         case SAMD_PEAK_VALU_I32: return threads * (double)iters * kChains;
         case SAMD_PEAK_MFMA_I8: return threads / 64.0 * (double)iters * kMfmaAcc * 16.0 * 16.0 * 64.0;
         case SAMD_PEAK_COPY: return 2.0 * (double)bytes;
+        case SAMD_PEAK_LDS: return threads * (double)iters * kLdsReads * 16.0;
         default: return (double)bytes;
     }
 }
@@ -144,7 +176,8 @@ int samd_peak_launch(int kind, int64_t iters, int32_t blocks, const void *src, v
         set_error("samd_peak_launch: NULL buffer");
         return SAMD_EINVAL;
     }
-    if ((kind == SAMD_PEAK_COPY || kind == SAMD_PEAK_READ) && (((uintptr_t)src | (uintptr_t)dst) & 15)) {
+    if ((kind == SAMD_PEAK_COPY || kind == SAMD_PEAK_READ || kind == SAMD_PEAK_WRITE) &&
+        (((uintptr_t)src | (uintptr_t)dst) & 15)) {
         set_error("samd_peak_launch: src and dst must be 16-byte aligned");
         return SAMD_EALIGN;
     }
@@ -159,6 +192,12 @@ int samd_peak_launch(int kind, int64_t iters, int32_t blocks, const void *src, v
             break;
         case SAMD_PEAK_MFMA_I8:
             hipLaunchKernelGGL(peak_mfma_kernel, grid, block, 0, stream, (int)iters, 3, -5, out);
+            break;
+        case SAMD_PEAK_WRITE:
+            hipLaunchKernelGGL(peak_write_kernel, grid, block, 0, stream, (int4 *)dst, bytes / 16, (int32_t)iters);
+            break;
+        case SAMD_PEAK_LDS:
+            hipLaunchKernelGGL(peak_lds_kernel, grid, block, 0, stream, (int)iters, 3, -5, out);
             break;
         case SAMD_PEAK_COPY:
             hipLaunchKernelGGL(peak_copy_kernel, grid, block, 0, stream, (const int4 *)src, (int4 *)dst, bytes / 16);

@@ -128,6 +128,13 @@ size_t conv2d_i8_workspace_bytes(const samd_conv2d_desc &d, samd_fmt xf);
 int launch_conv2d_i8_prepare(const int8_t *w, samd_fmt xf, const samd_conv2d_desc &d, void *ws, hipStream_t s);
 int launch_conv2d_i8(const void *x, samd_fmt xf, const samd_conv2d_desc &d, int32_t *y, const void *ws,
                      hipStream_t s);
+// The int8 kernel and tile samd_conv2d_int8 uses for a layer with 16-byte aligned
+// activations (host only).
+int conv2d_i8_tiles(const samd_conv2d_desc &d, samd_fmt xf, samd_conv2d_int8_plan &out);
+// Every launch the int8 baseline can make for a layer, and the override of its choice
+// (plan NULL: back to the model's choice).
+int conv2d_i8_candidates(const samd_conv2d_desc &d, samd_fmt xf, std::vector<samd_conv2d_int8_plan> &out);
+int conv2d_i8_use_plan(const samd_conv2d_desc &d, samd_fmt xf, const samd_conv2d_int8_plan *plan);
 int launch_max_i32(const int32_t *src, int64_t n, int32_t *dev_max, hipStream_t s);
 int launch_count_mismatch(const int32_t *a, const int32_t *b, int64_t n, int32_t *count, hipStream_t s);
 int launch_lanewise(int op, const uint32_t *a, const uint32_t *b, int64_t nwords, int bits, uint32_t scalar,

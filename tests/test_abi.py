@@ -278,3 +278,55 @@ def test_planner_refuses_a_spread_of_2_to_the_32_threads():
     assert b"index ranges" in L.samd_last_error()
     n = ctypes.c_size_t(0)
     assert L.samd_conv2d_workspace(ctypes.byref(d), Fmt(8, False), Fmt(8, True), ctypes.byref(n)) == EUNSUP
+
+
+def test_int8_halo_tiles_cover_every_kernel():
+    """The int8 layers of the GPU tests, with all their candidate launches, reach both
+    kernels, every halo tile shape, both tile modes and both channel steps (host-only
+    queries of the launches the library makes)."""
+    import sys
+    sys.path.insert(0, os.path.join(ROOT, "tests"))
+    import samd_workloads as wl
+    from test_gpu_parity import HALO
+    seen = set()
+    for shape in HALO:
+        cands = samd.conv2d_int8_candidates(shape, Fmt(8, False), Fmt(8, True))
+        assert cands and cands[-1].halo == 0
+        for p in cands:
+            kc = 64 if shape.C <= 64 else 128
+            seen.add((p.halo, p.mtile, p.positions, p.row_segments, kc if p.halo else 0))
+            if p.halo:
+                assert p.lds_bytes <= 160 * 1024 and p.workgroups >= 1
+        # the library's own choice is one of the candidates
+        own = samd.conv2d_int8_plan(shape, Fmt(8, False), Fmt(8, True))
+        assert any((own.halo, own.mtile, own.positions) == (c.halo, c.mtile, c.positions) for c in cands)
+    assert {(1, 128, 128), (1, 128, 64), (1, 64, 128), (1, 64, 64)} <= {k[:3] for k in seen}, seen
+    assert {(0, 128, 64), (0, 128, 32)} <= {k[:3] for k in seen}
+    assert {0, 1} <= {k[3] for k in seen if k[0] == 1}
+    assert {64, 128} <= {k[4] for k in seen if k[0] == 1}
+    assert not any(c.halo for c in samd.conv2d_int8_candidates(HALO[-1], Fmt(8, False), Fmt(8, True)))
+    # the mid-size layer and the extremes-heavy layer take the halo kernel
+    for shape in (wl.MID, wl.STRESS):
+        assert samd.conv2d_int8_plan(shape, Fmt(8, False), Fmt(8, True)).halo == 1
+    # strided layers and channel counts that are not a multiple of 16 take the im2col kernel
+    assert samd.conv2d_int8_plan(wl.Conv2dShape(1, 16, 9, 9, 8, 3, 3, 2, 2, 1, 1), Fmt(8, 1), Fmt(8, 1)).halo == 0
+    assert samd.conv2d_int8_plan(wl.Conv2dShape(1, 24, 9, 9, 8, 3, 3, 1, 1, 1, 1), Fmt(8, 1), Fmt(8, 1)).halo == 0
+
+
+def test_int8_use_plan_installs_and_reverts():
+    import samd_workloads as wl
+    xf, wf = Fmt(8, False), Fmt(8, True)
+    own = samd.conv2d_int8_plan(wl.MID, xf, wf)
+    cands = samd.conv2d_int8_candidates(wl.MID, xf, wf)
+    other = [c for c in cands if (c.halo, c.mtile, c.positions) != (own.halo, own.mtile, own.positions)][0]
+    try:
+        samd.conv2d_int8_use_plan(wl.MID, xf, wf, other)
+        p = samd.conv2d_int8_plan(wl.MID, xf, wf)
+        assert (p.halo, p.mtile, p.positions) == (other.halo, other.mtile, other.positions)
+        bad = samd.Conv2dInt8Plan(1, 48, 64, 0, 0, 0)
+        with pytest.raises(samd.SamdError):
+            samd.conv2d_int8_use_plan(wl.MID, xf, wf, bad)
+    finally:
+        samd.conv2d_int8_use_plan(wl.MID, xf, wf, None)
+    p = samd.conv2d_int8_plan(wl.MID, xf, wf)
+    assert (p.halo, p.mtile, p.positions) == (own.halo, own.mtile, own.positions)

@@ -280,6 +280,50 @@ def test_conv2d_int8_baseline_edges(shape, bx, sx):
     np.testing.assert_array_equal(got, ref.conv2d(x, w, shape.as_tuple()))
 
 
+# Layers of the halo-tiled int8 kernel (stride 1, C a multiple of 16): flat and
+# row-segment tiles, 64- and 128-channel steps, channel counts that leave part of a chunk
+# (or a whole chunk) empty, output channels that are not a multiple of the tile, ragged
+# last tiles, 1x1 to 7x7 and asymmetric kernels; the last one has no halo that fits and
+# takes the im2col kernel.  Every candidate launch of each layer is tested;
+# tests/test_abi.py checks on the CPU that they include every tile shape.
+HALO = [
+    wl.Conv2dShape(2, 16, 9, 20, 24, 3, 3, 1, 1, 1, 1),        # small: 16 x 64 tiles
+    wl.Conv2dShape(1, 48, 30, 61, 70, 3, 3, 1, 1, 1, 1),       # C = 48: a partly empty chunk
+    wl.Conv2dShape(1, 80, 7, 150, 33, 3, 3, 1, 1, 1, 1),       # wide rows: row segments
+    wl.Conv2dShape(2, 32, 12, 12, 130, 5, 5, 1, 1, 2, 2),      # 5x5, M = 130
+    wl.Conv2dShape(1, 64, 1, 40, 16, 1, 3, 1, 1, 0, 1),        # H = 1, 1x3
+    wl.Conv2dShape(3, 16, 20, 21, 8, 1, 1, 1, 1, 0, 0),        # 1x1
+    wl.Conv2dShape(1, 144, 14, 14, 200, 3, 3, 1, 1, 1, 1),     # C = 144: an all-empty fourth chunk
+    wl.Conv2dShape(2, 96, 28, 28, 100, 3, 3, 1, 1, 1, 1),      # 128-channel steps, C = 96
+    wl.Conv2dShape(1, 256, 10, 10, 64, 3, 3, 1, 1, 1, 1),      # two 128-channel chunks
+    wl.Conv2dShape(2, 16, 56, 56, 128, 3, 3, 1, 1, 1, 1),      # the mid-size layer's image size
+    wl.Conv2dShape(1, 16, 5, 7, 16, 3, 7, 1, 1, 1, 3),         # 3x7, pad (1, 3)
+    wl.Conv2dShape(1, 32, 6, 6, 16, 7, 7, 1, 1, 3, 3),         # 7x7 on a 6x6 image
+    wl.Conv2dShape(1, 16, 20, 80, 16, 11, 11, 1, 1, 5, 5),     # no halo fits: im2col kernel
+]
+
+
+@pytest.mark.parametrize("shape", HALO, ids=lambda s: "x".join(map(str, s.as_tuple())))
+@pytest.mark.parametrize("bx,sx", [(8, 0), (8, 1), (4, 0)])
+def test_conv2d_int8_every_launch(shape, bx, sx):
+    """Every launch the int8 baseline can make for the layer (each halo tile that fits and
+    the im2col kernel), installed in turn, against the oracle; then the library's own
+    choice again."""
+    rng = np.random.default_rng(1000 + bx + sx)
+    x = wl.half_extremes(rng, (shape.N, shape.C, shape.H, shape.W), bx, bool(sx))
+    w = wl.half_extremes(rng, (shape.M, shape.C, shape.KH, shape.KW), 8, True)
+    xf, wf = samd.Fmt(bx, sx), samd.Fmt(8, 1)
+    want = ref.conv2d(x, w, shape.as_tuple())
+    try:
+        for plan in samd.conv2d_int8_candidates(shape, xf, wf):
+            samd.conv2d_int8_use_plan(shape, xf, wf, plan)
+            got = run_conv2d_int8(x, w, shape, xf, wf)
+            np.testing.assert_array_equal(got, want, err_msg=f"halo={plan.halo} {plan.mtile}x{plan.positions}")
+    finally:
+        samd.conv2d_int8_use_plan(shape, xf, wf, None)
+    np.testing.assert_array_equal(run_conv2d_int8(x, w, shape, xf, wf), want)
+
+
 # --- requantisation and the AlexNet-shaped stack (workload 5) ---------------------------
 
 @pytest.mark.parametrize("bits", [1, 2, 4, 8])
