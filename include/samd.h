@@ -208,6 +208,26 @@ int samd_conv2d_stage(const uint32_t *x, samd_fmt xf, samd_fmt wf, const samd_co
 int samd_conv2d_accumulate(samd_fmt xf, samd_fmt wf, const samd_conv2d_desc *d, int32_t *y, const void *ws,
                            size_t ws_bytes, hipStream_t stream);
 
+/* ---- Allocation-free convolution ----
+ * For callers that cannot allocate device memory (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc): samd_conv2d with its workspace in a
+ * device array inside the library instead of a caller buffer.  The array holds
+ * SAMD_NOALLOC_SCRATCH_BYTES per GPU, allocated by the HIP runtime when the library's
+ * device code is loaded on that GPU and held until the process ends.
+ *   x, w, y, *d, xf, wf  as for samd_conv2d
+ * The call itself allocates nothing (no hipMalloc, hipFree or allocating library
+ * routine).  A layer whose workspace (samd_conv2d_workspace) exceeds
+ * SAMD_NOALLOC_SCRATCH_BYTES is refused with SAMD_ENOSPC before any HIP call.  Every call
+ * on one GPU uses that GPU's one array, and each call prepares it from scratch (kernel
+ * words and the zeroed ticket counters are written by the call's own kernels), so the
+ * previous call's contents do not matter; but calls that may overlap on one GPU (several
+ * streams, several host threads, concurrent graph branches) race on the array and must
+ * be serialised by the caller. */
+#define SAMD_NOALLOC_SCRATCH_BYTES (64u << 20)
+
+int samd_conv2d_noalloc(const uint32_t *x, samd_fmt xf, const uint32_t *w, samd_fmt wf,
+                        const samd_conv2d_desc *d, int32_t *y, hipStream_t stream);
+
 /* ---- Autotuning ----
  * The paper specialises the SAMD instruction sequence for each precision with a code
  * generator (Sec. 1, Sec. 7).  Here the specialisations are compiled kernel templates

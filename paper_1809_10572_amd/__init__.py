@@ -18,7 +18,7 @@ import torch
 __all__ = ["Fmt", "Conv2dDesc", "Conv1dPlan", "Conv2dPlan", "SamdError", "lib", "row_words", "pack", "unpack", "conv1d",
            "conv1d_plan", "conv2d_plan", "conv2d_candidates", "conv2d_tune_workspace", "conv2d_tune", "conv2d_untune",
            "conv2d_use_plan", "plan_key",
-           "conv2d_workspace", "conv2d", "conv2d_prepare", "conv2d_prepared",
+           "conv2d_workspace", "conv2d", "conv2d_noalloc", "conv2d_prepare", "conv2d_prepared",
            "conv2d_stage", "conv2d_accumulate",
            "conv2d_int8_prepare", "conv2d_int8_prepared", "conv2d_int8_workspace", "conv2d_int8", "conv2d_int8_plan",
            "conv2d_int8_candidates", "conv2d_int8_use_plan", "max_i32",
@@ -135,6 +135,7 @@ def lib():
             "samd_conv2d_untune": (ctypes.c_int, [ctypes.POINTER(Conv2dDesc), Fmt, Fmt]),
             "samd_conv2d_use_plan": (ctypes.c_int, [ctypes.POINTER(Conv2dDesc), Fmt, Fmt,
                                                     ctypes.POINTER(Conv2dPlan)]),
+            "samd_conv2d_noalloc": (ctypes.c_int, [_p, Fmt, _p, Fmt, ctypes.POINTER(Conv2dDesc), _p, _p]),
             "samd_peak_launch": (ctypes.c_int, [ctypes.c_int, _i64, _i32, _p, _p, _i64, _p]),
             "samd_peak_work": (ctypes.c_double, [ctypes.c_int, _i64, _i32, _i64]),
         }
@@ -364,6 +365,22 @@ def conv2d(xp: torch.Tensor, xfmt: Fmt, wp: torch.Tensor, wfmt: Fmt, shape, ws: 
     _out(out, d.N * d.M * Ho * Wo)
     _check(lib().samd_conv2d(xp.data_ptr(), xfmt, wp.data_ptr(), wfmt, ctypes.byref(d), out.data_ptr(),
                              ws.data_ptr(), _ws_bytes(ws), _stream(xp)))
+    return out
+
+
+NOALLOC_SCRATCH_BYTES = 64 << 20
+
+
+def conv2d_noalloc(xp: torch.Tensor, xfmt: Fmt, wp: torch.Tensor, wfmt: Fmt, shape, out: torch.Tensor) -> torch.Tensor:
+    """conv2d with the library's own scratch array as the workspace (the call allocates no
+    device memory; `out` must be given).  Calls that may overlap on one GPU race."""
+    _x_words(xp, shape, xfmt)
+    _w_words(wp, shape, wfmt)
+    d = Conv2dDesc.of(shape)
+    Ho, Wo = out_hw(shape)
+    _out(out, d.N * d.M * Ho * Wo)
+    _check(lib().samd_conv2d_noalloc(xp.data_ptr(), xfmt, wp.data_ptr(), wfmt, ctypes.byref(d), out.data_ptr(),
+                                     _stream(xp)))
     return out
 
 

@@ -18,7 +18,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libsamd.so")
-SOURCES = ["api.cpp", "plan.cpp", "pack.hip", "conv1d.hip", "conv2d_samd.hip", "conv2d_i8.hip", "epilogue.hip", "lanewise.hip", "peaks.hip"]
+SOURCES = ["api.cpp", "plan.cpp", "pack.hip", "conv1d.hip", "conv2d_samd.hip", "conv2d_i8.hip", "epilogue.hip", "lanewise.hip", "peaks.hip", "noalloc.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-Wall", "-Wno-unused-function",

@@ -341,6 +341,27 @@ int samd_conv2d(const uint32_t *x, samd_fmt xf, const uint32_t *w, samd_fmt wf, 
     return launch_conv2d_samd(x, g, y, ws, stream);
 }
 
+int samd_conv2d_noalloc(const uint32_t *x, samd_fmt xf, const uint32_t *w, samd_fmt wf, const samd_conv2d_desc *d,
+                        int32_t *y, hipStream_t stream) {
+    set_error("");
+    int st = check_fmt(xf, "xf");
+    if (!st) st = check_fmt(wf, "wf");
+    if (!st) st = check_conv2d_desc(d);
+    if (!st) st = check_overflow(d, xf, wf);
+    if (st) return st;
+    if (!x || !w || !y) return fail(SAMD_EINVAL, "x, w and y must not be NULL");
+    if (!aligned4(x) || !aligned4(w) || !aligned4(y)) return fail(SAMD_EALIGN, "x / w / y not aligned");
+    Conv2dGeom g;
+    std::string err;
+    st = plan_conv2d(*d, xf, wf, g, err);
+    if (st) return fail(st, "%s", err.c_str());
+    const size_t need = conv2d_workspace_bytes(g);
+    if (need > (size_t)SAMD_NOALLOC_SCRATCH_BYTES)
+        return fail(SAMD_ENOSPC, "the layer needs a %zu-byte workspace; the scratch array holds %zu bytes", need,
+                    (size_t)SAMD_NOALLOC_SCRATCH_BYTES);
+    return launch_conv2d_noalloc(x, w, g, y, stream);
+}
+
 namespace {
 
 // The 8-bit baseline takes signed activations, or unsigned ones of up to 8 bits, and

@@ -124,6 +124,9 @@ int launch_conv2d_prepare(const uint32_t *w, const Conv2dGeom &g, void *ws, hipS
 int launch_conv2d_samd(const uint32_t *x, const Conv2dGeom &g, int32_t *y, const void *ws, hipStream_t s);
 int launch_conv2d_spread(const uint32_t *x, const Conv2dGeom &g, void *ws, hipStream_t s);
 int launch_conv2d_multiply(const Conv2dGeom &g, int32_t *y, const void *ws, hipStream_t s);
+// samd_conv2d with the library's scratch array as the workspace (SAMD_ENOSPC when the
+// layer's workspace does not fit it).
+int launch_conv2d_noalloc(const uint32_t *x, const uint32_t *w, const Conv2dGeom &g, int32_t *y, hipStream_t s);
 size_t conv2d_i8_workspace_bytes(const samd_conv2d_desc &d, samd_fmt xf);
 int launch_conv2d_i8_prepare(const int8_t *w, samd_fmt xf, const samd_conv2d_desc &d, void *ws, hipStream_t s);
 int launch_conv2d_i8(const void *x, samd_fmt xf, const samd_conv2d_desc &d, int32_t *y, const void *ws,

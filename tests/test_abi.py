@@ -330,3 +330,16 @@ def test_int8_use_plan_installs_and_reverts():
         samd.conv2d_int8_use_plan(wl.MID, xf, wf, None)
     p = samd.conv2d_int8_plan(wl.MID, xf, wf)
     assert (p.halo, p.mtile, p.positions) == (own.halo, own.mtile, own.positions)
+
+
+def test_noalloc_validation_before_any_hip_call():
+    L = samd.lib()
+    f = L.samd_conv2d_noalloc
+    x8, w8 = Fmt(8, False), Fmt(8, True)
+    assert f(P4, x8, P4, w8, None, P4, None) == EINVAL
+    assert f(None, x8, P4, w8, ctypes.byref(MID), P4, None) == EINVAL
+    assert f(P1, x8, P4, w8, ctypes.byref(MID), P4, None) == EALIGN
+    assert f(P4, Fmt(9, 0), P4, w8, ctypes.byref(MID), P4, None) == EINVAL
+    big = Conv2dDesc(16, 512, 55, 55, 384, 3, 3, 1, 1, 1, 1)   # workspace beyond the 64 MiB array
+    assert f(P4, x8, P4, w8, ctypes.byref(big), P4, None) == ENOSPC
+    assert b"scratch array" in L.samd_last_error()
