@@ -25,6 +25,9 @@ Readings of the paper (each one is pinned by a test in tests/test_samd_model.py)
 * signed-values section: a negative lane n lowers lane n+1 (the more significant
   neighbour) by one; the fix-up adds lane n's sign bit into lane n+1.
 * 1-bit signed values are {-1, 0} (two's complement).
+* optimisations for permanent spacer bits (Sec. 6.1): where every result lane keeps its
+  MSB as a spacer (its value fits lane - 1 bits), the fix-up's final xor is left out and
+  each lane is read from its low lane - 1 bits (``fixup_spacer``, ``decode_spacer``).
 """
 from __future__ import annotations
 
@@ -178,6 +181,30 @@ def fixup(product: int, lane: int, width: int) -> int:
     lane is its own two's-complement value."""
     s = product & msb_lane_mask(lane, width)
     return ((product + s) & wmask(width)) ^ s
+
+
+def fixup_spacer(product: int, lane: int, count: int, width: int) -> int:
+    """The fix-up with a permanent spacer bit in every lane's MSB (Sec. 6.1): the sign
+    bits of the result lanes below the top one are added to themselves as in ``fixup``,
+    and the final xor, which only restores the MSBs, is left out.  Lane values must then
+    fit lane - 1 bits (the MSB carries no value bit)."""
+    s = product & msb_lane_mask(lane, width) & wmask((count - 1) * lane)
+    return (product + s) & wmask(width)
+
+
+def decode_spacer(product: int, lane: int, count: int, width: int) -> List[int]:
+    """Signed result lanes with a permanent spacer MSB: ``fixup_spacer``, then every lane
+    below the top one from its low lane - 1 bits, sign-extended, and the top lane from
+    all remaining bits of the word as a two's-complement number."""
+    w = fixup_spacer(product, lane, count, width)
+    out = []
+    for i in range(count - 1):
+        f = (w >> (i * lane)) & wmask(lane - 1)
+        out.append(f - (1 << (lane - 1)) if f >> (lane - 2) else f)
+    top_bits = width - (count - 1) * lane
+    t = w >> ((count - 1) * lane)
+    out.append(t - (1 << top_bits) if t >> (top_bits - 1) else t)
+    return out
 
 
 def fixup_obvious(product: int, lane: int, width: int) -> int:

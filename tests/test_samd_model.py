@@ -359,3 +359,66 @@ def test_samd2_holds_the_ternary_set():
     vals = [-1, 0, 1, -1, 1, 0, 0, 1]
     words, bad = ref.pack(np.array(vals), 2, True)
     assert bad == 0 and list(ref.unpack(words, len(vals), 2, True)) == vals
+
+
+# --- Sec. 6.1: optimisations for permanent spacer bits ------------------------------
+
+def test_spacer_fixup_exhaustive_small():
+    # every b <= 3 input vector of up to 4 lanes and kernel of up to 3 taps, summed over up
+    # to 3 channels, in lanes one bit wider than the accumulated range needs (the MSB is a
+    # permanent spacer): the fix-up without its xor, read from the low lane - 1 bits, gives
+    # every lane exactly, as the full fix-up does
+    for bits in (1, 2, 3):
+        vals = range(-(1 << (bits - 1)), 1 << (bits - 1))
+        for I, K, G in ((1, 1, 1), (2, 2, 1), (3, 2, 2), (4, 3, 1), (2, 3, 3)):
+            lane = (G * min(I, K) * (1 << (bits - 1)) ** 2).bit_length() + 2
+            cases = list(itertools.product(vals, repeat=I))
+            kernels = list(itertools.product(vals, repeat=K))
+            rnd = random.Random(7 + bits * 100 + I * 10 + K)
+            pairs = [(c, k) for c in cases for k in kernels] if len(cases) * len(kernels) <= 4096 else \
+                [(rnd.choice(cases), rnd.choice(kernels)) for _ in range(4096)]
+            for xs, ks in pairs:
+                acc = 0
+                want = np.zeros(I + K - 1, dtype=np.int64)
+                for g in range(G):
+                    xg = [((v + g) % (1 << bits)) - (1 << (bits - 1)) if g else v for v in xs]
+                    acc += sm.to_signed(sm.pack_lanes_signed(xg, bits, lane, True), 64) * \
+                        sm.to_signed(sm.pack_lanes_signed(ks, bits, lane, True), 64)
+                    want += np.convolve(xg, ks)
+                acc &= (1 << 128) - 1
+                n = I + K - 1
+                assert sm.decode_spacer(acc, lane, n, 128) == list(want)
+                assert sm.word_to_lanes(sm.fixup(acc, lane, 128), lane, n, signed=True) == list(want)
+
+
+def test_spacer_fixup_needs_the_spare_msb():
+    # a lane value that needs the MSB (outside lane - 1 signed bits) is misread without the
+    # xor: -2**(lane-2) - 1 in a 9-bit lane reads as a positive number
+    lane = 9
+    vals = [3, -(1 << (lane - 2)) - 1, 7]
+    word = sum(v << (i * lane) for i, v in enumerate(vals)) & ((1 << 64) - 1)
+    assert sm.word_to_lanes(sm.fixup(word, lane, 64), lane, 3, signed=True) == vals
+    assert sm.decode_spacer(word, lane, 3, 64)[1] != vals[1]
+    # random words whose lanes all fit lane - 1 bits: both decodes agree
+    rnd = random.Random(61)
+    for _ in range(4000):
+        n = rnd.randint(2, 7)
+        digits = [rnd.randint(-(1 << (lane - 2)), (1 << (lane - 2)) - 1) for _ in range(n - 1)]
+        digits.append(rnd.randint(-(1 << 20), 1 << 20))
+        word = sum(d << (i * lane) for i, d in enumerate(digits)) & ((1 << 128) - 1)
+        assert sm.decode_spacer(word, lane, n, 128) == digits
+
+
+def test_spacer_accumulation_needs_no_msb_clearing():
+    # Sec. 6.1's second point: results that feed further additions need no clearing of
+    # their MSBs.  Here every addition happens on the exact products before any lane is
+    # read, so sums over channels decode exactly with the spacer fix-up
+    rnd = random.Random(5)
+    bits, lane, G = 4, 13, 9
+    for _ in range(500):
+        xs = [[rnd.randint(-8, 7) for _ in range(4)] for _ in range(G)]
+        ks = [[rnd.randint(-8, 7) for _ in range(3)] for _ in range(G)]
+        acc = sum(sm.to_signed(sm.pack_lanes_signed(x, bits, lane, True), 64) *
+                  sm.to_signed(sm.pack_lanes_signed(k, bits, lane, True), 64) for x, k in zip(xs, ks))
+        want = sum(np.convolve(x, k) for x, k in zip(xs, ks))
+        assert sm.decode_spacer(acc & ((1 << 128) - 1), lane, 6, 128) == list(want)
