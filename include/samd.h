@@ -90,7 +90,10 @@ enum {
  *   rows_per_thread, shared_rows: output rows each lane computes, and whether they share
  *                operand loads (3-row, stride-1 kernels: RH + 2 loads per channel and
  *                kernel word instead of 3 RH)
- *   model_cost   the planner's cost estimate (issue cycles of one compute unit) */
+ *   model_cost   the planner's cost estimate (issue cycles of one compute unit)
+ *   layout_spaced 1: a plan of the permanent-spacer layout (samd_conv2d_spaced*)
+ *   spacer_msb   1: result lanes keep their MSB as a spacer bit; the decode leaves out
+ *                the fix-up's xor (Sec. 6.1) */
 typedef struct {
     int32_t lane_bits, lanes, taps_max, words_per_row, flush_channels, out_lanes, tap_words;
     int32_t phase[16], tap0[16], ntaps[16];
@@ -100,6 +103,7 @@ typedef struct {
     double macs_per_mad;
     int32_t rows_per_thread, shared_rows;
     double model_cost;
+    int32_t layout_spaced, spacer_msb;
 } samd_conv2d_plan;
 
 /* Human-readable name of a status code; never NULL. */
@@ -207,6 +211,75 @@ int samd_conv2d_stage(const uint32_t *x, samd_fmt xf, samd_fmt wf, const samd_co
                       size_t ws_bytes, hipStream_t stream);
 int samd_conv2d_accumulate(samd_fmt xf, samd_fmt wf, const samd_conv2d_desc *d, int32_t *y, const void *ws,
                            size_t ws_bytes, hipStream_t stream);
+
+/* ---- Permanent-spacer activations (Sec. 2.2 permanent spacer bits, Sec. 6.1) ----
+ * The packed format above keeps storage dense and inserts spacer bits inside every call
+ * (temporary spacer bits, Sec. 2.2); the multiply then reads operand words spread from
+ * it.  The permanent-spacer layout stores a layer's activations already spread: lanes of
+ * L bits with the spacer bits in place, in exactly the words the multiply reads, so a
+ * convolution from it has no spread pass (more bytes stored, fewer operations per call:
+ * the trade-off of the paper's permanent spacer bits).  Lanes of signed results keep
+ * their MSB as a permanent spacer bit (the planner bounds every lane's value to L - 1
+ * bits), so the decode leaves out the fix-up's final xor and reads L - 1-bit fields, the
+ * optimisation of Sec. 6.1; sums over channels are taken on the exact products before
+ * any lane is read, so no spacer ever needs clearing before an addition.
+ *
+ * The layout belongs to one layer (descriptor and formats) and its plan: word q of
+ * kernel-word variant t of padded row hp (hp in [0, H + 2 pad_h); rows of the zero padding
+ * are stored) of channel c of image n is word ((n C + c) padded_rows + hp) tap_words + t)
+ * words_per_row + q, the signed 32-bit sum over lanes i < lanes of (v - x_offset) 2^(i
+ * lane_bits), v the activation in row hp - pad_h, column stride_w (q lanes + delta[t] + i)
+ * + phase[t] - pad_w (0 outside the image), where delta[t] = tap0[t] + ntaps[t] - taps_max
+ * and phase/tap0/ntaps/taps_max are the plan's (samd_conv2d_spaced_plan_query).  One
+ * spare channel's words follow the last image (read, never used).  Plans of this layout
+ * are chosen, cached and tuned separately from the packed layout's; tuning the layout's
+ * plan changes the layout, so tensors must be written again after tuning. */
+typedef struct {
+    int32_t lane_bits, lanes, words_per_row, tap_words, padded_rows, x_offset, spacer_msb;
+    int64_t words;   /* int32 words of one layer's activations, the spare channel included */
+} samd_spaced_layout;
+
+/* Host-only: the layout of (xf, wf, *d) and the plan behind it. */
+int samd_conv2d_spaced_layout(const samd_conv2d_desc *d, samd_fmt xf, samd_fmt wf, samd_spaced_layout *out);
+int samd_conv2d_spaced_plan_query(const samd_conv2d_desc *d, samd_fmt xf, samd_fmt wf, samd_conv2d_plan *out);
+
+/* Workspace bytes of the permanent-spacer convolution (kernel words, correction table,
+ * ticket counters; no operand words), and its preparation (as samd_conv2d_prepare, under
+ * the layout's plan).  A workspace serves one launch at a time. */
+int samd_conv2d_spaced_workspace(const samd_conv2d_desc *d, samd_fmt xf, samd_fmt wf, size_t *bytes);
+int samd_conv2d_spaced_prepare(const uint32_t *w, samd_fmt wf, const samd_conv2d_desc *d, samd_fmt xf, void *ws,
+                               size_t ws_bytes, hipStream_t stream);
+
+/* Write a layer's activations in the layout: from 8-bit values (int8 when xf.is_signed,
+ * else uint8; N x C x H x W; each value enters as its low xf.bits bits), or from packed
+ * rows (the packed format; the samd_conv2d_stage step into a caller buffer).  dst holds
+ * samd_spaced_layout.words int32 words. */
+int samd_conv2d_spaced_pack(const void *src, samd_fmt xf, samd_fmt wf, const samd_conv2d_desc *d, uint32_t *dst,
+                            hipStream_t stream);
+int samd_conv2d_spaced_from_packed(const uint32_t *x, samd_fmt xf, samd_fmt wf, const samd_conv2d_desc *d,
+                                   uint32_t *dst, hipStream_t stream);
+
+/* The convolution of samd_conv2d from activations in the layout: xs as written above,
+ * ws prepared by samd_conv2d_spaced_prepare; y int32 N x M x Ho x Wo. */
+int samd_conv2d_spaced(const uint32_t *xs, samd_fmt xf, samd_fmt wf, const samd_conv2d_desc *d, int32_t *y,
+                       const void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* ReLU and requantisation of samd_relu_requant_pack, written as the next layer's
+ * activations in the layout (format xf, unsigned; weight format wf; descriptor *d of the
+ * next layer): the activations go from one layer's int32 outputs to the next layer's
+ * spaced lanes without the packed form.  dev_shift nullable. */
+int samd_relu_requant_spaced(const int32_t *acc, const int32_t *dev_max, samd_fmt xf, samd_fmt wf,
+                             const samd_conv2d_desc *d, uint32_t *dst, int32_t *dev_shift, hipStream_t stream);
+
+/* samd_conv2d_tune for the layout's plan: the candidates of the permanent-spacer plan,
+ * each timed on the multiply alone (the layout is written once per candidate, untimed),
+ * from x given as packed rows; the chosen plan becomes the layout's plan.  Arguments and
+ * workspace size (samd_conv2d_spaced_tune_workspace) as for samd_conv2d_tune. */
+int samd_conv2d_spaced_tune_workspace(const samd_conv2d_desc *d, samd_fmt xf, samd_fmt wf, int32_t candidates,
+                                      size_t *bytes);
+int samd_conv2d_spaced_tune(const uint32_t *x, samd_fmt xf, const uint32_t *w, samd_fmt wf,
+                            const samd_conv2d_desc *d, int32_t *y, void *ws, size_t ws_bytes, int32_t candidates,
+                            int32_t reps, samd_conv2d_plan *chosen, hipStream_t stream);
 
 /* ---- Allocation-free convolution ----
  * For callers that cannot allocate device memory (code under HIP graph capture, tight

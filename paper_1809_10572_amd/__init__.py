@@ -21,7 +21,9 @@ __all__ = ["Fmt", "Conv2dDesc", "Conv1dPlan", "Conv2dPlan", "SamdError", "lib", 
            "conv2d_workspace", "conv2d", "conv2d_noalloc", "conv2d_prepare", "conv2d_prepared",
            "conv2d_stage", "conv2d_accumulate",
            "conv2d_int8_prepare", "conv2d_int8_prepared", "conv2d_int8_workspace", "conv2d_int8", "conv2d_int8_plan",
-           "conv2d_int8_candidates", "conv2d_int8_use_plan", "max_i32",
+           "conv2d_int8_candidates", "conv2d_int8_use_plan",
+           "SpacedLayout", "conv2d_spaced_layout", "conv2d_spaced_plan", "conv2d_spaced_workspace", "conv2d_spaced_prepare",
+           "conv2d_spaced_pack", "conv2d_spaced_from_packed", "conv2d_spaced", "relu_requant_spaced", "conv2d_spaced_tune", "max_i32",
            "relu_requant_pack", "relu_requant_nhwc_u8", "out_hw", "peak_launch", "peak_work", "LIB_PATH"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsamd.so")
@@ -61,7 +63,14 @@ class Conv2dPlan(ctypes.Structure):
                 ("split_waves", ctypes.c_int32), ("chunk_channels", ctypes.c_int32), ("x_offset", ctypes.c_int32),
                 ("col_segments", ctypes.c_int32), ("segment_columns", ctypes.c_int32),
                 ("macs_per_mad", ctypes.c_double), ("rows_per_thread", ctypes.c_int32),
-                ("shared_rows", ctypes.c_int32), ("model_cost", ctypes.c_double)]
+                ("shared_rows", ctypes.c_int32), ("model_cost", ctypes.c_double),
+                ("layout_spaced", ctypes.c_int32), ("spacer_msb", ctypes.c_int32)]
+
+
+class SpacedLayout(ctypes.Structure):
+    _fields_ = [("lane_bits", ctypes.c_int32), ("lanes", ctypes.c_int32), ("words_per_row", ctypes.c_int32),
+                ("tap_words", ctypes.c_int32), ("padded_rows", ctypes.c_int32), ("x_offset", ctypes.c_int32),
+                ("spacer_msb", ctypes.c_int32), ("words", ctypes.c_int64)]
 
 
 class Conv2dInt8Plan(ctypes.Structure):
@@ -136,6 +145,21 @@ def lib():
             "samd_conv2d_use_plan": (ctypes.c_int, [ctypes.POINTER(Conv2dDesc), Fmt, Fmt,
                                                     ctypes.POINTER(Conv2dPlan)]),
             "samd_conv2d_noalloc": (ctypes.c_int, [_p, Fmt, _p, Fmt, ctypes.POINTER(Conv2dDesc), _p, _p]),
+            "samd_conv2d_spaced_layout": (ctypes.c_int, [ctypes.POINTER(Conv2dDesc), Fmt, Fmt,
+                                                         ctypes.POINTER(SpacedLayout)]),
+            "samd_conv2d_spaced_plan_query": (ctypes.c_int, [ctypes.POINTER(Conv2dDesc), Fmt, Fmt,
+                                                             ctypes.POINTER(Conv2dPlan)]),
+            "samd_conv2d_spaced_workspace": (ctypes.c_int, [ctypes.POINTER(Conv2dDesc), Fmt, Fmt,
+                                                            ctypes.POINTER(_sz)]),
+            "samd_conv2d_spaced_prepare": (ctypes.c_int, [_p, Fmt, ctypes.POINTER(Conv2dDesc), Fmt, _p, _sz, _p]),
+            "samd_conv2d_spaced_pack": (ctypes.c_int, [_p, Fmt, Fmt, ctypes.POINTER(Conv2dDesc), _p, _p]),
+            "samd_conv2d_spaced_from_packed": (ctypes.c_int, [_p, Fmt, Fmt, ctypes.POINTER(Conv2dDesc), _p, _p]),
+            "samd_conv2d_spaced": (ctypes.c_int, [_p, Fmt, Fmt, ctypes.POINTER(Conv2dDesc), _p, _p, _sz, _p]),
+            "samd_relu_requant_spaced": (ctypes.c_int, [_p, _p, Fmt, Fmt, ctypes.POINTER(Conv2dDesc), _p, _p, _p]),
+            "samd_conv2d_spaced_tune_workspace": (ctypes.c_int, [ctypes.POINTER(Conv2dDesc), Fmt, Fmt, _i32,
+                                                                 ctypes.POINTER(_sz)]),
+            "samd_conv2d_spaced_tune": (ctypes.c_int, [_p, Fmt, _p, Fmt, ctypes.POINTER(Conv2dDesc), _p, _p, _sz, _i32,
+                                                       _i32, ctypes.POINTER(Conv2dPlan), _p]),
             "samd_peak_launch": (ctypes.c_int, [ctypes.c_int, _i64, _i32, _p, _p, _i64, _p]),
             "samd_peak_work": (ctypes.c_double, [ctypes.c_int, _i64, _i32, _i64]),
         }
@@ -319,7 +343,7 @@ def conv2d_tune(xp: torch.Tensor, xfmt: Fmt, wp: torch.Tensor, wfmt: Fmt, shape,
 
 
 PLAN_KEY_FIELDS = ("lane_bits", "lanes", "x_offset", "shared_rows", "rows_per_thread", "rows_per_block", "mblock",
-                   "split_waves")
+                   "split_waves", "layout_spaced")
 
 
 def plan_key(plan: Conv2dPlan) -> dict:
@@ -332,7 +356,7 @@ def conv2d_use_plan(shape, xfmt: Fmt, wfmt: Fmt, plan) -> None:
     if isinstance(plan, dict):
         p = Conv2dPlan()
         for f in PLAN_KEY_FIELDS:
-            setattr(p, f, int(plan[f]))
+            setattr(p, f, int(plan.get(f, 0)))
         plan = p
     _check(lib().samd_conv2d_use_plan(ctypes.byref(Conv2dDesc.of(shape)), xfmt, wfmt, ctypes.byref(plan)))
 
@@ -599,3 +623,111 @@ def peak_launch(kind: int, iters: int, blocks: int, dst: torch.Tensor, src: Opti
         raise ValueError(f"dst must hold {need} bytes")
     _check(lib().samd_peak_launch(kind, iters, blocks, None if src is None else src.data_ptr(), dst.data_ptr(),
                                   nbytes, _stream(dst)))
+
+
+# --- permanent-spacer layout (include/samd.h, "Permanent-spacer activations") -----------
+
+def conv2d_spaced_layout(shape, xfmt: Fmt, wfmt: Fmt) -> SpacedLayout:
+    out = SpacedLayout()
+    _check(lib().samd_conv2d_spaced_layout(ctypes.byref(Conv2dDesc.of(shape)), xfmt, wfmt, ctypes.byref(out)))
+    return out
+
+
+def conv2d_spaced_plan(shape, xfmt: Fmt, wfmt: Fmt) -> Conv2dPlan:
+    plan = Conv2dPlan()
+    _check(lib().samd_conv2d_spaced_plan_query(ctypes.byref(Conv2dDesc.of(shape)), xfmt, wfmt, ctypes.byref(plan)))
+    return plan
+
+
+def conv2d_spaced_workspace(shape, xfmt: Fmt, wfmt: Fmt) -> int:
+    n = _sz(0)
+    _check(lib().samd_conv2d_spaced_workspace(ctypes.byref(Conv2dDesc.of(shape)), xfmt, wfmt, ctypes.byref(n)))
+    return int(n.value)
+
+
+def _spaced_out(out: Optional[torch.Tensor], shape, xfmt: Fmt, wfmt: Fmt, device) -> torch.Tensor:
+    words = conv2d_spaced_layout(shape, xfmt, wfmt).words
+    if out is None:
+        return torch.empty(words, dtype=torch.int32, device=device)
+    return _min(out, torch.int32, words, "out")
+
+
+def conv2d_spaced_prepare(wp: torch.Tensor, wfmt: Fmt, shape, xfmt: Fmt, ws: Optional[torch.Tensor] = None):
+    """Kernel words of one layer for the permanent-spacer convolution."""
+    _w_words(wp, shape, wfmt)
+    if ws is None:
+        ws = _workspace(conv2d_spaced_workspace(shape, xfmt, wfmt), wp.device)
+    _check(lib().samd_conv2d_spaced_prepare(wp.data_ptr(), wfmt, ctypes.byref(Conv2dDesc.of(shape)), xfmt,
+                                            ws.data_ptr(), _ws_bytes(ws), _stream(wp)))
+    return ws
+
+
+def conv2d_spaced_pack(values: torch.Tensor, xfmt: Fmt, wfmt: Fmt, shape,
+                       out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """8-bit activations (N x C x H x W, int8 when xfmt is signed, else uint8) written in
+    the layer's permanent-spacer layout."""
+    d = Conv2dDesc.of(shape)
+    _min(values, torch.int8 if xfmt.is_signed else torch.uint8, d.N * d.C * d.H * d.W, "values")
+    out = _spaced_out(out, shape, xfmt, wfmt, values.device)
+    _check(lib().samd_conv2d_spaced_pack(values.data_ptr(), xfmt, wfmt, ctypes.byref(d), out.data_ptr(),
+                                         _stream(values)))
+    return out
+
+
+def conv2d_spaced_from_packed(xp: torch.Tensor, xfmt: Fmt, wfmt: Fmt, shape,
+                              out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Packed activations (the packed format) rewritten in the permanent-spacer layout."""
+    _x_words(xp, shape, xfmt)
+    out = _spaced_out(out, shape, xfmt, wfmt, xp.device)
+    _check(lib().samd_conv2d_spaced_from_packed(xp.data_ptr(), xfmt, wfmt, ctypes.byref(Conv2dDesc.of(shape)),
+                                                out.data_ptr(), _stream(xp)))
+    return out
+
+
+def conv2d_spaced(xs: torch.Tensor, xfmt: Fmt, wfmt: Fmt, shape, ws: torch.Tensor,
+                  out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Convolution from activations in the permanent-spacer layout (no spread pass)."""
+    _min(xs, torch.int32, conv2d_spaced_layout(shape, xfmt, wfmt).words, "xs")
+    d = Conv2dDesc.of(shape)
+    Ho, Wo = out_hw(shape)
+    if out is None:
+        out = torch.empty((d.N, d.M, Ho, Wo), dtype=torch.int32, device=xs.device)
+    _out(out, d.N * d.M * Ho * Wo)
+    _check(lib().samd_conv2d_spaced(xs.data_ptr(), xfmt, wfmt, ctypes.byref(d), out.data_ptr(), ws.data_ptr(),
+                                    _ws_bytes(ws), _stream(xs)))
+    return out
+
+
+def relu_requant_spaced(acc: torch.Tensor, dev_max: torch.Tensor, bits: int, wfmt: Fmt, shape,
+                        out: Optional[torch.Tensor] = None, dev_shift: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """ReLU + requantisation to unsigned `bits`, written as the next layer's (descriptor
+    `shape`, weights `wfmt`) activations in the permanent-spacer layout."""
+    d = Conv2dDesc.of(shape)
+    _min(acc, torch.int32, d.N * d.C * d.H * d.W, "acc")
+    xf = Fmt(bits, False)
+    out = _spaced_out(out, shape, xf, wfmt, acc.device)
+    _check(lib().samd_relu_requant_spaced(acc.data_ptr(), _opt(dev_max, "dev_max"), xf, wfmt, ctypes.byref(d),
+                                          out.data_ptr(), _opt(dev_shift, "dev_shift"), _stream(acc)))
+    return out
+
+
+def conv2d_spaced_tune(xp: torch.Tensor, xfmt: Fmt, wp: torch.Tensor, wfmt: Fmt, shape, candidates: int = 16,
+                       reps: int = 5, ws: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None) -> Conv2dPlan:
+    """Tune the permanent-spacer layout's plan on packed inputs (blocks).  Tensors in the
+    layout and workspaces of the shape must be written and prepared again afterwards."""
+    _x_words(xp, shape, xfmt)
+    _w_words(wp, shape, wfmt)
+    d = Conv2dDesc.of(shape)
+    Ho, Wo = out_hw(shape)
+    if ws is None:
+        n = _sz(0)
+        _check(lib().samd_conv2d_spaced_tune_workspace(ctypes.byref(d), xfmt, wfmt, candidates, ctypes.byref(n)))
+        ws = _workspace(int(n.value), xp.device)
+    if out is None:
+        out = torch.empty((d.N, d.M, Ho, Wo), dtype=torch.int32, device=xp.device)
+    _out(out, d.N * d.M * Ho * Wo)
+    plan = Conv2dPlan()
+    _check(lib().samd_conv2d_spaced_tune(xp.data_ptr(), xfmt, wp.data_ptr(), wfmt, ctypes.byref(d), out.data_ptr(),
+                                         ws.data_ptr(), _ws_bytes(ws), candidates, reps, ctypes.byref(plan),
+                                         _stream(xp)))
+    return plan

@@ -206,6 +206,8 @@ void fill_plan(const Conv2dGeom &g, samd_conv2d_plan *out) {
     out->rows_per_thread = g.rh;
     out->shared_rows = g.rows_path;
     out->model_cost = g.cost;
+    out->layout_spaced = g.layout_spaced;
+    out->spacer_msb = g.spacer;
 }
 
 }  // namespace
@@ -339,6 +341,133 @@ int samd_conv2d(const uint32_t *x, samd_fmt xf, const uint32_t *w, samd_fmt wf, 
     st = launch_conv2d_prepare(w, g, ws, stream);
     if (st) return st;
     return launch_conv2d_samd(x, g, y, ws, stream);
+}
+
+}  // extern "C"
+
+namespace {
+
+// Validation and planning shared by the permanent-spacer entry points (ws may be NULL
+// where no workspace is used).
+int spaced_setup(samd_fmt xf, samd_fmt wf, const samd_conv2d_desc *d, Conv2dGeom &g) {
+    int st = check_fmt(xf, "xf");
+    if (!st) st = check_fmt(wf, "wf");
+    if (!st) st = check_conv2d_desc(d);
+    if (!st) st = check_overflow(d, xf, wf);
+    if (st) return st;
+    std::string err;
+    st = plan_conv2d(*d, xf, wf, g, err, 1);
+    if (st) return fail(st, "%s", err.c_str());
+    return SAMD_OK;
+}
+
+int spaced_ws(const Conv2dGeom &g, const void *ws, size_t ws_bytes) {
+    if (!ws) return fail(SAMD_EINVAL, "ws must not be NULL");
+    if (((uintptr_t)ws & 255) != 0) return fail(SAMD_EALIGN, "workspace not 256-byte aligned");
+    const size_t need = conv2d_xs_offset(g);
+    if (ws_bytes < need) return fail(SAMD_ENOSPC, "workspace %zu bytes < %zu needed", ws_bytes, need);
+    return SAMD_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int samd_conv2d_spaced_plan_query(const samd_conv2d_desc *d, samd_fmt xf, samd_fmt wf, samd_conv2d_plan *out) {
+    set_error("");
+    Conv2dGeom g;
+    int st = spaced_setup(xf, wf, d, g);
+    if (st) return st;
+    if (!out) return fail(SAMD_EINVAL, "out must not be NULL");
+    fill_plan(g, out);
+    return SAMD_OK;
+}
+
+int samd_conv2d_spaced_layout(const samd_conv2d_desc *d, samd_fmt xf, samd_fmt wf, samd_spaced_layout *out) {
+    set_error("");
+    Conv2dGeom g;
+    int st = spaced_setup(xf, wf, d, g);
+    if (st) return st;
+    if (!out) return fail(SAMD_EINVAL, "out must not be NULL");
+    *out = samd_spaced_layout{};
+    out->lane_bits = g.L;
+    out->lanes = g.I;
+    out->words_per_row = g.nq;
+    out->tap_words = g.ntw;
+    out->padded_rows = g.Hp;
+    out->x_offset = g.xoff;
+    out->spacer_msb = g.spacer;
+    out->words = g.spread_words + (int64_t)g.Hp * g.ntw * g.nq;
+    return SAMD_OK;
+}
+
+int samd_conv2d_spaced_workspace(const samd_conv2d_desc *d, samd_fmt xf, samd_fmt wf, size_t *bytes) {
+    set_error("");
+    Conv2dGeom g;
+    int st = spaced_setup(xf, wf, d, g);
+    if (st) return st;
+    if (!bytes) return fail(SAMD_EINVAL, "bytes must not be NULL");
+    *bytes = conv2d_xs_offset(g);
+    return SAMD_OK;
+}
+
+int samd_conv2d_spaced_prepare(const uint32_t *w, samd_fmt wf, const samd_conv2d_desc *d, samd_fmt xf, void *ws,
+                               size_t ws_bytes, hipStream_t stream) {
+    set_error("");
+    Conv2dGeom g;
+    int st = spaced_setup(xf, wf, d, g);
+    if (!st) st = spaced_ws(g, ws, ws_bytes);
+    if (st) return st;
+    if (!w) return fail(SAMD_EINVAL, "w must not be NULL");
+    if (!aligned4(w)) return fail(SAMD_EALIGN, "w not aligned");
+    return launch_conv2d_prepare(w, g, ws, stream);
+}
+
+int samd_conv2d_spaced_pack(const void *src, samd_fmt xf, samd_fmt wf, const samd_conv2d_desc *d, uint32_t *dst,
+                            hipStream_t stream) {
+    set_error("");
+    Conv2dGeom g;
+    int st = spaced_setup(xf, wf, d, g);
+    if (st) return st;
+    if (!src || !dst) return fail(SAMD_EINVAL, "src and dst must not be NULL");
+    if (!aligned4(dst)) return fail(SAMD_EALIGN, "dst not aligned");
+    return launch_conv2d_spread_bytes(src, g, (int32_t *)dst, stream);
+}
+
+int samd_conv2d_spaced_from_packed(const uint32_t *x, samd_fmt xf, samd_fmt wf, const samd_conv2d_desc *d,
+                                   uint32_t *dst, hipStream_t stream) {
+    set_error("");
+    Conv2dGeom g;
+    int st = spaced_setup(xf, wf, d, g);
+    if (st) return st;
+    if (!x || !dst) return fail(SAMD_EINVAL, "x and dst must not be NULL");
+    if (!aligned4(x) || !aligned4(dst)) return fail(SAMD_EALIGN, "x / dst not aligned");
+    return launch_conv2d_spread(x, g, nullptr, stream, (int32_t *)dst);
+}
+
+int samd_conv2d_spaced(const uint32_t *xs, samd_fmt xf, samd_fmt wf, const samd_conv2d_desc *d, int32_t *y,
+                       const void *ws, size_t ws_bytes, hipStream_t stream) {
+    set_error("");
+    Conv2dGeom g;
+    int st = spaced_setup(xf, wf, d, g);
+    if (!st) st = spaced_ws(g, ws, ws_bytes);
+    if (st) return st;
+    if (!xs || !y) return fail(SAMD_EINVAL, "xs and y must not be NULL");
+    if (!aligned4(xs) || !aligned4(y)) return fail(SAMD_EALIGN, "xs / y not aligned");
+    return launch_conv2d_multiply(g, y, ws, stream, (const int32_t *)xs);
+}
+
+int samd_relu_requant_spaced(const int32_t *acc, const int32_t *dev_max, samd_fmt xf, samd_fmt wf,
+                             const samd_conv2d_desc *d, uint32_t *dst, int32_t *dev_shift, hipStream_t stream) {
+    set_error("");
+    if (xf.is_signed) return fail(SAMD_EINVAL, "requantised activations are unsigned");
+    Conv2dGeom g;
+    int st = spaced_setup(xf, wf, d, g);
+    if (st) return st;
+    if (!acc || !dev_max || !dst) return fail(SAMD_EINVAL, "acc, dev_max and dst must not be NULL");
+    if (!aligned4(acc) || !aligned4(dev_max) || !aligned4(dst) || (dev_shift && !aligned4(dev_shift)))
+        return fail(SAMD_EALIGN, "acc / dev_max / dst / dev_shift not aligned");
+    return launch_relu_requant_stage(acc, dev_max, g, nullptr, dev_shift, stream, (int32_t *)dst);
 }
 
 int samd_conv2d_noalloc(const uint32_t *x, samd_fmt xf, const uint32_t *w, samd_fmt wf, const samd_conv2d_desc *d,
@@ -588,15 +717,19 @@ int samd_conv2d_candidates(const samd_conv2d_desc *d, samd_fmt xf, samd_fmt wf, 
     return SAMD_OK;
 }
 
-int samd_conv2d_tune_workspace(const samd_conv2d_desc *d, samd_fmt xf, samd_fmt wf, int32_t candidates,
-                               size_t *bytes) {
+}  // extern "C"
+
+namespace {
+
+int tune_workspace_impl(const samd_conv2d_desc *d, samd_fmt xf, samd_fmt wf, int32_t candidates, size_t *bytes,
+                        int spaced) {
     set_error("");
     int st = check_tune_args(d, xf, wf, candidates);
     if (st) return st;
     if (!bytes) return fail(SAMD_EINVAL, "bytes must not be NULL");
     std::vector<Conv2dGeom> cands;
     std::string err;
-    st = conv2d_candidates(*d, xf, wf, candidates, cands, err);
+    st = conv2d_candidates(*d, xf, wf, candidates, cands, err, spaced);
     if (st) return fail(st, "%s", err.c_str());
     size_t most = 0;
     for (const Conv2dGeom &c : cands) most = std::max(most, conv2d_workspace_bytes(c));
@@ -604,9 +737,30 @@ int samd_conv2d_tune_workspace(const samd_conv2d_desc *d, samd_fmt xf, samd_fmt 
     return SAMD_OK;
 }
 
-int samd_conv2d_tune(const uint32_t *x, samd_fmt xf, const uint32_t *w, samd_fmt wf, const samd_conv2d_desc *d,
-                     int32_t *y, void *ws, size_t ws_bytes, int32_t candidates, int32_t reps,
-                     samd_conv2d_plan *chosen, hipStream_t stream) {
+}  // namespace
+
+extern "C" {
+
+int samd_conv2d_tune_workspace(const samd_conv2d_desc *d, samd_fmt xf, samd_fmt wf, int32_t candidates,
+                               size_t *bytes) {
+    return tune_workspace_impl(d, xf, wf, candidates, bytes, 0);
+}
+
+int samd_conv2d_spaced_tune_workspace(const samd_conv2d_desc *d, samd_fmt xf, samd_fmt wf, int32_t candidates,
+                                      size_t *bytes) {
+    return tune_workspace_impl(d, xf, wf, candidates, bytes, 1);
+}
+
+}  // extern "C"
+
+namespace {
+
+// The tuner of both layouts.  Packed layout: each timed run is stage + accumulate.
+// Permanent-spacer layout: each candidate's operand words are written once (untimed) and
+// the timed run is the multiply alone - the spaced convolution.
+int tune_impl(const uint32_t *x, samd_fmt xf, const uint32_t *w, samd_fmt wf, const samd_conv2d_desc *d,
+              int32_t *y, void *ws, size_t ws_bytes, int32_t candidates, int32_t reps, samd_conv2d_plan *chosen,
+              hipStream_t stream, int spaced) {
     set_error("");
     int st = check_tune_args(d, xf, wf, candidates);
     if (st) return st;
@@ -616,7 +770,7 @@ int samd_conv2d_tune(const uint32_t *x, samd_fmt xf, const uint32_t *w, samd_fmt
     if (((uintptr_t)ws & 255) != 0) return fail(SAMD_EALIGN, "workspace not 256-byte aligned");
     std::vector<Conv2dGeom> cands;
     std::string err;
-    st = conv2d_candidates(*d, xf, wf, candidates, cands, err);
+    st = conv2d_candidates(*d, xf, wf, candidates, cands, err, spaced);
     if (st) return fail(st, "%s", err.c_str());
     // the candidates whose workspace fits next to the second output and its counter
     const size_t extra = tune_extra_bytes(*d, cands[0]);
@@ -653,7 +807,7 @@ int samd_conv2d_tune(const uint32_t *x, samd_fmt xf, const uint32_t *w, samd_fmt
     auto run = [&](const Conv2dGeom &c, int32_t *out, int n) {
         int rs = SAMD_OK;
         for (int r = 0; r < n && !rs; ++r)
-            if (!(rs = launch_conv2d_spread(x, c, ws, stream))) rs = launch_conv2d_multiply(c, out, ws, stream);
+            if (spaced || !(rs = launch_conv2d_spread(x, c, ws, stream))) rs = launch_conv2d_multiply(c, out, ws, stream);
         return rs;
     };
     auto timed = [&](const Conv2dGeom &c, int32_t *out, float &ms) {
@@ -671,7 +825,9 @@ int samd_conv2d_tune(const uint32_t *x, samd_fmt xf, const uint32_t *w, samd_fmt
         for (size_t i = 0; i < fit.size(); ++i) {
             const Conv2dGeom &c = fit[i];
             int32_t *out = i == 0 ? y : y_alt;   // the model's plan writes the reference into y
-            if ((st = launch_conv2d_prepare(w, c, ws, stream)) || (st = run(c, out, 1))) return cleanup(st);
+            if ((st = launch_conv2d_prepare(w, c, ws, stream)) ||
+                (spaced && (st = launch_conv2d_spread(x, c, ws, stream))) || (st = run(c, out, 1)))
+                return cleanup(st);
             if (pass == 0 && i == 0 && (st = run(c, out, 4 * reps))) return cleanup(st);
             if (pass == 0 && i > 0) {
                 // every candidate must reproduce the model plan's result exactly
@@ -705,6 +861,22 @@ int samd_conv2d_tune(const uint32_t *x, samd_fmt xf, const uint32_t *w, samd_fmt
     return cleanup(SAMD_OK);
 }
 
+}  // namespace
+
+extern "C" {
+
+int samd_conv2d_tune(const uint32_t *x, samd_fmt xf, const uint32_t *w, samd_fmt wf, const samd_conv2d_desc *d,
+                     int32_t *y, void *ws, size_t ws_bytes, int32_t candidates, int32_t reps,
+                     samd_conv2d_plan *chosen, hipStream_t stream) {
+    return tune_impl(x, xf, w, wf, d, y, ws, ws_bytes, candidates, reps, chosen, stream, 0);
+}
+
+int samd_conv2d_spaced_tune(const uint32_t *x, samd_fmt xf, const uint32_t *w, samd_fmt wf,
+                            const samd_conv2d_desc *d, int32_t *y, void *ws, size_t ws_bytes, int32_t candidates,
+                            int32_t reps, samd_conv2d_plan *chosen, hipStream_t stream) {
+    return tune_impl(x, xf, w, wf, d, y, ws, ws_bytes, candidates, reps, chosen, stream, 1);
+}
+
 int samd_conv2d_use_plan(const samd_conv2d_desc *d, samd_fmt xf, samd_fmt wf, const samd_conv2d_plan *plan) {
     set_error("");
     int st = check_tune_args(d, xf, wf, 1);
@@ -720,7 +892,7 @@ int samd_conv2d_use_plan(const samd_conv2d_desc *d, samd_fmt xf, samd_fmt wf, co
                    c.rows_path == want.shared_rows && c.rh == want.rows_per_thread &&
                    c.rows_blk == want.rows_per_block && c.mblk == want.mblock && c.ks == want.split_waves;
         },
-        g, err);
+        g, err, want.layout_spaced ? 1 : 0);
     if (st) return fail(st, "%s", err.c_str());
     set_tuned_conv2d(*d, xf, wf, g);
     return SAMD_OK;

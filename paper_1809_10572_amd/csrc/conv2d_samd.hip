@@ -134,6 +134,40 @@ __global__ __launch_bounds__(256) void spread_kernel(const uint32_t *__restrict_
     }
 }
 
+// The same operand words built from unpacked 8-bit values (int8 when S, else uint8; N C H W
+// row-major) instead of packed rows: the permanent-spacer layout written straight from
+// the values a caller holds.  Each value enters as its low b bits (sign-extended when S).
+template <int B, bool S>
+__global__ __launch_bounds__(256) void spread_bytes_kernel(const uint8_t *__restrict__ x, const Conv2dGeom g,
+                                                           int qshift, int32_t *__restrict__ xs) {
+    const uint32_t row = blockIdx.x * (256u >> qshift) + (threadIdx.x >> qshift);   // (n*C + c)*Hp + hp
+    if (row >= (uint32_t)(g.N * g.C * g.Hp)) return;
+    const uint32_t nc = row / (uint32_t)g.Hp;
+    const int hp = (int)(row - nc * (uint32_t)g.Hp);
+    const int h = hp - g.ph;
+    const bool inside = h >= 0 && h < g.H;
+    const uint8_t *src = x + ((int64_t)nc * g.H + (inside ? h : 0)) * g.W;
+    for (int q = threadIdx.x & ((1 << qshift) - 1); q < g.nq; q += 1 << qshift) {
+        int32_t *dst = xs + (int64_t)row * g.ntw * g.nq + q;
+        for (int t = 0; t < g.ntw; ++t) {
+            const int delta = g.tw_tap0[t] + g.tw_ntaps[t] - g.Kmax;
+            const int col0 = g.sw * (q * g.I + delta) + g.tw_phase[t] - g.pw;
+            uint32_t word = 0;
+            if (inside) {
+                for (int ii = 0; ii < g.I; ++ii) {
+                    const int col = col0 + g.sw * ii;
+                    if (col >= 0 && col < g.W) {
+                        const uint32_t f = src[col] & ((1u << B) - 1);
+                        const int32_t v = (S ? ((int32_t)(f << (32 - B)) >> (32 - B)) : (int32_t)f) - g.xoff;
+                        word += (uint32_t)v << (ii * g.L);
+                    }
+                }
+            }
+            dst[t * g.nq] = (int32_t)word;
+        }
+    }
+}
+
 // Operand words are read through a buffer resource over one image's operand words: the
 // per-lane byte offset is a VGPR, the per-step offset an SGPR (no address arithmetic in
 // the vector unit).  Word 3 is the gfx9 raw-buffer format (32-bit data, no swizzle).
@@ -163,30 +197,35 @@ __device__ __forceinline__ int32_t low_field(uint32_t w, int L) {
 // Decode of one accumulator (Sec. 6): the fix-up of the signed-convolution figure for
 // signed results, then lanes from the bottom - take the low L bits, shift them out -
 // each added into its output column (p + j); lane NL-1 takes all remaining bits.
-template <bool SG, int NL>
-__device__ __forceinline__ void decode_word(uint64_t v, uint64_t msb_mask, int L, int32_t *p) {
+// PS (permanent spacer bits, Sec. 6.1): every lane's MSB is a spacer bit (the planner
+// keeps its values within L - 1 bits), so the fix-up's final xor, which only restores the
+// MSB, is left out and each lane is read from its low L - 1 bits.
+template <bool SG, int NL, bool PS>
+__device__ __forceinline__ void decode_word(uint64_t v, uint64_t msb_mask, int L, int fw, int32_t *p) {
     if (SG) {
         const uint64_t s = v & msb_mask;
-        v = (v + s) ^ s;
+        v += s;
+        if (!PS) v ^= s;
     }
 #pragma unroll
     for (int j = 0; j < NL - 1; ++j) {
-        atomicAdd(p + j, low_field<SG>((uint32_t)v, L));
+        atomicAdd(p + j, low_field<SG>((uint32_t)v, PS ? fw : L));
         v = SG ? (uint64_t)((int64_t)v >> L) : v >> L;
     }
     atomicAdd(p + NL - 1, (int32_t)v);
 }
 
 // The same for a lane count known only at run time.
-template <bool SG>
-__device__ __forceinline__ void decode_word_n(uint64_t v, uint64_t msb_mask, int L, int nl, int32_t *p) {
+template <bool SG, bool PS>
+__device__ __forceinline__ void decode_word_n(uint64_t v, uint64_t msb_mask, int L, int fw, int nl, int32_t *p) {
     if (SG) {
         const uint64_t s = v & msb_mask;
-        v = (v + s) ^ s;
+        v += s;
+        if (!PS) v ^= s;
     }
 #pragma unroll 1
     for (int j = 0; j < nl - 1; ++j) {
-        atomicAdd(p + j, low_field<SG>((uint32_t)v, L));
+        atomicAdd(p + j, low_field<SG>((uint32_t)v, PS ? fw : L));
         v = SG ? (uint64_t)((int64_t)v >> L) : v >> L;
     }
     atomicAdd(p + nl - 1, (int32_t)v);
@@ -277,7 +316,7 @@ __global__ __launch_bounds__(1024) void conv2d_samd_kernel(const int32_t *__rest
     auto decode = [&]() {
         if (lane_ok) {
             const uint64_t msb = g.msb_mask;
-            const int L = g.L;
+            const int L = g.L, fw = g.L - 1;
             int ti = tidx0;
 #define SAMD_DECODE_LOOP(CALL)                                                                        \
     _Pragma("unroll") for (int m = 0; m < RM; ++m) {                                                 \
@@ -289,16 +328,27 @@ __global__ __launch_bounds__(1024) void conv2d_samd_kernel(const int32_t *__rest
         }                                                                                             \
         ti += mstride;                                                                                \
     }
-#define SAMD_DECODE_NL(NL_)                                                                           \
+#define SAMD_DECODE_NL(NL_, PS_)                                                                      \
     case NL_:                                                                                         \
-        SAMD_DECODE_LOOP((decode_word<SG, NL_>((uint64_t)acc[r][m], msb, L, tile + tr)))              \
+        SAMD_DECODE_LOOP((decode_word<SG, NL_, PS_>((uint64_t)acc[r][m], msb, L, fw, tile + tr)))     \
         break;
-            switch (g.nl) {
-                SAMD_DECODE_NL(2) SAMD_DECODE_NL(3) SAMD_DECODE_NL(4) SAMD_DECODE_NL(5)
-                SAMD_DECODE_NL(6) SAMD_DECODE_NL(7) SAMD_DECODE_NL(8)
-            default:
-                SAMD_DECODE_LOOP((decode_word_n<SG>((uint64_t)acc[r][m], msb, L, g.nl, tile + tr)))
+#define SAMD_DECODE_ALL(PS_)                                                                          \
+    switch (g.nl) {                                                                                   \
+        SAMD_DECODE_NL(2, PS_) SAMD_DECODE_NL(3, PS_) SAMD_DECODE_NL(4, PS_) SAMD_DECODE_NL(5, PS_)   \
+        SAMD_DECODE_NL(6, PS_) SAMD_DECODE_NL(7, PS_) SAMD_DECODE_NL(8, PS_)                          \
+    default:                                                                                          \
+        SAMD_DECODE_LOOP((decode_word_n<SG, PS_>((uint64_t)acc[r][m], msb, L, fw, g.nl, tile + tr)))  \
+    }
+            if constexpr (SG) {
+                if (g.spacer) {
+                    SAMD_DECODE_ALL(true)
+                } else {
+                    SAMD_DECODE_ALL(false)
+                }
+            } else {
+                SAMD_DECODE_ALL(false)
             }
+#undef SAMD_DECODE_ALL
 #undef SAMD_DECODE_NL
 #undef SAMD_DECODE_LOOP
         }
@@ -613,8 +663,8 @@ int launch_conv2d_prepare(const uint32_t *w, const Conv2dGeom &g, void *ws, hipS
     return check_launch("conv2d correction table");
 }
 
-int launch_conv2d_spread(const uint32_t *x, const Conv2dGeom &g, void *ws, hipStream_t s) {
-    int32_t *xs = (int32_t *)((char *)ws + conv2d_xs_offset(g));
+int launch_conv2d_spread(const uint32_t *x, const Conv2dGeom &g, void *ws, hipStream_t s, int32_t *dst) {
+    int32_t *xs = dst ? dst : (int32_t *)((char *)ws + conv2d_xs_offset(g));
     // 2^qshift threads per row, each building about 2.5 of its words (words q, q + 2^qshift,
     // ...): one word per thread was 5-23 % slower at the mid-size layer
     const int qshift = spread_qshift(g.nq);
@@ -636,6 +686,31 @@ int launch_conv2d_spread(const uint32_t *x, const Conv2dGeom &g, void *ws, hipSt
     SAMD_FOR_EACH_FMT(SAMD_SPREAD_CASE)
 #undef SAMD_SPREAD_CASE
     return check_launch("conv2d operand spread");
+}
+
+int launch_conv2d_spread_bytes(const void *x, const Conv2dGeom &g, int32_t *dst, hipStream_t s) {
+    const int qshift = spread_qshift(g.nq);
+    const int64_t nrows = (int64_t)g.N * g.C * g.Hp;
+    const int rpb = 256 >> qshift;
+    const int64_t blocks = (nrows + rpb - 1) / rpb;
+    // the planner refuses layers that would need 2^32 threads or more (addressable())
+    if (blocks * 256 > (int64_t)0xffffffff) {
+        set_error("conv2d spaced pack: more than 2^32 threads in one launch");
+        return SAMD_EUNSUPPORTED;
+    }
+    // the stored values' format: signed when the activations are (recentred unsigned
+    // activations are stored unsigned and shifted by xoff inside the kernel)
+    const bool sgn = g.xsigned != 0;
+    bool launched = false;
+#define SAMD_SPREAD_BYTES_CASE(B, SG)                                                                    \
+    if (!launched && g.xbits == B && sgn == SG) {                                                        \
+        hipLaunchKernelGGL((spread_bytes_kernel<B, SG>), dim3((unsigned)blocks), dim3(256), 0, s,       \
+                           (const uint8_t *)x, g, qshift, dst);                                          \
+        launched = true;                                                                                 \
+    }
+    SAMD_FOR_EACH_FMT(SAMD_SPREAD_BYTES_CASE)
+#undef SAMD_SPREAD_BYTES_CASE
+    return check_launch("conv2d spaced pack");
 }
 
 namespace {
@@ -673,12 +748,12 @@ int resident_workgroups(const void *kernel, int block, size_t shm, int &out) {
 }
 
 template <int RH, int NRT, bool SG, int RNTW, bool SEG>
-int launch_multiply_seg(const Conv2dGeom &g, int32_t *y, const void *ws, hipStream_t s) {
+int launch_multiply_seg(const Conv2dGeom &g, int32_t *y, const void *ws, hipStream_t s, const int32_t *src) {
     const int32_t *kw = (const int32_t *)ws;
     const int32_t *pre = (const int32_t *)((const char *)ws + conv2d_kw_bytes(g));
     unsigned long long *tickets =
         (unsigned long long *)((char *)const_cast<void *>(ws) + conv2d_queue_offset(g));
-    const int32_t *xs = (const int32_t *)((const char *)ws + conv2d_xs_offset(g));
+    const int32_t *xs = src ? src : (const int32_t *)((const char *)ws + conv2d_xs_offset(g));
     const int block = g.wm * g.ks * 64;
     const size_t shm = (size_t)g.lds_words * 4;
     const void *fn = (const void *)conv2d_samd_kernel<RH, NRT, SG, RNTW, SEG>;
@@ -694,18 +769,18 @@ int launch_multiply_seg(const Conv2dGeom &g, int32_t *y, const void *ws, hipStre
 }
 
 template <int RH, int NRT, bool SG, int RNTW>
-int launch_multiply(const Conv2dGeom &g, int32_t *y, const void *ws, hipStream_t s) {
-    return g.ncs > 1 ? launch_multiply_seg<RH, NRT, SG, RNTW, true>(g, y, ws, s)
-                     : launch_multiply_seg<RH, NRT, SG, RNTW, false>(g, y, ws, s);
+int launch_multiply(const Conv2dGeom &g, int32_t *y, const void *ws, hipStream_t s, const int32_t *src) {
+    return g.ncs > 1 ? launch_multiply_seg<RH, NRT, SG, RNTW, true>(g, y, ws, s, src)
+                     : launch_multiply_seg<RH, NRT, SG, RNTW, false>(g, y, ws, s, src);
 }
 
 }  // namespace
 
-int launch_conv2d_multiply(const Conv2dGeom &g, int32_t *y, const void *ws, hipStream_t s) {
+int launch_conv2d_multiply(const Conv2dGeom &g, int32_t *y, const void *ws, hipStream_t s, const int32_t *src) {
     if (g.rows_path) {
 #define SAMD_ROWS_CASE(RH_, NTW_, SG_)                                                                \
     if (g.rh == RH_ && g.ntw == NTW_ && (bool)g.result_signed == SG_)                                 \
-        return launch_multiply<RH_, 0, SG_, NTW_>(g, y, ws, s);
+        return launch_multiply<RH_, 0, SG_, NTW_>(g, y, ws, s, src);
         SAMD_ROWS_CASE(1, 1, false) SAMD_ROWS_CASE(2, 1, false) SAMD_ROWS_CASE(3, 1, false) SAMD_ROWS_CASE(4, 1, false)
         SAMD_ROWS_CASE(1, 2, false) SAMD_ROWS_CASE(2, 2, false) SAMD_ROWS_CASE(3, 2, false) SAMD_ROWS_CASE(4, 2, false)
         SAMD_ROWS_CASE(1, 1, true) SAMD_ROWS_CASE(2, 1, true) SAMD_ROWS_CASE(3, 1, true) SAMD_ROWS_CASE(4, 1, true)
@@ -715,7 +790,7 @@ int launch_conv2d_multiply(const Conv2dGeom &g, int32_t *y, const void *ws, hipS
 #define SAMD_CONV_CASE(RH_, NRT_, SG_)                                                                \
     if (g.rh == RH_ && (NRT_ == 0 ? (g.nrt != 3 && g.nrt != 6) : g.nrt == NRT_) &&                     \
         (bool)g.result_signed == SG_)                                                                 \
-        return launch_multiply<RH_, NRT_, SG_, 0>(g, y, ws, s);
+        return launch_multiply<RH_, NRT_, SG_, 0>(g, y, ws, s, src);
         SAMD_CONV_CASE(1, 3, false) SAMD_CONV_CASE(1, 6, false) SAMD_CONV_CASE(1, 0, false)
         SAMD_CONV_CASE(2, 3, false) SAMD_CONV_CASE(2, 6, false) SAMD_CONV_CASE(2, 0, false)
         SAMD_CONV_CASE(1, 3, true) SAMD_CONV_CASE(1, 6, true) SAMD_CONV_CASE(1, 0, true)
@@ -727,9 +802,9 @@ int launch_conv2d_multiply(const Conv2dGeom &g, int32_t *y, const void *ws, hipS
 }
 
 int launch_conv2d_samd(const uint32_t *x, const Conv2dGeom &g, int32_t *y, const void *ws, hipStream_t s) {
-    const int st = launch_conv2d_spread(x, g, const_cast<void *>(ws), s);
+    const int st = launch_conv2d_spread(x, g, const_cast<void *>(ws), s, nullptr);
     if (st) return st;
-    return launch_conv2d_multiply(g, y, ws, s);
+    return launch_conv2d_multiply(g, y, ws, s, nullptr);
 }
 
 }  // namespace samd

@@ -175,8 +175,8 @@ int launch_relu_requant_pack(const int32_t *acc, int64_t rows, int64_t len, cons
 }
 
 int launch_relu_requant_stage(const int32_t *acc, const int32_t *dev_max, const Conv2dGeom &g, void *ws,
-                              int32_t *dev_shift, hipStream_t s) {
-    int32_t *xs = (int32_t *)((char *)ws + conv2d_xs_offset(g));
+                              int32_t *dev_shift, hipStream_t s, int32_t *dst) {
+    int32_t *xs = dst ? dst : (int32_t *)((char *)ws + conv2d_xs_offset(g));
     const int qshift = spread_qshift(g.nq);   // ~2.5 words per thread, as the spread
     const int64_t nrows = (int64_t)g.N * g.C * g.Hp;
     const int rpb = kBlock >> qshift;

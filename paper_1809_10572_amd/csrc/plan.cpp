@@ -197,7 +197,10 @@ namespace {
 // xf: the activations as the lanes see them; xoff: the value subtracted from every
 // stored activation before it enters a lane (0, or 2^(b-1) for recentred unsigned
 // activations, which then behave as signed b-bit values).
-int search_lanes(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, int xoff, Conv2dGeom &best,
+// spacer: the permanent-spacer layout (Sec. 6.1): lanes of signed results keep their MSB
+// as a spacer bit - their values fit L - 1 bits - so the decode can leave out the
+// fix-up's final xor.
+int search_lanes(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, int xoff, int spacer, Conv2dGeom &best,
                  std::string &err, std::vector<Conv2dGeom> *all = nullptr) {
     Conv2dGeom g = {};
     g.N = d.N; g.C = d.C; g.H = d.H; g.W = d.W; g.M = d.M; g.KH = d.KH; g.KW = d.KW;
@@ -207,6 +210,8 @@ int search_lanes(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, int xoff, 
     g.xbits = xf.bits; g.xsigned = xoff ? 0 : xf.is_signed; g.wbits = wf.bits; g.wsigned = wf.is_signed;
     g.xoff = xoff;
     g.result_signed = (xf.is_signed || wf.is_signed) ? 1 : 0;
+    g.layout_spaced = spacer ? 1 : 0;
+    g.spacer = spacer && g.result_signed ? 1 : 0;
     g.xrw = (int32_t)row_words(d.W, xf.bits);
     g.wrw = (int32_t)row_words(d.KW, wf.bits);
 
@@ -260,7 +265,7 @@ int search_lanes(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, int xoff, 
             c.nl = top + 1;
             if (c.nl > kMaxOutLanes) continue;
             // largest number of channels whose sums every lane (and the whole word) holds
-            const i128 cap = c.result_signed ? pow2(L - 1) - 1 : pow2(L) - 1;
+            const i128 cap = c.result_signed ? (c.spacer ? pow2(L - 2) - 1 : pow2(L - 1) - 1) : pow2(L) - 1;
             i128 gmax = d.C;
             i128 place = 0;
             for (int j = 0; j < c.nl; ++j) {
@@ -322,15 +327,15 @@ int search_lanes(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, int xoff, 
 // signed b-bit value, so products are half as large and a lane holds twice as many;
 // the offset comes back exactly as 2^(b-1) times the sum of the weights over each
 // output's in-image taps.  Both are planned and the cheaper kept.
-int search_conv2d(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, Conv2dGeom &best, std::string &err,
-                  std::vector<Conv2dGeom> *all = nullptr) {
-    int st = search_lanes(d, xf, wf, 0, best, err, all);
+int search_conv2d(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, int spacer, Conv2dGeom &best,
+                  std::string &err, std::vector<Conv2dGeom> *all = nullptr) {
+    int st = search_lanes(d, xf, wf, 0, spacer, best, err, all);
     if (!xf.is_signed && wf.is_signed && xf.bits >= 2) {
         Conv2dGeom alt;
         std::string err2;
         const samd_fmt xs = {xf.bits, 1};
         const size_t first = all ? all->size() : 0;
-        if (search_lanes(d, xs, wf, 1 << (xf.bits - 1), alt, err2, all) == SAMD_OK) {
+        if (search_lanes(d, xs, wf, 1 << (xf.bits - 1), spacer, alt, err2, all) == SAMD_OK) {
             // the correction: four table lookups and a multiply-add per output, issued after
             // the last barrier where nothing hides their latency (about 40 issue cycles per
             // output in measurements on MI355X)
@@ -349,7 +354,7 @@ int search_conv2d(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, Conv2dGeo
 
 // Plans are a pure function of (shape, formats); the search prices thousands of launch
 // shapes, so found plans are kept (under a lock) and later calls look them up.
-using PlanKey = std::array<int32_t, 15>;
+using PlanKey = std::array<int32_t, 16>;
 std::mutex plan_mu;
 std::map<PlanKey, Conv2dGeom> plan_cache;
 constexpr size_t kPlanCacheMax = 4096;
@@ -357,15 +362,16 @@ constexpr size_t kPlanCacheMax = 4096;
 // and are kept until cleared, since workspaces prepared under them depend on them.
 std::map<PlanKey, Conv2dGeom> tuned_plans;
 
-PlanKey plan_key(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf) {
+PlanKey plan_key(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, int spacer) {
     return {d.N, d.C, d.H, d.W, d.M, d.KH, d.KW, d.stride_h, d.stride_w, d.pad_h, d.pad_w,
-            xf.bits, xf.is_signed, wf.bits, wf.is_signed};
+            xf.bits, xf.is_signed, wf.bits, wf.is_signed, spacer};
 }
 
 }  // namespace
 
-int plan_conv2d(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, Conv2dGeom &g, std::string &err) {
-    const PlanKey key = plan_key(d, xf, wf);
+int plan_conv2d(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, Conv2dGeom &g, std::string &err,
+                int spacer) {
+    const PlanKey key = plan_key(d, xf, wf, spacer);
     {
         std::lock_guard<std::mutex> lock(plan_mu);
         auto tu = tuned_plans.find(key);
@@ -379,7 +385,7 @@ int plan_conv2d(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, Conv2dGeom 
             return SAMD_OK;
         }
     }
-    int st = search_conv2d(d, xf, wf, g, err);
+    int st = search_conv2d(d, xf, wf, spacer, g, err);
     if (st == SAMD_OK && !addressable(d, g)) {
         err = "the layer exceeds the kernels' index ranges (operand words of one image above 2 GiB, a kernel-word "
               "slice above 2^31 words, or an operand spread of 2^32 threads or more)";
@@ -394,12 +400,12 @@ int plan_conv2d(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, Conv2dGeom 
 }
 
 int conv2d_candidates(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, int max_count,
-                      std::vector<Conv2dGeom> &out, std::string &err) {
+                      std::vector<Conv2dGeom> &out, std::string &err, int spacer) {
     out.clear();
     // the model alone (no cache, no tuned plan): its choice, then every priced candidate
     Conv2dGeom model;
     std::vector<Conv2dGeom> all;
-    int st = search_conv2d(d, xf, wf, model, err, &all);
+    int st = search_conv2d(d, xf, wf, spacer, model, err, &all);
     if (st) return st;
     if (!addressable(d, model)) {
         err = "the layer exceeds the kernels' index ranges (operand words of one image above 2 GiB, a kernel-word "
@@ -427,11 +433,11 @@ int conv2d_candidates(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, int m
 
 int find_conv2d_candidate(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf,
                           const std::function<bool(const Conv2dGeom &)> &match, Conv2dGeom &out,
-                          std::string &err) {
+                          std::string &err, int spacer) {
     // every priced candidate, unsorted (matching needs no ranking)
     Conv2dGeom model;
     std::vector<Conv2dGeom> all;
-    int st = search_conv2d(d, xf, wf, model, err, &all);
+    int st = search_conv2d(d, xf, wf, spacer, model, err, &all);
     if (st) return st;
     for (const Conv2dGeom &c : all)
         if (addressable(d, c) && match(c)) {
@@ -444,7 +450,7 @@ int find_conv2d_candidate(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf,
 
 void set_tuned_conv2d(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, const Conv2dGeom &g) {
     std::lock_guard<std::mutex> lock(plan_mu);
-    tuned_plans[plan_key(d, xf, wf)] = g;
+    tuned_plans[plan_key(d, xf, wf, g.layout_spaced)] = g;
 }
 
 void clear_tuned_conv2d(const samd_conv2d_desc *d, samd_fmt xf, samd_fmt wf) {
@@ -452,7 +458,7 @@ void clear_tuned_conv2d(const samd_conv2d_desc *d, samd_fmt xf, samd_fmt wf) {
     if (!d)
         tuned_plans.clear();
     else
-        tuned_plans.erase(plan_key(*d, xf, wf));
+        for (int spacer : {0, 1}) tuned_plans.erase(plan_key(*d, xf, wf, spacer));
 }
 
 // Workspace: kernel-word streams, the recentring correction table, the work queues of

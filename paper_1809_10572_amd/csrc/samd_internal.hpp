@@ -45,6 +45,10 @@ struct Conv2dGeom {
     int32_t L, I, Kmax, nq, G;      // lane bits, values/word, widest phase, words/row, flush channels
     int32_t nl;                     // decoded lanes per accumulator; lane nl-1 takes the remaining bits
     int32_t result_signed;          // any operand signed: lanes need the fix-up
+    int32_t layout_spaced;          // planned for the permanent-spacer layout (caller-held operand words)
+    int32_t spacer;                 // layout_spaced and result_signed: every decoded lane keeps its MSB
+                                    // as a spacer bit (values fit L - 1 bits), so the decode leaves out
+                                    // the fix-up's final xor and reads L - 1-bit fields (Sec. 6.1)
     uint64_t msb_mask;              // sign bit of lanes 0 .. nl-2
     int32_t ntw;                    // kernel words (and operand-word variants) per (channel, kernel row)
     int32_t tw_phase[kMaxTapWords], tw_tap0[kMaxTapWords], tw_ntaps[kMaxTapWords];
@@ -93,19 +97,23 @@ struct Conv1dGeom {
 };
 
 // Host planning (pure C++, no HIP calls).  Return SAMD_OK or an error with `err` set.
-int plan_conv2d(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, Conv2dGeom &g, std::string &err);
+// spacer: plan for the permanent-spacer layout (samd_conv2d_spaced*) instead of the
+// packed one; the two are planned, cached and tuned separately.
+int plan_conv2d(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, Conv2dGeom &g, std::string &err,
+                int spacer = 0);
 int plan_conv1d(int64_t n, samd_fmt xf, const int32_t *taps, int32_t K, samd_fmt kf, Conv1dGeom &g,
                 std::string &err);
 // Candidate plans of a shape, ranked by the model's cost, the model's choice first, at
 // most max_count of them (distinct lane geometries and launch shapes).
 int conv2d_candidates(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, int max_count,
-                      std::vector<Conv2dGeom> &out, std::string &err);
+                      std::vector<Conv2dGeom> &out, std::string &err, int spacer = 0);
 // The first of all candidate plans (no count limit) that `match` accepts.
 int find_conv2d_candidate(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf,
                           const std::function<bool(const Conv2dGeom &)> &match, Conv2dGeom &out,
-                          std::string &err);
+                          std::string &err, int spacer = 0);
 // Plans chosen by measurement take precedence in plan_conv2d until cleared (d == NULL:
-// every shape).
+// every shape; otherwise both layouts of the shape).  A plan is kept under its own
+// layout (g.layout_spaced).
 void set_tuned_conv2d(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, const Conv2dGeom &g);
 void clear_tuned_conv2d(const samd_conv2d_desc *d, samd_fmt xf, samd_fmt wf);
 size_t conv2d_workspace_bytes(const Conv2dGeom &g);
@@ -122,8 +130,12 @@ int launch_unpack(const uint32_t *src, int64_t rows, int64_t len, int bits, int 
 int launch_conv1d(const uint32_t *x, const Conv1dGeom &g, int32_t *y, hipStream_t s);
 int launch_conv2d_prepare(const uint32_t *w, const Conv2dGeom &g, void *ws, hipStream_t s);
 int launch_conv2d_samd(const uint32_t *x, const Conv2dGeom &g, int32_t *y, const void *ws, hipStream_t s);
-int launch_conv2d_spread(const uint32_t *x, const Conv2dGeom &g, void *ws, hipStream_t s);
-int launch_conv2d_multiply(const Conv2dGeom &g, int32_t *y, const void *ws, hipStream_t s);
+// The operand spread writes the workspace's operand words, or dst when given (the
+// permanent-spacer layout held by the caller); the multiply reads the workspace's, or src.
+int launch_conv2d_spread(const uint32_t *x, const Conv2dGeom &g, void *ws, hipStream_t s, int32_t *dst = nullptr);
+int launch_conv2d_spread_bytes(const void *x, const Conv2dGeom &g, int32_t *dst, hipStream_t s);
+int launch_conv2d_multiply(const Conv2dGeom &g, int32_t *y, const void *ws, hipStream_t s,
+                           const int32_t *src = nullptr);
 // samd_conv2d with the library's scratch array as the workspace (SAMD_ENOSPC when the
 // layer's workspace does not fit it).
 int launch_conv2d_noalloc(const uint32_t *x, const uint32_t *w, const Conv2dGeom &g, int32_t *y, hipStream_t s);
@@ -145,7 +157,7 @@ int launch_lanewise(int op, const uint32_t *a, const uint32_t *b, int64_t nwords
 int launch_relu_requant_pack(const int32_t *acc, int64_t rows, int64_t len, const int32_t *dev_max, int bits,
                              uint32_t *dst, int32_t *dev_shift, hipStream_t s);
 int launch_relu_requant_stage(const int32_t *acc, const int32_t *dev_max, const Conv2dGeom &g, void *ws,
-                              int32_t *dev_shift, hipStream_t s);
+                              int32_t *dev_shift, hipStream_t s, int32_t *dst = nullptr);
 int launch_relu_requant_nhwc_u8(const int32_t *acc, int N, int C, int H, int W, const int32_t *dev_max,
                                 int bits, uint8_t *dst, hipStream_t s);
 

@@ -343,3 +343,41 @@ def test_noalloc_validation_before_any_hip_call():
     big = Conv2dDesc(16, 512, 55, 55, 384, 3, 3, 1, 1, 1, 1)   # workspace beyond the 64 MiB array
     assert f(P4, x8, P4, w8, ctypes.byref(big), P4, None) == ENOSPC
     assert b"scratch array" in L.samd_last_error()
+
+
+def test_spaced_validation_before_any_hip_call():
+    L = samd.lib()
+    x8, w8 = Fmt(8, False), Fmt(8, True)
+    d = ctypes.byref(MID)
+    assert L.samd_conv2d_spaced(P4, x8, w8, None, P4, P4, 1 << 30, None) == EINVAL
+    assert L.samd_conv2d_spaced(None, x8, w8, d, P4, P4, 1 << 30, None) == EINVAL
+    assert L.samd_conv2d_spaced(P1, x8, w8, d, P4, P4, 1 << 30, None) == EALIGN
+    assert L.samd_conv2d_spaced(P4, x8, w8, d, P4, 0x10010, 1 << 30, None) == EALIGN   # workspace alignment
+    assert L.samd_conv2d_spaced(P4, x8, w8, d, P4, P4, 256, None) == ENOSPC
+    assert L.samd_conv2d_spaced_pack(None, x8, w8, d, P4, None) == EINVAL
+    assert L.samd_conv2d_spaced_pack(P4, x8, w8, d, P1, None) == EALIGN
+    assert L.samd_conv2d_spaced_from_packed(P1, x8, w8, d, P4, None) == EALIGN
+    assert L.samd_conv2d_spaced_prepare(None, w8, d, x8, P4, 1 << 30, None) == EINVAL
+    assert L.samd_relu_requant_spaced(P4, P4, Fmt(8, 1), w8, d, P4, None, None) == EINVAL   # signed activations
+    assert L.samd_relu_requant_spaced(P4, P4, x8, w8, d, P1, None, None) == EALIGN
+    assert L.samd_conv2d_spaced_pack(P4, Fmt(0, 0), w8, d, P4, None) == EINVAL
+    big = Conv2dDesc(1, 512, 16, 16, 1, 16, 16, 1, 1, 0, 0)
+    assert L.samd_conv2d_spaced_pack(P4, x8, w8, ctypes.byref(big), P4, None) == EOVERFLOW
+
+
+@pytest.mark.parametrize("bits", range(1, 9))
+def test_spaced_layout_and_workspace(bits):
+    import samd_workloads as wl
+    xf, wf = Fmt(bits, False), Fmt(bits, True)
+    lay = samd.conv2d_spaced_layout(wl.MID, xf, wf)
+    plan = samd.conv2d_spaced_plan(wl.MID, xf, wf)
+    assert (lay.lane_bits, lay.lanes, lay.words_per_row, lay.tap_words) == \
+        (plan.lane_bits, plan.lanes, plan.words_per_row, plan.tap_words)
+    d = wl.MID
+    assert lay.padded_rows == d.H + 2 * d.pad_h
+    assert lay.words == (d.N * d.C + 1) * lay.padded_rows * lay.tap_words * lay.words_per_row
+    # signed results keep every lane's MSB as a spacer: one bit of headroom more per lane
+    assert plan.layout_spaced == 1 and plan.spacer_msb == 1
+    assert samd.conv2d_spaced_workspace(d, xf, wf) < samd.conv2d_workspace(d, xf, wf)
+    # unsigned results need no fix-up, so no spacer bit
+    assert samd.conv2d_spaced_plan(d, xf, Fmt(bits, False)).spacer_msb == 0
