@@ -82,6 +82,10 @@ def parse():
     p.add_argument("--configs", action="store_true",
                    help="instead of the default workload, time the other workloads: the single small layer, "
                         "the 2^20-value conv1d (b = 1..8, 3 and 5 taps) and the extremes-heavy signed layer")
+    p.add_argument("--spacers", action="store_true",
+                   help="instead of the default workload, compare temporary and permanent spacer bits per bit width "
+                        "on the single, mid-size and extremes-heavy layers: time and HBM bytes of a convolution from "
+                        "packed activations (spread + multiply) and from the permanent-spacer layout (multiply)")
     p.add_argument("--lanewise", action="store_true",
                    help="instead of the default workload, time lane-wise add/sub/mul/scale on packed words (GB/s)")
     p.add_argument("--int8-counters", action="store_true",
@@ -587,6 +591,91 @@ def run_configs(args):
                       **out}), flush=True)
 
 
+def run_spacers(args):
+    """Temporary against permanent spacer bits (Sec. 2.2, Sec. 6.1, the two result sets of
+    Sec. 7): per workload and bit width, the convolution from packed activations (the
+    spread pass that inserts the spacer bits, then the multiply) and from activations
+    stored in the permanent-spacer layout (the multiply alone, whose decode also leaves
+    out the fix-up's xor), with the bytes each stores and moves, both checked against the
+    oracle.  Prints one JSON line."""
+    import numpy as np
+    import torch
+
+    import paper_1809_10572_amd as samd
+    import samd_workloads as wl
+    from oracle import reference as ref
+
+    dev = torch.device("cuda:0")
+    out = {}
+    for name, cfg, shape, bits_list in (("single", 1, wl.SINGLE, range(1, 9)), ("mid", 3, wl.MID, range(1, 9)),
+                                        ("stress", 4, wl.STRESS, wl.BITS_SWEEP[4])):
+        rows = []
+        Ho, Wo = samd.out_hw(shape)
+        macs = shape.N * shape.M * Ho * Wo * shape.C * shape.KH * shape.KW
+        for b in bits_list:
+            case = wl.conv2d_case(cfg, b, shape)
+            xf, wf = samd.Fmt(b, case.x_signed), samd.Fmt(b, case.w_signed)
+            x = torch.from_numpy(case.x.astype(np.int8 if case.x_signed else np.uint8)).to(dev)
+            wp = samd.pack(torch.from_numpy(case.w.astype(np.int8)).to(dev), b, case.w_signed)
+            xp = samd.pack(x, b, case.x_signed)
+            if not args.no_tune:
+                samd.conv2d_tune(xp, xf, wp, wf, shape, candidates=args.tune_candidates, reps=10)
+                samd.conv2d_spaced_tune(xp, xf, wp, wf, shape, candidates=args.tune_candidates, reps=10)
+            ws = samd.conv2d_prepare(wp, wf, shape, xf)
+            ws_s = samd.conv2d_spaced_prepare(wp, wf, shape, xf)
+            spaced = samd.conv2d_spaced_pack(x, xf, wf, shape)
+            y = torch.empty((shape.N, shape.M, Ho, Wo), dtype=torch.int32, device=dev)
+            y_s = torch.empty_like(y)
+            t_temp, t_temp_min = timed_graph_stats(lambda: samd.conv2d_prepared(xp, xf, wf, shape, ws, out=y),
+                                                   args.reps, args.kernel_warm_s, args.samples)
+            t_perm, t_perm_min = timed_graph_stats(lambda: samd.conv2d_spaced(spaced, xf, wf, shape, ws_s, out=y_s),
+                                                   args.reps, args.kernel_warm_s, args.samples)
+            t_spread, _ = timed_graph_stats(lambda: samd.conv2d_stage(xp, xf, wf, shape, ws), args.reps,
+                                            args.kernel_warm_s, args.samples)
+            samd.conv2d_prepared(xp, xf, wf, shape, ws, out=y)
+            samd.conv2d_spaced(spaced, xf, wf, shape, ws_s, out=y_s)
+            torch.cuda.synchronize()
+            rng = np.random.default_rng(cfg * 100 + b)
+            idx = np.stack([rng.integers(0, n, 512) for n in (shape.N, shape.M, Ho, Wo)], axis=1)
+            want = ref.conv2d_points(case.x, case.w, shape.as_tuple(), idx)
+            ok_t = bool(np.array_equal(y.cpu().numpy()[tuple(idx.T)], want))
+            ok_p = bool(np.array_equal(y_s.cpu().numpy()[tuple(idx.T)], want))
+            pt, pp = samd.conv2d_plan(shape, xf, wf), samd.conv2d_spaced_plan(shape, xf, wf)
+            lay = samd.conv2d_spaced_layout(shape, xf, wf)
+            packed_bytes = shape.N * shape.C * shape.H * samd.row_words(shape.W, b) * 4
+            words_t = shape.N * shape.C * (shape.H + 2 * shape.pad_h) * pt.tap_words * pt.words_per_row * 4
+            spaced_bytes = (lay.words - lay.padded_rows * lay.tap_words * lay.words_per_row) * 4
+            kw_t = shape.M * shape.C * shape.KH * pt.tap_words * 4
+            kw_p = shape.M * shape.C * shape.KH * pp.tap_words * 4
+            y_bytes = shape.N * shape.M * Ho * Wo * 4
+            rows.append({
+                "bits": b,
+                "temporary_us": round(t_temp * 1e6, 2), "temporary_us_min": round(t_temp_min * 1e6, 2),
+                "spread_us": round(t_spread * 1e6, 2),
+                "permanent_us": round(t_perm * 1e6, 2), "permanent_us_min": round(t_perm_min * 1e6, 2),
+                "temporary_gmacs": round(macs / t_temp / 1e9, 1), "permanent_gmacs": round(macs / t_perm / 1e9, 1),
+                "permanent_speedup": round(t_temp / t_perm, 3),
+                # bytes the activations occupy, and the bytes one call moves at best
+                "stored_bytes_temporary": packed_bytes, "stored_bytes_permanent": spaced_bytes,
+                "moved_bytes_temporary": packed_bytes + 2 * words_t + kw_t + y_bytes,
+                "moved_bytes_permanent": spaced_bytes + kw_p + y_bytes,
+                "lanes_temporary": f"L={pt.lane_bits} I={pt.lanes} G={pt.flush_channels}",
+                "lanes_permanent": f"L={pp.lane_bits} I={pp.lanes} G={pp.flush_channels} msb_spacer={pp.spacer_msb}",
+                "parity_temporary": ok_t, "parity_permanent": ok_p})
+            print(f"spacers: {name} b={b} temporary {t_temp * 1e6:.2f} us permanent {t_perm * 1e6:.2f} us "
+                  f"parity {ok_t} {ok_p}", file=sys.stderr, flush=True)
+        out[name] = rows
+    print(json.dumps({"metric": "temporary vs permanent spacer bits: conv2d time and bytes per bit width",
+                      "unit": "us", "n_gpus": 1, "data": "synthetic", "dtype": "int64",
+                      "config": {"single": "1x16x16x16 -> 16, 3x3, u_b x s_b",
+                                 "mid": "8x128x56x56 -> 128, 3x3, u_b x s_b",
+                                 "stress": "4x256x28x28 -> 256, 3x3, s_b x s_b, half the values at the range ends",
+                                 "temporary": "conv2d_prepared: spread of the packed activations + multiply",
+                                 "permanent": "conv2d_spaced: multiply from the permanent-spacer layout",
+                                 "plans": "model" if args.no_tune else "each layout's plan tuned at set-up"},
+                      **out}), flush=True)
+
+
 def run_vggb(args):
     """The paper's own experiment (Sec. 7): every VGG-B convolution layer at batch 1 with
     N-bit signed activations and weights, N = 8 down to 2, next to the native-int8
@@ -600,7 +689,7 @@ def run_vggb(args):
 
     dev = torch.device("cuda:0")
     bits_list = [int(b) for b in args.bits.split(",")] if args.bits_given else wl.BITS_SWEEP[6]
-    rows, tot_macs, tot_s, tot_int8_s = [], 0, 0.0, 0.0
+    rows, tot_macs, tot_s, tot_int8_s, tot_perm_s = [], 0, 0.0, 0.0, 0.0
     for li, shape in enumerate(wl.VGGB_LAYERS):
         Ho, Wo = samd.out_hw(shape)
         macs = shape.N * shape.M * Ho * Wo * shape.C * shape.KH * shape.KW
@@ -626,15 +715,27 @@ def run_vggb(args):
                                  args.kernel_warm_s)
             t_int8 = timed_graph(lambda: samd.conv2d_int8_prepared(x_nhwc, f, f, shape, ws8, out=y8), args.reps,
                                  args.kernel_warm_s)
+            # permanent spacer bits: the activations stored in the layer's spaced layout
+            if not args.no_tune:
+                samd.conv2d_spaced_tune(xp, f, wp, f, shape, candidates=args.tune_candidates, reps=10)
+            ws_s = samd.conv2d_spaced_prepare(wp, f, shape, f)
+            spaced = samd.conv2d_spaced_pack(x, f, f, shape)
+            y_s = torch.empty_like(y)
+            t_perm = timed_graph(lambda: samd.conv2d_spaced(spaced, f, f, shape, ws_s, out=y_s), args.reps,
+                                 args.kernel_warm_s)
+            samd.conv2d_spaced(spaced, f, f, shape, ws_s, out=y_s)
             torch.cuda.synchronize()
             rng = np.random.default_rng(li * 10 + b)
             idx = np.stack([rng.integers(0, n, 256) for n in (shape.N, shape.M, Ho, Wo)], axis=1)
             want = ref.conv2d_points(case.x, case.w, shape.as_tuple(), idx)
             ok = bool(np.array_equal(y.cpu().numpy()[tuple(idx.T)], want) and
-                      np.array_equal(y8.cpu().numpy()[tuple(idx.T)], want))
+                      np.array_equal(y8.cpu().numpy()[tuple(idx.T)], want) and
+                      np.array_equal(y_s.cpu().numpy()[tuple(idx.T)], want))
             p = samd.conv2d_plan(shape, f, f)
             rows.append({"layer": li + 1, "C": shape.C, "M": shape.M, "HW": shape.H, "bits": b,
                          "samd_us": round(t_samd * 1e6, 2), "pack_us": round(t_pack * 1e6, 2),
+                         "permanent_us": round(t_perm * 1e6, 2),
+                         "permanent_speedup_vs_int8": round(t_int8 / t_perm, 3),
                          "int8_us": round(t_int8 * 1e6, 2), "samd_gmacs": round(macs / t_samd / 1e9, 1),
                          "int8_gmacs": round(macs / t_int8 / 1e9, 1), "speedup_vs_int8": round(t_int8 / t_samd, 3),
                          "lane_bits": p.lane_bits, "lanes": p.lanes, "tap_words": p.tap_words,
@@ -644,16 +745,19 @@ def run_vggb(args):
             tot_macs += macs
             tot_s += t_samd
             tot_int8_s += t_int8
-            print(f"vggb: layer {li + 1} b={b} samd {t_samd * 1e6:.1f} us int8 {t_int8 * 1e6:.1f} us "
-                  f"parity {ok}", file=sys.stderr, flush=True)
+            tot_perm_s += t_perm
+            print(f"vggb: layer {li + 1} b={b} samd {t_samd * 1e6:.1f} us permanent {t_perm * 1e6:.1f} us "
+                  f"int8 {t_int8 * 1e6:.1f} us parity {ok}", file=sys.stderr, flush=True)
     line = {"metric": "VGG-B conv layers, N-bit signed activations and weights (N = 8..2), GMAC/s",
             "value": round(tot_macs / tot_s / 1e9, 1), "unit": "GMAC/s", "n_gpus": 1,
             "higher_is_better": True, "dtype": "int64", "data": "synthetic",
             "config": {"workload": "VGG-B's ten 3x3 convolution layers, batch 1, each layer on its own; "
-                                   "one call = stage + accumulate with prepared kernel words",
+                                   "one call = stage + accumulate with prepared kernel words (temporary spacer bits) "
+                                   "or the multiply from the permanent-spacer layout (permanent spacer bits)",
                        "bits": bits_list,
                        "plans": "model" if args.no_tune else f"tuned at set-up ({args.tune_candidates} candidates timed)"},
             "int8_gmacs": round(tot_macs / tot_int8_s / 1e9, 1),
+            "permanent_gmacs": round(tot_macs / tot_perm_s / 1e9, 1),
             "per_layer": rows}
     print(json.dumps(line), flush=True)
 
@@ -856,6 +960,9 @@ def main():
         return
     if args.lanewise:
         run_lanewise(args)
+        return
+    if args.spacers:
+        run_spacers(args)
         return
     if args.stack:
         run_stack(args)

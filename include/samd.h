@@ -218,11 +218,13 @@ int samd_conv2d_accumulate(samd_fmt xf, samd_fmt wf, const samd_conv2d_desc *d, 
  * it.  The permanent-spacer layout stores a layer's activations already spread: lanes of
  * L bits with the spacer bits in place, in exactly the words the multiply reads, so a
  * convolution from it has no spread pass (more bytes stored, fewer operations per call:
- * the trade-off of the paper's permanent spacer bits).  Lanes of signed results keep
- * their MSB as a permanent spacer bit (the planner bounds every lane's value to L - 1
- * bits), so the decode leaves out the fix-up's final xor and reads L - 1-bit fields, the
- * optimisation of Sec. 6.1; sums over channels are taken on the exact products before
- * any lane is read, so no spacer ever needs clearing before an addition.
+ * the trade-off of the paper's permanent spacer bits).  Lanes of signed results can keep
+ * their MSB as a permanent spacer bit (the planner then bounds every lane's value to
+ * L - 1 bits), so the decode leaves out the fix-up's final xor and reads L - 1-bit
+ * fields, the optimisation of Sec. 6.1; it halves the channels a lane holds before a
+ * decode, so the planner prices plans with and without it (samd_conv2d_plan.spacer_msb
+ * reports the choice).  Sums over channels are taken on the exact products before any
+ * lane is read, so no spacer ever needs clearing before an addition.
  *
  * The layout belongs to one layer (descriptor and formats) and its plan: word q of
  * kernel-word variant t of padded row hp (hp in [0, H + 2 pad_h); rows of the zero padding

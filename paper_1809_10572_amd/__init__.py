@@ -343,7 +343,7 @@ def conv2d_tune(xp: torch.Tensor, xfmt: Fmt, wp: torch.Tensor, wfmt: Fmt, shape,
 
 
 PLAN_KEY_FIELDS = ("lane_bits", "lanes", "x_offset", "shared_rows", "rows_per_thread", "rows_per_block", "mblock",
-                   "split_waves", "layout_spaced")
+                   "split_waves", "layout_spaced", "spacer_msb")
 
 
 def plan_key(plan: Conv2dPlan) -> dict:

@@ -890,7 +890,8 @@ int samd_conv2d_use_plan(const samd_conv2d_desc *d, samd_fmt xf, samd_fmt wf, co
         [&](const Conv2dGeom &c) {
             return c.L == want.lane_bits && c.I == want.lanes && c.xoff == want.x_offset &&
                    c.rows_path == want.shared_rows && c.rh == want.rows_per_thread &&
-                   c.rows_blk == want.rows_per_block && c.mblk == want.mblock && c.ks == want.split_waves;
+                   c.rows_blk == want.rows_per_block && c.mblk == want.mblock && c.ks == want.split_waves &&
+                   c.spacer == want.spacer_msb;
         },
         g, err, want.layout_spaced ? 1 : 0);
     if (st) return fail(st, "%s", err.c_str());

