@@ -82,6 +82,9 @@ def parse():
     p.add_argument("--configs", action="store_true",
                    help="instead of the default workload, time the other workloads: the single small layer, "
                         "the 2^20-value conv1d (b = 1..8, 3 and 5 taps) and the extremes-heavy signed layer")
+    p.add_argument("--conv1d", action="store_true",
+                   help="instead of the default workload, time the 2^20-value conv1d (b = 1..8, 3 and 5 taps) "
+                        "next to a store-only kernel writing the same output bytes")
     p.add_argument("--spacers", action="store_true",
                    help="instead of the default workload, compare temporary and permanent spacer bits per bit width "
                         "on the single, mid-size and extremes-heavy layers: time and HBM bytes of a convolution from "
@@ -565,20 +568,7 @@ def run_configs(args):
 
     for b in (4,):
         out["single"].append(conv2d_row(1, b, wl.SINGLE, wl.conv2d_case(1, b)))
-    for b in range(1, 9):
-        for K in (3, 5):
-            case = wl.conv1d_case(b, K)
-            n = case.x.size
-            xp = samd.pack(torch.from_numpy(case.x.astype(np.uint8)).to(dev).view(1, n), b, False).view(-1)
-            y = samd.conv1d(xp, n, b, case.k.tolist(), b)
-            t = timed_graph(lambda: samd.conv1d(xp, n, b, case.k.tolist(), b, out=y), args.reps, args.kernel_warm_s)
-            torch.cuda.synchronize()
-            ok = bool(np.array_equal(y.cpu().numpy(), ref.conv1d(case.x, case.k)))
-            nbytes = samd.row_words(n, b) * 4 + (n - K + 1) * 4
-            out["conv1d"].append({"bits": b, "taps": K, "us": round(t * 1e6, 2),
-                                  "gmacs": round((n - K + 1) * K / t / 1e9, 1),
-                                  "gbps": round(nbytes / t / 1e9, 1), "hbm_frac": round(nbytes / t / PEAK_HBM, 4),
-                                  "parity": ok})
+    out["conv1d"] = conv1d_rows(args)
     for b in wl.BITS_SWEEP[4]:
         out["stress"].append(conv2d_row(4, b, wl.STRESS, wl.conv2d_case(4, b)))
     print(json.dumps({"metric": "SAMD workloads 1, 2 and 4: GMAC/s and roofline fractions", "n_gpus": 1,
@@ -589,6 +579,71 @@ def run_configs(args):
                                  "timing": "stage + accumulate (kernel words prepared once); conv1d whole call",
                                  "plans": "model" if args.no_tune else "tuned at set-up"},
                       **out}), flush=True)
+
+
+def conv1d_rows(args):
+    """Workload 2 (2^20 unsigned b-bit values, 3 and 5 unsigned taps, valid mode) per
+    (b, K): the whole call's time, its algorithmic bytes (packed input + 4 B per output)
+    as a fraction of HBM peak, two floors timed the same way (a kernel that only stores
+    the output's bytes, and one that copies a buffer of that size: a load, then a store)
+    and a full-output parity check against the oracle."""
+    import numpy as np
+    import torch
+
+    import paper_1809_10572_amd as samd
+    import samd_workloads as wl
+    from oracle import reference as ref
+
+    dev = torch.device("cuda:0")
+    rows, floors = [], {}
+    for b in range(1, 9):
+        for K in (3, 5):
+            case = wl.conv1d_case(b, K)
+            n = case.x.size
+            xp = samd.pack(torch.from_numpy(case.x.astype(np.uint8)).to(dev).view(1, n), b, False).view(-1)
+            y = samd.conv1d(xp, n, b, case.k.tolist(), b)
+            t = timed_graph(lambda: samd.conv1d(xp, n, b, case.k.tolist(), b, out=y), args.reps, args.kernel_warm_s)
+            torch.cuda.synchronize()
+            ok = bool(np.array_equal(y.cpu().numpy(), ref.conv1d(case.x, case.k)))
+            out_bytes = (n - K + 1) * 4
+            if out_bytes not in floors:
+                # the output's bytes stored by the plain grid-stride store kernel (16 B per
+                # lane), and copied from a buffer of the same size (read + write)
+                n16 = out_bytes // 16
+                src = torch.ones(n16 * 16, dtype=torch.uint8, device=dev)
+                dst = torch.empty(n16 * 16, dtype=torch.uint8, device=dev)
+                blocks = (n16 + 255) // 256
+                floors[out_bytes] = (
+                    timed_graph(lambda: samd.peak_launch(samd.PEAK_WRITE, 1, blocks, dst, None, n16 * 16),
+                                args.reps, args.kernel_warm_s),
+                    timed_graph(lambda: samd.peak_launch(samd.PEAK_COPY, 1, blocks, dst, src, n16 * 16),
+                                args.reps, args.kernel_warm_s))
+            nbytes = samd.row_words(n, b) * 4 + out_bytes
+            p = samd.conv1d_plan(n, b, case.k.tolist(), b)
+            rows.append({"bits": b, "taps": K, "us": round(t * 1e6, 2),
+                         "gmacs": round((n - K + 1) * K / t / 1e9, 1),
+                         "gbps": round(nbytes / t / 1e9, 1), "hbm_frac": round(nbytes / t / PEAK_HBM, 4),
+                         "store_floor_us": round(floors[out_bytes][0] * 1e6, 2),
+                         "copy_floor_us": round(floors[out_bytes][1] * 1e6, 2),
+                         "vs_store_floor": round(t / floors[out_bytes][0], 3),
+                         "vs_copy_floor": round(t / floors[out_bytes][1], 3),
+                         "lane_bits": p.lane_bits, "lanes": p.lanes, "groups": p.groups, "extra": p.extra,
+                         "parity": ok})
+            print(f"conv1d: b={b} K={K} {t * 1e6:.2f} us (store floor {floors[out_bytes][0] * 1e6:.2f} us, "
+                  f"copy floor {floors[out_bytes][1] * 1e6:.2f} us) parity {ok}", file=sys.stderr, flush=True)
+    return rows
+
+
+def run_conv1d(args):
+    """Workload 2 alone (see conv1d_rows).  Prints one JSON line."""
+    import torch
+    print(json.dumps({"metric": "SAMD conv1d: time per call, HBM fraction and store-only floor", "n_gpus": 1,
+                      "device": device_info(torch), "data": "synthetic", "dtype": "int64",
+                      "config": {"conv1d": "2^20 unsigned b-bit values, 3 and 5 unsigned taps, valid mode",
+                                 "timing": "whole call (one kernel), median of graph-replay samples",
+                                 "floors": "grid-stride store (and copy) kernels over the output's bytes, 16 B per "
+                                           "lane"},
+                      "conv1d": conv1d_rows(args)}), flush=True)
 
 
 def run_spacers(args):
@@ -957,6 +1012,9 @@ def main():
         return
     if args.configs:
         run_configs(args)
+        return
+    if args.conv1d:
+        run_conv1d(args)
         return
     if args.lanewise:
         run_lanewise(args)

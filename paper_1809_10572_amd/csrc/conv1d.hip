@@ -4,8 +4,9 @@
 // (I values with L - b temporary spacer bits above each).  Kernel word B_g holds the
 // group's taps in natural order, one per lane.  One 32x32 -> 64-bit multiply per group
 // gives lanes j = 0 .. I+K-2, lane j holding the partial full-convolution sum for output
-// q*I + j - (K - 1) (the "parallelogram" of Sec. 5.1).  An output's complete value is its
-// lane in word q plus the low lanes of the following words (overlap-add).
+// q*I + j - (K - 1) (the "parallelogram" of Sec. 5.1); the groups' lanes line up, so
+// their products add into one 64-bit word P_q.  An output's complete value is its lane in
+// P_q plus the low lanes of the following words' products (overlap-add).
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -19,90 +20,158 @@ namespace {
 
 constexpr int kBlock = 256;
 
-// The computation is staged through LDS, with the overlap-add done there.  A block of W = 256 threads owns output words q0 .. q0 + W - 1,
-// i.e. outputs
-// q0 I .. q0 I + W I - 1; word q's lanes reach outputs q I - (K - 1) .. q I + I - 1, so
-// those outputs take lanes of words q0 .. q0 + W - 1 + extra.  The block
-//   1. unpacks every value those words read into LDS (one value per thread and pass,
-//      coalesced reads of the packed row, 32-bit indices, P a compile-time constant);
-//   2. builds each word's operand words from LDS, multiplies them by the kernel words
-//      (one 32x32 -> 64-bit product per tap group), and adds every lane into its output
-//      in an LDS row (atomic adds: lanes of up to 1 + extra words meet in one output);
-//   3. stores its W I outputs, coalesced.
-// The extra words past the block's own are computed by its first threads (and again,
-// as their own, by the next block).  LDS indices are skewed by one word per 16 (sk), so
-// that the lanes of neighbouring words, I apart, fall in different banks.
-__device__ __forceinline__ int sk(int i) { return i + (i >> 4); }
+// Lane j of the 64-bit product (lo, hi), j L < 64; the highest non-zero lane (nl - 1)
+// takes all the remaining bits, every other lane L of them.  Arguments other than the
+// product are uniform: the selection compiles to scalar code.
+__device__ __forceinline__ uint32_t lane_of(uint32_t lo, uint32_t hi, int j, int L, int nl, uint32_t lmask) {
+    const int sh = j * L;
+    const uint32_t v = sh < 32 ? __builtin_amdgcn_alignbit(hi, lo, sh) : hi >> (sh - 32);
+    return j < nl - 1 ? v & lmask : v;
+}
 
-template <int B>
-__global__ __launch_bounds__(kBlock) void conv1d_lds_kernel(const uint32_t *__restrict__ x, int32_t *__restrict__ y,
-                                                            Conv1dGeom g, int dmin, int nvals, int nouts) {
-    extern __shared__ uint32_t sh[];
-    uint32_t *vals = sh;                              // nvals values
-    uint32_t *outs = sh + sk(nvals);                  // nouts outputs; outs[sk(K - 1)] is output q0 I
-    constexpr int P = 32 / B;
-    const int I = g.I, L = g.L, K = g.K, nl = g.nl;
-    const int W = blockDim.x;
-    const int64_t q0 = (int64_t)blockIdx.x * W;
-    const int64_t u0 = q0 * I + dmin;   // 64-bit: rows may hold more than 2^31 values
-    for (int t = threadIdx.x; t < nvals; t += W) {
-        const int64_t u = u0 + t;
-        uint32_t f = 0;
-        if (u >= 0 && u < g.n) f = (x[(uint64_t)u / P] >> (((uint64_t)u % P) * B)) & ((1u << B) - 1);
-        vals[sk(t)] = f;
-    }
-    for (int t = threadIdx.x; t < sk(nouts); t += W) outs[t] = 0;
-    __syncthreads();
-    const uint64_t lmask = (1ull << L) - 1;   // L <= 32
-    for (int w = threadIdx.x; w < W + g.extra; w += W) {
-        if (q0 + w >= g.nwords + g.extra) break;   // words past the row only reach discarded outputs
-        uint64_t p = 0;
-        for (int gi = 0; gi < g.ngroups; ++gi) {
-            const int v0 = w * I + g.g_delta[gi] - dmin;
-            uint32_t A = 0;
-            for (int i = 0; i < I; ++i) A |= vals[sk(v0 + i)] << (i * L);
-            p += (uint64_t)A * g.g_word[gi];
+// One thread per output word and row (I <= 4 values per word, IM >= I a compile-time
+// bound the per-output registers are unrolled over).  Each (row, wave) stores the
+// outputs of own = 64 - extra consecutive words; the last `extra` lanes of each compute
+// the products of the following words only, which the storing lanes read with
+// cross-lane shuffles for the overlap-add.  A lane works on kRows rows, which share
+// every scalar decision (which lane of which product an output takes).
+//   1. The workgroup copies the packed words its lanes read into LDS, with words outside
+//      the row and fields past its end cleared (coalesced loads, the only wait on
+//      memory).
+//   2. Each lane builds its words' operand words per group from the (at most two)
+//      packed words its I values occupy, multiplies and sums the groups' products.
+//   3. Overlap-add through shuffles; a lane's I outputs are stored next to those of its
+//      neighbours.
+// Per-lane index arithmetic is 32-bit; 64-bit positions are per workgroup (scalar).
+constexpr int kRows = 2;
+
+template <int B, int IM>
+__global__ __launch_bounds__(kBlock) void conv1d_kernel(const uint32_t *__restrict__ x, int32_t *__restrict__ y,
+                                                        const Conv1dGeom g, int dmin, int nwin) {
+    constexpr int P = 32 / B;   // fields per packed word
+    constexpr uint32_t vmask = (1u << B) - 1;
+    constexpr uint32_t wmask = P * B == 32 ? 0xffffffffu : (1u << (P * B)) - 1;   // the P fields
+    constexpr int kWaves = kBlock / 64, R = kRows;
+    extern __shared__ uint32_t pk[];   // nwin + 1 packed words
+    const int I = g.I, L = g.L, K = g.K, nl = g.nl, extra = g.extra;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, own = 64 - extra;
+    const int64_t qb = (int64_t)blockIdx.x * (R * kWaves) * own;   // the workgroup's first word
+    // field 0 of pk[0] holds value ub - fb (fb < P): the workgroup's first value ub
+    const int64_t ub = qb * I + dmin;
+    const int64_t kb = ub >= 0 ? ub / P : -((P - 1 - ub) / P);
+    const int fb = (int)(ub - kb * P);
+    {
+        const int64_t wlast = (g.n - 1) / P;   // packed word of the row's last value
+        const int keep = (int)((g.n - 1) - wlast * P + 1);
+        for (int k = tid; k <= nwin; k += kBlock) {
+            const int64_t wi = kb + k;
+            uint32_t v = 0;
+            if (wi >= 0 && wi <= wlast) {
+                v = x[wi] & wmask;
+                if (wi == wlast && keep < P) v &= (1u << (keep * B)) - 1;
+            }
+            pk[k] = v;
         }
-        // lane j of word w is output w I + j - (K - 1), at outs[sk(w I + j)]
-        const int o = w * I;
-        for (int j = 0; j < nl - 1; ++j) {
-            atomicAdd(outs + sk(o + j), (uint32_t)(p & lmask));
-            p >>= L;
-        }
-        atomicAdd(outs + sk(o + nl - 1), (uint32_t)p);
     }
     __syncthreads();
-    const int64_t o0 = q0 * I;
-    for (int t = threadIdx.x; t < W * I; t += W) {
-        const int64_t o = o0 + t;
-        if (o < g.nout) y[o] = (int32_t)outs[sk(t + K - 1)];
+    const uint32_t fmask = I * B >= 32 ? 0xffffffffu : (1u << (I * B)) - 1;   // I fields
+    int r0[R];   // field of value q I relative to pk[0]'s field 0, per row
+#pragma unroll
+    for (int r = 0; r < R; ++r) r0[r] = fb + ((r * kWaves + wave) * own + lane) * I - dmin;
+    uint64_t prod[R] = {};
+    for (int gi = 0; gi < g.ngroups; ++gi) {
+        const uint32_t word = g.g_word[gi];
+        const int delta = g.g_delta[gi];
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            const int f = r0[r] + delta;
+            const int k = f / P, fk = f - k * P;
+            const uint32_t w0 = pk[k], w1 = pk[k + 1];
+            // the two words' fields back to back (w0 has no bits above its P fields)
+            uint32_t clo = w0, chi = w1;
+            if constexpr (P * B < 32) {
+                clo = w0 | (w1 << (P * B));
+                chi = w1 >> (32 - P * B);
+            }
+            const uint32_t bits = __builtin_amdgcn_alignbit(chi, clo, fk * B) & fmask;
+            // spread: field i to bit i L (fields past the I-th are zero, whatever their shift)
+            uint32_t A = bits & vmask;
+#pragma unroll
+            for (int i = 1; i < IM; ++i) A |= ((bits >> (i * B)) & vmask) << ((i * L) & 31);
+            prod[r] += (uint64_t)A * word;
+        }
+    }
+    const uint32_t lmask = L >= 32 ? 0xffffffffu : (1u << L) - 1;
+    uint32_t lo[R], hi[R], out[R][IM];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        lo[r] = (uint32_t)prod[r];
+        hi[r] = (uint32_t)(prod[r] >> 32);
+    }
+#pragma unroll
+    for (int t = 0; t < IM; ++t) {
+        const int j = t + K - 1;
+        const bool take = t < I && j < nl;
+#pragma unroll
+        for (int r = 0; r < R; ++r) out[r][t] = take ? lane_of(lo[r], hi[r], j, L, nl, lmask) : 0u;
+    }
+    for (int e = 1; e <= extra; ++e) {
+        uint32_t elo[R], ehi[R];
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            elo[r] = __shfl_down(lo[r], e, 64);
+            ehi[r] = __shfl_down(hi[r], e, 64);
+        }
+#pragma unroll
+        for (int t = 0; t < IM; ++t) {
+            const int j = t + K - 1 - e * I;
+            if (t < I && j >= 0 && j < nl) {
+#pragma unroll
+                for (int r = 0; r < R; ++r) out[r][t] += lane_of(elo[r], ehi[r], j, L, nl, lmask);
+            }
+        }
+    }
+    if (lane < own) {
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            const int64_t o = (qb + (r * kWaves + wave) * own + lane) * I;
+#pragma unroll
+            for (int t = 0; t < IM; ++t)
+                if (t < I && o + t < g.nout) y[o + t] = (int32_t)out[r][t];
+        }
     }
 }
 
 }  // namespace
 
 int launch_conv1d(const uint32_t *x, const Conv1dGeom &g, int32_t *y, hipStream_t s) {
-    const int64_t grid = (g.nwords + kBlock - 1) / kBlock;
-    if (grid > INT32_MAX) {
+    const int own = 64 - g.extra;
+    const int64_t per_block = (int64_t)kRows * (kBlock / 64) * own;
+    const int64_t grid = (g.nwords + per_block - 1) / per_block;
+    if (g.extra >= 64 || g.I > kConv1dMaxLanes || grid > INT32_MAX) {
         set_error("conv1d: row too long");
         return SAMD_EUNSUPPORTED;
     }
-    // the values a block reads: words q0 .. q0 + kBlock - 1 + extra, each from offset
-    // delta_g of its window, I values per operand word
     int dmin = 0, dmax = 0;
     for (int gi = 0; gi < g.ngroups; ++gi) {
         dmin = std::min(dmin, g.g_delta[gi]);
         dmax = std::max(dmax, g.g_delta[gi]);
     }
-    const int nvals = (kBlock + g.extra) * g.I + dmax - dmin;
-    // lanes of words 0 .. kBlock + extra - 1 land at outs[w I + j], j < nl
-    const int nouts = std::max((kBlock + g.extra - 1) * g.I + g.nl, kBlock * g.I + g.K - 1);
-    const size_t shm = ((size_t)(nvals + (nvals >> 4) + 1) + (size_t)(nouts + (nouts >> 4) + 1)) * 4;
-#define SAMD_C1_CASE(B)                                                                                   \
-    if (g.bits == B) {                                                                                    \
-        hipLaunchKernelGGL((conv1d_lds_kernel<B>), dim3((unsigned)grid), dim3(kBlock), shm, s, x, y, g, dmin, \
-                           nvals, nouts);                                                                 \
-        return check_launch("conv1d");                                                                    \
+    // fields the workgroup reads from pk[0]'s field 0: below fb + kRows 256 I + dmax - dmin
+    const int P = 32 / g.bits;
+    const int fields = (P - 1) + kRows * kBlock * g.I + dmax - dmin;
+    const int nwin = (fields + P - 1) / P;
+    const size_t shm = (size_t)(nwin + 1) * 4;
+    const int im = g.I <= 1 ? 1 : g.I <= 2 ? 2 : 4;
+#define SAMD_C1_CASE(B)                                                                                        \
+    if (g.bits == B) {                                                                                         \
+        if (im == 1)                                                                                           \
+            hipLaunchKernelGGL((conv1d_kernel<B, 1>), dim3((unsigned)grid), dim3(kBlock), shm, s, x, y, g, dmin, nwin); \
+        else if (im == 2)                                                                                      \
+            hipLaunchKernelGGL((conv1d_kernel<B, 2>), dim3((unsigned)grid), dim3(kBlock), shm, s, x, y, g, dmin, nwin); \
+        else                                                                                                   \
+            hipLaunchKernelGGL((conv1d_kernel<B, 4>), dim3((unsigned)grid), dim3(kBlock), shm, s, x, y, g, dmin, nwin); \
+        return check_launch("conv1d");                                                                         \
     }
     SAMD_C1_CASE(1) SAMD_C1_CASE(2) SAMD_C1_CASE(3) SAMD_C1_CASE(4)
     SAMD_C1_CASE(5) SAMD_C1_CASE(6) SAMD_C1_CASE(7) SAMD_C1_CASE(8)

@@ -517,7 +517,7 @@ int plan_conv1d(int64_t n, samd_fmt xf, const int32_t *taps, int32_t K, samd_fmt
         int imax = 0;
         for (int i = 1; i <= 32; ++i)
             if (word_fits(xf.bits, false, L, i, 0, u32max)) imax = i;
-        for (int I = 1; I <= imax; ++I) {
+        for (int I = 1; I <= std::min(imax, kConv1dMaxLanes); ++I) {
             Conv1dGeom c = g;
             c.L = L;
             c.I = I;

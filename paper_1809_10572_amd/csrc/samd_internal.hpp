@@ -18,6 +18,9 @@ constexpr int kMaxLanes = 16;      // I: values per operand word
 constexpr int kMaxOutLanes = 20;   // I + Kmax - 1: lanes of an accumulator that are decoded
 constexpr int kWaveM = 8;          // output channels per wave (kernel words per step, in SGPRs)
 constexpr int kMaxConv1dExtra = 15; // following words whose low lanes reach a 1-D output word
+// Values per 1-D operand word: the conv1d kernel keeps a lane's outputs in registers and
+// stores them directly; more, shorter words per row also give the GPU more lanes to run.
+constexpr int kConv1dMaxLanes = 4;
 constexpr int kStepBatch = 3;      // kernel-word steps fetched per scalar-load batch
 constexpr int kStreamPad = 2 * kStepBatch;  // zero steps after each kernel-word stream
 constexpr int kMaxBlockWaves = 16; // waves per conv2d workgroup
