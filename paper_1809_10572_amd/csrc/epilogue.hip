@@ -20,12 +20,25 @@ __global__ void max_init_kernel(int32_t *dev_max) {
     if (threadIdx.x == 0 && blockIdx.x == 0) *dev_max = INT_MIN;
 }
 
+// The maximum of n values: each workgroup reduces its grid-stride share (shuffles, then
+// LDS across its waves) and only then touches *dev_max, with one atomic, and only when
+// its maximum exceeds what *dev_max already holds.  Atomics on one address serialise
+// (about 12 ns each), so one per wave of a large grid would cost far more than the
+// reading; the check makes most workgroups skip theirs once a large value is in.
 __global__ __launch_bounds__(kBlock) void max_kernel(const int32_t *__restrict__ src, int64_t n, int32_t *dev_max) {
+    __shared__ int32_t part[kBlock / 64];
     int32_t m = INT_MIN;
+#pragma unroll 4
     for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < n; i += (int64_t)gridDim.x * kBlock)
         m = max(m, src[i]);
     for (int off = 32; off > 0; off >>= 1) m = max(m, __shfl_xor(m, off, 64));
-    if ((threadIdx.x & 63) == 0) atomicMax(dev_max, m);
+    if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = m;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+#pragma unroll
+        for (int w = 1; w < kBlock / 64; ++w) m = max(m, part[w]);
+        if (m > __hip_atomic_load(dev_max, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) atomicMax(dev_max, m);
+    }
 }
 
 __global__ void zero_count_kernel(int32_t *count) {
@@ -120,20 +133,55 @@ __global__ __launch_bounds__(kBlock) void relu_requant_stage_kernel(const int32_
     }
 }
 
-// One thread per NHWC output byte; reads the NCHW accumulator.
+// NCHW accumulators to NHWC bytes through an LDS tile: a workgroup takes kNhwcCols
+// columns of one image row and up to kNhwcChans channels at a time; it reads each
+// channel's columns as one contiguous run (coalesced), requantises them into the tile,
+// then writes the tile's pixels, whose channel bytes are contiguous in NHWC, with
+// consecutive threads on consecutive bytes (whole 32-bit words when the run is aligned).
+constexpr int kNhwcCols = 64;
+constexpr int kNhwcChans = 256;
 __global__ __launch_bounds__(kBlock) void relu_requant_nhwc_kernel(const int32_t *__restrict__ acc, int N, int C,
                                                                    int H, int W, const int32_t *__restrict__ dev_max,
                                                                    int bits, uint8_t *__restrict__ dst) {
+    __shared__ uint8_t tile[kNhwcChans * (kNhwcCols + 4)];   // [channel][column], 4 bytes of row padding
+    constexpr int kPitch = kNhwcCols + 4;
     const int shift = requant_shift(*dev_max, bits);
-    const int64_t total = (int64_t)N * C * H * W;
-    for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < total; i += (int64_t)gridDim.x * kBlock) {
-        const int c = (int)(i % C);
-        const int64_t p = i / C;   // (n, h, w)
-        const int w = (int)(p % W);
-        const int64_t t = p / W;
-        const int h = (int)(t % H);
-        const int n = (int)(t / H);
-        dst[i] = (uint8_t)requant(acc[(((int64_t)n * C + c) * H + h) * W + w], shift, bits);
+    const int tiles_w = (W + kNhwcCols - 1) / kNhwcCols;
+    const int tw = blockIdx.x % tiles_w;
+    const int nh = blockIdx.x / tiles_w;   // n H + h
+    const int n = nh / H, h = nh - n * H;
+    const int w0 = tw * kNhwcCols;
+    const int cols = min(kNhwcCols, W - w0);
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    // NHWC offset of pixel (n, h, w0): the tile's pixels are cols consecutive pixels
+    const int64_t pix0 = ((int64_t)nh * W + w0) * C;
+    for (int c0 = 0; c0 < C; c0 += kNhwcChans) {
+        const int cc = min(kNhwcChans, C - c0);
+        for (int c = wave; c < cc; c += kBlock / 64) {
+            if (lane < cols) {
+                const int32_t v = acc[(((int64_t)n * C + c0 + c) * H + h) * W + w0 + lane];
+                tile[c * kPitch + lane] = (uint8_t)requant(v, shift, bits);
+            }
+        }
+        __syncthreads();
+        // pixel j's channels c0 .. c0 + cc - 1 sit at dst[pix0 + j C + c0 ...]
+        const bool words = (cc & 3) == 0 && (C & 3) == 0 && (c0 & 3) == 0 && (((uintptr_t)dst + pix0) & 3) == 0;
+        if (words) {
+            const int per = cc >> 2;   // 32-bit words per pixel
+            for (int k = threadIdx.x; k < cols * per; k += kBlock) {
+                const int j = k / per, c = (k - j * per) << 2;
+                const uint32_t v = (uint32_t)tile[c * kPitch + j] | ((uint32_t)tile[(c + 1) * kPitch + j] << 8) |
+                                   ((uint32_t)tile[(c + 2) * kPitch + j] << 16) |
+                                   ((uint32_t)tile[(c + 3) * kPitch + j] << 24);
+                *(uint32_t *)(dst + pix0 + (int64_t)j * C + c0 + c) = v;
+            }
+        } else {
+            for (int k = threadIdx.x; k < cols * cc; k += kBlock) {
+                const int j = k / cc, c = k - j * cc;
+                dst[pix0 + (int64_t)j * C + c0 + c] = tile[c * kPitch + j];
+            }
+        }
+        __syncthreads();
     }
 }
 
@@ -193,8 +241,13 @@ int launch_relu_requant_stage(const int32_t *acc, const int32_t *dev_max, const 
 
 int launch_relu_requant_nhwc_u8(const int32_t *acc, int N, int C, int H, int W, const int32_t *dev_max, int bits,
                                 uint8_t *dst, hipStream_t s) {
-    const int grid = grid_for((int64_t)N * C * H * W, kBlock);
-    hipLaunchKernelGGL(relu_requant_nhwc_kernel, dim3(grid), dim3(kBlock), 0, s, acc, N, C, H, W, dev_max, bits, dst);
+    const int64_t grid = (int64_t)N * H * ((W + kNhwcCols - 1) / kNhwcCols);
+    if (grid > INT32_MAX) {
+        set_error("relu_requant_nhwc_u8: too many image rows");
+        return SAMD_EUNSUPPORTED;
+    }
+    hipLaunchKernelGGL(relu_requant_nhwc_kernel, dim3((unsigned)grid), dim3(kBlock), 0, s, acc, N, C, H, W, dev_max,
+                       bits, dst);
     return check_launch("relu_requant_nhwc_u8");
 }
 

@@ -346,6 +346,35 @@ def test_max_and_relu_requant(bits):
         np.testing.assert_array_equal(nhwc.cpu().numpy(), np.transpose(q, (0, 2, 3, 1)))
 
 
+@pytest.mark.parametrize("shape", [(2, 3, 3, 1), (1, 96, 2, 64), (2, 301, 2, 65), (1, 260, 1, 130),
+                                   (1, 8, 4, 200)], ids=lambda s: "x".join(map(str, s)))
+def test_relu_requant_nhwc_tiles(shape):
+    """The NHWC requantisation's tiling: rows wider than one column tile, channel counts
+    above one channel chunk and not a multiple of 4 (the byte path), one column."""
+    rng = np.random.default_rng(sum(shape))
+    acc = rng.integers(-5000, 60000, shape).astype(np.int32)
+    a = torch.from_numpy(acc).to(DEV)
+    for bits in (2, 8):
+        nhwc = samd.relu_requant_nhwc_u8(a, samd.max_i32(a), bits)
+        torch.cuda.synchronize()
+        s = ref.requant_shift(acc.astype(np.int64), bits)
+        q = ref.relu_requant(acc.astype(np.int64), s, bits)
+        np.testing.assert_array_equal(nhwc.cpu().numpy(), np.transpose(q, (0, 2, 3, 1)))
+
+
+@pytest.mark.parametrize("n", [1, 255, 1 << 20, 5_000_003])
+def test_max_i32_many_workgroups(n):
+    rng = np.random.default_rng(n)
+    for where in (0, n // 2, n - 1):
+        v = rng.integers(-(1 << 31), (1 << 30), n).astype(np.int32)
+        v[where] = (1 << 31) - 1 - where % 7
+        got = samd.max_i32(torch.from_numpy(v).to(DEV))
+        torch.cuda.synchronize()
+        assert int(got.item()) == int(v.max())
+    neg = np.full(n, -(1 << 31), dtype=np.int32)
+    assert int(samd.max_i32(torch.from_numpy(neg).to(DEV)).item()) == -(1 << 31)
+
+
 def run_stack_samd(case):
     bits = case.bits
     x = samd.pack(gpu_vals(case.x, False), bits, False)
