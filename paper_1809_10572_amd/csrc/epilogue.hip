@@ -20,17 +20,30 @@ __global__ void max_init_kernel(int32_t *dev_max) {
     if (threadIdx.x == 0 && blockIdx.x == 0) *dev_max = INT_MIN;
 }
 
-// The maximum of n values: each workgroup reduces its grid-stride share (shuffles, then
-// LDS across its waves) and only then touches *dev_max, with one atomic, and only when
-// its maximum exceeds what *dev_max already holds.  Atomics on one address serialise
-// (about 12 ns each), so one per wave of a large grid would cost far more than the
-// reading; the check makes most workgroups skip theirs once a large value is in.
+// The maximum of n values: each workgroup reduces its grid-stride share (16-byte loads
+// when src is 16-byte aligned, four in flight per thread; shuffles, then LDS across its
+// waves) and only then touches *dev_max, with one atomic, and only when its maximum
+// exceeds what *dev_max already holds.  Atomics on one address serialise (about 12 ns
+// each), and the workgroups of one launch finish at nearly the same time, so the grid is
+// kept to a few hundred workgroups that each read many values.
+constexpr int kMaxGrid = 512;
 __global__ __launch_bounds__(kBlock) void max_kernel(const int32_t *__restrict__ src, int64_t n, int32_t *dev_max) {
     __shared__ int32_t part[kBlock / 64];
     int32_t m = INT_MIN;
+    const int64_t stride = (int64_t)gridDim.x * kBlock;
+    const int64_t tid = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    int64_t head = 0;   // values before the first 16-byte vector
+    if (((uintptr_t)src & 15) == 0) {
+        const int4 *v = (const int4 *)src;
+        const int64_t n4 = n >> 2;
 #pragma unroll 4
-    for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < n; i += (int64_t)gridDim.x * kBlock)
-        m = max(m, src[i]);
+        for (int64_t i = tid; i < n4; i += stride) {
+            const int4 q = v[i];
+            m = max(m, max(max(q.x, q.y), max(q.z, q.w)));
+        }
+        head = n4 << 2;
+    }
+    for (int64_t i = head + tid; i < n; i += stride) m = max(m, src[i]);
     for (int off = 32; off > 0; off >>= 1) m = max(m, __shfl_xor(m, off, 64));
     if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = m;
     __syncthreads();
@@ -71,12 +84,48 @@ __device__ inline uint32_t requant(int32_t v, int shift, int bits) {
     return (uint32_t)(q < top ? q : top);
 }
 
+// Rows of at most kPackVals values: a workgroup takes whole consecutive rows (their
+// values are one contiguous run of acc), reads them coalesced into LDS as requantised
+// bytes, then builds and stores one packed word per thread.  Longer rows: one thread
+// per packed word, reading its values directly.
+constexpr int kPackVals = 4096;
+
 template <int B>
 __global__ __launch_bounds__(kBlock) void relu_requant_pack_kernel(const int32_t *__restrict__ acc, int64_t rows,
-                                                                   int64_t len, int64_t words_per_row,
+                                                                   int32_t len, int32_t words_per_row, int32_t rpb,
                                                                    const int32_t *__restrict__ dev_max,
                                                                    uint32_t *__restrict__ dst,
                                                                    int32_t *__restrict__ dev_shift) {
+    constexpr int P = 32 / B;
+    __shared__ uint8_t q8[kPackVals];
+    const int shift = requant_shift(*dev_max, B);
+    if (dev_shift && blockIdx.x == 0 && threadIdx.x == 0) *dev_shift = shift;
+    const int64_t r0 = (int64_t)blockIdx.x * rpb;
+    const int R = (int)min((int64_t)rpb, rows - r0);
+    const int nv = R * len;   // <= kPackVals
+    const int32_t *a = acc + r0 * len;
+#pragma unroll 4
+    for (int i = threadIdx.x; i < nv; i += kBlock) q8[i] = (uint8_t)requant(a[i], shift, B);
+    __syncthreads();
+    const int nw = R * words_per_row;
+    for (int k = threadIdx.x; k < nw; k += kBlock) {
+        const int r = k / words_per_row, qw = k - r * words_per_row;
+        const int j0 = qw * P, cnt = min(P, len - j0);
+        const uint8_t *src = q8 + r * len + j0;
+        uint32_t word = 0;
+#pragma unroll
+        for (int i = 0; i < P; ++i)
+            if (i < cnt) word |= (uint32_t)src[i] << (i * B);
+        dst[(r0 + r) * words_per_row + qw] = word;
+    }
+}
+
+template <int B>
+__global__ __launch_bounds__(kBlock) void relu_requant_pack_long_kernel(const int32_t *__restrict__ acc, int64_t rows,
+                                                                        int64_t len, int64_t words_per_row,
+                                                                        const int32_t *__restrict__ dev_max,
+                                                                        uint32_t *__restrict__ dst,
+                                                                        int32_t *__restrict__ dev_shift) {
     constexpr int P = 32 / B;
     const int shift = requant_shift(*dev_max, B);
     if (dev_shift && blockIdx.x == 0 && threadIdx.x == 0) *dev_shift = shift;
@@ -134,54 +183,53 @@ __global__ __launch_bounds__(kBlock) void relu_requant_stage_kernel(const int32_
 }
 
 // NCHW accumulators to NHWC bytes through an LDS tile: a workgroup takes kNhwcCols
-// columns of one image row and up to kNhwcChans channels at a time; it reads each
-// channel's columns as one contiguous run (coalesced), requantises them into the tile,
-// then writes the tile's pixels, whose channel bytes are contiguous in NHWC, with
-// consecutive threads on consecutive bytes (whole 32-bit words when the run is aligned).
+// columns of one image row and kNhwcChans channels (grid: image rows x column tiles x
+// channel chunks); it reads each channel's columns as one contiguous run (coalesced,
+// several channels' loads in flight per wave), requantises them into the tile, then
+// writes the tile's pixels, whose chunk of channel bytes is contiguous in NHWC, with
+// consecutive threads on consecutive bytes (whole 32-bit words when aligned).
 constexpr int kNhwcCols = 64;
-constexpr int kNhwcChans = 256;
+constexpr int kNhwcChans = 64;
 __global__ __launch_bounds__(kBlock) void relu_requant_nhwc_kernel(const int32_t *__restrict__ acc, int N, int C,
                                                                    int H, int W, const int32_t *__restrict__ dev_max,
                                                                    int bits, uint8_t *__restrict__ dst) {
-    __shared__ uint8_t tile[kNhwcChans * (kNhwcCols + 4)];   // [channel][column], 4 bytes of row padding
-    constexpr int kPitch = kNhwcCols + 4;
+    constexpr int kPitch = kNhwcCols + 4;   // bytes per tile row (channel), padded
+    __shared__ uint8_t tile[kNhwcChans * kPitch];
     const int shift = requant_shift(*dev_max, bits);
     const int tiles_w = (W + kNhwcCols - 1) / kNhwcCols;
-    const int tw = blockIdx.x % tiles_w;
-    const int nh = blockIdx.x / tiles_w;   // n H + h
+    const int chunks = (C + kNhwcChans - 1) / kNhwcChans;
+    int b = blockIdx.x;
+    const int ch = b % chunks;
+    b /= chunks;
+    const int tw = b % tiles_w;
+    const int nh = b / tiles_w;   // n H + h
     const int n = nh / H, h = nh - n * H;
-    const int w0 = tw * kNhwcCols;
-    const int cols = min(kNhwcCols, W - w0);
+    const int w0 = tw * kNhwcCols, c0 = ch * kNhwcChans;
+    const int cols = min(kNhwcCols, W - w0), cc = min(kNhwcChans, C - c0);
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    // NHWC offset of pixel (n, h, w0): the tile's pixels are cols consecutive pixels
-    const int64_t pix0 = ((int64_t)nh * W + w0) * C;
-    for (int c0 = 0; c0 < C; c0 += kNhwcChans) {
-        const int cc = min(kNhwcChans, C - c0);
-        for (int c = wave; c < cc; c += kBlock / 64) {
-            if (lane < cols) {
-                const int32_t v = acc[(((int64_t)n * C + c0 + c) * H + h) * W + w0 + lane];
-                tile[c * kPitch + lane] = (uint8_t)requant(v, shift, bits);
-            }
+    const int32_t *a = acc + (((int64_t)n * C + c0) * H + h) * W + w0 + lane;
+    const int64_t cstride = (int64_t)H * W;
+#pragma unroll 4
+    for (int c = wave; c < cc; c += kBlock / 64)
+        if (lane < cols) tile[c * kPitch + lane] = (uint8_t)requant(a[c * cstride], shift, bits);
+    __syncthreads();
+    // pixel j's channels c0 .. c0 + cc - 1 sit at dst[pix0 + j C + c0 ...]
+    const int64_t pix0 = ((int64_t)nh * W + w0) * C + c0;
+    const bool words = (cc & 3) == 0 && (C & 3) == 0 && (((uintptr_t)dst + pix0) & 3) == 0;
+    if (words) {
+        const int per = cc >> 2;   // 32-bit words per pixel
+        for (int k = threadIdx.x; k < cols * per; k += kBlock) {
+            const int j = k / per, c = (k - j * per) << 2;
+            const uint32_t v = (uint32_t)tile[c * kPitch + j] | ((uint32_t)tile[(c + 1) * kPitch + j] << 8) |
+                               ((uint32_t)tile[(c + 2) * kPitch + j] << 16) |
+                               ((uint32_t)tile[(c + 3) * kPitch + j] << 24);
+            *(uint32_t *)(dst + pix0 + (int64_t)j * C + c) = v;
         }
-        __syncthreads();
-        // pixel j's channels c0 .. c0 + cc - 1 sit at dst[pix0 + j C + c0 ...]
-        const bool words = (cc & 3) == 0 && (C & 3) == 0 && (c0 & 3) == 0 && (((uintptr_t)dst + pix0) & 3) == 0;
-        if (words) {
-            const int per = cc >> 2;   // 32-bit words per pixel
-            for (int k = threadIdx.x; k < cols * per; k += kBlock) {
-                const int j = k / per, c = (k - j * per) << 2;
-                const uint32_t v = (uint32_t)tile[c * kPitch + j] | ((uint32_t)tile[(c + 1) * kPitch + j] << 8) |
-                                   ((uint32_t)tile[(c + 2) * kPitch + j] << 16) |
-                                   ((uint32_t)tile[(c + 3) * kPitch + j] << 24);
-                *(uint32_t *)(dst + pix0 + (int64_t)j * C + c0 + c) = v;
-            }
-        } else {
-            for (int k = threadIdx.x; k < cols * cc; k += kBlock) {
-                const int j = k / cc, c = k - j * cc;
-                dst[pix0 + (int64_t)j * C + c0 + c] = tile[c * kPitch + j];
-            }
+    } else {
+        for (int k = threadIdx.x; k < cols * cc; k += kBlock) {
+            const int j = k / cc, c = k - j * cc;
+            dst[pix0 + (int64_t)j * C + c] = tile[c * kPitch + j];
         }
-        __syncthreads();
     }
 }
 
@@ -191,7 +239,7 @@ int launch_max_i32(const int32_t *src, int64_t n, int32_t *dev_max, hipStream_t 
     hipLaunchKernelGGL(max_init_kernel, dim3(1), dim3(64), 0, s, dev_max);
     int st = check_launch("max init");
     if (st) return st;
-    const int grid = std::min(grid_for(n, kBlock), 2048);
+    const int grid = std::min(grid_for((n + 15) / 16, kBlock), kMaxGrid);   // ~16 values per thread or more
     hipLaunchKernelGGL(max_kernel, dim3(grid), dim3(kBlock), 0, s, src, n, dev_max);
     return check_launch("max");
 }
@@ -208,16 +256,34 @@ int launch_count_mismatch(const int32_t *a, const int32_t *b, int64_t n, int32_t
 int launch_relu_requant_pack(const int32_t *acc, int64_t rows, int64_t len, const int32_t *dev_max, int bits,
                              uint32_t *dst, int32_t *dev_shift, hipStream_t s) {
     const int64_t wpr = row_words(len, bits);
-    const int grid = grid_for(rows * wpr, kBlock);
-#define SAMD_REQ_CASE(B)                                                                                         \
-    if (bits == B) {                                                                                             \
-        hipLaunchKernelGGL((relu_requant_pack_kernel<B>), dim3(grid), dim3(kBlock), 0, s, acc, rows, len, wpr, \
-                           dev_max, dst, dev_shift);                                                           \
-        return check_launch("relu_requant_pack");                                                              \
-    }
-    SAMD_REQ_CASE(1) SAMD_REQ_CASE(2) SAMD_REQ_CASE(3) SAMD_REQ_CASE(4)
-    SAMD_REQ_CASE(5) SAMD_REQ_CASE(6) SAMD_REQ_CASE(7) SAMD_REQ_CASE(8)
+    if (len <= kPackVals) {
+        const int rpb = (int)(kPackVals / len);
+        const int64_t grid = (rows + rpb - 1) / rpb;
+        if (grid > INT32_MAX) {
+            set_error("relu_requant_pack: too many rows");
+            return SAMD_EUNSUPPORTED;
+        }
+#define SAMD_REQ_CASE(B)                                                                                          \
+        if (bits == B) {                                                                                          \
+            hipLaunchKernelGGL((relu_requant_pack_kernel<B>), dim3((unsigned)grid), dim3(kBlock), 0, s, acc, rows, \
+                               (int32_t)len, (int32_t)wpr, rpb, dev_max, dst, dev_shift);                         \
+            return check_launch("relu_requant_pack");                                                             \
+        }
+        SAMD_REQ_CASE(1) SAMD_REQ_CASE(2) SAMD_REQ_CASE(3) SAMD_REQ_CASE(4)
+        SAMD_REQ_CASE(5) SAMD_REQ_CASE(6) SAMD_REQ_CASE(7) SAMD_REQ_CASE(8)
 #undef SAMD_REQ_CASE
+    } else {
+        const int grid = grid_for(rows * wpr, kBlock);
+#define SAMD_REQ_CASE(B)                                                                                          \
+        if (bits == B) {                                                                                          \
+            hipLaunchKernelGGL((relu_requant_pack_long_kernel<B>), dim3(grid), dim3(kBlock), 0, s, acc, rows, len, \
+                               wpr, dev_max, dst, dev_shift);                                                     \
+            return check_launch("relu_requant_pack");                                                             \
+        }
+        SAMD_REQ_CASE(1) SAMD_REQ_CASE(2) SAMD_REQ_CASE(3) SAMD_REQ_CASE(4)
+        SAMD_REQ_CASE(5) SAMD_REQ_CASE(6) SAMD_REQ_CASE(7) SAMD_REQ_CASE(8)
+#undef SAMD_REQ_CASE
+    }
     set_error("relu_requant_pack: unsupported bits");
     return SAMD_EINVAL;
 }
@@ -241,7 +307,7 @@ int launch_relu_requant_stage(const int32_t *acc, const int32_t *dev_max, const 
 
 int launch_relu_requant_nhwc_u8(const int32_t *acc, int N, int C, int H, int W, const int32_t *dev_max, int bits,
                                 uint8_t *dst, hipStream_t s) {
-    const int64_t grid = (int64_t)N * H * ((W + kNhwcCols - 1) / kNhwcCols);
+    const int64_t grid = (int64_t)N * H * ((W + kNhwcCols - 1) / kNhwcCols) * ((C + kNhwcChans - 1) / kNhwcChans);
     if (grid > INT32_MAX) {
         set_error("relu_requant_nhwc_u8: too many image rows");
         return SAMD_EUNSUPPORTED;

@@ -362,6 +362,25 @@ def test_relu_requant_nhwc_tiles(shape):
         np.testing.assert_array_equal(nhwc.cpu().numpy(), np.transpose(q, (0, 2, 3, 1)))
 
 
+@pytest.mark.parametrize("shape", [(40, 11, 55), (7, 3, 5000), (2, 1, 4096), (3, 700, 1), (1, 1, 4097)],
+                         ids=lambda s: "x".join(map(str, s)))
+def test_relu_requant_pack_row_tiles(shape):
+    """The packed requantisation's tiling: many workgroups of whole rows, rows of exactly
+    one tile, rows of one value, and rows longer than a tile (one thread per word)."""
+    rng = np.random.default_rng(sum(shape))
+    acc = rng.integers(-70000, 70000, shape).astype(np.int32)
+    a = torch.from_numpy(acc).to(DEV)
+    for bits in (1, 3, 8):
+        shift = torch.zeros(1, dtype=torch.int32, device=DEV)
+        packed = samd.relu_requant_pack(a, samd.max_i32(a), bits, shift_out=shift)
+        torch.cuda.synchronize()
+        s = ref.requant_shift(acc.astype(np.int64), bits)
+        assert int(shift.item()) == s
+        q = ref.relu_requant(acc.astype(np.int64), s, bits)
+        want, _ = ref.pack(q.reshape(-1, shape[-1]), bits, False)
+        np.testing.assert_array_equal(host_words(packed).reshape(-1, want.shape[-1]), want)
+
+
 @pytest.mark.parametrize("n", [1, 255, 1 << 20, 5_000_003])
 def test_max_i32_many_workgroups(n):
     rng = np.random.default_rng(n)
@@ -373,6 +392,12 @@ def test_max_i32_many_workgroups(n):
         assert int(got.item()) == int(v.max())
     neg = np.full(n, -(1 << 31), dtype=np.int32)
     assert int(samd.max_i32(torch.from_numpy(neg).to(DEV)).item()) == -(1 << 31)
+    # a source that starts 4 bytes past a 16-byte boundary (the scalar path)
+    v = rng.integers(-1000, 1000, n + 1).astype(np.int32)
+    v[-1] = 5000
+    t = torch.from_numpy(v).to(DEV)[1:]
+    assert t.data_ptr() % 16 == 4
+    assert int(samd.max_i32(t).item()) == 5000
 
 
 def run_stack_samd(case):
