@@ -483,6 +483,28 @@ def test_alexnet_stack_full_batch(bits):
         np.testing.assert_array_equal(g, w, err_msg=f"SAMD layer {li + 1}")
 
 
+@pytest.mark.parametrize("bits", [2, 8])
+def test_alexnet_stack_full_batch_fused_tuned(bits):
+    """The chain the stack benchmark times: batch 16, each layer's plan tuned on that
+    layer's own input, ReLU + requantisation written straight into the next layer's
+    operand words; every layer's accumulators and shifts against the oracle."""
+    case = wl.stack_case(bits)
+    shapes = [l.as_tuple() for l in case.layers]
+    want_accs, want_acts, want_shifts = ref.stack(case.x, case.ws, shapes, bits)
+    xf, wf = samd.Fmt(bits, False), samd.Fmt(bits, True)
+    try:
+        for li, (w, shp) in enumerate(zip(case.ws, case.layers)):
+            xp = samd.pack(gpu_vals(want_acts[li], False), bits, False)
+            samd.conv2d_tune(xp, xf, samd.pack(gpu_vals(w, True), bits, True), wf, shp, candidates=6, reps=2)
+        got_accs, got_shifts = run_stack_samd_fused(case)
+        assert got_shifts == list(want_shifts)
+        for li, (g, w) in enumerate(zip(got_accs, want_accs)):
+            np.testing.assert_array_equal(g, w, err_msg=f"SAMD layer {li + 1}")
+    finally:
+        for shp in case.layers:
+            samd.conv2d_untune(shp, xf, wf)
+
+
 @pytest.mark.parametrize("bits", [1, 4, 8])
 def test_prepared_weights_are_reusable(bits):
     shape = EDGE[2]
