@@ -195,8 +195,10 @@ __device__ __forceinline__ int32_t low_field(uint32_t w, int L) {
 }
 
 // Decode of one accumulator (Sec. 6): the fix-up of the signed-convolution figure for
-// signed results, then lanes from the bottom - take the low L bits, shift them out -
-// each added into its output column (p + j); lane NL-1 takes all remaining bits.
+// signed results, after which lane j is the (sign-extended) field at bit j L, each
+// added into its output column (p + j); lane NL-1 takes all remaining bits.  Every lane
+// is cut from the fixed-up word directly (no chain of shifts), so the lanes' extractions
+// are independent instructions.
 // PS (permanent spacer bits, Sec. 6.1): every lane's MSB is a spacer bit (the planner
 // keeps its values within L - 1 bits), so the fix-up's final xor, which only restores the
 // MSB, is left out and each lane is read from its low L - 1 bits.
@@ -208,11 +210,9 @@ __device__ __forceinline__ void decode_word(uint64_t v, uint64_t msb_mask, int L
         if (!PS) v ^= s;
     }
 #pragma unroll
-    for (int j = 0; j < NL - 1; ++j) {
-        atomicAdd(p + j, low_field<SG>((uint32_t)v, PS ? fw : L));
-        v = SG ? (uint64_t)((int64_t)v >> L) : v >> L;
-    }
-    atomicAdd(p + NL - 1, (int32_t)v);
+    for (int j = 0; j < NL - 1; ++j) atomicAdd(p + j, low_field<SG>((uint32_t)(v >> (j * L)), PS ? fw : L));
+    const int top = (NL - 1) * L;
+    atomicAdd(p + NL - 1, (int32_t)(SG ? (uint64_t)((int64_t)v >> top) : v >> top));
 }
 
 // The same for a lane count known only at run time.
@@ -224,11 +224,9 @@ __device__ __forceinline__ void decode_word_n(uint64_t v, uint64_t msb_mask, int
         if (!PS) v ^= s;
     }
 #pragma unroll 1
-    for (int j = 0; j < nl - 1; ++j) {
-        atomicAdd(p + j, low_field<SG>((uint32_t)v, PS ? fw : L));
-        v = SG ? (uint64_t)((int64_t)v >> L) : v >> L;
-    }
-    atomicAdd(p + nl - 1, (int32_t)v);
+    for (int j = 0; j < nl - 1; ++j) atomicAdd(p + j, low_field<SG>((uint32_t)(v >> (j * L)), PS ? fw : L));
+    const int top = (nl - 1) * L;
+    atomicAdd(p + nl - 1, (int32_t)(SG ? (uint64_t)((int64_t)v >> top) : v >> top));
 }
 
 // Work item: rows_blk output rows x all Wo columns x mblk output channels of one image,
