@@ -36,6 +36,25 @@ def run_conv2d(x, w, shape, xf, wf):
     return y.cpu().numpy()
 
 
+@pytest.mark.parametrize("bits,xs,ws", [(2, 0, 1), (4, 1, 1), (8, 0, 1), (3, 1, 0)])
+def test_fully_connected_as_1x1(bits, xs, ws):
+    """A fully connected layer (batch 37, 300 -> 70) through conv2d as a 1x1 layer whose
+    row is the batch (N = 1, C = inputs, H = 1, W = batch): the vector-scale form of the
+    method, one tap per kernel word and I batch elements per operand word, against the
+    plain matrix product."""
+    rng = np.random.default_rng(bits * 7 + xs)
+    batch, nin, nout = 37, 300, 70
+    a = wl.uniform(rng, (batch, nin), bits, bool(xs))
+    wt = wl.uniform(rng, (nout, nin), bits, bool(ws))
+    shape = wl.Conv2dShape(1, nin, 1, batch, nout, 1, 1, 1, 1, 0, 0)
+    x = np.ascontiguousarray(a.T).reshape(1, nin, 1, batch)
+    w = wt.reshape(nout, nin, 1, 1)
+    got = run_conv2d(x, w, shape, samd.Fmt(bits, xs), samd.Fmt(bits, ws)).reshape(nout, batch)
+    want = (wt.astype(np.int64) @ a.astype(np.int64).T)
+    np.testing.assert_array_equal(got, want)
+    np.testing.assert_array_equal(got.reshape(1, nout, 1, batch), ref.conv2d(x, w, shape.as_tuple()))
+
+
 def run_conv2d_int8(x, w, shape, xf, wf):
     xs = gpu_vals(np.transpose(x, (0, 2, 3, 1)), xf.is_signed)   # NHWC
     ws = gpu_vals(w, True)
