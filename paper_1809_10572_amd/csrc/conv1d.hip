@@ -47,7 +47,7 @@ constexpr int kRows = 2;
 
 template <int B, int IM>
 __global__ __launch_bounds__(kBlock) void conv1d_kernel(const uint32_t *__restrict__ x, int32_t *__restrict__ y,
-                                                        const Conv1dGeom g, int dmin, int nwin) {
+                                                        const Conv1dGeom g, int dmin, int nwin, bool aligned) {
     constexpr int P = 32 / B;   // fields per packed word
     constexpr uint32_t vmask = (1u << B) - 1;
     constexpr uint32_t wmask = P * B == 32 ? 0xffffffffu : (1u << (P * B)) - 1;   // the P fields
@@ -135,6 +135,21 @@ __global__ __launch_bounds__(kBlock) void conv1d_kernel(const uint32_t *__restri
 #pragma unroll
         for (int r = 0; r < R; ++r) {
             const int64_t o = (qb + (r * kWaves + wave) * own + lane) * I;
+            // I = 2, 3 or 4 with y 16-byte aligned: the lane's outputs in one 8-, 12- or 16-byte
+            // store (o is a multiple of I, so the store is aligned to its element count's
+            // power of two, or to 4 bytes for 3); otherwise, and at the row's end, one by one
+            if constexpr (IM == 2 || IM == 4) {
+                if (I >= IM - 1 && I > 1 && aligned && o + I <= g.nout) {
+                    if constexpr (IM == 2) {
+                        *(uint2 *)(y + o) = uint2{out[r][0], out[r][1]};
+                    } else if (I == 4) {
+                        *(uint4 *)(y + o) = uint4{out[r][0], out[r][1], out[r][2], out[r][3]};
+                    } else {
+                        *(uint3 *)(y + o) = uint3{out[r][0], out[r][1], out[r][2]};
+                    }
+                    continue;
+                }
+            }
 #pragma unroll
             for (int t = 0; t < IM; ++t)
                 if (t < I && o + t < g.nout) y[o + t] = (int32_t)out[r][t];
@@ -163,14 +178,15 @@ int launch_conv1d(const uint32_t *x, const Conv1dGeom &g, int32_t *y, hipStream_
     const int nwin = (fields + P - 1) / P;
     const size_t shm = (size_t)(nwin + 1) * 4;
     const int im = g.I <= 1 ? 1 : g.I <= 2 ? 2 : 4;
+    const bool aligned = ((uintptr_t)y & 15) == 0;
 #define SAMD_C1_CASE(B)                                                                                        \
     if (g.bits == B) {                                                                                         \
         if (im == 1)                                                                                           \
-            hipLaunchKernelGGL((conv1d_kernel<B, 1>), dim3((unsigned)grid), dim3(kBlock), shm, s, x, y, g, dmin, nwin); \
+            hipLaunchKernelGGL((conv1d_kernel<B, 1>), dim3((unsigned)grid), dim3(kBlock), shm, s, x, y, g, dmin, nwin, aligned); \
         else if (im == 2)                                                                                      \
-            hipLaunchKernelGGL((conv1d_kernel<B, 2>), dim3((unsigned)grid), dim3(kBlock), shm, s, x, y, g, dmin, nwin); \
+            hipLaunchKernelGGL((conv1d_kernel<B, 2>), dim3((unsigned)grid), dim3(kBlock), shm, s, x, y, g, dmin, nwin, aligned); \
         else                                                                                                   \
-            hipLaunchKernelGGL((conv1d_kernel<B, 4>), dim3((unsigned)grid), dim3(kBlock), shm, s, x, y, g, dmin, nwin); \
+            hipLaunchKernelGGL((conv1d_kernel<B, 4>), dim3((unsigned)grid), dim3(kBlock), shm, s, x, y, g, dmin, nwin, aligned); \
         return check_launch("conv1d");                                                                         \
     }
     SAMD_C1_CASE(1) SAMD_C1_CASE(2) SAMD_C1_CASE(3) SAMD_C1_CASE(4)

@@ -115,6 +115,17 @@ def test_conv1d_ragged_and_degenerate(bits):
         y = samd.conv1d(gpu_words(words), n, bits, k.tolist(), bits)
         torch.cuda.synchronize()
         np.testing.assert_array_equal(y.cpu().numpy(), ref.conv1d(x, k), err_msg=f"n={n} K={K}")
+    # outputs written from an address that is not 16-byte aligned (the one-by-one stores)
+    for n, K in ((5000, 3), (4099, 5)):
+        x = wl.uniform(rng, (n,), bits, False)
+        k = wl.uniform(rng, (K,), bits, False)
+        words, _ = ref.pack(x, bits, False)
+        buf = torch.full((n - K + 2,), -7, dtype=torch.int32, device=DEV)
+        y = samd.conv1d(gpu_words(words), n, bits, k.tolist(), bits, out=buf[1:])
+        torch.cuda.synchronize()
+        assert buf[1:].data_ptr() % 16 == 4
+        np.testing.assert_array_equal(buf[1:].cpu().numpy(), ref.conv1d(x, k), err_msg=f"unaligned n={n} K={K}")
+        assert int(buf[0].item()) == -7
     # every value at the top of the range
     x = np.full(999, (1 << bits) - 1, np.int32)
     k = np.full(5, (1 << bits) - 1, np.int32)
