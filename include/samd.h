@@ -138,7 +138,8 @@ int samd_unpack(const uint32_t *src, int64_t rows, int64_t len, samd_fmt f, void
  * i.e. the complete lanes of the long multiplication of Sec. 5.1, with partial lanes
  * of neighbouring words added (overlap-add of the "parallelograms").  y holds n-K+1
  * int32.  Both formats must be unsigned (the standalone 1-D operator of the paper's
- * Sec. 5); 1 <= K <= 16 and K <= n. */
+ * Sec. 5); 1 <= K <= 16, K <= n, n <= 2^40 and the packed row below 2^31 words (rows
+ * of more than 2^31 values are supported: positions are 64-bit). */
 int samd_conv1d(const uint32_t *x, int64_t n, samd_fmt xf, const int32_t *taps, int32_t K,
                 samd_fmt kf, int32_t *y, hipStream_t stream);
 

@@ -130,7 +130,8 @@ int conv1d_checks(int64_t n, samd_fmt xf, const int32_t *taps, int32_t K, samd_f
     if (!taps) return fail(SAMD_EINVAL, "taps must not be NULL");
     if (K < 1 || K > 16) return fail(SAMD_EINVAL, "K = %d is outside 1..16", K);
     if (n < K) return fail(SAMD_EINVAL, "n = %lld is shorter than the kernel", (long long)n);
-    if (n > ((int64_t)1 << 31)) return fail(SAMD_EINVAL, "n = %lld too large", (long long)n);
+    if (row_words(n, xf.bits) > INT32_MAX || n > ((int64_t)1 << 40))
+        return fail(SAMD_EINVAL, "n = %lld too large", (long long)n);
     for (int t = 0; t < K; ++t)
         if (taps[t] < 0 || taps[t] > (1 << kf.bits) - 1)
             return fail(SAMD_EINVAL, "tap %d = %d outside the %d-bit unsigned range", t, taps[t], kf.bits);

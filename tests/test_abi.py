@@ -76,6 +76,11 @@ def test_conv1d_validation():
     bad = (ctypes.c_int32 * 3)(1, 16, 3)
     assert L.samd_conv1d(P4, 100, Fmt(4, 0), bad, 3, Fmt(4, 0), P4, None) == EINVAL       # tap too wide
     assert L.samd_conv1d(P1, 100, Fmt(4, 0), taps, 3, Fmt(4, 0), P4, None) == EALIGN
+    # rows past 2^31 values are accepted (64-bit positions) up to 2^31 packed words
+    plan = samd.conv1d_plan((1 << 31) + 1000, 8, [1, 2, 3], 8)
+    assert plan.lanes >= 1
+    with pytest.raises(samd.SamdError):
+        samd.conv1d_plan(1 << 36, 1, [1], 1)          # 2^31 words of 1-bit values
 
 
 def test_conv2d_validation():

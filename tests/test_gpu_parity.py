@@ -102,6 +102,31 @@ def test_conv1d_full_size(bits, K):
     np.testing.assert_array_equal(y.cpu().numpy(), want)
 
 
+@pytest.mark.parametrize("bits,K", [(2, 3), (8, 5)])
+def test_conv1d_row_past_2_31_values(bits, K):
+    """A row of 2^31 + 1000 values (64-bit value, word and output indices): pack and conv1d
+    on the GPU (8.6 GB of outputs), sampled outputs - both ends, around index 2^31, and
+    random ones - against the oracle on the windows that define them."""
+    n = (1 << 31) + 1000
+    gen = torch.Generator(device=DEV).manual_seed(1809 + bits)
+    vals = torch.randint(0, 1 << bits, (n,), dtype=torch.uint8, device=DEV, generator=gen)
+    taps = [int(t) for t in np.random.default_rng(bits).integers(0, 1 << bits, K)]
+    xp = samd.pack(vals.view(1, n), bits, False).view(-1)
+    y = samd.conv1d(xp, n, bits, taps, bits)
+    torch.cuda.synchronize()
+    del xp
+    nout = n - K + 1
+    rng = np.random.default_rng(bits * 31)
+    idx = np.unique(np.concatenate([np.arange(0, 4), np.arange((1 << 31) - 8, (1 << 31) + 8),
+                                    np.arange(nout - 4, nout), rng.integers(0, nout, 64)]))
+    got = y[torch.from_numpy(idx).to(DEV)].cpu().numpy()
+    for o, g in zip(idx, got):
+        window = vals[int(o):int(o) + K].cpu().numpy().astype(np.int64)
+        assert g == ref.conv1d(window, np.asarray(taps))[0], (bits, K, int(o))
+    del y, vals
+    torch.cuda.empty_cache()
+
+
 @pytest.mark.parametrize("bits", range(1, 9))
 def test_conv1d_ragged_and_degenerate(bits):
     rng = np.random.default_rng(bits)
