@@ -320,6 +320,13 @@ def timed_graph(fn, reps, warm_s, samples=5):
     return timed_graph_stats(fn, reps, warm_s, samples)[0]
 
 
+def int8_launch_name(plan):
+    """A readable name of an int8 launch: kernel, output channels x positions per
+    workgroup (weight-resident: the longest run of positions), waves per workgroup."""
+    kind = {0: "im2col", 1: "halo", 2: "resident"}[plan.halo]
+    return f"{kind} {plan.mtile}x{plan.positions}" + (f" w{plan.waves}" if plan.halo == 2 else "")
+
+
 def tune_int8(samd, shape, xf, wf, run, warm_s=0.05):
     """Set-up: time every launch the int8 baseline can make for the layer (run() makes one
     call) and install the fastest; returns (the chosen plan as a dict, {launch: us})."""
@@ -328,13 +335,12 @@ def tune_int8(samd, shape, xf, wf, run, warm_s=0.05):
     for plan in samd.conv2d_int8_candidates(shape, xf, wf):
         samd.conv2d_int8_use_plan(shape, xf, wf, plan)
         t = timed_graph(run, 10, warm_s, samples=3)
-        key = f"{'halo' if plan.halo else 'im2col'} {plan.mtile}x{plan.positions}"
-        times[key] = round(t * 1e6, 2)
+        times[int8_launch_name(plan)] = round(t * 1e6, 2)
         if best_t is None or t < best_t:
             best, best_t = plan, t
     samd.conv2d_int8_use_plan(shape, xf, wf, best)
     return ({"halo": best.halo, "mtile": best.mtile, "positions": best.positions,
-             "row_segments": best.row_segments}, times)
+             "row_segments": best.row_segments, "waves": best.waves}, times)
 
 
 INT8_COUNTERS = ("SQ_WAVES SQ_BUSY_CYCLES SQ_WAVE_CYCLES SQ_WAIT_INST_ANY SQ_VALU_MFMA_BUSY_CYCLES "
@@ -369,7 +375,7 @@ def run_int8_counters(args):
         for _ in range(2):
             samd.conv2d_int8_prepared(x_nhwc, xf, wf, shape, ws8, out=y)
         torch.cuda.synchronize()
-        print(f"int8-counters: {'halo' if plan.halo else 'im2col'} {plan.mtile}x{plan.positions} launched twice",
+        print(f"int8-counters: {int8_launch_name(plan)} launched twice",
               flush=True)
     samd.conv2d_int8_use_plan(shape, xf, wf, None)
 
@@ -417,7 +423,7 @@ def int8_summary(folders):
         def g(name):
             return c.get(name, float("nan"))
         hit, miss = g("TCC_HIT_sum"), g("TCC_MISS_sum")
-        out.append(f"| {'halo' if plan.halo else 'im2col'} {plan.mtile}x{plan.positions} | {e['name']} | "
+        out.append(f"| {int8_launch_name(plan)} | {e['name']} | "
                    f"{dur * 1e6:.2f} | {100 * macs / dur / PEAK_I8_MACS:.1f} | {g('SQ_WAVES'):.0f} | "
                    f"{100 * g('SQ_WAIT_INST_ANY') / max(g('SQ_WAVE_CYCLES'), 1):.0f} | "
                    f"{g('SQ_LDS_BANK_CONFLICT'):.3g} | {g('SQ_WAIT_INST_LDS'):.3g} | "
@@ -1098,7 +1104,7 @@ def main():
         if args.no_tune_int8:
             p8 = samd.conv2d_int8_plan(shape, L["xf"], L["wf"])
             L["int8_plan"], L["int8_cands"] = {"halo": p8.halo, "mtile": p8.mtile, "positions": p8.positions,
-                                               "row_segments": p8.row_segments}, None
+                                               "row_segments": p8.row_segments, "waves": p8.waves}, None
         else:
             L["int8_plan"], L["int8_cands"] = tune_int8(
                 samd, shape, L["xf"], L["wf"],

@@ -376,16 +376,20 @@ int samd_conv2d_int8(const void *x, samd_fmt xf, const int8_t *w, samd_fmt wf,
 
 /* Library utility (host only, for inspection and tests): the kernel and tile
  * samd_conv2d_int8 uses for this layer when the activations are 16-byte aligned.
- *   halo         1: the halo-tiled kernel (stride-1 layers with C a multiple of 16);
+ *   halo         2: the weight-resident kernel (stride-1 3x3 and 1x1 layers, C a
+ *                multiple of 16 and at most 128): each workgroup keeps its filters'
+ *                weights in registers and walks one run of positions of one image;
+ *                1: the halo-tiled kernel (stride-1 layers with C a multiple of 16);
  *                0: the im2col kernel (any other layer, or misaligned activations)
  *   mtile        output channels per workgroup
- *   positions    output positions per workgroup
+ *   positions    output positions per workgroup (weight-resident: the longest run)
  *   row_segments 1: tiles are segments of one output row; 0: runs of positions that may
  *                span several rows (halo kernel only)
  *   lds_bytes    dynamic LDS per workgroup (halo kernel: two halo buffers)
+ *   waves        wavefronts per workgroup (4, or 8 for one weight-resident variant)
  *   workgroups   workgroups of one call */
 typedef struct {
-    int32_t halo, mtile, positions, row_segments, lds_bytes;
+    int32_t halo, mtile, positions, row_segments, lds_bytes, waves;
     int64_t workgroups;
 } samd_conv2d_int8_plan;
 
@@ -393,13 +397,13 @@ int samd_conv2d_int8_plan_query(const samd_conv2d_desc *d, samd_fmt xf, samd_fmt
 
 /* Host-only, for measuring the baseline at its best (the SAMD path is tuned the same way,
  * samd_conv2d_tune): every launch samd_conv2d_int8 can make for the layer, the halo
- * tiles that fit first, then the im2col kernel; out holds max_count entries, *count
+ * tiles that fit first, then the weight-resident launches, then the im2col kernel; out holds max_count entries, *count
  * receives the number written. */
 int samd_conv2d_int8_candidates(const samd_conv2d_desc *d, samd_fmt xf, samd_fmt wf, int32_t max_count,
                                 samd_conv2d_int8_plan *out, int32_t *count);
 
-/* Host-only: make `plan` (one of the layer's candidates, matched by halo, mtile and
- * positions) the launch of (xf, *d) for every later samd_conv2d_int8 call in this process;
+/* Host-only: make `plan` (one of the layer's candidates, matched by halo, mtile,
+ * positions and waves) the launch of (xf, *d) for every later samd_conv2d_int8 call in this process;
  * plan NULL restores the library's own choice.  Process-wide state, like tuned SAMD
  * plans; the workspace does not depend on it.  SAMD_EINVAL when no candidate matches. */
 int samd_conv2d_int8_use_plan(const samd_conv2d_desc *d, samd_fmt xf, samd_fmt wf, const samd_conv2d_int8_plan *plan);

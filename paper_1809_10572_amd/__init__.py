@@ -75,7 +75,8 @@ class SpacedLayout(ctypes.Structure):
 
 class Conv2dInt8Plan(ctypes.Structure):
     _fields_ = [("halo", ctypes.c_int32), ("mtile", ctypes.c_int32), ("positions", ctypes.c_int32),
-                ("row_segments", ctypes.c_int32), ("lds_bytes", ctypes.c_int32), ("workgroups", ctypes.c_int64)]
+                ("row_segments", ctypes.c_int32), ("lds_bytes", ctypes.c_int32), ("waves", ctypes.c_int32),
+                ("workgroups", ctypes.c_int64)]
 
 
 class Conv1dPlan(ctypes.Structure):
@@ -484,7 +485,7 @@ def conv2d_int8_plan(shape, xfmt: Fmt, wfmt: Fmt) -> Conv2dInt8Plan:
 
 
 def conv2d_int8_candidates(shape, xfmt: Fmt, wfmt: Fmt) -> List[Conv2dInt8Plan]:
-    """Every launch conv2d_int8 can make for this layer (halo tiles first, then im2col)."""
+    """Every launch conv2d_int8 can make for this layer (halo tiles, weight-resident runs, then im2col)."""
     arr = (Conv2dInt8Plan * MAX_CANDIDATES)()
     n = _i32(0)
     _check(lib().samd_conv2d_int8_candidates(ctypes.byref(Conv2dDesc.of(shape)), xfmt, wfmt, MAX_CANDIDATES, arr,

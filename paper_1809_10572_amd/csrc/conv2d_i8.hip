@@ -578,6 +578,198 @@ __global__ __launch_bounds__(256) void conv2d_i8_halo_kernel(const uint8_t *__re
     }
 }
 
+// Weight-resident implicit GEMM for stride-1 3x3 and 1x1 layers of 64 or 128 (padded)
+// channels.  A workgroup owns one group of 32 filters and one contiguous run of output
+// positions of one image (the layer is cut into about one workgroup per compute unit).
+// It stages the group's weights (32 x K bytes, K = Cp*KH*KW) and the halo of the whole
+// run - every input pixel the run's positions read, all channels - in LDS once; then each
+// of its 8 waves (two per SIMD) copies the weights into its registers (2 x K/64 fragments
+// of 16 bytes per lane, 144 registers at K = 1152) and walks its share of the run's
+// 16-position tiles with no further global reads and no barrier.  A tile's outputs are
+// stored as soon as its MFMAs end, so the int32 output writes overlap the matrix work of
+// the later tiles.  Owning 32 filters rather than all of them keeps the bytes a compute
+// unit pulls from L2 before its first tile small (the group's weights and the halo of a
+// longer run): that prologue bounds such a kernel, since every compute unit starts at
+// once and they share the L2 bandwidth.
+//
+// The activations are the MFMA's A operand (rows = output positions, read from the halo
+// at the tap's shift) and the weights its B operand (columns = filters), so a lane's four
+// accumulator values are four consecutive positions of one filter: one 16-byte store.
+//
+// Unsigned 8-bit activations and the zero padding enter as v - 128, as in the halo
+// kernel: one correction constant per output channel.
+constexpr int kResThreads = 512;
+constexpr int kResWaves = kResThreads / 64;
+constexpr int kResPieces = 5120;   // 16-byte halo pieces of one workgroup at most
+constexpr int kResTile = 16;       // output positions per tile
+constexpr int kResGroup = 32;      // filters per workgroup
+
+struct ResTiles {
+    int R;      // position runs per image
+    int U;      // tiles of 16 positions per image
+    int items;  // work items: N * R * (Mp / 32)
+    int halo;   // LDS bytes of the halo (the weights follow it)
+    int vec;    // 1: 16-byte output stores (Ho * Wo a multiple of 4, y 16-byte aligned)
+};
+
+template <int KH, int KW, int CB>
+__global__ __launch_bounds__(kResThreads) void conv2d_i8_resident_kernel(const uint8_t *__restrict__ x,
+                                                                        const int8_t *__restrict__ wr,
+                                                                        const int32_t *__restrict__ pre,
+                                                                        int32_t *__restrict__ y, const I8Geom g,
+                                                                        const ResTiles rt) {
+    constexpr int NT = kResThreads, NW = kResWaves;
+    constexpr int NC = 2;                 // 16-filter MFMA tiles per wave
+    constexpr int KHW = KH * KW;
+    constexpr int NKB = KHW * CB;         // k-blocks of 64: taps x channel blocks
+    constexpr int KC = 64 * CB;           // padded channels (the weight layout's Cp)
+    constexpr int PIX = KC + 16;          // LDS bytes per halo pixel (16 against bank conflicts)
+    constexpr int PPP = KC / 16;          // 16-byte pieces per pixel
+    constexpr int HPER = kResPieces / NT; // halo pieces per thread at most
+    constexpr int WPIECES = NC * NKB * 64;          // the group's weights in 16-byte pieces
+    constexpr int WPER = (WPIECES + NT - 1) / NT;
+    constexpr int D = NKB % 3 == 0 ? 3 : NKB;       // k-blocks of A fragments read ahead
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    char *halo = smem;
+    char *wlds = smem + rt.halo;   // fragment (c, kb): 1 KB at (c*NKB + kb)*1024, lane l at l*16
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int li = lane & 15, lg = lane >> 4;
+    // items ordered (image, run, filter group); XCD x takes a contiguous share, so the
+    // filter groups of one run and neighbouring runs (which share halo rows) meet in one L2
+    const int xcd = blockIdx.x % kNumXcd, kk = blockIdx.x / kNumXcd;
+    const int ib = (int)((int64_t)xcd * rt.items / kNumXcd), ie = (int)((int64_t)(xcd + 1) * rt.items / kNumXcd);
+    if (ib + kk >= ie) return;
+    const int item = ib + kk;
+    const int ngrp = g.Mp / kResGroup;
+    const int run = item / ngrp;
+    const int m0 = (item - run * ngrp) * kResGroup;
+    const int n = run / rt.R, r = run - n * rt.R;
+    const int HWo = g.Ho * g.Wo;
+    const int ua = (int)((int64_t)r * rt.U / rt.R), ub = (int)((int64_t)(r + 1) * rt.U / rt.R);
+    const int ps = ua * kResTile, pe = min(ub * kResTile, HWo), nt = ub - ua;
+    const int ho_a = ps / g.Wo, ho_b = (pe - 1) / g.Wo;
+    const int hw = g.Wo + KW - 1;                  // halo columns: the padded row
+    const int npc = (ho_b - ho_a + KH) * hw * PPP;
+    const int ih0 = ho_a - g.ph;
+    const int flip = g.zero_point ? (int)0x80808080u : 0;
+
+    // halo pieces of this thread: k = tid + NT u -> pixel rc = k / PPP = (row, column) of
+    // the halo, channels (k % PPP) * 16 .. +15
+    const __amdgpu_buffer_rsrc_t xrs =
+        __builtin_amdgcn_make_buffer_rsrc((void *)x, (short)0, g.N * g.H * g.W * g.C, 0x00020000);
+    const FastDiv by_hw(hw);
+    v4i hv[HPER];
+    uint32_t inside = 0;
+#pragma unroll
+    for (int u = 0; u < HPER; ++u) {
+        const int k = tid + NT * u;
+        const int q = k % PPP, rc = k / PPP;
+        const int rr = by_hw.div(rc), jc = rc - rr * hw;
+        const int ih = ih0 + rr, iw = jc - g.pw;
+        const bool in = k < npc && ih >= 0 && ih < g.H && iw >= 0 && iw < g.W && q * 16 < g.C;
+        inside |= in ? 1u << u : 0u;
+        hv[u] = load16(xrs, in ? ((n * g.H + ih) * g.W + iw) * g.C + q * 16 : 0);
+    }
+    // the group's weights, 16 bytes per piece e = tid + NT u: fragment e / 64, lane e % 64
+    // -> filter m0 + c*16 + (lane & 15), bytes kb*64 + (lane >> 4)*16 .. +15 of its K
+    const __amdgpu_buffer_rsrc_t wrs = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)(wr + (int64_t)m0 * KHW * KC), (short)0, kResGroup * KHW * KC, 0x00020000);
+    v4i wv[WPER];
+#pragma unroll
+    for (int u = 0; u < WPER; ++u) {
+        const int e = min(tid + NT * u, WPIECES - 1);
+        const int f = e >> 6, l = e & 63;
+        const int c = f / NKB, kb = f - c * NKB;
+        wv[u] = load16(wrs, (c * 16 + (l & 15)) * KHW * KC + kb * 64 + (l >> 4) * 16);
+    }
+    // the zero-point correction of this lane's filters
+    constexpr int full = KH * (KW + 1) + KW;   // prefix-table entry of the whole filter
+    const __amdgpu_buffer_rsrc_t prs = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)pre, (short)0, g.M * (KH + 1) * (KW + 1) * 4, 0x00020000);
+    int32_t corr[NC];
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+        const int m = min(m0 + c * 16 + li, g.M - 1);
+        corr[c] = __builtin_amdgcn_raw_buffer_load_b32(prs, (m * (KH + 1) * (KW + 1) + full) * 4, 0, 0);
+    }
+
+    {
+        const v4i pad = {flip, flip, flip, flip};
+#pragma unroll
+        for (int u = 0; u < HPER; ++u) {
+            const int k = tid + NT * u;
+            if (k < npc) *(v4i *)(halo + (k / PPP) * PIX + (k % PPP) * 16) = ((inside >> u) & 1) ? (hv[u] ^ flip) : pad;
+        }
+#pragma unroll
+        for (int u = 0; u < WPER; ++u) {
+            const int e = tid + NT * u;
+            if (e < WPIECES) *(v4i *)(wlds + e * 16) = wv[u];
+        }
+    }
+    __syncthreads();
+
+    // this wave's copy of the group's weights: B fragment (c, kb) is column li (filter
+    // m0 + c*16 + li), bytes kb*64 + lg*16 .. +15 of the filter's K
+    v4i wb[NC][NKB];
+#pragma unroll
+    for (int c = 0; c < NC; ++c)
+#pragma unroll
+        for (int kb = 0; kb < NKB; ++kb) wb[c][kb] = *(const v4i *)(wlds + (c * NKB + kb) * 1024 + lane * 16);
+
+    // halo address of this lane's A row (position) in tile t, at tap (0, 0) and channel
+    // block 0; lanes past the run read its last position (their sums are not stored)
+    const FastDiv by_wo(g.Wo);
+    auto lane_addr = [&](int t) {
+        const int pos = min(ps + t * kResTile + li, pe - 1);
+        const int ho = by_wo.div(pos), wo = pos - ho * g.Wo;
+        return ((ho - ho_a) * hw + wo) * PIX + lg * 16;
+    };
+    const int rowsh = hw * PIX;
+    auto shift = [&](int kb) {   // kb is a compile-time constant after unrolling
+        const int tap = kb / CB;
+        return (tap / KW) * rowsh + (tap % KW) * PIX + (kb % CB) * 64;
+    };
+
+    // tiles wave, wave + NW, ... of the run
+    int cad = lane_addr(min(wave, nt - 1)), nad;
+    v4i a[D];
+#pragma unroll
+    for (int s = 0; s < D; ++s) a[s] = *(const v4i *)(halo + cad + shift(s));
+    for (int t = wave; t < nt; t += NW) {
+        nad = lane_addr(min(t + NW, nt - 1));
+        v4i acc[NC];
+#pragma unroll
+        for (int c = 0; c < NC; ++c) acc[c] = v4i{0, 0, 0, 0};
+#pragma unroll
+        for (int kb = 0; kb < NKB; ++kb) {
+            const int sl = kb % D;
+#pragma unroll
+            for (int c = 0; c < NC; ++c) acc[c] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a[sl], wb[c][kb], acc[c], 0, 0, 0);
+            // the slot is consumed: read k-block kb + D (of this tile, or of the next)
+            const int kn = kb + D;
+            a[sl] = *(const v4i *)(halo + (kn < NKB ? cad : nad) + shift(kn % NKB));
+        }
+        cad = nad;
+        // D[row][col]: lane holds positions 4*lg + v (rows) of filter li (column)
+        const int q0 = ps + t * kResTile + lg * 4;
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+            const int m = m0 + c * 16 + li;
+            if (m >= g.M) continue;
+            int32_t *ym = y + ((int64_t)n * g.M + m) * HWo;
+            const v4i o = acc[c] + (g.zero_point ? 128 * corr[c] : 0);
+            if (rt.vec) {
+                if (q0 < pe) *(v4i *)(ym + q0) = o;
+            } else {
+#pragma unroll
+                for (int v = 0; v < 4; ++v)
+                    if (q0 + v < pe) ym[q0 + v] = o[v];
+            }
+        }
+    }
+}
+
 I8Geom make_geom(const samd_conv2d_desc &d, samd_fmt xf) {
     I8Geom g;
     g.N = d.N; g.C = d.C; g.H = d.H; g.W = d.W; g.M = d.M; g.KH = d.KH; g.KW = d.KW;
@@ -680,6 +872,64 @@ int launch_halo(const void *x, const I8Geom &g, const HaloTiles &ht, int lds, co
     return check_launch("conv2d_int8 (halo tiles)");
 }
 
+// Position runs of the weight-resident kernel: R runs per image, so that the layer gives
+// about `target` workgroups; false when the layer is not one the kernel serves or a run's
+// halo exceeds the LDS or the register-held pieces.
+bool res_tiles(const I8Geom &g, int target, ResTiles &rt, int &lds, int64_t &wgs, int &positions) {
+    if (g.sh != 1 || g.sw != 1 || g.C % 16 != 0) return false;
+    if (!((g.KH == 3 && g.KW == 3) || (g.KH == 1 && g.KW == 1)) || (g.Cp != 64 && g.Cp != 128)) return false;
+    const int64_t HWo = (int64_t)g.Ho * g.Wo;
+    const int hw = g.Wo + g.KW - 1;
+    // fast divisions (positions below 2^22, divisors below 2^12) and 32-bit byte offsets
+    if (HWo >= (1 << 22) || hw >= 4096 || (int64_t)g.N * g.H * g.W * g.C >= INT32_MAX) return false;
+    const int ngrp = g.Mp / kResGroup;
+    rt.U = (int)((HWo + kResTile - 1) / kResTile);
+    const int64_t per_img = (int64_t)g.N * ngrp;
+    rt.R = (int)std::max<int64_t>(1, std::min<int64_t>(rt.U, (target + per_img - 1) / per_img));
+    const int maxu = (rt.U + rt.R - 1) / rt.R;
+    positions = (int)std::min<int64_t>(HWo, (int64_t)maxu * kResTile);
+    // rows a run of that many positions spans (starting anywhere in a row), and its halo
+    const int64_t rows = std::min<int64_t>(g.Ho, (positions - 1) / g.Wo + 2) + g.KH - 1;
+    const int64_t pixels = rows * hw;
+    const int64_t halo = (pixels * (g.Cp + 16) + 15) / 16 * 16;
+    rt.halo = (int)std::min<int64_t>(halo, INT32_MAX);
+    const int64_t total = halo + (int64_t)kResGroup * g.KH * g.KW * g.Cp;
+    lds = (int)std::min<int64_t>(total, INT32_MAX);
+    wgs = (int64_t)g.N * rt.R * ngrp;
+    rt.items = (int)std::min<int64_t>(wgs, INT32_MAX);
+    return pixels * (g.Cp / 16) <= kResPieces && total <= kHaloMaxLds && wgs < ((int64_t)1 << 31) - 8;
+}
+
+template <int KH, int KW, int CB>
+int launch_res(const void *x, const I8Geom &g, ResTiles rt, int lds, const I8Workspace &p, int32_t *y,
+               hipStream_t s) {
+    const void *fn = (const void *)conv2d_i8_resident_kernel<KH, KW, CB>;
+    static std::once_flag once;
+    static hipError_t attr = hipSuccess;
+    std::call_once(once, [&] { attr = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, kHaloMaxLds); });
+    if (attr != hipSuccess) {
+        set_error(std::string("conv2d_int8: LDS attribute: ") + hipGetErrorString(attr));
+        return SAMD_EHIP;
+    }
+    rt.vec = ((int64_t)g.Ho * g.Wo) % 4 == 0 && ((uintptr_t)y % 16) == 0;
+    const int64_t per_xcd = ((int64_t)rt.items + kNumXcd - 1) / kNumXcd;
+    hipLaunchKernelGGL((conv2d_i8_resident_kernel<KH, KW, CB>), dim3((unsigned)(per_xcd * kNumXcd)),
+                       dim3(kResThreads), (size_t)lds, s, (const uint8_t *)x, p.wr, p.pre, y, g, rt);
+    return check_launch("conv2d_int8 (weight-resident)");
+}
+
+int launch_res_any(const void *x, const I8Geom &g, const ResTiles &rt, int lds, const I8Workspace &p, int32_t *y,
+                   hipStream_t s) {
+#define SAMD_RES(KH_, KW_, CB_)                                                                              \
+    if (g.KH == KH_ && g.KW == KW_ && g.Cp == 64 * CB_) return launch_res<KH_, KW_, CB_>(x, g, rt, lds, p, y, s);
+    SAMD_RES(3, 3, 2) SAMD_RES(3, 3, 1) SAMD_RES(1, 1, 2) SAMD_RES(1, 1, 1)
+#undef SAMD_RES
+    set_error("conv2d_int8: no weight-resident kernel for this layer");
+    return SAMD_EUNSUPPORTED;
+}
+
+constexpr int kResTargets[2] = {256, 512};   // workgroups: one per compute unit, or two
+
 // Every launch the int8 baseline can make for a layer: the halo tiles that fit (stride-1
 // layers, C a multiple of 16), then the im2col kernel with 64 and 32 positions per
 // workgroup.
@@ -697,8 +947,26 @@ void int8_candidates(const I8Geom &g, std::vector<samd_conv2d_int8_plan> &out) {
             c.positions = sh[1];
             c.row_segments = ht.rowseg;
             c.lds_bytes = lds;
+            c.waves = 4;
             c.workgroups = wgs;
             out.push_back(c);
+        }
+        for (int target : kResTargets) {
+            ResTiles rt{};
+            int64_t wgs = 0;
+            int lds = 0, positions = 0;
+            if (!res_tiles(g, target, rt, lds, wgs, positions)) continue;
+            samd_conv2d_int8_plan c{};
+            c.halo = 2;
+            c.mtile = kResGroup;
+            c.positions = positions;
+            c.row_segments = 0;
+            c.lds_bytes = lds;
+            c.waves = kResWaves;
+            c.workgroups = wgs;
+            bool dup = false;
+            for (const auto &o : out) dup = dup || (o.halo == 2 && o.positions == positions);
+            if (!dup) out.push_back(c);
         }
     }
     for (int tp : {64, 32}) {
@@ -707,24 +975,30 @@ void int8_candidates(const I8Geom &g, std::vector<samd_conv2d_int8_plan> &out) {
         c.mtile = kTM;
         c.positions = tp;
         c.lds_bytes = 0;
+        c.waves = 4;
         c.workgroups = (g.P + tp - 1) / tp * (g.Mp / kTM);
         out.push_back(c);
     }
 }
 
-// The model's choice among the candidates: in the order 64 x 128, 128 x 128, 64 x 64,
+// The model's choice among the candidates: the weight-resident launch of one workgroup
+// per compute unit (at most 256 workgroups, at least 160); else in the order 64 x 128, 128 x 128, 64 x 64,
 // 128 x 64 (output channels x positions; the order of their times on the mid-size layer),
 // the first halo tile that still gives at least 160 workgroups (about two thirds of the
 // compute units), else the halo tile with the most workgroups, else the im2col kernel
 // with 64 positions when that gives every compute unit a workgroup, else 32.
 samd_conv2d_int8_plan model_choice(const std::vector<samd_conv2d_int8_plan> &cands) {
+    // the weight-resident kernel with about one workgroup per compute unit, when the layer
+    // fills at least two thirds of them
+    for (const auto &c : cands)
+        if (c.halo == 2 && c.workgroups >= 160 && c.workgroups <= 256) return c;
     static const int order[4][2] = {{64, 128}, {128, 128}, {64, 64}, {128, 64}};
     for (const auto &o : order)
         for (const auto &c : cands)
-            if (c.halo && c.mtile == o[0] && c.positions == o[1] && c.workgroups >= 160) return c;
+            if (c.halo == 1 && c.mtile == o[0] && c.positions == o[1] && c.workgroups >= 160) return c;
     int most = -1;
     for (size_t i = 0; i < cands.size(); ++i) {
-        if (!cands[i].halo) continue;
+        if (cands[i].halo != 1) continue;
         if (most < 0 || cands[i].workgroups > cands[most].workgroups) most = (int)i;
     }
     if (most >= 0) return cands[most];
@@ -743,7 +1017,7 @@ Int8Key int8_key(const samd_conv2d_desc &d, samd_fmt xf) {
 }
 
 bool same_launch(const samd_conv2d_int8_plan &a, const samd_conv2d_int8_plan &b) {
-    return a.halo == b.halo && a.mtile == b.mtile && a.positions == b.positions;
+    return a.halo == b.halo && a.mtile == b.mtile && a.positions == b.positions && a.waves == b.waves;
 }
 
 }  // namespace
@@ -792,7 +1066,17 @@ int launch_conv2d_i8(const void *x, samd_fmt xf, const samd_conv2d_desc &d, int3
     const bool vec = (g.C % 16) == 0 && ((uintptr_t)x % 16) == 0;
     samd_conv2d_int8_plan plan{};
     conv2d_i8_tiles(d, xf, plan);
-    if (plan.halo && vec) {
+    if (plan.halo == 2 && vec) {
+        // the plan's runs again: the plan records the workgroup count its target gave
+        for (int target : kResTargets) {
+            ResTiles rt{};
+            int64_t wgs = 0;
+            int lds = 0, positions = 0;
+            if (res_tiles(g, target, rt, lds, wgs, positions) && positions == plan.positions)
+                return launch_res_any(x, g, rt, lds, p, y, s);
+        }
+    }
+    if (plan.halo == 1 && vec) {
         const int wm = plan.mtile / 4, tp = plan.positions;
         HaloTiles ht{};
         int64_t wgs = 0;

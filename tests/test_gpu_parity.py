@@ -339,7 +339,9 @@ def test_conv2d_int8_baseline_edges(shape, bx, sx):
 # row-segment tiles, 64- and 128-channel steps, channel counts that leave part of a chunk
 # (or a whole chunk) empty, output channels that are not a multiple of the tile, ragged
 # last tiles, 1x1 to 7x7 and asymmetric kernels; the last one has no halo that fits and
-# takes the im2col kernel.  Every candidate launch of each layer is tested;
+# takes the im2col kernel.  The stride-1 3x3 and 1x1 layers of at most 128 channels also
+# have weight-resident launches (position counts that are and are not multiples of 4 and
+# of the 32-position tile, filter counts that leave a wave's filters partly empty).  Every candidate launch of each layer is tested;
 # tests/test_abi.py checks on the CPU that they include every tile shape.
 HALO = [
     wl.Conv2dShape(2, 16, 9, 20, 24, 3, 3, 1, 1, 1, 1),        # small: 16 x 64 tiles
@@ -354,8 +356,27 @@ HALO = [
     wl.Conv2dShape(2, 16, 56, 56, 128, 3, 3, 1, 1, 1, 1),      # the mid-size layer's image size
     wl.Conv2dShape(1, 16, 5, 7, 16, 3, 7, 1, 1, 1, 3),         # 3x7, pad (1, 3)
     wl.Conv2dShape(1, 32, 6, 6, 16, 7, 7, 1, 1, 3, 3),         # 7x7 on a 6x6 image
+    wl.Conv2dShape(1, 64, 14, 14, 200, 3, 3, 1, 1, 1, 1),     # two 128-filter tiles, the second partial
+    wl.Conv2dShape(2, 128, 7, 9, 96, 1, 1, 1, 1, 0, 0),        # 1x1 with 128-channel steps, 63 positions
     wl.Conv2dShape(1, 16, 20, 80, 16, 11, 11, 1, 1, 5, 5),     # no halo fits: im2col kernel
 ]
+
+
+@pytest.mark.parametrize("bits", [8, 5])
+def test_conv2d_int8_every_launch_mid(bits):
+    """Every launch the int8 baseline can make for the mid-size layer (halo tiles,
+    weight-resident runs of 400 and 208 positions, im2col), installed in turn, against the
+    oracle at full size."""
+    case, xf, wf, want = conv2d_full(3, bits)
+    cands = samd.conv2d_int8_candidates(case.shape, xf, wf)
+    assert sorted(p.positions for p in cands if p.halo == 2) == [208, 400]
+    try:
+        for plan in cands:
+            samd.conv2d_int8_use_plan(case.shape, xf, wf, plan)
+            np.testing.assert_array_equal(run_conv2d_int8(case.x, case.w, case.shape, xf, wf), want,
+                                          err_msg=f"halo={plan.halo} {plan.mtile}x{plan.positions} w{plan.waves}")
+    finally:
+        samd.conv2d_int8_use_plan(case.shape, xf, wf, None)
 
 
 @pytest.mark.parametrize("shape", HALO, ids=lambda s: "x".join(map(str, s.as_tuple())))
@@ -373,7 +394,7 @@ def test_conv2d_int8_every_launch(shape, bx, sx):
         for plan in samd.conv2d_int8_candidates(shape, xf, wf):
             samd.conv2d_int8_use_plan(shape, xf, wf, plan)
             got = run_conv2d_int8(x, w, shape, xf, wf)
-            np.testing.assert_array_equal(got, want, err_msg=f"halo={plan.halo} {plan.mtile}x{plan.positions}")
+            np.testing.assert_array_equal(got, want, err_msg=f"halo={plan.halo} {plan.mtile}x{plan.positions} w{plan.waves}")
     finally:
         samd.conv2d_int8_use_plan(shape, xf, wf, None)
     np.testing.assert_array_equal(run_conv2d_int8(x, w, shape, xf, wf), want)
