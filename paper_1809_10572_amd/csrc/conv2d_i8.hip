@@ -760,7 +760,7 @@ __global__ __launch_bounds__(kResThreads) void conv2d_i8_resident_kernel(const u
             int32_t *ym = y + ((int64_t)n * g.M + m) * HWo;
             const v4i o = acc[c] + (g.zero_point ? 128 * corr[c] : 0);
             if (rt.vec) {
-                if (q0 < pe) *(v4i *)(ym + q0) = o;
+                if (q0 < pe) __builtin_nontemporal_store(o, (v4i *)(ym + q0));
             } else {
 #pragma unroll
                 for (int v = 0; v < 4; ++v)
