@@ -379,6 +379,37 @@ def test_conv2d_int8_every_launch_mid(bits):
         samd.conv2d_int8_use_plan(case.shape, xf, wf, None)
 
 
+@pytest.mark.parametrize("shape", [wl.Conv2dShape(2, 16, 56, 56, 128, 3, 3, 1, 1, 1, 1),
+                                   wl.Conv2dShape(3, 16, 20, 21, 8, 1, 1, 1, 1, 0, 0)],
+                         ids=lambda s: "x".join(map(str, s.as_tuple())))
+def test_conv2d_int8_resident_unaligned_output(shape):
+    """The weight-resident launches writing into an output 4 bytes past a 16-byte
+    boundary (the per-element store path) and into an aligned one, against the oracle."""
+    rng = np.random.default_rng(5)
+    x = wl.uniform(rng, (shape.N, shape.C, shape.H, shape.W), 8, False)
+    w = wl.uniform(rng, (shape.M, shape.C, shape.KH, shape.KW), 8, True)
+    xf, wf = samd.Fmt(8, 0), samd.Fmt(8, 1)
+    want = ref.conv2d(x, w, shape.as_tuple())
+    xs = gpu_vals(np.transpose(x, (0, 2, 3, 1)), False)
+    ws = gpu_vals(w, True)
+    cands = [p for p in samd.conv2d_int8_candidates(shape, xf, wf) if p.halo == 2]
+    assert cands
+    buf = torch.full((want.size + 8,), -7, dtype=torch.int32, device=DEV)
+    try:
+        for plan in cands:
+            samd.conv2d_int8_use_plan(shape, xf, wf, plan)
+            for off in (1, 4):
+                buf.fill_(-7)
+                samd.conv2d_int8(xs, xf, ws, wf, shape, out=buf[off:off + want.size])
+                torch.cuda.synchronize()
+                got = buf.cpu().numpy()
+                np.testing.assert_array_equal(got[off:off + want.size].reshape(want.shape), want,
+                                              err_msg=f"offset {off} positions {plan.positions}")
+                assert (got[:off] == -7).all() and (got[off + want.size:] == -7).all()
+    finally:
+        samd.conv2d_int8_use_plan(shape, xf, wf, None)
+
+
 @pytest.mark.parametrize("shape", HALO, ids=lambda s: "x".join(map(str, s.as_tuple())))
 @pytest.mark.parametrize("bx,sx", [(8, 0), (8, 1), (4, 0)])
 def test_conv2d_int8_every_launch(shape, bx, sx):
