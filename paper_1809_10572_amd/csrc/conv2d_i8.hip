@@ -604,11 +604,18 @@ constexpr int kResPieces = 5120;   // 16-byte halo pieces of one workgroup at mo
 constexpr int kResTile = 16;       // output positions per tile
 constexpr int kResGroup = 32;      // filters per workgroup
 
+constexpr int kResChunk = 64;      // chunked kernel: input channels per K chunk
+constexpr int kResTPW = 4;         // ... tiles per wave at most: runs of at most 512 positions
+constexpr int kResHalo = 6;        // ... halo pieces (16 bytes) per thread and chunk at most
+constexpr int kResMaxChunks = 8;   // ... padded channels up to 512
+
 struct ResTiles {
     int R;      // position runs per image
     int U;      // tiles of 16 positions per image
     int items;  // work items: N * R * (Mp / 32)
-    int halo;   // LDS bytes of the halo (the weights follow it)
+    int nch;    // K chunks of 64 channels (chunked kernel)
+    int halo;   // LDS bytes of the halo (of one chunk's halo, chunked kernel); the weights follow it
+    int buf;    // LDS bytes of one chunk buffer: halo and weights (chunked kernel)
     int vec;    // 1: 16-byte output stores (Ho * Wo a multiple of 4, y 16-byte aligned)
 };
 
@@ -770,6 +777,206 @@ __global__ __launch_bounds__(kResThreads) void conv2d_i8_resident_kernel(const u
     }
 }
 
+// The same for layers of 256 to 512 (padded) channels, whose weights do not fit a wave's
+// registers whole.  A workgroup owns one group of 32 filters and one contiguous run of output
+// positions of one image (the layer is cut into about one workgroup per compute unit).
+// It walks K in chunks of 64 input channels: for each chunk it stages the group's weights
+// of the chunk (32 x KH*KW x 64 bytes) and the run's halo of the chunk (every input pixel
+// the run's positions read, 64 channels) in LDS, each of its 8 waves (two per SIMD)
+// copies the chunk's weights into registers (2 x KH*KW fragments of 16 bytes per lane,
+// 72 registers at 3x3) and adds the chunk's products of its share of the run's
+// 16-position tiles into accumulators it keeps for all its tiles.  The next chunk is
+// requested before the current one's MFMAs and written to the other LDS buffer after
+// them (one barrier per chunk); the outputs are stored during the last chunk, each tile's
+// as soon as its MFMAs end, so the int32 output writes overlap the last chunk's MFMAs,
+// and no wait for a chunk's loads ever has an output store ahead of it (loads and stores
+// complete in order on one counter).  Owning 32 filters rather than all of them keeps the
+// bytes a compute unit pulls from L2 small (the group's weights and a halo of a longer
+// run); that traffic, with every compute unit starting at once, bounds such a kernel, and
+// the chunks let the first MFMAs start after one chunk of it.  Operands, output stores
+// and the zero point as in the kernel above.
+template <int KH, int KW>
+__global__ __launch_bounds__(kResThreads) void conv2d_i8_resident_chunked_kernel(const uint8_t *__restrict__ x,
+                                                                        const int8_t *__restrict__ wr,
+                                                                        const int32_t *__restrict__ pre,
+                                                                        int32_t *__restrict__ y, const I8Geom g,
+                                                                        const ResTiles rt) {
+    constexpr int NT = kResThreads, NW = kResWaves;
+    constexpr int NC = 2;                 // 16-filter MFMA tiles per wave
+    constexpr int KHW = KH * KW;
+    constexpr int NKB = KHW;              // k-blocks of a chunk: one per tap
+    constexpr int PIX = kResChunk + 16;   // LDS bytes per halo pixel (16 against bank conflicts)
+    constexpr int PPP = kResChunk / 16;   // 16-byte pieces per pixel
+    constexpr int WPIECES = NC * NKB * 64;          // a chunk's weights in 16-byte pieces
+    constexpr int WPER = (WPIECES + NT - 1) / NT;
+    constexpr int D = NKB % 3 == 0 ? 3 : NKB;       // k-blocks of A fragments read ahead
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int li = lane & 15, lg = lane >> 4;
+    // items ordered (image, run, filter group); XCD x takes a contiguous share, so the
+    // filter groups of one run and neighbouring runs (which share halo rows) meet in one L2
+    const int xcd = blockIdx.x % kNumXcd, kk = blockIdx.x / kNumXcd;
+    const int ib = (int)((int64_t)xcd * rt.items / kNumXcd), ie = (int)((int64_t)(xcd + 1) * rt.items / kNumXcd);
+    if (ib + kk >= ie) return;
+    const int item = ib + kk;
+    const int ngrp = g.Mp / kResGroup;
+    const int run = item / ngrp;
+    const int m0 = (item - run * ngrp) * kResGroup;
+    const int n = run / rt.R, r = run - n * rt.R;
+    const int HWo = g.Ho * g.Wo;
+    const int ua = (int)((int64_t)r * rt.U / rt.R), ub = (int)((int64_t)(r + 1) * rt.U / rt.R);
+    const int ps = ua * kResTile, pe = min(ub * kResTile, HWo), nt = ub - ua;
+    const int ho_a = ps / g.Wo, ho_b = (pe - 1) / g.Wo;
+    const int hw = g.Wo + KW - 1;                  // halo columns: the padded row
+    const int npc = (ho_b - ho_a + KH) * hw * PPP; // 16-byte pieces of a chunk's halo
+    const int ih0 = ho_a - g.ph;
+    const int flip = g.zero_point ? (int)0x80808080u : 0;
+    const int Kw = KHW * g.Cp;                     // bytes of one filter's weights
+
+    const __amdgpu_buffer_rsrc_t xrs =
+        __builtin_amdgcn_make_buffer_rsrc((void *)x, (short)0, g.N * g.H * g.W * g.C, 0x00020000);
+    const __amdgpu_buffer_rsrc_t wrs = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)(wr + (int64_t)m0 * Kw), (short)0, kResGroup * Kw, 0x00020000);
+    const FastDiv by_hw(hw);
+    // chunk ch into registers: halo piece k = tid + NT u is pixel k / PPP of the halo (row,
+    // column), channels ch*64 + (k % PPP)*16 .. +15; weight piece e = tid + NT u is
+    // fragment e / 64 = (c, kb), lane e % 64 -> filter m0 + c*16 + (lane & 15), tap kb,
+    // channels ch*64 + (lane >> 4)*16 .. +15
+    auto chunk_load = [&](int ch, v4i (&hv)[kResHalo], uint32_t &inside, v4i (&wv)[WPER]) {
+        const int c0 = ch * kResChunk;
+        inside = 0;
+#pragma unroll
+        for (int u = 0; u < kResHalo; ++u) {
+            const int k = tid + NT * u;
+            const int q = k % PPP, rc = k / PPP;
+            const int rr = by_hw.div(rc), jc = rc - rr * hw;
+            const int ih = ih0 + rr, iw = jc - g.pw;
+            const bool in = k < npc && ih >= 0 && ih < g.H && iw >= 0 && iw < g.W && c0 + q * 16 < g.C;
+            inside |= in ? 1u << u : 0u;
+            hv[u] = load16(xrs, in ? ((n * g.H + ih) * g.W + iw) * g.C + c0 + q * 16 : 0);
+        }
+#pragma unroll
+        for (int u = 0; u < WPER; ++u) {
+            const int e = min(tid + NT * u, WPIECES - 1);
+            const int f = e >> 6, l = e & 63;
+            const int c = f / NKB, kb = f - c * NKB;
+            wv[u] = load16(wrs, (c * 16 + (l & 15)) * Kw + kb * g.Cp + c0 + (l >> 4) * 16);
+        }
+    };
+    // ... and from registers into LDS buffer buf: the halo at 0, the weights after it, as
+    // fragment (c, kb): 1 KB at (c*NKB + kb)*1024, lane l at l*16
+    auto chunk_store = [&](int buf, const v4i (&hv)[kResHalo], uint32_t inside, const v4i (&wv)[WPER]) {
+        char *hb = smem + buf * rt.buf;
+        char *wl = hb + rt.halo;
+        const v4i pad = {flip, flip, flip, flip};
+#pragma unroll
+        for (int u = 0; u < kResHalo; ++u) {
+            const int k = tid + NT * u;
+            if (k < npc) *(v4i *)(hb + (k / PPP) * PIX + (k % PPP) * 16) = ((inside >> u) & 1) ? (hv[u] ^ flip) : pad;
+        }
+#pragma unroll
+        for (int u = 0; u < WPER; ++u) {
+            const int e = tid + NT * u;
+            if (e < WPIECES) *(v4i *)(wl + e * 16) = wv[u];
+        }
+    };
+
+    v4i hv[kResHalo], wv[WPER];
+    uint32_t inside;
+    chunk_load(0, hv, inside, wv);
+    // the zero-point correction of this lane's filters
+    constexpr int full = KH * (KW + 1) + KW;   // prefix-table entry of the whole filter
+    const __amdgpu_buffer_rsrc_t prs = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)pre, (short)0, g.M * (KH + 1) * (KW + 1) * 4, 0x00020000);
+    int32_t corr[NC];
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+        const int m = min(m0 + c * 16 + li, g.M - 1);
+        corr[c] = __builtin_amdgcn_raw_buffer_load_b32(prs, (m * (KH + 1) * (KW + 1) + full) * 4, 0, 0);
+    }
+    chunk_store(0, hv, inside, wv);
+    __syncthreads();
+
+    // halo offset of this lane's A row (position) in tile t, at tap (0, 0); lanes past the
+    // run read its last position (their sums are not stored)
+    const FastDiv by_wo(g.Wo);
+    auto lane_addr = [&](int t) {
+        const int pos = min(ps + t * kResTile + li, pe - 1);
+        const int ho = by_wo.div(pos), wo = pos - ho * g.Wo;
+        return ((ho - ho_a) * hw + wo) * PIX + lg * 16;
+    };
+    const int rowsh = hw * PIX;
+    auto shift = [&](int kb) {   // kb is a compile-time constant after unrolling
+        return (kb / KW) * rowsh + (kb % KW) * PIX;
+    };
+    // D[row][col]: lane holds positions 4*lg + v (rows) of filter li (column)
+    auto store_tile = [&](const v4i (&acc)[NC], int t) {
+        const int q0 = ps + t * kResTile + lg * 4;
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+            const int m = m0 + c * 16 + li;
+            if (m >= g.M) continue;
+            int32_t *ym = y + ((int64_t)n * g.M + m) * HWo;
+            const v4i o = acc[c] + (g.zero_point ? 128 * corr[c] : 0);
+            if (rt.vec) {
+                if (q0 < pe) __builtin_nontemporal_store(o, (v4i *)(ym + q0));
+            } else {
+#pragma unroll
+                for (int v = 0; v < 4; ++v)
+                    if (q0 + v < pe) ym[q0 + v] = o[v];
+            }
+        }
+    };
+
+    v4i acc[kResTPW][NC];
+#pragma unroll
+    for (int tt = 0; tt < kResTPW; ++tt)
+#pragma unroll
+        for (int c = 0; c < NC; ++c) acc[tt][c] = v4i{0, 0, 0, 0};
+    for (int ch = 0; ch < rt.nch; ++ch) {
+        const bool more = ch + 1 < rt.nch;
+        if (more) chunk_load(ch + 1, hv, inside, wv);
+        const char *hb = smem + (ch & 1) * rt.buf;
+        const char *wl = hb + rt.halo;
+        // this wave's copy of the chunk's weights: B fragment (c, kb) is column li (filter
+        // m0 + c*16 + li), tap kb, channels ch*64 + lg*16 .. +15
+        v4i wb[NC][NKB];
+#pragma unroll
+        for (int c = 0; c < NC; ++c)
+#pragma unroll
+            for (int kb = 0; kb < NKB; ++kb) wb[c][kb] = *(const v4i *)(wl + (c * NKB + kb) * 1024 + lane * 16);
+        // tiles wave, wave + NW, ... of the run; the first D k-blocks of the next tile are
+        // read while a tile's last MFMAs run
+        int cad = lane_addr(min(wave, nt - 1));
+        v4i a[D];
+#pragma unroll
+        for (int s = 0; s < D; ++s) a[s] = *(const v4i *)(hb + cad + shift(s));
+#pragma unroll
+        for (int tt = 0; tt < kResTPW; ++tt) {
+            const int t = wave + tt * NW;
+            if (t < nt) {
+                const int nad = lane_addr(min(t + NW, nt - 1));
+#pragma unroll
+                for (int kb = 0; kb < NKB; ++kb) {
+                    const int sl = kb % D;
+#pragma unroll
+                    for (int c = 0; c < NC; ++c)
+                        acc[tt][c] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a[sl], wb[c][kb], acc[tt][c], 0, 0, 0);
+                    const int kn = kb + D;
+                    a[sl] = *(const v4i *)(hb + (kn < NKB ? cad : nad) + shift(kn % NKB));
+                }
+                cad = nad;
+                if (!more) store_tile(acc[tt], t);
+            }
+        }
+        if (more) {
+            chunk_store((ch + 1) & 1, hv, inside, wv);
+            __syncthreads();
+        }
+    }
+}
+
 I8Geom make_geom(const samd_conv2d_desc &d, samd_fmt xf) {
     I8Geom g;
     g.N = d.N; g.C = d.C; g.H = d.H; g.W = d.W; g.M = d.M; g.KH = d.KH; g.KW = d.KW;
@@ -872,58 +1079,93 @@ int launch_halo(const void *x, const I8Geom &g, const HaloTiles &ht, int lds, co
     return check_launch("conv2d_int8 (halo tiles)");
 }
 
-// Position runs of the weight-resident kernel: R runs per image, so that the layer gives
-// about `target` workgroups; false when the layer is not one the kernel serves or a run's
-// halo exceeds the LDS or the register-held pieces.
+// Position runs of the weight-resident kernels: R runs per image, so that the layer
+// gives about `target` workgroups; false when the layer is not one they serve or a run's
+// halo exceeds the LDS or the register-held pieces.  Padded channels up to 128: the
+// kernel that holds a filter's whole K in registers; 256 to 512: the chunked kernel (no
+// run of more than kResTPW tiles per wave).
 bool res_tiles(const I8Geom &g, int target, ResTiles &rt, int &lds, int64_t &wgs, int &positions) {
     if (g.sh != 1 || g.sw != 1 || g.C % 16 != 0) return false;
-    if (!((g.KH == 3 && g.KW == 3) || (g.KH == 1 && g.KW == 1)) || (g.Cp != 64 && g.Cp != 128)) return false;
+    if (!((g.KH == 3 && g.KW == 3) || (g.KH == 1 && g.KW == 1))) return false;
+    const bool chunked = g.Cp > 128;
+    if (g.Cp % kResChunk != 0 || g.Cp / kResChunk > kResMaxChunks) return false;
     const int64_t HWo = (int64_t)g.Ho * g.Wo;
     const int hw = g.Wo + g.KW - 1;
     // fast divisions (positions below 2^22, divisors below 2^12) and 32-bit byte offsets
     if (HWo >= (1 << 22) || hw >= 4096 || (int64_t)g.N * g.H * g.W * g.C >= INT32_MAX) return false;
+    if ((int64_t)g.Mp * g.KH * g.KW * g.Cp >= INT32_MAX) return false;
     const int ngrp = g.Mp / kResGroup;
     rt.U = (int)((HWo + kResTile - 1) / kResTile);
     const int64_t per_img = (int64_t)g.N * ngrp;
-    rt.R = (int)std::max<int64_t>(1, std::min<int64_t>(rt.U, (target + per_img - 1) / per_img));
+    int64_t R = std::max<int64_t>(1, (target + per_img - 1) / per_img);
+    if (chunked) R = std::max<int64_t>(R, (rt.U + kResTPW * kResWaves - 1) / (kResTPW * kResWaves));
+    rt.R = (int)std::min<int64_t>(rt.U, R);
     const int maxu = (rt.U + rt.R - 1) / rt.R;
     positions = (int)std::min<int64_t>(HWo, (int64_t)maxu * kResTile);
     // rows a run of that many positions spans (starting anywhere in a row), and its halo
     const int64_t rows = std::min<int64_t>(g.Ho, (positions - 1) / g.Wo + 2) + g.KH - 1;
     const int64_t pixels = rows * hw;
-    const int64_t halo = (pixels * (g.Cp + 16) + 15) / 16 * 16;
+    const int kc = chunked ? kResChunk : g.Cp;   // channels in LDS at a time
+    const int64_t halo = (pixels * (kc + 16) + 15) / 16 * 16;
+    const int64_t buf = halo + (int64_t)kResGroup * g.KH * g.KW * kc;
+    rt.nch = g.Cp / kc;
     rt.halo = (int)std::min<int64_t>(halo, INT32_MAX);
-    const int64_t total = halo + (int64_t)kResGroup * g.KH * g.KW * g.Cp;
+    rt.buf = (int)std::min<int64_t>(buf, INT32_MAX);
+    const int64_t total = (rt.nch > 1 ? 2 : 1) * buf;
     lds = (int)std::min<int64_t>(total, INT32_MAX);
     wgs = (int64_t)g.N * rt.R * ngrp;
     rt.items = (int)std::min<int64_t>(wgs, INT32_MAX);
-    return pixels * (g.Cp / 16) <= kResPieces && total <= kHaloMaxLds && wgs < ((int64_t)1 << 31) - 8;
+    const bool pieces = chunked ? (maxu <= kResTPW * kResWaves && pixels * (kc / 16) <= (int64_t)kResHalo * kResThreads)
+                                : pixels * (kc / 16) <= kResPieces;
+    return pieces && total <= kHaloMaxLds && wgs < ((int64_t)1 << 31) - 8;
 }
 
-template <int KH, int KW, int CB>
-int launch_res(const void *x, const I8Geom &g, ResTiles rt, int lds, const I8Workspace &p, int32_t *y,
-               hipStream_t s) {
-    const void *fn = (const void *)conv2d_i8_resident_kernel<KH, KW, CB>;
-    static std::once_flag once;
-    static hipError_t attr = hipSuccess;
-    std::call_once(once, [&] { attr = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, kHaloMaxLds); });
+template <typename F>
+int launch_res_kernel(F kernel, const void *x, const I8Geom &g, ResTiles rt, int lds, const I8Workspace &p,
+                      int32_t *y, hipStream_t s, std::once_flag &once, hipError_t &attr) {
+    std::call_once(once, [&] {
+        attr = hipFuncSetAttribute((const void *)kernel, hipFuncAttributeMaxDynamicSharedMemorySize, kHaloMaxLds);
+    });
     if (attr != hipSuccess) {
         set_error(std::string("conv2d_int8: LDS attribute: ") + hipGetErrorString(attr));
         return SAMD_EHIP;
     }
     rt.vec = ((int64_t)g.Ho * g.Wo) % 4 == 0 && ((uintptr_t)y % 16) == 0;
     const int64_t per_xcd = ((int64_t)rt.items + kNumXcd - 1) / kNumXcd;
-    hipLaunchKernelGGL((conv2d_i8_resident_kernel<KH, KW, CB>), dim3((unsigned)(per_xcd * kNumXcd)),
-                       dim3(kResThreads), (size_t)lds, s, (const uint8_t *)x, p.wr, p.pre, y, g, rt);
+    hipLaunchKernelGGL(kernel, dim3((unsigned)(per_xcd * kNumXcd)), dim3(kResThreads), (size_t)lds, s,
+                       (const uint8_t *)x, (const int8_t *)p.wr, (const int32_t *)p.pre, y, g, rt);
     return check_launch("conv2d_int8 (weight-resident)");
+}
+
+template <int KH, int KW, int CB>
+int launch_res(const void *x, const I8Geom &g, const ResTiles &rt, int lds, const I8Workspace &p, int32_t *y,
+               hipStream_t s) {
+    static std::once_flag once;
+    static hipError_t attr = hipSuccess;
+    return launch_res_kernel(conv2d_i8_resident_kernel<KH, KW, CB>, x, g, rt, lds, p, y, s, once, attr);
+}
+
+template <int KH, int KW>
+int launch_res_chunked(const void *x, const I8Geom &g, const ResTiles &rt, int lds, const I8Workspace &p, int32_t *y,
+                       hipStream_t s) {
+    static std::once_flag once;
+    static hipError_t attr = hipSuccess;
+    return launch_res_kernel(conv2d_i8_resident_chunked_kernel<KH, KW>, x, g, rt, lds, p, y, s, once, attr);
 }
 
 int launch_res_any(const void *x, const I8Geom &g, const ResTiles &rt, int lds, const I8Workspace &p, int32_t *y,
                    hipStream_t s) {
-#define SAMD_RES(KH_, KW_, CB_)                                                                              \
-    if (g.KH == KH_ && g.KW == KW_ && g.Cp == 64 * CB_) return launch_res<KH_, KW_, CB_>(x, g, rt, lds, p, y, s);
-    SAMD_RES(3, 3, 2) SAMD_RES(3, 3, 1) SAMD_RES(1, 1, 2) SAMD_RES(1, 1, 1)
-#undef SAMD_RES
+    const bool k3 = g.KH == 3 && g.KW == 3, k1 = g.KH == 1 && g.KW == 1;
+    if (g.Cp > 128) {
+        if (k3) return launch_res_chunked<3, 3>(x, g, rt, lds, p, y, s);
+        if (k1) return launch_res_chunked<1, 1>(x, g, rt, lds, p, y, s);
+    } else if (g.Cp == 128) {
+        if (k3) return launch_res<3, 3, 2>(x, g, rt, lds, p, y, s);
+        if (k1) return launch_res<1, 1, 2>(x, g, rt, lds, p, y, s);
+    } else {
+        if (k3) return launch_res<3, 3, 1>(x, g, rt, lds, p, y, s);
+        if (k1) return launch_res<1, 1, 1>(x, g, rt, lds, p, y, s);
+    }
     set_error("conv2d_int8: no weight-resident kernel for this layer");
     return SAMD_EUNSUPPORTED;
 }

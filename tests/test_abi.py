@@ -306,11 +306,12 @@ def test_int8_halo_tiles_cover_every_kernel():
         own = samd.conv2d_int8_plan(shape, Fmt(8, False), Fmt(8, True))
         assert any((own.halo, own.mtile, own.positions) == (c.halo, c.mtile, c.positions) for c in cands)
     assert {(1, 128, 128), (1, 128, 64), (1, 64, 128), (1, 64, 64)} <= {k[:3] for k in seen}, seen
-    # weight-resident launches (32 filters per workgroup) for 3x3 and 1x1 layers of 64- and
-    # 128-channel steps
-    res = {(sh.KH, 64 if sh.C <= 64 else 128) for sh in HALO
+    # weight-resident launches (32 filters per workgroup) for 3x3 and 1x1 layers of 1 to 4
+    # blocks of 64 input channels (whole K in registers up to 128 padded channels, K in
+    # chunks of 64 channels above)
+    res = {(sh.KH, -(-sh.C // 64)) for sh in HALO
            for p in samd.conv2d_int8_candidates(sh, Fmt(8, False), Fmt(8, True)) if p.halo == 2}
-    assert {(3, 64), (3, 128), (1, 64), (1, 128)} <= res, res
+    assert {(3, 1), (3, 2), (3, 3), (3, 4), (1, 1), (1, 2)} <= res, res
     mid = samd.conv2d_int8_candidates(wl.MID, Fmt(8, False), Fmt(8, True))
     assert [(p.mtile, p.positions, p.waves, p.workgroups) for p in mid if p.halo == 2] == [(32, 400, 8, 256),
                                                                                           (32, 208, 8, 512)]
@@ -318,10 +319,10 @@ def test_int8_halo_tiles_cover_every_kernel():
     assert {0, 1} <= {k[3] for k in seen if k[0] == 1}
     assert {64, 128} <= {k[4] for k in seen if k[0] == 1}
     assert not any(c.halo for c in samd.conv2d_int8_candidates(HALO[-1], Fmt(8, False), Fmt(8, True)))
-    # the mid-size layer takes the weight-resident kernel, the extremes-heavy layer (256
-    # channels) the halo kernel
-    assert samd.conv2d_int8_plan(wl.MID, Fmt(8, False), Fmt(8, True)).halo == 2
-    assert samd.conv2d_int8_plan(wl.STRESS, Fmt(8, False), Fmt(8, True)).halo == 1
+    # the mid-size layer, the extremes-heavy layer (256 channels) and VGG-B's 3x3 layers of
+    # 64 to 512 channels take the weight-resident kernel
+    for shape in [wl.MID, wl.STRESS] + list(wl.VGGB_LAYERS[2:]):
+        assert samd.conv2d_int8_plan(shape, Fmt(8, False), Fmt(8, True)).halo == 2, shape
     # strided layers and channel counts that are not a multiple of 16 take the im2col kernel
     assert samd.conv2d_int8_plan(wl.Conv2dShape(1, 16, 9, 9, 8, 3, 3, 2, 2, 1, 1), Fmt(8, 1), Fmt(8, 1)).halo == 0
     assert samd.conv2d_int8_plan(wl.Conv2dShape(1, 24, 9, 9, 8, 3, 3, 1, 1, 1, 1), Fmt(8, 1), Fmt(8, 1)).halo == 0
