@@ -376,9 +376,10 @@ int samd_conv2d_int8(const void *x, samd_fmt xf, const int8_t *w, samd_fmt wf,
 
 /* Library utility (host only, for inspection and tests): the kernel and tile
  * samd_conv2d_int8 uses for this layer when the activations are 16-byte aligned.
- *   halo         2: the weight-resident kernel (stride-1 3x3 and 1x1 layers, C a
- *                multiple of 16 and at most 128): each workgroup keeps its filters'
- *                weights in registers and walks one run of positions of one image;
+ *   halo         2: a weight-resident kernel (stride-1 3x3 and 1x1 layers, C a
+ *                multiple of 16 and at most 512): each workgroup keeps its 32 filters'
+ *                weights in registers (whole, or 64 channels at a time above 128
+ *                padded channels) and walks one run of positions of one image;
  *                1: the halo-tiled kernel (stride-1 layers with C a multiple of 16);
  *                0: the im2col kernel (any other layer, or misaligned activations)
  *   mtile        output channels per workgroup
@@ -386,7 +387,7 @@ int samd_conv2d_int8(const void *x, samd_fmt xf, const int8_t *w, samd_fmt wf,
  *   row_segments 1: tiles are segments of one output row; 0: runs of positions that may
  *                span several rows (halo kernel only)
  *   lds_bytes    dynamic LDS per workgroup (halo kernel: two halo buffers)
- *   waves        wavefronts per workgroup (4, or 8 for one weight-resident variant)
+ *   waves        wavefronts per workgroup (4; 8 for the weight-resident kernels)
  *   workgroups   workgroups of one call */
 typedef struct {
     int32_t halo, mtile, positions, row_segments, lds_bytes, waves;
