@@ -738,13 +738,15 @@ __global__ __launch_bounds__(kResThreads) void conv2d_i8_resident_kernel(const u
         return (tap / KW) * rowsh + (tap % KW) * PIX + (kb % CB) * 64;
     };
 
-    // tiles wave, wave + NW, ... of the run
-    int cad = lane_addr(min(wave, nt - 1)), nad;
+    // tile pairs: the wave's i-th tile is 2 (wave + NW (i / 2)) + i % 2, so both 64-byte
+    // halves of an output line come from one wave, one right after the other
+    auto tile_of = [&](int i) { return 2 * (wave + NW * (i >> 1)) + (i & 1); };
+    int cad = lane_addr(min(tile_of(0), nt - 1)), nad;
     v4i a[D];
 #pragma unroll
     for (int s = 0; s < D; ++s) a[s] = *(const v4i *)(halo + cad + shift(s));
-    for (int t = wave; t < nt; t += NW) {
-        nad = lane_addr(min(t + NW, nt - 1));
+    for (int i = 0, t = tile_of(0); t < nt; t = tile_of(++i)) {
+        nad = lane_addr(min(tile_of(i + 1), nt - 1));
         v4i acc[NC];
 #pragma unroll
         for (int c = 0; c < NC; ++c) acc[c] = v4i{0, 0, 0, 0};
