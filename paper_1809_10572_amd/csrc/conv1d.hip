@@ -33,15 +33,15 @@ __device__ __forceinline__ uint32_t lane_of(uint32_t lo, uint32_t hi, int j, int
 // bound the per-output registers are unrolled over).  Each (row, wave) stores the
 // outputs of own = 64 - extra consecutive words; the last `extra` lanes of each compute
 // the products of the following words only, which the storing lanes read with
-// cross-lane shuffles for the overlap-add.  A lane works on kRows rows, which share
+// whole-wave lane shifts for the overlap-add.  A lane works on kRows rows, which share
 // every scalar decision (which lane of which product an output takes).
 //   1. The workgroup copies the packed words its lanes read into LDS, with words outside
 //      the row and fields past its end cleared (coalesced loads, the only wait on
 //      memory).
 //   2. Each lane builds its words' operand words per group from the (at most two)
 //      packed words its I values occupy, multiplies and sums the groups' products.
-//   3. Overlap-add through shuffles; a lane's I outputs are stored next to those of its
-//      neighbours.
+//   3. Overlap-add through whole-wave lane shifts; a lane's I outputs are stored next to
+//      those of its neighbours.
 // Per-lane index arithmetic is 32-bit; 64-bit positions are per workgroup (scalar).
 constexpr int kRows = 2;
 
@@ -115,12 +115,19 @@ __global__ __launch_bounds__(kBlock) void conv1d_kernel(const uint32_t *__restri
 #pragma unroll
         for (int r = 0; r < R; ++r) out[r][t] = take ? lane_of(lo[r], hi[r], j, L, nl, lmask) : 0u;
     }
+    // the product of the word e lanes up: e whole-wave shifts by one lane (DPP wave_shl,
+    // a register move; the top lanes receive zeros and store nothing)
+    uint32_t elo[R], ehi[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        elo[r] = lo[r];
+        ehi[r] = hi[r];
+    }
     for (int e = 1; e <= extra; ++e) {
-        uint32_t elo[R], ehi[R];
 #pragma unroll
         for (int r = 0; r < R; ++r) {
-            elo[r] = __shfl_down(lo[r], e, 64);
-            ehi[r] = __shfl_down(hi[r], e, 64);
+            elo[r] = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)elo[r], 0x130, 0xf, 0xf, false);
+            ehi[r] = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)ehi[r], 0x130, 0xf, 0xf, false);
         }
 #pragma unroll
         for (int t = 0; t < IM; ++t) {
