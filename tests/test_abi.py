@@ -328,6 +328,20 @@ def test_int8_halo_tiles_cover_every_kernel():
     assert samd.conv2d_int8_plan(wl.Conv2dShape(1, 24, 9, 9, 8, 3, 3, 1, 1, 1, 1), Fmt(8, 1), Fmt(8, 1)).halo == 0
 
 
+def test_int8_resident_bounds():
+    """The weight-resident launches are offered only where their 32-bit offsets and
+    register-held chunks hold: not for activations of 2^31 bytes or more, not past 512
+    channels, not for strided or 5x5 layers."""
+    def resident(shape):
+        return [p for p in samd.conv2d_int8_candidates(shape, Fmt(8, False), Fmt(8, True)) if p.halo == 2]
+    assert resident(Conv2dDesc(1, 512, 14, 14, 64, 3, 3, 1, 1, 1, 1))
+    assert not resident(Conv2dDesc(1, 576, 14, 14, 64, 3, 3, 1, 1, 1, 1))       # 640 padded channels
+    assert not resident(Conv2dDesc(1, 64, 14, 14, 64, 3, 3, 2, 2, 1, 1))        # stride 2
+    assert not resident(Conv2dDesc(1, 64, 14, 14, 64, 5, 5, 1, 1, 2, 2))        # 5x5
+    assert resident(Conv2dDesc(2, 64, 128, 128, 64, 3, 3, 1, 1, 1, 1))
+    assert not resident(Conv2dDesc(2048, 64, 128, 128, 64, 3, 3, 1, 1, 1, 1))   # 2^31 bytes of activations
+
+
 def test_int8_use_plan_installs_and_reverts():
     import samd_workloads as wl
     xf, wf = Fmt(8, False), Fmt(8, True)
