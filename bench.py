@@ -320,6 +320,20 @@ def timed_graph(fn, reps, warm_s, samples=5):
     return timed_graph_stats(fn, reps, warm_s, samples)[0]
 
 
+def host_cpu():
+    """The host processor the CPU oracle ran on: model name and logical processors."""
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"model": model, "logical_cpus": os.cpu_count()}
+
+
 def int8_launch_name(plan):
     """A readable name of an int8 launch: kernel, output channels x positions per
     workgroup (weight-resident: the longest run of positions), waves per workgroup."""
@@ -1289,7 +1303,8 @@ def main():
             nlayers += 1
         cpu = {"value": round(done / spent / 1e9, 2), "unit": "GMAC/s", "cores": ref.threads(), "kind": "oracle",
                "sample": f"int64 direct conv2d of the same layer, the step's bit widths {bits_list} in turn "
-                         f"({nlayers} layers, {done / 1e9:.1f} GMAC, {spent:.1f} s)"}
+                         f"({nlayers} layers, {done / 1e9:.1f} GMAC, {spent:.1f} s)",
+               "host": host_cpu()}
 
     achieved = tot_mads / tot_conv_s
     line = {
