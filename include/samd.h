@@ -378,8 +378,8 @@ int samd_conv2d_int8(const void *x, samd_fmt xf, const int8_t *w, samd_fmt wf,
  * samd_conv2d_int8 uses for this layer when the activations are 16-byte aligned.
  *   halo         2: a weight-resident kernel (stride-1 3x3 and 1x1 layers, C a
  *                multiple of 16 and at most 512): each workgroup keeps its 32 filters'
- *                weights in registers (whole, or 64 channels at a time above 128
- *                padded channels) and walks one run of positions of one image;
+ *                weights in registers (whole, or in chunks of 128 or 64 channels
+ *                above 128 padded channels) and walks one run of positions of one image;
  *                1: the halo-tiled kernel (stride-1 layers with C a multiple of 16);
  *                0: the im2col kernel (any other layer, or misaligned activations)
  *   mtile        output channels per workgroup

@@ -604,7 +604,7 @@ constexpr int kResPieces = 5120;   // 16-byte halo pieces of one workgroup at mo
 constexpr int kResTile = 16;       // output positions per tile
 constexpr int kResGroup = 32;      // filters per workgroup
 
-constexpr int kResChunk = 64;      // chunked kernel: input channels per K chunk
+constexpr int kResChunk = 64;      // chunked kernel: input channels per K chunk (or twice that)
 constexpr int kResTPW = 4;         // ... tiles per wave at most: runs of at most 512 positions
 constexpr int kResHalo = 6;        // ... halo pieces (16 bytes) per thread and chunk at most
 constexpr int kResMaxChunks = 8;   // ... padded channels up to 512
@@ -613,7 +613,7 @@ struct ResTiles {
     int R;      // position runs per image
     int U;      // tiles of 16 positions per image
     int items;  // work items: N * R * (Mp / 32)
-    int nch;    // K chunks of 64 channels (chunked kernel)
+    int nch;    // K chunks of 64 or 128 channels (chunked kernel)
     int halo;   // LDS bytes of the halo (of one chunk's halo, chunked kernel); the weights follow it
     int buf;    // LDS bytes of one chunk buffer: halo and weights (chunked kernel)
     int vec;    // 1: 16-byte output stores (Ho * Wo a multiple of 4, y 16-byte aligned)
@@ -782,12 +782,15 @@ __global__ __launch_bounds__(kResThreads) void conv2d_i8_resident_kernel(const u
 // The same for layers of 256 to 512 (padded) channels, whose weights do not fit a wave's
 // registers whole.  A workgroup owns one group of 32 filters and one contiguous run of output
 // positions of one image (the layer is cut into about one workgroup per compute unit).
-// It walks K in chunks of 64 input channels: for each chunk it stages the group's weights
-// of the chunk (32 x KH*KW x 64 bytes) and the run's halo of the chunk (every input pixel
-// the run's positions read, 64 channels) in LDS, each of its 8 waves (two per SIMD)
-// copies the chunk's weights into registers (2 x KH*KW fragments of 16 bytes per lane,
-// 72 registers at 3x3) and adds the chunk's products of its share of the run's
-// 16-position tiles into accumulators it keeps for all its tiles.  The next chunk is
+// It walks K in chunks of CH = 64 CB input channels (128 where a chunk's halo fits the
+// staging registers and two chunks fit the LDS, else 64): for each chunk it stages the
+// group's weights of the chunk (32 x KH*KW x CH bytes) and the run's halo of the chunk
+// (every input pixel the run's positions read, CH channels) in LDS; for each 64-channel
+// block of the chunk, each of its 8 waves (two per SIMD) copies the block's weights into
+// registers (2 x KH*KW fragments of 16 bytes per lane, 72 registers at 3x3) and adds the
+// block's products of its share of the run's 16-position tiles into accumulators it keeps
+// for all its tiles.  128-channel chunks halve the chunk round trips (load, LDS write,
+// barrier) that the 256-512-channel layers serialise on.  The next chunk is
 // requested before the current one's MFMAs and written to the other LDS buffer after
 // them (one barrier per chunk); the outputs are stored during the last chunk, each tile's
 // as soon as its MFMAs end, so the int32 output writes overlap the last chunk's MFMAs,
@@ -797,7 +800,7 @@ __global__ __launch_bounds__(kResThreads) void conv2d_i8_resident_kernel(const u
 // run); that traffic, with every compute unit starting at once, bounds such a kernel, and
 // the chunks let the first MFMAs start after one chunk of it.  Operands, output stores
 // and the zero point as in the kernel above.
-template <int KH, int KW>
+template <int KH, int KW, int CB>
 __global__ __launch_bounds__(kResThreads) void conv2d_i8_resident_chunked_kernel(const uint8_t *__restrict__ x,
                                                                         const int8_t *__restrict__ wr,
                                                                         const int32_t *__restrict__ pre,
@@ -806,12 +809,14 @@ __global__ __launch_bounds__(kResThreads) void conv2d_i8_resident_chunked_kernel
     constexpr int NT = kResThreads, NW = kResWaves;
     constexpr int NC = 2;                 // 16-filter MFMA tiles per wave
     constexpr int KHW = KH * KW;
-    constexpr int NKB = KHW;              // k-blocks of a chunk: one per tap
-    constexpr int PIX = kResChunk + 16;   // LDS bytes per halo pixel (16 against bank conflicts)
-    constexpr int PPP = kResChunk / 16;   // 16-byte pieces per pixel
+    constexpr int CH = 64 * CB;           // input channels per chunk
+    constexpr int NKB = KHW * CB;         // k-blocks of a chunk: taps x 64-channel blocks
+    constexpr int PIX = CH + 16;          // LDS bytes per halo pixel (16 against bank conflicts)
+    constexpr int PPP = CH / 16;          // 16-byte pieces per pixel
+    constexpr int HPER = kResHalo;        // halo pieces per thread and chunk
     constexpr int WPIECES = NC * NKB * 64;          // a chunk's weights in 16-byte pieces
     constexpr int WPER = (WPIECES + NT - 1) / NT;
-    constexpr int D = NKB % 3 == 0 ? 3 : NKB;       // k-blocks of A fragments read ahead
+    constexpr int D = KHW % 3 == 0 ? 3 : KHW;       // taps of A fragments read ahead
     extern __shared__ __attribute__((aligned(16))) char smem[];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -842,14 +847,14 @@ __global__ __launch_bounds__(kResThreads) void conv2d_i8_resident_chunked_kernel
         (void *)(wr + (int64_t)m0 * Kw), (short)0, kResGroup * Kw, 0x00020000);
     const FastDiv by_hw(hw);
     // chunk ch into registers: halo piece k = tid + NT u is pixel k / PPP of the halo (row,
-    // column), channels ch*64 + (k % PPP)*16 .. +15; weight piece e = tid + NT u is
-    // fragment e / 64 = (c, kb), lane e % 64 -> filter m0 + c*16 + (lane & 15), tap kb,
-    // channels ch*64 + (lane >> 4)*16 .. +15
-    auto chunk_load = [&](int ch, v4i (&hv)[kResHalo], uint32_t &inside, v4i (&wv)[WPER]) {
-        const int c0 = ch * kResChunk;
+    // column), channels ch*CH + (k % PPP)*16 .. +15; weight piece e = tid + NT u is
+    // fragment e / 64 = (c, kb), lane e % 64 -> filter m0 + c*16 + (lane & 15), tap kb / CB,
+    // channels ch*CH + (kb % CB)*64 + (lane >> 4)*16 .. +15
+    auto chunk_load = [&](int ch, v4i (&hv)[HPER], uint32_t &inside, v4i (&wv)[WPER]) {
+        const int c0 = ch * CH;
         inside = 0;
 #pragma unroll
-        for (int u = 0; u < kResHalo; ++u) {
+        for (int u = 0; u < HPER; ++u) {
             const int k = tid + NT * u;
             const int q = k % PPP, rc = k / PPP;
             const int rr = by_hw.div(rc), jc = rc - rr * hw;
@@ -863,17 +868,17 @@ __global__ __launch_bounds__(kResThreads) void conv2d_i8_resident_chunked_kernel
             const int e = min(tid + NT * u, WPIECES - 1);
             const int f = e >> 6, l = e & 63;
             const int c = f / NKB, kb = f - c * NKB;
-            wv[u] = load16(wrs, (c * 16 + (l & 15)) * Kw + kb * g.Cp + c0 + (l >> 4) * 16);
+            wv[u] = load16(wrs, (c * 16 + (l & 15)) * Kw + (kb / CB) * g.Cp + c0 + (kb % CB) * 64 + (l >> 4) * 16);
         }
     };
     // ... and from registers into LDS buffer buf: the halo at 0, the weights after it, as
     // fragment (c, kb): 1 KB at (c*NKB + kb)*1024, lane l at l*16
-    auto chunk_store = [&](int buf, const v4i (&hv)[kResHalo], uint32_t inside, const v4i (&wv)[WPER]) {
+    auto chunk_store = [&](int buf, const v4i (&hv)[HPER], uint32_t inside, const v4i (&wv)[WPER]) {
         char *hb = smem + buf * rt.buf;
         char *wl = hb + rt.halo;
         const v4i pad = {flip, flip, flip, flip};
 #pragma unroll
-        for (int u = 0; u < kResHalo; ++u) {
+        for (int u = 0; u < HPER; ++u) {
             const int k = tid + NT * u;
             if (k < npc) *(v4i *)(hb + (k / PPP) * PIX + (k % PPP) * 16) = ((inside >> u) & 1) ? (hv[u] ^ flip) : pad;
         }
@@ -884,7 +889,7 @@ __global__ __launch_bounds__(kResThreads) void conv2d_i8_resident_chunked_kernel
         }
     };
 
-    v4i hv[kResHalo], wv[WPER];
+    v4i hv[HPER], wv[WPER];
     uint32_t inside;
     chunk_load(0, hv, inside, wv);
     // the zero-point correction of this lane's filters
@@ -909,8 +914,8 @@ __global__ __launch_bounds__(kResThreads) void conv2d_i8_resident_chunked_kernel
         return ((ho - ho_a) * hw + wo) * PIX + lg * 16;
     };
     const int rowsh = hw * PIX;
-    auto shift = [&](int kb) {   // kb is a compile-time constant after unrolling
-        return (kb / KW) * rowsh + (kb % KW) * PIX;
+    auto shift = [&](int tap) {   // tap is a compile-time constant after unrolling
+        return (tap / KW) * rowsh + (tap % KW) * PIX;
     };
     // D[row][col]: lane holds positions 4*lg + v (rows) of filter li (column)
     auto store_tile = [&](const v4i (&acc)[NC], int t) {
@@ -941,35 +946,40 @@ __global__ __launch_bounds__(kResThreads) void conv2d_i8_resident_chunked_kernel
         if (more) chunk_load(ch + 1, hv, inside, wv);
         const char *hb = smem + (ch & 1) * rt.buf;
         const char *wl = hb + rt.halo;
-        // this wave's copy of the chunk's weights: B fragment (c, kb) is column li (filter
-        // m0 + c*16 + li), tap kb, channels ch*64 + lg*16 .. +15
-        v4i wb[NC][NKB];
 #pragma unroll
-        for (int c = 0; c < NC; ++c)
+        for (int h = 0; h < CB; ++h) {
+            // this wave's copy of the weights of the chunk's 64-channel block h: B fragment
+            // (c, tap) is column li (filter m0 + c*16 + li), channels ch*CH + h*64 + lg*16 .. +15
+            v4i wb[NC][KHW];
 #pragma unroll
-            for (int kb = 0; kb < NKB; ++kb) wb[c][kb] = *(const v4i *)(wl + (c * NKB + kb) * 1024 + lane * 16);
-        // tiles wave, wave + NW, ... of the run; the first D k-blocks of the next tile are
-        // read while a tile's last MFMAs run
-        int cad = lane_addr(min(wave, nt - 1));
-        v4i a[D];
+            for (int c = 0; c < NC; ++c)
 #pragma unroll
-        for (int s = 0; s < D; ++s) a[s] = *(const v4i *)(hb + cad + shift(s));
+                for (int kb = 0; kb < KHW; ++kb)
+                    wb[c][kb] = *(const v4i *)(wl + (c * NKB + kb * CB + h) * 1024 + lane * 16);
+            // tiles wave, wave + NW, ... of the run; the first D taps of the next tile are
+            // read while a tile's last MFMAs run
+            const char *hh = hb + h * 64;
+            int cad = lane_addr(min(wave, nt - 1));
+            v4i a[D];
 #pragma unroll
-        for (int tt = 0; tt < kResTPW; ++tt) {
-            const int t = wave + tt * NW;
-            if (t < nt) {
-                const int nad = lane_addr(min(t + NW, nt - 1));
+            for (int s = 0; s < D; ++s) a[s] = *(const v4i *)(hh + cad + shift(s));
 #pragma unroll
-                for (int kb = 0; kb < NKB; ++kb) {
-                    const int sl = kb % D;
+            for (int tt = 0; tt < kResTPW; ++tt) {
+                const int t = wave + tt * NW;
+                if (t < nt) {
+                    const int nad = lane_addr(min(t + NW, nt - 1));
 #pragma unroll
-                    for (int c = 0; c < NC; ++c)
-                        acc[tt][c] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a[sl], wb[c][kb], acc[tt][c], 0, 0, 0);
-                    const int kn = kb + D;
-                    a[sl] = *(const v4i *)(hb + (kn < NKB ? cad : nad) + shift(kn % NKB));
+                    for (int kb = 0; kb < KHW; ++kb) {
+                        const int sl = kb % D;
+#pragma unroll
+                        for (int c = 0; c < NC; ++c)
+                            acc[tt][c] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a[sl], wb[c][kb], acc[tt][c], 0, 0, 0);
+                        const int kn = kb + D;
+                        a[sl] = *(const v4i *)(hh + (kn < KHW ? cad : nad) + shift(kn % KHW));
+                    }
+                    cad = nad;
+                    if (!more && h == CB - 1) store_tile(acc[tt], t);
                 }
-                cad = nad;
-                if (!more) store_tile(acc[tt], t);
             }
         }
         if (more) {
@@ -1107,9 +1117,20 @@ bool res_tiles(const I8Geom &g, int target, ResTiles &rt, int &lds, int64_t &wgs
     // rows a run of that many positions spans (starting anywhere in a row), and its halo
     const int64_t rows = std::min<int64_t>(g.Ho, (positions - 1) / g.Wo + 2) + g.KH - 1;
     const int64_t pixels = rows * hw;
-    const int kc = chunked ? kResChunk : g.Cp;   // channels in LDS at a time
-    const int64_t halo = (pixels * (kc + 16) + 15) / 16 * 16;
-    const int64_t buf = halo + (int64_t)kResGroup * g.KH * g.KW * kc;
+    // channels in LDS at a time: the whole K up to 128 padded channels; above, chunks of
+    // 128 channels where a chunk's halo fits the registers that stage it and two chunks
+    // fit the LDS, else of 64
+    auto bytes = [&](int kc, int64_t &halo) {
+        halo = (pixels * (kc + 16) + 15) / 16 * 16;
+        return halo + (int64_t)kResGroup * g.KH * g.KW * kc;
+    };
+    int64_t halo;
+    int kc = g.Cp;
+    if (chunked) {
+        kc = g.Cp % 128 == 0 && pixels * 8 <= (int64_t)kResHalo * kResThreads && 2 * bytes(128, halo) <= kHaloMaxLds
+                 ? 128 : kResChunk;
+    }
+    const int64_t buf = bytes(kc, halo);
     rt.nch = g.Cp / kc;
     rt.halo = (int)std::min<int64_t>(halo, INT32_MAX);
     rt.buf = (int)std::min<int64_t>(buf, INT32_MAX);
@@ -1147,12 +1168,19 @@ int launch_res(const void *x, const I8Geom &g, const ResTiles &rt, int lds, cons
     return launch_res_kernel(conv2d_i8_resident_kernel<KH, KW, CB>, x, g, rt, lds, p, y, s, once, attr);
 }
 
+template <int KH, int KW, int CB>
+int launch_res_chunked_cb(const void *x, const I8Geom &g, const ResTiles &rt, int lds, const I8Workspace &p,
+                          int32_t *y, hipStream_t s) {
+    static std::once_flag once;
+    static hipError_t attr = hipSuccess;
+    return launch_res_kernel(conv2d_i8_resident_chunked_kernel<KH, KW, CB>, x, g, rt, lds, p, y, s, once, attr);
+}
+
 template <int KH, int KW>
 int launch_res_chunked(const void *x, const I8Geom &g, const ResTiles &rt, int lds, const I8Workspace &p, int32_t *y,
                        hipStream_t s) {
-    static std::once_flag once;
-    static hipError_t attr = hipSuccess;
-    return launch_res_kernel(conv2d_i8_resident_chunked_kernel<KH, KW>, x, g, rt, lds, p, y, s, once, attr);
+    return g.Cp / rt.nch == 128 ? launch_res_chunked_cb<KH, KW, 2>(x, g, rt, lds, p, y, s)
+                                : launch_res_chunked_cb<KH, KW, 1>(x, g, rt, lds, p, y, s);
 }
 
 int launch_res_any(const void *x, const I8Geom &g, const ResTiles &rt, int lds, const I8Workspace &p, int32_t *y,

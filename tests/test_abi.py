@@ -312,6 +312,22 @@ def test_int8_halo_tiles_cover_every_kernel():
     res = {(sh.KH, -(-sh.C // 64)) for sh in HALO
            for p in samd.conv2d_int8_candidates(sh, Fmt(8, False), Fmt(8, True)) if p.halo == 2}
     assert {(3, 1), (3, 2), (3, 3), (3, 4), (1, 1), (1, 2)} <= res, res
+    # above 128 padded channels both chunk widths (128 and 64 channels), for 3x3 and 1x1
+    widths = set()
+    for sh in HALO:
+        cp = -(-sh.C // 128) * 128
+        if cp <= 128:
+            continue
+        for p in samd.conv2d_int8_candidates(sh, Fmt(8, False), Fmt(8, True)):
+            if p.halo != 2:
+                continue
+            rows = min(sh.H, (p.positions - 1) // sh.W + 2) + sh.KH - 1
+            pixels = rows * (sh.W + sh.KW - 1)
+            kc = [k for k in (64, 128)
+                  if p.lds_bytes == 2 * ((pixels * (k + 16) + 15) // 16 * 16 + 32 * sh.KH * sh.KW * k)]
+            assert len(kc) == 1, (sh, p)
+            widths.add((sh.KH, kc[0]))
+    assert widths == {(3, 64), (3, 128), (1, 64), (1, 128)}, widths
     mid = samd.conv2d_int8_candidates(wl.MID, Fmt(8, False), Fmt(8, True))
     assert [(p.mtile, p.positions, p.waves, p.workgroups) for p in mid if p.halo == 2] == [(32, 400, 8, 256),
                                                                                           (32, 208, 8, 512)]
@@ -340,6 +356,28 @@ def test_int8_resident_bounds():
     assert not resident(Conv2dDesc(1, 64, 14, 14, 64, 5, 5, 1, 1, 2, 2))        # 5x5
     assert resident(Conv2dDesc(2, 64, 128, 128, 64, 3, 3, 1, 1, 1, 1))
     assert not resident(Conv2dDesc(2048, 64, 128, 128, 64, 3, 3, 1, 1, 1, 1))   # 2^31 bytes of activations
+
+
+def test_int8_resident_chunk_width():
+    """Layers of 256-512 padded channels walk K in 128-channel chunks where a chunk's halo
+    fits six 16-byte pieces per thread and two chunks fit 160 KB of LDS, else in 64-channel
+    chunks: each chunk buffer holds the halo (pixels x (chunk + 16) bytes) and 32 filters'
+    weights of the chunk (32 x 9 x chunk bytes), and two buffers alternate."""
+    import samd_workloads as wl
+
+    def lds(pixels, kc):
+        return 2 * ((pixels * (kc + 16) + 15) // 16 * 16 + 32 * 9 * kc)
+
+    def resident(shape):
+        return {p.positions: p.lds_bytes
+                for p in samd.conv2d_int8_candidates(shape, Fmt(8, False), Fmt(8, True)) if p.halo == 2}
+    # 28-wide rows: 112 positions read 5 + 2 halo rows of 30 columns, 64 read 4 + 2
+    assert resident(wl.STRESS) == {112: lds(7 * 30, 128), 64: lds(6 * 30, 128)}
+    # 56-wide rows: 112 or 64 positions read 3 + 2 rows of 58 columns (290 pixels, 157 KB)
+    assert resident(wl.VGGB_LAYERS[5]) == {112: lds(5 * 58, 128), 64: lds(5 * 58, 128)}
+    # 112-wide rows: 208 positions read 3 + 2 rows of 114 columns, 570 pixels: too many
+    # for 128-channel chunks (8 pieces each), 64-channel ones fit; 400 positions fit neither
+    assert resident(Conv2dDesc(1, 256, 112, 112, 256, 3, 3, 1, 1, 1, 1)) == {208: lds(5 * 114, 64)}
 
 
 def test_int8_use_plan_installs_and_reverts():

@@ -358,8 +358,10 @@ HALO = [
     wl.Conv2dShape(1, 32, 6, 6, 16, 7, 7, 1, 1, 3, 3),         # 7x7 on a 6x6 image
     wl.Conv2dShape(1, 64, 14, 14, 200, 3, 3, 1, 1, 1, 1),     # two 128-filter tiles, the second partial
     wl.Conv2dShape(2, 128, 7, 9, 96, 1, 1, 1, 1, 0, 0),        # 1x1 with 128-channel steps, 63 positions
-    wl.Conv2dShape(1, 256, 9, 11, 40, 3, 3, 1, 1, 1, 1),       # 4 chunks of 64 channels, 99 positions, M = 40
-    wl.Conv2dShape(2, 384, 5, 7, 48, 1, 1, 1, 1, 0, 0),        # 1x1 in 6 chunks, 35 positions
+    wl.Conv2dShape(1, 256, 9, 11, 40, 3, 3, 1, 1, 1, 1),       # 2 chunks of 128 channels, 99 positions, M = 40
+    wl.Conv2dShape(2, 384, 5, 7, 48, 1, 1, 1, 1, 0, 0),        # 1x1 in 3 chunks, 35 positions
+    wl.Conv2dShape(1, 256, 4, 150, 40, 3, 3, 1, 1, 1, 1),      # wide rows: 4 chunks of 64 channels
+    wl.Conv2dShape(1, 256, 2, 300, 16, 1, 1, 1, 1, 0, 0),      # 1x1, wide rows: 4 chunks of 64 channels
     wl.Conv2dShape(1, 16, 20, 80, 16, 11, 11, 1, 1, 5, 5),     # no halo fits: im2col kernel
 ]
 
