@@ -337,7 +337,7 @@ def host_cpu():
 def int8_launch_name(plan):
     """A readable name of an int8 launch: kernel, output channels x positions per
     workgroup (weight-resident: the longest run of positions), waves per workgroup."""
-    kind = {0: "im2col", 1: "halo", 2: "resident"}[plan.halo]
+    kind = {0: "im2col", 1: "halo", 2: "resident", 3: "packed-row"}[plan.halo]
     return f"{kind} {plan.mtile}x{plan.positions}" + (f" w{plan.waves}" if plan.halo == 2 else "")
 
 

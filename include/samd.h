@@ -359,8 +359,9 @@ int samd_conv2d_use_plan(const samd_conv2d_desc *d, samd_fmt xf, samd_fmt wf, co
  * (xf and wf are then ignored); the planner's model decides again. */
 int samd_conv2d_untune(const samd_conv2d_desc *d, samd_fmt xf, samd_fmt wf);
 
-/* Library utility: the workspace bytes samd_conv2d_int8 needs (reordered int8 weights
- * and the per-filter weight sums of the zero-point correction). */
+/* Library utility: the workspace bytes samd_conv2d_int8 needs (reordered int8 weights,
+ * the per-filter weight sums of the zero-point correction and, for layers that take the
+ * packed-row kernel, the weights in that kernel's K order). */
 int samd_conv2d_int8_workspace(const samd_conv2d_desc *d, samd_fmt xf, size_t *bytes);
 
 /* The native 8-bit baseline of Sec. 7: the same convolution on values unpacked to
@@ -376,17 +377,23 @@ int samd_conv2d_int8(const void *x, samd_fmt xf, const int8_t *w, samd_fmt wf,
 
 /* Library utility (host only, for inspection and tests): the kernel and tile
  * samd_conv2d_int8 uses for this layer when the activations are 16-byte aligned.
- *   halo         2: a weight-resident kernel (stride-1 3x3 and 1x1 layers, C a
+ *   halo         3: the packed-row kernel (few input channels, any stride: K laid out
+ *                by kernel row, ceil(KW*C / 16) 16-byte slots per row, where that at
+ *                least halves the k-blocks of the 64-channel layout; activations a
+ *                whole number of 4-byte words and 4-byte aligned);
+ *                2: a weight-resident kernel (stride-1 3x3 and 1x1 layers, C a
  *                multiple of 16 and at most 512): each workgroup keeps its 32 filters'
  *                weights in registers (whole, or in chunks of 128 or 64 channels
  *                above 128 padded channels) and walks one run of positions of one image;
  *                1: the halo-tiled kernel (stride-1 layers with C a multiple of 16);
  *                0: the im2col kernel (any other layer, or misaligned activations)
  *   mtile        output channels per workgroup
- *   positions    output positions per workgroup (weight-resident: the longest run)
+ *   positions    output positions per workgroup (weight-resident: the longest run;
+ *                packed-row: 4 waves x 16-position tiles per wave x 16)
  *   row_segments 1: tiles are segments of one output row; 0: runs of positions that may
  *                span several rows (halo kernel only)
- *   lds_bytes    dynamic LDS per workgroup (halo kernel: two halo buffers)
+ *   lds_bytes    dynamic LDS per workgroup (halo kernel: two halo buffers; packed-row:
+ *                the weight fragments of up to 128 filters)
  *   waves        wavefronts per workgroup (4; 8 for the weight-resident kernels)
  *   workgroups   workgroups of one call */
 typedef struct {

@@ -34,13 +34,37 @@ struct I8Geom {
     int Mp;          // output channels padded to 128
     int zero_point;  // 1: unsigned 8-bit activations, shifted by -128
     int64_t P;       // output positions N * Ho * Wo
+    int rk;          // packed-row K: bytes of one kernel row's window in NHWC, KW * C
+    int rs;          // ... 16-byte slots per kernel row, ceil(rk / 16)
+    int pkb;         // ... 64-byte k-blocks, ceil(KH * rs / 4); 0 where that layout is not offered
 };
 
 // Reorder weights to [Mp][KH][KW][Cp] int8 (zero padded) and, for the zero-point path,
 // per-m 2-D prefix sums of the channel-summed kernel (the correction of an output is the
 // sum over its in-image taps: a rectangle, four lookups).
+//
+// Where the packed-row K applies, the weights are also written in that K order, as MFMA B
+// fragments: fragment (cb, kb) (filters cb*16 .. +15, k-block kb) is 1 KB at
+// (cb * pkb + kb) * 1024, lane l's 16 bytes at l * 16 holding filter cb*16 + (l & 15),
+// slot s = kb*4 + (l >> 4): kernel row s / rs, window bytes j = (s % rs)*16 .. +15, byte j
+// being tap column j / C, channel j % C (zero past the row's rk bytes, past the last slot
+// and past the last filter).
 __global__ __launch_bounds__(256) void i8_prep_kernel(const int8_t *__restrict__ w, const I8Geom g,
-                                                      int8_t *__restrict__ wr, int32_t *__restrict__ pre) {
+                                                      int8_t *__restrict__ wr, int32_t *__restrict__ pre,
+                                                      int8_t *__restrict__ wk) {
+    if (g.pkb) {
+        const int64_t ptotal = (int64_t)((g.M + 15) / 16) * g.pkb * 1024;
+        for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < ptotal; i += (int64_t)gridDim.x * 256) {
+            const int f = (int)(i >> 10), l = (int)((i >> 4) & 63), b = (int)(i & 15);
+            const int cb = f / g.pkb, kb = f - cb * g.pkb;
+            const int m = cb * 16 + (l & 15), sl = kb * 4 + (l >> 4);
+            const int ky = sl / g.rs, j = (sl - ky * g.rs) * 16 + b;
+            int8_t v = 0;
+            if (m < g.M && ky < g.KH && j < g.rk)
+                v = w[(((int64_t)m * g.C + j % g.C) * g.KH + ky) * g.KW + j / g.C];
+            wk[i] = v;
+        }
+    }
     const int64_t total = (int64_t)g.Mp * g.KH * g.KW * g.Cp;
     for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < total; i += (int64_t)gridDim.x * 256) {
         const int c = (int)(i % g.Cp);
@@ -989,6 +1013,182 @@ __global__ __launch_bounds__(kResThreads) void conv2d_i8_resident_chunked_kernel
     }
 }
 
+// Packed-row implicit GEMM for layers with few input channels (an image network's first
+// layer: 3 channels), where padding C to a 64-channel K step would spend most of the
+// matrix-core work and most of the activation reads on zeros (at 3 channels and 3x3,
+// 27 useful bytes of K = 576).  In NHWC the KW pixels one kernel row covers at an output
+// position are KW*C consecutive bytes, whatever the stride, so K is laid out by kernel
+// row: row kh owns rs = ceil(KW*C / 16) slots of 16 bytes, four slots per 64-byte k-block
+// (3x3 on 3 channels: one k-block; 11x11 on 3 channels: nine, against 121).  The weight
+// fragments of up to 128 filters (the prepared packed layout) are staged in LDS once per
+// workgroup; each lane builds its A fragment (16 bytes of one position's slot) from five
+// aligned 4-byte loads, a byte shift, and a mask that puts the padding value on bytes of
+// pixels outside the image.  The next step's loads
+// (the next k-block, or the next tile's first) are issued before a step's MFMAs, and a
+// tile's outputs are stored after the next tile's first loads, so no wait for operands
+// has that tile's stores ahead of it.  Operands, output stores and the zero point as in
+// the weight-resident kernels.
+constexpr int kPkThreads = 256;
+constexpr int kPkBlocks = 8;    // 16-filter MFMA column blocks per workgroup at most
+constexpr int kPkMaxKb = 16;    // k-blocks at most (LDS: 8 blocks x 16 k-blocks x 1 KB)
+
+struct PkTiles {
+    int tiles_img;   // 16-position tiles per image
+    int tiles;       // N * tiles_img
+    int tpw;         // tiles per wave
+    int items;       // workgroups along the positions: ceil(tiles / (4 tpw))
+    int vec;         // 1: 16-byte output stores
+};
+
+__global__ __launch_bounds__(kPkThreads) void conv2d_i8_packed_kernel(const uint8_t *__restrict__ x,
+                                                                      const int8_t *__restrict__ wk,
+                                                                      const int32_t *__restrict__ pre,
+                                                                      int32_t *__restrict__ y, const I8Geom g,
+                                                                      const PkTiles pt) {
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int li = lane & 15, lg = lane >> 4;
+    // items dealt per XCD in contiguous shares: neighbouring tiles read the same input rows
+    const int xcd = blockIdx.x % kNumXcd, kk = blockIdx.x / kNumXcd;
+    const int ib = (int)((int64_t)xcd * pt.items / kNumXcd), ie = (int)((int64_t)(xcd + 1) * pt.items / kNumXcd);
+    if (ib + kk >= ie) return;
+    const int item = ib + kk;
+    const int nkb = g.pkb;
+    const int cb0 = blockIdx.y * kPkBlocks;
+    const int ncb = min(kPkBlocks, (g.M + 15) / 16 - cb0);
+
+    // the group's fragments (cb0 + c, kb) to LDS at (c * nkb + kb) * 1024
+    {
+        const v4i *src = (const v4i *)(wk + (int64_t)cb0 * nkb * 1024);
+        const int pieces = ncb * nkb * 64;
+        for (int e = tid; e < pieces; e += kPkThreads) *(v4i *)(smem + e * 16) = src[e];
+    }
+    const int flip = g.zero_point ? (int)0x80808080u : 0;
+    const int pstride = (g.KH + 1) * (g.KW + 1);
+    int32_t corr[kPkBlocks];
+#pragma unroll
+    for (int c = 0; c < kPkBlocks; ++c) {
+        const int m = min((cb0 + c) * 16 + li, g.M - 1);
+        corr[c] = g.zero_point ? 128 * pre[m * pstride + pstride - 1] : 0;
+    }
+    __syncthreads();
+
+    const int HWo = g.Ho * g.Wo;
+    const FastDiv by_wo(g.Wo), by_rs(g.rs);
+    const int slots = g.KH * g.rs;
+    const int nrec = g.N * g.H * g.W * g.C;   // a whole number of 4-byte words, at least one
+    const __amdgpu_buffer_rsrc_t xrs = __builtin_amdgcn_make_buffer_rsrc((void *)x, (short)0, nrec, 0x00020000);
+
+    // a lane's position in tile i of the wave (tiles item*4*tpw + 4 i + wave)
+    struct Geo {
+        int n, p0;    // image, first position of the tile
+        int row0;     // (n*H + ho*sh - ph)*W + wo*sw - pw: the window's first pixel at kernel row 0
+        int ih0;      // ho*sh - ph
+        int jl, jh;   // window bytes inside the image: [jl, jh)
+    };
+    auto geo = [&](int i, Geo &o) {
+        const int t = item * 4 * pt.tpw + 4 * i + wave;
+        if (i >= pt.tpw || t >= pt.tiles) return false;
+        o.n = t / pt.tiles_img;
+        o.p0 = (t - o.n * pt.tiles_img) * 16;
+        const int pos = min(o.p0 + li, HWo - 1);
+        const int ho = by_wo.div(pos), wo = pos - ho * g.Wo;
+        o.ih0 = ho * g.sh - g.ph;
+        const int iw0 = wo * g.sw - g.pw;
+        o.row0 = (o.n * g.H + o.ih0) * g.W + iw0;
+        o.jl = max(0, -iw0) * g.C;
+        o.jh = min(g.KW, g.W - iw0) * g.C;
+        return true;
+    };
+    // step (tile geometry, k-block kb): the lane's five dwords, byte shift and valid range
+    struct Ld {
+        uint32_t r[5];
+        int sb, lo, hi;
+    };
+    auto issue = [&](const Geo &o, int kb, Ld &ld) {
+        const int sl = kb * 4 + lg;
+        const int ky = by_rs.div(sl), part = sl - ky * g.rs;
+        const int ih = o.ih0 + ky;
+        const bool ok = sl < slots && ih >= 0 && ih < g.H;
+        const int off = (o.row0 + ky * g.W) * g.C + part * 16;
+        ld.lo = ok ? o.jl - part * 16 : 16;
+        ld.hi = ok ? o.jh - part * 16 : 0;
+        ld.sb = off & 3;
+        // each word's offset clamped into the activations: a word before the first byte or
+        // past the last holds only bytes of pixels outside the image (or past the window),
+        // which the mask replaces, so every load stays in range (and the clamps keep the
+        // five loads from being merged into one wider load)
+        const int a = ok ? off - ld.sb : 0;
+#pragma unroll
+        for (int d = 0; d < 5; ++d)
+            ld.r[d] = __builtin_amdgcn_raw_buffer_load_b32(xrs, min(max(a + 4 * d, 0), nrec - 4), 0, 0);
+    };
+    auto build = [&](const Ld &ld) {
+        v4i a;
+#pragma unroll
+        for (int d = 0; d < 4; ++d) {
+            const uint32_t v = __builtin_amdgcn_alignbyte(ld.r[d + 1], ld.r[d], (uint32_t)ld.sb);
+            const int lo = min(max(ld.lo - 4 * d, 0), 4), hi = min(max(ld.hi - 4 * d, 0), 4);
+            const uint32_t m = hi > lo ? (uint32_t)((0xFFFFFFFFull << (8 * lo)) & ((1ull << (8 * hi)) - 1)) : 0u;
+            a[d] = (int)(((v ^ (uint32_t)flip) & m) | ((uint32_t)flip & ~m));
+        }
+        return a;
+    };
+    auto store = [&](const v4i (&acc)[kPkBlocks], const Geo &o) {
+        const int q0 = o.p0 + lg * 4;
+#pragma unroll
+        for (int c = 0; c < kPkBlocks; ++c) {
+            const int m = (cb0 + c) * 16 + li;
+            if (c >= ncb || m >= g.M) continue;
+            int32_t *ym = y + ((int64_t)o.n * g.M + m) * HWo;
+            const v4i v = acc[c] + corr[c];
+            if (pt.vec) {
+                if (q0 < HWo) __builtin_nontemporal_store(v, (v4i *)(ym + q0));
+            } else {
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    if (q0 + e < HWo) ym[q0 + e] = v[e];
+            }
+        }
+    };
+
+    Geo cur;
+    if (!geo(0, cur)) return;
+    Ld ld;
+    issue(cur, 0, ld);
+    v4i acc[kPkBlocks];
+#pragma unroll
+    for (int c = 0; c < kPkBlocks; ++c) acc[c] = v4i{0, 0, 0, 0};
+    int i = 0, kb = 0;
+    while (true) {
+        const v4i a = build(ld);
+        // the next step: the next k-block of this tile, or the first of the next tile
+        Geo nxt = cur;
+        int i2 = i, kb2 = kb + 1;
+        bool more = true;
+        if (kb2 == nkb) {
+            kb2 = 0;
+            i2 = i + 1;
+            more = geo(i2, nxt);
+        }
+        if (more) issue(nxt, kb2, ld);
+        const char *bf = smem + kb * 1024 + lane * 16;
+#pragma unroll
+        for (int c = 0; c < kPkBlocks; ++c)
+            if (c < ncb)
+                acc[c] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a, *(const v4i *)(bf + c * nkb * 1024), acc[c], 0, 0, 0);
+        if (kb == nkb - 1) {
+            store(acc, cur);
+#pragma unroll
+            for (int c = 0; c < kPkBlocks; ++c) acc[c] = v4i{0, 0, 0, 0};
+        }
+        if (!more) break;
+        cur = nxt;
+        i = i2;
+        kb = kb2;
+    }
+}
+
 I8Geom make_geom(const samd_conv2d_desc &d, samd_fmt xf) {
     I8Geom g;
     g.N = d.N; g.C = d.C; g.H = d.H; g.W = d.W; g.M = d.M; g.KH = d.KH; g.KW = d.KW;
@@ -1000,10 +1200,24 @@ I8Geom make_geom(const samd_conv2d_desc &d, samd_fmt xf) {
     g.Mp = (d.M + 127) / 128 * 128;
     g.zero_point = (!xf.is_signed && xf.bits == 8) ? 1 : 0;
     g.P = (int64_t)d.N * g.Ho * g.Wo;
+    // the packed-row K where it at most halves the padded layout's k-blocks, with 32-bit
+    // byte offsets into the activations, activations a whole number of 4-byte words (no
+    // word straddles the end, which a range-checked load would read as zero), positions
+    // below 2^22, output rows below 2^12 (fast divisions) and the group's fragments in LDS
+    g.rk = d.KW * d.C;
+    g.rs = (g.rk + 15) / 16;
+    g.pkb = (d.KH * g.rs + 3) / 4;
+    const bool pk = 2 * g.pkb <= d.KH * d.KW * g.Cp / 64 && g.pkb <= kPkMaxKb &&
+                    (int64_t)d.N * d.H * d.W * d.C + 64 < INT32_MAX && (int64_t)d.N * d.H * d.W * d.C % 4 == 0 &&
+                    (int64_t)g.Ho * g.Wo < (1 << 22) &&
+                    g.Wo < 4096 && (int64_t)d.N * ((int64_t)g.Ho * g.Wo + 15) / 16 < INT32_MAX / 2;
+    if (!pk) g.pkb = 0;
     return g;
 }
 
 size_t align256(size_t v) { return (v + 255) / 256 * 256; }
+
+size_t packed_bytes(const I8Geom &g) { return g.pkb ? align256((size_t)((g.M + 15) / 16) * g.pkb * 1024) : 0; }
 
 }  // namespace
 
@@ -1011,7 +1225,7 @@ size_t conv2d_i8_workspace_bytes(const samd_conv2d_desc &d, samd_fmt xf) {
     I8Geom g = make_geom(d, xf);
     size_t wr = align256((size_t)g.Mp * g.KH * g.KW * g.Cp);
     size_t pre = align256((size_t)g.M * (g.KH + 1) * (g.KW + 1) * 4);
-    return wr + pre;
+    return wr + pre + packed_bytes(g);
 }
 
 namespace {
@@ -1019,12 +1233,15 @@ namespace {
 struct I8Workspace {
     int8_t *wr;
     int32_t *pre;
+    int8_t *wk;   // packed-row weight fragments (null where that layout is not offered)
 };
 
 I8Workspace carve(const I8Geom &g, void *ws) {
     I8Workspace w;
     w.wr = (int8_t *)ws;
-    w.pre = (int32_t *)((char *)ws + align256((size_t)g.Mp * g.KH * g.KW * g.Cp));
+    const size_t wr = align256((size_t)g.Mp * g.KH * g.KW * g.Cp);
+    w.pre = (int32_t *)((char *)ws + wr);
+    w.wk = g.pkb ? (int8_t *)ws + wr + align256((size_t)g.M * (g.KH + 1) * (g.KW + 1) * 4) : nullptr;
     return w;
 }
 
@@ -1034,7 +1251,7 @@ int launch_conv2d_i8_prepare(const int8_t *w, samd_fmt xf, const samd_conv2d_des
     const I8Geom g = make_geom(d, xf);
     const I8Workspace p = carve(g, ws);
     const int pgrid = grid_for((int64_t)g.Mp * g.KH * g.KW * g.Cp, 256);
-    hipLaunchKernelGGL(i8_prep_kernel, dim3(pgrid), dim3(256), 0, s, w, g, p.wr, p.pre);
+    hipLaunchKernelGGL(i8_prep_kernel, dim3(pgrid), dim3(256), 0, s, w, g, p.wr, p.pre, p.wk);
     return check_launch("conv2d_int8 weight reorder");
 }
 
@@ -1202,11 +1419,64 @@ int launch_res_any(const void *x, const I8Geom &g, const ResTiles &rt, int lds, 
 
 constexpr int kResTargets[2] = {256, 512};   // workgroups: one per compute unit, or two
 
+// Tiling of the packed-row kernel with tpw 16-position tiles per wave; false where the
+// layer does not take the packed-row K.
+bool pk_tiles(const I8Geom &g, int tpw, PkTiles &pt, int &lds, int64_t &wgs) {
+    if (!g.pkb) return false;
+    const int64_t HWo = (int64_t)g.Ho * g.Wo;
+    pt.tiles_img = (int)((HWo + 15) / 16);
+    pt.tiles = g.N * pt.tiles_img;
+    pt.tpw = tpw;
+    pt.items = (int)(((int64_t)pt.tiles + 4 * tpw - 1) / (4 * tpw));
+    pt.vec = 0;
+    const int nblk = (g.M + 15) / 16;
+    lds = std::min(kPkBlocks, nblk) * g.pkb * 1024;
+    wgs = (int64_t)pt.items * ((nblk + kPkBlocks - 1) / kPkBlocks);
+    return lds <= kHaloMaxLds && wgs < ((int64_t)1 << 31) - 8;
+}
+
+constexpr int kPkTpw[3] = {4, 2, 1};   // tiles per wave of the packed-row candidates
+
+int launch_packed(const void *x, const I8Geom &g, PkTiles pt, int lds, const I8Workspace &p, int32_t *y,
+                  hipStream_t s) {
+    static std::once_flag once;
+    static hipError_t attr = hipSuccess;
+    std::call_once(once, [&] {
+        attr = hipFuncSetAttribute((const void *)conv2d_i8_packed_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                   kHaloMaxLds);
+    });
+    if (attr != hipSuccess) {
+        set_error(std::string("conv2d_int8: LDS attribute: ") + hipGetErrorString(attr));
+        return SAMD_EHIP;
+    }
+    pt.vec = ((int64_t)g.Ho * g.Wo) % 4 == 0 && ((uintptr_t)y % 16) == 0;
+    const int64_t per_xcd = ((int64_t)pt.items + kNumXcd - 1) / kNumXcd;
+    const unsigned gy = (unsigned)(((g.M + 15) / 16 + kPkBlocks - 1) / kPkBlocks);
+    hipLaunchKernelGGL(conv2d_i8_packed_kernel, dim3((unsigned)(per_xcd * kNumXcd), gy), dim3(kPkThreads),
+                       (size_t)lds, s, (const uint8_t *)x, (const int8_t *)p.wk, (const int32_t *)p.pre, y, g, pt);
+    return check_launch("conv2d_int8 (packed rows)");
+}
+
 // Every launch the int8 baseline can make for a layer: the halo tiles that fit (stride-1
 // layers, C a multiple of 16), then the im2col kernel with 64 and 32 positions per
 // workgroup.
 void int8_candidates(const I8Geom &g, std::vector<samd_conv2d_int8_plan> &out) {
     out.clear();
+    for (int tpw : kPkTpw) {
+        PkTiles pt{};
+        int lds = 0;
+        int64_t wgs = 0;
+        if (!pk_tiles(g, tpw, pt, lds, wgs)) continue;
+        samd_conv2d_int8_plan c{};
+        c.halo = 3;
+        c.mtile = std::min(kPkBlocks, (g.M + 15) / 16) * 16;
+        c.positions = 4 * kResTile * tpw;
+        c.row_segments = 0;
+        c.lds_bytes = lds;
+        c.waves = kPkThreads / 64;
+        c.workgroups = wgs;
+        out.push_back(c);
+    }
     if (g.sh == 1 && g.sw == 1 && g.C % 16 == 0) {
         for (const auto &sh : kHaloShapes) {
             HaloTiles ht{};
@@ -1260,6 +1530,15 @@ void int8_candidates(const I8Geom &g, std::vector<samd_conv2d_int8_plan> &out) {
 // compute units), else the halo tile with the most workgroups, else the im2col kernel
 // with 64 positions when that gives every compute unit a workgroup, else 32.
 samd_conv2d_int8_plan model_choice(const std::vector<samd_conv2d_int8_plan> &cands) {
+    // the packed-row kernel where the layer takes it (few input channels), with the most
+    // tiles per wave that still gives every compute unit a workgroup
+    const samd_conv2d_int8_plan *pk = nullptr;
+    for (const auto &c : cands) {
+        if (c.halo != 3) continue;
+        if (c.workgroups >= 256) return c;
+        pk = &c;   // from 4 tiles per wave down to 1: the last has the most workgroups
+    }
+    if (pk) return *pk;
     // the weight-resident kernel with about one workgroup per compute unit, when the layer
     // fills at least two thirds of them
     for (const auto &c : cands)
@@ -1338,6 +1617,12 @@ int launch_conv2d_i8(const void *x, samd_fmt xf, const samd_conv2d_desc &d, int3
     const bool vec = (g.C % 16) == 0 && ((uintptr_t)x % 16) == 0;
     samd_conv2d_int8_plan plan{};
     conv2d_i8_tiles(d, xf, plan);
+    if (plan.halo == 3 && ((uintptr_t)x % 4) == 0) {
+        PkTiles pt{};
+        int lds = 0;
+        int64_t wgs = 0;
+        if (pk_tiles(g, plan.positions / (4 * kResTile), pt, lds, wgs)) return launch_packed(x, g, pt, lds, p, y, s);
+    }
     if (plan.halo == 2 && vec) {
         // the plan's runs again: the plan records the workgroup count its target gave
         for (int target : kResTargets) {

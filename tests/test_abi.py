@@ -334,14 +334,54 @@ def test_int8_halo_tiles_cover_every_kernel():
     assert {(0, 128, 64), (0, 128, 32)} <= {k[:3] for k in seen}
     assert {0, 1} <= {k[3] for k in seen if k[0] == 1}
     assert {64, 128} <= {k[4] for k in seen if k[0] == 1}
-    assert not any(c.halo for c in samd.conv2d_int8_candidates(HALO[-1], Fmt(8, False), Fmt(8, True)))
+    im2col_only = wl.Conv2dShape(1, 16, 20, 80, 16, 11, 11, 1, 1, 5, 5)
+    assert im2col_only in HALO
+    assert not any(c.halo for c in samd.conv2d_int8_candidates(im2col_only, Fmt(8, False), Fmt(8, True)))
     # the mid-size layer, the extremes-heavy layer (256 channels) and VGG-B's 3x3 layers of
     # 64 to 512 channels take the weight-resident kernel
     for shape in [wl.MID, wl.STRESS] + list(wl.VGGB_LAYERS[2:]):
         assert samd.conv2d_int8_plan(shape, Fmt(8, False), Fmt(8, True)).halo == 2, shape
-    # strided layers and channel counts that are not a multiple of 16 take the im2col kernel
-    assert samd.conv2d_int8_plan(wl.Conv2dShape(1, 16, 9, 9, 8, 3, 3, 2, 2, 1, 1), Fmt(8, 1), Fmt(8, 1)).halo == 0
-    assert samd.conv2d_int8_plan(wl.Conv2dShape(1, 24, 9, 9, 8, 3, 3, 1, 1, 1, 1), Fmt(8, 1), Fmt(8, 1)).halo == 0
+    # strided layers and channel counts that are not a multiple of 16 take the packed-row
+    # kernel where it at least halves the k-blocks (16 or 24 channels at 3x3), else im2col
+    assert samd.conv2d_int8_plan(wl.Conv2dShape(1, 16, 9, 9, 8, 3, 3, 2, 2, 1, 1), Fmt(8, 1), Fmt(8, 1)).halo == 3
+    assert samd.conv2d_int8_plan(wl.Conv2dShape(1, 24, 9, 9, 8, 3, 3, 1, 1, 1, 1), Fmt(8, 1), Fmt(8, 1)).halo == 3
+    assert samd.conv2d_int8_plan(wl.Conv2dShape(1, 40, 9, 9, 8, 3, 3, 2, 2, 1, 1), Fmt(8, 1), Fmt(8, 1)).halo == 0
+
+
+def test_int8_packed_rows():
+    """The packed-row launches: K laid out by kernel row (ceil(KW*C / 16) slots of 16
+    bytes per row, four slots per k-block), offered where that at least halves the
+    k-blocks of the 64-channel layout and the activations are whole 4-byte words; the
+    group's fragments (up to 8 blocks of 16 filters x k-blocks x 1 KB) in LDS; the
+    workspace grows by the packed fragments."""
+    import samd_workloads as wl
+    xf, wf = Fmt(8, False), Fmt(8, True)
+
+    def packed(shape):
+        return [(p.mtile, p.positions, p.lds_bytes, p.workgroups)
+                for p in samd.conv2d_int8_candidates(shape, xf, wf) if p.halo == 3]
+    # VGG-B layer 1: 3x3 on 3 channels = 9 bytes per row, one slot each, one k-block;
+    # 224 x 224 positions = 3136 tiles of 16, 4, 2 or 1 per wave and 4 waves
+    assert packed(wl.VGGB_LAYERS[0]) == [(64, 256, 4 * 1024, 196), (64, 128, 4 * 1024, 392),
+                                         (64, 64, 4 * 1024, 784)]
+    # AlexNet layer 1: 11x11 stride 4 on 3 channels = 33 bytes per row, 3 slots, 33 slots =
+    # 9 k-blocks (against 121); 96 filters = 6 blocks; 16 images of 55 x 55 = 16 x 190 tiles
+    assert packed(wl.ALEXNET_LAYERS[0]) == [(96, 256, 6 * 9 * 1024, 190), (96, 128, 6 * 9 * 1024, 380),
+                                            (96, 64, 6 * 9 * 1024, 760)]
+    for shape in (wl.VGGB_LAYERS[0], wl.ALEXNET_LAYERS[0]):
+        assert samd.conv2d_int8_plan(shape, xf, wf).halo == 3
+    # 200 filters: two workgroup rows (8 + 5 blocks), LDS for 8
+    assert packed(Conv2dDesc(1, 3, 8, 8, 200, 3, 3, 1, 1, 1, 1))[0][2:] == (8 * 1024, 2)
+    # 64 channels, 1x1 layers and 32 channels at 3x3 keep the 64-channel layout
+    assert not packed(wl.MID) and not packed(Conv2dDesc(1, 16, 8, 8, 8, 1, 1, 1, 1, 0, 0))
+    assert not packed(Conv2dDesc(1, 32, 8, 8, 8, 3, 3, 1, 1, 1, 1))
+    # activations not a whole number of words (3 x 9 x 9 bytes)
+    assert not packed(Conv2dDesc(1, 3, 9, 9, 8, 3, 3, 1, 1, 1, 1))
+    n = ctypes.c_size_t(0)
+    d = Conv2dDesc(*wl.VGGB_LAYERS[0].as_tuple())
+    assert samd.lib().samd_conv2d_int8_workspace(ctypes.byref(d), xf, ctypes.byref(n)) == OK
+    a256 = lambda v: -(-v // 256) * 256
+    assert n.value == a256(128 * 9 * 64) + a256(64 * 16 * 4) + a256(4 * 1 * 1024)
 
 
 def test_int8_resident_bounds():

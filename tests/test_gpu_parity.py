@@ -363,6 +363,15 @@ HALO = [
     wl.Conv2dShape(1, 256, 4, 150, 40, 3, 3, 1, 1, 1, 1),      # wide rows: 4 chunks of 64 channels
     wl.Conv2dShape(1, 256, 2, 300, 16, 1, 1, 1, 1, 0, 0),      # 1x1, wide rows: 4 chunks of 64 channels
     wl.Conv2dShape(1, 16, 20, 80, 16, 11, 11, 1, 1, 5, 5),     # no halo fits: im2col kernel
+    # packed-row K (few channels): 3 channels at 3x3 (one k-block), 11x11 stride 4 on 3
+    # channels (nine), 1 channel with 130 filters (two workgroup rows), 5x5 with strides
+    # (1, 2), 24 channels, and 42 positions per image (per-element output stores)
+    wl.Conv2dShape(1, 3, 10, 8, 20, 3, 3, 1, 1, 1, 1),
+    wl.Conv2dShape(2, 3, 30, 30, 24, 11, 11, 4, 4, 2, 2),
+    wl.Conv2dShape(1, 1, 5, 8, 130, 3, 3, 1, 1, 1, 1),
+    wl.Conv2dShape(2, 5, 6, 7, 17, 5, 5, 1, 2, 2, 1),
+    wl.Conv2dShape(1, 24, 9, 9, 8, 3, 3, 1, 1, 1, 1),
+    wl.Conv2dShape(2, 3, 6, 7, 70, 3, 3, 1, 1, 1, 1),
 ]
 
 
@@ -417,9 +426,9 @@ def test_conv2d_int8_resident_unaligned_output(shape):
 @pytest.mark.parametrize("shape", HALO, ids=lambda s: "x".join(map(str, s.as_tuple())))
 @pytest.mark.parametrize("bx,sx", [(8, 0), (8, 1), (4, 0)])
 def test_conv2d_int8_every_launch(shape, bx, sx):
-    """Every launch the int8 baseline can make for the layer (each halo tile that fits and
-    the im2col kernel), installed in turn, against the oracle; then the library's own
-    choice again."""
+    """Every launch the int8 baseline can make for the layer (the packed-row launches,
+    each halo tile and weight-resident run that fits, and the im2col kernel), installed in
+    turn, against the oracle; then the library's own choice again."""
     rng = np.random.default_rng(1000 + bx + sx)
     x = wl.half_extremes(rng, (shape.N, shape.C, shape.H, shape.W), bx, bool(sx))
     w = wl.half_extremes(rng, (shape.M, shape.C, shape.KH, shape.KW), 8, True)
