@@ -393,7 +393,9 @@ int samd_conv2d_int8(const void *x, samd_fmt xf, const int8_t *w, samd_fmt wf,
  *   row_segments 1: tiles are segments of one output row; 0: runs of positions that may
  *                span several rows (halo kernel only)
  *   lds_bytes    dynamic LDS per workgroup (halo kernel: two halo buffers; packed-row:
- *                the weight fragments of up to 128 filters)
+ *                the weight fragments of up to 128 filters and their zero-point
+ *                corrections; chunked weight-resident: two chunk buffers and the
+ *                group's corrections)
  *   waves        wavefronts per workgroup (4; 8 for the weight-resident kernels)
  *   workgroups   workgroups of one call */
 typedef struct {

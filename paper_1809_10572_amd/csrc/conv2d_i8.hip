@@ -622,6 +622,19 @@ __global__ __launch_bounds__(256) void conv2d_i8_halo_kernel(const uint8_t *__re
 //
 // Unsigned 8-bit activations and the zero padding enter as v - 128, as in the halo
 // kernel: one correction constant per output channel.
+// One k-block of a 16 x 16 output tile from the activation fragment a (lane li: position
+// li) and the weight fragment w (lane li: filter li).  TR = false: the result's rows are
+// positions, so a lane holds 4 consecutive positions of filter li (one 16-byte store
+// where the output is 16-byte aligned and an image's positions a multiple of 4); TR =
+// true: the rows are filters, so a lane holds position li of filters 4 lg .. 4 lg + 3 and
+// 16 lanes store 16 consecutive positions of a filter, 64 contiguous bytes at any
+// alignment (the element stores of the other layout would be scattered 4-byte writes).
+template <bool TR>
+__device__ __forceinline__ v4i mfma_tile(v4i a, v4i w, v4i acc) {
+    return TR ? __builtin_amdgcn_mfma_i32_16x16x64_i8(w, a, acc, 0, 0, 0)
+              : __builtin_amdgcn_mfma_i32_16x16x64_i8(a, w, acc, 0, 0, 0);
+}
+
 constexpr int kResThreads = 512;
 constexpr int kResWaves = kResThreads / 64;
 constexpr int kResPieces = 5120;   // 16-byte halo pieces of one workgroup at most
@@ -643,7 +656,49 @@ struct ResTiles {
     int vec;    // 1: 16-byte output stores (Ho * Wo a multiple of 4, y 16-byte aligned)
 };
 
-template <int KH, int KW, int CB>
+// Store a 16-position tile (positions p0 .., of which those below pe exist) of NC
+// 16-filter tiles from filter m0, adding 128 x the filter sums where the activations carry
+// the zero point (corr per lane: filter li, or filters 4 lg + v with TR); lanes follow
+// mfma_tile's layouts.  Non-temporal: the outputs are not read again by this kernel.
+template <int NC, bool TR>
+__device__ __forceinline__ void store_res_tile(const v4i (&acc)[NC], const int32_t (&corr)[NC][TR ? 4 : 1],
+                                               int32_t *__restrict__ y, const I8Geom &g, int n, int m0, int p0,
+                                               int pe, int HWo, int vec, int li, int lg) {
+    if constexpr (TR) {
+        // through a buffer over the NC*16 filters' outputs of image n: one per-lane offset
+        // and a scalar one per (c, v), so no per-store 64-bit addresses stay live
+        const int pos = p0 + li;
+        if (pos >= pe) return;
+        const __amdgpu_buffer_rsrc_t yrs = __builtin_amdgcn_make_buffer_rsrc(
+            (void *)(y + ((int64_t)n * g.M + m0) * HWo), (short)0, min(NC * 16, g.M - m0) * HWo * 4, 0x00020000);
+        const int voff = (lg * 4 * HWo + pos) * 4;
+#pragma unroll
+        for (int c = 0; c < NC; ++c)
+#pragma unroll
+            for (int v = 0; v < 4; ++v)
+                if (m0 + c * 16 + lg * 4 + v < g.M)   // aux 2: non-temporal
+                    __builtin_amdgcn_raw_buffer_store_b32(acc[c][v] + (g.zero_point ? 128 * corr[c][v] : 0), yrs,
+                                                          voff, (c * 16 + v) * HWo * 4, 2);
+    } else {
+        const int q0 = p0 + lg * 4;
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+            const int m = m0 + c * 16 + li;
+            if (m >= g.M) continue;
+            int32_t *ym = y + ((int64_t)n * g.M + m) * HWo;
+            const v4i o = acc[c] + (g.zero_point ? 128 * corr[c][0] : 0);
+            if (vec) {
+                if (q0 < pe) __builtin_nontemporal_store(o, (v4i *)(ym + q0));
+            } else {
+#pragma unroll
+                for (int v = 0; v < 4; ++v)
+                    if (q0 + v < pe) ym[q0 + v] = o[v];
+            }
+        }
+    }
+}
+
+template <int KH, int KW, int CB, bool TR>
 __global__ __launch_bounds__(kResThreads) void conv2d_i8_resident_kernel(const uint8_t *__restrict__ x,
                                                                         const int8_t *__restrict__ wr,
                                                                         const int32_t *__restrict__ pre,
@@ -718,12 +773,15 @@ __global__ __launch_bounds__(kResThreads) void conv2d_i8_resident_kernel(const u
     constexpr int full = KH * (KW + 1) + KW;   // prefix-table entry of the whole filter
     const __amdgpu_buffer_rsrc_t prs = __builtin_amdgcn_make_buffer_rsrc(
         (void *)pre, (short)0, g.M * (KH + 1) * (KW + 1) * 4, 0x00020000);
-    int32_t corr[NC];
+    constexpr int NV = TR ? 4 : 1;   // filters per lane and 16-filter tile
+    int32_t corr[NC][NV];
 #pragma unroll
-    for (int c = 0; c < NC; ++c) {
-        const int m = min(m0 + c * 16 + li, g.M - 1);
-        corr[c] = __builtin_amdgcn_raw_buffer_load_b32(prs, (m * (KH + 1) * (KW + 1) + full) * 4, 0, 0);
-    }
+    for (int c = 0; c < NC; ++c)
+#pragma unroll
+        for (int v = 0; v < NV; ++v) {
+            const int m = min(m0 + c * 16 + (TR ? lg * 4 + v : li), g.M - 1);
+            corr[c][v] = __builtin_amdgcn_raw_buffer_load_b32(prs, (m * (KH + 1) * (KW + 1) + full) * 4, 0, 0);
+        }
 
     {
         const v4i pad = {flip, flip, flip, flip};
@@ -778,28 +836,13 @@ __global__ __launch_bounds__(kResThreads) void conv2d_i8_resident_kernel(const u
         for (int kb = 0; kb < NKB; ++kb) {
             const int sl = kb % D;
 #pragma unroll
-            for (int c = 0; c < NC; ++c) acc[c] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a[sl], wb[c][kb], acc[c], 0, 0, 0);
+            for (int c = 0; c < NC; ++c) acc[c] = mfma_tile<TR>(a[sl], wb[c][kb], acc[c]);
             // the slot is consumed: read k-block kb + D (of this tile, or of the next)
             const int kn = kb + D;
             a[sl] = *(const v4i *)(halo + (kn < NKB ? cad : nad) + shift(kn % NKB));
         }
         cad = nad;
-        // D[row][col]: lane holds positions 4*lg + v (rows) of filter li (column)
-        const int q0 = ps + t * kResTile + lg * 4;
-#pragma unroll
-        for (int c = 0; c < NC; ++c) {
-            const int m = m0 + c * 16 + li;
-            if (m >= g.M) continue;
-            int32_t *ym = y + ((int64_t)n * g.M + m) * HWo;
-            const v4i o = acc[c] + (g.zero_point ? 128 * corr[c] : 0);
-            if (rt.vec) {
-                if (q0 < pe) __builtin_nontemporal_store(o, (v4i *)(ym + q0));
-            } else {
-#pragma unroll
-                for (int v = 0; v < 4; ++v)
-                    if (q0 + v < pe) ym[q0 + v] = o[v];
-            }
-        }
+        store_res_tile<NC, TR>(acc, corr, y, g, n, m0, ps + t * kResTile, pe, HWo, rt.vec, li, lg);
     }
 }
 
@@ -824,7 +867,7 @@ __global__ __launch_bounds__(kResThreads) void conv2d_i8_resident_kernel(const u
 // run); that traffic, with every compute unit starting at once, bounds such a kernel, and
 // the chunks let the first MFMAs start after one chunk of it.  Operands, output stores
 // and the zero point as in the kernel above.
-template <int KH, int KW, int CB>
+template <int KH, int KW, int CB, bool TR>
 __global__ __launch_bounds__(kResThreads) void conv2d_i8_resident_chunked_kernel(const uint8_t *__restrict__ x,
                                                                         const int8_t *__restrict__ wr,
                                                                         const int32_t *__restrict__ pre,
@@ -920,11 +963,21 @@ __global__ __launch_bounds__(kResThreads) void conv2d_i8_resident_chunked_kernel
     constexpr int full = KH * (KW + 1) + KW;   // prefix-table entry of the whole filter
     const __amdgpu_buffer_rsrc_t prs = __builtin_amdgcn_make_buffer_rsrc(
         (void *)pre, (short)0, g.M * (KH + 1) * (KW + 1) * 4, 0x00020000);
-    int32_t corr[NC];
+    // (in registers for lane li's filters; with TR, where a lane stores four filters, in
+    // LDS after the two chunk buffers and read back only for the stores)
+    int32_t corr[NC][1];
+    int32_t *corr_lds = (int32_t *)(smem + 2 * rt.buf);
+    if constexpr (TR) {
+        if (tid < kResGroup) {
+            const int m = min(m0 + tid, g.M - 1);
+            corr_lds[tid] = __builtin_amdgcn_raw_buffer_load_b32(prs, (m * (KH + 1) * (KW + 1) + full) * 4, 0, 0);
+        }
+    } else {
 #pragma unroll
-    for (int c = 0; c < NC; ++c) {
-        const int m = min(m0 + c * 16 + li, g.M - 1);
-        corr[c] = __builtin_amdgcn_raw_buffer_load_b32(prs, (m * (KH + 1) * (KW + 1) + full) * 4, 0, 0);
+        for (int c = 0; c < NC; ++c) {
+            const int m = min(m0 + c * 16 + li, g.M - 1);
+            corr[c][0] = __builtin_amdgcn_raw_buffer_load_b32(prs, (m * (KH + 1) * (KW + 1) + full) * 4, 0, 0);
+        }
     }
     chunk_store(0, hv, inside, wv);
     __syncthreads();
@@ -941,22 +994,18 @@ __global__ __launch_bounds__(kResThreads) void conv2d_i8_resident_chunked_kernel
     auto shift = [&](int tap) {   // tap is a compile-time constant after unrolling
         return (tap / KW) * rowsh + (tap % KW) * PIX;
     };
-    // D[row][col]: lane holds positions 4*lg + v (rows) of filter li (column)
     auto store_tile = [&](const v4i (&acc)[NC], int t) {
-        const int q0 = ps + t * kResTile + lg * 4;
+        if constexpr (TR) {
+            int32_t cr[NC][4];
 #pragma unroll
-        for (int c = 0; c < NC; ++c) {
-            const int m = m0 + c * 16 + li;
-            if (m >= g.M) continue;
-            int32_t *ym = y + ((int64_t)n * g.M + m) * HWo;
-            const v4i o = acc[c] + (g.zero_point ? 128 * corr[c] : 0);
-            if (rt.vec) {
-                if (q0 < pe) __builtin_nontemporal_store(o, (v4i *)(ym + q0));
-            } else {
+            for (int c = 0; c < NC; ++c) {
+                const v4i cv = *(const v4i *)(corr_lds + c * 16 + lg * 4);
 #pragma unroll
-                for (int v = 0; v < 4; ++v)
-                    if (q0 + v < pe) ym[q0 + v] = o[v];
+                for (int v = 0; v < 4; ++v) cr[c][v] = cv[v];
             }
+            store_res_tile<NC, TR>(acc, cr, y, g, n, m0, ps + t * kResTile, pe, HWo, rt.vec, li, lg);
+        } else {
+            store_res_tile<NC, TR>(acc, corr, y, g, n, m0, ps + t * kResTile, pe, HWo, rt.vec, li, lg);
         }
     };
 
@@ -997,7 +1046,7 @@ __global__ __launch_bounds__(kResThreads) void conv2d_i8_resident_chunked_kernel
                         const int sl = kb % D;
 #pragma unroll
                         for (int c = 0; c < NC; ++c)
-                            acc[tt][c] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a[sl], wb[c][kb], acc[tt][c], 0, 0, 0);
+                            acc[tt][c] = mfma_tile<TR>(a[sl], wb[c][kb], acc[tt][c]);
                         const int kn = kb + D;
                         a[sl] = *(const v4i *)(hh + (kn < KHW ? cad : nad) + shift(kn % KHW));
                     }
@@ -1040,6 +1089,7 @@ struct PkTiles {
     int vec;         // 1: 16-byte output stores
 };
 
+template <bool TR>
 __global__ __launch_bounds__(kPkThreads) void conv2d_i8_packed_kernel(const uint8_t *__restrict__ x,
                                                                       const int8_t *__restrict__ wk,
                                                                       const int32_t *__restrict__ pre,
@@ -1057,20 +1107,20 @@ __global__ __launch_bounds__(kPkThreads) void conv2d_i8_packed_kernel(const uint
     const int cb0 = blockIdx.y * kPkBlocks;
     const int ncb = min(kPkBlocks, (g.M + 15) / 16 - cb0);
 
-    // the group's fragments (cb0 + c, kb) to LDS at (c * nkb + kb) * 1024
+    // the group's fragments (cb0 + c, kb) to LDS at (c * nkb + kb) * 1024, and after them
+    // the zero-point correction (128 x the filter's sum) of each of the group's filters
     {
         const v4i *src = (const v4i *)(wk + (int64_t)cb0 * nkb * 1024);
         const int pieces = ncb * nkb * 64;
         for (int e = tid; e < pieces; e += kPkThreads) *(v4i *)(smem + e * 16) = src[e];
     }
-    const int flip = g.zero_point ? (int)0x80808080u : 0;
-    const int pstride = (g.KH + 1) * (g.KW + 1);
-    int32_t corr[kPkBlocks];
-#pragma unroll
-    for (int c = 0; c < kPkBlocks; ++c) {
-        const int m = min((cb0 + c) * 16 + li, g.M - 1);
-        corr[c] = g.zero_point ? 128 * pre[m * pstride + pstride - 1] : 0;
+    int32_t *corr = (int32_t *)(smem + ncb * nkb * 1024);
+    if (tid < ncb * 16) {
+        const int pstride = (g.KH + 1) * (g.KW + 1);
+        const int m = min(cb0 * 16 + tid, g.M - 1);
+        corr[tid] = g.zero_point ? 128 * pre[m * pstride + pstride - 1] : 0;
     }
+    const int flip = g.zero_point ? (int)0x80808080u : 0;
     __syncthreads();
 
     const int HWo = g.Ho * g.Wo;
@@ -1134,20 +1184,37 @@ __global__ __launch_bounds__(kPkThreads) void conv2d_i8_packed_kernel(const uint
         }
         return a;
     };
+    // the tile's outputs in mfma_tile's layouts (TR: position o.p0 + li of filters
+    // 4 lg .. 4 lg + 3 of each 16-filter block; else positions o.p0 + 4 lg .. of filter li)
     auto store = [&](const v4i (&acc)[kPkBlocks], const Geo &o) {
-        const int q0 = o.p0 + lg * 4;
+        if constexpr (TR) {
+            const int pos = o.p0 + li;
+            if (pos >= HWo) return;
+            int32_t *yb = y + ((int64_t)o.n * g.M + cb0 * 16 + lg * 4) * HWo + pos;   // filter cb0*16 + 4 lg
 #pragma unroll
-        for (int c = 0; c < kPkBlocks; ++c) {
-            const int m = (cb0 + c) * 16 + li;
-            if (c >= ncb || m >= g.M) continue;
-            int32_t *ym = y + ((int64_t)o.n * g.M + m) * HWo;
-            const v4i v = acc[c] + corr[c];
-            if (pt.vec) {
-                if (q0 < HWo) __builtin_nontemporal_store(v, (v4i *)(ym + q0));
-            } else {
+            for (int c = 0; c < kPkBlocks; ++c) {
+                if (c >= ncb) continue;
+                const v4i cv = *(const v4i *)(corr + c * 16 + lg * 4);
 #pragma unroll
-                for (int e = 0; e < 4; ++e)
-                    if (q0 + e < HWo) ym[q0 + e] = v[e];
+                for (int v = 0; v < 4; ++v)
+                    if ((cb0 + c) * 16 + lg * 4 + v < g.M)
+                        __builtin_nontemporal_store(acc[c][v] + cv[v], yb + (int64_t)(c * 16 + v) * HWo);
+            }
+        } else {
+            const int q0 = o.p0 + lg * 4;
+#pragma unroll
+            for (int c = 0; c < kPkBlocks; ++c) {
+                const int m = (cb0 + c) * 16 + li;
+                if (c >= ncb || m >= g.M) continue;
+                int32_t *ym = y + ((int64_t)o.n * g.M + m) * HWo;
+                const v4i v = acc[c] + corr[c * 16 + li];
+                if (pt.vec) {
+                    if (q0 < HWo) __builtin_nontemporal_store(v, (v4i *)(ym + q0));
+                } else {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        if (q0 + e < HWo) ym[q0 + e] = v[e];
+                }
             }
         }
     };
@@ -1176,7 +1243,7 @@ __global__ __launch_bounds__(kPkThreads) void conv2d_i8_packed_kernel(const uint
 #pragma unroll
         for (int c = 0; c < kPkBlocks; ++c)
             if (c < ncb)
-                acc[c] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a, *(const v4i *)(bf + c * nkb * 1024), acc[c], 0, 0, 0);
+                acc[c] = mfma_tile<TR>(a, *(const v4i *)(bf + c * nkb * 1024), acc[c]);
         if (kb == nkb - 1) {
             store(acc, cur);
 #pragma unroll
@@ -1344,20 +1411,28 @@ bool res_tiles(const I8Geom &g, int target, ResTiles &rt, int &lds, int64_t &wgs
     int64_t halo;
     int kc = g.Cp;
     if (chunked) {
-        kc = g.Cp % 128 == 0 && pixels * 8 <= (int64_t)kResHalo * kResThreads && 2 * bytes(128, halo) <= kHaloMaxLds
+        kc = g.Cp % 128 == 0 && pixels * 8 <= (int64_t)kResHalo * kResThreads &&
+                     2 * bytes(128, halo) + kResGroup * 4 <= kHaloMaxLds
                  ? 128 : kResChunk;
     }
     const int64_t buf = bytes(kc, halo);
     rt.nch = g.Cp / kc;
     rt.halo = (int)std::min<int64_t>(halo, INT32_MAX);
     rt.buf = (int)std::min<int64_t>(buf, INT32_MAX);
-    const int64_t total = (rt.nch > 1 ? 2 : 1) * buf;
+    // chunked: two chunk buffers, then the group's zero-point corrections (transposed stores)
+    const int64_t total = chunked ? 2 * buf + kResGroup * 4 : buf;
     lds = (int)std::min<int64_t>(total, INT32_MAX);
     wgs = (int64_t)g.N * rt.R * ngrp;
     rt.items = (int)std::min<int64_t>(wgs, INT32_MAX);
     const bool pieces = chunked ? (maxu <= kResTPW * kResWaves && pixels * (kc / 16) <= (int64_t)kResHalo * kResThreads)
                                 : pixels * (kc / 16) <= kResPieces;
     return pieces && total <= kHaloMaxLds && wgs < ((int64_t)1 << 31) - 8;
+}
+
+// 16-byte output stores where every image's positions are a multiple of 4 and the output
+// 16-byte aligned; else the transposed tile layout (64-byte runs of one filter's positions)
+bool vec_out(const I8Geom &g, const int32_t *y) {
+    return ((int64_t)g.Ho * g.Wo) % 4 == 0 && ((uintptr_t)y % 16) == 0;
 }
 
 template <typename F>
@@ -1370,27 +1445,41 @@ int launch_res_kernel(F kernel, const void *x, const I8Geom &g, ResTiles rt, int
         set_error(std::string("conv2d_int8: LDS attribute: ") + hipGetErrorString(attr));
         return SAMD_EHIP;
     }
-    rt.vec = ((int64_t)g.Ho * g.Wo) % 4 == 0 && ((uintptr_t)y % 16) == 0;
+    rt.vec = vec_out(g, y);
     const int64_t per_xcd = ((int64_t)rt.items + kNumXcd - 1) / kNumXcd;
     hipLaunchKernelGGL(kernel, dim3((unsigned)(per_xcd * kNumXcd)), dim3(kResThreads), (size_t)lds, s,
                        (const uint8_t *)x, (const int8_t *)p.wr, (const int32_t *)p.pre, y, g, rt);
     return check_launch("conv2d_int8 (weight-resident)");
 }
 
+template <int KH, int KW, int CB, bool TR>
+int launch_res_tr(const void *x, const I8Geom &g, const ResTiles &rt, int lds, const I8Workspace &p, int32_t *y,
+                  hipStream_t s) {
+    static std::once_flag once;
+    static hipError_t attr = hipSuccess;
+    return launch_res_kernel(conv2d_i8_resident_kernel<KH, KW, CB, TR>, x, g, rt, lds, p, y, s, once, attr);
+}
+
 template <int KH, int KW, int CB>
 int launch_res(const void *x, const I8Geom &g, const ResTiles &rt, int lds, const I8Workspace &p, int32_t *y,
                hipStream_t s) {
+    return vec_out(g, y) ? launch_res_tr<KH, KW, CB, false>(x, g, rt, lds, p, y, s)
+                         : launch_res_tr<KH, KW, CB, true>(x, g, rt, lds, p, y, s);
+}
+
+template <int KH, int KW, int CB, bool TR>
+int launch_res_chunked_tr(const void *x, const I8Geom &g, const ResTiles &rt, int lds, const I8Workspace &p,
+                          int32_t *y, hipStream_t s) {
     static std::once_flag once;
     static hipError_t attr = hipSuccess;
-    return launch_res_kernel(conv2d_i8_resident_kernel<KH, KW, CB>, x, g, rt, lds, p, y, s, once, attr);
+    return launch_res_kernel(conv2d_i8_resident_chunked_kernel<KH, KW, CB, TR>, x, g, rt, lds, p, y, s, once, attr);
 }
 
 template <int KH, int KW, int CB>
 int launch_res_chunked_cb(const void *x, const I8Geom &g, const ResTiles &rt, int lds, const I8Workspace &p,
                           int32_t *y, hipStream_t s) {
-    static std::once_flag once;
-    static hipError_t attr = hipSuccess;
-    return launch_res_kernel(conv2d_i8_resident_chunked_kernel<KH, KW, CB>, x, g, rt, lds, p, y, s, once, attr);
+    return vec_out(g, y) ? launch_res_chunked_tr<KH, KW, CB, false>(x, g, rt, lds, p, y, s)
+                         : launch_res_chunked_tr<KH, KW, CB, true>(x, g, rt, lds, p, y, s);
 }
 
 template <int KH, int KW>
@@ -1430,31 +1519,38 @@ bool pk_tiles(const I8Geom &g, int tpw, PkTiles &pt, int &lds, int64_t &wgs) {
     pt.items = (int)(((int64_t)pt.tiles + 4 * tpw - 1) / (4 * tpw));
     pt.vec = 0;
     const int nblk = (g.M + 15) / 16;
-    lds = std::min(kPkBlocks, nblk) * g.pkb * 1024;
+    lds = std::min(kPkBlocks, nblk) * g.pkb * 1024 + kPkBlocks * 16 * 4;
     wgs = (int64_t)pt.items * ((nblk + kPkBlocks - 1) / kPkBlocks);
     return lds <= kHaloMaxLds && wgs < ((int64_t)1 << 31) - 8;
 }
 
 constexpr int kPkTpw[3] = {4, 2, 1};   // tiles per wave of the packed-row candidates
 
-int launch_packed(const void *x, const I8Geom &g, PkTiles pt, int lds, const I8Workspace &p, int32_t *y,
-                  hipStream_t s) {
+template <bool TR>
+int launch_packed_tr(const void *x, const I8Geom &g, PkTiles pt, int lds, const I8Workspace &p, int32_t *y,
+                     hipStream_t s) {
     static std::once_flag once;
     static hipError_t attr = hipSuccess;
     std::call_once(once, [&] {
-        attr = hipFuncSetAttribute((const void *)conv2d_i8_packed_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                   kHaloMaxLds);
+        attr = hipFuncSetAttribute((const void *)conv2d_i8_packed_kernel<TR>,
+                                   hipFuncAttributeMaxDynamicSharedMemorySize, kHaloMaxLds);
     });
     if (attr != hipSuccess) {
         set_error(std::string("conv2d_int8: LDS attribute: ") + hipGetErrorString(attr));
         return SAMD_EHIP;
     }
-    pt.vec = ((int64_t)g.Ho * g.Wo) % 4 == 0 && ((uintptr_t)y % 16) == 0;
+    pt.vec = vec_out(g, y);
     const int64_t per_xcd = ((int64_t)pt.items + kNumXcd - 1) / kNumXcd;
     const unsigned gy = (unsigned)(((g.M + 15) / 16 + kPkBlocks - 1) / kPkBlocks);
-    hipLaunchKernelGGL(conv2d_i8_packed_kernel, dim3((unsigned)(per_xcd * kNumXcd), gy), dim3(kPkThreads),
+    hipLaunchKernelGGL(conv2d_i8_packed_kernel<TR>, dim3((unsigned)(per_xcd * kNumXcd), gy), dim3(kPkThreads),
                        (size_t)lds, s, (const uint8_t *)x, (const int8_t *)p.wk, (const int32_t *)p.pre, y, g, pt);
     return check_launch("conv2d_int8 (packed rows)");
+}
+
+int launch_packed(const void *x, const I8Geom &g, const PkTiles &pt, int lds, const I8Workspace &p, int32_t *y,
+                  hipStream_t s) {
+    return vec_out(g, y) ? launch_packed_tr<false>(x, g, pt, lds, p, y, s)
+                         : launch_packed_tr<true>(x, g, pt, lds, p, y, s);
 }
 
 // Every launch the int8 baseline can make for a layer: the halo tiles that fit (stride-1

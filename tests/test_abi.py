@@ -324,7 +324,7 @@ def test_int8_halo_tiles_cover_every_kernel():
             rows = min(sh.H, (p.positions - 1) // sh.W + 2) + sh.KH - 1
             pixels = rows * (sh.W + sh.KW - 1)
             kc = [k for k in (64, 128)
-                  if p.lds_bytes == 2 * ((pixels * (k + 16) + 15) // 16 * 16 + 32 * sh.KH * sh.KW * k)]
+                  if p.lds_bytes == 2 * ((pixels * (k + 16) + 15) // 16 * 16 + 32 * sh.KH * sh.KW * k) + 32 * 4]
             assert len(kc) == 1, (sh, p)
             widths.add((sh.KH, kc[0]))
     assert widths == {(3, 64), (3, 128), (1, 64), (1, 128)}, widths
@@ -353,7 +353,8 @@ def test_int8_packed_rows():
     bytes per row, four slots per k-block), offered where that at least halves the
     k-blocks of the 64-channel layout and the activations are whole 4-byte words; the
     group's fragments (up to 8 blocks of 16 filters x k-blocks x 1 KB) in LDS; the
-    workspace grows by the packed fragments."""
+    workspace grows by the packed fragments.  LDS: the fragments, then 8 x 16 zero-point
+    corrections of 4 bytes."""
     import samd_workloads as wl
     xf, wf = Fmt(8, False), Fmt(8, True)
 
@@ -362,16 +363,16 @@ def test_int8_packed_rows():
                 for p in samd.conv2d_int8_candidates(shape, xf, wf) if p.halo == 3]
     # VGG-B layer 1: 3x3 on 3 channels = 9 bytes per row, one slot each, one k-block;
     # 224 x 224 positions = 3136 tiles of 16, 4, 2 or 1 per wave and 4 waves
-    assert packed(wl.VGGB_LAYERS[0]) == [(64, 256, 4 * 1024, 196), (64, 128, 4 * 1024, 392),
-                                         (64, 64, 4 * 1024, 784)]
+    assert packed(wl.VGGB_LAYERS[0]) == [(64, 256, 4 * 1024 + 512, 196), (64, 128, 4 * 1024 + 512, 392),
+                                         (64, 64, 4 * 1024 + 512, 784)]
     # AlexNet layer 1: 11x11 stride 4 on 3 channels = 33 bytes per row, 3 slots, 33 slots =
     # 9 k-blocks (against 121); 96 filters = 6 blocks; 16 images of 55 x 55 = 16 x 190 tiles
-    assert packed(wl.ALEXNET_LAYERS[0]) == [(96, 256, 6 * 9 * 1024, 190), (96, 128, 6 * 9 * 1024, 380),
-                                            (96, 64, 6 * 9 * 1024, 760)]
+    assert packed(wl.ALEXNET_LAYERS[0]) == [(96, 256, 6 * 9 * 1024 + 512, 190), (96, 128, 6 * 9 * 1024 + 512, 380),
+                                            (96, 64, 6 * 9 * 1024 + 512, 760)]
     for shape in (wl.VGGB_LAYERS[0], wl.ALEXNET_LAYERS[0]):
         assert samd.conv2d_int8_plan(shape, xf, wf).halo == 3
     # 200 filters: two workgroup rows (8 + 5 blocks), LDS for 8
-    assert packed(Conv2dDesc(1, 3, 8, 8, 200, 3, 3, 1, 1, 1, 1))[0][2:] == (8 * 1024, 2)
+    assert packed(Conv2dDesc(1, 3, 8, 8, 200, 3, 3, 1, 1, 1, 1))[0][2:] == (8 * 1024 + 512, 2)
     # 64 channels, 1x1 layers and 32 channels at 3x3 keep the 64-channel layout
     assert not packed(wl.MID) and not packed(Conv2dDesc(1, 16, 8, 8, 8, 1, 1, 1, 1, 0, 0))
     assert not packed(Conv2dDesc(1, 32, 8, 8, 8, 3, 3, 1, 1, 1, 1))
@@ -402,11 +403,12 @@ def test_int8_resident_chunk_width():
     """Layers of 256-512 padded channels walk K in 128-channel chunks where a chunk's halo
     fits six 16-byte pieces per thread and two chunks fit 160 KB of LDS, else in 64-channel
     chunks: each chunk buffer holds the halo (pixels x (chunk + 16) bytes) and 32 filters'
-    weights of the chunk (32 x 9 x chunk bytes), and two buffers alternate."""
+    weights of the chunk (32 x 9 x chunk bytes), two buffers alternate, and the 32
+    filters' zero-point corrections (4 bytes each) follow them."""
     import samd_workloads as wl
 
     def lds(pixels, kc):
-        return 2 * ((pixels * (kc + 16) + 15) // 16 * 16 + 32 * 9 * kc)
+        return 2 * ((pixels * (kc + 16) + 15) // 16 * 16 + 32 * 9 * kc) + 32 * 4
 
     def resident(shape):
         return {p.positions: p.lds_bytes

@@ -393,11 +393,16 @@ def test_conv2d_int8_every_launch_mid(bits):
 
 
 @pytest.mark.parametrize("shape", [wl.Conv2dShape(2, 16, 56, 56, 128, 3, 3, 1, 1, 1, 1),
-                                   wl.Conv2dShape(3, 16, 20, 21, 8, 1, 1, 1, 1, 0, 0)],
+                                   wl.Conv2dShape(3, 16, 20, 21, 8, 1, 1, 1, 1, 0, 0),
+                                   wl.Conv2dShape(1, 256, 9, 12, 40, 3, 3, 1, 1, 1, 1),
+                                   wl.Conv2dShape(2, 384, 4, 8, 48, 1, 1, 1, 1, 0, 0),
+                                   wl.Conv2dShape(1, 3, 10, 8, 20, 3, 3, 1, 1, 1, 1)],
                          ids=lambda s: "x".join(map(str, s.as_tuple())))
 def test_conv2d_int8_resident_unaligned_output(shape):
-    """The weight-resident launches writing into an output 4 bytes past a 16-byte
-    boundary (the per-element store path) and into an aligned one, against the oracle."""
+    """The weight-resident (whole-K and chunked) and packed-row launches writing into an
+    output 4 bytes past a 16-byte boundary (the transposed-tile store path) and into an
+    aligned one (16-byte stores), against the oracle; nothing around the output is
+    written."""
     rng = np.random.default_rng(5)
     x = wl.uniform(rng, (shape.N, shape.C, shape.H, shape.W), 8, False)
     w = wl.uniform(rng, (shape.M, shape.C, shape.KH, shape.KW), 8, True)
@@ -405,7 +410,7 @@ def test_conv2d_int8_resident_unaligned_output(shape):
     want = ref.conv2d(x, w, shape.as_tuple())
     xs = gpu_vals(np.transpose(x, (0, 2, 3, 1)), False)
     ws = gpu_vals(w, True)
-    cands = [p for p in samd.conv2d_int8_candidates(shape, xf, wf) if p.halo == 2]
+    cands = [p for p in samd.conv2d_int8_candidates(shape, xf, wf) if p.halo in (2, 3)]
     assert cands
     buf = torch.full((want.size + 8,), -7, dtype=torch.int32, device=DEV)
     try:
