@@ -92,8 +92,11 @@ def parse():
     p.add_argument("--lanewise", action="store_true",
                    help="instead of the default workload, time lane-wise add/sub/mul/scale on packed words (GB/s)")
     p.add_argument("--int8-counters", action="store_true",
-                   help="launch every int8 baseline candidate once on the mid-size layer (b = 4), eagerly, and exit "
-                        "(the program rocprofv3 --pmc passes of the int8 kernels run)")
+                   help="launch every int8 baseline candidate once on the --int8-layer layer (b = 4), eagerly, and "
+                        "exit (the program rocprofv3 --pmc passes of the int8 kernels run)")
+    p.add_argument("--int8-layer", choices=sorted(INT8_LAYERS), default="mid",
+                   help="layer of --int8-counters and --int8-summary: the mid-size layer, VGG-B layer 1 or an "
+                        "AlexNet-shaped stack layer (batch 16)")
     p.add_argument("--int8-summary", nargs="+", metavar="PMC_DIR",
                    help="print the counter table of --int8-counters runs profiled with rocprofv3 --pmc (one "
                         "folder per pass)")
@@ -365,8 +368,21 @@ INT8_COUNTERS = ("SQ_WAVES SQ_BUSY_CYCLES SQ_WAVE_CYCLES SQ_WAIT_INST_ANY SQ_VAL
                  "SQ_INSTS_VMEM_WR SQ_INSTS_LDS")
 
 
+# Layers of the int8 counter runs: name -> (index into VGGB_LAYERS / ALEXNET_LAYERS, or
+# None for the mid-size layer)
+INT8_LAYERS = {"mid": None, "vggb1": ("VGGB_LAYERS", 0),
+               **{f"alexnet{i + 1}": ("ALEXNET_LAYERS", i) for i in range(5)}}
+
+
+def int8_layer(name):
+    """The shape of an --int8-layer choice."""
+    import samd_workloads as wl
+    ref = INT8_LAYERS[name]
+    return wl.MID if ref is None else getattr(wl, ref[0])[ref[1]]
+
+
 def run_int8_counters(args):
-    """One eager launch of every int8 baseline candidate on the mid-size layer (4-bit
+    """One eager launch of every int8 baseline candidate on the chosen layer (4-bit
     unsigned activations, 4-bit signed weights), each after an untimed launch of the
     same candidate; prints the launch order."""
     import numpy as np
@@ -376,11 +392,17 @@ def run_int8_counters(args):
     import samd_workloads as wl
 
     dev = torch.device("cuda:0")
-    shape, b = wl.MID, 4
-    case = wl.conv2d_case(3, b)
+    shape, b = int8_layer(args.int8_layer), 4
+    if args.int8_layer == "mid":
+        case = wl.conv2d_case(3, b)
+        xv, wv = case.x, case.w
+    else:
+        rng = np.random.default_rng(wl.seed_for(6, b))
+        xv = wl.uniform(rng, (shape.N, shape.C, shape.H, shape.W), b, False)
+        wv = wl.uniform(rng, (shape.M, shape.C, shape.KH, shape.KW), b, True)
     xf, wf = samd.Fmt(b, False), samd.Fmt(b, True)
-    x_nhwc = torch.from_numpy(np.ascontiguousarray(np.transpose(case.x, (0, 2, 3, 1))).astype(np.uint8)).to(dev)
-    w8 = torch.from_numpy(case.w.astype(np.int8)).to(dev)
+    x_nhwc = torch.from_numpy(np.ascontiguousarray(np.transpose(xv, (0, 2, 3, 1))).astype(np.uint8)).to(dev)
+    w8 = torch.from_numpy(wv.astype(np.int8)).to(dev)
     ws8 = samd.conv2d_int8_prepare(w8, wf, shape, xf)
     Ho, Wo = samd.out_hw(shape)
     y = torch.empty((shape.N, shape.M, Ho, Wo), dtype=torch.int32, device=dev)
@@ -394,7 +416,7 @@ def run_int8_counters(args):
     samd.conv2d_int8_use_plan(shape, xf, wf, None)
 
 
-def int8_summary(folders):
+def int8_summary(folders, layer="mid"):
     """Markdown table of rocprofv3 --pmc passes over --int8-counters: per int8 launch (the
     second of each candidate's two dispatches), its duration and counters."""
     import csv
@@ -417,16 +439,17 @@ def int8_summary(folders):
                     e["name"] = r["Kernel_Name"].replace("samd::(anonymous namespace)::", "").replace("void ", "").split("(")[0]
                     e["c"][r["Counter_Name"]] = e["c"].get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
                     e["dur"].append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-9)
-    cands = samd.conv2d_int8_candidates(wl.MID, samd.Fmt(4, False), samd.Fmt(4, True))
-    Ho, Wo = samd.out_hw(wl.MID)
-    macs = wl.MID.N * wl.MID.M * Ho * Wo * wl.MID.C * 9
+    shape = int8_layer(layer)
+    cands = samd.conv2d_int8_candidates(shape, samd.Fmt(4, False), samd.Fmt(4, True))
+    Ho, Wo = samd.out_hw(shape)
+    macs = shape.N * shape.M * Ho * Wo * shape.C * shape.KH * shape.KW
     # Busy and issue cycles are not divided by GRBM_GUI_ACTIVE: under --pmc that counter
     # spans the profiler's per-dispatch overhead as well, so the table keeps raw counts
     # and the quantities that need no clock (requests, hit rates, latencies per request).
     out = ["| launch | kernel | dispatch us | MAC/s % of int8 peak | waves | wait % of wave cycles | "
            "LDS bank conflict cycles | LDS wait cycles | L1->L2 read requests | L2 hit % | L2->HBM read requests | "
-           "L1->L2 read latency (cycles per request) | VMEM reads | LDS instructions |",
-           "|---|---|---|---|---|---|---|---|---|---|---|---|---|---|"]
+           "L1->L2 read latency (cycles per request) | L1->L2 write requests | VMEM reads | LDS instructions |",
+           "|---|---|---|---|---|---|---|---|---|---|---|---|---|---|---|"]
     for k in sorted(disp):
         if k % 2 == 0:
             continue   # the first launch of each candidate warms it
@@ -444,7 +467,7 @@ def int8_summary(folders):
                    f"{g('TCP_TCC_READ_REQ_sum'):.4g} | {100 * hit / max(hit + miss, 1):.1f} | "
                    f"{g('TCC_EA0_RDREQ_sum'):.4g} | "
                    f"{g('TCP_TCC_READ_REQ_LATENCY_sum') / max(g('TCP_TCC_READ_REQ_sum'), 1):.0f} | "
-                   f"{g('SQ_INSTS_VMEM_RD'):.4g} | {g('SQ_INSTS_LDS'):.4g} |")
+                   f"{g('TCP_TCC_WRITE_REQ_sum'):.4g} | {g('SQ_INSTS_VMEM_RD'):.4g} | {g('SQ_INSTS_LDS'):.4g} |")
     return "\n".join(out)
 
 
@@ -1028,7 +1051,7 @@ def main():
         run_int8_counters(args)
         return
     if args.int8_summary:
-        print(int8_summary(args.int8_summary))
+        print(int8_summary(args.int8_summary, args.int8_layer))
         return
     if args.vggb:
         run_vggb(args)

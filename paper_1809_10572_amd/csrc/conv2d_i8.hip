@@ -1078,6 +1078,7 @@ __global__ __launch_bounds__(kResThreads) void conv2d_i8_resident_chunked_kernel
 // has that tile's stores ahead of it.  Operands, output stores and the zero point as in
 // the weight-resident kernels.
 constexpr int kPkThreads = 256;
+constexpr int kPkWaves = kPkThreads / 64;
 constexpr int kPkBlocks = 8;    // 16-filter MFMA column blocks per workgroup at most
 constexpr int kPkMaxKb = 16;    // k-blocks at most (LDS: 8 blocks x 16 k-blocks x 1 KB)
 
@@ -1137,7 +1138,7 @@ __global__ __launch_bounds__(kPkThreads) void conv2d_i8_packed_kernel(const uint
         int jl, jh;   // window bytes inside the image: [jl, jh)
     };
     auto geo = [&](int i, Geo &o) {
-        const int t = item * 4 * pt.tpw + 4 * i + wave;
+        const int t = item * kPkWaves * pt.tpw + kPkWaves * i + wave;
         if (i >= pt.tpw || t >= pt.tiles) return false;
         o.n = t / pt.tiles_img;
         o.p0 = (t - o.n * pt.tiles_img) * 16;
@@ -1146,8 +1147,10 @@ __global__ __launch_bounds__(kPkThreads) void conv2d_i8_packed_kernel(const uint
         o.ih0 = ho * g.sh - g.ph;
         const int iw0 = wo * g.sw - g.pw;
         o.row0 = (o.n * g.H + o.ih0) * g.W + iw0;
+        // a window inside the image leaves its bytes past KW*C unmasked (their weights are
+        // zero), so every slot of an inside window takes the unmasked path below
         o.jl = max(0, -iw0) * g.C;
-        o.jh = min(g.KW, g.W - iw0) * g.C;
+        o.jh = iw0 + g.KW <= g.W ? 1 << 20 : (g.W - iw0) * g.C;
         return true;
     };
     // step (tile geometry, k-block kb): the lane's five dwords, byte shift and valid range
@@ -1175,12 +1178,18 @@ __global__ __launch_bounds__(kPkThreads) void conv2d_i8_packed_kernel(const uint
     };
     auto build = [&](const Ld &ld) {
         v4i a;
+        if (ld.lo <= 0 && ld.hi >= 16) {   // every byte inside the image (or past the window)
 #pragma unroll
-        for (int d = 0; d < 4; ++d) {
-            const uint32_t v = __builtin_amdgcn_alignbyte(ld.r[d + 1], ld.r[d], (uint32_t)ld.sb);
-            const int lo = min(max(ld.lo - 4 * d, 0), 4), hi = min(max(ld.hi - 4 * d, 0), 4);
-            const uint32_t m = hi > lo ? (uint32_t)((0xFFFFFFFFull << (8 * lo)) & ((1ull << (8 * hi)) - 1)) : 0u;
-            a[d] = (int)(((v ^ (uint32_t)flip) & m) | ((uint32_t)flip & ~m));
+            for (int d = 0; d < 4; ++d)
+                a[d] = (int)(__builtin_amdgcn_alignbyte(ld.r[d + 1], ld.r[d], (uint32_t)ld.sb) ^ (uint32_t)flip);
+        } else {
+#pragma unroll
+            for (int d = 0; d < 4; ++d) {
+                const uint32_t v = __builtin_amdgcn_alignbyte(ld.r[d + 1], ld.r[d], (uint32_t)ld.sb);
+                const int lo = min(max(ld.lo - 4 * d, 0), 4), hi = min(max(ld.hi - 4 * d, 0), 4);
+                const uint32_t m = hi > lo ? (uint32_t)((0xFFFFFFFFull << (8 * lo)) & ((1ull << (8 * hi)) - 1)) : 0u;
+                a[d] = (int)(((v ^ (uint32_t)flip) & m) | ((uint32_t)flip & ~m));
+            }
         }
         return a;
     };
@@ -1516,7 +1525,7 @@ bool pk_tiles(const I8Geom &g, int tpw, PkTiles &pt, int &lds, int64_t &wgs) {
     pt.tiles_img = (int)((HWo + 15) / 16);
     pt.tiles = g.N * pt.tiles_img;
     pt.tpw = tpw;
-    pt.items = (int)(((int64_t)pt.tiles + 4 * tpw - 1) / (4 * tpw));
+    pt.items = (int)(((int64_t)pt.tiles + kPkWaves * tpw - 1) / (kPkWaves * tpw));
     pt.vec = 0;
     const int nblk = (g.M + 15) / 16;
     lds = std::min(kPkBlocks, nblk) * g.pkb * 1024 + kPkBlocks * 16 * 4;
@@ -1566,10 +1575,10 @@ void int8_candidates(const I8Geom &g, std::vector<samd_conv2d_int8_plan> &out) {
         samd_conv2d_int8_plan c{};
         c.halo = 3;
         c.mtile = std::min(kPkBlocks, (g.M + 15) / 16) * 16;
-        c.positions = 4 * kResTile * tpw;
+        c.positions = kPkWaves * kResTile * tpw;
         c.row_segments = 0;
         c.lds_bytes = lds;
-        c.waves = kPkThreads / 64;
+        c.waves = kPkWaves;
         c.workgroups = wgs;
         out.push_back(c);
     }
