@@ -349,6 +349,7 @@ struct HaloTiles {
     int halo_bytes;  // LDS bytes of one halo buffer (the largest tile's)
     int nch;         // chunks of KC channels: Cp / KC
     int items;       // work items: N * tiles_img * channel tiles
+    int kc;          // channels per chunk: the K step, or 64 where a 128-channel chunk does not fit
 };
 
 // n / d for 0 <= n < 2^22 and 1 <= d < 2^12 by a float reciprocal estimate and one exact
@@ -1354,14 +1355,21 @@ bool halo_tiles(const I8Geom &g, int wm, int tp, HaloTiles &ht, int64_t &wgs, in
     }
     // the kernel's fast divisions need positions per image below 2^22, divisors below 2^12
     if ((int64_t)g.Ho * g.Wo >= (1 << 22) || g.Wo >= 4096 || hwmax >= 4096) return false;
-    const int kc = g.ks;
     const int64_t pixels = (int64_t)rmax * hwmax;
-    ht.halo_bytes = (int)std::min<int64_t>(pixels * (kc + 16), 1 << 30);
-    ht.nch = g.Cp / kc;
-    lds = (ht.nch > 1 ? 2 : 1) * ht.halo_bytes;
     wgs = (int64_t)g.N * ht.tiles_img * ((g.M + 4 * wm - 1) / (4 * wm));
     ht.items = (int)std::min<int64_t>(wgs, INT32_MAX);
-    return pixels * (kc / 16) <= kHaloPieces && lds <= kHaloMaxLds && wgs < ((int64_t)1 << 31) - 8;
+    if (wgs >= ((int64_t)1 << 31) - 8) return false;
+    // chunks of the weight layout's K step, or of 64 channels where a 128-channel chunk's
+    // halo does not fit (the weights of a chunk are the same bytes either way)
+    for (int kc : {g.ks, 64}) {
+        if (kc > g.ks) continue;
+        ht.kc = kc;
+        ht.halo_bytes = (int)std::min<int64_t>(pixels * (kc + 16), 1 << 30);
+        ht.nch = g.Cp / kc;
+        lds = (ht.nch > 1 ? 2 : 1) * ht.halo_bytes;
+        if (pixels * (kc / 16) <= kHaloPieces && lds <= kHaloMaxLds) return true;
+    }
+    return false;
 }
 
 template <int WM, int TP, int KC>
@@ -1746,8 +1754,8 @@ int launch_conv2d_i8(const void *x, samd_fmt xf, const samd_conv2d_desc &d, int3
         if (halo_tiles(g, wm, tp, ht, wgs, lds)) {
 #define SAMD_HALO(WM_, TP_)                                                                                  \
     if (wm == WM_ && tp == TP_)                                                                              \
-        return g.ks == 128 ? launch_halo<WM_, TP_, 128>(x, g, ht, lds, p, y, s)                              \
-                           : launch_halo<WM_, TP_, 64>(x, g, ht, lds, p, y, s);
+        return ht.kc == 128 ? launch_halo<WM_, TP_, 128>(x, g, ht, lds, p, y, s)                             \
+                            : launch_halo<WM_, TP_, 64>(x, g, ht, lds, p, y, s);
             SAMD_HALO(32, 128) SAMD_HALO(32, 64) SAMD_HALO(16, 128) SAMD_HALO(16, 64)
 #undef SAMD_HALO
         }

@@ -363,6 +363,7 @@ HALO = [
     wl.Conv2dShape(1, 256, 4, 150, 40, 3, 3, 1, 1, 1, 1),      # wide rows: 4 chunks of 64 channels
     wl.Conv2dShape(1, 256, 2, 300, 16, 1, 1, 1, 1, 0, 0),      # 1x1, wide rows: 4 chunks of 64 channels
     wl.Conv2dShape(1, 16, 20, 80, 16, 11, 11, 1, 1, 5, 5),     # no halo fits: im2col kernel
+    wl.Conv2dShape(1, 96, 12, 40, 40, 5, 5, 1, 1, 2, 2),       # 5x5, 96 channels: 64-channel halo chunks at 128 positions
     # packed-row K (few channels): 3 channels at 3x3 (one k-block), 11x11 stride 4 on 3
     # channels (nine), 1 channel with 130 filters (two workgroup rows), 5x5 with strides
     # (1, 2), 24 channels, and 42 positions per image (per-element output stores)
