@@ -429,6 +429,37 @@ def test_conv2d_int8_resident_unaligned_output(shape):
         samd.conv2d_int8_use_plan(shape, xf, wf, None)
 
 
+@pytest.mark.parametrize("shape", [wl.Conv2dShape(1, 3, 10, 8, 20, 3, 3, 1, 1, 1, 1),
+                                   wl.Conv2dShape(2, 16, 12, 12, 40, 3, 3, 1, 1, 1, 1),
+                                   wl.Conv2dShape(1, 256, 9, 12, 40, 3, 3, 1, 1, 1, 1)],
+                         ids=lambda s: "x".join(map(str, s.as_tuple())))
+def test_conv2d_int8_misaligned_activations(shape):
+    """Every int8 launch of the layer with the activations 1 and 4 bytes past a 16-byte
+    boundary: the kernels that need 16-byte (weight-resident, halo) or 4-byte (packed-row)
+    aligned activations give way to the im2col kernel, or run where their alignment holds;
+    every result against the oracle."""
+    rng = np.random.default_rng(11)
+    x = wl.half_extremes(rng, (shape.N, shape.C, shape.H, shape.W), 8, False)
+    w = wl.half_extremes(rng, (shape.M, shape.C, shape.KH, shape.KW), 8, True)
+    xf, wf = samd.Fmt(8, 0), samd.Fmt(8, 1)
+    want = ref.conv2d(x, w, shape.as_tuple())
+    xh = np.ascontiguousarray(np.transpose(x, (0, 2, 3, 1))).astype(np.uint8).reshape(-1)
+    ws = gpu_vals(w, True)
+    buf = torch.zeros(xh.size + 32, dtype=torch.uint8, device=DEV)
+    try:
+        for plan in samd.conv2d_int8_candidates(shape, xf, wf):
+            samd.conv2d_int8_use_plan(shape, xf, wf, plan)
+            for off in (1, 4):
+                xs = buf[off:off + xh.size]
+                xs.copy_(torch.from_numpy(xh).to(DEV))
+                assert xs.data_ptr() % 16 == off % 16
+                got = samd.conv2d_int8(xs, xf, ws, wf, shape).cpu().numpy()
+                np.testing.assert_array_equal(got, want, err_msg=f"offset {off} halo={plan.halo} "
+                                              f"{plan.mtile}x{plan.positions}")
+    finally:
+        samd.conv2d_int8_use_plan(shape, xf, wf, None)
+
+
 @pytest.mark.parametrize("shape", HALO, ids=lambda s: "x".join(map(str, s.as_tuple())))
 @pytest.mark.parametrize("bx,sx", [(8, 0), (8, 1), (4, 0)])
 def test_conv2d_int8_every_launch(shape, bx, sx):
