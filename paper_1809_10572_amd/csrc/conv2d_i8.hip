@@ -4,10 +4,18 @@
 //
 // GEMM view: D[m][p] = sum_k Wr[m][k] * X[k][p] with p an output position (n, ho, wo)
 // and k = (ky, kx, c); weights are reordered once per call to [M][KH][KW][Cp] (Cp = C
-// rounded up to the K step, 64 or 128 channels) and activations are read in NHWC, so every lane fetches 16
-// consecutive channels with one 128-bit load.  Unsigned 8-bit activations do not fit
-// int8; they enter as v - 128 and the product gains 128 * (sum of the weights whose
-// input lies inside the image) back in the epilogue.
+// rounded up to the K step, 64 or 128 channels) and activations are read in NHWC, so
+// every lane fetches 16 consecutive channels with one 128-bit load.  Layers with few
+// input channels also get the weights in a packed-row K order (k = (ky, kx*C + c), each
+// kernel row padded to 16-byte slots), which the packed-row kernel reads instead of
+// padding C to 64.  Unsigned 8-bit activations do not fit int8; they enter as v - 128
+// and the product gains 128 * (sum of the weights whose input lies inside the image)
+// back in the epilogue.
+//
+// Kernels: im2col tiles (any layer), halo tiles (stride-1 layers with C a multiple of
+// 16), weight-resident runs (stride-1 3x3 and 1x1 layers, whole K or K in chunks), and
+// packed rows (few input channels, any stride); the host lists the launches that fit a
+// layer and a model or a measurement picks one.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
