@@ -1369,8 +1369,9 @@ bool halo_tiles(const I8Geom &g, int wm, int tp, HaloTiles &ht, int64_t &wgs, in
     if (wgs >= ((int64_t)1 << 31) - 8) return false;
     // chunks of the weight layout's K step, or of 64 channels where a 128-channel chunk's
     // halo does not fit (the weights of a chunk are the same bytes either way)
-    for (int kc : {g.ks, 64}) {
-        if (kc > g.ks) continue;
+    const int opts[2] = {g.ks, 64};
+    for (int o = 0; o < (g.ks == 64 ? 1 : 2); ++o) {
+        const int kc = opts[o];
         ht.kc = kc;
         ht.halo_bytes = (int)std::min<int64_t>(pixels * (kc + 16), 1 << 30);
         ht.nch = g.Cp / kc;
