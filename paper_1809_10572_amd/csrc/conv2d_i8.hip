@@ -1081,11 +1081,11 @@ __global__ __launch_bounds__(kResThreads) void conv2d_i8_resident_chunked_kernel
 // fragments of up to 128 filters (the prepared packed layout) are staged in LDS once per
 // workgroup; each lane builds its A fragment (16 bytes of one position's slot) from five
 // aligned 4-byte loads, a byte shift, and a mask that puts the padding value on bytes of
-// pixels outside the image.  The next step's loads
-// (the next k-block, or the next tile's first) are issued before a step's MFMAs, and a
-// tile's outputs are stored after the next tile's first loads, so no wait for operands
-// has that tile's stores ahead of it.  Operands, output stores and the zero point as in
-// the weight-resident kernels.
+// pixels outside the image (skipped where the whole window lies inside).  The next step's
+// loads (the next k-block, or the next tile's first) are issued before a step's MFMAs,
+// and a tile's outputs are stored after the next tile's first loads, so no wait for
+// operands has that tile's stores ahead of it.  Output layouts (TR) and the zero point as
+// in the weight-resident kernels; the corrections sit in LDS after the fragments.
 constexpr int kPkThreads = 256;
 constexpr int kPkWaves = kPkThreads / 64;
 constexpr int kPkBlocks = 8;    // 16-filter MFMA column blocks per workgroup at most
