@@ -280,6 +280,23 @@ def test_conv2d_edge_shapes(shape, bx, sx, bw, sw):
     np.testing.assert_array_equal(run_conv2d(x, w, shape, xf, wf), ref.conv2d(x, w, shape.as_tuple()))
 
 
+@pytest.mark.parametrize("sx", [0, 1])
+def test_conv2d_largest_stack_accumulator(sx):
+    """The largest accumulator the AlexNet-shaped stack can reach: 384 channels of 3x3 at
+    8 bits with every product at its extreme (u8 x s8: 255 x -128; s8 x s8: -128 x -128),
+    through the SAMD path and the int8 baseline; an interior output is the closed form
+    384 * 9 * x * w (-112,803,840 and 56,623,104), the borders the oracle's."""
+    shape = wl.Conv2dShape(1, 384, 6, 6, 16, 3, 3, 1, 1, 1, 1)
+    xv = -128 if sx else 255
+    x = np.full((shape.N, shape.C, shape.H, shape.W), xv, np.int32)
+    w = np.full((shape.M, shape.C, shape.KH, shape.KW), -128, np.int32)
+    want = ref.conv2d(x, w, shape.as_tuple())
+    assert int(want[0, 0, 2, 2]) == 384 * 9 * xv * -128
+    xf, wf = samd.Fmt(8, sx), samd.Fmt(8, 1)
+    np.testing.assert_array_equal(run_conv2d(x, w, shape, xf, wf), want)
+    np.testing.assert_array_equal(run_conv2d_int8(x, w, shape, xf, wf), want)
+
+
 def test_conv2d_rejects_and_leaves_output_untouched():
     shape = wl.Conv2dShape(1, 512, 16, 16, 1, 16, 16, 1, 1, 0, 0)
     x = torch.zeros(512 * 16 * 4, dtype=torch.int32, device=DEV)
